@@ -1,0 +1,140 @@
+"""Pins for the oracle's backward pass (CPU only).
+
+Two pins outside the oracle's own arithmetic:
+  * a separate dense formulation of the whole layer in torch (float64): each branch is one
+    masked softmax over an explicit [N, keys] mask, the compression MLP is built from
+    torch.nn.functional layers, and torch autograd differentiates it;
+  * central finite differences of sum(o * dO) on the oracle's own forward.
+Both hold the top-k selection fixed (it is piecewise constant, so it has no gradient).
+"""
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from oracle import bsa
+from oracle.bsa import Params
+
+
+def _inputs(seed, B=2, H=2, n=64, d=8, n_real=53, P=None):
+    rng = np.random.default_rng(seed)
+    P = P or Params(ball=16, cmp_block=4, slc_block=8, topk=2, group=4)
+    valid = np.zeros((B, n), bool)
+    for b in range(B):
+        valid[b, rng.choice(n, n_real, replace=False)] = True
+    x = lambda *s: rng.standard_normal(s)
+    phi = lambda: {"w1": x(P.cmp_block * d, d) * 0.2, "b1": x(d) * 0.2, "w2": x(d, d) * 0.2,
+                   "b2": x(d) * 0.2}
+    return dict(P=P, q=x(B, H, n, d), k=x(B, H, n, d), v=x(B, H, n, d), valid=valid,
+                gate=x(B, n, 3), phi_k=phi(), phi_v=phi(), do=x(B, H, n, d))
+
+
+def _dense_torch(inp, sel):
+    """The layer as three dense masked softmaxes, differentiable by torch autograd."""
+    P = inp["P"]
+    t = lambda a: torch.tensor(a, dtype=torch.float64, requires_grad=True)
+    q, k, v, gate = t(inp["q"]), t(inp["k"]), t(inp["v"]), t(inp["gate"])
+    pk = {w: t(a) for w, a in inp["phi_k"].items()}
+    pv = {w: t(a) for w, a in inp["phi_v"].items()}
+    B, H, n, d = q.shape
+    valid = torch.from_numpy(inp["valid"])
+    l, ls, g, m = P.cmp_block, P.slc_block, P.group, P.ball
+    idx = torch.arange(n)
+    out = torch.zeros(B, H, n, d, dtype=torch.float64)
+
+    def masked_attn(qq, kk, vv, mask):
+        s = qq @ kk.T / d ** 0.5
+        s = s.masked_fill(~mask, float("-inf"))
+        p = torch.softmax(s, dim=-1)
+        p = torch.nan_to_num(p, nan=0.0)          # rows with no key
+        return p @ vv
+
+    def mlp(x, phi):
+        return F.linear(F.gelu(F.linear(x, phi["w1"].T, phi["b1"]), approximate="none"),
+                        phi["w2"].T, phi["b2"])
+
+    for b in range(B):
+        vb = valid[b]
+        qmask = vb[:, None]
+        for h in range(H):
+            qq, kk, vv = q[b, h], k[b, h], v[b, h]
+            ball_mask = (idx[:, None] // m == idx[None, :] // m) & vb[None, :] & qmask
+            kz = torch.where(vb[:, None], kk, 0.0).reshape(n // l, l * d)
+            vz = torch.where(vb[:, None], vv, 0.0).reshape(n // l, l * d)
+            kc, vc = mlp(kz, pk), mlp(vz, pv)
+            cval = vb.reshape(n // l, l).any(dim=1)
+            cmp_mask = cval[None, :] & qmask
+            chosen = torch.zeros(n // g, n // ls, dtype=torch.bool)
+            for p in range(n // g):
+                for j in sel[b, h, p]:
+                    if j >= 0:
+                        chosen[p, j] = True
+            slc_mask = chosen[idx // g][:, idx // ls] & vb[None, :] & qmask
+            sg = torch.sigmoid(gate[b])
+            out[b, h] = (sg[:, 0:1] * masked_attn(qq, kk, vv, ball_mask)
+                         + sg[:, 1:2] * masked_attn(qq, kc, vc, cmp_mask)
+                         + sg[:, 2:3] * masked_attn(qq, kk, vv, slc_mask))
+    loss = (out * torch.from_numpy(inp["do"])).sum()
+    loss.backward()
+    g = lambda x: x.grad.numpy()
+    return out.detach().numpy(), {
+        "dq": g(q), "dk": g(k), "dv": g(v), "dgate": g(gate),
+        "dphi_k": {w: g(a) for w, a in pk.items()}, "dphi_v": {w: g(a) for w, a in pv.items()},
+    }
+
+
+def _run_oracle(inp):
+    fwd = bsa.forward(inp["q"], inp["k"], inp["v"], inp["valid"], inp["gate"], inp["phi_k"],
+                      inp["phi_v"], inp["P"])
+    grads = bsa.backward(inp["q"], inp["k"], inp["v"], inp["valid"], inp["gate"], inp["phi_k"],
+                         inp["phi_v"], inp["P"], fwd, inp["do"])
+    return fwd, grads
+
+
+@pytest.mark.parametrize("seed,mask_own", [(0, True), (1, False)])
+def test_against_torch_dense_autograd(seed, mask_own):
+    P = Params(ball=16, cmp_block=4, slc_block=8, topk=2, group=4, mask_own_ball=mask_own)
+    inp = _inputs(seed, P=P)
+    fwd, grads = _run_oracle(inp)
+    o_ref, g_ref = _dense_torch(inp, fwd["sel"])
+    assert np.allclose(fwd["o"], o_ref, atol=1e-12)
+    for name in ("dq", "dk", "dv", "dgate"):
+        assert np.allclose(grads[name], g_ref[name], atol=1e-11), name
+    for which in ("dphi_k", "dphi_v"):
+        for w in ("w1", "b1", "w2", "b2"):
+            assert np.allclose(grads[which][w], g_ref[which][w], atol=1e-11), (which, w)
+
+
+def test_finite_differences():
+    inp = _inputs(5, B=1, H=1, n=32, n_real=29,
+                  P=Params(ball=16, cmp_block=4, slc_block=8, topk=1, group=4))
+    fwd, grads = _run_oracle(inp)
+    sel = fwd["sel"]
+    h = 1e-6
+    rng = np.random.default_rng(9)
+
+    def loss(mod):
+        f = bsa.forward(mod["q"], mod["k"], mod["v"], inp["valid"], mod["gate"], mod["phi_k"],
+                        mod["phi_v"], inp["P"])
+        assert np.array_equal(f["sel"], sel)      # the perturbation must not flip top-k
+        return float(np.sum(f["o"] * inp["do"]))
+
+    def check(get, grad_at, shape_src):
+        for _ in range(6):
+            ix = tuple(rng.integers(0, s) for s in shape_src.shape)
+            plus = {k: (dict((w, a.copy()) for w, a in v.items()) if isinstance(v, dict) else
+                        (v.copy() if isinstance(v, np.ndarray) else v)) for k, v in inp.items()}
+            minus = {k: (dict((w, a.copy()) for w, a in v.items()) if isinstance(v, dict) else
+                         (v.copy() if isinstance(v, np.ndarray) else v)) for k, v in inp.items()}
+            get(plus)[ix] += h
+            get(minus)[ix] -= h
+            fd = (loss(plus) - loss(minus)) / (2 * h)
+            an = grad_at[ix]
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (ix, fd, an)
+
+    check(lambda m: m["q"], grads["dq"], inp["q"])
+    check(lambda m: m["k"], grads["dk"], inp["k"])
+    check(lambda m: m["v"], grads["dv"], inp["v"])
+    check(lambda m: m["gate"], grads["dgate"], inp["gate"])
+    check(lambda m: m["phi_k"]["w1"], grads["dphi_k"]["w1"], inp["phi_k"]["w1"])
+    check(lambda m: m["phi_v"]["b2"], grads["dphi_v"]["b2"], inp["phi_v"]["b2"])
