@@ -1,0 +1,164 @@
+/*
+ * bsa.h - C ABI of the Ball Sparse Attention (BSA) layer library for AMD MI355X (gfx950).
+ *
+ * The layer (arXiv 2506.12541, Section 2.2) orders an irregular point set with a ball
+ * tree, then sums three attention branches over the ordered tokens, each scaled by a
+ * sigmoid gate (Eq. 9): attention inside each ball (Ball Tree Attention, Eq. 3),
+ * attention to MLP-compressed key/value blocks (Eq. 5), and attention to the top-k key
+ * blocks selected per query group from the compressed scores (Eq. 6-8, 10-12).
+ *
+ * General conventions
+ *  - Every pointer argument is a device pointer on the current HIP device unless stated
+ *    otherwise. Every call is asynchronous on `stream` (a hipStream_t passed as void*;
+ *    NULL = the default stream) and returns once its kernels are queued.
+ *  - The library never allocates device memory and keeps no pointer after a call
+ *    returns. The caller owns every buffer; sizes come from bsa_sizes() and
+ *    bsa_ball_tree_workspace_bytes().
+ *  - Arguments are validated on the host before anything is launched; an invalid call
+ *    returns a non-zero status and launches nothing. A failed launch returns
+ *    BSA_ERR_HIP. A fault inside a kernel surfaces at the caller's next synchronisation.
+ *    bsa_last_error() gives a human-readable detail of the last failure on the calling
+ *    thread. No C++ exception crosses this boundary.
+ *  - Token layout: Q, K, V, O and their gradients are [B, H, N, d] row-major in ball
+ *    order (slot order of the tree), so a ball, a compression block, a selection block
+ *    and a query group of one head are each one contiguous run of rows.
+ */
+#ifndef BSA_H
+#define BSA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BSA_OK = 0,
+  BSA_ERR_INVALID_ARGUMENT = 1,   /* a size, pointer or parameter is invalid            */
+  BSA_ERR_UNSUPPORTED = 2,        /* valid but not implemented (e.g. head_dim not 32/64) */
+  BSA_ERR_WORKSPACE_TOO_SMALL = 3,
+  BSA_ERR_HIP = 4                 /* a HIP runtime call or kernel launch failed          */
+} bsa_status_t;
+
+typedef enum { BSA_F32 = 0, BSA_BF16 = 1 } bsa_dtype_t;
+typedef enum { BSA_POOL_MLP = 0, BSA_POOL_MEAN = 1 } bsa_pool_t;
+
+/* Layer hyper-parameters (notation of Section 2). */
+typedef struct {
+  int32_t batch;          /* B: independent point clouds                               */
+  int32_t n;              /* N: token slots per cloud (power of two, >= 64)            */
+  int32_t heads;          /* H                                                         */
+  int32_t head_dim;       /* d: 32 or 64                                               */
+  int32_t ball_size;      /* m: ball size of Eq. 3 (power of two, divides N)           */
+  int32_t cmp_block;      /* l: compression block length of Eq. 5 (power of two)       */
+  int32_t cmp_stride;     /* compression stride; must equal cmp_block (Eq. 5)          */
+  int32_t slc_block;      /* l': selection block length of Eq. 8 (l'=r*l, r in 1,2,4;
+                             multiple of 16; divides m)                                */
+  int32_t topk;           /* k*: selected blocks per group (Eq. 7), 1..32              */
+  int32_t group_size;     /* g: query group size of Eq. 10 (8, 16, 32 or 64; divides m) */
+  int32_t mask_own_ball;  /* 1: a group may not select blocks of its own ball          */
+  int32_t store_lse;      /* must be 1: log-sum-exp rows are saved by the forward pass */
+  int32_t deterministic;  /* accepted for 0 and 1: every kernel is atomic-free on floats */
+  int32_t kv_pool;        /* bsa_pool_t: MLP (default) or mean pooling of Eq. 5        */
+  int32_t dtype;          /* bsa_dtype_t of Q, K, V, O, dO and the saved branch outputs */
+  float softmax_scale;    /* 0 -> 1/sqrt(d)                                            */
+} bsa_params_t;
+
+/* One compression MLP phi (Eq. 5): y = GELU_erf(x W1 + b1) W2 + b2 for the token-major
+ * flatten x of an l x d block (dummy rows zero). Float32, shared across heads:
+ * w1 [l*d, d], b1 [d], w2 [d, d], b2 [d], row-major. For bf16 layers w1 should hold
+ * bf16-representable values: the first layer runs on bf16 matrix cores. */
+typedef struct { const float *w1, *b1, *w2, *b2; } bsa_mlp_t;
+typedef struct { float *w1, *b1, *w2, *b2; } bsa_mlp_grad_t;
+
+/* Tensors the forward pass saves for the backward pass (all device, caller-owned).
+ * bsa_saved_view() carves them out of one buffer of bsa_sizes()'s saved_bytes. */
+typedef struct {
+  int32_t* sel_idx;  /* [B, H, N/g, k*] selected block ids, ascending, -1 = empty slot  */
+  float* lse;        /* [3, B, H, N] natural-log log-sum-exp per branch, -inf = no key  */
+  void* o_branch;    /* [3, B, H, N, d] dtype: ball, compression, selection outputs     */
+  float* kcmp;       /* [B, H, N/l, d] compressed keys                                  */
+  float* vcmp;       /* [B, H, N/l, d] compressed values                                */
+  float* hid_k;      /* [B, H, N/l, d] hidden pre-activation of phi_k                   */
+  float* hid_v;      /* [B, H, N/l, d] hidden pre-activation of phi_v                   */
+  uint8_t* cvalid;   /* [B, N/l] 1 if the compression block holds a real token          */
+} bsa_saved_t;
+
+/* ---- Ball tree (Section 2.1 "Ball Tree Attention"; the ordering every branch uses) ---- */
+
+/* Workspace bytes for bsa_build_ball_tree with these sizes (0 on invalid sizes). */
+size_t bsa_ball_tree_workspace_bytes(int64_t n_real, int64_t n_pad, int32_t dim, int32_t batch);
+
+/* Order each cloud by recursive median splits: a node of capacity C (a power of two)
+ * holding the point set S splits on the axis of largest spread (max - min, formed in
+ * float64; equal spreads -> lowest axis), its points ordered by (coordinate, index)
+ * with -0.0 equal to +0.0; the first ceil(|S|/2) go to the left child (slots
+ * [0, C/2)), the rest to the right child; recursion down to single slots.
+ *   points: [batch, n_real, dim] float32, finite; dim = 3 (2 and 1 also accepted).
+ *   perm:   [batch, n_pad] int32 output; slot -> point index within its cloud, -1 for a
+ *           padding slot. 1 <= n_real <= n_pad, n_pad a power of two, n_pad <= 2^24.
+ *   ws:     workspace of at least bsa_ball_tree_workspace_bytes() bytes. */
+bsa_status_t bsa_build_ball_tree(const float* points, int64_t n_real, int32_t dim,
+                                 int64_t n_pad, int32_t batch, int32_t* perm,
+                                 void* ws, size_t ws_bytes, void* stream);
+
+/* Gather per-point rows into ball order (the ordering step before Eq. 3):
+ *   src  [batch, n_real, heads*head_dim] (dtype) -> dst [batch, heads, n_pad, head_dim],
+ *   dst row = 0 where perm is -1. valid_out [batch, n_pad] (may be NULL) receives
+ *   1 for real slots and 0 for padding. head_dim may be any value >= 1 (e.g. heads=1,
+ *   head_dim=3 orders the gate logits). */
+bsa_status_t bsa_permute(const void* src, const int32_t* perm, int64_t n_real, int64_t n_pad,
+                         int32_t batch, int32_t heads, int32_t head_dim, int32_t dtype,
+                         void* dst, uint8_t* valid_out, void* stream);
+
+/* Inverse of bsa_permute: src [batch, heads, n_pad, head_dim] -> dst [batch, n_real,
+ * heads*head_dim]; padding slots are dropped. dtype BSA_F32 or BSA_BF16. */
+bsa_status_t bsa_unpermute(const void* src, const int32_t* perm, int64_t n_real, int64_t n_pad,
+                           int32_t batch, int32_t heads, int32_t head_dim, int32_t dtype,
+                           void* dst, void* stream);
+
+/* ---- The layer (Section 2.2, Eq. 3, 5-12, 9) ---- */
+
+/* Validate p and report the sizes of the forward workspace, the backward workspace and
+ * the saved-tensor buffer. Any pointer may be NULL. */
+bsa_status_t bsa_sizes(const bsa_params_t* p, size_t* ws_fwd_bytes, size_t* ws_bwd_bytes,
+                       size_t* saved_bytes);
+
+/* Point the fields of *out into the caller's buffer `base` of saved_bytes bytes
+ * (256-byte aligned sub-buffers). Host-only arithmetic; launches nothing. */
+bsa_status_t bsa_saved_view(const bsa_params_t* p, void* base, bsa_saved_t* out);
+
+/* Forward pass.
+ *   q, k, v: [B, H, N, d] dtype in ball order. valid: [B, N] uint8 (1 = real token) or
+ *   NULL (all real). gate: [B, N, 3] float32 logits gamma_b in branch order (ball,
+ *   compression, selection), shared across heads (Eq. 9). phi_k / phi_v: compression
+ *   MLPs for keys / values (ignored for BSA_POOL_MEAN).
+ *   o: [B, H, N, d] dtype output = sum_b sigmoid(gamma_b) * o_b; rows of padding slots 0.
+ *   saved: filled for bsa_backward (and readable as per-branch outputs, LSE and the
+ *   selected block ids). ws: at least ws_fwd_bytes. */
+bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, const void* v,
+                         const uint8_t* valid, const float* gate, const bsa_mlp_t* phi_k,
+                         const bsa_mlp_t* phi_v, void* o, const bsa_saved_t* saved,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/* Backward pass of bsa_forward given dO = d(loss)/d(o) ([B, H, N, d] dtype).
+ * Outputs (overwritten, float32): dq, dk, dv [B, H, N, d]; dgate [B, N, 3];
+ * dphi_k / dphi_v weight gradients summed over batch, heads and blocks (may be NULL for
+ * BSA_POOL_MEAN). No gradient flows through the top-k selection. Rows of padding slots
+ * get zero gradients. ws: at least ws_bwd_bytes. */
+bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, const void* v,
+                          const uint8_t* valid, const float* gate, const bsa_mlp_t* phi_k,
+                          const bsa_mlp_t* phi_v, const bsa_saved_t* saved, const void* d_o,
+                          float* dq, float* dk, float* dv, float* dgate,
+                          const bsa_mlp_grad_t* dphi_k, const bsa_mlp_grad_t* dphi_v,
+                          void* ws, size_t ws_bytes, void* stream);
+
+const char* bsa_status_string(bsa_status_t s);
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* bsa_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BSA_H */

@@ -1,0 +1,229 @@
+"""Thin torch binding of the BSA C ABI (argument marshalling only).
+
+Torch provides device memory and the current stream; every step of the layer runs in the
+HIP kernels of libbsa.so. Function names follow the C entry points of include/bsa.h.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import dataclasses
+import math
+
+import torch
+
+from . import _lib
+from ._lib import BSA_BF16, BSA_F32, BSA_POOL_MEAN, BSA_POOL_MLP, check
+
+__all__ = ["Params", "Saved", "build_ball_tree", "permute", "unpermute", "sizes", "forward", "backward",
+           "BSA_F32", "BSA_BF16", "BSA_POOL_MLP", "BSA_POOL_MEAN"]
+
+
+@dataclasses.dataclass
+class Params:
+    batch: int
+    n: int
+    heads: int
+    head_dim: int
+    ball_size: int
+    cmp_block: int
+    slc_block: int
+    topk: int
+    group_size: int
+    cmp_stride: int | None = None
+    mask_own_ball: int = 1
+    store_lse: int = 1
+    deterministic: int = 1
+    kv_pool: int = BSA_POOL_MLP
+    dtype: int = BSA_BF16
+    softmax_scale: float = 0.0
+
+    def c(self) -> _lib.bsa_params_t:
+        return _lib.bsa_params_t(
+            self.batch, self.n, self.heads, self.head_dim, self.ball_size, self.cmp_block,
+            self.cmp_block if self.cmp_stride is None else self.cmp_stride, self.slc_block, self.topk,
+            self.group_size, self.mask_own_ball, self.store_lse, self.deterministic, self.kv_pool,
+            self.dtype, self.softmax_scale)
+
+    @property
+    def torch_dtype(self) -> torch.dtype:
+        return torch.bfloat16 if self.dtype == BSA_BF16 else torch.float32
+
+    @classmethod
+    def from_config(cls, cfg, **kw) -> "Params":
+        return cls(batch=cfg.batch, n=cfg.n_pad, heads=cfg.heads, head_dim=cfg.head_dim, ball_size=cfg.ball,
+                   cmp_block=cfg.cmp_block, cmp_stride=cfg.cmp_stride, slc_block=cfg.slc_block, topk=cfg.topk,
+                   group_size=cfg.group, dtype=BSA_BF16 if cfg.dtype == "bf16" else BSA_F32, **kw)
+
+
+def _ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return C.c_void_p(s.cuda_stream)
+
+
+def _require(t, name, dtype, shape=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def build_ball_tree(points: torch.Tensor, n_pad: int, stream=None) -> torch.Tensor:
+    """Slot -> point permutation [B, n_pad] int32 (-1 = padding) of clouds [B, n_real, dim] f32."""
+    lib = _lib.load()
+    _require(points, "points", torch.float32)
+    B, n_real, dim = points.shape
+    ws_bytes = lib.bsa_ball_tree_workspace_bytes(n_real, n_pad, dim, B)
+    if ws_bytes == 0:
+        raise ValueError("invalid ball-tree sizes")
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=points.device)
+    perm = torch.empty((B, n_pad), dtype=torch.int32, device=points.device)
+    check(lib.bsa_build_ball_tree(_ptr(points), n_real, dim, n_pad, B, _ptr(perm), _ptr(ws), ws_bytes,
+                                  _stream(stream)), "bsa_build_ball_tree")
+    return perm
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return BSA_F32
+    if t.dtype == torch.bfloat16:
+        return BSA_BF16
+    raise ValueError("only float32 and bfloat16 are supported")
+
+
+def permute(src: torch.Tensor, perm: torch.Tensor, heads: int, head_dim: int, with_valid: bool = False,
+            stream=None):
+    """[B, n_real, heads*head_dim] -> [B, heads, n_pad, head_dim] in ball order (+ valid [B, n_pad] u8)."""
+    lib = _lib.load()
+    B, n_real, cols = src.shape
+    assert cols == heads * head_dim
+    _require(src, "src", src.dtype)
+    _require(perm, "perm", torch.int32)
+    n_pad = perm.shape[1]
+    dst = torch.empty((B, heads, n_pad, head_dim), dtype=src.dtype, device=src.device)
+    valid = torch.empty((B, n_pad), dtype=torch.uint8, device=src.device) if with_valid else None
+    check(lib.bsa_permute(_ptr(src), _ptr(perm), n_real, n_pad, B, heads, head_dim, _dtype_code(src), _ptr(dst),
+                          _ptr(valid), _stream(stream)), "bsa_permute")
+    return (dst, valid) if with_valid else dst
+
+
+def unpermute(src: torch.Tensor, perm: torch.Tensor, n_real: int, stream=None) -> torch.Tensor:
+    """[B, heads, n_pad, head_dim] in ball order -> [B, n_real, heads*head_dim]."""
+    lib = _lib.load()
+    B, heads, n_pad, hd = src.shape
+    _require(src, "src", src.dtype)
+    _require(perm, "perm", torch.int32)
+    dst = torch.empty((B, n_real, heads * hd), dtype=src.dtype, device=src.device)
+    check(lib.bsa_unpermute(_ptr(src), _ptr(perm), n_real, n_pad, B, heads, hd, _dtype_code(src), _ptr(dst),
+                            _stream(stream)), "bsa_unpermute")
+    return dst
+
+
+def sizes(p: Params):
+    """(forward workspace, backward workspace, saved) byte counts; raises on invalid params."""
+    lib = _lib.load()
+    a, b, c = C.c_size_t(), C.c_size_t(), C.c_size_t()
+    cp = p.c()
+    check(lib.bsa_sizes(C.byref(cp), C.byref(a), C.byref(b), C.byref(c)), "bsa_sizes")
+    return a.value, b.value, c.value
+
+
+class Saved:
+    """Tensors saved by forward(): one device buffer plus typed views of its parts."""
+
+    def __init__(self, p: Params, device):
+        lib = _lib.load()
+        _, _, nbytes = sizes(p)
+        self.p = p
+        self.buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        self.c = _lib.bsa_saved_t()
+        cp = p.c()
+        check(lib.bsa_saved_view(C.byref(cp), _ptr(self.buf), C.byref(self.c)), "bsa_saved_view")
+        base = self.buf.data_ptr()
+        B, H, N, d = p.batch, p.heads, p.n, p.head_dim
+
+        def view(ptr, dtype, shape):
+            off = ptr - base
+            count = math.prod(shape)
+            esz = torch.empty((), dtype=dtype).element_size()
+            return self.buf[off:off + count * esz].view(dtype).view(shape)
+
+        self.sel_idx = view(self.c.sel_idx, torch.int32, (B, H, N // p.group_size, p.topk))
+        self.lse = view(self.c.lse, torch.float32, (3, B, H, N))
+        self.o_branch = view(self.c.o_branch, p.torch_dtype, (3, B, H, N, d))
+        self.kcmp = view(self.c.kcmp, torch.float32, (B, H, N // p.cmp_block, d))
+        self.vcmp = view(self.c.vcmp, torch.float32, (B, H, N // p.cmp_block, d))
+        self.hid_k = view(self.c.hid_k, torch.float32, (B, H, N // p.cmp_block, d))
+        self.hid_v = view(self.c.hid_v, torch.float32, (B, H, N // p.cmp_block, d))
+        self.cvalid = view(self.c.cvalid, torch.uint8, (B, N // p.cmp_block))
+
+
+def _mlp(phi):
+    if phi is None:
+        return None
+    for w in ("w1", "b1", "w2", "b2"):
+        _require(phi[w], f"phi.{w}", torch.float32)
+    return _lib.bsa_mlp_t(phi["w1"].data_ptr(), phi["b1"].data_ptr(), phi["w2"].data_ptr(), phi["b2"].data_ptr())
+
+
+def forward(p: Params, q, k, v, valid, gate, phi_k, phi_v, saved: Saved | None = None, stream=None):
+    """Layer forward. Returns (o, saved)."""
+    lib = _lib.load()
+    shape = (p.batch, p.heads, p.n, p.head_dim)
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _require(t, name, p.torch_dtype, shape)
+    _require(gate, "gate", torch.float32, (p.batch, p.n, 3))
+    if valid is not None:
+        _require(valid, "valid", torch.uint8, (p.batch, p.n))
+    ws_bytes, _, _ = sizes(p)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
+    saved = saved or Saved(p, q.device)
+    o = torch.empty(shape, dtype=p.torch_dtype, device=q.device)
+    mk, mv = _mlp(phi_k), _mlp(phi_v)
+    cp = p.c()
+    check(lib.bsa_forward(C.byref(cp), _ptr(q), _ptr(k), _ptr(v), _ptr(valid), _ptr(gate),
+                          C.byref(mk) if mk else None, C.byref(mv) if mv else None, _ptr(o), C.byref(saved.c),
+                          _ptr(ws), ws_bytes, _stream(stream)), "bsa_forward")
+    return o, saved
+
+
+def backward(p: Params, q, k, v, valid, gate, phi_k, phi_v, saved: Saved, d_o, stream=None):
+    """Layer backward. Returns dict(dq, dk, dv, dgate, dphi_k, dphi_v) (float32)."""
+    lib = _lib.load()
+    shape = (p.batch, p.heads, p.n, p.head_dim)
+    for name, t in (("q", q), ("k", k), ("v", v), ("d_o", d_o)):
+        _require(t, name, p.torch_dtype, shape)
+    _require(gate, "gate", torch.float32, (p.batch, p.n, 3))
+    dev = q.device
+    _, ws_bytes, _ = sizes(p)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    dq = torch.empty(shape, dtype=torch.float32, device=dev)
+    dk = torch.empty_like(dq)
+    dv = torch.empty_like(dq)
+    dgate = torch.empty((p.batch, p.n, 3), dtype=torch.float32, device=dev)
+    grads = {}
+    cgr = []
+    for name, phi in (("dphi_k", phi_k), ("dphi_v", phi_v)):
+        if p.kv_pool == BSA_POOL_MLP:
+            g = {w: torch.empty_like(phi[w]) for w in ("w1", "b1", "w2", "b2")}
+            grads[name] = g
+            cgr.append(_lib.bsa_mlp_t(g["w1"].data_ptr(), g["b1"].data_ptr(), g["w2"].data_ptr(), g["b2"].data_ptr()))
+        else:
+            grads[name] = {}
+            cgr.append(None)
+    mk, mv = _mlp(phi_k), _mlp(phi_v)
+    cp = p.c()
+    check(lib.bsa_backward(C.byref(cp), _ptr(q), _ptr(k), _ptr(v), _ptr(valid), _ptr(gate),
+                           C.byref(mk) if mk else None, C.byref(mv) if mv else None, C.byref(saved.c), _ptr(d_o),
+                           _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dgate),
+                           C.byref(cgr[0]) if cgr[0] else None, C.byref(cgr[1]) if cgr[1] else None,
+                           _ptr(ws), ws_bytes, _stream(stream)), "bsa_backward")
+    grads.update(dq=dq, dk=dk, dv=dv, dgate=dgate)
+    return grads

@@ -1,0 +1,285 @@
+// C ABI of the BSA library: argument validation, buffer carving and the launch order of
+// the forward pass on the caller's stream. Declarations and contracts: include/bsa.h.
+#include "../../include/bsa.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <string>
+
+#include "kernels.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+bsa_status_t fail(bsa_status_t s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+bool pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+bsa_status_t hip_status(hipError_t e, const char* where) {
+  if (e == hipSuccess) return BSA_OK;
+  return fail(BSA_ERR_HIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+#define BSA_TRY(expr, where)                         \
+  do {                                               \
+    bsa_status_t _s = hip_status((expr), (where));   \
+    if (_s != BSA_OK) return _s;                     \
+  } while (0)
+
+// Validate p and fill the internal sizes.
+bsa_status_t check_params(const bsa_params_t* p, bsa::Dims* D) {
+  if (!p) return fail(BSA_ERR_INVALID_ARGUMENT, "params is NULL");
+  if (p->batch < 1 || p->heads < 1) return fail(BSA_ERR_INVALID_ARGUMENT, "batch and heads must be >= 1");
+  if (!pow2(p->n) || p->n < 64 || p->n > (1 << 24))
+    return fail(BSA_ERR_INVALID_ARGUMENT, "n must be a power of two in [64, 2^24]");
+  if (p->head_dim != 32 && p->head_dim != 64) return fail(BSA_ERR_UNSUPPORTED, "head_dim must be 32 or 64");
+  if (!pow2(p->ball_size) || p->ball_size < 64 || p->ball_size > p->n)
+    return fail(BSA_ERR_INVALID_ARGUMENT, "ball_size must be a power of two in [64, n]");
+  if (!pow2(p->cmp_block) || p->n / p->cmp_block < 16)
+    return fail(BSA_ERR_INVALID_ARGUMENT, "cmp_block must be a power of two with n/cmp_block >= 16");
+  if (p->cmp_stride != p->cmp_block)
+    return fail(BSA_ERR_UNSUPPORTED, "cmp_stride must equal cmp_block (non-overlapping blocks, Eq. 5)");
+  if (p->slc_block % 16 != 0 || p->slc_block % p->cmp_block != 0 || p->ball_size % p->slc_block != 0)
+    return fail(BSA_ERR_INVALID_ARGUMENT, "slc_block must be a multiple of 16 and of cmp_block and divide ball_size");
+  const int r = p->slc_block / p->cmp_block;
+  if (r != 1 && r != 2 && r != 4) return fail(BSA_ERR_UNSUPPORTED, "slc_block / cmp_block must be 1, 2 or 4");
+  if (!pow2(p->group_size) || p->group_size < 8 || p->ball_size % p->group_size != 0)
+    return fail(BSA_ERR_INVALID_ARGUMENT, "group_size must be a power of two >= 8 dividing ball_size");
+  if (p->topk < 1 || p->topk > 16) return fail(BSA_ERR_UNSUPPORTED, "topk must be in [1, 16]");
+  const int G = p->group_size >= 16 ? 1 : 16 / p->group_size;
+  if (G * p->topk * (p->slc_block / 16) > 256)
+    return fail(BSA_ERR_UNSUPPORTED, "too many selected tokens per 16-query block (limit 4096)");
+  if (p->mask_own_ball != 0 && p->mask_own_ball != 1) return fail(BSA_ERR_INVALID_ARGUMENT, "mask_own_ball must be 0/1");
+  if (p->store_lse != 1) return fail(BSA_ERR_UNSUPPORTED, "store_lse must be 1");
+  if (p->deterministic != 0 && p->deterministic != 1) return fail(BSA_ERR_INVALID_ARGUMENT, "deterministic must be 0/1");
+  if (p->kv_pool != BSA_POOL_MLP && p->kv_pool != BSA_POOL_MEAN) return fail(BSA_ERR_INVALID_ARGUMENT, "bad kv_pool");
+  if (p->dtype != BSA_F32 && p->dtype != BSA_BF16) return fail(BSA_ERR_INVALID_ARGUMENT, "bad dtype");
+  if (!(p->softmax_scale >= 0.0f) || std::isinf(p->softmax_scale))
+    return fail(BSA_ERR_INVALID_ARGUMENT, "softmax_scale must be finite and >= 0");
+  D->B = p->batch;
+  D->H = p->heads;
+  D->N = p->n;
+  D->d = p->head_dim;
+  D->m = p->ball_size;
+  D->l = p->cmp_block;
+  D->ls = p->slc_block;
+  D->k = p->topk;
+  D->g = p->group_size;
+  D->mask_own = p->mask_own_ball;
+  D->pool = p->kv_pool;
+  D->bf16 = p->dtype == BSA_BF16;
+  D->scale = p->softmax_scale > 0.f ? p->softmax_scale : 1.0f / std::sqrt((float)p->head_dim);
+  return BSA_OK;
+}
+
+size_t elem_bytes(const bsa::Dims& D) { return D.bf16 ? 2 : 4; }
+
+struct SavedLayout {
+  size_t sel, lse, ob, kc, vc, hk, hv, cv, total;
+};
+
+SavedLayout saved_layout(const bsa::Dims& D) {
+  SavedLayout L{};
+  const size_t rows = (size_t)D.rows();
+  const size_t crows = (size_t)D.cmp_rows();
+  size_t off = 0;
+  auto put = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
+  L.sel = put(sizeof(int32_t) * (size_t)D.B * D.H * (D.N / D.g) * D.k);
+  L.lse = put(sizeof(float) * 3 * rows);
+  L.ob = put(elem_bytes(D) * 3 * rows * D.d);
+  L.kc = put(sizeof(float) * crows * D.d);
+  L.vc = put(sizeof(float) * crows * D.d);
+  L.hk = put(sizeof(float) * crows * D.d);
+  L.hv = put(sizeof(float) * crows * D.d);
+  L.cv = put((size_t)D.B * (D.N / D.l));
+  L.total = off;
+  return L;
+}
+
+struct FwdWs {
+  size_t w1t_k, w1t_v, kc_lp, vc_lp, total;
+};
+
+FwdWs fwd_ws_layout(const bsa::Dims& D) {
+  FwdWs W{};
+  size_t off = 0;
+  auto put = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
+  const size_t w1 = elem_bytes(D) * (size_t)D.l * D.d * D.d;
+  W.w1t_k = put(w1);
+  W.w1t_v = put(w1);
+  W.kc_lp = put(elem_bytes(D) * (size_t)D.cmp_rows() * D.d);
+  W.vc_lp = put(elem_bytes(D) * (size_t)D.cmp_rows() * D.d);
+  W.total = off;
+  return W;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* bsa_status_string(bsa_status_t s) {
+  switch (s) {
+    case BSA_OK: return "ok";
+    case BSA_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case BSA_ERR_UNSUPPORTED: return "unsupported";
+    case BSA_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case BSA_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* bsa_last_error(void) { return g_last_error.c_str(); }
+
+size_t bsa_ball_tree_workspace_bytes(int64_t n_real, int64_t n_pad, int32_t dim, int32_t batch) {
+  if (n_real < 1 || n_real > n_pad || !pow2(n_pad) || n_pad > (1 << 24) || dim < 1 || dim > 3 || batch < 1) return 0;
+  if ((int64_t)batch * n_pad > (int64_t(1) << 30)) return 0;
+  return bsa::tree_workspace_bytes(n_real, n_pad, batch);
+}
+
+bsa_status_t bsa_build_ball_tree(const float* points, int64_t n_real, int32_t dim, int64_t n_pad, int32_t batch,
+                                 int32_t* perm, void* ws, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (!points || !perm) return fail(BSA_ERR_INVALID_ARGUMENT, "points and perm must be non-NULL");
+  if (dim < 1 || dim > 3) return fail(BSA_ERR_UNSUPPORTED, "dim must be 1, 2 or 3");
+  if (batch < 1) return fail(BSA_ERR_INVALID_ARGUMENT, "batch must be >= 1");
+  if (!pow2(n_pad) || n_pad > (1 << 24)) return fail(BSA_ERR_INVALID_ARGUMENT, "n_pad must be a power of two <= 2^24");
+  if (n_real < 1 || n_real > n_pad) return fail(BSA_ERR_INVALID_ARGUMENT, "need 1 <= n_real <= n_pad");
+  const size_t need = bsa_ball_tree_workspace_bytes(n_real, n_pad, dim, batch);
+  if (need == 0) return fail(BSA_ERR_INVALID_ARGUMENT, "batch * n_pad too large");
+  if (!ws || ws_bytes < need)
+    return fail(BSA_ERR_WORKSPACE_TOO_SMALL, "tree workspace needs " + std::to_string(need) + " bytes");
+  BSA_TRY(bsa::launch_build_tree(points, n_real, dim, n_pad, batch, perm, ws, (hipStream_t)stream),
+          "bsa_build_ball_tree");
+  return BSA_OK;
+}
+
+static bsa_status_t permute_common(const void* src, const int32_t* perm, int64_t n_real, int64_t n_pad, int32_t batch,
+                                   int32_t heads, int32_t head_dim, int32_t dtype, void* dst) {
+  if (!src || !perm || !dst) return fail(BSA_ERR_INVALID_ARGUMENT, "src, perm and dst must be non-NULL");
+  if (batch < 1 || heads < 1 || head_dim < 1) return fail(BSA_ERR_INVALID_ARGUMENT, "batch, heads, head_dim >= 1");
+  if (n_real < 1 || n_real > n_pad || n_pad > (1 << 24)) return fail(BSA_ERR_INVALID_ARGUMENT, "need 1 <= n_real <= n_pad <= 2^24");
+  if (dtype != BSA_F32 && dtype != BSA_BF16) return fail(BSA_ERR_INVALID_ARGUMENT, "bad dtype");
+  return BSA_OK;
+}
+
+bsa_status_t bsa_permute(const void* src, const int32_t* perm, int64_t n_real, int64_t n_pad, int32_t batch,
+                         int32_t heads, int32_t head_dim, int32_t dtype, void* dst, uint8_t* valid_out, void* stream) {
+  g_last_error.clear();
+  bsa_status_t s = permute_common(src, perm, n_real, n_pad, batch, heads, head_dim, dtype, dst);
+  if (s != BSA_OK) return s;
+  BSA_TRY(bsa::launch_permute(src, perm, n_real, n_pad, batch, heads, head_dim, dtype, dst, valid_out, false,
+                              (hipStream_t)stream),
+          "bsa_permute");
+  return BSA_OK;
+}
+
+bsa_status_t bsa_unpermute(const void* src, const int32_t* perm, int64_t n_real, int64_t n_pad, int32_t batch,
+                           int32_t heads, int32_t head_dim, int32_t dtype, void* dst, void* stream) {
+  g_last_error.clear();
+  bsa_status_t s = permute_common(src, perm, n_real, n_pad, batch, heads, head_dim, dtype, dst);
+  if (s != BSA_OK) return s;
+  BSA_TRY(bsa::launch_permute(src, perm, n_real, n_pad, batch, heads, head_dim, dtype, dst, nullptr, true,
+                              (hipStream_t)stream),
+          "bsa_unpermute");
+  return BSA_OK;
+}
+
+bsa_status_t bsa_sizes(const bsa_params_t* p, size_t* ws_fwd_bytes, size_t* ws_bwd_bytes, size_t* saved_bytes) {
+  g_last_error.clear();
+  bsa::Dims D;
+  bsa_status_t s = check_params(p, &D);
+  if (s != BSA_OK) return s;
+  if (ws_fwd_bytes) *ws_fwd_bytes = fwd_ws_layout(D).total;
+  if (ws_bwd_bytes) *ws_bwd_bytes = 0;
+  if (saved_bytes) *saved_bytes = saved_layout(D).total;
+  return BSA_OK;
+}
+
+bsa_status_t bsa_saved_view(const bsa_params_t* p, void* base, bsa_saved_t* out) {
+  g_last_error.clear();
+  bsa::Dims D;
+  bsa_status_t s = check_params(p, &D);
+  if (s != BSA_OK) return s;
+  if (!base || !out) return fail(BSA_ERR_INVALID_ARGUMENT, "base and out must be non-NULL");
+  SavedLayout L = saved_layout(D);
+  char* c = (char*)base;
+  out->sel_idx = (int32_t*)(c + L.sel);
+  out->lse = (float*)(c + L.lse);
+  out->o_branch = (void*)(c + L.ob);
+  out->kcmp = (float*)(c + L.kc);
+  out->vcmp = (float*)(c + L.vc);
+  out->hid_k = (float*)(c + L.hk);
+  out->hid_v = (float*)(c + L.hv);
+  out->cvalid = (uint8_t*)(c + L.cv);
+  return BSA_OK;
+}
+
+static bool saved_ok(const bsa_saved_t* sv) {
+  return sv && sv->sel_idx && sv->lse && sv->o_branch && sv->kcmp && sv->vcmp && sv->hid_k && sv->hid_v && sv->cvalid;
+}
+
+bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, const void* v, const uint8_t* valid,
+                         const float* gate, const bsa_mlp_t* phi_k, const bsa_mlp_t* phi_v, void* o,
+                         const bsa_saved_t* saved, void* ws, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  bsa::Dims D;
+  bsa_status_t s = check_params(p, &D);
+  if (s != BSA_OK) return s;
+  if (!q || !k || !v || !gate || !o) return fail(BSA_ERR_INVALID_ARGUMENT, "q, k, v, gate and o must be non-NULL");
+  if (!saved_ok(saved)) return fail(BSA_ERR_INVALID_ARGUMENT, "every saved buffer must be non-NULL");
+  if (D.pool == 0) {
+    if (!phi_k || !phi_v || !phi_k->w1 || !phi_k->b1 || !phi_k->w2 || !phi_k->b2 || !phi_v->w1 || !phi_v->b1 ||
+        !phi_v->w2 || !phi_v->b2)
+      return fail(BSA_ERR_INVALID_ARGUMENT, "MLP pooling needs phi_k and phi_v with all four tensors");
+  }
+  const FwdWs W = fwd_ws_layout(D);
+  if (!ws || ws_bytes < W.total)
+    return fail(BSA_ERR_WORKSPACE_TOO_SMALL, "forward workspace needs " + std::to_string(W.total) + " bytes");
+  hipStream_t st = (hipStream_t)stream;
+  char* w = (char*)ws;
+  const size_t rows = (size_t)D.rows();
+  char* ob = (char*)saved->o_branch;
+  const size_t ob_stride = rows * D.d * elem_bytes(D);
+  bsa::Mlp mk{}, mv{};
+  if (D.pool == 0) {
+    mk = {phi_k->w1, phi_k->b1, phi_k->w2, phi_k->b2};
+    mv = {phi_v->w1, phi_v->b1, phi_v->w2, phi_v->b2};
+  }
+  void* kc_lp = w + W.kc_lp;
+  void* vc_lp = w + W.vc_lp;
+  BSA_TRY(bsa::launch_block_valid(D, valid, saved->cvalid, st), "block_valid");
+  BSA_TRY(bsa::launch_compress_fwd(D, k, valid, mk, saved->kcmp, saved->hid_k, kc_lp, w + W.w1t_k, st), "compress K");
+  BSA_TRY(bsa::launch_compress_fwd(D, v, valid, mv, saved->vcmp, saved->hid_v, vc_lp, w + W.w1t_v, st), "compress V");
+  BSA_TRY(bsa::launch_select_topk(D, q, valid, saved->kcmp, saved->cvalid, saved->sel_idx, st), "select");
+  BSA_TRY(bsa::launch_ball_fwd(D, q, k, v, valid, ob, saved->lse, st), "ball attention");
+  BSA_TRY(bsa::launch_cmp_fwd(D, q, kc_lp, vc_lp, valid, saved->cvalid, ob + ob_stride, saved->lse + rows, st),
+          "compressed attention");
+  BSA_TRY(bsa::launch_slc_fwd(D, q, k, v, valid, saved->sel_idx, ob + 2 * ob_stride, saved->lse + 2 * rows, st),
+          "selection attention");
+  BSA_TRY(bsa::launch_gate_fwd(D, ob, gate, valid, o, st), "gate");
+  return BSA_OK;
+}
+
+bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, const void* v, const uint8_t* valid,
+                          const float* gate, const bsa_mlp_t* phi_k, const bsa_mlp_t* phi_v, const bsa_saved_t* saved,
+                          const void* d_o, float* dq, float* dk, float* dv, float* dgate,
+                          const bsa_mlp_grad_t* dphi_k, const bsa_mlp_grad_t* dphi_v, void* ws, size_t ws_bytes,
+                          void* stream) {
+  g_last_error.clear();
+  bsa::Dims D;
+  bsa_status_t s = check_params(p, &D);
+  if (s != BSA_OK) return s;
+  (void)q; (void)k; (void)v; (void)valid; (void)gate; (void)phi_k; (void)phi_v; (void)saved; (void)d_o;
+  (void)dq; (void)dk; (void)dv; (void)dgate; (void)dphi_k; (void)dphi_v; (void)ws; (void)ws_bytes; (void)stream;
+  return fail(BSA_ERR_UNSUPPORTED, "backward pass not built yet");
+}
+
+}  // extern "C"

@@ -1,0 +1,75 @@
+"""Shared helpers of the GPU parity tests: run the HIP path through the C ABI, run the
+float64 oracle on the same seeded inputs, and compare with the stated tolerances."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from oracle import bsa as ob
+from oracle.tree import build_ball_tree
+from paper_2506_12541_amd import bsa as gb
+from workloads import make_inputs, make_points
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}   # max-abs output tolerance per storage type
+TIE = 1e-6                          # score gap under which two blocks count as tied
+
+
+def oracle_params(cfg, **kw) -> ob.Params:
+    return ob.Params(ball=cfg.ball, cmp_block=cfg.cmp_block, slc_block=cfg.slc_block, topk=cfg.topk,
+                     group=cfg.group, **kw)
+
+
+def valid_from_tree(cfg, seed=None) -> np.ndarray:
+    """Real/padding slots of each cloud, from the oracle's tree on the config's points."""
+    if cfg.n_real == cfg.n_pad:
+        return np.ones((cfg.batch, cfg.n_pad), bool)
+    pts = make_points(cfg, seed)
+    return np.stack([build_ball_tree(pts[b], cfg.n_pad) >= 0 for b in range(cfg.batch)])
+
+
+def to_dev(x, dtype):
+    return torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(dtype)
+
+
+def gpu_forward(cfg, inp, valid, **pkw):
+    p = gb.Params.from_config(cfg, **pkw)
+    dt = p.torch_dtype
+    q, k, v = (to_dev(inp[n], dt) for n in ("q", "k", "v"))
+    gate = to_dev(inp["gate"], torch.float32)
+    vd = None if valid is None else to_dev(valid.astype(np.uint8), torch.uint8)
+    phi_k = {w: to_dev(a, torch.float32) for w, a in inp["phi_k"].items()}
+    phi_v = {w: to_dev(a, torch.float32) for w, a in inp["phi_v"].items()}
+    o, saved = gb.forward(p, q, k, v, vd, gate, phi_k, phi_v)
+    torch.cuda.synchronize()
+    f = lambda t: t.float().cpu().numpy()
+    return {"o": f(o), "o_branch": f(saved.o_branch), "lse": saved.lse.cpu().numpy(),
+            "sel": saved.sel_idx.cpu().numpy().astype(np.int64), "kc": saved.kcmp.cpu().numpy(),
+            "vc": saved.vcmp.cpu().numpy()}, (p, q, k, v, vd, gate, phi_k, phi_v, saved, o)
+
+
+def check_indices(sel_gpu, sel_or, scores):
+    """Bit-exact selected blocks, except where every differing block is within TIE of the
+    oracle's k-th score. Returns the number of rows that differ (all of them tie-justified)."""
+    assert sel_gpu.shape == sel_or.shape
+    k = sel_or.shape[-1]
+    diff_rows = 0
+    flat_g = sel_gpu.reshape(-1, k)
+    flat_o = sel_or.reshape(-1, k)
+    flat_s = scores.reshape(-1, scores.shape[-1])
+    for r in np.nonzero(np.any(flat_g != flat_o, axis=1))[0]:
+        g = set(int(x) for x in flat_g[r] if x >= 0)
+        o = set(int(x) for x in flat_o[r] if x >= 0)
+        assert len(g) == len(o), (r, flat_g[r], flat_o[r])
+        assert list(flat_g[r]) == sorted(g) + [-1] * (k - len(g)), "GPU row not ascending/-1 padded"
+        kth = np.sort(flat_s[r][np.isfinite(flat_s[r])])[::-1][len(o) - 1]
+        for blk in g ^ o:
+            assert abs(flat_s[r][blk] - kth) < TIE, (r, blk, flat_s[r][blk], kth)
+        diff_rows += 1
+    return diff_rows
+
+
+def max_abs(a, b, mask=None):
+    d = np.abs(np.asarray(a, np.float64) - np.asarray(b, np.float64))
+    if mask is not None:
+        d = d[mask]
+    return float(d.max()) if d.size else 0.0

@@ -1,0 +1,96 @@
+"""The C-ABI library loads, exports every entry point of include/bsa.h, and validates
+its arguments on the host (no kernel is launched by these tests)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2506_12541_amd import _lib
+from paper_2506_12541_amd.bsa import Params
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2506_12541_amd.build import build
+        build()
+    return _lib.load()
+
+
+def declared_symbols():
+    text = open(os.path.join(ROOT, "include", "bsa.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bsa_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_symbols()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(_lib._SIGS), "binding and header disagree"
+
+
+def _sizes(lib, p):
+    a, b, c = C.c_size_t(), C.c_size_t(), C.c_size_t()
+    cp = p.c()
+    return lib.bsa_sizes(C.byref(cp), C.byref(a), C.byref(b), C.byref(c)), a.value, c.value
+
+
+def base(**kw):
+    d = dict(batch=1, n=1024, heads=4, head_dim=32, ball_size=64, cmp_block=8, slc_block=16, topk=4, group_size=8)
+    d.update(kw)
+    return Params(**d)
+
+
+def test_valid_params(lib):
+    st, ws, saved = _sizes(lib, base())
+    assert st == _lib.BSA_OK and ws > 0 and saved > 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=1000), _lib.BSA_ERR_INVALID_ARGUMENT),
+    (dict(head_dim=48), _lib.BSA_ERR_UNSUPPORTED),
+    (dict(ball_size=96), _lib.BSA_ERR_INVALID_ARGUMENT),
+    (dict(ball_size=2048), _lib.BSA_ERR_INVALID_ARGUMENT),
+    (dict(cmp_block=8, cmp_stride=4), _lib.BSA_ERR_UNSUPPORTED),
+    (dict(slc_block=24), _lib.BSA_ERR_INVALID_ARGUMENT),
+    (dict(slc_block=64, cmp_block=8), _lib.BSA_ERR_UNSUPPORTED),
+    (dict(group_size=12), _lib.BSA_ERR_INVALID_ARGUMENT),
+    (dict(group_size=4), _lib.BSA_ERR_INVALID_ARGUMENT),
+    (dict(topk=0), _lib.BSA_ERR_UNSUPPORTED),
+    (dict(topk=17), _lib.BSA_ERR_UNSUPPORTED),
+    (dict(store_lse=0), _lib.BSA_ERR_UNSUPPORTED),
+    (dict(dtype=7), _lib.BSA_ERR_INVALID_ARGUMENT),
+    (dict(softmax_scale=-1.0), _lib.BSA_ERR_INVALID_ARGUMENT),
+])
+def test_invalid_params(lib, kw, code):
+    st, _, _ = _sizes(lib, base(**kw))
+    assert st == code
+    assert lib.bsa_last_error().decode() != ""
+
+
+def test_null_params(lib):
+    assert lib.bsa_sizes(None, None, None, None) == _lib.BSA_ERR_INVALID_ARGUMENT
+
+
+def test_forward_rejects_before_launch(lib):
+    p = base()
+    cp = p.c()
+    saved = _lib.bsa_saved_t()
+    # NULL q: rejected on the host, nothing launched
+    st = lib.bsa_forward(C.byref(cp), None, None, None, None, None, None, None, None, C.byref(saved), None, 0, None)
+    assert st == _lib.BSA_ERR_INVALID_ARGUMENT
+
+
+def test_tree_argument_errors(lib):
+    assert lib.bsa_ball_tree_workspace_bytes(100, 96, 3, 1) == 0
+    assert lib.bsa_ball_tree_workspace_bytes(100, 128, 3, 1) > 0
+    fake = C.c_void_p(16)
+    assert lib.bsa_build_ball_tree(None, 10, 3, 16, 1, fake, fake, 1 << 20, None) == _lib.BSA_ERR_INVALID_ARGUMENT
+    assert lib.bsa_build_ball_tree(fake, 10, 4, 16, 1, fake, fake, 1 << 20, None) == _lib.BSA_ERR_UNSUPPORTED
+    assert lib.bsa_build_ball_tree(fake, 20, 3, 16, 1, fake, fake, 1 << 20, None) == _lib.BSA_ERR_INVALID_ARGUMENT
+    assert lib.bsa_build_ball_tree(fake, 10, 3, 16, 1, fake, fake, 1, None) == _lib.BSA_ERR_WORKSPACE_TOO_SMALL

@@ -1,0 +1,101 @@
+"""GPU forward pass vs the float64 oracle on the same seeded inputs.
+
+Selected blocks must match bit-exactly except where the oracle's own scores tie within
+1e-6; branch outputs are compared with the oracle re-run on the GPU's selection, at
+max-abs 1e-4 (f32 layers) or 2e-2 (bf16 layers)."""
+import numpy as np
+import pytest
+
+from oracle import bsa as ob
+from parity import TOL, check_indices, gpu_forward, max_abs, oracle_params, valid_from_tree
+from workloads import CONFIGS, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _f64(x):
+    return np.asarray(x, np.float64)
+
+
+def _check_head(cfg, inp, valid, g, b, h, P, tol, groups=None):
+    q, k, v = (_f64(inp[n][b, h]) for n in ("q", "k", "v"))
+    phk = {w: _f64(a) for w, a in inp["phi_k"].items()}
+    phv = {w: _f64(a) for w, a in inp["phi_v"].items()}
+    vb = valid[b]
+    kc, _ = ob.compress(k, vb, phk, P)
+    vc, _ = ob.compress(v, vb, phv, P)
+    assert max_abs(g["kc"][b, h], kc) < 1e-4 and max_abs(g["vc"][b, h], vc) < 1e-4
+    scores = ob.group_block_scores(q, kc, vb, P)
+    n = q.shape[0]
+    gsel = g["sel"][b, h]
+    if groups is None:
+        groups = np.arange(n // P.group)
+        rows = np.arange(n)
+    else:
+        rows = (groups[:, None] * P.group + np.arange(P.group)[None, :]).reshape(-1)
+    osel = ob.topk_blocks(scores[groups], P.topk)
+    ndiff = check_indices(gsel[groups], osel, scores[groups])
+    # branch outputs given the GPU's selection
+    rmask = np.zeros(n, bool)
+    rmask[rows] = True
+    rv = rmask & vb
+    o_ball, l_ball = ob.ball_branch(q, k, v, vb, P)
+    o_cmp, l_cmp = ob.compression_branch(q, kc, vc, ob.block_valid(vb, P.cmp_block), vb, P, rows=rows)
+    o_slc, l_slc = ob.selection_branch(q, k, v, vb, gsel, P, groups=groups)
+    outs = (o_ball, o_cmp, o_slc)
+    lses = (l_ball, l_cmp, l_slc)
+    for br in range(3):
+        err = max_abs(g["o_branch"][br, b, h], outs[br], rv)
+        assert err < tol, (br, err)
+        assert max_abs(g["lse"][br, b, h], lses[br], rv) < tol, br
+        assert not np.any(g["o_branch"][br, b, h][rmask & ~vb]), "padding rows must be zero"
+    sg = 1.0 / (1.0 + np.exp(-_f64(inp["gate"][b])))
+    o = sum(sg[:, br, None] * outs[br] for br in range(3))
+    assert max_abs(g["o"][b, h], o, rv) < tol
+    assert not np.any(g["o"][b, h][rmask & ~vb])
+    return ndiff
+
+
+@pytest.mark.parametrize("cfg_id", [1, 2])
+def test_forward_full(cfg_id):
+    cfg = CONFIGS[cfg_id]
+    print(f"forward parity config {cfg_id}", flush=True)
+    inp = make_inputs(cfg, layout="ball", with_grad=False)
+    valid = valid_from_tree(cfg)
+    g, _ = gpu_forward(cfg, inp, valid)
+    P = oracle_params(cfg)
+    tol = TOL[cfg.dtype]
+    ndiff = 0
+    for b in range(cfg.batch):
+        for h in range(cfg.heads):
+            ndiff += _check_head(cfg, inp, valid, g, b, h, P, tol)
+    print(f"tie-justified index differences: {ndiff} rows")
+
+
+def test_forward_scaling_sampled():
+    """The 65536-point workload at full size; oracle on 96 sampled groups of two heads."""
+    cfg = CONFIGS[3]
+    print("forward parity config 3 (sampled)", flush=True)
+    inp = make_inputs(cfg, layout="ball", with_grad=False)
+    valid = valid_from_tree(cfg)
+    g, _ = gpu_forward(cfg, inp, valid)
+    P = oracle_params(cfg)
+    rng = np.random.default_rng(3)
+    ngroups = cfg.n_pad // cfg.group
+    for h in (0, cfg.heads - 1):
+        groups = np.sort(np.concatenate([[0, ngroups - 1], rng.choice(ngroups, 94, replace=False)]))
+        groups = np.unique(groups)
+        _check_head(cfg, inp, valid, g, 0, h, P, TOL[cfg.dtype], groups=groups)
+
+
+def test_forward_no_own_ball_mask_and_mean_pool():
+    cfg = CONFIGS[1]
+    inp = make_inputs(cfg, layout="ball", with_grad=False)
+    valid = np.ones((1, cfg.n_pad), bool)
+    valid[0, 100:140] = False
+    for kw, okw in ((dict(mask_own_ball=0), dict(mask_own_ball=False)), (dict(kv_pool=1), dict(kv_pool="mean"))):
+        print(f"forward variant {kw}", flush=True)
+        g, _ = gpu_forward(cfg, inp, valid, **kw)
+        P = oracle_params(cfg, **okw)
+        for h in range(cfg.heads):
+            _check_head(cfg, inp, valid, g, 0, h, P, TOL[cfg.dtype])
