@@ -49,16 +49,14 @@ __device__ __forceinline__ void store_col4(float* dst, float a, float b, float c
 // Stage 4 rows x 8 columns of V (row pointers may be null = zero rows) into V^T.
 template <typename T>
 __device__ __forceinline__ void stage_vt(const T* const (&rows)[4], int dc, T* vt, int vstr, int key_off) {
-  typename Chunk<T>::type c[4];
+  T vals[4][8];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    c[u] = zero_chunk(c[u]);
-    if (rows[u]) c[u] = load_chunk(rows[u] + dc);
-  }
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int x = 0; x < 8; ++x) vals[u][x] = rows[u] ? rows[u][dc + x] : T(0);
 #pragma unroll
   for (int x = 0; x < 8; ++x)
-    store_col4(vt + (dc + x) * vstr + key_off, __builtin_bit_cast(T, c[0][x]), __builtin_bit_cast(T, c[1][x]),
-               __builtin_bit_cast(T, c[2][x]), __builtin_bit_cast(T, c[3][x]));
+    store_col4(vt + (dc + x) * vstr + key_off, vals[0][x], vals[1][x], vals[2][x], vals[3][x]);
 }
 
 // Online-softmax state of one wave over QB blocks of 16 queries.
