@@ -61,6 +61,8 @@ bsa_status_t check_params(const bsa_params_t* p, bsa::Dims* D) {
   if (p->store_lse != 1) return fail(BSA_ERR_UNSUPPORTED, "store_lse must be 1");
   if (p->deterministic != 0 && p->deterministic != 1) return fail(BSA_ERR_INVALID_ARGUMENT, "deterministic must be 0/1");
   if (p->kv_pool != BSA_POOL_MLP && p->kv_pool != BSA_POOL_MEAN) return fail(BSA_ERR_INVALID_ARGUMENT, "bad kv_pool");
+  if (p->kv_pool == BSA_POOL_MLP && (p->cmp_block * p->head_dim) % 64 != 0)
+    return fail(BSA_ERR_UNSUPPORTED, "MLP pooling needs cmp_block * head_dim to be a multiple of 64");
   if (p->dtype != BSA_F32 && p->dtype != BSA_BF16) return fail(BSA_ERR_INVALID_ARGUMENT, "bad dtype");
   if (!(p->softmax_scale >= 0.0f) || std::isinf(p->softmax_scale))
     return fail(BSA_ERR_INVALID_ARGUMENT, "softmax_scale must be finite and >= 0");
@@ -117,6 +119,43 @@ FwdWs fwd_ws_layout(const bsa::Dims& D) {
   W.w1t_v = put(w1);
   W.kc_lp = put(elem_bytes(D) * (size_t)D.cmp_rows() * D.d);
   W.vc_lp = put(elem_bytes(D) * (size_t)D.cmp_rows() * D.d);
+  W.total = off;
+  return W;
+}
+
+struct BwdWs {
+  size_t R, kc_lp, vc_lp, dkc_part, dvc_part, dkc, dvc, pk, pv, pkt, pvt, hist, seg_s, seg_e, dpre, pw1, psm, total;
+  int cmp_chunks, mlp_chunks;
+  long long pairs, nseg;
+};
+
+BwdWs bwd_ws_layout(const bsa::Dims& D) {
+  BwdWs W{};
+  size_t off = 0;
+  auto put = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
+  const size_t rows = (size_t)D.rows();
+  const size_t crows = (size_t)D.cmp_rows();
+  W.cmp_chunks = D.N / 8 >= 64 ? 8 : 1;
+  W.mlp_chunks = bsa::mlp_bwd_chunks(D);
+  W.pairs = (long long)D.B * D.H * (D.N / D.g) * D.k;
+  W.nseg = (long long)D.B * D.H * (D.N / D.ls);
+  W.R = put(sizeof(float) * 3 * rows);
+  W.kc_lp = put(elem_bytes(D) * crows * D.d);
+  W.vc_lp = put(elem_bytes(D) * crows * D.d);
+  W.dkc_part = put(sizeof(float) * W.cmp_chunks * crows * D.d);
+  W.dvc_part = put(sizeof(float) * W.cmp_chunks * crows * D.d);
+  W.dkc = put(sizeof(float) * crows * D.d);
+  W.dvc = put(sizeof(float) * crows * D.d);
+  W.pk = put(4 * (size_t)W.pairs);
+  W.pv = put(4 * (size_t)W.pairs);
+  W.pkt = put(4 * (size_t)W.pairs);
+  W.pvt = put(4 * (size_t)W.pairs);
+  W.hist = put(4 * bsa::radix_sort_hist_words(W.pairs));
+  W.seg_s = put(4 * (size_t)W.nseg);
+  W.seg_e = put(4 * (size_t)W.nseg);
+  W.dpre = put(sizeof(float) * crows * D.d);
+  W.pw1 = put(sizeof(float) * (size_t)W.mlp_chunks * D.l * D.d * D.d);
+  W.psm = put(sizeof(float) * (size_t)W.mlp_chunks * ((size_t)D.d * D.d + 2 * D.d));
   W.total = off;
   return W;
 }
@@ -198,7 +237,7 @@ bsa_status_t bsa_sizes(const bsa_params_t* p, size_t* ws_fwd_bytes, size_t* ws_b
   bsa_status_t s = check_params(p, &D);
   if (s != BSA_OK) return s;
   if (ws_fwd_bytes) *ws_fwd_bytes = fwd_ws_layout(D).total;
-  if (ws_bwd_bytes) *ws_bwd_bytes = 0;
+  if (ws_bwd_bytes) *ws_bwd_bytes = bwd_ws_layout(D).total;
   if (saved_bytes) *saved_bytes = saved_layout(D).total;
   return BSA_OK;
 }
@@ -277,9 +316,47 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   bsa::Dims D;
   bsa_status_t s = check_params(p, &D);
   if (s != BSA_OK) return s;
-  (void)q; (void)k; (void)v; (void)valid; (void)gate; (void)phi_k; (void)phi_v; (void)saved; (void)d_o;
-  (void)dq; (void)dk; (void)dv; (void)dgate; (void)dphi_k; (void)dphi_v; (void)ws; (void)ws_bytes; (void)stream;
-  return fail(BSA_ERR_UNSUPPORTED, "backward pass not built yet");
+  if (!q || !k || !v || !gate || !d_o || !dq || !dk || !dv || !dgate)
+    return fail(BSA_ERR_INVALID_ARGUMENT, "q, k, v, gate, d_o, dq, dk, dv and dgate must be non-NULL");
+  if (!saved_ok(saved)) return fail(BSA_ERR_INVALID_ARGUMENT, "every saved buffer must be non-NULL");
+  if (D.pool == 0) {
+    auto full = [](const bsa_mlp_t* m) { return m && m->w1 && m->b1 && m->w2 && m->b2; };
+    auto fullg = [](const bsa_mlp_grad_t* m) { return m && m->w1 && m->b1 && m->w2 && m->b2; };
+    if (!full(phi_k) || !full(phi_v) || !fullg(dphi_k) || !fullg(dphi_v))
+      return fail(BSA_ERR_INVALID_ARGUMENT, "MLP pooling needs phi_k, phi_v, dphi_k and dphi_v with all four tensors");
+  }
+  const BwdWs W = bwd_ws_layout(D);
+  if (!ws || ws_bytes < W.total)
+    return fail(BSA_ERR_WORKSPACE_TOO_SMALL, "backward workspace needs " + std::to_string(W.total) + " bytes");
+  hipStream_t st = (hipStream_t)stream;
+  char* w = (char*)ws;
+  bsa::BwdArgs A{};
+  A.q = q; A.k = k; A.v = v; A.dout = d_o; A.valid = valid; A.gate = gate;
+  A.o_branch = saved->o_branch; A.lse = saved->lse; A.kcmp = saved->kcmp; A.vcmp = saved->vcmp;
+  A.hid_k = saved->hid_k; A.hid_v = saved->hid_v; A.sel = saved->sel_idx; A.cvalid = saved->cvalid;
+  A.dq = dq; A.dk = dk; A.dv = dv; A.dgate = dgate;
+  A.R = (float*)(w + W.R);
+  A.kc_lp = w + W.kc_lp; A.vc_lp = w + W.vc_lp;
+  A.dkc_part = (float*)(w + W.dkc_part); A.dvc_part = (float*)(w + W.dvc_part);
+  A.dkc = (float*)(w + W.dkc); A.dvc = (float*)(w + W.dvc);
+  A.pair_keys = (uint32_t*)(w + W.pk); A.pair_vals = (uint32_t*)(w + W.pv);
+  A.pair_keys_tmp = (uint32_t*)(w + W.pkt); A.pair_vals_tmp = (uint32_t*)(w + W.pvt);
+  A.sort_hist = (uint32_t*)(w + W.hist);
+  A.seg_start = (int*)(w + W.seg_s); A.seg_end = (int*)(w + W.seg_e);
+  BSA_TRY(bsa::launch_attn_bwd(D, A, st), "attention backward");
+  bsa::MlpBwdWs mw{(float*)(w + W.dpre), (float*)(w + W.pw1), (float*)(w + W.psm), W.mlp_chunks};
+  bsa::Mlp mk{}, mv{};
+  bsa::MlpGrad gk{}, gv{};
+  if (D.pool == 0) {
+    mk = {phi_k->w1, phi_k->b1, phi_k->w2, phi_k->b2};
+    mv = {phi_v->w1, phi_v->b1, phi_v->w2, phi_v->b2};
+    gk = {dphi_k->w1, dphi_k->b1, dphi_k->w2, dphi_k->b2};
+    gv = {dphi_v->w1, dphi_v->b1, dphi_v->w2, dphi_v->b2};
+  }
+  BSA_TRY(bsa::launch_compress_bwd(D, k, valid, mk, saved->hid_k, A.dkc, dk, gk, mw, st), "compression backward K");
+  BSA_TRY(bsa::launch_compress_bwd(D, v, valid, mv, saved->hid_v, A.dvc, dv, gv, mw, st), "compression backward V");
+  BSA_TRY(bsa::launch_slc_csr(D, A, st), "selection backward");
+  return BSA_OK;
 }
 
 }  // extern "C"

@@ -1,0 +1,806 @@
+// Backward pass of the three attention branches and of the gate (Section 2.2, Eq. 3, 5,
+// 8, 9). With dO_b = sigmoid(gamma_b) dO and per-row delta D_b = rowsum(dO_b * o_b), each
+// branch is softmax attention, so with P = exp(S - LSE):
+//     dP = dO_b V^T,  dS = P * (dP - D_b),  dQ = scale dS K,  dK = scale dS^T Q,  dV = P^T dO_b.
+// No gradient flows through the top-k selection (it is piecewise constant).
+//
+// Every gradient is produced without floating-point atomics, so results are
+// deterministic: a query-major pass per branch accumulates dQ (forward layout: a lane
+// owns one query, S^T = K Q^T), and a key-major pass accumulates dK and dV (a lane owns
+// one key, S = Q K^T). The compressed branch splits its queries into chunks whose
+// partial dK/dV are summed in a fixed order; the selection branch inverts the selected
+// block lists (block -> groups, ascending) by a stable radix sort first.
+#include "common.hpp"
+#include "kernels.hpp"
+#include "attn_common.hpp"
+
+namespace bsa {
+namespace {
+
+__device__ __forceinline__ float sigmoidf(float x) { return 1.0f / (1.0f + __expf(-x)); }
+
+// log2-domain LSE; rows without keys get +inf so that every probability is zero.
+__device__ __forceinline__ float lse_log2(float lse) { return lse == -__builtin_huge_valf() ? __builtin_huge_valf() : lse * kLog2e; }
+
+// ---- gate backward: R_b = rowsum(dO * o_b) per (b,h,n); dgamma_b = s'(gamma_b) sum_h R_b ----
+template <typename T>
+__global__ void gate_bwd_rows_kernel(const T* dout, const T* ob, long long rows, int hd, float* R) {
+  long long row = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (row >= rows) return;
+  const long long per = rows * hd;
+  float acc[3] = {0.f, 0.f, 0.f};
+  const T* d = dout + row * hd;
+  for (int c = 0; c < hd; c += 8) {
+    auto dc = load_chunk(d + c);
+#pragma unroll
+    for (int br = 0; br < 3; ++br) {
+      auto oc = load_chunk(ob + br * per + row * hd + c);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[br] += (float)dc[e] * (float)oc[e];
+    }
+  }
+#pragma unroll
+  for (int br = 0; br < 3; ++br) R[br * rows + row] = acc[br];
+}
+
+__global__ void gate_bwd_kernel(const float* R, const float* gate, const uint8_t* valid, int B, int H, int N,
+                                float* dgate) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= B * N) return;
+  int b = i / N, n = i % N;
+  const long long rows = (long long)B * H * N;
+#pragma unroll
+  for (int br = 0; br < 3; ++br) {
+    float sum = 0.f;
+    if (valid == nullptr || valid[i])
+      for (int h = 0; h < H; ++h) sum += R[br * rows + ((long long)b * H + h) * N + n];
+    float s = sigmoidf(gate[(size_t)i * 3 + br]);
+    dgate[(size_t)i * 3 + br] = s * (1.f - s) * sum;
+  }
+}
+
+template <typename T>
+__global__ void cast_kernel(const float* x, long long n, T* y) {
+  long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) y[i] = from_f32<T>(x[i]);
+}
+
+__global__ void sum_chunks_kernel(const float* part, int nchunks, long long n, float* out) {
+  long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  for (int c = 0; c < nchunks; ++c) s += part[(long long)c * n + i];
+  out[i] = s;
+}
+
+// Per-query terms of one branch: log2 LSE, delta D = s * R, gate scale s.
+struct QTerms {
+  const float* lse;   // [B,H,N] of this branch
+  const float* R;     // [B,H,N] rowsum(dO * o_b) of this branch
+  const float* gate;  // [B,N,3]
+  int br;
+};
+
+// ==== query-major pass, dense key sets (ball: own ball; compression: all tokens) ====
+template <typename T, int HD, int QB, bool BALL, bool ADD>
+__global__ void __launch_bounds__(256) dense_bwd_q_kernel(const T* q, const T* k, const T* v, const T* dout,
+                                                          const uint8_t* kvalid_all, QTerms qt, int H, int N,
+                                                          int nkeys_total, int m, float sl2, float scale, float* dq) {
+  constexpr int NCH = HD / 32, DB = HD / 16;
+  constexpr int KSTR = HD + 16 / (int)sizeof(T);
+  constexpr int VSTR = kKT + 4;
+  constexpr int EPV = 16 / (int)sizeof(T);
+  typedef typename Chunk<T>::type CT;
+  __shared__ __attribute__((aligned(16))) T ks[kKT * KSTR];
+  __shared__ __attribute__((aligned(16))) T vs[kKT * KSTR];
+  __shared__ __attribute__((aligned(16))) T kt[HD * VSTR];
+  __shared__ uint8_t kok[kKT];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r = lane & 15, j = lane >> 4;
+  const int b = blockIdx.z, h = blockIdx.y;
+  const long long bh = (long long)b * H + h;
+  const int q0 = blockIdx.x * (64 * QB);
+  const int nkeys = BALL ? m : nkeys_total;
+  const int key0 = BALL ? (q0 / m) * m : 0;
+  const T* kh = k + (bh * nkeys_total + key0) * HD;
+  const T* vh = v + (bh * nkeys_total + key0) * HD;
+  const uint8_t* kval = kvalid_all ? kvalid_all + (size_t)b * nkeys_total + key0 : nullptr;
+  const int wq0 = q0 + wid * 16 * QB;
+
+  CT qf[QB][NCH], df[QB][NCH];
+  float l2[QB], dd[QB], gs[QB];
+  f32x4 acc[QB][DB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const long long row = bh * N + wq0 + 16 * qb + r;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      qf[qb][c] = load_chunk(q + row * HD + 32 * c + 8 * j);
+      df[qb][c] = load_chunk(dout + row * HD + 32 * c + 8 * j);
+    }
+    l2[qb] = lse_log2(qt.lse[row]);
+    gs[qb] = sigmoidf(qt.gate[((size_t)b * N + wq0 + 16 * qb + r) * 3 + qt.br]);
+    dd[qb] = gs[qb] * qt.R[row];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) acc[qb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  for (int t0 = 0; t0 < nkeys; t0 += kKT) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < kKT * HD / EPV; e += 256) {
+      const int row = e / (HD / EPV), col = (e % (HD / EPV)) * EPV;
+      uint4 kv = make_uint4(0, 0, 0, 0), vv = kv;
+      if (t0 + row < nkeys) {
+        kv = *reinterpret_cast<const uint4*>(kh + (size_t)(t0 + row) * HD + col);
+        vv = *reinterpret_cast<const uint4*>(vh + (size_t)(t0 + row) * HD + col);
+      }
+      *reinterpret_cast<uint4*>(&ks[row * KSTR + col]) = kv;
+      *reinterpret_cast<uint4*>(&vs[row * KSTR + col]) = vv;
+    }
+    for (int e = threadIdx.x; e < (kKT / 4) * (HD / 8); e += 256) {
+      const int kq = e / (HD / 8), dc = (e % (HD / 8)) * 8;
+      const T* rows[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int key = t0 + 4 * kq + u;
+        rows[u] = key < nkeys ? kh + (size_t)key * HD : nullptr;
+      }
+      stage_vt(rows, dc, kt, VSTR, 4 * kq);
+    }
+    if (threadIdx.x < kKT) {
+      const int key = t0 + threadIdx.x;
+      kok[threadIdx.x] = key < nkeys && (kval == nullptr || kval[key]);
+    }
+    __syncthreads();
+    constexpr int KB = kKT / 16;
+    f32x4 s[QB][KB], dp[QB][KB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) { s[qb][kb] = f32x4{0.f, 0.f, 0.f, 0.f}; dp[qb][kb] = s[qb][kb]; }
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        CT ak = load_chunk(&ks[(kb * 16 + r) * KSTR + 32 * c + 8 * j]);
+        CT av = load_chunk(&vs[(kb * 16 + r) * KSTR + 32 * c + 8 * j]);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+          s[qb][kb] = mma(ak, qf[qb][c], s[qb][kb]);
+          dp[qb][kb] = mma(av, df[qb][c], dp[qb][kb]);
+        }
+      }
+    CT dsf[QB][KB / 2];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float v8[KB][4];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const bool ok = kok[kb * 16 + 4 * j + i] != 0;
+          const float p = ok ? fast_exp2(__builtin_fmaf(s[qb][kb][i], sl2, -l2[qb])) : 0.f;
+          v8[kb][i] = p * __builtin_fmaf(dp[qb][kb][i], gs[qb], -dd[qb]);
+        }
+#pragma unroll
+      for (int kp = 0; kp < KB / 2; ++kp) {
+        float w8[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) { w8[i] = v8[2 * kp][i]; w8[4 + i] = v8[2 * kp + 1][i]; }
+        dsf[qb][kp] = make_chunk<T>(w8);
+      }
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int kp = 0; kp < KB / 2; ++kp) {
+        CT a = load_4x2(&kt[(16 * db + r) * VSTR + 32 * kp + 4 * j]);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) acc[qb][db] = mma(a, dsf[qb][kp], acc[qb][db]);
+      }
+  }
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const long long row = bh * N + wq0 + 16 * qb + r;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      float* dst = dq + row * HD + 16 * db + 4 * j;
+      f32x4 val = acc[qb][db] * scale;
+      if (ADD) {
+        float4 old = *reinterpret_cast<float4*>(dst);
+        val[0] += old.x; val[1] += old.y; val[2] += old.z; val[3] += old.w;
+      }
+      store4(dst, val, 1.0f);
+    }
+  }
+}
+
+// ==== key-major pass, dense key sets: dK, dV of NW*32 keys per workgroup ====
+// Queries are staged 64 at a time in LDS (row-major for the S and dP products, transposed
+// for the dK^T and dV^T products); each wave owns 32 keys in registers.
+constexpr int kQT = 64;
+
+template <typename T, int HD, int NW, bool BALL>
+__global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const T* k, const T* v, const T* dout,
+                                                               const uint8_t* kvalid_all, QTerms qt, int H, int N,
+                                                               int nkeys_total, int m, int nchunks, float sl2,
+                                                               float scale, float* dk_out, float* dv_out) {
+  constexpr int NCH = HD / 32, DB = HD / 16;
+  constexpr int QSTR = HD + 16 / (int)sizeof(T);
+  constexpr int TSTR = kQT + 4;
+  constexpr int EPV = 16 / (int)sizeof(T);
+  constexpr int KBW = 2;  // 16-key blocks per wave
+  typedef typename Chunk<T>::type CT;
+  __shared__ __attribute__((aligned(16))) T qs[kQT * QSTR];
+  __shared__ __attribute__((aligned(16))) T ds_[kQT * QSTR];
+  __shared__ __attribute__((aligned(16))) T qtr[HD * TSTR];
+  __shared__ __attribute__((aligned(16))) T dtr[HD * TSTR];
+  __shared__ __attribute__((aligned(16))) float l2s[kQT], dds[kQT], gss[kQT];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r = lane & 15, j = lane >> 4;
+  const int bh = blockIdx.z;
+  const int b = bh / H;
+  const int chunk = blockIdx.y;
+  const int key0 = blockIdx.x * (NW * 32);
+  const int wk0 = key0 + wid * 32;
+  // query range of this workgroup
+  int qbeg, qend;
+  if (BALL) {
+    qbeg = (key0 / m) * m;
+    qend = qbeg + m;
+  } else {
+    const int per = N / nchunks;
+    qbeg = chunk * per;
+    qend = qbeg + per;
+  }
+  const T* qh = q + (size_t)bh * N * HD;
+  const T* dh = dout + (size_t)bh * N * HD;
+  const long long rowbase = (long long)bh * N;
+
+  CT kf[KBW][NCH], vf[KBW][NCH];
+  bool kok[KBW];
+#pragma unroll
+  for (int kb = 0; kb < KBW; ++kb) {
+    const int key = wk0 + 16 * kb + r;
+    kok[kb] = key < nkeys_total && (kvalid_all == nullptr || kvalid_all[(size_t)b * nkeys_total + key]);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      kf[kb][c] = zero_chunk(kf[kb][c]);
+      vf[kb][c] = zero_chunk(vf[kb][c]);
+      if (key < nkeys_total) {
+        kf[kb][c] = load_chunk(k + ((size_t)bh * nkeys_total + key) * HD + 32 * c + 8 * j);
+        vf[kb][c] = load_chunk(v + ((size_t)bh * nkeys_total + key) * HD + 32 * c + 8 * j);
+      }
+    }
+  }
+  f32x4 dka[KBW][DB], dva[KBW][DB];
+#pragma unroll
+  for (int kb = 0; kb < KBW; ++kb)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) { dka[kb][db] = f32x4{0.f, 0.f, 0.f, 0.f}; dva[kb][db] = dka[kb][db]; }
+
+  for (int t0 = qbeg; t0 < qend; t0 += kQT) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < kQT * HD / EPV; e += NW * 64) {
+      const int row = e / (HD / EPV), col = (e % (HD / EPV)) * EPV;
+      *reinterpret_cast<uint4*>(&qs[row * QSTR + col]) =
+          *reinterpret_cast<const uint4*>(qh + (size_t)(t0 + row) * HD + col);
+      *reinterpret_cast<uint4*>(&ds_[row * QSTR + col]) =
+          *reinterpret_cast<const uint4*>(dh + (size_t)(t0 + row) * HD + col);
+    }
+    for (int e = threadIdx.x; e < 2 * (kQT / 4) * (HD / 8); e += NW * 64) {
+      const int which = e / ((kQT / 4) * (HD / 8));
+      const int ee = e % ((kQT / 4) * (HD / 8));
+      const int kq = ee / (HD / 8), dc = (ee % (HD / 8)) * 8;
+      const T* base = which ? dh : qh;
+      const T* rows[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) rows[u] = base + (size_t)(t0 + 4 * kq + u) * HD;
+      stage_vt(rows, dc, which ? dtr : qtr, TSTR, 4 * kq);
+    }
+    for (int e = threadIdx.x; e < kQT; e += NW * 64) {
+      const long long row = rowbase + t0 + e;
+      const float g = sigmoidf(qt.gate[((size_t)b * N + t0 + e) * 3 + qt.br]);
+      l2s[e] = lse_log2(qt.lse[row]);
+      gss[e] = g;
+      dds[e] = g * qt.R[row];
+    }
+    __syncthreads();
+    constexpr int QBT = kQT / 16;
+    f32x4 s[QBT][KBW], dp[QBT][KBW];
+#pragma unroll
+    for (int qb = 0; qb < QBT; ++qb)
+#pragma unroll
+      for (int kb = 0; kb < KBW; ++kb) { s[qb][kb] = f32x4{0.f, 0.f, 0.f, 0.f}; dp[qb][kb] = s[qb][kb]; }
+#pragma unroll
+    for (int qb = 0; qb < QBT; ++qb)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        CT aq = load_chunk(&qs[(16 * qb + r) * QSTR + 32 * c + 8 * j]);
+        CT ad = load_chunk(&ds_[(16 * qb + r) * QSTR + 32 * c + 8 * j]);
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb) {
+          s[qb][kb] = mma(aq, kf[kb][c], s[qb][kb]);
+          dp[qb][kb] = mma(ad, vf[kb][c], dp[qb][kb]);
+        }
+      }
+    // lane holds queries 16qb + 4j + i for its key
+    float pg[QBT][KBW][4], dsv[QBT][KBW][4];
+#pragma unroll
+    for (int qb = 0; qb < QBT; ++qb) {
+      const float4 L = *reinterpret_cast<const float4*>(&l2s[16 * qb + 4 * j]);
+      const float4 Dd = *reinterpret_cast<const float4*>(&dds[16 * qb + 4 * j]);
+      const float4 G = *reinterpret_cast<const float4*>(&gss[16 * qb + 4 * j]);
+      const float lv[4] = {L.x, L.y, L.z, L.w}, dv4[4] = {Dd.x, Dd.y, Dd.z, Dd.w}, gv[4] = {G.x, G.y, G.z, G.w};
+#pragma unroll
+      for (int kb = 0; kb < KBW; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float p = kok[kb] ? fast_exp2(__builtin_fmaf(s[qb][kb][i], sl2, -lv[i])) : 0.f;
+          pg[qb][kb][i] = p * gv[i];
+          dsv[qb][kb][i] = p * __builtin_fmaf(dp[qb][kb][i], gv[i], -dv4[i]);
+        }
+    }
+#pragma unroll
+    for (int qp = 0; qp < QBT / 2; ++qp) {
+      CT pf[KBW], sf[KBW];
+#pragma unroll
+      for (int kb = 0; kb < KBW; ++kb) {
+        float a8[8], b8[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          a8[i] = pg[2 * qp][kb][i]; a8[4 + i] = pg[2 * qp + 1][kb][i];
+          b8[i] = dsv[2 * qp][kb][i]; b8[4 + i] = dsv[2 * qp + 1][kb][i];
+        }
+        pf[kb] = make_chunk<T>(a8);
+        sf[kb] = make_chunk<T>(b8);
+      }
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        CT ao = load_4x2(&dtr[(16 * db + r) * TSTR + 32 * qp + 4 * j]);
+        CT aq = load_4x2(&qtr[(16 * db + r) * TSTR + 32 * qp + 4 * j]);
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb) {
+          dva[kb][db] = mma(ao, pf[kb], dva[kb][db]);
+          dka[kb][db] = mma(aq, sf[kb], dka[kb][db]);
+        }
+      }
+    }
+  }
+  // lane: key wk0 + 16kb + r, dims 16db + 4j + i
+  const size_t out_base = (size_t)chunk * ((size_t)gridDim.z * nkeys_total * HD);
+#pragma unroll
+  for (int kb = 0; kb < KBW; ++kb) {
+    const int key = wk0 + 16 * kb + r;
+    if (key >= nkeys_total) continue;
+    const size_t off = out_base + ((size_t)bh * nkeys_total + key) * HD;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      store4(dk_out + off + 16 * db + 4 * j, dka[kb][db], scale);
+      store4(dv_out + off + 16 * db + 4 * j, dva[kb][db], 1.0f);
+    }
+  }
+}
+
+// ==== selection branch, query-major: dQ over the tokens of the selected blocks ====
+template <typename T, int HD>
+__global__ void __launch_bounds__(256) slc_bwd_q_kernel(const T* q, const T* k, const T* v, const T* dout,
+                                                        const uint8_t* valid_all, const int* sel, QTerms qt, int H,
+                                                        int N, int ls, int kk, int g, float sl2, float scale,
+                                                        float* dq) {
+  constexpr int NCH = HD / 32, DB = HD / 16;
+  constexpr int VSTR = 32 + 4;
+  typedef typename Chunk<T>::type CT;
+  __shared__ __attribute__((aligned(16))) T kt_all[4][HD * VSTR];
+  __shared__ int sub_all[4][kMaxSub];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r = lane & 15, j = lane >> 4;
+  const int b = blockIdx.z, h = blockIdx.y;
+  const long long bh = (long long)b * H + h;
+  const int wq0 = (blockIdx.x * 4 + wid) * 16;
+  const int G = g >= 16 ? 1 : 16 / g;
+  const int p0 = wq0 / g;
+  const int my_gi = g >= 16 ? 0 : r / g;
+  const int ngroups = N / g;
+  const T* kh = k + bh * N * HD;
+  const T* vh = v + bh * N * HD;
+  const uint8_t* val = valid_all ? valid_all + (size_t)b * N : nullptr;
+  const int* selp = sel + ((size_t)bh * ngroups + p0) * kk;
+  T* kt = kt_all[wid];
+  int* sub = sub_all[wid];
+
+  const int nsub = G * kk * (ls / 16);
+  for (int e = lane; e < nsub; e += 64) {
+    const int slot = (e * 16) / ls;
+    const int gi = slot / kk;
+    const int id = selp[gi * kk + slot % kk];
+    sub[e] = id < 0 ? -1 : ((gi << 24) | (id * ls + (e * 16) % ls));
+  }
+  const long long row = bh * N + wq0 + r;
+  CT qf[NCH], df[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    qf[c] = load_chunk(q + row * HD + 32 * c + 8 * j);
+    df[c] = load_chunk(dout + row * HD + 32 * c + 8 * j);
+  }
+  const float l2 = lse_log2(qt.lse[row]);
+  const float gs = sigmoidf(qt.gate[((size_t)b * N + wq0 + r) * 3 + qt.br]);
+  const float dd = gs * qt.R[row];
+  f32x4 acc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  __syncthreads();
+
+  for (int sb0 = 0; sb0 < nsub; sb0 += 2) {
+    const int ent[2] = {sub[sb0], sb0 + 1 < nsub ? sub[sb0 + 1] : -1};
+    CT kf[2][NCH], vf[2][NCH];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        kf[kb][c] = zero_chunk(kf[kb][c]);
+        vf[kb][c] = zero_chunk(vf[kb][c]);
+        if (ent[kb] >= 0) {
+          const size_t o = (size_t)((ent[kb] & 0xFFFFFF) + r) * HD + 32 * c + 8 * j;
+          kf[kb][c] = load_chunk(kh + o);
+          vf[kb][c] = load_chunk(vh + o);
+        }
+      }
+    bool ok[2][4];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = ent[kb];
+        ok[kb][i] = e >= 0 && (e >> 24) == my_gi && (val == nullptr || val[(e & 0xFFFFFF) + 4 * j + i]);
+      }
+    __syncthreads();
+    for (int e = lane; e < 8 * (HD / 8); e += 64) {
+      const int kq = e / (HD / 8), dc = (e % (HD / 8)) * 8;
+      const int en = ent[kq >> 2];
+      const T* rows[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) rows[u] = en >= 0 ? kh + (size_t)((en & 0xFFFFFF) + 4 * (kq & 3) + u) * HD : nullptr;
+      stage_vt(rows, dc, kt, VSTR, 4 * kq);
+    }
+    __syncthreads();
+    f32x4 s[2], dp[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dp[kb] = s[kb];
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        s[kb] = mma(kf[kb][c], qf[c], s[kb]);
+        dp[kb] = mma(vf[kb][c], df[c], dp[kb]);
+      }
+    }
+    float w8[8];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = ok[kb][i] ? fast_exp2(__builtin_fmaf(s[kb][i], sl2, -l2)) : 0.f;
+        w8[4 * kb + i] = p * __builtin_fmaf(dp[kb][i], gs, -dd);
+      }
+    const CT dsf = make_chunk<T>(w8);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) acc[db] = mma(load_4x2(&kt[(16 * db + r) * VSTR + 4 * j]), dsf, acc[db]);
+  }
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    float* dst = dq + row * HD + 16 * db + 4 * j;
+    float4 old = *reinterpret_cast<float4*>(dst);
+    f32x4 val = acc[db] * scale;
+    val[0] += old.x; val[1] += old.y; val[2] += old.z; val[3] += old.w;
+    store4(dst, val, 1.0f);
+  }
+}
+
+// ==== selection branch, key-major: dK, dV of each selection block from its groups ====
+// (b,h,block) -> sorted list of the groups that selected it: pairs[seg_start .. seg_end).
+
+// 16x16 MFMA with a 16-deep contraction: 4 values per lane group (k = 4*(L/16) + i).
+__device__ __forceinline__ f32x4 mma16(const float (&a)[4], const float (&bv)[4], f32x4 c, bf16_t) {
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  bf16x4 x = {(__bf16)a[0], (__bf16)a[1], (__bf16)a[2], (__bf16)a[3]};
+  bf16x4 y = {(__bf16)bv[0], (__bf16)bv[1], (__bf16)bv[2], (__bf16)bv[3]};
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, x), __builtin_bit_cast(s16x4, y), c, 0,
+                                                   0, 0);
+}
+__device__ __forceinline__ f32x4 mma16(const float (&a)[4], const float (&bv)[4], f32x4 c, float) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], bv[i], c, 0, 0, 0);
+  return c;
+}
+
+__global__ void slc_pairs_kernel(const int* sel, long long total, int kk, int ngroups, int nblk, uint32_t sentinel,
+                                 uint32_t* keys, uint32_t* vals) {
+  long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const long long row = i / kk;             // (bh, p)
+  const int p = (int)(row % ngroups);
+  const long long bh = row / ngroups;
+  const int id = sel[i];
+  keys[i] = id < 0 ? sentinel : (uint32_t)(bh * nblk + id);
+  vals[i] = (uint32_t)p;
+}
+
+__global__ void fill_kernel(int* x, long long n, int v) {
+  long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) x[i] = v;
+}
+
+__global__ void seg_bounds_kernel(const uint32_t* keys, long long total, uint32_t sentinel, int* seg_start,
+                                  int* seg_end) {
+  long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const uint32_t kx = keys[i];
+  if (kx == sentinel) return;
+  if (i == 0 || keys[i - 1] != kx) seg_start[kx] = (int)i;
+  if (i == total - 1 || keys[i + 1] != kx) seg_end[kx] = (int)(i + 1);
+}
+
+template <typename T, int HD, int KBW>
+__global__ void __launch_bounds__(256) slc_bwd_kv_kernel(const T* q, const T* k, const T* v, const T* dout,
+                                                         const uint8_t* valid_all, const uint32_t* groups,
+                                                         const int* seg_start, const int* seg_end, QTerms qt, int H,
+                                                         int N, int ls, int g, long long nseg, float sl2, float scale,
+                                                         float* dk, float* dv) {
+  constexpr int NCH = HD / 32, DB = HD / 16;
+  constexpr int TSTR = 16 + 4;
+  typedef typename Chunk<T>::type CT;
+  __shared__ __attribute__((aligned(16))) T qtr_all[4][HD * TSTR];
+  __shared__ __attribute__((aligned(16))) T dtr_all[4][HD * TSTR];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r = lane & 15, j = lane >> 4;
+  const long long seg = (long long)blockIdx.x * 4 + wid;
+  if (seg >= nseg) return;                  // whole wave leaves together; no block barrier below
+  const int nblk = N / ls;
+  const long long bh = seg / nblk;
+  const int blk = (int)(seg % nblk);
+  const int b = (int)(bh / H);
+  const int s0 = seg_start[seg], s1 = seg_end[seg];
+  if (s1 <= s0) return;
+  T* qtr = qtr_all[wid];
+  T* dtr = dtr_all[wid];
+  const T* qh = q + (size_t)bh * N * HD;
+  const T* dh = dout + (size_t)bh * N * HD;
+  const uint8_t* val = valid_all ? valid_all + (size_t)b * N : nullptr;
+
+  CT kf[KBW][NCH], vf[KBW][NCH];
+  bool kok[KBW];
+#pragma unroll
+  for (int kb = 0; kb < KBW; ++kb) {
+    const int key = blk * ls + 16 * kb + r;
+    kok[kb] = val == nullptr || val[key];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      kf[kb][c] = load_chunk(k + ((size_t)bh * N + key) * HD + 32 * c + 8 * j);
+      vf[kb][c] = load_chunk(v + ((size_t)bh * N + key) * HD + 32 * c + 8 * j);
+    }
+  }
+  f32x4 dka[KBW][DB], dva[KBW][DB];
+#pragma unroll
+  for (int kb = 0; kb < KBW; ++kb)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) { dka[kb][db] = f32x4{0.f, 0.f, 0.f, 0.f}; dva[kb][db] = dka[kb][db]; }
+
+  const int qblocks = g >= 16 ? g / 16 : 1;
+  const int qrows = g >= 16 ? 16 : g;       // real rows of each 16-query block
+  for (int e = s0; e < s1; ++e) {
+    const int p = (int)groups[e];
+    for (int qbk = 0; qbk < qblocks; ++qbk) {
+      const int qr0 = p * g + 16 * qbk;      // first query row of this block
+      // stage Q^T and dO^T of the 16 queries (rows beyond qrows are zero)
+      for (int it = lane; it < 4 * (HD / 8); it += 64) {
+        const int kq = it / (HD / 8), dc = (it % (HD / 8)) * 8;
+        const T* rq[4];
+        const T* rd[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int rr = 4 * kq + u;
+          rq[u] = rr < qrows ? qh + (size_t)(qr0 + rr) * HD : nullptr;
+          rd[u] = rr < qrows ? dh + (size_t)(qr0 + rr) * HD : nullptr;
+        }
+        stage_vt(rq, dc, qtr, TSTR, 4 * kq);
+        stage_vt(rd, dc, dtr, TSTR, 4 * kq);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      // A operands of S and dP: query rows (lane row = query r)
+      const bool rok = r < qrows;
+      CT aq[NCH], ad[NCH];
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        aq[c] = zero_chunk(aq[c]);
+        ad[c] = zero_chunk(ad[c]);
+        if (rok) {
+          aq[c] = load_chunk(qh + (size_t)(qr0 + r) * HD + 32 * c + 8 * j);
+          ad[c] = load_chunk(dh + (size_t)(qr0 + r) * HD + 32 * c + 8 * j);
+        }
+      }
+      // per-query terms of the rows 4j+i this lane holds
+      float lv[4], dvv[4], gv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int rr = 4 * j + i;
+        lv[i] = __builtin_huge_valf();
+        dvv[i] = 0.f;
+        gv[i] = 0.f;
+        if (rr < qrows) {
+          const long long row = bh * N + qr0 + rr;
+          lv[i] = lse_log2(qt.lse[row]);
+          gv[i] = sigmoidf(qt.gate[((size_t)b * N + qr0 + rr) * 3 + qt.br]);
+          dvv[i] = gv[i] * qt.R[row];
+        }
+      }
+#pragma unroll
+      for (int kb = 0; kb < KBW; ++kb) {
+        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f}, dp = s;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+          s = mma(aq[c], kf[kb][c], s);
+          dp = mma(ad[c], vf[kb][c], dp);
+        }
+        float pg[4], dsv[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float pr = kok[kb] ? fast_exp2(__builtin_fmaf(s[i], sl2, -lv[i])) : 0.f;
+          pg[i] = pr * gv[i];
+          dsv[i] = pr * __builtin_fmaf(dp[i], gv[i], -dvv[i]);
+        }
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const T* pd = &dtr[(16 * db + r) * TSTR + 4 * j];
+          const T* pq = &qtr[(16 * db + r) * TSTR + 4 * j];
+          float ao[4], aqv[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) { ao[i] = to_f32<T>(pd[i]); aqv[i] = to_f32<T>(pq[i]); }
+          dva[kb][db] = mma16(ao, pg, dva[kb][db], T(0));
+          dka[kb][db] = mma16(aqv, dsv, dka[kb][db], T(0));
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+  }
+#pragma unroll
+  for (int kb = 0; kb < KBW; ++kb) {
+    const size_t off = ((size_t)bh * N + blk * ls + 16 * kb + r) * HD;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      float* pk = dk + off + 16 * db + 4 * j;
+      float* pv = dv + off + 16 * db + 4 * j;
+      float4 ok4 = *reinterpret_cast<float4*>(pk), ov4 = *reinterpret_cast<float4*>(pv);
+      f32x4 a = dka[kb][db] * scale, c = dva[kb][db];
+      a[0] += ok4.x; a[1] += ok4.y; a[2] += ok4.z; a[3] += ok4.w;
+      c[0] += ov4.x; c[1] += ov4.y; c[2] += ov4.z; c[3] += ov4.w;
+      store4(pk, a, 1.0f);
+      store4(pv, c, 1.0f);
+    }
+  }
+}
+
+constexpr int kCmpChunks = 8;   // query chunks of the compressed branch's key-major pass
+
+template <typename T, int HD>
+hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
+  const long long rows = D.rows();
+  const float sl2 = D.scale * kLog2e;
+  const int nct = D.N / D.l;
+  // per-branch row sums and the gate gradient
+  hipLaunchKernelGGL(gate_bwd_rows_kernel<T>, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, st, (const T*)A.dout,
+                     (const T*)A.o_branch, rows, HD, A.R);
+  hipLaunchKernelGGL(gate_bwd_kernel, dim3((D.B * D.N + 255) / 256), dim3(256), 0, st, A.R, A.gate, A.valid, D.B, D.H,
+                     D.N, A.dgate);
+  QTerms qball{A.lse, A.R, A.gate, 0};
+  QTerms qcmp{A.lse + rows, A.R + rows, A.gate, 1};
+  QTerms qslc{A.lse + 2 * rows, A.R + 2 * rows, A.gate, 2};
+  const T* q = (const T*)A.q;
+  const T* k = (const T*)A.k;
+  const T* v = (const T*)A.v;
+  const T* dout = (const T*)A.dout;
+  // compressed tokens in the storage type, as the forward pass consumed them
+  const T* kc = (const T*)A.kc_lp;
+  const T* vc = (const T*)A.vc_lp;
+  if (D.bf16) {
+    const long long n = D.cmp_rows() * HD;
+    hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.kcmp, n, (T*)A.kc_lp);
+    hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.vcmp, n, (T*)A.vc_lp);
+  } else {
+    kc = (const T*)A.kcmp;
+    vc = (const T*)A.vcmp;
+  }
+  // ---- dQ: ball (write), compressed (add), selection (add) ----
+  if (D.m >= 128) {
+    hipLaunchKernelGGL((dense_bwd_q_kernel<T, HD, 2, true, false>), dim3(D.N / 128, D.H, D.B), dim3(256), 0, st, q, k,
+                       v, dout, A.valid, qball, D.H, D.N, D.N, D.m, sl2, D.scale, A.dq);
+  } else {
+    hipLaunchKernelGGL((dense_bwd_q_kernel<T, HD, 1, true, false>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, q, k,
+                       v, dout, A.valid, qball, D.H, D.N, D.N, D.m, sl2, D.scale, A.dq);
+  }
+  hipLaunchKernelGGL((dense_bwd_q_kernel<T, HD, 2, false, true>), dim3(D.N / 128, D.H, D.B), dim3(256), 0, st, q, kc,
+                     vc, dout, A.cvalid, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq);
+  hipLaunchKernelGGL((slc_bwd_q_kernel<T, HD>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, q, k, v, dout, A.valid,
+                     A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq);
+  // ---- dK, dV of the ball branch (written) ----
+  if (D.m >= 128) {
+    hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, 4, true>), dim3(D.N / 128, 1, D.B * D.H), dim3(256), 0, st, q, k,
+                       v, dout, A.valid, qball, D.H, D.N, D.N, D.m, 1, sl2, D.scale, A.dk, A.dv);
+  } else {
+    hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, 2, true>), dim3(D.N / 64, 1, D.B * D.H), dim3(128), 0, st, q, k, v,
+                       dout, A.valid, qball, D.H, D.N, D.N, D.m, 1, sl2, D.scale, A.dk, A.dv);
+  }
+  // ---- dK^, dV^ of the compressed branch: chunked partials, then a fixed-order sum ----
+  {
+    const int nch = D.N / kCmpChunks >= kQT ? kCmpChunks : 1;
+    hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, 4, false>), dim3((nct + 127) / 128, nch, D.B * D.H), dim3(256), 0,
+                       st, q, kc, vc, dout, A.cvalid, qcmp, D.H, D.N, nct, D.m, nch, sl2, D.scale, A.dkc_part,
+                       A.dvc_part);
+    const long long n = D.cmp_rows() * HD;
+    hipLaunchKernelGGL(sum_chunks_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.dkc_part, nch, n,
+                       A.dkc);
+    hipLaunchKernelGGL(sum_chunks_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.dvc_part, nch, n,
+                       A.dvc);
+  }
+  return hipGetLastError();
+}
+
+template <typename T, int HD>
+hipError_t slc_kv_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
+  const long long rows = D.rows();
+  const float sl2 = D.scale * kLog2e;
+  QTerms qslc{A.lse + 2 * rows, A.R + 2 * rows, A.gate, 2};
+  const long long nseg = (long long)D.B * D.H * (D.N / D.ls);
+  const int kbw = D.ls / 16;
+  const dim3 grid((unsigned)((nseg + 3) / 4));
+  const T* q = (const T*)A.q;
+  const T* k = (const T*)A.k;
+  const T* v = (const T*)A.v;
+  const T* dout = (const T*)A.dout;
+  if (kbw == 1)
+    hipLaunchKernelGGL((slc_bwd_kv_kernel<T, HD, 1>), grid, dim3(256), 0, st, q, k, v, dout, A.valid, A.pair_groups,
+                       A.seg_start, A.seg_end, qslc, D.H, D.N, D.ls, D.g, nseg, sl2, D.scale, A.dk, A.dv);
+  else if (kbw == 2)
+    hipLaunchKernelGGL((slc_bwd_kv_kernel<T, HD, 2>), grid, dim3(256), 0, st, q, k, v, dout, A.valid, A.pair_groups,
+                       A.seg_start, A.seg_end, qslc, D.H, D.N, D.ls, D.g, nseg, sl2, D.scale, A.dk, A.dv);
+  else
+    hipLaunchKernelGGL((slc_bwd_kv_kernel<T, HD, 4>), grid, dim3(256), 0, st, q, k, v, dout, A.valid, A.pair_groups,
+                       A.seg_start, A.seg_end, qslc, D.H, D.N, D.ls, D.g, nseg, sl2, D.scale, A.dk, A.dv);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attn_bwd(const Dims& D, const BwdArgs& A, hipStream_t st) {
+  return BSA_DISPATCH(bwd_impl, D, A, st);
+}
+
+hipError_t launch_slc_csr(const Dims& D, const BwdArgs& A, hipStream_t st) {
+  const long long total = (long long)D.B * D.H * (D.N / D.g) * D.k;
+  const int nblk = D.N / D.ls;
+  const long long nseg = (long long)D.B * D.H * nblk;
+  const uint32_t sentinel = (uint32_t)nseg;
+  int bits = 1;
+  while ((1ll << bits) <= (long long)sentinel) ++bits;
+  hipLaunchKernelGGL(slc_pairs_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, A.sel, total, D.k,
+                     D.N / D.g, nblk, sentinel, A.pair_keys, A.pair_vals);
+  hipLaunchKernelGGL(fill_kernel, dim3((unsigned)((nseg + 255) / 256)), dim3(256), 0, st, A.seg_start, nseg, 0);
+  hipLaunchKernelGGL(fill_kernel, dim3((unsigned)((nseg + 255) / 256)), dim3(256), 0, st, A.seg_end, nseg, 0);
+  uint32_t* kout = nullptr;
+  uint32_t* vout = nullptr;
+  hipError_t e = launch_radix_sort_pairs(A.pair_keys, A.pair_vals, A.pair_keys_tmp, A.pair_vals_tmp, A.sort_hist,
+                                         total, bits, &kout, &vout, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(seg_bounds_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, kout, total, sentinel,
+                     A.seg_start, A.seg_end);
+  BwdArgs A2 = A;
+  A2.pair_groups = vout;
+  return BSA_DISPATCH(slc_kv_impl, D, A2, st);
+}
+
+}  // namespace bsa

@@ -1,0 +1,197 @@
+// Building blocks shared by the forward and backward attention kernels: packed
+// LDS/global moves, V^T-style transposed staging, and the wave-level online-softmax
+// step of the forward pass (see attn_fwd.hip for the formulation).
+#pragma once
+#include "common.hpp"
+
+namespace bsa {
+namespace {
+
+constexpr int kKT = 64;       // keys per LDS tile of the dense kernels
+constexpr int kMaxSub = 256;  // 16-key sub-blocks per selection wave (G * k* * l' / 16)
+constexpr float kNegInf = -__builtin_huge_valf();
+
+// Two runs of 4 consecutive elements (at p and p + 16) as one 8-element chunk.
+__device__ __forceinline__ bf16x8 load_4x2(const bf16_t* p) {
+  uint2 a = *reinterpret_cast<const uint2*>(p);
+  uint2 b = *reinterpret_cast<const uint2*>(p + 16);
+  return __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
+}
+__device__ __forceinline__ f32x8 load_4x2(const float* p) {
+  float4 a = *reinterpret_cast<const float4*>(p);
+  float4 b = *reinterpret_cast<const float4*>(p + 16);
+  return f32x8{a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+}
+__device__ __forceinline__ void store4(bf16_t* dst, f32x4 v, float sc) {
+  uint32_t lo = (uint32_t)f2bf(v[0] * sc) | ((uint32_t)f2bf(v[1] * sc) << 16);
+  uint32_t hi = (uint32_t)f2bf(v[2] * sc) | ((uint32_t)f2bf(v[3] * sc) << 16);
+  *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
+}
+__device__ __forceinline__ void store4(float* dst, f32x4 v, float sc) {
+  *reinterpret_cast<float4*>(dst) = make_float4(v[0] * sc, v[1] * sc, v[2] * sc, v[3] * sc);
+}
+// Stage 4 rows x 8 columns of V (row pointers may be null = zero rows) into V^T: one
+// 16-byte (bf16) or two 16-byte (f32) loads per row, then 8 packed 4-key column writes.
+__device__ __forceinline__ void stage_vt(const bf16_t* const (&rows)[4], int dc, bf16_t* vt, int vstr, int key_off) {
+  uint32_t w[4][4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    uint4 t = rows[u] ? *reinterpret_cast<const uint4*>(rows[u] + dc) : make_uint4(0, 0, 0, 0);
+    w[u][0] = t.x; w[u][1] = t.y; w[u][2] = t.z; w[u][3] = t.w;
+  }
+#pragma unroll
+  for (int x = 0; x < 8; ++x) {
+    const int wd = x >> 1;
+    uint32_t lo, hi;
+    if (x & 1) {
+      lo = (w[0][wd] >> 16) | (w[1][wd] & 0xFFFF0000u);
+      hi = (w[2][wd] >> 16) | (w[3][wd] & 0xFFFF0000u);
+    } else {
+      lo = (w[0][wd] & 0xFFFFu) | (w[1][wd] << 16);
+      hi = (w[2][wd] & 0xFFFFu) | (w[3][wd] << 16);
+    }
+    *reinterpret_cast<uint2*>(vt + (dc + x) * vstr + key_off) = make_uint2(lo, hi);
+  }
+}
+__device__ __forceinline__ void stage_vt(const float* const (&rows)[4], int dc, float* vt, int vstr, int key_off) {
+  float w[4][8];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+    if (rows[u]) {
+      a = *reinterpret_cast<const float4*>(rows[u] + dc);
+      b = *reinterpret_cast<const float4*>(rows[u] + dc + 4);
+    }
+    w[u][0] = a.x; w[u][1] = a.y; w[u][2] = a.z; w[u][3] = a.w;
+    w[u][4] = b.x; w[u][5] = b.y; w[u][6] = b.z; w[u][7] = b.w;
+  }
+#pragma unroll
+  for (int x = 0; x < 8; ++x)
+    *reinterpret_cast<float4*>(vt + (dc + x) * vstr + key_off) = make_float4(w[0][x], w[1][x], w[2][x], w[3][x]);
+}
+
+// Same as stage_vt for an explicit base pointer per row (columns [dc, dc+8)).
+template <typename T>
+__device__ __forceinline__ void stage_t(const T* const (&rows)[4], int dc, T* dst, int stride, int off) {
+  stage_vt(rows, dc, dst, stride, off);
+}
+
+// Online-softmax state of one wave over QB blocks of 16 queries.
+template <typename T, int HD, int QB>
+struct WaveAttn {
+  static constexpr int NCH = HD / 32;  // chunks of the head dim
+  static constexpr int DB = HD / 16;   // 16-wide dim blocks of O^T
+  typedef typename Chunk<T>::type CT;
+  CT qf[QB][NCH];
+  float mx[QB];      // running max (log2 domain, scaled)
+  float lsum[QB];    // this lane's partial row sum
+  f32x4 o[QB][DB];
+
+  __device__ void init() {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      mx[qb] = kNegInf;
+      lsum[qb] = 0.f;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) o[qb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+
+  // Process one tile of KB 16-key blocks (KB even). kfrag(kb, c) gives the A chunk of
+  // key block kb, vfrag(db, kp) the A chunk of V^T for dim block db and key pair kp,
+  // keyok(kb, i, qb) whether key 4j+i of block kb may be seen by this lane's query.
+  template <int KB, typename KF, typename VF, typename OK>
+  __device__ __forceinline__ void tile(float sl2, KF kfrag, VF vfrag, OK keyok) {
+    f32x4 s[QB][KB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) s[qb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        CT a = kfrag(kb, c);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) s[qb][kb] = mma(a, qf[qb][c], s[qb][kb]);
+      }
+    CT pf[QB][KB / 2];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float tmax = kNegInf;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float x = keyok(kb, i, qb) ? s[qb][kb][i] : kNegInf;
+          s[qb][kb][i] = x;
+          tmax = fmaxf(tmax, x);
+        }
+      tmax = col_max(tmax) * sl2;          // scale > 0 keeps the order
+      const float mnew = fmaxf(mx[qb], tmax);
+      const float mref = mnew == kNegInf ? 0.f : mnew;
+      const float alpha = fast_exp2(mx[qb] - mref);
+      mx[qb] = mnew;
+      float ps = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float p = fast_exp2(__builtin_fmaf(s[qb][kb][i], sl2, -mref));
+          s[qb][kb][i] = p;
+          ps += p;
+        }
+      lsum[qb] = lsum[qb] * alpha + ps;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) o[qb][db] *= alpha;
+#pragma unroll
+      for (int kp = 0; kp < KB / 2; ++kp) {
+        float v8[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          v8[i] = s[qb][2 * kp][i];
+          v8[4 + i] = s[qb][2 * kp + 1][i];
+        }
+        pf[qb][kp] = make_chunk<T>(v8);
+      }
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int kp = 0; kp < KB / 2; ++kp) {
+        CT a = vfrag(db, kp);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) o[qb][db] = mma(a, pf[qb][kp], o[qb][db]);
+      }
+  }
+
+  // Normalise and store O rows (query q0 + 16 qb + r) and natural-log LSE.
+  __device__ void finish(int lane, long long row0, T* out, float* lse, const uint8_t* qvalid, int qidx0) {
+    const int r = lane & 15, j = lane >> 4;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const float l = col_sum(lsum[qb]);
+      const bool qok = qvalid == nullptr || qvalid[qidx0 + 16 * qb + r];
+      const bool any = qok && l > 0.f;
+      const float inv = any ? 1.0f / l : 0.f;
+      const long long row = row0 + 16 * qb + r;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) store4(out + row * HD + 16 * db + 4 * j, o[qb][db], inv);
+      if (j == 0) lse[row] = any ? (mx[qb] + log2f(l)) * kLn2 : kNegInf;
+    }
+  }
+};
+
+template <typename T, int HD, int QB>
+__device__ __forceinline__ void load_q(WaveAttn<T, HD, QB>& w, const T* qrow0, int lane) {
+  const int r = lane & 15, j = lane >> 4;
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int c = 0; c < WaveAttn<T, HD, QB>::NCH; ++c)
+      w.qf[qb][c] = load_chunk(qrow0 + (size_t)(16 * qb + r) * HD + 32 * c + 8 * j);
+}
+
+
+}  // namespace
+}  // namespace bsa

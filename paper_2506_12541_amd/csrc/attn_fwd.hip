@@ -14,169 +14,12 @@
 // as V^T, which the kernels stage through LDS (transposing while storing).
 #include "common.hpp"
 #include "kernels.hpp"
+#include "attn_common.hpp"
 
 namespace bsa {
 namespace {
 
-constexpr float kNegInf = -__builtin_huge_valf();
-
-// Two runs of 4 consecutive elements (at p and p + 16) as one 8-element chunk.
-__device__ __forceinline__ bf16x8 load_4x2(const bf16_t* p) {
-  uint2 a = *reinterpret_cast<const uint2*>(p);
-  uint2 b = *reinterpret_cast<const uint2*>(p + 16);
-  return __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
-}
-__device__ __forceinline__ f32x8 load_4x2(const float* p) {
-  float4 a = *reinterpret_cast<const float4*>(p);
-  float4 b = *reinterpret_cast<const float4*>(p + 16);
-  return f32x8{a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-}
-__device__ __forceinline__ void store4(bf16_t* dst, f32x4 v, float sc) {
-  uint32_t lo = (uint32_t)f2bf(v[0] * sc) | ((uint32_t)f2bf(v[1] * sc) << 16);
-  uint32_t hi = (uint32_t)f2bf(v[2] * sc) | ((uint32_t)f2bf(v[3] * sc) << 16);
-  *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
-}
-__device__ __forceinline__ void store4(float* dst, f32x4 v, float sc) {
-  *reinterpret_cast<float4*>(dst) = make_float4(v[0] * sc, v[1] * sc, v[2] * sc, v[3] * sc);
-}
-// Write 4 consecutive keys of one dim of V^T (values of 4 rows, same column).
-__device__ __forceinline__ void store_col4(bf16_t* dst, bf16_t a, bf16_t b, bf16_t c, bf16_t d) {
-  *reinterpret_cast<uint2*>(dst) = make_uint2((uint32_t)a | ((uint32_t)b << 16), (uint32_t)c | ((uint32_t)d << 16));
-}
-__device__ __forceinline__ void store_col4(float* dst, float a, float b, float c, float d) {
-  *reinterpret_cast<float4*>(dst) = make_float4(a, b, c, d);
-}
-// Stage 4 rows x 8 columns of V (row pointers may be null = zero rows) into V^T.
-template <typename T>
-__device__ __forceinline__ void stage_vt(const T* const (&rows)[4], int dc, T* vt, int vstr, int key_off) {
-  T vals[4][8];
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int x = 0; x < 8; ++x) vals[u][x] = rows[u] ? rows[u][dc + x] : T(0);
-#pragma unroll
-  for (int x = 0; x < 8; ++x)
-    store_col4(vt + (dc + x) * vstr + key_off, vals[0][x], vals[1][x], vals[2][x], vals[3][x]);
-}
-
-// Online-softmax state of one wave over QB blocks of 16 queries.
-template <typename T, int HD, int QB>
-struct WaveAttn {
-  static constexpr int NCH = HD / 32;  // chunks of the head dim
-  static constexpr int DB = HD / 16;   // 16-wide dim blocks of O^T
-  typedef typename Chunk<T>::type CT;
-  CT qf[QB][NCH];
-  float mx[QB];      // running max (log2 domain, scaled)
-  float lsum[QB];    // this lane's partial row sum
-  f32x4 o[QB][DB];
-
-  __device__ void init() {
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      mx[qb] = kNegInf;
-      lsum[qb] = 0.f;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) o[qb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-  }
-
-  // Process one tile of KB 16-key blocks (KB even). kfrag(kb, c) gives the A chunk of
-  // key block kb, vfrag(db, kp) the A chunk of V^T for dim block db and key pair kp,
-  // keyok(kb, i, qb) whether key 4j+i of block kb may be seen by this lane's query.
-  template <int KB, typename KF, typename VF, typename OK>
-  __device__ __forceinline__ void tile(float sl2, KF kfrag, VF vfrag, OK keyok) {
-    f32x4 s[QB][KB];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) s[qb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        CT a = kfrag(kb, c);
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) s[qb][kb] = mma(a, qf[qb][c], s[qb][kb]);
-      }
-    CT pf[QB][KB / 2];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      float tmax = kNegInf;
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float x = keyok(kb, i, qb) ? s[qb][kb][i] * sl2 : kNegInf;
-          s[qb][kb][i] = x;
-          tmax = fmaxf(tmax, x);
-        }
-      tmax = col_max(tmax);
-      const float mnew = fmaxf(mx[qb], tmax);
-      const float mref = mnew == kNegInf ? 0.f : mnew;
-      const float alpha = fast_exp2(mx[qb] - mref);
-      mx[qb] = mnew;
-      float ps = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float p = fast_exp2(s[qb][kb][i] - mref);
-          s[qb][kb][i] = p;
-          ps += p;
-        }
-      lsum[qb] = lsum[qb] * alpha + ps;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) o[qb][db] *= alpha;
-#pragma unroll
-      for (int kp = 0; kp < KB / 2; ++kp) {
-        float v8[8];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          v8[i] = s[qb][2 * kp][i];
-          v8[4 + i] = s[qb][2 * kp + 1][i];
-        }
-        pf[qb][kp] = make_chunk<T>(v8);
-      }
-    }
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int kp = 0; kp < KB / 2; ++kp) {
-        CT a = vfrag(db, kp);
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) o[qb][db] = mma(a, pf[qb][kp], o[qb][db]);
-      }
-  }
-
-  // Normalise and store O rows (query q0 + 16 qb + r) and natural-log LSE.
-  __device__ void finish(int lane, long long row0, T* out, float* lse, const uint8_t* qvalid, int qidx0) {
-    const int r = lane & 15, j = lane >> 4;
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      const float l = col_sum(lsum[qb]);
-      const bool qok = qvalid == nullptr || qvalid[qidx0 + 16 * qb + r];
-      const bool any = qok && l > 0.f;
-      const float inv = any ? 1.0f / l : 0.f;
-      const long long row = row0 + 16 * qb + r;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) store4(out + row * HD + 16 * db + 4 * j, o[qb][db], inv);
-      if (j == 0) lse[row] = any ? (mx[qb] + log2f(l)) * kLn2 : kNegInf;
-    }
-  }
-};
-
-template <typename T, int HD, int QB>
-__device__ __forceinline__ void load_q(WaveAttn<T, HD, QB>& w, const T* qrow0, int lane) {
-  const int r = lane & 15, j = lane >> 4;
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-    for (int c = 0; c < WaveAttn<T, HD, QB>::NCH; ++c)
-      w.qf[qb][c] = load_chunk(qrow0 + (size_t)(16 * qb + r) * HD + 32 * c + 8 * j);
-}
-
 // ---- dense kernel: ball branch (keys = own ball) and compressed branch (all tokens) ----
-constexpr int kKT = 64;  // keys per LDS tile
 
 template <typename T, int HD, int QB, bool BALL>
 __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, const T* v, const uint8_t* qvalid_all,
@@ -221,7 +64,7 @@ __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, 
         const int key = t0 + 4 * kq + u;
         rows[u] = key < nkeys ? vh + (size_t)key * HD : nullptr;
       }
-      stage_vt<T>(rows, dc, vt, VSTR, 4 * kq);
+      stage_vt(rows, dc, vt, VSTR, 4 * kq);
     }
     if (threadIdx.x < kKT) {
       const int key = t0 + threadIdx.x;
@@ -230,8 +73,12 @@ __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, 
     __syncthreads();
     auto kfrag = [&](int kb, int c) { return load_chunk(&ks[(kb * 16 + r) * KSTR + 32 * c + 8 * j]); };
     auto vfrag = [&](int db, int kp) { return load_4x2(&vt[(16 * db + r) * VSTR + 32 * kp + 4 * j]); };
-    auto keyok = [&](int kb, int i, int) { return kok[kb * 16 + 4 * j + i] != 0; };
-    w.template tile<kKT / 16>(sl2, kfrag, vfrag, keyok);
+    if (kval == nullptr && t0 + kKT <= nkeys) {
+      w.template tile<kKT / 16>(sl2, kfrag, vfrag, [](int, int, int) { return true; });
+    } else {
+      auto keyok = [&](int kb, int i, int) { return kok[kb * 16 + 4 * j + i] != 0; };
+      w.template tile<kKT / 16>(sl2, kfrag, vfrag, keyok);
+    }
   }
   w.finish(lane, bh * N + wq0, out, lse, qval, wq0);
 }
@@ -241,7 +88,6 @@ __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, 
 // 16 queries belong to (one group when g >= 16); a lane only accepts keys of its own
 // group's blocks. Keys are walked in tiles of 32 (two 16-key sub-blocks, each inside one
 // selected block since l' is a multiple of 16).
-constexpr int kMaxSub = 256;  // 16-key sub-blocks per wave (G * k* * l' / 16)
 
 template <typename T, int HD>
 __global__ void __launch_bounds__(256) slc_fwd_kernel(const T* q, const T* k, const T* v, const uint8_t* valid_all,
@@ -310,7 +156,7 @@ __global__ void __launch_bounds__(256) slc_fwd_kernel(const T* q, const T* k, co
       const T* rows[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) rows[u] = en >= 0 ? vh + (size_t)((en & 0xFFFFFF) + 4 * (kq & 3) + u) * HD : nullptr;
-      stage_vt<T>(rows, dc, vt, VSTR, 4 * kq);
+      stage_vt(rows, dc, vt, VSTR, 4 * kq);
     }
     __syncthreads();
     auto kfrag = [&](int kb, int c) { return kf[kb][c]; };
@@ -378,10 +224,6 @@ hipError_t slc_impl(const Dims& D, const void* q, const void* k, const void* v, 
 }
 
 }  // namespace
-
-#define BSA_DISPATCH(FN, ...)                                                              \
-  (D.bf16 ? (D.d == 64 ? FN<bf16_t, 64>(__VA_ARGS__) : FN<bf16_t, 32>(__VA_ARGS__))       \
-          : (D.d == 64 ? FN<float, 64>(__VA_ARGS__) : FN<float, 32>(__VA_ARGS__)))
 
 hipError_t launch_ball_fwd(const Dims& D, const void* q, const void* k, const void* v, const uint8_t* valid, void* o,
                            float* lse, hipStream_t st) {

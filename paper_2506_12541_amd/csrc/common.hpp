@@ -25,12 +25,8 @@ constexpr float kLn2 = 0.6931471805599453f;
 
 __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
-// Round to nearest even; inputs are finite in this library.
-__device__ __forceinline__ bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
+// Round to nearest even (hardware v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
 // Storage traits: element type in memory, and its 8-wide chunk register type.
 template <typename T> struct Chunk;
@@ -64,7 +60,7 @@ template <typename T> __device__ __forceinline__ typename Chunk<T>::type make_ch
 template <> __device__ __forceinline__ bf16x8 make_chunk<bf16_t>(const float* v) {
   bf16x8 r;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) r[i] = __builtin_bit_cast(__bf16, f2bf(v[i]));
+  for (int i = 0; i < 8; ++i) r[i] = (__bf16)v[i];
   return r;
 }
 template <> __device__ __forceinline__ f32x8 make_chunk<float>(const float* v) {

@@ -8,6 +8,7 @@
 // so that the compressed keys feed the top-k scoring at f32 accuracy.
 #include "common.hpp"
 #include "kernels.hpp"
+#include "attn_common.hpp"
 
 namespace bsa {
 namespace {
@@ -165,6 +166,259 @@ __global__ void mean_pool_kernel(const T* x, const uint8_t* valid, int H, int N,
   out_lp[i] = from_f32<T>(s);
 }
 
+// ---------------------------------------------------------------------------------
+// Backward of phi. With y = h W2 + b2, h = GELU(pre), pre = x W1 + b1 (per row = block):
+//   dh = dy W2^T, dpre = dh * GELU'(pre), dx = dpre W1^T,
+//   dW2 = h^T dy, db2 = sum dy, dW1 = x^T dpre, db1 = sum dpre   (sums over all rows).
+// Rows are split into fixed chunks whose weight-gradient partials are summed in order.
+// ---------------------------------------------------------------------------------
+__device__ __forceinline__ float gelu_erf_grad(float x) {
+  return 0.5f * (1.0f + erff(x * 0.70710678118654752f)) + x * 0.3989422804014327f * __expf(-0.5f * x * x);
+}
+
+// One wave per 16 rows: dpre (stored), and dx = dpre W1^T added into the token gradients.
+template <int HD>
+__global__ void __launch_bounds__(256) mlp_bwd_rows_kernel(const float* dy, const float* pre, const uint8_t* valid,
+                                                           int H, int N, int l, long long rows, const float* w1,
+                                                           const float* w2, float* dpre_out, float* dx_accum) {
+  constexpr int NCH = HD / 32, OB = HD / 16;
+  __shared__ float w2s[HD * (HD + 4)];
+  __shared__ __attribute__((aligned(16))) float dps_all[4][16 * (HD + 4)];
+  for (int i = threadIdx.x; i < HD * HD; i += blockDim.x) w2s[(i / HD) * (HD + 4) + i % HD] = w2[i];
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r = lane & 15, j = lane >> 4;
+  const long long row0 = ((long long)blockIdx.x * 4 + wid) * 16;
+  const long long row = row0 + r;
+  const bool rok = row < rows;
+  float* dps = dps_all[wid];
+  // dh^T[o][row] = sum_o2 W2[o][o2] dy[row][o2]; A = W2 rows (o), B = dy^T
+  f32x8 by[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) by[c] = rok ? load_chunk(dy + row * HD + 32 * c + 8 * j) : f32x8{};
+#pragma unroll
+  for (int ob = 0; ob < OB; ++ob) {
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      f32x8 a;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) a[e] = w2s[(16 * ob + r) * (HD + 4) + 32 * c + 8 * j + e];
+      acc = mma(a, by[c], acc);
+    }
+    // lane: row r, hidden units o = 16 ob + 4 j + i
+    float4 pv = rok ? *reinterpret_cast<const float4*>(pre + row * HD + 16 * ob + 4 * j) : make_float4(0, 0, 0, 0);
+    const float pa[4] = {pv.x, pv.y, pv.z, pv.w};
+    float d4[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) d4[i] = acc[i] * gelu_erf_grad(pa[i]);
+    *reinterpret_cast<float4*>(&dps[r * (HD + 4) + 16 * ob + 4 * j]) = make_float4(d4[0], d4[1], d4[2], d4[3]);
+    if (rok) *reinterpret_cast<float4*>(dpre_out + row * HD + 16 * ob + 4 * j) = make_float4(d4[0], d4[1], d4[2], d4[3]);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  // dx^T[i][row] = sum_o W1[i][o] dpre[row][o]; A = W1 rows (i), B = dpre^T
+  f32x8 bd[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) bd[c] = *reinterpret_cast<const f32x8*>(&dps[r * (HD + 4) + 32 * c + 8 * j]);
+  const int ld = l * HD;
+  const int nblk = N / l;
+  long long bhh = rok ? row / nblk : 0;
+  const int blk = rok ? (int)(row % nblk) : 0;
+  const int b = (int)(bhh / H);
+  for (int ib = 0; ib < ld / 16; ++ib) {
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) acc = mma(load_chunk(w1 + (size_t)(16 * ib + r) * HD + 32 * c + 8 * j), bd[c], acc);
+    // lane: row r, flat indices i = 16 ib + 4 j + t (one token, 4 consecutive channels)
+    const int i0 = 16 * ib + 4 * j;
+    const int tok = i0 / HD, ch = i0 % HD;
+    if (rok && (valid == nullptr || valid[(size_t)b * N + (size_t)blk * l + tok])) {
+      float* dst = dx_accum + (row * l + tok) * HD + ch;
+      float4 o = *reinterpret_cast<float4*>(dst);
+      o.x += acc[0]; o.y += acc[1]; o.z += acc[2]; o.w += acc[3];
+      *reinterpret_cast<float4*>(dst) = o;
+    }
+  }
+}
+
+// dW1 partials: workgroup = (64 flattened inputs i, row chunk); wave w owns i in [16w, 16w+16).
+template <typename T, int HD>
+__global__ void __launch_bounds__(256) mlp_bwd_w1_kernel(const T* x, const uint8_t* valid, const float* dpre, int H,
+                                                         int N, int l, long long rows, long long rows_per_chunk,
+                                                         float* part) {
+  constexpr int TSTR = 32 + 4;
+  constexpr int OB = HD / 16;
+  typedef typename Chunk<T>::type CT;
+  __shared__ __attribute__((aligned(16))) T xt[64 * TSTR];
+  __shared__ __attribute__((aligned(16))) T dt[HD * TSTR];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r = lane & 15, j = lane >> 4;
+  const int ld = l * HD;
+  const int i0 = blockIdx.x * 64;
+  const int chunk = blockIdx.y;
+  const long long rbeg = chunk * rows_per_chunk;
+  const long long rend = rbeg + rows_per_chunk < rows ? rbeg + rows_per_chunk : rows;
+  const int nblk = N / l;
+  f32x4 acc[OB];
+#pragma unroll
+  for (int ob = 0; ob < OB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (long long r0 = rbeg; r0 < rend; r0 += 32) {
+    __syncthreads();
+    // x^T tile [64 i][32 rows]: items of 4 rows x 8 columns
+    for (int e = threadIdx.x; e < 8 * 8; e += 256) {
+      const int kq = e / 8, dc = (e % 8) * 8;
+      const int tok = (i0 + dc) / HD;
+      const T* rp[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const long long row = r0 + 4 * kq + u;
+        bool ok = row < rend;
+        if (ok && valid) {
+          const long long bhh = row / nblk;
+          const int blk = (int)(row % nblk);
+          ok = valid[(size_t)(bhh / H) * N + (size_t)blk * l + tok] != 0;
+        }
+        rp[u] = ok ? x + row * ld + i0 : nullptr;
+      }
+      stage_t(rp, dc, xt, TSTR, 4 * kq);
+    }
+    // dpre^T tile [HD][32 rows]
+    for (int e = threadIdx.x; e < 8 * (HD / 8); e += 256) {
+      const int kq = e / (HD / 8), dc = (e % (HD / 8)) * 8;
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) {
+        float v4[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const long long row = r0 + 4 * kq + u;
+          v4[u] = row < rend ? dpre[row * HD + dc + cc] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) dt[(dc + cc) * TSTR + 4 * kq + u] = from_f32<T>(v4[u]);
+      }
+    }
+    __syncthreads();
+    // D[i][o] += sum_rows xt[i][row] dt[o][row]; contraction over 32 rows = one chunk
+    CT a = load_4x2(&xt[(16 * wid + r) * TSTR + 4 * j]);
+#pragma unroll
+    for (int ob = 0; ob < OB; ++ob) acc[ob] = mma(a, load_4x2(&dt[(16 * ob + r) * TSTR + 4 * j]), acc[ob]);
+  }
+  // lane: o = 16 ob + r (column), i = i0 + 16 wid + 4 j + t (rows)
+  float* out = part + (size_t)chunk * ld * HD;
+#pragma unroll
+  for (int ob = 0; ob < OB; ++ob)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) out[(size_t)(i0 + 16 * wid + 4 * j + t) * HD + 16 * ob + r] = acc[ob][t];
+}
+
+// dW2, db1, db2 partials over a row chunk: thread (o2, o-slice).
+template <int HD>
+__global__ void __launch_bounds__(256) mlp_bwd_small_kernel(const float* dy, const float* pre, const float* dpre,
+                                                            long long rows, long long rows_per_chunk, float* part) {
+  __shared__ float hs[32][HD];
+  __shared__ float ys[32][HD];
+  __shared__ float ps[32][HD];
+  const int chunk = blockIdx.x;
+  const long long rbeg = chunk * rows_per_chunk;
+  const long long rend = rbeg + rows_per_chunk < rows ? rbeg + rows_per_chunk : rows;
+  constexpr int PER = HD * HD / 256;  // dW2 entries per thread
+  const int o2 = threadIdx.x % HD;
+  const int ob = (threadIdx.x / HD) * PER;
+  float acc[PER];
+#pragma unroll
+  for (int t = 0; t < PER; ++t) acc[t] = 0.f;
+  float sb1 = 0.f, sb2 = 0.f;
+  for (long long r0 = rbeg; r0 < rend; r0 += 32) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < 32 * HD; e += 256) {
+      const int rr = e / HD, c = e % HD;
+      const long long row = r0 + rr;
+      float pv = 0.f, yv = 0.f, dv = 0.f;
+      if (row < rend) {
+        pv = pre[row * HD + c];
+        yv = dy[row * HD + c];
+        dv = dpre[row * HD + c];
+      }
+      hs[rr][c] = row < rend ? gelu_erf(pv) : 0.f;
+      ys[rr][c] = yv;
+      ps[rr][c] = dv;
+    }
+    __syncthreads();
+    for (int rr = 0; rr < 32; ++rr) {
+      const float y = ys[rr][o2];
+#pragma unroll
+      for (int t = 0; t < PER; ++t) acc[t] += hs[rr][ob + t] * y;
+      if (threadIdx.x < HD) { sb1 += ps[rr][o2]; sb2 += y; }
+    }
+  }
+  float* out = part + (size_t)chunk * (HD * HD + 2 * HD);
+#pragma unroll
+  for (int t = 0; t < PER; ++t) out[(ob + t) * HD + o2] = acc[t];
+  if (threadIdx.x < HD) {
+    out[HD * HD + o2] = sb1;
+    out[HD * HD + HD + o2] = sb2;
+  }
+}
+
+__global__ void sum_parts_kernel(const float* part, int chunks, long long n, long long stride, float* out) {
+  long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  for (int c = 0; c < chunks; ++c) s += part[(long long)c * stride + i];
+  out[i] = s;
+}
+
+// Mean pooling backward: every real token of a block receives dy / l.
+__global__ void mean_pool_bwd_kernel(const float* dy, const uint8_t* valid, int H, int N, int l, int hd, long long rows,
+                                     float* dx_accum) {
+  long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows * l * hd) return;
+  const int c = (int)(i % hd);
+  const long long tokrow = i / hd;          // (b*H + h) * N + n
+  const long long row = tokrow / l;         // block row
+  const int t = (int)(tokrow % l);
+  const int nblk = N / l;
+  const long long bhh = row / nblk;
+  const int blk = (int)(row % nblk);
+  const int b = (int)(bhh / H);
+  if (valid && !valid[(size_t)b * N + (size_t)blk * l + t]) return;
+  dx_accum[i] += dy[row * hd + c] / (float)l;
+}
+
+template <typename T, int HD>
+hipError_t compress_bwd_impl(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi, const float* pre,
+                             const float* dy, float* dx_accum, const MlpGrad& grad, const MlpBwdWs& ws,
+                             hipStream_t st) {
+  const long long rows = D.cmp_rows();
+  if (D.pool == 1) {
+    const long long tot = rows * D.l * HD;
+    hipLaunchKernelGGL(mean_pool_bwd_kernel, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, st, dy, valid, D.H, D.N,
+                       D.l, HD, rows, dx_accum);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL((mlp_bwd_rows_kernel<HD>), dim3((unsigned)((rows + 63) / 64)), dim3(256), 0, st, dy, pre, valid,
+                     D.H, D.N, D.l, rows, phi.w1, phi.w2, ws.dpre, dx_accum);
+  const int ld = D.l * HD;
+  const long long rpc = ((rows + ws.chunks - 1) / ws.chunks + 31) / 32 * 32;
+  hipLaunchKernelGGL((mlp_bwd_w1_kernel<T, HD>), dim3(ld / 64, ws.chunks), dim3(256), 0, st, (const T*)x, valid, ws.dpre,
+                     D.H, D.N, D.l, rows, rpc, ws.part_w1);
+  hipLaunchKernelGGL((mlp_bwd_small_kernel<HD>), dim3(ws.chunks), dim3(256), 0, st, dy, pre, ws.dpre, rows, rpc,
+                     ws.part_small);
+  const long long n1 = (long long)ld * HD;
+  hipLaunchKernelGGL(sum_parts_kernel, dim3((unsigned)((n1 + 255) / 256)), dim3(256), 0, st, ws.part_w1, ws.chunks, n1,
+                     n1, grad.w1);
+  const long long ss = (long long)HD * HD + 2 * HD;
+  hipLaunchKernelGGL(sum_parts_kernel, dim3((HD * HD + 255) / 256), dim3(256), 0, st, ws.part_small, ws.chunks,
+                     (long long)HD * HD, ss, grad.w2);
+  hipLaunchKernelGGL(sum_parts_kernel, dim3(1), dim3(256), 0, st, ws.part_small + HD * HD, ws.chunks, (long long)HD, ss,
+                     grad.b1);
+  hipLaunchKernelGGL(sum_parts_kernel, dim3(1), dim3(256), 0, st, ws.part_small + HD * HD + HD, ws.chunks,
+                     (long long)HD, ss, grad.b2);
+  return hipGetLastError();
+}
+
 template <typename T, int HD>
 hipError_t compress_impl(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi, float* out,
                          float* pre, void* out_lp, void* w1t_ws, hipStream_t st) {
@@ -191,6 +445,20 @@ hipError_t launch_block_valid(const Dims& D, const uint8_t* valid, uint8_t* cval
   const int total = D.B * (D.N / D.l);
   hipLaunchKernelGGL(block_valid_kernel, dim3((total + 255) / 256), dim3(256), 0, st, valid, total, D.l, cvalid);
   return hipGetLastError();
+}
+
+int mlp_bwd_chunks(const Dims& D) {
+  const long long rows = D.cmp_rows();
+  long long c = rows / 512;
+  if (c < 1) c = 1;
+  if (c > 64) c = 64;
+  return (int)c;
+}
+
+hipError_t launch_compress_bwd(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi, const float* pre,
+                               const float* dy, float* dx_accum, const MlpGrad& grad, const MlpBwdWs& ws,
+                               hipStream_t st) {
+  return BSA_DISPATCH(compress_bwd_impl, D, x, valid, phi, pre, dy, dx_accum, grad, ws, st);
 }
 
 hipError_t launch_compress_fwd(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi, float* out,

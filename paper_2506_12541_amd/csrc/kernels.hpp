@@ -52,4 +52,50 @@ hipError_t launch_slc_fwd(const Dims& D, const void* q, const void* k, const voi
 hipError_t launch_gate_fwd(const Dims& D, const void* ob, const float* gate, const uint8_t* valid, void* o,
                            hipStream_t st);
 
+// Backward pass buffers (inputs, saved tensors, outputs and workspace parts).
+struct BwdArgs {
+  const void *q, *k, *v, *dout;
+  const uint8_t* valid;
+  const float* gate;
+  const void* o_branch;
+  const float *lse, *kcmp, *vcmp, *hid_k, *hid_v;
+  const int* sel;
+  const uint8_t* cvalid;
+  float *dq, *dk, *dv, *dgate;
+  // workspace
+  float* R;                      // [3, B, H, N]
+  void *kc_lp, *vc_lp;           // compressed tokens in the storage type
+  float *dkc_part, *dvc_part;    // [chunks, B, H, N/l, d]
+  float *dkc, *dvc;              // [B, H, N/l, d]
+  uint32_t *pair_keys, *pair_vals, *pair_keys_tmp, *pair_vals_tmp, *sort_hist;
+  int *seg_start, *seg_end;
+  const uint32_t* pair_groups;   // set internally: sorted group ids
+};
+
+// attn_bwd.hip
+hipError_t launch_attn_bwd(const Dims& D, const BwdArgs& A, hipStream_t st);
+hipError_t launch_slc_csr(const Dims& D, const BwdArgs& A, hipStream_t st);
+
+// compress.hip: backward of phi (dK^ -> token gradients added into dx, weight gradients)
+struct MlpBwdWs {
+  float* dpre;        // [rows, d]
+  float* part_w1;     // [chunks, l*d, d]
+  float* part_small;  // [chunks, d*d + 2d]
+  int chunks;
+};
+int mlp_bwd_chunks(const Dims& D);
+hipError_t launch_compress_bwd(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi, const float* pre,
+                               const float* dy, float* dx_accum, const MlpGrad& grad, const MlpBwdWs& ws,
+                               hipStream_t st);
+
+// tree.hip: stable LSD radix sort of (key, value) pairs on the low `bits` key bits.
+size_t radix_sort_hist_words(long long n);
+hipError_t launch_radix_sort_pairs(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
+                                   uint32_t* hist, long long n, int bits, uint32_t** keys_out, uint32_t** vals_out,
+                                   hipStream_t st);
+
+#define BSA_DISPATCH(FN, ...)                                                              \
+  (D.bf16 ? (D.d == 64 ? FN<bf16_t, 64>(__VA_ARGS__) : FN<bf16_t, 32>(__VA_ARGS__))       \
+          : (D.d == 64 ? FN<float, 64>(__VA_ARGS__) : FN<float, 32>(__VA_ARGS__)))
+
 }  // namespace bsa

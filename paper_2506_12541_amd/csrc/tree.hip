@@ -520,6 +520,28 @@ hipError_t launch_build_tree(const float* pts, int64_t n_real, int dim, int64_t 
   return hipGetLastError();
 }
 
+size_t radix_sort_hist_words(long long n) { return (size_t)16 * ((n + kSortTile - 1) / kSortTile); }
+
+hipError_t launch_radix_sort_pairs(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
+                                   uint32_t* hist, long long n, int bits, uint32_t** keys_out, uint32_t** vals_out,
+                                   hipStream_t st) {
+  const int ntiles = (int)((n + kSortTile - 1) / kSortTile);
+  const int passes = (bits + 3) / 4;  // key digits only (pass < 8)
+  uint32_t *ka = keys, *va = vals, *kb = keys_tmp, *vb = vals_tmp;
+  for (int pass = 0; pass < passes; ++pass) {
+    hipLaunchKernelGGL(sort_hist_kernel, dim3(ntiles, 1), dim3(kSortThreads), 0, st, ka, va, (int)n, pass, 1, ntiles,
+                       hist);
+    hipLaunchKernelGGL(sort_scan_kernel, dim3(1, 1), dim3(1024), 0, st, hist, ntiles);
+    hipLaunchKernelGGL(sort_scatter_kernel, dim3(ntiles, 1), dim3(kSortThreads), 0, st, ka, va, kb, vb, (int)n, pass,
+                       1, ntiles, hist);
+    std::swap(ka, kb);
+    std::swap(va, vb);
+  }
+  *keys_out = ka;
+  *vals_out = va;
+  return hipGetLastError();
+}
+
 hipError_t launch_permute(const void* src, const int* perm, int64_t n_real, int64_t n_pad, int batch,
                           int heads, int hd, int dtype, void* dst, uint8_t* valid, bool inverse,
                           hipStream_t st) {

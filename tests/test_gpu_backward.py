@@ -1,0 +1,97 @@
+"""GPU backward pass vs the float64 oracle's analytic gradients on the same inputs.
+
+The oracle runs with the GPU's selected blocks (ties within 1e-6 may pick different
+blocks; the gradient is defined for a fixed selection). dQ, dK, dV are compared by
+max-abs error; weight and gate-logit gradients, which are sums over many terms, by
+max-abs error relative to the largest oracle entry. Bar: 1e-4 (f32) / 2e-2 (bf16)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import bsa as ob
+from parity import TOL, gpu_forward, max_abs, oracle_params, to_dev, valid_from_tree
+from paper_2506_12541_amd import bsa as gb
+from workloads import CONFIGS, Config, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def oracle_with_sel(inp, valid, P, sel):
+    """Oracle forward caches, with the selection branch re-run on the given blocks."""
+    f64 = lambda a: np.asarray(a, np.float64)
+    q, k, v = f64(inp["q"]), f64(inp["k"]), f64(inp["v"])
+    fwd = ob.forward(q, k, v, valid, inp["gate"], inp["phi_k"], inp["phi_v"], P)
+    fwd["sel"] = sel
+    B, H = q.shape[:2]
+    for b in range(B):
+        for h in range(H):
+            fwd["o_branch"][2, b, h], fwd["lse"][2, b, h] = ob.selection_branch(q[b, h], k[b, h], v[b, h], valid[b],
+                                                                                sel[b, h], P)
+    return fwd
+
+
+def run_case(cfg, seed=None, gate_scale=1.0, **pkw):
+    inp = make_inputs(cfg, seed, layout="ball", with_grad=True)
+    inp["gate"] = (inp["gate"] * gate_scale).astype(np.float32)
+    valid = valid_from_tree(cfg)
+    g, (p, q, k, v, vd, gate, phi_k, phi_v, saved, o) = gpu_forward(cfg, inp, valid, **pkw)
+    dout = to_dev(inp["do"], p.torch_dtype)
+    grads = gb.backward(p, q, k, v, vd, gate, phi_k, phi_v, saved, dout)
+    torch.cuda.synchronize()
+    okw = {}
+    if pkw.get("kv_pool") == 1:
+        okw["kv_pool"] = "mean"
+    if pkw.get("mask_own_ball") == 0:
+        okw["mask_own_ball"] = False
+    P = oracle_params(cfg, **okw)
+    fwd = oracle_with_sel(inp, valid, P, g["sel"])
+    ref = ob.backward(inp["q"], inp["k"], inp["v"], valid, inp["gate"], inp["phi_k"], inp["phi_v"], P, fwd, inp["do"])
+    tol = TOL[cfg.dtype]
+    out = {n: grads[n].cpu().numpy() for n in ("dq", "dk", "dv", "dgate")}
+    errs = {}
+    for n in ("dq", "dk", "dv"):
+        errs[n] = max_abs(out[n], ref[n])
+    errs["dgate"] = max_abs(out["dgate"], ref["dgate"]) / max(1e-30, np.abs(ref["dgate"]).max())
+    if P.kv_pool == "mlp":
+        for which in ("dphi_k", "dphi_v"):
+            for w in ("w1", "b1", "w2", "b2"):
+                r = ref[which][w]
+                errs[f"{which}.{w}"] = max_abs(grads[which][w].cpu().numpy(), r) / max(1e-30, np.abs(r).max())
+    print({k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    bad = {k: v for k, v in errs.items() if not v < tol}
+    assert not bad, bad
+    # padding slots carry no gradient
+    for n in ("dq", "dk", "dv"):
+        for b in range(cfg.batch):
+            assert not np.any(out[n][b][:, ~valid[b]])
+
+
+def test_backward_tiny_fp32():
+    print("backward parity config 1", flush=True)
+    run_case(CONFIGS[1])
+
+
+def test_backward_tiny_fp32_isolated_branches():
+    # saturated gates isolate each branch (sigmoid(+-12) ~ 1 / 6e-6)
+    cfg = CONFIGS[1]
+    for scale in (30.0,):
+        print(f"backward parity config 1, gate scale {scale}", flush=True)
+        run_case(cfg, gate_scale=scale)
+
+
+def test_backward_airflow_bf16():
+    print("backward parity config 5", flush=True)
+    run_case(CONFIGS[5])
+
+
+def test_backward_variants():
+    cfg = CONFIGS[1]
+    for kw in (dict(mask_own_ball=0), dict(kv_pool=1)):
+        print(f"backward variant {kw}", flush=True)
+        run_case(cfg, **kw)
+
+
+def test_backward_small_bf16_with_padding():
+    cfg = Config("small_bf16", 2, 900, 1024, 2, 64, "bf16", 128, 16, 16, 32, 4, 16, "uniform", "fwdbwd")
+    print("backward parity small bf16 d=64", flush=True)
+    run_case(cfg, seed=11)
