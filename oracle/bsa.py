@@ -165,6 +165,9 @@ def compress_backward(dout, cache, valid, phi, P: Params):
     dpre = (dout @ phi["w2"].T) * gelu_grad(cache["pre"])
     grads["w1"] = cache["flat"].T @ dpre
     grads["b1"] = dpre.sum(axis=0)
+    # magnitude of the summed terms of each weight gradient (error scale of a sum)
+    grads["abs"] = {"w2": np.abs(cache["hid"]).T @ np.abs(dout), "b2": np.abs(dout).sum(axis=0),
+                    "w1": np.abs(cache["flat"]).T @ np.abs(dpre), "b1": np.abs(dpre).sum(axis=0)}
     dx = (dpre @ phi["w1"].T).reshape(-1, d)
     return np.where(valid[:, None], dx, 0.0), grads
 
@@ -344,12 +347,16 @@ def backward(q, k, v, valid, gate, phi_k, phi_v, P: Params, fwd, do):
     ob, lse, sel = fwd["o_branch"], fwd["lse"], fwd["sel"]
     sg = sigmoid(gate)
     dgate = np.zeros((B, n, 3))
+    dgate_abs = np.zeros((B, n, 3))
     for br in range(3):
         dgate[:, :, br] = sg[:, :, br] * (1.0 - sg[:, :, br]) * np.sum(do * ob[br], axis=(1, 3))
+        dgate_abs[:, :, br] = sg[:, :, br] * (1.0 - sg[:, :, br]) * np.sum(np.abs(do * ob[br]), axis=(1, 3))
     dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
     wkeys = ("w1", "b1", "w2", "b2")
     dphi_k = {w: np.zeros_like(phi_k[w]) for w in wkeys} if P.kv_pool == "mlp" else {}
     dphi_v = {w: np.zeros_like(phi_v[w]) for w in wkeys} if P.kv_pool == "mlp" else {}
+    abs_k = {w: np.zeros_like(phi_k[w]) for w in wkeys} if P.kv_pool == "mlp" else {}
+    abs_v = {w: np.zeros_like(phi_v[w]) for w in wkeys} if P.kv_pool == "mlp" else {}
     for b in range(B):
         vb = valid[b]
         cvalid = block_valid(vb, l)
@@ -367,7 +374,10 @@ def backward(q, k, v, valid, gate, phi_k, phi_v, P: Params, fwd, do):
             dq[b, h] = g0[0] + gq + g2[0]
             dk[b, h] = g0[1] + dk_c + g2[1]
             dv[b, h] = g0[2] + dv_c + g2[2]
-            for w in wk:
+            for w in wkeys if wk else ():
                 dphi_k[w] += wk[w]
                 dphi_v[w] += wv[w]
-    return {"dq": dq, "dk": dk, "dv": dv, "dgate": dgate, "dphi_k": dphi_k, "dphi_v": dphi_v}
+                abs_k[w] += wk["abs"][w]
+                abs_v[w] += wv["abs"][w]
+    return {"dq": dq, "dk": dk, "dv": dv, "dgate": dgate, "dphi_k": dphi_k, "dphi_v": dphi_v,
+            "abs": {"dgate": dgate_abs, "dphi_k": abs_k, "dphi_v": abs_v}}

@@ -2,8 +2,11 @@
 
 The oracle runs with the GPU's selected blocks (ties within 1e-6 may pick different
 blocks; the gradient is defined for a fixed selection). dQ, dK, dV are compared by
-max-abs error; weight and gate-logit gradients, which are sums over many terms, by
-max-abs error relative to the largest oracle entry. Bar: 1e-4 (f32) / 2e-2 (bf16)."""
+max-abs error; weight and gate-logit gradients, which are sums over many terms, by the
+error of each entry relative to the magnitude of its summed terms (sum of |term|, the
+standard error bound of a sum; the bias of the key MLP's last layer has an identically
+zero gradient because a shift of every compressed key leaves each softmax unchanged).
+Bar: 1e-4 (f32) / 2e-2 (bf16)."""
 import numpy as np
 import pytest
 import torch
@@ -51,12 +54,13 @@ def run_case(cfg, seed=None, gate_scale=1.0, **pkw):
     errs = {}
     for n in ("dq", "dk", "dv"):
         errs[n] = max_abs(out[n], ref[n])
-    errs["dgate"] = max_abs(out["dgate"], ref["dgate"]) / max(1e-30, np.abs(ref["dgate"]).max())
+    # summed gradients: |gpu - oracle| relative to the magnitude of the summed terms
+    rel = lambda g, r, a: float(np.max(np.abs(np.asarray(g, np.float64) - r) / np.maximum(a, 1e-30)))
+    errs["dgate"] = rel(out["dgate"], ref["dgate"], ref["abs"]["dgate"])
     if P.kv_pool == "mlp":
         for which in ("dphi_k", "dphi_v"):
             for w in ("w1", "b1", "w2", "b2"):
-                r = ref[which][w]
-                errs[f"{which}.{w}"] = max_abs(grads[which][w].cpu().numpy(), r) / max(1e-30, np.abs(r).max())
+                errs[f"{which}.{w}"] = rel(grads[which][w].cpu().numpy(), ref[which][w], ref["abs"][which][w])
     print({k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
     bad = {k: v for k, v in errs.items() if not v < tol}
     assert not bad, bad
