@@ -348,9 +348,10 @@ def backward(q, k, v, valid, gate, phi_k, phi_v, P: Params, fwd, do):
     sg = sigmoid(gate)
     dgate = np.zeros((B, n, 3))
     dgate_abs = np.zeros((B, n, 3))
+    dsg = sg * sigmoid(-gate)            # sigmoid'(x) = s(x) s(-x), no cancellation when saturated
     for br in range(3):
-        dgate[:, :, br] = sg[:, :, br] * (1.0 - sg[:, :, br]) * np.sum(do * ob[br], axis=(1, 3))
-        dgate_abs[:, :, br] = sg[:, :, br] * (1.0 - sg[:, :, br]) * np.sum(np.abs(do * ob[br]), axis=(1, 3))
+        dgate[:, :, br] = dsg[:, :, br] * np.sum(do * ob[br], axis=(1, 3))
+        dgate_abs[:, :, br] = dsg[:, :, br] * np.sum(np.abs(do * ob[br]), axis=(1, 3))
     dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
     wkeys = ("w1", "b1", "w2", "b2")
     dphi_k = {w: np.zeros_like(phi_k[w]) for w in wkeys} if P.kv_pool == "mlp" else {}

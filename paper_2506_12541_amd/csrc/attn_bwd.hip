@@ -54,8 +54,8 @@ __global__ void gate_bwd_kernel(const float* R, const float* gate, const uint8_t
     float sum = 0.f;
     if (valid == nullptr || valid[i])
       for (int h = 0; h < H; ++h) sum += R[br * rows + ((long long)b * H + h) * N + n];
-    float s = sigmoidf(gate[(size_t)i * 3 + br]);
-    dgate[(size_t)i * 3 + br] = s * (1.f - s) * sum;
+    const float x = gate[(size_t)i * 3 + br];
+    dgate[(size_t)i * 3 + br] = sigmoidf(x) * sigmoidf(-x) * sum;   // s(1-s) without cancellation
   }
 }
 
