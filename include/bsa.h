@@ -154,6 +154,20 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
                           const bsa_mlp_grad_t* dphi_k, const bsa_mlp_grad_t* dphi_v,
                           void* ws, size_t ws_bytes, void* stream);
 
+/* ---- Measurement support (not part of the layer's computation) ---- */
+
+/* on = 1: start recording, clearing earlier records; on = 0: stop and clear. While on,
+ * every timed phase of the library records a start and a stop HIP event on the stream
+ * its kernels are launched on. Phases: "tree", "permute", "fwd.compress", "fwd.select",
+ * "fwd.ball", "fwd.cmp", "fwd.slc", "fwd.gate", "bwd.gate", "bwd.dq_ball", "bwd.dq_cmp",
+ * "bwd.dq_slc", "bwd.kv_ball", "bwd.kv_cmp", "bwd.mlp", "bwd.slc_csr", "bwd.slc_kv".
+ * Host-side bookkeeping only; no device memory is allocated. */
+bsa_status_t bsa_timing_enable(int32_t on);
+
+/* Sum of the recorded durations of `phase` (milliseconds) and the number of records;
+ * waits for the recorded events to complete. */
+bsa_status_t bsa_timing_query(const char* phase, double* total_ms, int32_t* count);
+
 const char* bsa_status_string(bsa_status_t s);
 /* Detail of the last failure on the calling thread ("" if none). */
 const char* bsa_last_error(void);

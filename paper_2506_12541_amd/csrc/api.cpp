@@ -177,6 +177,21 @@ const char* bsa_status_string(bsa_status_t s) {
 
 const char* bsa_last_error(void) { return g_last_error.c_str(); }
 
+bsa_status_t bsa_timing_enable(int32_t on) {
+  g_last_error.clear();
+  bsa::timing_set(on != 0);
+  return BSA_OK;
+}
+
+bsa_status_t bsa_timing_query(const char* phase, double* total_ms, int32_t* count) {
+  g_last_error.clear();
+  if (!phase || !total_ms || !count) return fail(BSA_ERR_INVALID_ARGUMENT, "phase, total_ms and count must be non-NULL");
+  int n = 0;
+  BSA_TRY(bsa::timing_query(phase, total_ms, &n), "bsa_timing_query");
+  *count = n;
+  return BSA_OK;
+}
+
 size_t bsa_ball_tree_workspace_bytes(int64_t n_real, int64_t n_pad, int32_t dim, int32_t batch) {
   if (n_real < 1 || n_real > n_pad || !pow2(n_pad) || n_pad > (1 << 24) || dim < 1 || dim > 3 || batch < 1) return 0;
   if ((int64_t)batch * n_pad > (int64_t(1) << 30)) return 0;
@@ -195,8 +210,10 @@ bsa_status_t bsa_build_ball_tree(const float* points, int64_t n_real, int32_t di
   if (need == 0) return fail(BSA_ERR_INVALID_ARGUMENT, "batch * n_pad too large");
   if (!ws || ws_bytes < need)
     return fail(BSA_ERR_WORKSPACE_TOO_SMALL, "tree workspace needs " + std::to_string(need) + " bytes");
-  BSA_TRY(bsa::launch_build_tree(points, n_real, dim, n_pad, batch, perm, ws, (hipStream_t)stream),
-          "bsa_build_ball_tree");
+  hipError_t e;
+  BSA_PHASE("tree", (hipStream_t)stream,
+            e = bsa::launch_build_tree(points, n_real, dim, n_pad, batch, perm, ws, (hipStream_t)stream));
+  BSA_TRY(e, "bsa_build_ball_tree");
   return BSA_OK;
 }
 
@@ -214,9 +231,11 @@ bsa_status_t bsa_permute(const void* src, const int32_t* perm, int64_t n_real, i
   g_last_error.clear();
   bsa_status_t s = permute_common(src, perm, n_real, n_pad, batch, heads, head_dim, dtype, dst);
   if (s != BSA_OK) return s;
-  BSA_TRY(bsa::launch_permute(src, perm, n_real, n_pad, batch, heads, head_dim, dtype, dst, valid_out, false,
-                              (hipStream_t)stream),
-          "bsa_permute");
+  hipError_t e;
+  BSA_PHASE("permute", (hipStream_t)stream,
+            e = bsa::launch_permute(src, perm, n_real, n_pad, batch, heads, head_dim, dtype, dst, valid_out, false,
+                                    (hipStream_t)stream));
+  BSA_TRY(e, "bsa_permute");
   return BSA_OK;
 }
 
@@ -294,16 +313,29 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   }
   void* kc_lp = w + W.kc_lp;
   void* vc_lp = w + W.vc_lp;
-  BSA_TRY(bsa::launch_block_valid(D, valid, saved->cvalid, st), "block_valid");
-  BSA_TRY(bsa::launch_compress_fwd(D, k, valid, mk, saved->kcmp, saved->hid_k, kc_lp, w + W.w1t_k, st), "compress K");
-  BSA_TRY(bsa::launch_compress_fwd(D, v, valid, mv, saved->vcmp, saved->hid_v, vc_lp, w + W.w1t_v, st), "compress V");
-  BSA_TRY(bsa::launch_select_topk(D, q, valid, saved->kcmp, saved->cvalid, saved->sel_idx, st), "select");
-  BSA_TRY(bsa::launch_ball_fwd(D, q, k, v, valid, ob, saved->lse, st), "ball attention");
-  BSA_TRY(bsa::launch_cmp_fwd(D, q, kc_lp, vc_lp, valid, saved->cvalid, ob + ob_stride, saved->lse + rows, st),
-          "compressed attention");
-  BSA_TRY(bsa::launch_slc_fwd(D, q, k, v, valid, saved->sel_idx, ob + 2 * ob_stride, saved->lse + 2 * rows, st),
-          "selection attention");
-  BSA_TRY(bsa::launch_gate_fwd(D, ob, gate, valid, o, st), "gate");
+  hipError_t e = hipSuccess;
+#define BSA_STEP(name, call, what)        \
+  BSA_PHASE(name, st, e = (call));         \
+  BSA_TRY(e, what)
+  BSA_STEP("fwd.compress", (bsa::launch_block_valid(D, valid, saved->cvalid, st) != hipSuccess
+                                ? hipGetLastError()
+                                : bsa::launch_compress_fwd(D, k, valid, mk, saved->kcmp, saved->hid_k, kc_lp,
+                                                           w + W.w1t_k, st) != hipSuccess
+                                      ? hipGetLastError()
+                                      : bsa::launch_compress_fwd(D, v, valid, mv, saved->vcmp, saved->hid_v, vc_lp,
+                                                                 w + W.w1t_v, st)),
+           "compression");
+  BSA_STEP("fwd.select", bsa::launch_select_topk(D, q, valid, saved->kcmp, saved->cvalid, saved->sel_idx, st),
+           "select");
+  BSA_STEP("fwd.ball", bsa::launch_ball_fwd(D, q, k, v, valid, ob, saved->lse, st), "ball attention");
+  BSA_STEP("fwd.cmp",
+           bsa::launch_cmp_fwd(D, q, kc_lp, vc_lp, valid, saved->cvalid, ob + ob_stride, saved->lse + rows, st),
+           "compressed attention");
+  BSA_STEP("fwd.slc",
+           bsa::launch_slc_fwd(D, q, k, v, valid, saved->sel_idx, ob + 2 * ob_stride, saved->lse + 2 * rows, st),
+           "selection attention");
+  BSA_STEP("fwd.gate", bsa::launch_gate_fwd(D, ob, gate, valid, o, st), "gate");
+#undef BSA_STEP
   return BSA_OK;
 }
 
@@ -353,8 +385,11 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
     gk = {dphi_k->w1, dphi_k->b1, dphi_k->w2, dphi_k->b2};
     gv = {dphi_v->w1, dphi_v->b1, dphi_v->w2, dphi_v->b2};
   }
-  BSA_TRY(bsa::launch_compress_bwd(D, k, valid, mk, saved->hid_k, A.dkc, dk, gk, mw, st), "compression backward K");
-  BSA_TRY(bsa::launch_compress_bwd(D, v, valid, mv, saved->hid_v, A.dvc, dv, gv, mw, st), "compression backward V");
+  hipError_t e;
+  BSA_PHASE("bwd.mlp", st, e = bsa::launch_compress_bwd(D, k, valid, mk, saved->hid_k, A.dkc, dk, gk, mw, st));
+  BSA_TRY(e, "compression backward K");
+  BSA_PHASE("bwd.mlp", st, e = bsa::launch_compress_bwd(D, v, valid, mv, saved->hid_v, A.dvc, dv, gv, mw, st));
+  BSA_TRY(e, "compression backward V");
   BSA_TRY(bsa::launch_slc_csr(D, A, st), "selection backward");
   return BSA_OK;
 }

@@ -693,10 +693,12 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
   const float sl2 = D.scale * kLog2e;
   const int nct = D.N / D.l;
   // per-branch row sums and the gate gradient
+  BSA_PHASE("bwd.gate", st, {
   hipLaunchKernelGGL(gate_bwd_rows_kernel<T>, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, st, (const T*)A.dout,
                      (const T*)A.o_branch, rows, HD, A.R);
   hipLaunchKernelGGL(gate_bwd_kernel, dim3((D.B * D.N + 255) / 256), dim3(256), 0, st, A.R, A.gate, A.valid, D.B, D.H,
                      D.N, A.dgate);
+  });
   QTerms qball{A.lse, A.R, A.gate, 0};
   QTerms qcmp{A.lse + rows, A.R + rows, A.gate, 1};
   QTerms qslc{A.lse + 2 * rows, A.R + 2 * rows, A.gate, 2};
@@ -716,6 +718,7 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
     vc = (const T*)A.vcmp;
   }
   // ---- dQ: ball (write), compressed (add), selection (add) ----
+  BSA_PHASE("bwd.dq_ball", st, {
   if (D.m >= 128) {
     hipLaunchKernelGGL((dense_bwd_q_kernel<T, HD, 2, true, false>), dim3(D.N / 128, D.H, D.B), dim3(256), 0, st, q, k,
                        v, dout, A.valid, qball, D.H, D.N, D.N, D.m, sl2, D.scale, A.dq);
@@ -723,11 +726,15 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
     hipLaunchKernelGGL((dense_bwd_q_kernel<T, HD, 1, true, false>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, q, k,
                        v, dout, A.valid, qball, D.H, D.N, D.N, D.m, sl2, D.scale, A.dq);
   }
+  });
+  BSA_PHASE("bwd.dq_cmp", st,
   hipLaunchKernelGGL((dense_bwd_q_kernel<T, HD, 2, false, true>), dim3(D.N / 128, D.H, D.B), dim3(256), 0, st, q, kc,
-                     vc, dout, A.cvalid, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq);
+                     vc, dout, A.cvalid, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq));
+  BSA_PHASE("bwd.dq_slc", st,
   hipLaunchKernelGGL((slc_bwd_q_kernel<T, HD>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, q, k, v, dout, A.valid,
-                     A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq);
+                     A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq));
   // ---- dK, dV of the ball branch (written) ----
+  BSA_PHASE("bwd.kv_ball", st, {
   if (D.m >= 128) {
     hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, 4, true>), dim3(D.N / 128, 1, D.B * D.H), dim3(256), 0, st, q, k,
                        v, dout, A.valid, qball, D.H, D.N, D.N, D.m, 1, sl2, D.scale, A.dk, A.dv);
@@ -735,12 +742,14 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
     hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, 2, true>), dim3(D.N / 64, 1, D.B * D.H), dim3(128), 0, st, q, k, v,
                        dout, A.valid, qball, D.H, D.N, D.N, D.m, 1, sl2, D.scale, A.dk, A.dv);
   }
+  });
   // ---- dK^, dV^ of the compressed branch: chunked partials, then a fixed-order sum ----
   {
     const int nch = D.N / kCmpChunks >= kQT ? kCmpChunks : 1;
+    BSA_PHASE("bwd.kv_cmp", st,
     hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, 4, false>), dim3((nct + 127) / 128, nch, D.B * D.H), dim3(256), 0,
                        st, q, kc, vc, dout, A.cvalid, qcmp, D.H, D.N, nct, D.m, nch, sl2, D.scale, A.dkc_part,
-                       A.dvc_part);
+                       A.dvc_part));
     const long long n = D.cmp_rows() * HD;
     hipLaunchKernelGGL(sum_chunks_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.dkc_part, nch, n,
                        A.dkc);
@@ -787,6 +796,7 @@ hipError_t launch_slc_csr(const Dims& D, const BwdArgs& A, hipStream_t st) {
   const uint32_t sentinel = (uint32_t)nseg;
   int bits = 1;
   while ((1ll << bits) <= (long long)sentinel) ++bits;
+  const int tid = timing_begin("bwd.slc_csr", st);
   hipLaunchKernelGGL(slc_pairs_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, A.sel, total, D.k,
                      D.N / D.g, nblk, sentinel, A.pair_keys, A.pair_vals);
   hipLaunchKernelGGL(fill_kernel, dim3((unsigned)((nseg + 255) / 256)), dim3(256), 0, st, A.seg_start, nseg, 0);
@@ -798,9 +808,12 @@ hipError_t launch_slc_csr(const Dims& D, const BwdArgs& A, hipStream_t st) {
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(seg_bounds_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, kout, total, sentinel,
                      A.seg_start, A.seg_end);
+  timing_end(tid, st);
   BwdArgs A2 = A;
   A2.pair_groups = vout;
-  return BSA_DISPATCH(slc_kv_impl, D, A2, st);
+  hipError_t r;
+  BSA_PHASE("bwd.slc_kv", st, r = BSA_DISPATCH(slc_kv_impl, D, A2, st));
+  return r;
 }
 
 }  // namespace bsa

@@ -94,6 +94,21 @@ hipError_t launch_radix_sort_pairs(uint32_t* keys, uint32_t* vals, uint32_t* key
                                    uint32_t* hist, long long n, int bits, uint32_t** keys_out, uint32_t** vals_out,
                                    hipStream_t st);
 
+// timing.cpp: optional per-phase HIP-event timing (see bsa_timing_enable in bsa.h)
+bool timing_on();
+void timing_set(bool on);
+int timing_begin(const char* name, hipStream_t st);
+void timing_end(int id, hipStream_t st);
+hipError_t timing_query(const char* name, double* total_ms, int* count);
+
+// Run `stmt` (kernel launches on stream st) as the timed phase `name`.
+#define BSA_PHASE(name, st, stmt)                     \
+  do {                                                \
+    const int _tid = ::bsa::timing_begin((name), (st)); \
+    stmt;                                             \
+    ::bsa::timing_end(_tid, (st));                    \
+  } while (0)
+
 #define BSA_DISPATCH(FN, ...)                                                              \
   (D.bf16 ? (D.d == 64 ? FN<bf16_t, 64>(__VA_ARGS__) : FN<bf16_t, 32>(__VA_ARGS__))       \
           : (D.d == 64 ? FN<float, 64>(__VA_ARGS__) : FN<float, 32>(__VA_ARGS__)))
