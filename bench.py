@@ -122,8 +122,10 @@ def main():
         k = gb.permute(xk, perm, H, d)
         v = gb.permute(xv, perm, H, d)
         gate = gb.permute(gate_pts, perm, 1, 3).view(cfg.batch, cfg.n_pad, 3)
-        o, sv = gb.forward(p, q, k, v, valid, gate, phi_k, phi_v, saved=saved)
-        grads = gb.backward(p, q, k, v, valid, gate, phi_k, phi_v, sv, dout)
+        # every slot holds a real point when n_real == n_pad: the layer may skip key masks
+        vmask = None if cfg.n_real == cfg.n_pad else valid
+        o, sv = gb.forward(p, q, k, v, vmask, gate, phi_k, phi_v, saved=saved)
+        grads = gb.backward(p, q, k, v, vmask, gate, phi_k, phi_v, sv, dout)
         return o, grads
 
     for _ in range(args.warmup):

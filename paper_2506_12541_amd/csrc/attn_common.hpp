@@ -76,22 +76,114 @@ __device__ __forceinline__ void stage_t(const T* const (&rows)[4], int dc, T* ds
   stage_vt(rows, dc, dst, stride, off);
 }
 
+
+// ---- register-prefetched staging of a 64-row tile (rows [t0, t0 + 64) of a [*, HD] matrix) ----
+// Row-major copy: RV 16-byte vectors per thread. Transposed copy (rows become columns):
+// each of the first (64/4)*(HD/4) threads moves a 4-row x 4-column block.
+template <typename T> struct Vec4T;
+template <> struct Vec4T<bf16_t> { typedef uint2 type; };
+template <> struct Vec4T<float> { typedef float4 type; };
+
+template <typename T, int HD, int ROWS = kKT>
+struct TileIO {
+  static constexpr int VPR = HD * (int)sizeof(T) / 16;           // 16-byte vectors per row
+  static constexpr int RV = (ROWS * VPR + 255) / 256;            // row vectors per thread
+  static constexpr int TI = (ROWS / 4) * (HD / 4);               // transposed 4x4 items
+  static constexpr int TV = (TI + 255) / 256;                    // transposed items per thread
+  typedef typename Vec4T<T>::type V4;
+
+  __device__ static void load_rows(uint4 (&r)[RV], const T* base, int t0, int nrows) {
+#pragma unroll
+    for (int u = 0; u < RV; ++u) {
+      const int e = threadIdx.x + 256 * u;
+      const int row = e / VPR, c = (e % VPR) * (16 / (int)sizeof(T));
+      r[u] = make_uint4(0, 0, 0, 0);
+      if (e < ROWS * VPR && t0 + row < nrows) r[u] = *reinterpret_cast<const uint4*>(base + (size_t)(t0 + row) * HD + c);
+    }
+  }
+  __device__ static void store_rows(const uint4 (&r)[RV], T* lds, int stride) {
+#pragma unroll
+    for (int u = 0; u < RV; ++u) {
+      const int e = threadIdx.x + 256 * u;
+      const int row = e / VPR, c = (e % VPR) * (16 / (int)sizeof(T));
+      if (e < ROWS * VPR) *reinterpret_cast<uint4*>(lds + row * stride + c) = r[u];
+    }
+  }
+  __device__ static void load_tr(V4 (&r)[TV][4], const T* base, int t0, int nrows) {
+#pragma unroll
+    for (int w = 0; w < TV; ++w) {
+      const int it = threadIdx.x + 256 * w;
+      const int kq = it / (HD / 4), dq = it % (HD / 4);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int row = t0 + 4 * kq + u;
+        r[w][u] = V4{};
+        if (it < TI && row < nrows) r[w][u] = *reinterpret_cast<const V4*>(base + (size_t)row * HD + 4 * dq);
+      }
+    }
+  }
+  __device__ static void store_tr(const V4 (&r)[TV][4], T* lds, int stride) {
+#pragma unroll
+    for (int w = 0; w < TV; ++w) {
+      const int it = threadIdx.x + 256 * w;
+      if (it >= TI) continue;
+      const int kq = it / (HD / 4), dq = it % (HD / 4);
+      store_tr4(r[w], lds + (4 * dq) * stride + 4 * kq, stride);
+    }
+  }
+  // 4x4 transpose: column x of the rows -> 4 consecutive elements of LDS row x
+  __device__ static void store_tr4(const uint2 (&r)[4], bf16_t* dst, int stride) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const int sh = 16 * (x & 1);
+      uint32_t e[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) e[u] = ((x < 2 ? r[u].x : r[u].y) >> sh) & 0xFFFFu;
+      *reinterpret_cast<uint2*>(dst + x * stride) = make_uint2(e[0] | (e[1] << 16), e[2] | (e[3] << 16));
+    }
+  }
+  __device__ static void store_tr4(const float4 (&r)[4], float* dst, int stride) {
+    *reinterpret_cast<float4*>(dst + 0 * stride) = make_float4(r[0].x, r[1].x, r[2].x, r[3].x);
+    *reinterpret_cast<float4*>(dst + 1 * stride) = make_float4(r[0].y, r[1].y, r[2].y, r[3].y);
+    *reinterpret_cast<float4*>(dst + 2 * stride) = make_float4(r[0].z, r[1].z, r[2].z, r[3].z);
+    *reinterpret_cast<float4*>(dst + 3 * stride) = make_float4(r[0].w, r[1].w, r[2].w, r[3].w);
+  }
+};
+
 // Online-softmax state of one wave over QB blocks of 16 queries.
+// Two VALU savings on the hot path: (1) the reference maximum is only raised when a new
+// tile maximum exceeds it by more than kRescale (log2 units), so the O accumulators are
+// rescaled rarely (probabilities stay <= 2^kRescale, far from f32 overflow); (2) the row
+// sums come from the matrix cores: an all-ones A operand in the PV product accumulates
+// sum_k P for each query in the same pass as O.
+constexpr float kRescale = 8.0f;
+
+template <typename T> __device__ __forceinline__ typename Chunk<T>::type ones_chunk();
+template <> __device__ __forceinline__ bf16x8 ones_chunk<bf16_t>() {
+  bf16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = (__bf16)1.0f;
+  return r;
+}
+template <> __device__ __forceinline__ f32x8 ones_chunk<float>() {
+  return f32x8{1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f};
+}
+
 template <typename T, int HD, int QB>
 struct WaveAttn {
   static constexpr int NCH = HD / 32;  // chunks of the head dim
   static constexpr int DB = HD / 16;   // 16-wide dim blocks of O^T
   typedef typename Chunk<T>::type CT;
   CT qf[QB][NCH];
-  float mx[QB];      // running max (log2 domain, scaled)
-  float lsum[QB];    // this lane's partial row sum
+  float mx[QB];      // reference maximum (log2 domain, scaled)
   f32x4 o[QB][DB];
+  f32x4 lsum[QB];    // row sums (every element holds the same sum)
 
   __device__ void init() {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       mx[qb] = kNegInf;
-      lsum[qb] = 0.f;
+      lsum[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int db = 0; db < DB; ++db) o[qb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
@@ -104,16 +196,12 @@ struct WaveAttn {
   __device__ __forceinline__ void tile(float sl2, KF kfrag, VF vfrag, OK keyok) {
     f32x4 s[QB][KB];
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) s[qb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int c = 0; c < NCH; ++c) {
         CT a = kfrag(kb, c);
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) s[qb][kb] = mma(a, qf[qb][c], s[qb][kb]);
+        for (int qb = 0; qb < QB; ++qb) s[qb][kb] = mma(a, qf[qb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : s[qb][kb]);
       }
     CT pf[QB][KB / 2];
 #pragma unroll
@@ -128,33 +216,32 @@ struct WaveAttn {
           tmax = fmaxf(tmax, x);
         }
       tmax = col_max(tmax) * sl2;          // scale > 0 keeps the order
-      const float mnew = fmaxf(mx[qb], tmax);
-      const float mref = mnew == kNegInf ? 0.f : mnew;
-      const float alpha = fast_exp2(mx[qb] - mref);
-      mx[qb] = mnew;
-      float ps = 0.f;
+      const bool raise = tmax > mx[qb] + kRescale;
+      if (__builtin_amdgcn_ballot_w64(raise)) {   // wave-uniform: rescale only when needed
+        const float mnew = raise ? tmax : mx[qb];
+        const float alpha = raise ? fast_exp2(mx[qb] - mnew) : 1.0f;
+        mx[qb] = mnew;
+        lsum[qb] *= alpha;
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float p = fast_exp2(__builtin_fmaf(s[qb][kb][i], sl2, -mref));
-          s[qb][kb][i] = p;
-          ps += p;
-        }
-      lsum[qb] = lsum[qb] * alpha + ps;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) o[qb][db] *= alpha;
+        for (int db = 0; db < DB; ++db) o[qb][db] *= alpha;
+      }
+      const float mref = mx[qb] == kNegInf ? 0.f : mx[qb];
 #pragma unroll
       for (int kp = 0; kp < KB / 2; ++kp) {
         float v8[8];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          v8[i] = s[qb][2 * kp][i];
-          v8[4 + i] = s[qb][2 * kp + 1][i];
+          v8[i] = fast_exp2(__builtin_fmaf(s[qb][2 * kp][i], sl2, -mref));
+          v8[4 + i] = fast_exp2(__builtin_fmaf(s[qb][2 * kp + 1][i], sl2, -mref));
         }
         pf[qb][kp] = make_chunk<T>(v8);
       }
     }
+    const CT ones = ones_chunk<T>();
+#pragma unroll
+    for (int kp = 0; kp < KB / 2; ++kp)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) lsum[qb] = mma(ones, pf[qb][kp], lsum[qb]);
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -170,7 +257,7 @@ struct WaveAttn {
     const int r = lane & 15, j = lane >> 4;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
-      const float l = col_sum(lsum[qb]);
+      const float l = lsum[qb][0];
       const bool qok = qvalid == nullptr || qvalid[qidx0 + 16 * qb + r];
       const bool any = qok && l > 0.f;
       const float inv = any ? 1.0f / l : 0.f;

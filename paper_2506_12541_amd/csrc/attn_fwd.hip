@@ -21,16 +21,18 @@ namespace {
 
 // ---- dense kernel: ball branch (keys = own ball) and compressed branch (all tokens) ----
 
+// Keys are staged 128 at a time (one pair of barriers) and consumed as two 64-key
+// halves; the next 128 keys are loaded into registers while the current ones are used.
 template <typename T, int HD, int QB, bool BALL>
 __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, const T* v, const uint8_t* qvalid_all,
                                                         const uint8_t* kvalid_all, int H, int N, int nkeys_total,
                                                         int m, float sl2, T* out, float* lse) {
+  constexpr int kFT = sizeof(T) == 2 ? 128 : 64;  // keys per staged tile (LDS stays < 64 KB)
   constexpr int KSTR = HD + 16 / (int)sizeof(T);  // LDS row stride of K (elements)
-  constexpr int VSTR = kKT + 4;                   // LDS row stride of V^T
-  constexpr int EPV = 16 / (int)sizeof(T);        // elements per 16-byte vector
-  __shared__ __attribute__((aligned(16))) T ks[kKT * KSTR];
+  constexpr int VSTR = kFT + 4;                   // LDS row stride of V^T
+  __shared__ __attribute__((aligned(16))) T ks[kFT * KSTR];
   __shared__ __attribute__((aligned(16))) T vt[HD * VSTR];
-  __shared__ uint8_t kok[kKT];
+  __shared__ uint8_t kok[kFT];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r = lane & 15, j = lane >> 4;
   const int b = blockIdx.z, h = blockIdx.y;
@@ -48,36 +50,36 @@ __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, 
   const int wq0 = q0 + wid * 16 * QB;
   load_q(w, q + (bh * N + wq0) * HD, lane);
 
-  for (int t0 = 0; t0 < nkeys; t0 += kKT) {
+  typedef TileIO<T, HD, kFT> IO;
+  uint4 kreg[IO::RV];
+  typename IO::V4 vreg[IO::TV][4];
+  IO::load_rows(kreg, kh, 0, nkeys);
+  IO::load_tr(vreg, vh, 0, nkeys);
+  for (int t0 = 0; t0 < nkeys; t0 += kFT) {
     __syncthreads();
-    for (int e = threadIdx.x; e < kKT * HD / EPV; e += 256) {
-      const int row = e / (HD / EPV), col = (e % (HD / EPV)) * EPV;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (t0 + row < nkeys) val = *reinterpret_cast<const uint4*>(kh + (size_t)(t0 + row) * HD + col);
-      *reinterpret_cast<uint4*>(&ks[row * KSTR + col]) = val;
-    }
-    for (int e = threadIdx.x; e < (kKT / 4) * (HD / 8); e += 256) {
-      const int kq = e / (HD / 8), dc = (e % (HD / 8)) * 8;
-      const T* rows[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int key = t0 + 4 * kq + u;
-        rows[u] = key < nkeys ? vh + (size_t)key * HD : nullptr;
-      }
-      stage_vt(rows, dc, vt, VSTR, 4 * kq);
-    }
-    if (threadIdx.x < kKT) {
+    IO::store_rows(kreg, ks, KSTR);
+    IO::store_tr(vreg, vt, VSTR);
+    if (threadIdx.x < kFT) {
       const int key = t0 + threadIdx.x;
       kok[threadIdx.x] = key < nkeys && (kval == nullptr || kval[key]);
     }
     __syncthreads();
-    auto kfrag = [&](int kb, int c) { return load_chunk(&ks[(kb * 16 + r) * KSTR + 32 * c + 8 * j]); };
-    auto vfrag = [&](int db, int kp) { return load_4x2(&vt[(16 * db + r) * VSTR + 32 * kp + 4 * j]); };
-    if (kval == nullptr && t0 + kKT <= nkeys) {
-      w.template tile<kKT / 16>(sl2, kfrag, vfrag, [](int, int, int) { return true; });
-    } else {
-      auto keyok = [&](int kb, int i, int) { return kok[kb * 16 + 4 * j + i] != 0; };
-      w.template tile<kKT / 16>(sl2, kfrag, vfrag, keyok);
+    if (t0 + kFT < nkeys) {   // next keys in flight while these are used
+      IO::load_rows(kreg, kh, t0 + kFT, nkeys);
+      IO::load_tr(vreg, vh, t0 + kFT, nkeys);
+    }
+#pragma unroll
+    for (int half = 0; half < kFT / kKT; ++half) {
+      const int h0 = half * kKT;
+      if (t0 + h0 >= nkeys) break;
+      auto kfrag = [&](int kb, int c) { return load_chunk(&ks[(h0 + kb * 16 + r) * KSTR + 32 * c + 8 * j]); };
+      auto vfrag = [&](int db, int kp) { return load_4x2(&vt[(16 * db + r) * VSTR + h0 + 32 * kp + 4 * j]); };
+      if (kval == nullptr && t0 + h0 + kKT <= nkeys) {
+        w.template tile<kKT / 16>(sl2, kfrag, vfrag, [](int, int, int) { return true; });
+      } else {
+        auto keyok = [&](int kb, int i, int) { return kok[h0 + kb * 16 + 4 * j + i] != 0; };
+        w.template tile<kKT / 16>(sl2, kfrag, vfrag, keyok);
+      }
     }
   }
   w.finish(lane, bh * N + wq0, out, lse, qval, wq0);
