@@ -124,8 +124,9 @@ FwdWs fwd_ws_layout(const bsa::Dims& D) {
 }
 
 struct BwdWs {
-  size_t R, kc_lp, vc_lp, dkc_part, dvc_part, dkc, dvc, pk, pv, pkt, pvt, hist, seg_s, seg_e, dpre, pw1, psm, total;
-  int cmp_chunks, mlp_chunks;
+  size_t R, kc_lp, vc_lp, dkc_part, dvc_part, dkc, dvc, pk, pv, pkt, pvt, hist, seg_s, seg_e, dpre, pw1, psm, w1lp,
+      total;
+  int cmp_chunks, mlp_chunks, mlp_chunks_small;
   long long pairs, nseg;
 };
 
@@ -137,6 +138,7 @@ BwdWs bwd_ws_layout(const bsa::Dims& D) {
   const size_t crows = (size_t)D.cmp_rows();
   W.cmp_chunks = D.N / 8 >= 64 ? 8 : 1;
   W.mlp_chunks = bsa::mlp_bwd_chunks(D);
+  W.mlp_chunks_small = bsa::mlp_bwd_chunks_small(D);
   W.pairs = (long long)D.B * D.H * (D.N / D.g) * D.k;
   W.nseg = (long long)D.B * D.H * (D.N / D.ls);
   W.R = put(sizeof(float) * 3 * rows);
@@ -155,7 +157,8 @@ BwdWs bwd_ws_layout(const bsa::Dims& D) {
   W.seg_e = put(4 * (size_t)W.nseg);
   W.dpre = put(sizeof(float) * crows * D.d);
   W.pw1 = put(sizeof(float) * (size_t)W.mlp_chunks * D.l * D.d * D.d);
-  W.psm = put(sizeof(float) * (size_t)W.mlp_chunks * ((size_t)D.d * D.d + 2 * D.d));
+  W.psm = put(sizeof(float) * (size_t)W.mlp_chunks_small * ((size_t)D.d * D.d + 2 * D.d));
+  W.w1lp = put(elem_bytes(D) * (size_t)D.l * D.d * D.d);
   W.total = off;
   return W;
 }
@@ -376,7 +379,8 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   A.sort_hist = (uint32_t*)(w + W.hist);
   A.seg_start = (int*)(w + W.seg_s); A.seg_end = (int*)(w + W.seg_e);
   BSA_TRY(bsa::launch_attn_bwd(D, A, st), "attention backward");
-  bsa::MlpBwdWs mw{(float*)(w + W.dpre), (float*)(w + W.pw1), (float*)(w + W.psm), W.mlp_chunks};
+  bsa::MlpBwdWs mw{(float*)(w + W.dpre), (float*)(w + W.pw1), (float*)(w + W.psm), (void*)(w + W.w1lp),
+                   W.mlp_chunks, W.mlp_chunks_small};
   bsa::Mlp mk{}, mv{};
   bsa::MlpGrad gk{}, gv{};
   if (D.pool == 0) {

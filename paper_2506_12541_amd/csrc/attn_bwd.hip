@@ -23,24 +23,40 @@ __device__ __forceinline__ float sigmoidf(float x) { return 1.0f / (1.0f + __exp
 __device__ __forceinline__ float lse_log2(float lse) { return lse == -__builtin_huge_valf() ? __builtin_huge_valf() : lse * kLog2e; }
 
 // ---- gate backward: R_b = rowsum(dO * o_b) per (b,h,n); dgamma_b = s'(gamma_b) sum_h R_b ----
+// 8 lanes per row, each lane a 16-byte piece per tensor; partial sums reduced by shuffles.
 template <typename T>
 __global__ void gate_bwd_rows_kernel(const T* dout, const T* ob, long long rows, int hd, float* R) {
-  long long row = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (row >= rows) return;
+  constexpr int EPV = 16 / (int)sizeof(T);
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long row = gid >> 3;
+  const int part = (int)(gid & 7);
   const long long per = rows * hd;
   float acc[3] = {0.f, 0.f, 0.f};
-  const T* d = dout + row * hd;
-  for (int c = 0; c < hd; c += 8) {
-    auto dc = load_chunk(d + c);
+  if (row < rows) {
+    for (int c = part * EPV; c < hd; c += 8 * EPV) {
+      const uint4 dv = *reinterpret_cast<const uint4*>(dout + row * hd + c);
+      const T* dp = reinterpret_cast<const T*>(&dv);
 #pragma unroll
-    for (int br = 0; br < 3; ++br) {
-      auto oc = load_chunk(ob + br * per + row * hd + c);
+      for (int br = 0; br < 3; ++br) {
+        const uint4 ov = *reinterpret_cast<const uint4*>(ob + br * per + row * hd + c);
+        const T* op = reinterpret_cast<const T*>(&ov);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[br] += (float)dc[e] * (float)oc[e];
+        for (int e = 0; e < EPV; ++e) acc[br] += to_f32<T>(dp[e]) * to_f32<T>(op[e]);
+      }
     }
   }
 #pragma unroll
-  for (int br = 0; br < 3; ++br) R[br * rows + row] = acc[br];
+  for (int br = 0; br < 3; ++br) {
+    float x = acc[br];
+    x += __shfl_xor(x, 1, 64);
+    x += __shfl_xor(x, 2, 64);
+    x += __shfl_xor(x, 4, 64);
+    acc[br] = x;
+  }
+  if (row < rows && part == 0) {
+#pragma unroll
+    for (int br = 0; br < 3; ++br) R[br * rows + row] = acc[br];
+  }
 }
 
 __global__ void gate_bwd_kernel(const float* R, const float* gate, const uint8_t* valid, int B, int H, int N,
@@ -542,6 +558,9 @@ __global__ void seg_bounds_kernel(const uint32_t* keys, long long total, uint32_
   if (i == total - 1 || keys[i + 1] != kx) seg_end[kx] = (int)(i + 1);
 }
 
+// One workgroup per (b, h, block): wave w takes the block's groups w, w+4, ... (prefetching
+// the next group's rows while computing the current one) and keeps partial dK, dV in
+// registers; the four partials are then summed in wave order through LDS.
 template <typename T, int HD, int KBW>
 __global__ void __launch_bounds__(256) slc_bwd_kv_kernel(const T* q, const T* k, const T* v, const T* dout,
                                                          const uint8_t* valid_all, const uint32_t* groups,
@@ -553,16 +572,16 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_kernel(const T* q, const T* k,
   typedef typename Chunk<T>::type CT;
   __shared__ __attribute__((aligned(16))) T qtr_all[4][HD * TSTR];
   __shared__ __attribute__((aligned(16))) T dtr_all[4][HD * TSTR];
+  __shared__ __attribute__((aligned(16))) float red[2][KBW * 16 * HD];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r = lane & 15, j = lane >> 4;
-  const long long seg = (long long)blockIdx.x * 4 + wid;
-  if (seg >= nseg) return;                  // whole wave leaves together; no block barrier below
+  const long long seg = blockIdx.x;
   const int nblk = N / ls;
   const long long bh = seg / nblk;
   const int blk = (int)(seg % nblk);
   const int b = (int)(bh / H);
   const int s0 = seg_start[seg], s1 = seg_end[seg];
-  if (s1 <= s0) return;
+  if (s1 <= s0) return;                     // uniform over the workgroup
   T* qtr = qtr_all[wid];
   T* dtr = dtr_all[wid];
   const T* qh = q + (size_t)bh * N * HD;
@@ -589,85 +608,113 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_kernel(const T* q, const T* k,
 
   const int qblocks = g >= 16 ? g / 16 : 1;
   const int qrows = g >= 16 ? 16 : g;       // real rows of each 16-query block
-  for (int e = s0; e < s1; ++e) {
-    const int p = (int)groups[e];
-    for (int qbk = 0; qbk < qblocks; ++qbk) {
-      const int qr0 = p * g + 16 * qbk;      // first query row of this block
-      // stage Q^T and dO^T of the 16 queries (rows beyond qrows are zero)
-      for (int it = lane; it < 4 * (HD / 8); it += 64) {
-        const int kq = it / (HD / 8), dc = (it % (HD / 8)) * 8;
-        const T* rq[4];
-        const T* rd[4];
+  const int nwork = (s1 - s0) * qblocks;    // (group, 16-query block) items of this block
+  // per-item inputs: A rows of Q and dO (lane row = query r) and the terms of rows 4j+i
+  CT aq[NCH], ad[NCH];
+  float lv[4], dvv[4], gv[4];
+  auto fetch = [&](int item) {
+    const int e = s0 + item / qblocks;
+    const int qr0 = (int)groups[e] * g + 16 * (item % qblocks);
+    const bool rok = r < qrows;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int rr = 4 * kq + u;
-          rq[u] = rr < qrows ? qh + (size_t)(qr0 + rr) * HD : nullptr;
-          rd[u] = rr < qrows ? dh + (size_t)(qr0 + rr) * HD : nullptr;
-        }
-        stage_vt(rq, dc, qtr, TSTR, 4 * kq);
-        stage_vt(rd, dc, dtr, TSTR, 4 * kq);
+    for (int c = 0; c < NCH; ++c) {
+      aq[c] = zero_chunk(aq[c]);
+      ad[c] = zero_chunk(ad[c]);
+      if (rok) {
+        aq[c] = load_chunk(qh + (size_t)(qr0 + r) * HD + 32 * c + 8 * j);
+        ad[c] = load_chunk(dh + (size_t)(qr0 + r) * HD + 32 * c + 8 * j);
       }
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      // A operands of S and dP: query rows (lane row = query r)
-      const bool rok = r < qrows;
-      CT aq[NCH], ad[NCH];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rr = 4 * j + i;
+      lv[i] = __builtin_huge_valf();
+      dvv[i] = 0.f;
+      gv[i] = 0.f;
+      if (rr < qrows) {
+        const long long row = bh * N + qr0 + rr;
+        lv[i] = lse_log2(qt.lse[row]);
+        gv[i] = sigmoidf(qt.gate[((size_t)b * N + qr0 + rr) * 3 + qt.br]);
+        dvv[i] = gv[i] * qt.R[row];
+      }
+    }
+  };
+  if (wid < nwork) fetch(wid);
+  for (int item = wid; item < nwork; item += 4) {
+    CT cq[NCH], cd[NCH];
+    float cl[4], cdv[4], cg[4];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) { cq[c] = aq[c]; cd[c] = ad[c]; }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { cl[i] = lv[i]; cdv[i] = dvv[i]; cg[i] = gv[i]; }
+    if (item + 4 < nwork) fetch(item + 4);   // next item in flight
+    // Q^T and dO^T of the 16 queries, written from the row fragments this lane holds
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        qtr[(32 * c + 8 * j + e) * TSTR + r] = chunk_elem(cq[c], e);
+        dtr[(32 * c + 8 * j + e) * TSTR + r] = chunk_elem(cd[c], e);
+      }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int kb = 0; kb < KBW; ++kb) {
+      f32x4 sv = f32x4{0.f, 0.f, 0.f, 0.f}, dp = sv;
 #pragma unroll
       for (int c = 0; c < NCH; ++c) {
-        aq[c] = zero_chunk(aq[c]);
-        ad[c] = zero_chunk(ad[c]);
-        if (rok) {
-          aq[c] = load_chunk(qh + (size_t)(qr0 + r) * HD + 32 * c + 8 * j);
-          ad[c] = load_chunk(dh + (size_t)(qr0 + r) * HD + 32 * c + 8 * j);
-        }
+        sv = mma(cq[c], kf[kb][c], sv);
+        dp = mma(cd[c], vf[kb][c], dp);
       }
-      // per-query terms of the rows 4j+i this lane holds
-      float lv[4], dvv[4], gv[4];
+      float pg[4], dsv[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int rr = 4 * j + i;
-        lv[i] = __builtin_huge_valf();
-        dvv[i] = 0.f;
-        gv[i] = 0.f;
-        if (rr < qrows) {
-          const long long row = bh * N + qr0 + rr;
-          lv[i] = lse_log2(qt.lse[row]);
-          gv[i] = sigmoidf(qt.gate[((size_t)b * N + qr0 + rr) * 3 + qt.br]);
-          dvv[i] = gv[i] * qt.R[row];
-        }
+        const float pr = kok[kb] ? fast_exp2(__builtin_fmaf(sv[i], sl2, -cl[i])) : 0.f;
+        pg[i] = pr * cg[i];
+        dsv[i] = pr * __builtin_fmaf(dp[i], cg[i], -cdv[i]);
       }
 #pragma unroll
-      for (int kb = 0; kb < KBW; ++kb) {
-        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f}, dp = s;
+      for (int db = 0; db < DB; ++db) {
+        const T* pd = &dtr[(16 * db + r) * TSTR + 4 * j];
+        const T* pq = &qtr[(16 * db + r) * TSTR + 4 * j];
+        float ao[4], aqv[4];
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-          s = mma(aq[c], kf[kb][c], s);
-          dp = mma(ad[c], vf[kb][c], dp);
-        }
-        float pg[4], dsv[4];
+        for (int i = 0; i < 4; ++i) { ao[i] = to_f32<T>(pd[i]); aqv[i] = to_f32<T>(pq[i]); }
+        dva[kb][db] = mma16(ao, pg, dva[kb][db], T(0));
+        dka[kb][db] = mma16(aqv, dsv, dka[kb][db], T(0));
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  // fixed-order sum of the four waves' partials: wave 0 accumulates waves 1, 2, 3
+  for (int w = 1; w < 4; ++w) {
+    __syncthreads();
+    if (wid == w) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float pr = kok[kb] ? fast_exp2(__builtin_fmaf(s[i], sl2, -lv[i])) : 0.f;
-          pg[i] = pr * gv[i];
-          dsv[i] = pr * __builtin_fmaf(dp[i], gv[i], -dvv[i]);
-        }
+      for (int kb = 0; kb < KBW; ++kb)
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const T* pd = &dtr[(16 * db + r) * TSTR + 4 * j];
-          const T* pq = &qtr[(16 * db + r) * TSTR + 4 * j];
-          float ao[4], aqv[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) { ao[i] = to_f32<T>(pd[i]); aqv[i] = to_f32<T>(pq[i]); }
-          dva[kb][db] = mma16(ao, pg, dva[kb][db], T(0));
-          dka[kb][db] = mma16(aqv, dsv, dka[kb][db], T(0));
+          const int o = (16 * kb + r) * HD + 16 * db + 4 * j;
+          *reinterpret_cast<f32x4*>(&red[0][o]) = dka[kb][db];
+          *reinterpret_cast<f32x4*>(&red[1][o]) = dva[kb][db];
         }
-      }
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    __syncthreads();
+    if (wid == 0) {
+#pragma unroll
+      for (int kb = 0; kb < KBW; ++kb)
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const int o = (16 * kb + r) * HD + 16 * db + 4 * j;
+          dka[kb][db] += *reinterpret_cast<const f32x4*>(&red[0][o]);
+          dva[kb][db] += *reinterpret_cast<const f32x4*>(&red[1][o]);
+        }
     }
   }
+  if (wid != 0) return;
 #pragma unroll
   for (int kb = 0; kb < KBW; ++kb) {
     const size_t off = ((size_t)bh * N + blk * ls + 16 * kb + r) * HD;
@@ -694,7 +741,7 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
   const int nct = D.N / D.l;
   // per-branch row sums and the gate gradient
   BSA_PHASE("bwd.gate", st, {
-  hipLaunchKernelGGL(gate_bwd_rows_kernel<T>, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, st, (const T*)A.dout,
+  hipLaunchKernelGGL(gate_bwd_rows_kernel<T>, dim3((unsigned)((rows * 8 + 255) / 256)), dim3(256), 0, st, (const T*)A.dout,
                      (const T*)A.o_branch, rows, HD, A.R);
   hipLaunchKernelGGL(gate_bwd_kernel, dim3((D.B * D.N + 255) / 256), dim3(256), 0, st, A.R, A.gate, A.valid, D.B, D.H,
                      D.N, A.dgate);
@@ -766,7 +813,7 @@ hipError_t slc_kv_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
   QTerms qslc{A.lse + 2 * rows, A.R + 2 * rows, A.gate, 2};
   const long long nseg = (long long)D.B * D.H * (D.N / D.ls);
   const int kbw = D.ls / 16;
-  const dim3 grid((unsigned)((nseg + 3) / 4));
+  const dim3 grid((unsigned)nseg);
   const T* q = (const T*)A.q;
   const T* k = (const T*)A.k;
   const T* v = (const T*)A.v;

@@ -70,6 +70,14 @@ template <> __device__ __forceinline__ f32x8 make_chunk<float>(const float* v) {
   return r;
 }
 
+// Element e of a chunk as its storage bits (e must fold to a constant).
+__device__ __forceinline__ bf16_t chunk_elem(const bf16x8& c, int e) {
+  const uint4 u = __builtin_bit_cast(uint4, c);
+  const uint32_t w = e < 2 ? u.x : (e < 4 ? u.y : (e < 6 ? u.z : u.w));
+  return (bf16_t)((w >> (16 * (e & 1))) & 0xFFFFu);
+}
+__device__ __forceinline__ float chunk_elem(const f32x8& c, int e) { return c[e]; }
+
 __device__ __forceinline__ bf16x8 zero_chunk(bf16x8) { return bf16x8{}; }
 __device__ __forceinline__ f32x8 zero_chunk(f32x8) { return f32x8{}; }
 

@@ -177,9 +177,11 @@ __device__ __forceinline__ float gelu_erf_grad(float x) {
 }
 
 // One wave per 16 rows: dpre (stored), and dx = dpre W1^T added into the token gradients.
-template <int HD>
+// The dx product runs in the storage type (bf16 MFMA for bf16 layers; W1 holds
+// bf16-representable values there), the rest in f32.
+template <typename T, int HD>
 __global__ void __launch_bounds__(256) mlp_bwd_rows_kernel(const float* dy, const float* pre, const uint8_t* valid,
-                                                           int H, int N, int l, long long rows, const float* w1,
+                                                           int H, int N, int l, long long rows, const T* w1,
                                                            const float* w2, float* dpre_out, float* dx_accum) {
   constexpr int NCH = HD / 32, OB = HD / 16;
   __shared__ float w2s[HD * (HD + 4)];
@@ -219,9 +221,9 @@ __global__ void __launch_bounds__(256) mlp_bwd_rows_kernel(const float* dy, cons
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   // dx^T[i][row] = sum_o W1[i][o] dpre[row][o]; A = W1 rows (i), B = dpre^T
-  f32x8 bd[NCH];
+  typename Chunk<T>::type bd[NCH];
 #pragma unroll
-  for (int c = 0; c < NCH; ++c) bd[c] = *reinterpret_cast<const f32x8*>(&dps[r * (HD + 4) + 32 * c + 8 * j]);
+  for (int c = 0; c < NCH; ++c) bd[c] = make_chunk<T>(&dps[r * (HD + 4) + 32 * c + 8 * j]);
   const int ld = l * HD;
   const int nblk = N / l;
   long long bhh = rok ? row / nblk : 0;
@@ -241,6 +243,12 @@ __global__ void __launch_bounds__(256) mlp_bwd_rows_kernel(const float* dy, cons
       *reinterpret_cast<float4*>(dst) = o;
     }
   }
+}
+
+template <typename T>
+__global__ void cast_w_kernel(const float* x, int n, T* y) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) y[i] = from_f32<T>(x[i]);
 }
 
 // dW1 partials: workgroup = (64 flattened inputs i, row chunk); wave w owns i in [16w, 16w+16).
@@ -398,23 +406,29 @@ hipError_t compress_bwd_impl(const Dims& D, const void* x, const uint8_t* valid,
                        D.l, HD, rows, dx_accum);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL((mlp_bwd_rows_kernel<HD>), dim3((unsigned)((rows + 63) / 64)), dim3(256), 0, st, dy, pre, valid,
-                     D.H, D.N, D.l, rows, phi.w1, phi.w2, ws.dpre, dx_accum);
   const int ld = D.l * HD;
+  const T* w1 = (const T*)phi.w1;
+  if (sizeof(T) == 2) {
+    hipLaunchKernelGGL(cast_w_kernel<T>, dim3((ld * HD + 255) / 256), dim3(256), 0, st, phi.w1, ld * HD, (T*)ws.w1_lp);
+    w1 = (const T*)ws.w1_lp;
+  }
+  hipLaunchKernelGGL((mlp_bwd_rows_kernel<T, HD>), dim3((unsigned)((rows + 63) / 64)), dim3(256), 0, st, dy, pre, valid,
+                     D.H, D.N, D.l, rows, w1, phi.w2, ws.dpre, dx_accum);
   const long long rpc = ((rows + ws.chunks - 1) / ws.chunks + 31) / 32 * 32;
   hipLaunchKernelGGL((mlp_bwd_w1_kernel<T, HD>), dim3(ld / 64, ws.chunks), dim3(256), 0, st, (const T*)x, valid, ws.dpre,
                      D.H, D.N, D.l, rows, rpc, ws.part_w1);
-  hipLaunchKernelGGL((mlp_bwd_small_kernel<HD>), dim3(ws.chunks), dim3(256), 0, st, dy, pre, ws.dpre, rows, rpc,
+  const long long rps = ((rows + ws.chunks_small - 1) / ws.chunks_small + 31) / 32 * 32;
+  hipLaunchKernelGGL((mlp_bwd_small_kernel<HD>), dim3(ws.chunks_small), dim3(256), 0, st, dy, pre, ws.dpre, rows, rps,
                      ws.part_small);
   const long long n1 = (long long)ld * HD;
   hipLaunchKernelGGL(sum_parts_kernel, dim3((unsigned)((n1 + 255) / 256)), dim3(256), 0, st, ws.part_w1, ws.chunks, n1,
                      n1, grad.w1);
   const long long ss = (long long)HD * HD + 2 * HD;
-  hipLaunchKernelGGL(sum_parts_kernel, dim3((HD * HD + 255) / 256), dim3(256), 0, st, ws.part_small, ws.chunks,
+  hipLaunchKernelGGL(sum_parts_kernel, dim3((HD * HD + 255) / 256), dim3(256), 0, st, ws.part_small, ws.chunks_small,
                      (long long)HD * HD, ss, grad.w2);
-  hipLaunchKernelGGL(sum_parts_kernel, dim3(1), dim3(256), 0, st, ws.part_small + HD * HD, ws.chunks, (long long)HD, ss,
-                     grad.b1);
-  hipLaunchKernelGGL(sum_parts_kernel, dim3(1), dim3(256), 0, st, ws.part_small + HD * HD + HD, ws.chunks,
+  hipLaunchKernelGGL(sum_parts_kernel, dim3(1), dim3(256), 0, st, ws.part_small + HD * HD, ws.chunks_small,
+                     (long long)HD, ss, grad.b1);
+  hipLaunchKernelGGL(sum_parts_kernel, dim3(1), dim3(256), 0, st, ws.part_small + HD * HD + HD, ws.chunks_small,
                      (long long)HD, ss, grad.b2);
   return hipGetLastError();
 }
@@ -445,6 +459,14 @@ hipError_t launch_block_valid(const Dims& D, const uint8_t* valid, uint8_t* cval
   const int total = D.B * (D.N / D.l);
   hipLaunchKernelGGL(block_valid_kernel, dim3((total + 255) / 256), dim3(256), 0, st, valid, total, D.l, cvalid);
   return hipGetLastError();
+}
+
+int mlp_bwd_chunks_small(const Dims& D) {
+  const long long rows = D.cmp_rows();
+  long long c = rows / 128;
+  if (c < 1) c = 1;
+  if (c > 256) c = 256;
+  return (int)c;
 }
 
 int mlp_bwd_chunks(const Dims& D) {

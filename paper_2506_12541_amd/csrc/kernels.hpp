@@ -80,10 +80,12 @@ hipError_t launch_slc_csr(const Dims& D, const BwdArgs& A, hipStream_t st);
 struct MlpBwdWs {
   float* dpre;        // [rows, d]
   float* part_w1;     // [chunks, l*d, d]
-  float* part_small;  // [chunks, d*d + 2d]
-  int chunks;
+  float* part_small;  // [chunks_small, d*d + 2d]
+  void* w1_lp;        // [l*d, d] W1 in the storage type
+  int chunks, chunks_small;
 };
 int mlp_bwd_chunks(const Dims& D);
+int mlp_bwd_chunks_small(const Dims& D);
 hipError_t launch_compress_bwd(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi, const float* pre,
                                const float* dy, float* dx_accum, const MlpGrad& grad, const MlpBwdWs& ws,
                                hipStream_t st);

@@ -443,6 +443,38 @@ __global__ void unpermute_kernel(const T* src, const int* perm, int n_real, int 
   if (p >= 0) dst[((size_t)b * n_real + p) * heads * hd + (size_t)h * hd + c] = src[i];
 }
 
+// 16-byte variant: one work item moves one 16-byte piece of a head row.
+__global__ void permute16_kernel(const uint4* src, const int* perm, int n_real, int n_pad, int heads, int vpr,
+                                 uint4* dst, uint8_t* valid, size_t total) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  int c = (int)(i % vpr);
+  size_t r = i / vpr;
+  int s = (int)(r % n_pad);
+  r /= n_pad;
+  int h = (int)(r % heads);
+  int b = (int)(r / heads);
+  int p = perm[(size_t)b * n_pad + s];
+  uint4 val = make_uint4(0, 0, 0, 0);
+  if (p >= 0) val = src[((size_t)b * n_real + p) * heads * vpr + (size_t)h * vpr + c];
+  dst[i] = val;
+  if (valid && h == 0 && c == 0) valid[(size_t)b * n_pad + s] = p >= 0;
+}
+
+__global__ void unpermute16_kernel(const uint4* src, const int* perm, int n_real, int n_pad, int heads, int vpr,
+                                   uint4* dst, size_t total) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  int c = (int)(i % vpr);
+  size_t r = i / vpr;
+  int s = (int)(r % n_pad);
+  r /= n_pad;
+  int h = (int)(r % heads);
+  int b = (int)(r / heads);
+  int p = perm[(size_t)b * n_pad + s];
+  if (p >= 0) dst[((size_t)b * n_real + p) * heads * vpr + (size_t)h * vpr + c] = src[i];
+}
+
 inline int ilog2(int64_t x) {
   int r = 0;
   while ((int64_t(1) << r) < x) ++r;
@@ -545,6 +577,19 @@ hipError_t launch_radix_sort_pairs(uint32_t* keys, uint32_t* vals, uint32_t* key
 hipError_t launch_permute(const void* src, const int* perm, int64_t n_real, int64_t n_pad, int batch,
                           int heads, int hd, int dtype, void* dst, uint8_t* valid, bool inverse,
                           hipStream_t st) {
+  const size_t esz = dtype == 0 ? 4 : 2;
+  if ((hd * esz) % 16 == 0) {
+    const int vpr = (int)(hd * esz / 16);
+    const size_t total = (size_t)batch * heads * n_pad * vpr;
+    const unsigned blocks = (unsigned)((total + 255) / 256);
+    if (!inverse)
+      hipLaunchKernelGGL(permute16_kernel, dim3(blocks), dim3(256), 0, st, (const uint4*)src, perm, (int)n_real,
+                         (int)n_pad, heads, vpr, (uint4*)dst, valid, total);
+    else
+      hipLaunchKernelGGL(unpermute16_kernel, dim3(blocks), dim3(256), 0, st, (const uint4*)src, perm, (int)n_real,
+                         (int)n_pad, heads, vpr, (uint4*)dst, total);
+    return hipGetLastError();
+  }
   const size_t total = (size_t)batch * heads * n_pad * hd;
   const unsigned blocks = (unsigned)((total + 255) / 256);
   if (!inverse) {
