@@ -64,6 +64,8 @@ bsa_status_t check_params(const bsa_params_t* p, bsa::Dims* D) {
   if (p->kv_pool == BSA_POOL_MLP && (p->cmp_block * p->head_dim) % 64 != 0)
     return fail(BSA_ERR_UNSUPPORTED, "MLP pooling needs cmp_block * head_dim to be a multiple of 64");
   if (p->dtype != BSA_F32 && p->dtype != BSA_BF16) return fail(BSA_ERR_INVALID_ARGUMENT, "bad dtype");
+  if (p->dtype == BSA_F32 && p->head_dim != 32)
+    return fail(BSA_ERR_UNSUPPORTED, "float32 layers support head_dim 32 (bf16 layers: 32 and 64)");
   if (!(p->softmax_scale >= 0.0f) || std::isinf(p->softmax_scale))
     return fail(BSA_ERR_INVALID_ARGUMENT, "softmax_scale must be finite and >= 0");
   D->B = p->batch;
@@ -332,7 +334,8 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
            "select");
   BSA_STEP("fwd.ball", bsa::launch_ball_fwd(D, q, k, v, valid, ob, saved->lse, st), "ball attention");
   BSA_STEP("fwd.cmp",
-           bsa::launch_cmp_fwd(D, q, kc_lp, vc_lp, valid, saved->cvalid, ob + ob_stride, saved->lse + rows, st),
+           bsa::launch_cmp_fwd(D, q, kc_lp, vc_lp, valid, valid ? saved->cvalid : nullptr, ob + ob_stride,
+                               saved->lse + rows, st),
            "compressed attention");
   BSA_STEP("fwd.slc",
            bsa::launch_slc_fwd(D, q, k, v, valid, saved->sel_idx, ob + 2 * ob_stride, saved->lse + 2 * rows, st),

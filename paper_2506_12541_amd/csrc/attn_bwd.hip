@@ -103,14 +103,14 @@ __global__ void __launch_bounds__(256) dense_bwd_q_kernel(const T* q, const T* k
                                                           const uint8_t* kvalid_all, QTerms qt, int H, int N,
                                                           int nkeys_total, int m, float sl2, float scale, float* dq) {
   constexpr int NCH = HD / 32, DB = HD / 16;
+  constexpr int KT = 64;   // keys per staged tile
   constexpr int KSTR = HD + 16 / (int)sizeof(T);
-  constexpr int VSTR = kKT + 4;
-  constexpr int EPV = 16 / (int)sizeof(T);
+  constexpr int VSTR = KT + 4;
   typedef typename Chunk<T>::type CT;
-  __shared__ __attribute__((aligned(16))) T ks[kKT * KSTR];
-  __shared__ __attribute__((aligned(16))) T vs[kKT * KSTR];
+  __shared__ __attribute__((aligned(16))) T ks[KT * KSTR];
+  __shared__ __attribute__((aligned(16))) T vs[KT * KSTR];
   __shared__ __attribute__((aligned(16))) T kt[HD * VSTR];
-  __shared__ uint8_t kok[kKT];
+  __shared__ __attribute__((aligned(16))) uint8_t kok[KT];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r = lane & 15, j = lane >> 4;
   const int b = blockIdx.z, h = blockIdx.y;
@@ -141,79 +141,79 @@ __global__ void __launch_bounds__(256) dense_bwd_q_kernel(const T* q, const T* k
     for (int db = 0; db < DB; ++db) acc[qb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  for (int t0 = 0; t0 < nkeys; t0 += kKT) {
+  typedef TileIO<T, HD, KT> IO;
+  uint4 kreg[IO::RV], vreg[IO::RV];
+  typename IO::V4 treg[IO::TV][4];
+  IO::load_rows(kreg, kh, 0, nkeys);
+  IO::load_rows(vreg, vh, 0, nkeys);
+  IO::load_tr(treg, kh, 0, nkeys);
+  for (int t0 = 0; t0 < nkeys; t0 += KT) {
     __syncthreads();
-    for (int e = threadIdx.x; e < kKT * HD / EPV; e += 256) {
-      const int row = e / (HD / EPV), col = (e % (HD / EPV)) * EPV;
-      uint4 kv = make_uint4(0, 0, 0, 0), vv = kv;
-      if (t0 + row < nkeys) {
-        kv = *reinterpret_cast<const uint4*>(kh + (size_t)(t0 + row) * HD + col);
-        vv = *reinterpret_cast<const uint4*>(vh + (size_t)(t0 + row) * HD + col);
-      }
-      *reinterpret_cast<uint4*>(&ks[row * KSTR + col]) = kv;
-      *reinterpret_cast<uint4*>(&vs[row * KSTR + col]) = vv;
-    }
-    for (int e = threadIdx.x; e < (kKT / 4) * (HD / 8); e += 256) {
-      const int kq = e / (HD / 8), dc = (e % (HD / 8)) * 8;
-      const T* rows[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int key = t0 + 4 * kq + u;
-        rows[u] = key < nkeys ? kh + (size_t)key * HD : nullptr;
-      }
-      stage_vt(rows, dc, kt, VSTR, 4 * kq);
-    }
-    if (threadIdx.x < kKT) {
+    IO::store_rows(kreg, ks, KSTR);
+    IO::store_rows(vreg, vs, KSTR);
+    IO::store_tr(treg, kt, VSTR);
+    if (threadIdx.x < KT) {
       const int key = t0 + threadIdx.x;
       kok[threadIdx.x] = key < nkeys && (kval == nullptr || kval[key]);
     }
     __syncthreads();
-    constexpr int KB = kKT / 16;
-    f32x4 s[QB][KB], dp[QB][KB];
+    if (t0 + KT < nkeys) {
+      IO::load_rows(kreg, kh, t0 + KT, nkeys);
+      IO::load_rows(vreg, vh, t0 + KT, nkeys);
+      IO::load_tr(treg, kh, t0 + KT, nkeys);
+    }
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
+    for (int half = 0; half < KT / kKT; ++half) {
+      const int h0 = half * kKT;
+      if (t0 + h0 >= nkeys) break;
+      constexpr int KB = kKT / 16;
+      const bool all_ok = kval == nullptr && t0 + h0 + kKT <= nkeys;
+      // key validity of the rows 4j+i of each key block, one 32-bit word per block
+      uint32_t okw[KB];
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) { s[qb][kb] = f32x4{0.f, 0.f, 0.f, 0.f}; dp[qb][kb] = s[qb][kb]; }
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        CT ak = load_chunk(&ks[(kb * 16 + r) * KSTR + 32 * c + 8 * j]);
-        CT av = load_chunk(&vs[(kb * 16 + r) * KSTR + 32 * c + 8 * j]);
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-          s[qb][kb] = mma(ak, qf[qb][c], s[qb][kb]);
-          dp[qb][kb] = mma(av, df[qb][c], dp[qb][kb]);
-        }
-      }
-    CT dsf[QB][KB / 2];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      float v8[KB][4];
+      for (int kb = 0; kb < KB; ++kb) okw[kb] = all_ok ? 0x01010101u : *reinterpret_cast<const uint32_t*>(&kok[h0 + kb * 16 + 4 * j]);
+      f32x4 sv[QB][KB], dp[QB][KB];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const bool ok = kok[kb * 16 + 4 * j + i] != 0;
-          const float p = ok ? fast_exp2(__builtin_fmaf(s[qb][kb][i], sl2, -l2[qb])) : 0.f;
-          v8[kb][i] = p * __builtin_fmaf(dp[qb][kb][i], gs[qb], -dd[qb]);
+        for (int c = 0; c < NCH; ++c) {
+          CT ak = load_chunk(&ks[(h0 + kb * 16 + r) * KSTR + 32 * c + 8 * j]);
+          CT av = load_chunk(&vs[(h0 + kb * 16 + r) * KSTR + 32 * c + 8 * j]);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) {
+            sv[qb][kb] = mma(ak, qf[qb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sv[qb][kb]);
+            dp[qb][kb] = mma(av, df[qb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : dp[qb][kb]);
+          }
         }
+      CT dsf[QB][KB / 2];
 #pragma unroll
-      for (int kp = 0; kp < KB / 2; ++kp) {
-        float w8[8];
+      for (int qb = 0; qb < QB; ++qb) {
+        float v8[KB][4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) { w8[i] = v8[2 * kp][i]; w8[4 + i] = v8[2 * kp + 1][i]; }
-        dsf[qb][kp] = make_chunk<T>(w8);
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float e = fast_exp2(__builtin_fmaf(sv[qb][kb][i], sl2, -l2[qb]));
+            const float p = ((okw[kb] >> (8 * i)) & 1u) ? e : 0.f;
+            v8[kb][i] = p * __builtin_fmaf(dp[qb][kb][i], gs[qb], -dd[qb]);
+          }
+#pragma unroll
+        for (int kp = 0; kp < KB / 2; ++kp) {
+          float w8[8];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) { w8[i] = v8[2 * kp][i]; w8[4 + i] = v8[2 * kp + 1][i]; }
+          dsf[qb][kp] = make_chunk<T>(w8);
+        }
       }
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int kp = 0; kp < KB / 2; ++kp) {
+          CT a = load_4x2(&kt[(16 * db + r) * VSTR + h0 + 32 * kp + 4 * j]);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) acc[qb][db] = mma(a, dsf[qb][kp], acc[qb][db]);
+        }
     }
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int kp = 0; kp < KB / 2; ++kp) {
-        CT a = load_4x2(&kt[(16 * db + r) * VSTR + 32 * kp + 4 * j]);
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) acc[qb][db] = mma(a, dsf[qb][kp], acc[qb][db]);
-      }
   }
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
@@ -244,7 +244,6 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
   constexpr int NCH = HD / 32, DB = HD / 16;
   constexpr int QSTR = HD + 16 / (int)sizeof(T);
   constexpr int TSTR = kQT + 4;
-  constexpr int EPV = 16 / (int)sizeof(T);
   constexpr int KBW = 2;  // 16-key blocks per wave
   typedef typename Chunk<T>::type CT;
   __shared__ __attribute__((aligned(16))) T qs[kQT * QSTR];
@@ -259,7 +258,6 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
   const int chunk = blockIdx.y;
   const int key0 = blockIdx.x * (NW * 32);
   const int wk0 = key0 + wid * 32;
-  // query range of this workgroup
   int qbeg, qend;
   if (BALL) {
     qbeg = (key0 / m) * m;
@@ -295,81 +293,78 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
 #pragma unroll
     for (int db = 0; db < DB; ++db) { dka[kb][db] = f32x4{0.f, 0.f, 0.f, 0.f}; dva[kb][db] = dka[kb][db]; }
 
+  // query tiles: row-major Q, dO and transposed Q^T, dO^T, prefetched one tile ahead
+  typedef TileIO<T, HD, kQT, NW * 64> IO;
+  uint4 qreg[IO::RV], dreg[IO::RV];
+  typename IO::V4 qtreg[IO::TV][4], dtreg[IO::TV][4];
+  float tl = 0.f, tg = 0.f, tr = 0.f;
+  auto fetch = [&](int t0) {
+    IO::load_rows(qreg, qh, t0, N);
+    IO::load_rows(dreg, dh, t0, N);
+    IO::load_tr(qtreg, qh, t0, N);
+    IO::load_tr(dtreg, dh, t0, N);
+    if (threadIdx.x < kQT) {
+      const long long row = rowbase + t0 + threadIdx.x;
+      tl = qt.lse[row];
+      tg = qt.gate[((size_t)b * N + t0 + threadIdx.x) * 3 + qt.br];
+      tr = qt.R[row];
+    }
+  };
+  fetch(qbeg);
   for (int t0 = qbeg; t0 < qend; t0 += kQT) {
     __syncthreads();
-    for (int e = threadIdx.x; e < kQT * HD / EPV; e += NW * 64) {
-      const int row = e / (HD / EPV), col = (e % (HD / EPV)) * EPV;
-      *reinterpret_cast<uint4*>(&qs[row * QSTR + col]) =
-          *reinterpret_cast<const uint4*>(qh + (size_t)(t0 + row) * HD + col);
-      *reinterpret_cast<uint4*>(&ds_[row * QSTR + col]) =
-          *reinterpret_cast<const uint4*>(dh + (size_t)(t0 + row) * HD + col);
-    }
-    for (int e = threadIdx.x; e < 2 * (kQT / 4) * (HD / 8); e += NW * 64) {
-      const int which = e / ((kQT / 4) * (HD / 8));
-      const int ee = e % ((kQT / 4) * (HD / 8));
-      const int kq = ee / (HD / 8), dc = (ee % (HD / 8)) * 8;
-      const T* base = which ? dh : qh;
-      const T* rows[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) rows[u] = base + (size_t)(t0 + 4 * kq + u) * HD;
-      stage_vt(rows, dc, which ? dtr : qtr, TSTR, 4 * kq);
-    }
-    for (int e = threadIdx.x; e < kQT; e += NW * 64) {
-      const long long row = rowbase + t0 + e;
-      const float g = sigmoidf(qt.gate[((size_t)b * N + t0 + e) * 3 + qt.br]);
-      l2s[e] = lse_log2(qt.lse[row]);
-      gss[e] = g;
-      dds[e] = g * qt.R[row];
+    IO::store_rows(qreg, qs, QSTR);
+    IO::store_rows(dreg, ds_, QSTR);
+    IO::store_tr(qtreg, qtr, TSTR);
+    IO::store_tr(dtreg, dtr, TSTR);
+    if (threadIdx.x < kQT) {
+      const float g = sigmoidf(tg);
+      l2s[threadIdx.x] = lse_log2(tl);
+      gss[threadIdx.x] = g;
+      dds[threadIdx.x] = g * tr;
     }
     __syncthreads();
-    constexpr int QBT = kQT / 16;
-    f32x4 s[QBT][KBW], dp[QBT][KBW];
+    if (t0 + kQT < qend) fetch(t0 + kQT);
 #pragma unroll
-    for (int qb = 0; qb < QBT; ++qb)
+    for (int qp = 0; qp < kQT / 32; ++qp) {
+      f32x4 sv[2][KBW], dp[2][KBW];
 #pragma unroll
-      for (int kb = 0; kb < KBW; ++kb) { s[qb][kb] = f32x4{0.f, 0.f, 0.f, 0.f}; dp[qb][kb] = s[qb][kb]; }
+      for (int u = 0; u < 2; ++u) {
+        const int qb = 2 * qp + u;
 #pragma unroll
-    for (int qb = 0; qb < QBT; ++qb)
+        for (int c = 0; c < NCH; ++c) {
+          CT aq = load_chunk(&qs[(16 * qb + r) * QSTR + 32 * c + 8 * j]);
+          CT ad = load_chunk(&ds_[(16 * qb + r) * QSTR + 32 * c + 8 * j]);
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        CT aq = load_chunk(&qs[(16 * qb + r) * QSTR + 32 * c + 8 * j]);
-        CT ad = load_chunk(&ds_[(16 * qb + r) * QSTR + 32 * c + 8 * j]);
-#pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) {
-          s[qb][kb] = mma(aq, kf[kb][c], s[qb][kb]);
-          dp[qb][kb] = mma(ad, vf[kb][c], dp[qb][kb]);
+          for (int kb = 0; kb < KBW; ++kb) {
+            sv[u][kb] = mma(aq, kf[kb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sv[u][kb]);
+            dp[u][kb] = mma(ad, vf[kb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : dp[u][kb]);
+          }
         }
       }
-    // lane holds queries 16qb + 4j + i for its key
-    float pg[QBT][KBW][4], dsv[QBT][KBW][4];
-#pragma unroll
-    for (int qb = 0; qb < QBT; ++qb) {
-      const float4 L = *reinterpret_cast<const float4*>(&l2s[16 * qb + 4 * j]);
-      const float4 Dd = *reinterpret_cast<const float4*>(&dds[16 * qb + 4 * j]);
-      const float4 G = *reinterpret_cast<const float4*>(&gss[16 * qb + 4 * j]);
-      const float lv[4] = {L.x, L.y, L.z, L.w}, dv4[4] = {Dd.x, Dd.y, Dd.z, Dd.w}, gv[4] = {G.x, G.y, G.z, G.w};
-#pragma unroll
-      for (int kb = 0; kb < KBW; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float p = kok[kb] ? fast_exp2(__builtin_fmaf(s[qb][kb][i], sl2, -lv[i])) : 0.f;
-          pg[qb][kb][i] = p * gv[i];
-          dsv[qb][kb][i] = p * __builtin_fmaf(dp[qb][kb][i], gv[i], -dv4[i]);
-        }
-    }
-#pragma unroll
-    for (int qp = 0; qp < QBT / 2; ++qp) {
+      // lane holds queries 16qb + 4j + i for its key
       CT pf[KBW], sf[KBW];
+      float a8[KBW][8], b8[KBW][8];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int qb = 2 * qp + u;
+        const float4 L = *reinterpret_cast<const float4*>(&l2s[16 * qb + 4 * j]);
+        const float4 Dd = *reinterpret_cast<const float4*>(&dds[16 * qb + 4 * j]);
+        const float4 G = *reinterpret_cast<const float4*>(&gss[16 * qb + 4 * j]);
+        const float lv[4] = {L.x, L.y, L.z, L.w}, dv4[4] = {Dd.x, Dd.y, Dd.z, Dd.w}, gv[4] = {G.x, G.y, G.z, G.w};
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float p = kok[kb] ? fast_exp2(__builtin_fmaf(sv[u][kb][i], sl2, -lv[i])) : 0.f;
+            a8[kb][4 * u + i] = p * gv[i];
+            b8[kb][4 * u + i] = p * __builtin_fmaf(dp[u][kb][i], gv[i], -dv4[i]);
+          }
+      }
 #pragma unroll
       for (int kb = 0; kb < KBW; ++kb) {
-        float a8[8], b8[8];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          a8[i] = pg[2 * qp][kb][i]; a8[4 + i] = pg[2 * qp + 1][kb][i];
-          b8[i] = dsv[2 * qp][kb][i]; b8[4 + i] = dsv[2 * qp + 1][kb][i];
-        }
-        pf[kb] = make_chunk<T>(a8);
-        sf[kb] = make_chunk<T>(b8);
+        pf[kb] = make_chunk<T>(a8[kb]);
+        sf[kb] = make_chunk<T>(b8[kb]);
       }
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
@@ -776,7 +771,7 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
   });
   BSA_PHASE("bwd.dq_cmp", st,
   hipLaunchKernelGGL((dense_bwd_q_kernel<T, HD, 2, false, true>), dim3(D.N / 128, D.H, D.B), dim3(256), 0, st, q, kc,
-                     vc, dout, A.cvalid, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq));
+                     vc, dout, A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq));
   BSA_PHASE("bwd.dq_slc", st,
   hipLaunchKernelGGL((slc_bwd_q_kernel<T, HD>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, q, k, v, dout, A.valid,
                      A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq));
@@ -795,7 +790,8 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
     const int nch = D.N / kCmpChunks >= kQT ? kCmpChunks : 1;
     BSA_PHASE("bwd.kv_cmp", st,
     hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, 4, false>), dim3((nct + 127) / 128, nch, D.B * D.H), dim3(256), 0,
-                       st, q, kc, vc, dout, A.cvalid, qcmp, D.H, D.N, nct, D.m, nch, sl2, D.scale, A.dkc_part,
+                       st, q, kc, vc, dout, A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, nch, sl2,
+                       D.scale, A.dkc_part,
                        A.dvc_part));
     const long long n = D.cmp_rows() * HD;
     hipLaunchKernelGGL(sum_chunks_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.dkc_part, nch, n,

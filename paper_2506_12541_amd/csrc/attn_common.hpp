@@ -84,18 +84,28 @@ template <typename T> struct Vec4T;
 template <> struct Vec4T<bf16_t> { typedef uint2 type; };
 template <> struct Vec4T<float> { typedef float4 type; };
 
-template <typename T, int HD, int ROWS = kKT>
+template <typename T, int HD, int ROWS = kKT, int NT = 256>
 struct TileIO {
   static constexpr int VPR = HD * (int)sizeof(T) / 16;           // 16-byte vectors per row
-  static constexpr int RV = (ROWS * VPR + 255) / 256;            // row vectors per thread
+  static constexpr int RV = (ROWS * VPR + NT - 1) / NT;          // row vectors per thread
   static constexpr int TI = (ROWS / 4) * (HD / 4);               // transposed 4x4 items
-  static constexpr int TV = (TI + 255) / 256;                    // transposed items per thread
+  static constexpr int TV = (TI + NT - 1) / NT;                  // transposed items per thread
   typedef typename Vec4T<T>::type V4;
 
   __device__ static void load_rows(uint4 (&r)[RV], const T* base, int t0, int nrows) {
+    if (t0 + ROWS <= nrows) {   // full tile (uniform): no per-load bounds checks
+#pragma unroll
+      for (int u = 0; u < RV; ++u) {
+        const int e = threadIdx.x + NT * u;
+        const int row = e / VPR, c = (e % VPR) * (16 / (int)sizeof(T));
+        if (ROWS * VPR % NT == 0 || e < ROWS * VPR)
+          r[u] = *reinterpret_cast<const uint4*>(base + (size_t)(t0 + row) * HD + c);
+      }
+      return;
+    }
 #pragma unroll
     for (int u = 0; u < RV; ++u) {
-      const int e = threadIdx.x + 256 * u;
+      const int e = threadIdx.x + NT * u;
       const int row = e / VPR, c = (e % VPR) * (16 / (int)sizeof(T));
       r[u] = make_uint4(0, 0, 0, 0);
       if (e < ROWS * VPR && t0 + row < nrows) r[u] = *reinterpret_cast<const uint4*>(base + (size_t)(t0 + row) * HD + c);
@@ -104,15 +114,28 @@ struct TileIO {
   __device__ static void store_rows(const uint4 (&r)[RV], T* lds, int stride) {
 #pragma unroll
     for (int u = 0; u < RV; ++u) {
-      const int e = threadIdx.x + 256 * u;
+      const int e = threadIdx.x + NT * u;
       const int row = e / VPR, c = (e % VPR) * (16 / (int)sizeof(T));
       if (e < ROWS * VPR) *reinterpret_cast<uint4*>(lds + row * stride + c) = r[u];
     }
   }
   __device__ static void load_tr(V4 (&r)[TV][4], const T* base, int t0, int nrows) {
+    if (t0 + ROWS <= nrows) {   // full tile (uniform): no per-load bounds checks
+#pragma unroll
+      for (int w = 0; w < TV; ++w) {
+        const int it = threadIdx.x + NT * w;
+        const int kq = it / (HD / 4), dq = it % (HD / 4);
+        if (TI % NT == 0 || it < TI) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            r[w][u] = *reinterpret_cast<const V4*>(base + (size_t)(t0 + 4 * kq + u) * HD + 4 * dq);
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int w = 0; w < TV; ++w) {
-      const int it = threadIdx.x + 256 * w;
+      const int it = threadIdx.x + NT * w;
       const int kq = it / (HD / 4), dq = it % (HD / 4);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -125,7 +148,7 @@ struct TileIO {
   __device__ static void store_tr(const V4 (&r)[TV][4], T* lds, int stride) {
 #pragma unroll
     for (int w = 0; w < TV; ++w) {
-      const int it = threadIdx.x + 256 * w;
+      const int it = threadIdx.x + NT * w;
       if (it >= TI) continue;
       const int kq = it / (HD / 4), dq = it % (HD / 4);
       store_tr4(r[w], lds + (4 * dq) * stride + 4 * kq, stride);
