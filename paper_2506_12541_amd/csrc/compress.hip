@@ -370,12 +370,19 @@ __global__ void __launch_bounds__(256) mlp_bwd_small_kernel(const float* dy, con
   }
 }
 
-__global__ void sum_parts_kernel(const float* part, int chunks, long long n, long long stride, float* out) {
-  long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
+// out[i] = sum over chunks of part[c * stride + i]. A workgroup owns 64 outputs; its
+// 4 waves each sum every 4th chunk, then the four partial sums are added in wave order.
+__global__ void __launch_bounds__(256) sum_parts_kernel(const float* part, int chunks, long long n, long long stride,
+                                                        float* out) {
+  __shared__ float red[4][64];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const long long i = (long long)blockIdx.x * 64 + lane;
   float s = 0.f;
-  for (int c = 0; c < chunks; ++c) s += part[(long long)c * stride + i];
-  out[i] = s;
+  if (i < n)
+    for (int c = wid; c < chunks; c += 4) s += part[(long long)c * stride + i];
+  red[wid][lane] = s;
+  __syncthreads();
+  if (wid == 0 && i < n) out[i] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
 }
 
 // Mean pooling backward: every real token of a block receives dy / l.
@@ -421,15 +428,15 @@ hipError_t compress_bwd_impl(const Dims& D, const void* x, const uint8_t* valid,
   hipLaunchKernelGGL((mlp_bwd_small_kernel<HD>), dim3(ws.chunks_small), dim3(256), 0, st, dy, pre, ws.dpre, rows, rps,
                      ws.part_small);
   const long long n1 = (long long)ld * HD;
-  hipLaunchKernelGGL(sum_parts_kernel, dim3((unsigned)((n1 + 255) / 256)), dim3(256), 0, st, ws.part_w1, ws.chunks, n1,
+  hipLaunchKernelGGL(sum_parts_kernel, dim3((unsigned)((n1 + 63) / 64)), dim3(256), 0, st, ws.part_w1, ws.chunks, n1,
                      n1, grad.w1);
   const long long ss = (long long)HD * HD + 2 * HD;
-  hipLaunchKernelGGL(sum_parts_kernel, dim3((HD * HD + 255) / 256), dim3(256), 0, st, ws.part_small, ws.chunks_small,
+  hipLaunchKernelGGL(sum_parts_kernel, dim3((HD * HD + 63) / 64), dim3(256), 0, st, ws.part_small, ws.chunks_small,
                      (long long)HD * HD, ss, grad.w2);
-  hipLaunchKernelGGL(sum_parts_kernel, dim3(1), dim3(256), 0, st, ws.part_small + HD * HD, ws.chunks_small,
-                     (long long)HD, ss, grad.b1);
-  hipLaunchKernelGGL(sum_parts_kernel, dim3(1), dim3(256), 0, st, ws.part_small + HD * HD + HD, ws.chunks_small,
-                     (long long)HD, ss, grad.b2);
+  hipLaunchKernelGGL(sum_parts_kernel, dim3((HD + 63) / 64), dim3(256), 0, st, ws.part_small + HD * HD,
+                     ws.chunks_small, (long long)HD, ss, grad.b1);
+  hipLaunchKernelGGL(sum_parts_kernel, dim3((HD + 63) / 64), dim3(256), 0, st, ws.part_small + HD * HD + HD,
+                     ws.chunks_small, (long long)HD, ss, grad.b2);
   return hipGetLastError();
 }
 
