@@ -440,7 +440,7 @@ __global__ void __launch_bounds__(256) slc_bwd_q_kernel(const T* q, const T* k, 
   f32x4 acc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
-  __syncthreads();
+  wave_sync();   // LDS regions are per wave
 
   for (int sb0 = 0; sb0 < nsub; sb0 += 2) {
     const int ent[2] = {sub[sb0], sb0 + 1 < nsub ? sub[sb0 + 1] : -1};
@@ -465,7 +465,7 @@ __global__ void __launch_bounds__(256) slc_bwd_q_kernel(const T* q, const T* k, 
         const int e = ent[kb];
         ok[kb][i] = e >= 0 && (e >> 24) == my_gi && (val == nullptr || val[(e & 0xFFFFFF) + 4 * j + i]);
       }
-    __syncthreads();
+    wave_sync();   // LDS regions are per wave
     for (int e = lane; e < 8 * (HD / 8); e += 64) {
       const int kq = e / (HD / 8), dc = (e % (HD / 8)) * 8;
       const int en = ent[kq >> 2];
@@ -474,7 +474,7 @@ __global__ void __launch_bounds__(256) slc_bwd_q_kernel(const T* q, const T* k, 
       for (int u = 0; u < 4; ++u) rows[u] = en >= 0 ? kh + (size_t)((en & 0xFFFFFF) + 4 * (kq & 3) + u) * HD : nullptr;
       stage_vt(rows, dc, kt, VSTR, 4 * kq);
     }
-    __syncthreads();
+    wave_sync();   // LDS regions are per wave
     f32x4 s[2], dp[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -512,17 +512,21 @@ __global__ void __launch_bounds__(256) slc_bwd_q_kernel(const T* q, const T* k, 
 // (b,h,block) -> sorted list of the groups that selected it: pairs[seg_start .. seg_end).
 
 // 16x16 MFMA with a 16-deep contraction: 4 values per lane group (k = 4*(L/16) + i).
-__device__ __forceinline__ f32x4 mma16(const float (&a)[4], const float (&bv)[4], f32x4 c, bf16_t) {
+// A comes as 4 raw storage elements (8 bytes bf16 / 16 bytes f32), B as 4 f32 values.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ f32x4 mma16(const bf16_t* a, const float (&bv)[4], f32x4 c) {
   typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-  bf16x4 x = {(__bf16)a[0], (__bf16)a[1], (__bf16)a[2], (__bf16)a[3]};
+  const uint2 ar = *reinterpret_cast<const uint2*>(a);
   bf16x4 y = {(__bf16)bv[0], (__bf16)bv[1], (__bf16)bv[2], (__bf16)bv[3]};
-  typedef short s16x4 __attribute__((ext_vector_type(4)));
-  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, x), __builtin_bit_cast(s16x4, y), c, 0,
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, ar), __builtin_bit_cast(s16x4, y), c, 0,
                                                    0, 0);
 }
-__device__ __forceinline__ f32x4 mma16(const float (&a)[4], const float (&bv)[4], f32x4 c, float) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], bv[i], c, 0, 0, 0);
+__device__ __forceinline__ f32x4 mma16(const float* a, const float (&bv)[4], f32x4 c) {
+  const float4 ar = *reinterpret_cast<const float4*>(a);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(ar.x, bv[0], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(ar.y, bv[1], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(ar.z, bv[2], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(ar.w, bv[3], c, 0, 0, 0);
   return c;
 }
 
@@ -671,13 +675,8 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_kernel(const T* q, const T* k,
       }
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const T* pd = &dtr[(16 * db + r) * TSTR + 4 * j];
-        const T* pq = &qtr[(16 * db + r) * TSTR + 4 * j];
-        float ao[4], aqv[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) { ao[i] = to_f32<T>(pd[i]); aqv[i] = to_f32<T>(pq[i]); }
-        dva[kb][db] = mma16(ao, pg, dva[kb][db], T(0));
-        dka[kb][db] = mma16(aqv, dsv, dka[kb][db], T(0));
+        dva[kb][db] = mma16(&dtr[(16 * db + r) * TSTR + 4 * j], pg, dva[kb][db]);
+        dka[kb][db] = mma16(&qtr[(16 * db + r) * TSTR + 4 * j], dsv, dka[kb][db]);
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

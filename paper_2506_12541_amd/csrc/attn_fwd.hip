@@ -122,7 +122,7 @@ __global__ void __launch_bounds__(256) slc_fwd_kernel(const T* q, const T* k, co
     const int id = selp[gi * kk + slot % kk];
     sub[e] = id < 0 ? -1 : ((gi << 24) | (id * ls + (e * 16) % ls));
   }
-  __syncthreads();
+  wave_sync();   // LDS regions are per wave
 
   WaveAttn<T, HD, 1> w;
   w.init();
@@ -151,7 +151,7 @@ __global__ void __launch_bounds__(256) slc_fwd_kernel(const T* q, const T* k, co
         const int tok = (e & 0xFFFFFF) + 4 * j + i;
         ok[kb][i] = e >= 0 && (e >> 24) == my_gi && (val == nullptr || val[tok]);
       }
-    __syncthreads();
+    wave_sync();   // LDS regions are per wave
     for (int e = lane; e < 8 * (HD / 8); e += 64) {
       const int kq = e / (HD / 8), dc = (e % (HD / 8)) * 8;
       const int en = ent[kq >> 2];
@@ -160,7 +160,7 @@ __global__ void __launch_bounds__(256) slc_fwd_kernel(const T* q, const T* k, co
       for (int u = 0; u < 4; ++u) rows[u] = en >= 0 ? vh + (size_t)((en & 0xFFFFFF) + 4 * (kq & 3) + u) * HD : nullptr;
       stage_vt(rows, dc, vt, VSTR, 4 * kq);
     }
-    __syncthreads();
+    wave_sync();   // LDS regions are per wave
     auto kfrag = [&](int kb, int c) { return kf[kb][c]; };
     auto vfrag = [&](int db, int kp) { return load_4x2(&vt[(16 * db + r) * VSTR + 32 * kp + 4 * j]); };
     auto keyok = [&](int kb, int i, int) { return ok[kb][i]; };
