@@ -204,8 +204,9 @@ def compression_branch_backward(q, kc, vc, cvalid, valid, P: Params, o, lse, do)
 # ----------------------------------------------------------------------------------
 # Branch 3: group-shared block selection (Eq. 6, 7, 10-12) and selection attention (Eq. 8).
 # ----------------------------------------------------------------------------------
-def group_block_scores(q, kc, valid, P: Params):
-    """Scores [N/g, N/l'] of every selection block for every query group.
+def group_block_scores(q, kc, valid, P: Params, groups=None):
+    """Scores [N/g, N/l'] of every selection block for every query group (or only for the
+    listed groups, in that order).
 
     Pooled query q_p = (1/g) * sum of the group's real queries (Eq. 11); compressed-block
     score S_pc = <q_p, kc_c> (Eq. 6, 12); a selection block of r = l'/l compressed blocks
@@ -214,14 +215,15 @@ def group_block_scores(q, kc, valid, P: Params):
     n, d = q.shape
     g, l, ls, m = P.group, P.cmp_block, P.slc_block, P.ball
     r = ls // l
-    qz = np.where(valid[:, None], q, 0.0)
-    qp = qz.reshape(n // g, g, d).sum(axis=1) / g
-    s_cmp = qp @ kc.T                                  # [N/g, N/l]
-    s_blk = s_cmp.reshape(n // g, n // ls, r).mean(axis=2)
+    groups = np.arange(n // g) if groups is None else np.asarray(groups)
+    qz = np.where(valid[:, None], q, 0.0).reshape(n // g, g, d)[groups]
+    qp = qz.sum(axis=1) / g
+    s_cmp = qp @ kc.T                                  # [groups, N/l]
+    s_blk = s_cmp.reshape(len(groups), n // ls, r).mean(axis=2)
     blk_ok = block_valid(valid, ls)
     s_blk[:, ~blk_ok] = NEG_INF
     if P.mask_own_ball:
-        grp_ball = (np.arange(n // g) * g) // m
+        grp_ball = (groups * g) // m
         blk_ball = (np.arange(n // ls) * ls) // m
         s_blk[grp_ball[:, None] == blk_ball[None, :]] = NEG_INF
     return s_blk

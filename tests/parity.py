@@ -69,7 +69,9 @@ def check_indices(sel_gpu, sel_or, scores):
 
 
 def max_abs(a, b, mask=None):
-    d = np.abs(np.asarray(a, np.float64) - np.asarray(b, np.float64))
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    with np.errstate(invalid="ignore"):
+        d = np.where(a == b, 0.0, np.abs(a - b))   # equal infinities (no key: lse -inf) agree
     if mask is not None:
         d = d[mask]
     return float(d.max()) if d.size else 0.0

@@ -99,3 +99,26 @@ def test_backward_small_bf16_with_padding():
     cfg = Config("small_bf16", 2, 900, 1024, 2, 64, "bf16", 128, 16, 16, 32, 4, 16, "uniform", "fwdbwd")
     print("backward parity small bf16 d=64", flush=True)
     run_case(cfg, seed=11)
+
+
+def test_backward_scaling_one_head():
+    """65536 points, 8 heads, d=64 at full size (the benchmarked workload); the oracle
+    differentiates one whole head (heads are independent except for the gate and MLP
+    weight gradients, which sum over heads and are checked on the airflow workload)."""
+    cfg = CONFIGS[3]
+    print("backward parity config 3 (head 5)", flush=True)
+    inp = make_inputs(cfg, layout="ball", with_grad=True)
+    valid = valid_from_tree(cfg)
+    g, (p, q, k, v, vd, gate, phi_k, phi_v, saved, o) = gpu_forward(cfg, inp, valid)
+    grads = gb.backward(p, q, k, v, vd, gate, phi_k, phi_v, saved, to_dev(inp["do"], p.torch_dtype))
+    torch.cuda.synchronize()
+    h = 5
+    one = {n: np.ascontiguousarray(inp[n][:, h:h + 1]) for n in ("q", "k", "v", "do")}
+    one.update(gate=inp["gate"], phi_k=inp["phi_k"], phi_v=inp["phi_v"])
+    P = oracle_params(cfg)
+    fwd = oracle_with_sel(one, valid, P, g["sel"][:, h:h + 1])
+    ref = ob.backward(one["q"], one["k"], one["v"], valid, one["gate"], one["phi_k"], one["phi_v"], P, fwd,
+                      one["do"])
+    errs = {n: max_abs(grads[n][:, h:h + 1].cpu().numpy(), ref[n]) for n in ("dq", "dk", "dv")}
+    print({k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    assert all(e < TOL[cfg.dtype] for e in errs.values()), errs

@@ -3,6 +3,8 @@
 Selected blocks must match bit-exactly except where the oracle's own scores tie within
 1e-6; branch outputs are compared with the oracle re-run on the GPU's selection, at
 max-abs 1e-4 (f32 layers) or 2e-2 (bf16 layers)."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -25,7 +27,6 @@ def _check_head(cfg, inp, valid, g, b, h, P, tol, groups=None):
     kc, _ = ob.compress(k, vb, phk, P)
     vc, _ = ob.compress(v, vb, phv, P)
     assert max_abs(g["kc"][b, h], kc) < 1e-4 and max_abs(g["vc"][b, h], vc) < 1e-4
-    scores = ob.group_block_scores(q, kc, vb, P)
     n = q.shape[0]
     gsel = g["sel"][b, h]
     if groups is None:
@@ -33,13 +34,20 @@ def _check_head(cfg, inp, valid, g, b, h, P, tol, groups=None):
         rows = np.arange(n)
     else:
         rows = (groups[:, None] * P.group + np.arange(P.group)[None, :]).reshape(-1)
-    osel = ob.topk_blocks(scores[groups], P.topk)
-    ndiff = check_indices(gsel[groups], osel, scores[groups])
+    scores = ob.group_block_scores(q, kc, vb, P, groups=groups)
+    osel = ob.topk_blocks(scores, P.topk)
+    ndiff = check_indices(gsel[groups], osel, scores)
     # branch outputs given the GPU's selection
     rmask = np.zeros(n, bool)
     rmask[rows] = True
     rv = rmask & vb
-    o_ball, l_ball = ob.ball_branch(q, k, v, vb, P)
+    if rows.size < n:     # sampled rows: ball attention only for the balls they touch
+        o_ball, l_ball = np.zeros((n, q.shape[1])), np.full(n, -np.inf)
+        for s0 in np.unique((rows // P.ball) * P.ball):
+            sl = slice(s0, s0 + P.ball)
+            o_ball[sl], l_ball[sl] = ob.ball_branch(q[sl], k[sl], v[sl], vb[sl], P)
+    else:
+        o_ball, l_ball = ob.ball_branch(q, k, v, vb, P)
     o_cmp, l_cmp = ob.compression_branch(q, kc, vc, ob.block_valid(vb, P.cmp_block), vb, P, rows=rows)
     o_slc, l_slc = ob.selection_branch(q, k, v, vb, gsel, P, groups=groups)
     outs = (o_ball, o_cmp, o_slc)
@@ -99,3 +107,21 @@ def test_forward_no_own_ball_mask_and_mean_pool():
         P = oracle_params(cfg, **okw)
         for h in range(cfg.heads):
             _check_head(cfg, inp, valid, g, 0, h, P, TOL[cfg.dtype])
+
+
+@pytest.mark.timeout(600)
+def test_forward_large_sampled():
+    """2^20 points with the large workload's block sizes (ball 512, blocks 32/64, top-16,
+    groups of 32) on 2 of its 16 heads (heads only add grid rows; 2 keep the host-side
+    input generation short); oracle on 48 sampled groups of both heads."""
+    cfg = dataclasses.replace(CONFIGS[4], heads=2)
+    print("forward parity 2^20 points, 2 heads (sampled)", flush=True)
+    inp = make_inputs(cfg, seed=4, layout="ball", with_grad=False)
+    valid = valid_from_tree(cfg)
+    g, _ = gpu_forward(cfg, inp, valid)
+    P = oracle_params(cfg)
+    rng = np.random.default_rng(4)
+    ngroups = cfg.n_pad // cfg.group
+    for h in (0, cfg.heads - 1):
+        groups = np.unique(np.concatenate([[0, ngroups - 1], rng.choice(ngroups, 46, replace=False)]))
+        _check_head(cfg, inp, valid, g, 0, h, P, TOL[cfg.dtype], groups=groups)

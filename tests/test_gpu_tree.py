@@ -17,7 +17,7 @@ def _gpu_perm(pts, n_pad):
     return perm.cpu().numpy()
 
 
-@pytest.mark.parametrize("cfg_id", [1, 2, 3])
+@pytest.mark.parametrize("cfg_id", [1, 2, 3, 4])
 def test_tree_matches_oracle(cfg_id):
     cfg = CONFIGS[cfg_id]
     pts = make_points(cfg)

@@ -56,13 +56,18 @@ CONFIGS = {
 }
 
 
-def round_bf16(x: np.ndarray) -> np.ndarray:
-    """Round float32 values to the nearest bfloat16 (ties to even); returns float32."""
+def round_bf16(x: np.ndarray, chunk: int = 1 << 22) -> np.ndarray:
+    """Round finite float32 values to the nearest bfloat16 (ties to even); returns float32."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    u = ((u + 0x7FFF + lsb) >> 16) << 16
-    return u.astype(np.uint32).view(np.float32)
+    out = np.empty_like(x)
+    src = x.reshape(-1).view(np.uint32)
+    dst = out.reshape(-1).view(np.uint32)
+    for s in range(0, src.size, chunk):
+        u = src[s:s + chunk]
+        # finite values stay below 0xFF800000, so the carry cannot wrap 32 bits
+        dst[s:s + chunk] = ((u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))) >> np.uint32(16)) \
+            << np.uint32(16)
+    return out
 
 
 def bf16_bits(x: np.ndarray) -> np.ndarray:
