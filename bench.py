@@ -47,6 +47,122 @@ def algorithmic_flops(cfg):
     return fwd, bwd
 
 
+def phase_flops(cfg):
+    """Algorithmic FLOPs of each timed phase (same totals as algorithmic_flops).
+
+    Backward split: the key-major kernels compute the recomputed scores, dP, dK and dV
+    (4 products, 8 d FLOP per query-key pair); the query-major kernels are credited only
+    with dQ (2 d), their recomputation of scores and dP being overhead of the split.
+    """
+    B, H, N, d = cfg.batch, cfg.heads, cfg.n_pad, cfg.head_dim
+    m, l, ls, k, g = cfg.ball, cfg.cmp_block, cfg.slc_block, cfg.topk, cfg.group
+    pairs = {"ball": N * m, "cmp": N * (N // l), "slc": N * k * ls}
+    mlp = 2 * 2.0 * (N / l) * (l * d * d + d * d) * B * H
+    f = {"fwd.compress": mlp, "fwd.select": 2.0 * (N / g) * (N / l) * d * B * H, "bwd.mlp": 2 * mlp}
+    for br, kv in (("ball", "kv_ball"), ("cmp", "kv_cmp"), ("slc", "slc_kv")):
+        f[f"fwd.{br}"] = 4.0 * pairs[br] * d * B * H
+        f[f"bwd.dq_{br}"] = 2.0 * pairs[br] * d * B * H
+        f[f"bwd.{kv}"] = 8.0 * pairs[br] * d * B * H
+    return f
+
+
+# single-launch phases whose work is a dense bf16 contraction (roofline candidates)
+MFMA_PHASES = ("fwd.ball", "fwd.cmp", "fwd.slc", "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc", "bwd.kv_ball",
+               "bwd.kv_cmp")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_{phase}_{workload}.txt")
+
+
+def _sources_sha(files):
+    import hashlib
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(phase, workload):
+    """HBM bytes per launch of `phase` from the committed counter summary, or None when
+    there is none or the kernel's sources changed since the counters were taken."""
+    path = TRAFFIC_FILE.format(phase=phase.replace(".", "_"), workload=workload)
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith((" ", "#")):
+            key, val = line.split(":", 1)
+            kv[key.strip()] = val.strip()
+    try:
+        if _sources_sha(kv["sources"].split()) != kv["sources_sha256"]:
+            return None
+        return float(kv["traffic_bytes_per_launch"])
+    except (KeyError, OSError, ValueError):
+        return None
+
+
+COPY_BYTES = 1 << 30
+
+
+def copy_calibration():
+    """A plain device copy of known size (1 GiB read, 1 GiB written per launch), the
+    yardstick for the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(4):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": COPY_BYTES, "copy_bytes_written": COPY_BYTES, "launches": 4}))
+
+
+def _pmc_per_dispatch(csv_path, counter, match):
+    import csv
+    tot, disp = 0.0, set()
+    for r in csv.DictReader(open(csv_path)):
+        if r["Counter_Name"] == counter and match(r["Kernel_Name"]):
+            tot += float(r["Counter_Value"])
+            disp.add(r["Dispatch_Id"])
+    if not disp:
+        raise SystemExit(f"{csv_path}: no dispatch of the kernel with counter {counter}")
+    return tot / len(disp), len(disp)
+
+
+def summarize_traffic(args):
+    """Write the traffic summary of one phase's kernel from four rocprofv3 --pmc runs
+    (FETCH_SIZE and WRITE_SIZE over the bench, then over --copy-calibration)."""
+    fetch_csv, write_csv, cfetch_csv, cwrite_csv = args.summarize_traffic
+    kernel, phase = args.kernel, args.phase
+    from workloads import CONFIGS
+    cfg = CONFIGS[args.config]
+    short = lambda n: n.replace("(anonymous namespace)::", "").replace("void ", "").split("(")[0].split("::")[-1]
+    is_kernel = lambda n: short(n) == kernel
+    is_copy = lambda n: "copy" in n.lower()
+    f_kib, nf = _pmc_per_dispatch(fetch_csv, "FETCH_SIZE", is_kernel)
+    w_kib, nw = _pmc_per_dispatch(write_csv, "WRITE_SIZE", is_kernel)
+    cf_kib, _ = _pmc_per_dispatch(cfetch_csv, "FETCH_SIZE", is_copy)
+    cw_kib, _ = _pmc_per_dispatch(cwrite_csv, "WRITE_SIZE", is_copy)
+    ff = COPY_BYTES / (cf_kib * 1024)
+    fw = COPY_BYTES / (cw_kib * 1024)
+    traffic = f_kib * 1024 * ff + w_kib * 1024 * fw
+    srcs = args.sources.split()
+    out = TRAFFIC_FILE.format(phase=phase.replace(".", "_"), workload=cfg.name)
+    with open(out, "w") as fh:
+        fh.write(f"# HBM traffic per launch of the {phase} kernel, workload {cfg.name}\n")
+        fh.write("# Commands (repository root on the MI355X box, after cd /tmp && export TMPDIR=/tmp):\n")
+        for c in args.commands:
+            fh.write(f"#   {c}\n")
+        fh.write("# FETCH_SIZE / WRITE_SIZE are KiB per dispatch; each is scaled by the ratio of the known\n"
+                 "# bytes of a plain 1 GiB device copy to what the same counter reads for that copy.\n")
+        fh.write(f"phase: {phase}\nworkload: {cfg.name}\nkernel: {kernel}\n")
+        fh.write(f"dispatches: fetch {nf}, write {nw}\n")
+        fh.write(f"fetch_kib_per_dispatch: {f_kib:.1f}\nwrite_kib_per_dispatch: {w_kib:.1f}\n")
+        fh.write(f"copy_fetch_kib_per_dispatch: {cf_kib:.1f}\ncopy_write_kib_per_dispatch: {cw_kib:.1f}\n")
+        fh.write(f"fetch_scale: {ff:.4f}\nwrite_scale: {fw:.4f}\n")
+        fh.write(f"traffic_bytes_per_launch: {traffic:.0f}\n")
+        fh.write(f"sources: {' '.join(srcs)}\nsources_sha256: {_sources_sha(srcs)}\n")
+    print(open(out).read())
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -54,6 +170,15 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--cpu-baseline", type=int, default=1, help="time the float64 oracle on a sample (0 = skip)")
+    ap.add_argument("--copy-calibration", action="store_true", help="run only the 1 GiB plain copy")
+    ap.add_argument("--summarize-traffic", nargs=4, metavar="CSV",
+                    help="counter CSVs: FETCH_SIZE bench, WRITE_SIZE bench, FETCH_SIZE copy, WRITE_SIZE copy")
+    ap.add_argument("--phase", default="bwd.kv_cmp")
+    ap.add_argument("--kernel", default="dense_bwd_kv_kernel")
+    ap.add_argument("--sources", default="paper_2506_12541_amd/csrc/attn_bwd.hip paper_2506_12541_amd/csrc/attn_common.hpp "
+                                         "paper_2506_12541_amd/csrc/common.hpp paper_2506_12541_amd/csrc/kernels.hpp "
+                                         "paper_2506_12541_amd/build.py")
+    ap.add_argument("--commands", nargs="*", default=[])
     return ap.parse_args()
 
 
@@ -87,10 +212,17 @@ def cpu_baseline(cfg, pts_np, inp_np):
 
 def main():
     args = parse()
+    if args.summarize_traffic:
+        summarize_traffic(args)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the multi-GPU sharding is a design "
               "in DESIGN.md, not a measured path", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     import numpy as np
     import torch
@@ -154,10 +286,11 @@ def main():
     flops = sum(fwd_f.values()) + sum(bwd_f.values())
     layer_ms = sum(v for n, v in phases.items() if n.startswith(("fwd.", "bwd.")))
     tflops = flops / (layer_ms * 1e-3) / 1e12
-    # dominant kernel: the compressed-attention forward kernel (4 N (N/l) d per head)
-    cmp_ms = phases["fwd.cmp"]
-    cmp_flops = fwd_f["cmp"]
-    achieved = cmp_flops / (cmp_ms * 1e-3) / 1e12
+    pf = phase_flops(cfg)
+    # dominant kernel: the longest single-launch contraction phase
+    dom = max(MFMA_PHASES, key=lambda n: phases[n])
+    achieved = pf[dom] / (phases[dom] * 1e-3) / 1e12
+    traffic = measured_traffic(dom, cfg.name)
     result = {
         "metric": "BSA layer fwd+bwd points/sec and TFLOP/s (fraction of MFMA peak) at N=65536, 1 GPU",
         "value": cfg.batch * cfg.n_real / (ms * 1e-3),
@@ -180,9 +313,10 @@ def main():
         "mfma_frac": tflops * 1e12 / MFMA_BF16_PEAK,
         "algorithmic_gflop_per_step": flops / 1e9,
         "phase_ms": {n: round(v, 4) for n, v in phases.items()},
-        "roofline": {"bound": "mfma", "kernel": "compressed-attention forward (fwd.cmp)", "achieved": achieved,
-                     "peak": MFMA_BF16_PEAK / 1e12, "unit": "TFLOP/s", "frac": achieved * 1e12 / MFMA_BF16_PEAK,
-                     "traffic": None},
+        "phase_tflops": {n: round(pf[n] / (phases[n] * 1e-3) / 1e12, 1) for n in pf if phases[n] > 0},
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": MFMA_BF16_PEAK / 1e12,
+                     "unit": "TFLOP/s", "frac": achieved * 1e12 / MFMA_BF16_PEAK, "traffic": traffic,
+                     "algorithmic_gflop_per_launch": pf[dom] / 1e9},
     }
     if args.cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, pts_np, {**inp_np, **make_inputs(cfg, layout="ball",
