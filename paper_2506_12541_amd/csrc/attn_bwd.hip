@@ -147,6 +147,7 @@ __global__ void __launch_bounds__(256) dense_bwd_q_kernel(const T* q, const T* k
   IO::load_rows(kreg, kh, 0, nkeys);
   IO::load_rows(vreg, vh, 0, nkeys);
   IO::load_tr(treg, kh, 0, nkeys);
+  vm_drain();
   for (int t0 = 0; t0 < nkeys; t0 += KT) {
     __syncthreads();
     IO::store_rows(kreg, ks, KSTR);
@@ -311,6 +312,7 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
     }
   };
   fetch(qbeg);
+  vm_drain();
   for (int t0 = qbeg; t0 < qend; t0 += kQT) {
     __syncthreads();
     IO::store_rows(qreg, qs, QSTR);
@@ -441,6 +443,7 @@ __global__ void __launch_bounds__(256) slc_bwd_q_kernel(const T* q, const T* k, 
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
   wave_sync();   // LDS regions are per wave
+  vm_drain();
 
   for (int sb0 = 0; sb0 < nsub; sb0 += 2) {
     const int ent[2] = {sub[sb0], sb0 + 1 < nsub ? sub[sb0 + 1] : -1};
@@ -639,6 +642,7 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_kernel(const T* q, const T* k,
     }
   };
   if (wid < nwork) fetch(wid);
+  vm_drain();
   for (int item = wid; item < nwork; item += 4) {
     CT cq[NCH], cd[NCH];
     float cl[4], cdv[4], cg[4];

@@ -173,6 +173,69 @@ struct TileIO {
   }
 };
 
+// ---- bf16 tiles staged without registers: direct global->LDS loads, transpose reads ----
+// A tile of rows x HD bf16 lives in LDS row-major without padding; the 16-byte chunk c of
+// row x is stored at chunk c ^ swz(x). Row-fragment reads (16 lanes = 16 consecutive rows,
+// one chunk each) want consecutive rows on distinct banks (SWZ_ROW); transpose reads (16
+// lanes = 4 consecutive rows x two chunks) want those chunk pairs on distinct banks (SWZ_TR).
+enum { SWZ_ROW = 0, SWZ_TR = 1 };
+template <int HD, int MODE>
+__device__ __forceinline__ int swz(int x) {
+  static_assert(HD == 32 || HD == 64, "head dim");
+  if (HD == 64) return MODE == SWZ_ROW ? (x & 7) : (((x & 3) << 1) | ((x >> 2) & 1));
+  return MODE == SWZ_ROW ? ((x >> 1) & 3) : (x & 2);
+}
+
+// Rows [r0, r0 + ROWS) of a row-major [nrows, HD] matrix into an LDS tile, by NW waves.
+// Each wave instruction moves 64 lanes x 16 bytes into 1 KB of consecutive LDS (lane L
+// fills bytes [16L, 16L + 16)); the lane picks the global chunk that belongs there. Rows
+// at or past nrows repeat row nrows - 1 (the caller masks them). Completion is tracked by
+// vmcnt: vm_drain() and a barrier make the tile visible to the workgroup.
+template <int HD, int ROWS, int MODE, int NW>
+__device__ __forceinline__ void dma_tile(bf16_t* lds, const bf16_t* g, int r0, int nrows, int wid, int lane) {
+  constexpr int CPR = HD / 8;           // 16-byte chunks per row
+  constexpr int NI = ROWS * CPR / 64;   // 1 KB wave instructions per tile
+  static_assert(NI % NW == 0, "tile / wave split");
+#pragma unroll
+  for (int u = 0; u < NI / NW; ++u) {
+    const int blk = wid * (NI / NW) + u;
+    const int idx = blk * 64 + lane;
+    const int row = idx / CPR;
+    const int lc = (idx % CPR) ^ swz<HD, MODE>(row);
+    const int gr = r0 + row < nrows ? r0 + row : nrows - 1;
+    __builtin_amdgcn_global_load_lds(g + (size_t)gr * HD + 8 * lc, lds + blk * 512, 16, 0, 0);
+  }
+}
+
+// 8 consecutive elements of row x starting at logical chunk lc (an MFMA row fragment).
+template <int HD, int MODE>
+__device__ __forceinline__ bf16x8 lds_row_chunk(const bf16_t* t, int x, int lc) {
+  return *reinterpret_cast<const bf16x8*>(t + x * HD + 8 * (lc ^ swz<HD, MODE>(x)));
+}
+
+// MFMA A operand of the transposed tile, in the contraction order of a probability chunk
+// built from two 16-key accumulator tiles (elements 0-3: keys 4j + i of the first tile,
+// 4-7: keys 4j + i of the second): lane (r = lane % 16, j = lane / 16) receives
+// X[k0 + 4j + i][m0 + r] and X[k0 + 16 + 4j + i][m0 + r], i = 0..3, from the row-major
+// tile X (SWZ_TR layout), with two ds_read_b64_tr_b16. Within each 16-lane group that
+// instruction hands lane l element l % 4 of the 4-element runs addressed by lanes l / 4,
+// 4 + l / 4, 8 + l / 4, 12 + l / 4; lane p therefore addresses row k0 + 4j + p / 4 (then
+// + 16), columns m0 + 4 (p % 4) + [0, 4).
+template <int HD>
+__device__ __forceinline__ bf16x8 lds_tr_chunk(const bf16_t* t, int k0, int m0, int lane) {
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  const int p = lane & 15, j = lane >> 4;
+  const int col = m0 + 4 * (p & 3);
+  const int lc = col >> 3, sub = col & 7;
+  const int x0 = k0 + 4 * j + (p >> 2), x1 = x0 + 16;
+  const bf16_t* a0 = t + x0 * HD + 8 * (lc ^ swz<HD, SWZ_TR>(x0)) + sub;
+  const bf16_t* a1 = t + x1 * HD + 8 * (lc ^ swz<HD, SWZ_TR>(x1)) + sub;
+  const uint2 v0 = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)a0));
+  const uint2 v1 = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)a1));
+  return __builtin_bit_cast(bf16x8, make_uint4(v0.x, v0.y, v1.x, v1.y));
+}
+
 // Online-softmax state of one wave over QB blocks of 16 queries.
 // Two VALU savings on the hot path: (1) the reference maximum is only raised when a new
 // tile maximum exceeds it by more than kRescale (log2 units), so the O accumulators are
@@ -226,6 +289,12 @@ struct WaveAttn {
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) s[qb][kb] = mma(a, qf[qb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : s[qb][kb]);
       }
+    // V^T fragments are read now so that their LDS latency hides behind the softmax
+    CT vr[DB][KB / 2];
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int kp = 0; kp < KB / 2; ++kp) vr[db][kp] = vfrag(db, kp);
     CT pf[QB][KB / 2];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -268,11 +337,9 @@ struct WaveAttn {
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int kp = 0; kp < KB / 2; ++kp) {
-        CT a = vfrag(db, kp);
+      for (int kp = 0; kp < KB / 2; ++kp)
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) o[qb][db] = mma(a, pf[qb][kp], o[qb][db]);
-      }
+        for (int qb = 0; qb < QB; ++qb) o[qb][db] = mma(vr[db][kp], pf[qb][kp], o[qb][db]);
   }
 
   // Normalise and store O rows (query q0 + 16 qb + r) and natural-log LSE.

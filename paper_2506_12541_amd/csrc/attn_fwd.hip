@@ -55,6 +55,7 @@ __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, 
   typename IO::V4 vreg[IO::TV][4];
   IO::load_rows(kreg, kh, 0, nkeys);
   IO::load_tr(vreg, vh, 0, nkeys);
+  vm_drain();
   for (int t0 = 0; t0 < nkeys; t0 += kFT) {
     __syncthreads();
     IO::store_rows(kreg, ks, KSTR);
@@ -81,6 +82,70 @@ __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, 
         w.template tile<kKT / 16>(sl2, kfrag, vfrag, keyok);
       }
     }
+  }
+  w.finish(lane, bh * N + wq0, out, lse, qval, wq0);
+}
+
+// bf16 variant: 64-key K and V tiles double-buffered in LDS and filled by direct
+// global->LDS loads (no staging registers, one barrier per tile); V^T fragments come from
+// transpose reads of the row-major V tile. The two buffers are distinct LDS objects and
+// the loop is unrolled by two, so the compiler can tell that loads in flight into one
+// buffer do not alias reads of the other and need not be waited for.
+template <int HD, int QB, int NW, bool BALL>
+__global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
+                                                                const uint8_t* qvalid_all, const uint8_t* kvalid_all,
+                                                                int H, int N, int nkeys_total, int m, float sl2,
+                                                                bf16_t* out, float* lse) {
+  constexpr int kFT = kKT;
+  __shared__ __attribute__((aligned(16))) bf16_t ks0[kFT * HD], ks1[kFT * HD];
+  __shared__ __attribute__((aligned(16))) bf16_t vs0[kFT * HD], vs1[kFT * HD];
+  __shared__ uint8_t ok0[kFT], ok1[kFT];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r = lane & 15, j = lane >> 4;
+  const int b = blockIdx.z, h = blockIdx.y;
+  const long long bh = (long long)b * H + h;
+  const int q0 = blockIdx.x * (16 * QB * NW);
+  const int nkeys = BALL ? m : nkeys_total;
+  const int key0 = BALL ? (q0 / m) * m : 0;
+  const bf16_t* kh = k + (bh * nkeys_total + key0) * HD;
+  const bf16_t* vh = v + (bh * nkeys_total + key0) * HD;
+  const uint8_t* kval = kvalid_all ? kvalid_all + (size_t)b * nkeys_total + key0 : nullptr;
+  const uint8_t* qval = qvalid_all ? qvalid_all + (size_t)b * N : nullptr;
+
+  // key-validity bytes are read before the tile loads, so waiting for them does not
+  // wait for the tile
+  auto issue = [&](int t0, bf16_t* kd, bf16_t* vd, uint8_t* okd) {
+    uint8_t okv = 0;
+    if (threadIdx.x < kFT) {
+      const int key = t0 + threadIdx.x;
+      okv = key < nkeys && (kval == nullptr || kval[key]);
+    }
+    dma_tile<HD, kFT, SWZ_ROW, NW>(kd, kh, t0, nkeys, wid, lane);
+    dma_tile<HD, kFT, SWZ_TR, NW>(vd, vh, t0, nkeys, wid, lane);
+    if (threadIdx.x < kFT) okd[threadIdx.x] = okv;
+  };
+  WaveAttn<bf16_t, HD, QB> w;
+  w.init();
+  const int wq0 = q0 + wid * 16 * QB;
+  auto step = [&](int t0, const bf16_t* kt, const bf16_t* vt, const uint8_t* ok, bf16_t* kn, bf16_t* vn,
+                  uint8_t* okn) {
+    vm_drain();          // this wave's loads of the tile have landed
+    __syncthreads();     // ... and every wave's; the previous tile is no longer read
+    if (t0 + kFT < nkeys) issue(t0 + kFT, kn, vn, okn);
+    auto kfrag = [&](int kb, int c) { return lds_row_chunk<HD, SWZ_ROW>(kt, kb * 16 + r, 4 * c + j); };
+    auto vfrag = [&](int db, int kp) { return lds_tr_chunk<HD>(vt, 32 * kp, 16 * db, lane); };
+    if (kval == nullptr && t0 + kFT <= nkeys) {
+      w.template tile<kFT / 16>(sl2, kfrag, vfrag, [](int, int, int) { return true; });
+    } else {
+      auto keyok = [&](int kb, int i, int) { return ok[kb * 16 + 4 * j + i] != 0; };
+      w.template tile<kFT / 16>(sl2, kfrag, vfrag, keyok);
+    }
+  };
+  issue(0, ks0, vs0, ok0);
+  load_q(w, q + (bh * N + wq0) * HD, lane);
+  for (int t0 = 0; t0 < nkeys; t0 += 2 * kFT) {
+    step(t0, ks0, vs0, ok0, ks1, vs1, ok1);
+    if (t0 + kFT < nkeys) step(t0 + kFT, ks1, vs1, ok1, ks0, vs0, ok0);
   }
   w.finish(lane, bh * N + wq0, out, lse, qval, wq0);
 }
@@ -127,6 +192,7 @@ __global__ void __launch_bounds__(256) slc_fwd_kernel(const T* q, const T* k, co
   WaveAttn<T, HD, 1> w;
   w.init();
   load_q(w, q + (bh * N + wq0) * HD, lane);
+  vm_drain();
 
   for (int sb0 = 0; sb0 < nsub; sb0 += 2) {
     const int e0 = sub[sb0];
@@ -189,19 +255,29 @@ __global__ void gate_fwd_kernel(const T* ob, const float* gate, const uint8_t* v
   out[i] = from_f32<T>(acc);
 }
 
+// bf16 layers take the direct-load kernel (NW waves of QB 16-query blocks per workgroup);
+// f32 layers the register-staged one (4 waves).
+template <typename T, int HD, int QB, bool BALL, int NW = 4>
+void launch_dense_fwd(dim3 grid, hipStream_t st, const void* q, const void* k, const void* v, const uint8_t* qvalid,
+                      const uint8_t* kvalid, int H, int N, int nkeys_total, int m, float sl2, void* o, float* lse) {
+  if constexpr (sizeof(T) == 2)
+    hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL>), grid, dim3(64 * NW), 0, st, (const bf16_t*)q,
+                       (const bf16_t*)k, (const bf16_t*)v, qvalid, kvalid, H, N, nkeys_total, m, sl2, (bf16_t*)o, lse);
+  else
+    hipLaunchKernelGGL((dense_fwd_kernel<T, HD, QB, BALL>), grid, dim3(256), 0, st, (const T*)q, (const T*)k,
+                       (const T*)v, qvalid, kvalid, H, N, nkeys_total, m, sl2, (T*)o, lse);
+}
+
 template <typename T, int HD>
 hipError_t ball_impl(const Dims& D, const void* q, const void* k, const void* v, const uint8_t* valid, void* o,
                      float* lse, hipStream_t st) {
   const float sl2 = D.scale * kLog2e;
-  if (D.m >= 128) {
-    dim3 grid(D.N / 128, D.H, D.B);
-    hipLaunchKernelGGL((dense_fwd_kernel<T, HD, 2, true>), grid, dim3(256), 0, st, (const T*)q, (const T*)k,
-                       (const T*)v, valid, valid, D.H, D.N, D.N, D.m, sl2, (T*)o, lse);
-  } else {
-    dim3 grid(D.N / 64, D.H, D.B);
-    hipLaunchKernelGGL((dense_fwd_kernel<T, HD, 1, true>), grid, dim3(256), 0, st, (const T*)q, (const T*)k,
-                       (const T*)v, valid, valid, D.H, D.N, D.N, D.m, sl2, (T*)o, lse);
-  }
+  if (D.m >= 128)
+    launch_dense_fwd<T, HD, 2, true>(dim3(D.N / 128, D.H, D.B), st, q, k, v, valid, valid, D.H, D.N, D.N, D.m, sl2,
+                                     o, lse);
+  else
+    launch_dense_fwd<T, HD, 1, true>(dim3(D.N / 64, D.H, D.B), st, q, k, v, valid, valid, D.H, D.N, D.N, D.m, sl2,
+                                     o, lse);
   return hipGetLastError();
 }
 
@@ -209,9 +285,8 @@ template <typename T, int HD>
 hipError_t cmp_impl(const Dims& D, const void* q, const void* kc, const void* vc, const uint8_t* valid,
                     const uint8_t* cvalid, void* o, float* lse, hipStream_t st) {
   const float sl2 = D.scale * kLog2e;
-  dim3 grid(D.N / 128, D.H, D.B);
-  hipLaunchKernelGGL((dense_fwd_kernel<T, HD, 2, false>), grid, dim3(256), 0, st, (const T*)q, (const T*)kc,
-                     (const T*)vc, valid, cvalid, D.H, D.N, D.N / D.l, D.m, sl2, (T*)o, lse);
+  launch_dense_fwd<T, HD, 2, false>(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, valid, cvalid, D.H, D.N, D.N / D.l, D.m,
+                                    sl2, o, lse);
   return hipGetLastError();
 }
 

@@ -121,6 +121,12 @@ __device__ __forceinline__ float row16_sum(float x) {
 }
 
 // Order this wave's LDS accesses across lanes (data staged by the wave for itself).
+// Wait until every global load of this wave has returned (s_waitcnt vmcnt(0)). Placed
+// after loop-invariant operands are loaded and before a loop that prefetches its next
+// tile: the wait the compiler puts in front of the operands' first use inside the loop
+// would otherwise also wait, on every iteration, for that iteration's prefetch.
+__device__ __forceinline__ void vm_drain() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
