@@ -126,7 +126,7 @@ FwdWs fwd_ws_layout(const bsa::Dims& D) {
 }
 
 struct BwdWs {
-  size_t R, kc_lp, vc_lp, dkc_part, dvc_part, dkc, dvc, pk, pv, pkt, pvt, hist, seg_s, seg_e, dpre, pw1, psm, w1lp,
+  size_t R, terms, kc_lp, vc_lp, dkc_part, dvc_part, dkc, dvc, pk, pv, pkt, pvt, hist, seg_s, seg_e, dpre, pw1, psm, w1lp,
       total;
   int cmp_chunks, mlp_chunks, mlp_chunks_small;
   long long pairs, nseg;
@@ -144,6 +144,7 @@ BwdWs bwd_ws_layout(const bsa::Dims& D) {
   W.pairs = (long long)D.B * D.H * (D.N / D.g) * D.k;
   W.nseg = (long long)D.B * D.H * (D.N / D.ls);
   W.R = put(sizeof(float) * 3 * rows);
+  W.terms = put(sizeof(float) * 4 * 3 * rows);
   W.kc_lp = put(elem_bytes(D) * crows * D.d);
   W.vc_lp = put(elem_bytes(D) * crows * D.d);
   W.dkc_part = put(sizeof(float) * W.cmp_chunks * crows * D.d);
@@ -374,6 +375,7 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   A.hid_k = saved->hid_k; A.hid_v = saved->hid_v; A.sel = saved->sel_idx; A.cvalid = saved->cvalid;
   A.dq = dq; A.dk = dk; A.dv = dv; A.dgate = dgate;
   A.R = (float*)(w + W.R);
+  A.terms = (float*)(w + W.terms);
   A.kc_lp = w + W.kc_lp; A.vc_lp = w + W.vc_lp;
   A.dkc_part = (float*)(w + W.dkc_part); A.dvc_part = (float*)(w + W.dvc_part);
   A.dkc = (float*)(w + W.dkc); A.dvc = (float*)(w + W.dvc);

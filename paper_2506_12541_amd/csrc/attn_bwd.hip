@@ -24,8 +24,11 @@ __device__ __forceinline__ float lse_log2(float lse) { return lse == -__builtin_
 
 // ---- gate backward: R_b = rowsum(dO * o_b) per (b,h,n); dgamma_b = s'(gamma_b) sum_h R_b ----
 // 8 lanes per row, each lane a 16-byte piece per tensor; partial sums reduced by shuffles.
+// The same pass packs each query row's terms for the attention passes: log2 LSE, the gate
+// scale s = sigmoid(gamma_b) and delta D_b = s R_b (16 bytes per row and branch).
 template <typename T>
-__global__ void gate_bwd_rows_kernel(const T* dout, const T* ob, long long rows, int hd, float* R) {
+__global__ void gate_bwd_rows_kernel(const T* dout, const T* ob, long long rows, int hd, const float* lse,
+                                     const float* gate, int H, int N, float* R, float4* terms) {
   constexpr int EPV = 16 / (int)sizeof(T);
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long row = gid >> 3;
@@ -54,8 +57,13 @@ __global__ void gate_bwd_rows_kernel(const T* dout, const T* ob, long long rows,
     acc[br] = x;
   }
   if (row < rows && part == 0) {
+    const long long b = row / ((long long)H * N), n = row % N;
 #pragma unroll
-    for (int br = 0; br < 3; ++br) R[br * rows + row] = acc[br];
+    for (int br = 0; br < 3; ++br) {
+      R[br * rows + row] = acc[br];
+      const float sg = sigmoidf(gate[(b * N + n) * 3 + br]);
+      terms[br * rows + row] = make_float4(lse_log2(lse[br * rows + row]), sg, sg * acc[br], 0.f);
+    }
   }
 }
 
@@ -95,6 +103,7 @@ struct QTerms {
   const float* R;     // [B,H,N] rowsum(dO * o_b) of this branch
   const float* gate;  // [B,N,3]
   int br;
+  const float4* t4;   // [B,H,N] packed (log2 LSE, s, s * R, 0) of this branch
 };
 
 // ==== query-major pass, dense key sets (ball: own ball; compression: all tokens) ====
@@ -379,6 +388,146 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
         }
       }
     }
+  }
+  // lane: key wk0 + 16kb + r, dims 16db + 4j + i
+  const size_t out_base = (size_t)chunk * ((size_t)gridDim.z * nkeys_total * HD);
+#pragma unroll
+  for (int kb = 0; kb < KBW; ++kb) {
+    const int key = wk0 + 16 * kb + r;
+    if (key >= nkeys_total) continue;
+    const size_t off = out_base + ((size_t)bh * nkeys_total + key) * HD;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      store4(dk_out + off + 16 * db + 4 * j, dka[kb][db], scale);
+      store4(dv_out + off + 16 * db + 4 * j, dva[kb][db], 1.0f);
+    }
+  }
+}
+
+// bf16 variant of the key-major pass: 64-query tiles of Q, dO and the packed row terms
+// double-buffered in LDS (two distinct objects, loop unrolled by two) and filled by direct
+// global->LDS loads; the transposed operands of the dK^T and dV^T products come from
+// transpose reads of the same row-major tiles.
+template <int HD, int NW, bool BALL>
+__global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
+                                                                   const bf16_t* dout, const uint8_t* kvalid_all,
+                                                                   QTerms qt, int H, int N, int nkeys_total, int m,
+                                                                   int nchunks, float sl2, float scale, float* dk_out,
+                                                                   float* dv_out) {
+  constexpr int NCH = HD / 32, DB = HD / 16;
+  constexpr int KBW = 2;  // 16-key blocks per wave
+  typedef bf16x8 CT;
+  __shared__ __attribute__((aligned(16))) bf16_t qs0[kQT * HD], qs1[kQT * HD];
+  __shared__ __attribute__((aligned(16))) bf16_t ds0[kQT * HD], ds1[kQT * HD];
+  __shared__ __attribute__((aligned(16))) float4 tm0[kQT], tm1[kQT];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r = lane & 15, j = lane >> 4;
+  const int bh = blockIdx.z;
+  const int b = bh / H;
+  const int chunk = blockIdx.y;
+  const int key0 = blockIdx.x * (NW * 32);
+  const int wk0 = key0 + wid * 32;
+  int qbeg, qend;
+  if (BALL) {
+    qbeg = (key0 / m) * m;
+    qend = qbeg + m;
+  } else {
+    const int per = N / nchunks;
+    qbeg = chunk * per;
+    qend = qbeg + per;
+  }
+  const bf16_t* qh = q + (size_t)bh * N * HD;
+  const bf16_t* dh = dout + (size_t)bh * N * HD;
+  const float4* th = qt.t4 + (size_t)bh * N;
+
+  auto issue = [&](int t0, bf16_t* qd, bf16_t* dd, float4* td) {
+    dma_tile<HD, kQT, SWZ_TR, NW>(qd, qh, t0, N, wid, lane);
+    dma_tile<HD, kQT, SWZ_TR, NW>(dd, dh, t0, N, wid, lane);
+    if (wid == NW - 1) __builtin_amdgcn_global_load_lds(th + t0 + lane, td, 16, 0, 0);
+  };
+  issue(qbeg, qs0, ds0, tm0);
+
+  CT kf[KBW][NCH], vf[KBW][NCH];
+  bool kok[KBW];
+#pragma unroll
+  for (int kb = 0; kb < KBW; ++kb) {
+    const int key = wk0 + 16 * kb + r;
+    kok[kb] = key < nkeys_total && (kvalid_all == nullptr || kvalid_all[(size_t)b * nkeys_total + key]);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      kf[kb][c] = zero_chunk(kf[kb][c]);
+      vf[kb][c] = zero_chunk(vf[kb][c]);
+      if (key < nkeys_total) {
+        kf[kb][c] = load_chunk(k + ((size_t)bh * nkeys_total + key) * HD + 32 * c + 8 * j);
+        vf[kb][c] = load_chunk(v + ((size_t)bh * nkeys_total + key) * HD + 32 * c + 8 * j);
+      }
+    }
+  }
+  f32x4 dka[KBW][DB], dva[KBW][DB];
+#pragma unroll
+  for (int kb = 0; kb < KBW; ++kb)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) { dka[kb][db] = f32x4{0.f, 0.f, 0.f, 0.f}; dva[kb][db] = dka[kb][db]; }
+
+  auto step = [&](int t0, const bf16_t* qs, const bf16_t* ds, const float4* tm, bf16_t* qn, bf16_t* dn,
+                  float4* tn) {
+    vm_drain();          // this wave's loads of the tile have landed
+    __syncthreads();     // ... and every wave's; the previous tile is no longer read
+    if (t0 + kQT < qend) issue(t0 + kQT, qn, dn, tn);
+#pragma unroll
+    for (int qp = 0; qp < kQT / 32; ++qp) {
+      f32x4 sv[2][KBW], dp[2][KBW];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int qb = 2 * qp + u;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+          CT aq = lds_row_chunk<HD, SWZ_TR>(qs, 16 * qb + r, 4 * c + j);
+          CT ad = lds_row_chunk<HD, SWZ_TR>(ds, 16 * qb + r, 4 * c + j);
+#pragma unroll
+          for (int kb = 0; kb < KBW; ++kb) {
+            sv[u][kb] = mma(aq, kf[kb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sv[u][kb]);
+            dp[u][kb] = mma(ad, vf[kb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : dp[u][kb]);
+          }
+        }
+      }
+      // lane holds queries 16qb + 4j + i for its key
+      float a8[KBW][8], b8[KBW][8];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int qb = 2 * qp + u;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float4 t = tm[16 * qb + 4 * j + i];   // log2 LSE, s, s R
+#pragma unroll
+          for (int kb = 0; kb < KBW; ++kb) {
+            const float p = kok[kb] ? fast_exp2(__builtin_fmaf(sv[u][kb][i], sl2, -t.x)) : 0.f;
+            a8[kb][4 * u + i] = p * t.y;
+            b8[kb][4 * u + i] = p * __builtin_fmaf(dp[u][kb][i], t.y, -t.z);
+          }
+        }
+      }
+      CT pf[KBW], sf[KBW];
+#pragma unroll
+      for (int kb = 0; kb < KBW; ++kb) {
+        pf[kb] = make_chunk<bf16_t>(a8[kb]);
+        sf[kb] = make_chunk<bf16_t>(b8[kb]);
+      }
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        CT ao = lds_tr_chunk<HD>(ds, 32 * qp, 16 * db, lane);
+        CT aq = lds_tr_chunk<HD>(qs, 32 * qp, 16 * db, lane);
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb) {
+          dva[kb][db] = mma(ao, pf[kb], dva[kb][db]);
+          dka[kb][db] = mma(aq, sf[kb], dka[kb][db]);
+        }
+      }
+    }
+  };
+  for (int t0 = qbeg; t0 < qend; t0 += 2 * kQT) {
+    step(t0, qs0, ds0, tm0, qs1, ds1, tm1);
+    if (t0 + kQT < qend) step(t0 + kQT, qs1, ds1, tm1, qs0, ds0, tm0);
   }
   // lane: key wk0 + 16kb + r, dims 16db + 4j + i
   const size_t out_base = (size_t)chunk * ((size_t)gridDim.z * nkeys_total * HD);
@@ -732,6 +881,20 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_kernel(const T* q, const T* k,
 
 constexpr int kCmpChunks = 8;   // query chunks of the compressed branch's key-major pass
 
+// Key-major pass launcher: bf16 layers take the direct-load kernel, f32 layers the
+// register-staged one.
+template <typename T, int HD, int NW, bool BALL>
+void launch_bwd_kv(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v, const T* dout,
+                   const uint8_t* kvalid, QTerms qt, int H, int N, int nkeys_total, int m, int nchunks, float sl2,
+                   float scale, float* dk, float* dv) {
+  if constexpr (sizeof(T) == 2)
+    hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL>), grid, dim3(NW * 64), 0, st, q, k, v, dout, kvalid,
+                       qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
+  else
+    hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, NW, BALL>), grid, dim3(NW * 64), 0, st, q, k, v, dout, kvalid, qt,
+                       H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
+}
+
 template <typename T, int HD>
 hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
   const long long rows = D.rows();
@@ -740,13 +903,14 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
   // per-branch row sums and the gate gradient
   BSA_PHASE("bwd.gate", st, {
   hipLaunchKernelGGL(gate_bwd_rows_kernel<T>, dim3((unsigned)((rows * 8 + 255) / 256)), dim3(256), 0, st, (const T*)A.dout,
-                     (const T*)A.o_branch, rows, HD, A.R);
+                     (const T*)A.o_branch, rows, HD, A.lse, A.gate, D.H, D.N, A.R, (float4*)A.terms);
   hipLaunchKernelGGL(gate_bwd_kernel, dim3((D.B * D.N + 255) / 256), dim3(256), 0, st, A.R, A.gate, A.valid, D.B, D.H,
                      D.N, A.dgate);
   });
-  QTerms qball{A.lse, A.R, A.gate, 0};
-  QTerms qcmp{A.lse + rows, A.R + rows, A.gate, 1};
-  QTerms qslc{A.lse + 2 * rows, A.R + 2 * rows, A.gate, 2};
+  const float4* t4 = (const float4*)A.terms;
+  QTerms qball{A.lse, A.R, A.gate, 0, t4};
+  QTerms qcmp{A.lse + rows, A.R + rows, A.gate, 1, t4 + rows};
+  QTerms qslc{A.lse + 2 * rows, A.R + 2 * rows, A.gate, 2, t4 + 2 * rows};
   const T* q = (const T*)A.q;
   const T* k = (const T*)A.k;
   const T* v = (const T*)A.v;
@@ -780,22 +944,20 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
                      A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq));
   // ---- dK, dV of the ball branch (written) ----
   BSA_PHASE("bwd.kv_ball", st, {
-  if (D.m >= 128) {
-    hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, 4, true>), dim3(D.N / 128, 1, D.B * D.H), dim3(256), 0, st, q, k,
-                       v, dout, A.valid, qball, D.H, D.N, D.N, D.m, 1, sl2, D.scale, A.dk, A.dv);
-  } else {
-    hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, 2, true>), dim3(D.N / 64, 1, D.B * D.H), dim3(128), 0, st, q, k, v,
-                       dout, A.valid, qball, D.H, D.N, D.N, D.m, 1, sl2, D.scale, A.dk, A.dv);
-  }
+  if (D.m >= 128)
+    (launch_bwd_kv<T, HD, 4, true>)(dim3(D.N / 128, 1, D.B * D.H), st, q, k, v, dout, A.valid, qball, D.H, D.N, D.N,
+                                  D.m, 1, sl2, D.scale, A.dk, A.dv);
+  else
+    (launch_bwd_kv<T, HD, 2, true>)(dim3(D.N / 64, 1, D.B * D.H), st, q, k, v, dout, A.valid, qball, D.H, D.N, D.N,
+                                  D.m, 1, sl2, D.scale, A.dk, A.dv);
   });
   // ---- dK^, dV^ of the compressed branch: chunked partials, then a fixed-order sum ----
   {
     const int nch = D.N / kCmpChunks >= kQT ? kCmpChunks : 1;
     BSA_PHASE("bwd.kv_cmp", st,
-    hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, 4, false>), dim3((nct + 127) / 128, nch, D.B * D.H), dim3(256), 0,
-                       st, q, kc, vc, dout, A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, nch, sl2,
-                       D.scale, A.dkc_part,
-                       A.dvc_part));
+    (launch_bwd_kv<T, HD, 4, false>)(dim3((nct + 127) / 128, nch, D.B * D.H), st, q, kc, vc, dout,
+                                   A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, nch, sl2, D.scale,
+                                   A.dkc_part, A.dvc_part));
     const long long n = D.cmp_rows() * HD;
     hipLaunchKernelGGL(sum_chunks_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.dkc_part, nch, n,
                        A.dkc);

@@ -64,6 +64,7 @@ struct BwdArgs {
   float *dq, *dk, *dv, *dgate;
   // workspace
   float* R;                      // [3, B, H, N]
+  float* terms;                  // [3, B, H, N, 4]: log2 LSE, s, s * R, 0 per query row
   void *kc_lp, *vc_lp;           // compressed tokens in the storage type
   float *dkc_part, *dvc_part;    // [chunks, B, H, N/l, d]
   float *dkc, *dvc;              // [B, H, N/l, d]
