@@ -241,6 +241,138 @@ __global__ void __launch_bounds__(256) dense_bwd_q_kernel(const T* q, const T* k
   }
 }
 
+// bf16 variant of the query-major pass: 64-key K and V tiles double-buffered in LDS (two
+// distinct objects, loop unrolled by two) and filled by direct global->LDS loads; the K^T
+// operand of the dQ product comes from transpose reads of the row-major K tile.
+template <int HD, int QB, bool BALL, bool ADD>
+__global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
+                                                              const bf16_t* dout, const uint8_t* kvalid_all,
+                                                              QTerms qt, int H, int N, int nkeys_total, int m,
+                                                              float sl2, float scale, float* dq) {
+  constexpr int NCH = HD / 32, DB = HD / 16;
+  constexpr int KT = kKT;
+  constexpr int KB = KT / 16;
+  typedef bf16x8 CT;
+  __shared__ __attribute__((aligned(16))) bf16_t ks0[KT * HD], ks1[KT * HD];
+  __shared__ __attribute__((aligned(16))) bf16_t vs0[KT * HD], vs1[KT * HD];
+  __shared__ __attribute__((aligned(16))) uint8_t ok0[KT], ok1[KT];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r = lane & 15, j = lane >> 4;
+  const int b = blockIdx.z, h = blockIdx.y;
+  const long long bh = (long long)b * H + h;
+  const int q0 = blockIdx.x * (64 * QB);
+  const int nkeys = BALL ? m : nkeys_total;
+  const int key0 = BALL ? (q0 / m) * m : 0;
+  const bf16_t* kh = k + (bh * nkeys_total + key0) * HD;
+  const bf16_t* vh = v + (bh * nkeys_total + key0) * HD;
+  const uint8_t* kval = kvalid_all ? kvalid_all + (size_t)b * nkeys_total + key0 : nullptr;
+  const int wq0 = q0 + wid * 16 * QB;
+
+  // key-validity bytes are read before the tile loads, so waiting for them does not
+  // wait for the tile
+  auto issue = [&](int t0, bf16_t* kd, bf16_t* vd, uint8_t* okd) {
+    uint8_t okv = 0;
+    if (threadIdx.x < KT) {
+      const int key = t0 + threadIdx.x;
+      okv = key < nkeys && (kval == nullptr || kval[key]);
+    }
+    dma_tile<HD, KT, SWZ_TR, 4>(kd, kh, t0, nkeys, wid, lane);
+    dma_tile<HD, KT, SWZ_TR, 4>(vd, vh, t0, nkeys, wid, lane);
+    if (threadIdx.x < KT) okd[threadIdx.x] = okv;
+  };
+  issue(0, ks0, vs0, ok0);
+
+  CT qf[QB][NCH], df[QB][NCH];
+  float l2[QB], dd[QB], gs[QB];
+  f32x4 acc[QB][DB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const long long row = bh * N + wq0 + 16 * qb + r;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      qf[qb][c] = load_chunk(q + row * HD + 32 * c + 8 * j);
+      df[qb][c] = load_chunk(dout + row * HD + 32 * c + 8 * j);
+    }
+    const float4 t = qt.t4[row];   // log2 LSE, s, s R
+    l2[qb] = t.x;
+    gs[qb] = t.y;
+    dd[qb] = t.z;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) acc[qb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  auto step = [&](int t0, const bf16_t* kt, const bf16_t* vt, const uint8_t* ok, bf16_t* kn, bf16_t* vn,
+                  uint8_t* okn) {
+    vm_drain();          // this wave's loads of the tile have landed
+    __syncthreads();     // ... and every wave's; the previous tile is no longer read
+    if (t0 + KT < nkeys) issue(t0 + KT, kn, vn, okn);
+    const bool all_ok = kval == nullptr && t0 + KT <= nkeys;
+    // key validity of the rows 4j+i of each key block, one 32-bit word per block
+    uint32_t okw[KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) okw[kb] = all_ok ? 0x01010101u : *reinterpret_cast<const uint32_t*>(&ok[kb * 16 + 4 * j]);
+    f32x4 sv[QB][KB], dp[QB][KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        CT ak = lds_row_chunk<HD, SWZ_TR>(kt, kb * 16 + r, 4 * c + j);
+        CT av = lds_row_chunk<HD, SWZ_TR>(vt, kb * 16 + r, 4 * c + j);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+          sv[qb][kb] = mma(ak, qf[qb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sv[qb][kb]);
+          dp[qb][kb] = mma(av, df[qb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : dp[qb][kb]);
+        }
+      }
+    CT dsf[QB][KB / 2];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float v8[KB][4];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float e = fast_exp2(__builtin_fmaf(sv[qb][kb][i], sl2, -l2[qb]));
+          const float p = ((okw[kb] >> (8 * i)) & 1u) ? e : 0.f;
+          v8[kb][i] = p * __builtin_fmaf(dp[qb][kb][i], gs[qb], -dd[qb]);
+        }
+#pragma unroll
+      for (int kp = 0; kp < KB / 2; ++kp) {
+        float w8[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) { w8[i] = v8[2 * kp][i]; w8[4 + i] = v8[2 * kp + 1][i]; }
+        dsf[qb][kp] = make_chunk<bf16_t>(w8);
+      }
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int kp = 0; kp < KB / 2; ++kp) {
+        CT a = lds_tr_chunk<HD>(kt, 32 * kp, 16 * db, lane);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) acc[qb][db] = mma(a, dsf[qb][kp], acc[qb][db]);
+      }
+  };
+  for (int t0 = 0; t0 < nkeys; t0 += 2 * KT) {
+    step(t0, ks0, vs0, ok0, ks1, vs1, ok1);
+    if (t0 + KT < nkeys) step(t0 + KT, ks1, vs1, ok1, ks0, vs0, ok0);
+  }
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const long long row = bh * N + wq0 + 16 * qb + r;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      float* dst = dq + row * HD + 16 * db + 4 * j;
+      f32x4 val = acc[qb][db] * scale;
+      if (ADD) {
+        float4 old = *reinterpret_cast<float4*>(dst);
+        val[0] += old.x; val[1] += old.y; val[2] += old.z; val[3] += old.w;
+      }
+      store4(dst, val, 1.0f);
+    }
+  }
+}
+
 // ==== key-major pass, dense key sets: dK, dV of NW*32 keys per workgroup ====
 // Queries are staged 64 at a time in LDS (row-major for the S and dP products, transposed
 // for the dK^T and dV^T products); each wave owns 32 keys in registers.
@@ -881,6 +1013,20 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_kernel(const T* q, const T* k,
 
 constexpr int kCmpChunks = 8;   // query chunks of the compressed branch's key-major pass
 
+// Query-major pass launcher: bf16 layers take the direct-load kernel, f32 layers the
+// register-staged one.
+template <typename T, int HD, int QB, bool BALL, bool ADD>
+void launch_bwd_q(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v, const T* dout,
+                  const uint8_t* kvalid, QTerms qt, int H, int N, int nkeys_total, int m, float sl2, float scale,
+                  float* dq) {
+  if constexpr (sizeof(T) == 2)
+    hipLaunchKernelGGL((dense_bwd_q_dma_kernel<HD, QB, BALL, ADD>), grid, dim3(256), 0, st, q, k, v, dout, kvalid,
+                       qt, H, N, nkeys_total, m, sl2, scale, dq);
+  else
+    hipLaunchKernelGGL((dense_bwd_q_kernel<T, HD, QB, BALL, ADD>), grid, dim3(256), 0, st, q, k, v, dout, kvalid, qt,
+                       H, N, nkeys_total, m, sl2, scale, dq);
+}
+
 // Key-major pass launcher: bf16 layers take the direct-load kernel, f32 layers the
 // register-staged one.
 template <typename T, int HD, int NW, bool BALL>
@@ -928,17 +1074,16 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
   }
   // ---- dQ: ball (write), compressed (add), selection (add) ----
   BSA_PHASE("bwd.dq_ball", st, {
-  if (D.m >= 128) {
-    hipLaunchKernelGGL((dense_bwd_q_kernel<T, HD, 2, true, false>), dim3(D.N / 128, D.H, D.B), dim3(256), 0, st, q, k,
-                       v, dout, A.valid, qball, D.H, D.N, D.N, D.m, sl2, D.scale, A.dq);
-  } else {
-    hipLaunchKernelGGL((dense_bwd_q_kernel<T, HD, 1, true, false>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, q, k,
-                       v, dout, A.valid, qball, D.H, D.N, D.N, D.m, sl2, D.scale, A.dq);
-  }
+  if (D.m >= 128)
+    (launch_bwd_q<T, HD, 2, true, false>)(dim3(D.N / 128, D.H, D.B), st, q, k, v, dout, A.valid, qball, D.H, D.N,
+                                          D.N, D.m, sl2, D.scale, A.dq);
+  else
+    (launch_bwd_q<T, HD, 1, true, false>)(dim3(D.N / 64, D.H, D.B), st, q, k, v, dout, A.valid, qball, D.H, D.N,
+                                          D.N, D.m, sl2, D.scale, A.dq);
   });
   BSA_PHASE("bwd.dq_cmp", st,
-  hipLaunchKernelGGL((dense_bwd_q_kernel<T, HD, 2, false, true>), dim3(D.N / 128, D.H, D.B), dim3(256), 0, st, q, kc,
-                     vc, dout, A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq));
+  (launch_bwd_q<T, HD, 2, false, true>)(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, dout,
+                                        A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq));
   BSA_PHASE("bwd.dq_slc", st,
   hipLaunchKernelGGL((slc_bwd_q_kernel<T, HD>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, q, k, v, dout, A.valid,
                      A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq));
