@@ -236,6 +236,19 @@ __device__ __forceinline__ bf16x8 lds_tr_chunk(const bf16_t* t, int k0, int m0, 
   return __builtin_bit_cast(bf16x8, make_uint4(v0.x, v0.y, v1.x, v1.y));
 }
 
+// MFMA 16x16x16 A operand of the transposed tile: lane (r = lane % 16, j = lane / 16)
+// receives X[k0 + 4j + i][m0 + r], i = 0..3 (one ds_read_b64_tr_b16; addressing as above).
+template <int HD>
+__device__ __forceinline__ uint2 lds_tr4(const bf16_t* t, int k0, int m0, int lane) {
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  const int p = lane & 15, j = lane >> 4;
+  const int col = m0 + 4 * (p & 3);
+  const int x0 = k0 + 4 * j + (p >> 2);
+  const bf16_t* a0 = t + x0 * HD + 8 * ((col >> 3) ^ swz<HD, SWZ_TR>(x0)) + (col & 7);
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)a0));
+}
+
 // Online-softmax state of one wave over QB blocks of 16 queries.
 // Two VALU savings on the hot path: (1) the reference maximum is only raised when a new
 // tile maximum exceeds it by more than kRescale (log2 units), so the O accumulators are
