@@ -276,8 +276,8 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
       const int key = t0 + threadIdx.x;
       okv = key < nkeys && (kval == nullptr || kval[key]);
     }
-    dma_tile<HD, KT, SWZ_TR, 4>(kd, kh, t0, nkeys, wid, lane);
-    dma_tile<HD, KT, SWZ_TR, 4>(vd, vh, t0, nkeys, wid, lane);
+    dma_tile<HD, KT, 4>(kd, kh, t0, nkeys, wid, lane);
+    dma_tile<HD, KT, 4>(vd, vh, t0, nkeys, wid, lane);
     if (threadIdx.x < KT) okd[threadIdx.x] = okv;
   };
   issue(0, ks0, vs0, ok0);
@@ -316,8 +316,8 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int c = 0; c < NCH; ++c) {
-        CT ak = lds_row_chunk<HD, SWZ_TR>(kt, kb * 16 + r, 4 * c + j);
-        CT av = lds_row_chunk<HD, SWZ_TR>(vt, kb * 16 + r, 4 * c + j);
+        CT ak = lds_row_chunk<HD>(kt, kb * 16 + r, 4 * c + j);
+        CT av = lds_row_chunk<HD>(vt, kb * 16 + r, 4 * c + j);
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
           sv[qb][kb] = mma(ak, qf[qb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sv[qb][kb]);
@@ -573,8 +573,8 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
   const float4* th = qt.t4 + (size_t)bh * N;
 
   auto issue = [&](int t0, bf16_t* qd, bf16_t* dd, float4* td) {
-    dma_tile<HD, kQT, SWZ_TR, NW>(qd, qh, t0, N, wid, lane);
-    dma_tile<HD, kQT, SWZ_TR, NW>(dd, dh, t0, N, wid, lane);
+    dma_tile<HD, kQT, NW>(qd, qh, t0, N, wid, lane);
+    dma_tile<HD, kQT, NW>(dd, dh, t0, N, wid, lane);
     if (wid == NW - 1) __builtin_amdgcn_global_load_lds(th + t0 + lane, td, 16, 0, 0);
   };
   issue(qbeg, qs0, ds0, tm0);
@@ -614,8 +614,8 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
         const int qb = 2 * qp + u;
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-          CT aq = lds_row_chunk<HD, SWZ_TR>(qs, 16 * qb + r, 4 * c + j);
-          CT ad = lds_row_chunk<HD, SWZ_TR>(ds, 16 * qb + r, 4 * c + j);
+          CT aq = lds_row_chunk<HD>(qs, 16 * qb + r, 4 * c + j);
+          CT ad = lds_row_chunk<HD>(ds, 16 * qb + r, 4 * c + j);
 #pragma unroll
           for (int kb = 0; kb < KBW; ++kb) {
             sv[u][kb] = mma(aq, kf[kb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sv[u][kb]);
@@ -1184,8 +1184,8 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_dma_kernel(const bf16_t* q, co
   auto issue = [&](int i, bf16_t* slot) {
     const int qr0 = rows[min(i, cnt - 1)];
     bf16_t* base = slot + wid * SLOT;
-    dma_tile<HD, 16, SWZ_TR, 1>(base, qh, qr0, N, 0, lane);
-    dma_tile<HD, 16, SWZ_TR, 1>(base + SL, dh, qr0, N, 0, lane);
+    dma_tile<HD, 16, 1>(base, qh, qr0, N, 0, lane);
+    dma_tile<HD, 16, 1>(base + SL, dh, qr0, N, 0, lane);
     __builtin_amdgcn_global_load_lds(th + min(qr0 + (lane & 15), N - 1), base + 2 * SL, 16, 0, 0);
   };
   // global->LDS loads per item: waiting until at most this many are outstanding leaves
@@ -1201,8 +1201,8 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_dma_kernel(const bf16_t* q, co
     CT aq[NCH], ad[NCH];
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-      aq[c] = lds_row_chunk<HD, SWZ_TR>(qs, r, 4 * c + j);
-      ad[c] = lds_row_chunk<HD, SWZ_TR>(ds, r, 4 * c + j);
+      aq[c] = lds_row_chunk<HD>(qs, r, 4 * c + j);
+      ad[c] = lds_row_chunk<HD>(ds, r, 4 * c + j);
     }
     float cl[4], cg[4], cdv[4];
 #pragma unroll

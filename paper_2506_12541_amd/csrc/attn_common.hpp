@@ -175,15 +175,15 @@ struct TileIO {
 
 // ---- bf16 tiles staged without registers: direct global->LDS loads, transpose reads ----
 // A tile of rows x HD bf16 lives in LDS row-major without padding; the 16-byte chunk c of
-// row x is stored at chunk c ^ swz(x). Row-fragment reads (16 lanes = 16 consecutive rows,
-// one chunk each) want consecutive rows on distinct banks (SWZ_ROW); transpose reads (16
-// lanes = 4 consecutive rows x two chunks) want those chunk pairs on distinct banks (SWZ_TR).
-enum { SWZ_ROW = 0, SWZ_TR = 1 };
-template <int HD, int MODE>
+// row x is stored at chunk c ^ swz(x). The swizzle was chosen by measuring LDS bank
+// conflicts on gfx950 (SQ_LDS_BANK_CONFLICT): with it both access patterns below, row
+// fragments (ds_read_b128, 16 lanes = 16 consecutive rows) and transpose reads
+// (ds_read_b64_tr_b16, 16 lanes = 4 consecutive rows x two chunks), run conflict-free, at
+// 4 and 2 cycles per instruction.
+template <int HD>
 __device__ __forceinline__ int swz(int x) {
   static_assert(HD == 32 || HD == 64, "head dim");
-  if (HD == 64) return MODE == SWZ_ROW ? (x & 7) : (((x & 3) << 1) | ((x >> 2) & 1));
-  return MODE == SWZ_ROW ? ((x >> 1) & 3) : (x & 2);
+  return HD == 64 ? (x & 7) : ((x >> 1) & 3);
 }
 
 // Rows [r0, r0 + ROWS) of a row-major [nrows, HD] matrix into an LDS tile, by NW waves.
@@ -191,7 +191,7 @@ __device__ __forceinline__ int swz(int x) {
 // fills bytes [16L, 16L + 16)); the lane picks the global chunk that belongs there. Rows
 // at or past nrows repeat row nrows - 1 (the caller masks them). Completion is tracked by
 // vmcnt: vm_drain() and a barrier make the tile visible to the workgroup.
-template <int HD, int ROWS, int MODE, int NW>
+template <int HD, int ROWS, int NW>
 __device__ __forceinline__ void dma_tile(bf16_t* lds, const bf16_t* g, int r0, int nrows, int wid, int lane) {
   constexpr int CPR = HD / 8;           // 16-byte chunks per row
   constexpr int NI = ROWS * CPR / 64;   // 1 KB wave instructions per tile
@@ -201,23 +201,23 @@ __device__ __forceinline__ void dma_tile(bf16_t* lds, const bf16_t* g, int r0, i
     const int blk = wid * (NI / NW) + u;
     const int idx = blk * 64 + lane;
     const int row = idx / CPR;
-    const int lc = (idx % CPR) ^ swz<HD, MODE>(row);
+    const int lc = (idx % CPR) ^ swz<HD>(row);
     const int gr = r0 + row < nrows ? r0 + row : nrows - 1;
     __builtin_amdgcn_global_load_lds(g + (size_t)gr * HD + 8 * lc, lds + blk * 512, 16, 0, 0);
   }
 }
 
 // 8 consecutive elements of row x starting at logical chunk lc (an MFMA row fragment).
-template <int HD, int MODE>
+template <int HD>
 __device__ __forceinline__ bf16x8 lds_row_chunk(const bf16_t* t, int x, int lc) {
-  return *reinterpret_cast<const bf16x8*>(t + x * HD + 8 * (lc ^ swz<HD, MODE>(x)));
+  return *reinterpret_cast<const bf16x8*>(t + x * HD + 8 * (lc ^ swz<HD>(x)));
 }
 
 // MFMA A operand of the transposed tile, in the contraction order of a probability chunk
 // built from two 16-key accumulator tiles (elements 0-3: keys 4j + i of the first tile,
 // 4-7: keys 4j + i of the second): lane (r = lane % 16, j = lane / 16) receives
 // X[k0 + 4j + i][m0 + r] and X[k0 + 16 + 4j + i][m0 + r], i = 0..3, from the row-major
-// tile X (SWZ_TR layout), with two ds_read_b64_tr_b16. Within each 16-lane group that
+// tile X, with two ds_read_b64_tr_b16. Within each 16-lane group that
 // instruction hands lane l element l % 4 of the 4-element runs addressed by lanes l / 4,
 // 4 + l / 4, 8 + l / 4, 12 + l / 4; lane p therefore addresses row k0 + 4j + p / 4 (then
 // + 16), columns m0 + 4 (p % 4) + [0, 4).
@@ -229,8 +229,8 @@ __device__ __forceinline__ bf16x8 lds_tr_chunk(const bf16_t* t, int k0, int m0, 
   const int col = m0 + 4 * (p & 3);
   const int lc = col >> 3, sub = col & 7;
   const int x0 = k0 + 4 * j + (p >> 2), x1 = x0 + 16;
-  const bf16_t* a0 = t + x0 * HD + 8 * (lc ^ swz<HD, SWZ_TR>(x0)) + sub;
-  const bf16_t* a1 = t + x1 * HD + 8 * (lc ^ swz<HD, SWZ_TR>(x1)) + sub;
+  const bf16_t* a0 = t + x0 * HD + 8 * (lc ^ swz<HD>(x0)) + sub;
+  const bf16_t* a1 = t + x1 * HD + 8 * (lc ^ swz<HD>(x1)) + sub;
   const uint2 v0 = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)a0));
   const uint2 v1 = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)a1));
   return __builtin_bit_cast(bf16x8, make_uint4(v0.x, v0.y, v1.x, v1.y));
@@ -245,7 +245,7 @@ __device__ __forceinline__ uint2 lds_tr4(const bf16_t* t, int k0, int m0, int la
   const int p = lane & 15, j = lane >> 4;
   const int col = m0 + 4 * (p & 3);
   const int x0 = k0 + 4 * j + (p >> 2);
-  const bf16_t* a0 = t + x0 * HD + 8 * ((col >> 3) ^ swz<HD, SWZ_TR>(x0)) + (col & 7);
+  const bf16_t* a0 = t + x0 * HD + 8 * ((col >> 3) ^ swz<HD>(x0)) + (col & 7);
   return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)a0));
 }
 

@@ -120,8 +120,8 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q,
       const int key = t0 + threadIdx.x;
       okv = key < nkeys && (kval == nullptr || kval[key]);
     }
-    dma_tile<HD, kFT, SWZ_ROW, NW>(kd, kh, t0, nkeys, wid, lane);
-    dma_tile<HD, kFT, SWZ_TR, NW>(vd, vh, t0, nkeys, wid, lane);
+    dma_tile<HD, kFT, NW>(kd, kh, t0, nkeys, wid, lane);
+    dma_tile<HD, kFT, NW>(vd, vh, t0, nkeys, wid, lane);
     if (threadIdx.x < kFT) okd[threadIdx.x] = okv;
   };
   WaveAttn<bf16_t, HD, QB> w;
@@ -132,7 +132,7 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q,
     vm_drain();          // this wave's loads of the tile have landed
     __syncthreads();     // ... and every wave's; the previous tile is no longer read
     if (t0 + kFT < nkeys) issue(t0 + kFT, kn, vn, okn);
-    auto kfrag = [&](int kb, int c) { return lds_row_chunk<HD, SWZ_ROW>(kt, kb * 16 + r, 4 * c + j); };
+    auto kfrag = [&](int kb, int c) { return lds_row_chunk<HD>(kt, kb * 16 + r, 4 * c + j); };
     auto vfrag = [&](int db, int kp) { return lds_tr_chunk<HD>(vt, 32 * kp, 16 * db, lane); };
     if (kval == nullptr && t0 + kFT <= nkeys) {
       w.template tile<kFT / 16>(sl2, kfrag, vfrag, [](int, int, int) { return true; });
