@@ -847,6 +847,133 @@ __global__ void seg_bounds_kernel(const uint32_t* keys, long long total, uint32_
   if (i == total - 1 || keys[i + 1] != kx) seg_end[kx] = (int)(i + 1);
 }
 
+// bf16 variant of the selection query-major pass: each wave double-buffers its key tiles
+// (the 32 K rows and 32 V rows of two sub-blocks) in LDS, filled by direct global->LDS loads
+// one tile ahead (two distinct LDS objects, straight-line body unrolled by two; tiles past
+// the end are loaded from row 0 and masked). K^T for the dQ product comes from transpose
+// reads of the K tile. Key validity is gathered into 16-bit masks with the sub-block list.
+template <int HD, int NW>
+__global__ void __launch_bounds__(NW * 64) slc_bwd_q_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
+                                                                const bf16_t* dout, const uint8_t* valid_all,
+                                                                const int* sel, QTerms qt, int H, int N, int ls,
+                                                                int kk, int g, float sl2, float scale, float* dq) {
+  constexpr int NCH = HD / 32, DB = HD / 16;
+  constexpr int TILE = 32 * HD;    // one 32-key tile
+  constexpr int SLOT = 2 * TILE;   // K tile, V tile
+  typedef bf16x8 CT;
+  __shared__ __attribute__((aligned(16))) bf16_t buf0[NW * SLOT], buf1[NW * SLOT];
+  __shared__ int sub_all[NW][kMaxSub];
+  __shared__ uint32_t okm_all[NW][kMaxSub];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r = lane & 15, j = lane >> 4;
+  const int b = blockIdx.z, h = blockIdx.y;
+  const long long bh = (long long)b * H + h;
+  const int wq0 = (blockIdx.x * NW + wid) * 16;
+  const int G = g >= 16 ? 1 : 16 / g;
+  const int p0 = wq0 / g;
+  const int my_gi = g >= 16 ? 0 : r / g;
+  const int ngroups = N / g;
+  const bf16_t* kh = k + bh * N * HD;
+  const bf16_t* vh = v + bh * N * HD;
+  const uint8_t* val = valid_all ? valid_all + (size_t)b * N : nullptr;
+  const int* selp = sel + ((size_t)bh * ngroups + p0) * kk;
+  int* sub = sub_all[wid];
+  uint32_t* okm = okm_all[wid];
+
+  const int nsub = G * kk * (ls / 16);
+  for (int e = lane; e < nsub; e += 64) {
+    const int slot = (e * 16) / ls;
+    const int gi = slot / kk;
+    const int id = selp[gi * kk + slot % kk];
+    const int tok0 = id * ls + (e * 16) % ls;
+    sub[e] = id < 0 ? -1 : ((gi << 24) | tok0);
+    uint32_t m = 0;
+    if (id >= 0) {
+      m = 0xFFFFu;
+      if (val)
+        for (int t = 0; t < 16; ++t)
+          if (!val[tok0 + t]) m &= ~(1u << t);
+    }
+    okm[e] = m;
+  }
+  const long long row = bh * N + wq0 + r;
+  CT qf[NCH], df[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    qf[c] = load_chunk(q + row * HD + 32 * c + 8 * j);
+    df[c] = load_chunk(dout + row * HD + 32 * c + 8 * j);
+  }
+  const float4 tr = qt.t4[row];   // log2 LSE, s, s R of this lane's query
+  const float l2 = tr.x, gs = tr.y, dd = tr.z;
+  f32x4 acc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  vm_drain();
+  wave_sync();   // LDS regions are per wave
+
+  const int nt = __builtin_amdgcn_readfirstlane((nsub + 1) / 2);   // 32-key tiles
+  auto issue = [&](int t, bf16_t* slot) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const int e = 2 * t + kb < nsub ? sub[2 * t + kb] : -1;
+      const int r0 = e >= 0 ? (e & 0xFFFFFF) : 0;
+      bf16_t* base = slot + wid * SLOT + kb * 16 * HD;
+      dma_tile<HD, 16, 1>(base, kh, r0, N, 0, lane);
+      dma_tile<HD, 16, 1>(base + TILE, vh, r0, N, 0, lane);
+    }
+  };
+  auto step = [&](int t, const bf16_t* cur, bf16_t* next) {
+    vm_drain();   // this tile has landed
+    issue(t + 1, next);
+    const bf16_t* kt = cur + wid * SLOT;
+    const bf16_t* vt = kt + TILE;
+    uint32_t m[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const int se = 2 * t + kb;
+      const int e = t < nt && se < nsub ? sub[se] : -1;
+      m[kb] = e >= 0 && (e >> 24) == my_gi ? okm[se] : 0u;
+    }
+    f32x4 sv[2], dp[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      sv[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dp[kb] = sv[kb];
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        sv[kb] = mma(lds_row_chunk<HD>(kt, 16 * kb + r, 4 * c + j), qf[c], sv[kb]);
+        dp[kb] = mma(lds_row_chunk<HD>(vt, 16 * kb + r, 4 * c + j), df[c], dp[kb]);
+      }
+    }
+    float w8[8];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float e = fast_exp2(__builtin_fmaf(sv[kb][i], sl2, -l2));
+        const float p = ((m[kb] >> (4 * j + i)) & 1u) ? e : 0.f;
+        w8[4 * kb + i] = p * __builtin_fmaf(dp[kb][i], gs, -dd);
+      }
+    const CT dsf = make_chunk<bf16_t>(w8);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) acc[db] = mma(lds_tr_chunk_nowait<HD>(kt, 0, 16 * db, lane), dsf, acc[db]);
+  };
+  issue(0, buf0);
+  for (int t = 0; t < nt; t += 2) {   // straight-line body
+    step(t, buf0, buf1);
+    step(t + 1, buf1, buf0);
+  }
+  vm_drain();   // the loads past the end have landed
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    float* dst = dq + row * HD + 16 * db + 4 * j;
+    float4 old = *reinterpret_cast<float4*>(dst);
+    f32x4 val4 = acc[db] * scale;
+    val4[0] += old.x; val4[1] += old.y; val4[2] += old.z; val4[3] += old.w;
+    store4(dst, val4, 1.0f);
+  }
+}
+
 // One workgroup per (b, h, block): wave w takes the block's groups w, w+4, ... (prefetching
 // the next group's rows while computing the current one) and keeps partial dK, dV in
 // registers; the four partials are then summed in wave order through LDS.
@@ -1090,9 +1217,16 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
   BSA_PHASE("bwd.dq_cmp", st,
   (launch_bwd_q<T, HD, 2, false, true>)(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, dout,
                                         A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq));
-  BSA_PHASE("bwd.dq_slc", st,
-  hipLaunchKernelGGL((slc_bwd_q_kernel<T, HD>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, q, k, v, dout, A.valid,
-                     A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq));
+  BSA_PHASE("bwd.dq_slc", st, {
+  if constexpr (sizeof(T) == 2) {
+    constexpr int NW = 2;
+    hipLaunchKernelGGL((slc_bwd_q_dma_kernel<HD, NW>), dim3(D.N / (16 * NW), D.H, D.B), dim3(64 * NW), 0, st, q, k, v,
+                       dout, A.valid, A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq);
+  } else {
+    hipLaunchKernelGGL((slc_bwd_q_kernel<T, HD>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, q, k, v, dout, A.valid,
+                       A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq);
+  }
+  });
   // ---- dK, dV of the ball branch (written) ----
   BSA_PHASE("bwd.kv_ball", st, {
   if (D.m >= 128)

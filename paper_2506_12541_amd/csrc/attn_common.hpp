@@ -236,6 +236,27 @@ __device__ __forceinline__ bf16x8 lds_tr_chunk(const bf16_t* t, int k0, int m0, 
   return __builtin_bit_cast(bf16x8, make_uint4(v0.x, v0.y, v1.x, v1.y));
 }
 
+// lds_tr_chunk issued as inline assembly. The compiler's wait insertion treats the
+// transpose-read builtin as possibly overlapping any direct global->LDS load in flight and
+// waits for all of them before it; kernels that keep loads in flight into other buffers
+// while they read use this form. The two reads are waited for (lgkmcnt(0)) inside the
+// same statement, which also makes every use of the result follow the wait.
+template <int HD>
+__device__ __forceinline__ bf16x8 lds_tr_chunk_nowait(const bf16_t* t, int k0, int m0, int lane) {
+  const int p = lane & 15, j = lane >> 4;
+  const int col = m0 + 4 * (p & 3);
+  const int lc = col >> 3, sub = col & 7;
+  const int x0 = k0 + 4 * j + (p >> 2), x1 = x0 + 16;
+  const bf16_t* a0 = t + x0 * HD + 8 * (lc ^ swz<HD>(x0)) + sub;
+  const bf16_t* a1 = t + x1 * HD + 8 * (lc ^ swz<HD>(x1)) + sub;
+  const uint32_t o0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)a0;
+  const uint32_t o1 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)a1;
+  uint2 v0, v1;
+  asm volatile("ds_read_b64_tr_b16 %0, %2\n\tds_read_b64_tr_b16 %1, %3\n\ts_waitcnt lgkmcnt(0)"
+               : "=&v"(v0), "=&v"(v1) : "v"(o0), "v"(o1) : "memory");
+  return __builtin_bit_cast(bf16x8, make_uint4(v0.x, v0.y, v1.x, v1.y));
+}
+
 // MFMA 16x16x16 A operand of the transposed tile: lane (r = lane % 16, j = lane / 16)
 // receives X[k0 + 4j + i][m0 + r], i = 0..3 (one ds_read_b64_tr_b16; addressing as above).
 template <int HD>

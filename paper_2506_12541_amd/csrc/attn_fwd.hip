@@ -235,6 +235,99 @@ __global__ void __launch_bounds__(256) slc_fwd_kernel(const T* q, const T* k, co
   w.finish(lane, bh * N + wq0, out, lse, val, wq0);
 }
 
+// bf16 variant of the selection kernel. Each wave double-buffers its key tiles (the 32 K
+// rows and 32 V rows of two sub-blocks) in LDS, filled by direct global->LDS loads one tile
+// ahead; the two buffers are distinct LDS objects and the tile loop is unrolled by two with
+// a straight-line body (tiles past the end are loaded from row 0 and masked). Key validity
+// is gathered into 16-bit masks while the sub-block list is built, so no load other than
+// the tile loads runs in the loop.
+template <int HD, int NW>
+__global__ void __launch_bounds__(NW * 64) slc_fwd_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
+                                                              const uint8_t* valid_all, const int* sel, int H, int N,
+                                                              int ls, int kk, int g, float sl2, bf16_t* out,
+                                                              float* lse) {
+  constexpr int TILE = 32 * HD;    // one 32-key tile
+  constexpr int SLOT = 2 * TILE;   // K tile, V tile
+  __shared__ __attribute__((aligned(16))) bf16_t buf0[NW * SLOT], buf1[NW * SLOT];
+  __shared__ int sub_all[NW][kMaxSub];          // first token of each 16-key sub-block (or -1), group in bits 24+
+  __shared__ uint32_t okm_all[NW][kMaxSub];     // bit t: key t of the sub-block is a real token
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r = lane & 15, j = lane >> 4;
+  const int b = blockIdx.z, h = blockIdx.y;
+  const long long bh = (long long)b * H + h;
+  const int wq0 = (blockIdx.x * NW + wid) * 16;
+  const int G = g >= 16 ? 1 : 16 / g;
+  const int p0 = wq0 / g;
+  const int my_gi = g >= 16 ? 0 : r / g;
+  const int ngroups = N / g;
+  const bf16_t* kh = k + bh * N * HD;
+  const bf16_t* vh = v + bh * N * HD;
+  const uint8_t* val = valid_all ? valid_all + (size_t)b * N : nullptr;
+  const int* selp = sel + ((size_t)bh * ngroups + p0) * kk;
+  int* sub = sub_all[wid];
+  uint32_t* okm = okm_all[wid];
+
+  const int nsub = G * kk * (ls / 16);
+  for (int e = lane; e < nsub; e += 64) {
+    const int slot = (e * 16) / ls;
+    const int gi = slot / kk;
+    const int id = selp[gi * kk + slot % kk];
+    const int tok0 = id * ls + (e * 16) % ls;
+    sub[e] = id < 0 ? -1 : ((gi << 24) | tok0);
+    uint32_t m = 0;
+    if (id >= 0) {
+      m = 0xFFFFu;
+      if (val)
+        for (int t = 0; t < 16; ++t)
+          if (!val[tok0 + t]) m &= ~(1u << t);
+    }
+    okm[e] = m;
+  }
+  WaveAttn<bf16_t, HD, 1> w;
+  w.init();
+  load_q(w, q + (bh * N + wq0) * HD, lane);
+  vm_drain();
+  wave_sync();   // LDS regions are per wave
+
+  const int nt = __builtin_amdgcn_readfirstlane((nsub + 1) / 2);   // 32-key tiles
+  auto issue = [&](int t, bf16_t* slot) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const int e = 2 * t + kb < nsub ? sub[2 * t + kb] : -1;
+      const int row = e >= 0 ? (e & 0xFFFFFF) : 0;
+      bf16_t* base = slot + wid * SLOT + kb * 16 * HD;
+      dma_tile<HD, 16, 1>(base, kh, row, N, 0, lane);
+      dma_tile<HD, 16, 1>(base + TILE, vh, row, N, 0, lane);
+    }
+  };
+  auto step = [&](int t, const bf16_t* cur, bf16_t* next) {
+    vm_drain();   // this tile has landed
+    issue(t + 1, next);
+    const bf16_t* kt = cur + wid * SLOT;
+    const bf16_t* vt = kt + TILE;
+    bool ok[2][4];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const int se = 2 * t + kb;
+      const int e = t < nt && se < nsub ? sub[se] : -1;
+      const uint32_t m = e >= 0 && (e >> 24) == my_gi ? okm[se] : 0u;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ok[kb][i] = (m >> (4 * j + i)) & 1u;
+    }
+    auto kfrag = [&](int kb, int c) { return lds_row_chunk<HD>(kt, 16 * kb + r, 4 * c + j); };
+    auto vfrag = [&](int db, int kp) { return lds_tr_chunk_nowait<HD>(vt, 32 * kp, 16 * db, lane); };
+    auto keyok = [&](int kb, int i, int) { return ok[kb][i]; };
+    w.template tile<2>(sl2, kfrag, vfrag, keyok);
+  };
+  issue(0, buf0);
+  for (int t = 0; t < nt; t += 2) {   // straight-line body
+    step(t, buf0, buf1);
+    step(t + 1, buf1, buf0);
+  }
+  vm_drain();   // the loads past the end have landed
+  w.finish(lane, bh * N + wq0, out, lse, val, wq0);
+}
+
 template <typename T>
 __global__ void gate_fwd_kernel(const T* ob, const float* gate, const uint8_t* valid, int H, int N, int hd,
                                 long long per_branch, T* out) {
@@ -294,9 +387,15 @@ template <typename T, int HD>
 hipError_t slc_impl(const Dims& D, const void* q, const void* k, const void* v, const uint8_t* valid, const int* sel,
                     void* o, float* lse, hipStream_t st) {
   const float sl2 = D.scale * kLog2e;
-  dim3 grid(D.N / 64, D.H, D.B);
-  hipLaunchKernelGGL((slc_fwd_kernel<T, HD>), grid, dim3(256), 0, st, (const T*)q, (const T*)k, (const T*)v, valid,
-                     sel, D.H, D.N, D.ls, D.k, D.g, sl2, (T*)o, lse);
+  if constexpr (sizeof(T) == 2) {
+    constexpr int NW = 2;
+    hipLaunchKernelGGL((slc_fwd_dma_kernel<HD, NW>), dim3(D.N / (16 * NW), D.H, D.B), dim3(64 * NW), 0, st,
+                       (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, valid, sel, D.H, D.N, D.ls, D.k, D.g,
+                       sl2, (bf16_t*)o, lse);
+  } else {
+    hipLaunchKernelGGL((slc_fwd_kernel<T, HD>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, (const T*)q,
+                       (const T*)k, (const T*)v, valid, sel, D.H, D.N, D.ls, D.k, D.g, sl2, (T*)o, lse);
+  }
   return hipGetLastError();
 }
 
