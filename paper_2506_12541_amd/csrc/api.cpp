@@ -126,7 +126,7 @@ FwdWs fwd_ws_layout(const bsa::Dims& D) {
 }
 
 struct BwdWs {
-  size_t R, terms, kc_lp, vc_lp, dkc_part, dvc_part, dkc, dvc, pk, pv, pkt, pvt, hist, seg_s, seg_e, dpre, pw1, psm, w1lp,
+  size_t R, terms, dplp, kc_lp, vc_lp, dkc_part, dvc_part, dkc, dvc, pk, pv, pkt, pvt, hist, seg_s, seg_e, dpre, pw1, psm, w1lp,
       total;
   int cmp_chunks, mlp_chunks, mlp_chunks_small;
   long long pairs, nseg;
@@ -162,6 +162,7 @@ BwdWs bwd_ws_layout(const bsa::Dims& D) {
   W.pw1 = put(sizeof(float) * (size_t)W.mlp_chunks * D.l * D.d * D.d);
   W.psm = put(sizeof(float) * (size_t)W.mlp_chunks_small * ((size_t)D.d * D.d + 2 * D.d));
   W.w1lp = put(elem_bytes(D) * (size_t)D.l * D.d * D.d);
+  W.dplp = put(elem_bytes(D) * crows * D.d);
   W.total = off;
   return W;
 }
@@ -385,7 +386,7 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   A.seg_start = (int*)(w + W.seg_s); A.seg_end = (int*)(w + W.seg_e);
   BSA_TRY(bsa::launch_attn_bwd(D, A, st), "attention backward");
   bsa::MlpBwdWs mw{(float*)(w + W.dpre), (float*)(w + W.pw1), (float*)(w + W.psm), (void*)(w + W.w1lp),
-                   W.mlp_chunks, W.mlp_chunks_small};
+                   W.mlp_chunks, W.mlp_chunks_small, (void*)(w + W.dplp)};
   bsa::Mlp mk{}, mv{};
   bsa::MlpGrad gk{}, gv{};
   if (D.pool == 0) {

@@ -402,6 +402,271 @@ __global__ void mean_pool_bwd_kernel(const float* dy, const uint8_t* valid, int 
   dx_accum[i] += dy[row * hd + c] / (float)l;
 }
 
+// ---- bf16 layers: the backward of phi in four passes (both layers' weight gradients as
+// deterministic chunk partials, summed in order) ----
+
+// (1) Per 32-row tile, on the vector ALU in f32: dh = dy W2^T, dpre = dh GELU'(pre) (stored
+// in f32 and bf16), and this workgroup's partials of dW2 = h^T dy, db1 = sum dpre,
+// db2 = sum dy over its rows. Thread t owns row t / 8 and outputs 8 (t % 8) .. + 7.
+template <int HD>
+__global__ void __launch_bounds__(256) mlp_bwd_pre_kernel(const float* dy, const float* pre, const float* w2,
+                                                          long long rows, long long rows_per_wg, float* dpre,
+                                                          bf16_t* dpre_lp, float* part) {
+  constexpr int TR = 32;            // rows per tile
+  constexpr int PER = TR * HD / 256;   // tile entries per thread
+  __shared__ float w2s[HD][HD + 1];
+  __shared__ float hs[TR][HD + 1], ys[TR][HD + 1], ps[TR][HD + 1];
+  for (int i = threadIdx.x; i < HD * HD; i += 256) w2s[i / HD][i % HD] = w2[i];
+  const long long rbeg = blockIdx.x * rows_per_wg;
+  const long long rend = rbeg + rows_per_wg < rows ? rbeg + rows_per_wg : rows;
+  // dW2 / db accumulators: thread owns dW2 entries (o, o2) with o = t / (256 / HD) * ..., see below
+  constexpr int W2PER = HD * HD / 256;
+  float aw2[W2PER];
+#pragma unroll
+  for (int u = 0; u < W2PER; ++u) aw2[u] = 0.f;
+  float ab1 = 0.f, ab2 = 0.f;
+  const int t = threadIdx.x;
+  for (long long r0 = rbeg; r0 < rend; r0 += TR) {
+    __syncthreads();
+    float pv[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = t + 256 * u, rr = e / HD, c = e % HD;
+      const long long row = r0 + rr;
+      const bool ok = row < rend;
+      pv[u] = ok ? pre[row * HD + c] : 0.f;
+      ys[rr][c] = ok ? dy[row * HD + c] : 0.f;
+      hs[rr][c] = ok ? gelu_erf(pv[u]) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = t + 256 * u, rr = e / HD, o = e % HD;
+      float dh = 0.f;
+#pragma unroll 16
+      for (int o2 = 0; o2 < HD; ++o2) dh += ys[rr][o2] * w2s[o][o2];
+      const long long row = r0 + rr;
+      const float d = row < rend ? dh * gelu_erf_grad(pv[u]) : 0.f;
+      ps[rr][o] = d;
+      if (row < rend) {
+        dpre[row * HD + o] = d;
+        dpre_lp[row * HD + o] = f2bf(d);
+      }
+    }
+    __syncthreads();
+    // dW2[o][o2]: thread owns o2 = t % HD and o = W2PER * (t / HD) + u
+#pragma unroll
+    for (int u = 0; u < W2PER; ++u) {
+      const int o = W2PER * (t / HD) + u, o2 = t % HD;
+      float a = aw2[u];
+#pragma unroll 8
+      for (int rr = 0; rr < TR; ++rr) a += hs[rr][o] * ys[rr][o2];
+      aw2[u] = a;
+    }
+    if (t < HD) {
+#pragma unroll 8
+      for (int rr = 0; rr < TR; ++rr) { ab1 += ps[rr][t]; ab2 += ys[rr][t]; }
+    }
+  }
+  float* out = part + (size_t)blockIdx.x * (HD * HD + 2 * HD);
+#pragma unroll
+  for (int u = 0; u < W2PER; ++u) out[(W2PER * (t / HD) + u) * HD + t % HD] = aw2[u];
+  if (t < HD) {
+    out[HD * HD + t] = ab1;
+    out[HD * HD + HD + t] = ab2;
+  }
+}
+
+// (2) dx = dpre W1^T added into the token gradients, as C^T = W1 dpre^T on bf16 matrix
+// cores: a workgroup owns 256 flattened inputs i (their W1 rows staged in LDS by direct
+// loads) and 64 block rows per pass (wave w: rows 16w..16w+15, its dpre fragments from
+// global); a lane ends with 4 consecutive i of one row, added into the gradient as float4.
+template <int HD>
+__global__ void __launch_bounds__(256) mlp_bwd_dx_kernel(const bf16_t* dpre_lp, const bf16_t* w1, const uint8_t* valid,
+                                                         int H, int N, int l, long long rows, int passes,
+                                                         float* dx_accum) {
+  constexpr int NCH = HD / 32;
+  constexpr int IT = 256 / 16;   // i tiles per workgroup
+  __shared__ __attribute__((aligned(16))) bf16_t w1s[256 * HD];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r = lane & 15, j = lane >> 4;
+  const int ld = l * HD;
+  const int i0 = blockIdx.x * 256;
+  dma_tile<HD, 256, 4>(w1s, w1, i0, ld, wid, lane);
+  vm_drain();
+  __syncthreads();
+  const int nblk = N / l;
+  for (int pz = 0; pz < passes; ++pz) {
+    const long long row0 = ((long long)blockIdx.y * passes + pz) * 64 + 16 * wid;
+    if (row0 >= rows) break;
+    const long long row = row0 + r;
+    const bool rok = row < rows;
+    bf16x8 bd[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+      bd[c] = rok ? load_chunk(dpre_lp + row * HD + 32 * c + 8 * j) : zero_chunk(bd[c]);
+    const long long bhh = rok ? row / nblk : 0;
+    const int blk = rok ? (int)(row % nblk) : 0;
+    const int b = (int)(bhh / H);
+#pragma unroll 4
+    for (int it = 0; it < IT; ++it) {
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) acc = mma(lds_row_chunk<HD>(w1s, 16 * it + r, 4 * c + j), bd[c], acc);
+      // lane: row r, flat inputs i = i0 + 16 it + 4 j + t (one token, 4 consecutive channels)
+      const int i = i0 + 16 * it + 4 * j;
+      const int tok = i / HD, ch = i % HD;
+      if (rok && (valid == nullptr || valid[(size_t)b * N + (size_t)blk * l + tok])) {
+        float* dst = dx_accum + (row * l + tok) * HD + ch;
+        float4 o = *reinterpret_cast<float4*>(dst);
+        o.x += acc[0]; o.y += acc[1]; o.z += acc[2]; o.w += acc[3];
+        *reinterpret_cast<float4*>(dst) = o;
+      }
+    }
+  }
+}
+
+// (3) dW1 partials over a chunk of block rows, D[i][o] = sum_rows x[row][i] dpre[row][o],
+// on bf16 matrix cores: a workgroup owns 256 flattened inputs i (wave w: 64 of them) and
+// walks its rows 32 at a time; the x and dpre tiles are double-buffered in LDS (two
+// distinct objects, loop unrolled by two) by direct loads, and both operands, which run
+// along the rows, come from transpose reads. Inputs of padding tokens are zeroed in LDS.
+template <int HD>
+__global__ void __launch_bounds__(256) mlp_bwd_w1_dma_kernel(const bf16_t* x, const uint8_t* valid,
+                                                             const bf16_t* dpre_lp, int H, int N, int l,
+                                                             long long rows, long long rows_per_chunk, float* part) {
+  constexpr int XW = 256;          // inputs per workgroup (tile width)
+  constexpr int OB = HD / 16;
+  constexpr int TR = 32;           // rows per step
+  __shared__ __attribute__((aligned(16))) bf16_t xs0[TR * XW], xs1[TR * XW];
+  __shared__ __attribute__((aligned(16))) bf16_t ds0[TR * HD], ds1[TR * HD];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int r = lane & 15;
+  const int ld = l * HD;
+  const int i0 = blockIdx.x * XW;
+  const long long rbeg = (long long)blockIdx.y * rows_per_chunk;
+  const long long rend = rbeg + rows_per_chunk < rows ? rbeg + rows_per_chunk : rows;
+  const int nblk = N / l;
+  const bf16_t* xb = x + i0;   // column offset of this workgroup's inputs
+  auto issue = [&](long long r0, bf16_t* xd, bf16_t* dd) {
+    // x rows are ld elements apart: load each row's 256-input slice as its own 512-byte run
+#pragma unroll
+    for (int u = 0; u < TR * XW / 8 / 64 / 4; ++u) {
+      const int blkk = wid * (TR * XW / 8 / 64 / 4) + u;     // 1 KB LDS block
+      const int idx = blkk * 64 + lane;                      // 16-byte chunk of the tile
+      const int row = idx / (XW / 8);
+      const int lc = (idx % (XW / 8)) ^ swz<XW>(row);
+      const long long gr = r0 + row < rend ? r0 + row : rend - 1;
+      __builtin_amdgcn_global_load_lds(xb + gr * ld + 8 * lc, xd + blkk * 512, 16, 0, 0);
+    }
+    constexpr int NID = TR * HD * 2 / 1024;   // 1 KB blocks of the dpre tile
+    if constexpr (NID >= 4) {
+      dma_tile<HD, TR, 4>(dd, dpre_lp, (int)r0, (int)rend, wid, lane);
+    } else {
+      if (wid < NID) dma_tile<HD, TR, NID>(dd, dpre_lp, (int)r0, (int)rend, wid, lane);
+    }
+  };
+  f32x4 acc[4][OB];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int ob = 0; ob < OB; ++ob) acc[a][ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto step = [&](long long r0, bf16_t* xc, bf16_t* dc, bf16_t* xn, bf16_t* dn) {
+    vm_drain();
+    __syncthreads();
+    const bool tail = r0 + TR > rend;
+    if (valid != nullptr || tail) {   // zero inputs of padding tokens and rows past the chunk
+      for (int e = threadIdx.x; e < TR * (XW / HD); e += 256) {
+        const int rr = e / (XW / HD), tk = e % (XW / HD);
+        const long long row = r0 + rr;
+        bool ok = row < rend;
+        if (ok && valid) {
+          const long long bhh = row / nblk;
+          const int blk = (int)(row % nblk);
+          ok = valid[(size_t)(bhh / H) * N + (size_t)blk * l + (i0 + tk * HD) / HD] != 0;
+        }
+        if (!ok)
+          for (int c = 0; c < HD / 8; ++c)
+            *reinterpret_cast<uint4*>(&xc[rr * XW + 8 * (((tk * HD) / 8 + c) ^ swz<XW>(rr))]) = make_uint4(0, 0, 0, 0);
+      }
+      __syncthreads();
+    }
+    if (r0 + TR < rend) issue(r0 + TR, xn, dn);
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      const bf16x8 ax = lds_tr_chunk<XW>(xc, 0, 64 * wid + 16 * a, lane);
+#pragma unroll
+      for (int ob = 0; ob < OB; ++ob) acc[a][ob] = mma(ax, lds_tr_chunk<HD>(dc, 0, 16 * ob, lane), acc[a][ob]);
+    }
+  };
+  issue(rbeg, xs0, ds0);
+  for (long long r0 = rbeg; r0 < rend; r0 += 2 * TR) {
+    step(r0, xs0, ds0, xs1, ds1);
+    if (r0 + TR < rend) step(r0 + TR, xs1, ds1, xs0, ds0);
+  }
+  // lane: o = 16 ob + r (column), i = i0 + 64 wid + 16 a + 4 j + t (rows)
+  const int j = lane >> 4;
+  float* out = part + (size_t)blockIdx.y * ld * HD;
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int ob = 0; ob < OB; ++ob)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) out[(size_t)(i0 + 64 * wid + 16 * a + 4 * j + t) * HD + 16 * ob + r] = acc[a][ob][t];
+}
+
+// (4) out[i] = sum over chunks of part[c * stride + i], chunks in order; a workgroup owns
+// 64 outputs and its 4 waves take every 4th chunk, then add their sums in wave order.
+__global__ void __launch_bounds__(256) sum_parts_wide_kernel(const float* part, int chunks, long long n,
+                                                             long long stride, float* out) {
+  __shared__ float red[4][64];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const long long i = (long long)blockIdx.x * 64 + lane;
+  float s = 0.f;
+  if (i < n) {
+#pragma unroll 8
+    for (int c = wid; c < chunks; c += 4) s += part[(long long)c * stride + i];
+  }
+  red[wid][lane] = s;
+  __syncthreads();
+  if (wid == 0 && i < n) out[i] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+}
+
+template <int HD>
+hipError_t compress_bwd_bf16(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi, const float* pre,
+                             const float* dy, float* dx_accum, const MlpGrad& grad, const MlpBwdWs& ws,
+                             hipStream_t st) {
+  const long long rows = D.cmp_rows();
+  const int ld = D.l * HD;
+  bf16_t* w1 = (bf16_t*)ws.w1_lp;
+  bf16_t* dpl = (bf16_t*)ws.dpre_lp;
+  hipLaunchKernelGGL(cast_w_kernel<bf16_t>, dim3((ld * HD + 255) / 256), dim3(256), 0, st, phi.w1, ld * HD, w1);
+  const long long rps = ((rows + ws.chunks_small - 1) / ws.chunks_small + 31) / 32 * 32;
+  hipLaunchKernelGGL((mlp_bwd_pre_kernel<HD>), dim3(ws.chunks_small), dim3(256), 0, st, dy, pre, phi.w2, rows, rps,
+                     ws.dpre, dpl, ws.part_small);
+  constexpr int kPasses = 4;   // 64-row passes per workgroup of the dx product
+  const long long ry = (rows + 64 * kPasses - 1) / (64 * kPasses);
+  hipLaunchKernelGGL((mlp_bwd_dx_kernel<HD>), dim3(ld / 256, (unsigned)ry), dim3(256), 0, st, (const bf16_t*)dpl,
+                     (const bf16_t*)w1, valid, D.H, D.N, D.l, rows, kPasses, dx_accum);
+  const long long rpc = ((rows + ws.chunks - 1) / ws.chunks + 31) / 32 * 32;
+  const int nch = (int)((rows + rpc - 1) / rpc);
+  hipLaunchKernelGGL((mlp_bwd_w1_dma_kernel<HD>), dim3(ld / 256, nch), dim3(256), 0, st, (const bf16_t*)x, valid,
+                     (const bf16_t*)dpl, D.H, D.N, D.l, rows, rpc, ws.part_w1);
+  const long long n1 = (long long)ld * HD;
+  hipLaunchKernelGGL(sum_parts_wide_kernel, dim3((unsigned)((n1 + 63) / 64)), dim3(256), 0, st, ws.part_w1, nch, n1,
+                     n1, grad.w1);
+  const long long ss = (long long)HD * HD + 2 * HD;
+  const int nsm = (int)((rows + rps - 1) / rps);
+  float* tmp = grad.w2;   // W2, b1, b2 partials are summed into their three outputs
+  hipLaunchKernelGGL(sum_parts_wide_kernel, dim3((HD * HD + 63) / 64), dim3(256), 0, st, ws.part_small, nsm,
+                     (long long)HD * HD, ss, tmp);
+  hipLaunchKernelGGL(sum_parts_wide_kernel, dim3(1), dim3(256), 0, st, ws.part_small + HD * HD, nsm, (long long)HD,
+                     ss, grad.b1);
+  hipLaunchKernelGGL(sum_parts_wide_kernel, dim3(1), dim3(256), 0, st, ws.part_small + HD * HD + HD, nsm,
+                     (long long)HD, ss, grad.b2);
+  return hipGetLastError();
+}
+
 template <typename T, int HD>
 hipError_t compress_bwd_impl(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi, const float* pre,
                              const float* dy, float* dx_accum, const MlpGrad& grad, const MlpBwdWs& ws,
@@ -412,6 +677,9 @@ hipError_t compress_bwd_impl(const Dims& D, const void* x, const uint8_t* valid,
     hipLaunchKernelGGL(mean_pool_bwd_kernel, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, st, dy, valid, D.H, D.N,
                        D.l, HD, rows, dx_accum);
     return hipGetLastError();
+  }
+  if constexpr (sizeof(T) == 2) {
+    if (D.l * HD % 256 == 0) return compress_bwd_bf16<HD>(D, x, valid, phi, pre, dy, dx_accum, grad, ws, st);
   }
   const int ld = D.l * HD;
   const T* w1 = (const T*)phi.w1;

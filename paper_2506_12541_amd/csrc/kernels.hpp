@@ -84,6 +84,7 @@ struct MlpBwdWs {
   float* part_small;  // [chunks_small, d*d + 2d]
   void* w1_lp;        // [l*d, d] W1 in the storage type
   int chunks, chunks_small;
+  void* dpre_lp;      // [rows, d] dpre in the storage type
 };
 int mlp_bwd_chunks(const Dims& D);
 int mlp_bwd_chunks_small(const Dims& D);
