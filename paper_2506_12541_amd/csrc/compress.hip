@@ -407,61 +407,99 @@ __global__ void mean_pool_bwd_kernel(const float* dy, const uint8_t* valid, int 
 
 // (1) Per 32-row tile, on the vector ALU in f32: dh = dy W2^T, dpre = dh GELU'(pre) (stored
 // in f32 and bf16), and this workgroup's partials of dW2 = h^T dy, db1 = sum dpre,
-// db2 = sum dy over its rows. Thread t owns row t / 8 and outputs 8 (t % 8) .. + 7.
+// db2 = sum dy over its rows. Register blocking keeps LDS traffic low: for dh a thread
+// owns 2 rows x 4 outputs (W2 staged transposed so its 4 outputs are one float4 read), for
+// dW2 a 4 x 4 block.
 template <int HD>
 __global__ void __launch_bounds__(256) mlp_bwd_pre_kernel(const float* dy, const float* pre, const float* w2,
                                                           long long rows, long long rows_per_wg, float* dpre,
                                                           bf16_t* dpre_lp, float* part) {
-  constexpr int TR = 32;            // rows per tile
-  constexpr int PER = TR * HD / 256;   // tile entries per thread
-  __shared__ float w2s[HD][HD + 1];
-  __shared__ float hs[TR][HD + 1], ys[TR][HD + 1], ps[TR][HD + 1];
-  for (int i = threadIdx.x; i < HD * HD; i += 256) w2s[i / HD][i % HD] = w2[i];
+  constexpr int TR = 32;                       // rows per tile
+  constexpr int OQ = HD / 4;                   // 4-wide output groups per row
+  constexpr int RB = TR * OQ / 256;            // rows per thread in the dh pass (2 for HD=64, 1 for 32)
+  constexpr int NB4 = (HD / 4) * (HD / 4);      // 4x4 dW2 blocks (at most one per thread)
+  constexpr int W2B = 1;
+  static_assert(NB4 <= 256, "dW2 blocks");
+  static_assert(RB >= 1 && TR * OQ % 256 == 0, "tile split");
+  __shared__ __attribute__((aligned(16))) float w2t[HD][HD + 4];   // W2^T: w2t[o2][o] = W2[o][o2]
+  __shared__ __attribute__((aligned(16))) float hs[TR][HD + 4], ys[TR][HD + 4], ps[TR][HD + 4];
+  for (int i = threadIdx.x; i < HD * HD; i += 256) w2t[i % HD][i / HD] = w2[i];
   const long long rbeg = blockIdx.x * rows_per_wg;
   const long long rend = rbeg + rows_per_wg < rows ? rbeg + rows_per_wg : rows;
-  // dW2 / db accumulators: thread owns dW2 entries (o, o2) with o = t / (256 / HD) * ..., see below
-  constexpr int W2PER = HD * HD / 256;
-  float aw2[W2PER];
-#pragma unroll
-  for (int u = 0; u < W2PER; ++u) aw2[u] = 0.f;
-  float ab1 = 0.f, ab2 = 0.f;
   const int t = threadIdx.x;
+  const int oq = t % OQ;             // dh pass: outputs 4 oq .. 4 oq + 3
+  const int rr0 = (t / OQ) * RB;     // dh pass: rows rr0 .. rr0 + RB - 1
+  f32x4 aw2[W2B][4];                 // dW2 pass: block (o rows 4 bo + u, o2 4 bq .. + 3)
+#pragma unroll
+  for (int w = 0; w < W2B; ++w)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) aw2[w][u] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float ab1 = 0.f, ab2 = 0.f;
   for (long long r0 = rbeg; r0 < rend; r0 += TR) {
     __syncthreads();
-    float pv[PER];
-#pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int e = t + 256 * u, rr = e / HD, c = e % HD;
+    for (int e = t; e < TR * OQ; e += 256) {
+      const int rr = e / OQ, c = 4 * (e % OQ);
       const long long row = r0 + rr;
-      const bool ok = row < rend;
-      pv[u] = ok ? pre[row * HD + c] : 0.f;
-      ys[rr][c] = ok ? dy[row * HD + c] : 0.f;
-      hs[rr][c] = ok ? gelu_erf(pv[u]) : 0.f;
+      float4 pv = make_float4(0.f, 0.f, 0.f, 0.f), yv = pv;
+      if (row < rend) {
+        pv = *reinterpret_cast<const float4*>(pre + row * HD + c);
+        yv = *reinterpret_cast<const float4*>(dy + row * HD + c);
+      }
+      *reinterpret_cast<float4*>(&ys[rr][c]) = yv;
+      *reinterpret_cast<float4*>(&hs[rr][c]) = make_float4(gelu_erf(pv.x), gelu_erf(pv.y), gelu_erf(pv.z), gelu_erf(pv.w));
+      *reinterpret_cast<float4*>(&ps[rr][c]) = pv;   // pre, replaced by dpre below
     }
     __syncthreads();
+    f32x4 dh[RB];
 #pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int e = t + 256 * u, rr = e / HD, o = e % HD;
-      float dh = 0.f;
-#pragma unroll 16
-      for (int o2 = 0; o2 < HD; ++o2) dh += ys[rr][o2] * w2s[o][o2];
-      const long long row = r0 + rr;
-      const float d = row < rend ? dh * gelu_erf_grad(pv[u]) : 0.f;
-      ps[rr][o] = d;
-      if (row < rend) {
-        dpre[row * HD + o] = d;
-        dpre_lp[row * HD + o] = f2bf(d);
+    for (int u = 0; u < RB; ++u) dh[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+    for (int o2 = 0; o2 < HD; ++o2) {
+      const float4 wv = *reinterpret_cast<const float4*>(&w2t[o2][4 * oq]);
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+        const float yv = ys[rr0 + u][o2];
+        dh[u][0] += yv * wv.x; dh[u][1] += yv * wv.y; dh[u][2] += yv * wv.z; dh[u][3] += yv * wv.w;
       }
     }
-    __syncthreads();
-    // dW2[o][o2]: thread owns o2 = t % HD and o = W2PER * (t / HD) + u
+    float4 dv[RB];
 #pragma unroll
-    for (int u = 0; u < W2PER; ++u) {
-      const int o = W2PER * (t / HD) + u, o2 = t % HD;
-      float a = aw2[u];
-#pragma unroll 8
-      for (int rr = 0; rr < TR; ++rr) a += hs[rr][o] * ys[rr][o2];
-      aw2[u] = a;
+    for (int u = 0; u < RB; ++u) {
+      const int rr = rr0 + u;
+      const long long row = r0 + rr;
+      const float4 pv = *reinterpret_cast<const float4*>(&ps[rr][4 * oq]);
+      const bool ok = row < rend;
+      dv[u] = ok ? make_float4(dh[u][0] * gelu_erf_grad(pv.x), dh[u][1] * gelu_erf_grad(pv.y),
+                               dh[u][2] * gelu_erf_grad(pv.z), dh[u][3] * gelu_erf_grad(pv.w))
+                 : make_float4(0.f, 0.f, 0.f, 0.f);
+      if (ok) {
+        *reinterpret_cast<float4*>(dpre + row * HD + 4 * oq) = dv[u];
+        const uint32_t lo = (uint32_t)f2bf(dv[u].x) | ((uint32_t)f2bf(dv[u].y) << 16);
+        const uint32_t hi = (uint32_t)f2bf(dv[u].z) | ((uint32_t)f2bf(dv[u].w) << 16);
+        *reinterpret_cast<uint2*>(dpre_lp + row * HD + 4 * oq) = make_uint2(lo, hi);
+      }
+    }
+    __syncthreads();   // every thread has read its pre values
+#pragma unroll
+    for (int u = 0; u < RB; ++u) *reinterpret_cast<float4*>(&ps[rr0 + u][4 * oq]) = dv[u];
+    __syncthreads();
+    // dW2 blocks: thread owns o = 4 bo + u, o2 = 4 bq .. + 3
+#pragma unroll
+    for (int w = 0; w < W2B; ++w) {
+      const int blk = t * W2B + w;
+      const int bo = blk / OQ, bq = blk % OQ;
+      if (blk >= NB4) continue;
+#pragma unroll 4
+      for (int rr = 0; rr < TR; ++rr) {
+        const float4 hv = *reinterpret_cast<const float4*>(&hs[rr][4 * bo]);
+        const float4 yv = *reinterpret_cast<const float4*>(&ys[rr][4 * bq]);
+        const float h4[4] = {hv.x, hv.y, hv.z, hv.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          aw2[w][u][0] += h4[u] * yv.x; aw2[w][u][1] += h4[u] * yv.y;
+          aw2[w][u][2] += h4[u] * yv.z; aw2[w][u][3] += h4[u] * yv.w;
+        }
+      }
     }
     if (t < HD) {
 #pragma unroll 8
@@ -469,8 +507,18 @@ __global__ void __launch_bounds__(256) mlp_bwd_pre_kernel(const float* dy, const
     }
   }
   float* out = part + (size_t)blockIdx.x * (HD * HD + 2 * HD);
+  {
 #pragma unroll
-  for (int u = 0; u < W2PER; ++u) out[(W2PER * (t / HD) + u) * HD + t % HD] = aw2[u];
+    for (int w = 0; w < W2B; ++w) {
+      const int blk = t * W2B + w;
+      const int bo = blk / OQ, bq = blk % OQ;
+      if (blk >= NB4) continue;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        *reinterpret_cast<float4*>(out + (4 * bo + u) * HD + 4 * bq) =
+            make_float4(aw2[w][u][0], aw2[w][u][1], aw2[w][u][2], aw2[w][u][3]);
+    }
+  }
   if (t < HD) {
     out[HD * HD + t] = ab1;
     out[HD * HD + HD + t] = ab2;
@@ -480,7 +528,8 @@ __global__ void __launch_bounds__(256) mlp_bwd_pre_kernel(const float* dy, const
 // (2) dx = dpre W1^T added into the token gradients, as C^T = W1 dpre^T on bf16 matrix
 // cores: a workgroup owns 256 flattened inputs i (their W1 rows staged in LDS by direct
 // loads) and 64 block rows per pass (wave w: rows 16w..16w+15, its dpre fragments from
-// global); a lane ends with 4 consecutive i of one row, added into the gradient as float4.
+// global); a lane ends with 4 consecutive i of one row per 16-input tile. All tiles of a
+// pass are computed first, then the gradient rows are read together and written back.
 template <int HD>
 __global__ void __launch_bounds__(256) mlp_bwd_dx_kernel(const bf16_t* dpre_lp, const bf16_t* w1, const uint8_t* valid,
                                                          int H, int N, int l, long long rows, int passes,
@@ -508,20 +557,31 @@ __global__ void __launch_bounds__(256) mlp_bwd_dx_kernel(const bf16_t* dpre_lp, 
     const long long bhh = rok ? row / nblk : 0;
     const int blk = rok ? (int)(row % nblk) : 0;
     const int b = (int)(bhh / H);
-#pragma unroll 4
-    for (int it = 0; it < IT; ++it) {
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 acc[IT];
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) acc = mma(lds_row_chunk<HD>(w1s, 16 * it + r, 4 * c + j), bd[c], acc);
-      // lane: row r, flat inputs i = i0 + 16 it + 4 j + t (one token, 4 consecutive channels)
+    for (int it = 0; it < IT; ++it) {
+      acc[it] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) acc[it] = mma(lds_row_chunk<HD>(w1s, 16 * it + r, 4 * c + j), bd[c], acc[it]);
+    }
+    // lane: row r, flat inputs i = i0 + 16 it + 4 j + t (one token, 4 consecutive channels)
+    float4 old[IT];
+    bool ok[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
       const int i = i0 + 16 * it + 4 * j;
       const int tok = i / HD, ch = i % HD;
-      if (rok && (valid == nullptr || valid[(size_t)b * N + (size_t)blk * l + tok])) {
-        float* dst = dx_accum + (row * l + tok) * HD + ch;
-        float4 o = *reinterpret_cast<float4*>(dst);
-        o.x += acc[0]; o.y += acc[1]; o.z += acc[2]; o.w += acc[3];
-        *reinterpret_cast<float4*>(dst) = o;
-      }
+      ok[it] = rok && (valid == nullptr || valid[(size_t)b * N + (size_t)blk * l + tok]);
+      old[it] = ok[it] ? *reinterpret_cast<const float4*>(dx_accum + (row * l + tok) * HD + ch)
+                       : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int i = i0 + 16 * it + 4 * j;
+      const int tok = i / HD, ch = i % HD;
+      if (ok[it])
+        *reinterpret_cast<float4*>(dx_accum + (row * l + tok) * HD + ch) =
+            make_float4(old[it].x + acc[it][0], old[it].y + acc[it][1], old[it].z + acc[it][2], old[it].w + acc[it][3]);
     }
   }
 }
