@@ -109,7 +109,7 @@ SavedLayout saved_layout(const bsa::Dims& D) {
 }
 
 struct FwdWs {
-  size_t w1t_k, w1t_v, kc_lp, vc_lp, total;
+  size_t w1t_k, w1t_v, kc_lp, vc_lp, qpool, total;
 };
 
 FwdWs fwd_ws_layout(const bsa::Dims& D) {
@@ -121,6 +121,7 @@ FwdWs fwd_ws_layout(const bsa::Dims& D) {
   W.w1t_v = put(w1);
   W.kc_lp = put(elem_bytes(D) * (size_t)D.cmp_rows() * D.d);
   W.vc_lp = put(elem_bytes(D) * (size_t)D.cmp_rows() * D.d);
+  W.qpool = put(sizeof(float) * (size_t)D.B * D.H * (D.N / D.g) * D.d);
   W.total = off;
   return W;
 }
@@ -332,7 +333,8 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
                                       : bsa::launch_compress_fwd(D, v, valid, mv, saved->vcmp, saved->hid_v, vc_lp,
                                                                  w + W.w1t_v, st)),
            "compression");
-  BSA_STEP("fwd.select", bsa::launch_select_topk(D, q, valid, saved->kcmp, saved->cvalid, saved->sel_idx, st),
+  BSA_STEP("fwd.select", bsa::launch_select_topk(D, q, valid, saved->kcmp, saved->cvalid, saved->sel_idx,
+                                                  (float*)(w + W.qpool), st),
            "select");
   BSA_STEP("fwd.ball", bsa::launch_ball_fwd(D, q, k, v, valid, ob, saved->lse, st), "ball attention");
   BSA_STEP("fwd.cmp",

@@ -180,12 +180,13 @@ struct TileIO {
 // fragments (ds_read_b128, 16 lanes = 16 consecutive rows) and transpose reads
 // (ds_read_b64_tr_b16, 16 lanes = 4 consecutive rows x two chunks), run conflict-free, at
 // 4 and 2 cycles per instruction.
-// Rows wider than 64 elements are only read by transpose reads here; for them chunk pairs
-// of 8 consecutive rows land on distinct banks with c ^ 2 (x mod 8).
+// 128-wide rows (f32 rows of 64) are read as row fragments: 16 consecutive rows on
+// distinct banks with c ^ (x mod 16). Wider rows are only read by transpose reads; for
+// them chunk pairs of 8 consecutive rows land on distinct banks with c ^ 2 (x mod 8).
 template <int HD>
 __device__ __forceinline__ int swz(int x) {
-  static_assert(HD == 32 || HD == 64 || HD >= 256, "tile width");
-  return HD == 64 ? (x & 7) : HD == 32 ? ((x >> 1) & 3) : 2 * (x & 7);
+  static_assert(HD == 32 || HD == 64 || HD == 128 || HD >= 256, "tile width");
+  return HD == 64 ? (x & 7) : HD == 32 ? ((x >> 1) & 3) : HD == 128 ? (x & 15) : 2 * (x & 7);
 }
 
 // Rows [r0, r0 + ROWS) of a row-major [nrows, HD] matrix into an LDS tile, by NW waves.

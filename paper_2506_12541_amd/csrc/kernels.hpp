@@ -39,8 +39,9 @@ hipError_t launch_compress_fwd(const Dims& D, const void* x, const uint8_t* vali
                                float* out, float* pre, void* out_lp, void* w1t_ws, hipStream_t st);
 
 // select.hip: pooled-query block scores and group top-k (Eq. 6, 7, 10-12)
+// qpool: workspace of B*H*(N/g)*d floats for the pooled queries
 hipError_t launch_select_topk(const Dims& D, const void* q, const uint8_t* valid, const float* kcmp,
-                              const uint8_t* cvalid, int* sel, hipStream_t st);
+                              const uint8_t* cvalid, int* sel, float* qpool, hipStream_t st);
 
 // attn_fwd.hip: the three attention branches (Eq. 3, 5, 8) and the gate (Eq. 9)
 hipError_t launch_ball_fwd(const Dims& D, const void* q, const void* k, const void* v, const uint8_t* valid,

@@ -15,6 +15,7 @@
 // where two scores are closer than f32 rounding.
 #include "common.hpp"
 #include "kernels.hpp"
+#include "attn_common.hpp"
 
 namespace bsa {
 namespace {
@@ -49,85 +50,160 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int o) {
   return ((uint64_t)hi << 32) | lo;
 }
 
+// Pooled queries (Eq. 11): q_p = (1/g) * sum of the group's real queries, one thread per
+// (group, channel); consecutive threads read consecutive channels of each query row.
+template <typename T, int HD>
+__global__ void pool_q_kernel(const T* q, const uint8_t* valid, int H, int N, int g, long long total, float* qpool) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  const int c = (int)(i % HD);
+  const long long gp = i / HD;             // (b*H + h) * (N/g) + p
+  const int ngroups = N / g;
+  const long long bh = gp / ngroups;
+  const int p = (int)(gp % ngroups);
+  const int b = (int)(bh / H);
+  const T* qr = q + ((size_t)bh * N + (size_t)p * g) * HD + c;
+  const uint8_t* vb = valid ? valid + (size_t)b * N + (size_t)p * g : nullptr;
+  float s = 0.f;
+#pragma unroll 8
+  for (int t = 0; t < g; ++t)
+    if (vb == nullptr || vb[t]) s += to_f32<T>(qr[(size_t)t * HD]);
+  qpool[i] = s / (float)g;
+}
+
 template <typename T, int HD, int K, int R>
-__global__ void __launch_bounds__(kWaves * 64) select_kernel(const T* q, const uint8_t* valid, const float* kcmp,
+__global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool, const float* kcmp,
                                                              const uint8_t* cvalid, int H, int N, int l, int ls,
                                                              int m, int g, int mask_own, int kk, int* sel) {
   constexpr int NCH = HD / 32;
-  __shared__ float qp[16][HD + 4];
-  __shared__ uint64_t part[16][kWaves * 4 * K];
+  constexpr int KT = 64;        // compressed tokens per staged tile
+  constexpr int TW = 2 * HD;    // tile row width in 16-bit units (f32 rows)
+  constexpr int GW = 16 * kWaves;   // groups per workgroup
+  __shared__ __attribute__((aligned(16))) bf16_t ks0[KT * TW], ks1[KT * TW];
+  __shared__ uint8_t cv0[KT], cv1[KT];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r = lane & 15, j = lane >> 4;
   const int ngroups = N / g;
   const int bh = blockIdx.y;
   const int b = bh / H;
-  const int p0 = blockIdx.x * 16;
-  const T* qh = q + (size_t)bh * N * HD;
+  const int p0 = blockIdx.x * GW;
   const float* kh = kcmp + (size_t)bh * (N / l) * HD;
-  const uint8_t* vb = valid ? valid + (size_t)b * N : nullptr;
   const uint8_t* cv = cvalid + (size_t)b * (N / l);
+  const int ntok = N / l;
 
-  // pooled queries (Eq. 11) over the group's real queries
-  for (int e = threadIdx.x; e < 16 * HD; e += blockDim.x) {
-    int gi = e / HD, c = e % HD;
-    int p = p0 + gi;
-    float s = 0.f;
-    if (p < ngroups) {
-      for (int t = 0; t < g; ++t) {
-        int tok = p * g + t;
-        if (vb == nullptr || vb[tok]) s += to_f32<T>(qh[(size_t)tok * HD + c]);
-      }
-    }
-    qp[gi][c] = s / (float)g;
-  }
-  __syncthreads();
+  // compressed-token tiles: f32 rows moved as 2*HD 16-bit units by direct global->LDS
+  // loads; token validity bytes are read before the tile loads
+  auto issue = [&](int t0, bf16_t* kd, uint8_t* cd) {
+    uint8_t c = 0;
+    if (threadIdx.x < KT) c = t0 + (int)threadIdx.x < ntok ? cv[t0 + threadIdx.x] : 0;
+    dma_tile<TW, KT, kWaves>(kd, reinterpret_cast<const bf16_t*>(kh), t0, ntok, wid, lane);
+    if (threadIdx.x < KT) cd[threadIdx.x] = c;
+  };
+  issue(0, ks0, cv0);
+
+  // pooled queries of this lane's group (B operand)
+  const int pg = p0 + 16 * wid + r;
+  const float* qpr = qpool + ((size_t)bh * ngroups + (pg < ngroups ? pg : 0)) * HD;
   f32x8 bq[NCH];
 #pragma unroll
-  for (int c = 0; c < NCH; ++c)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) bq[c][e] = qp[r][32 * c + 8 * j + e];
+  for (int c = 0; c < NCH; ++c) bq[c] = load_chunk(qpr + 32 * c + 8 * j);
 
-  const int my_group = p0 + r;
+  const int my_group = p0 + 16 * wid + r;
   const int my_ball = (my_group * g) / m;
   uint64_t lst[K];
 #pragma unroll
   for (int t = 0; t < K; ++t) lst[t] = 0;
 
-  const int ntok = N / l;
-  for (int tb = wid; tb < ntok / 16; tb += kWaves) {
-    const float* kr = kh + (size_t)(tb * 16 + r) * HD;
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto step = [&](int t0, const bf16_t* kt, const uint8_t* ct, bf16_t* kn, uint8_t* cn) {
+    vm_drain();
+    __syncthreads();
+    if (t0 + KT < ntok) issue(t0 + KT, kn, cn);
+    // the tile's candidates of this lane (4 / R per 16-token sub-tile), 0 = none
+    constexpr int NCAND = (KT / 16) * (4 / R);
+    uint64_t cand[NCAND];
+    // scores of the tile's 4 sub-tiles: independent MFMA chains, interleaved
+    f32x4 accs[KT / 16];
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) acc = mma(load_chunk(kr + 32 * c + 8 * j), bq[c], acc);
-    // lane holds scores of compressed tokens tb*16 + 4j + i for group my_group
-    const int t0 = tb * 16 + 4 * j;
+    for (int st = 0; st < KT / 16; ++st) accs[st] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int u = 0; u < 4 / R; ++u) {
-      float s = 0.f;
-      bool ok = false;
+    for (int c = 0; c < NCH; ++c) {
+      f32x8 a[KT / 16];
 #pragma unroll
-      for (int i = 0; i < R; ++i) {
-        s += acc[u * R + i];
-        ok |= cv[t0 + u * R + i] != 0;
+      for (int st = 0; st < KT / 16; ++st) {
+        // 8 floats of row 16 st + r: 16-bit chunks 8c + 2j and 8c + 2j + 1
+        const uint4 lo = __builtin_bit_cast(uint4, lds_row_chunk<TW>(kt, 16 * st + r, 8 * c + 2 * j));
+        const uint4 hi = __builtin_bit_cast(uint4, lds_row_chunk<TW>(kt, 16 * st + r, 8 * c + 2 * j + 1));
+        a[st] = f32x8{__uint_as_float(lo.x), __uint_as_float(lo.y), __uint_as_float(lo.z), __uint_as_float(lo.w),
+                      __uint_as_float(hi.x), __uint_as_float(hi.y), __uint_as_float(hi.z), __uint_as_float(hi.w)};
       }
-      s *= 1.0f / (float)R;
-      const int blk = (t0 + u * R) / R;
-      if (mask_own && (blk * ls) / m == my_ball) ok = false;
-      if (ok) topk_insert<K>(lst, make_key(s, blk));
-    }
-  }
-  // partial lists -> LDS
 #pragma unroll
-  for (int t = 0; t < K; ++t) part[r][(wid * 4 + j) * K + t] = lst[t];
+      for (int e = 0; e < 8; ++e)
+#pragma unroll
+        for (int st = 0; st < KT / 16; ++st)
+          accs[st] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[st][e], bq[c][e], accs[st], 0, 0, 0);
+    }
+#pragma unroll
+    for (int st = 0; st < KT / 16; ++st) {
+      const f32x4 acc = accs[st];
+      // lane holds scores of compressed tokens t0 + 16 st + 4j + i for group my_group
+      const int tl = 16 * st + 4 * j;
+#pragma unroll
+      for (int u = 0; u < 4 / R; ++u) {
+        float sc = 0.f;
+        bool ok = t0 + 16 * st < ntok;
+        bool any = false;
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+          sc += acc[u * R + i];
+          any |= ct[tl + u * R + i] != 0;
+        }
+        sc *= 1.0f / (float)R;
+        const int blk = (t0 + tl + u * R) / R;
+        ok = ok && any && !(mask_own && (blk * ls) / m == my_ball);
+        const uint64_t key = make_key(sc, blk);
+        cand[st * (4 / R) + u] = ok && key > lst[K - 1] ? key : 0;
+      }
+    }
+    // insert the qualifying candidates best first; the wave repeats only as many times as
+    // its busiest lane needs (most candidates fall below the lane's current k-th key)
+    for (;;) {
+      uint64_t best = 0;
+#pragma unroll
+      for (int t = 0; t < NCAND; ++t) best = cand[t] > best ? cand[t] : best;
+      const bool take = best > lst[K - 1];
+      if (!__builtin_amdgcn_ballot_w64(take)) break;
+      if (take) {
+        topk_insert<K>(lst, best);
+#pragma unroll
+        for (int t = 0; t < NCAND; ++t) cand[t] = cand[t] == best ? 0 : cand[t];
+      } else {
+#pragma unroll
+        for (int t = 0; t < NCAND; ++t) cand[t] = 0;
+      }
+    }
+  };
+  for (int t0 = 0; t0 < ntok; t0 += 2 * KT) {
+    step(t0, ks0, cv0, ks1, cv1);
+    if (t0 + KT < ntok) step(t0 + KT, ks1, cv1, ks0, cv0);
+  }
+  // merge: the 4 partial lists of group r sit in lanes r, r+16, r+32, r+48; a wave's 16
+  // groups go through LDS (the idle tile buffers) and are finalised one group at a time
   __syncthreads();
-  // merge: wave w finalises groups w, w+4, ...
-  constexpr int NC = kWaves * 4 * K;  // candidates per group
-  for (int gi = wid; gi < 16; gi += kWaves) {
+  // 16 groups x 4 lists x K keys per wave: the two tile buffers hold them when large enough
+  constexpr bool kReuse = KT * TW * 2 >= 2 * 16 * 4 * K * 8;
+  __shared__ uint64_t part_own[kReuse ? 1 : kWaves * 16 * 4 * K];
+  uint64_t* part = kReuse ? reinterpret_cast<uint64_t*>(wid < 2 ? ks0 : ks1) + (wid & 1) * 16 * 4 * K
+                          : part_own + wid * 16 * 4 * K;
+#pragma unroll
+  for (int t = 0; t < K; ++t) part[r * 4 * K + j * K + t] = lst[t];
+  wave_sync();
+  constexpr int NC = 4 * K;   // candidates per group
+  for (int gl = 0; gl < 16; ++gl) {
     uint64_t cand[(NC + 63) / 64];
 #pragma unroll
     for (int u = 0; u < (NC + 63) / 64; ++u) {
       int idx = u * 64 + lane;
-      cand[u] = idx < NC ? part[gi][idx] : 0;
+      cand[u] = idx < NC ? part[gl * NC + idx] : 0;
     }
     int mine = -1;
     for (int t = 0; t < kk; ++t) {
@@ -147,7 +223,7 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const T* q, const u
       if (lane == t) mine = (int)(0xFFFFFFFFu - (uint32_t)(w & 0xFFFFFFFFu));
     }
     // ascending order of the chosen blocks: rank among lanes < K
-    const int p = p0 + gi;
+    const int p = p0 + 16 * wid + gl;
     int rank = 0;
     for (int t = 0; t < kk; ++t) {
       int other = __shfl(mine, t, 64);
@@ -165,39 +241,42 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const T* q, const u
 
 template <typename T, int HD, int K>
 hipError_t select_k(const Dims& D, const void* q, const uint8_t* valid, const float* kcmp, const uint8_t* cvalid,
-                    int* sel, hipStream_t st) {
+                    int* sel, float* qpool, hipStream_t st) {
+  const long long total = (long long)D.B * D.H * (D.N / D.g) * HD;
+  hipLaunchKernelGGL((pool_q_kernel<T, HD>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, (const T*)q, valid,
+                     D.H, D.N, D.g, total, qpool);
   const int ngroups = D.N / D.g;
-  dim3 grid((ngroups + 15) / 16, D.B * D.H);
+  dim3 grid((ngroups + 16 * kWaves - 1) / (16 * kWaves), D.B * D.H);
   const int R = D.ls / D.l;
   if (R == 1)
-    hipLaunchKernelGGL((select_kernel<T, HD, K, 1>), grid, dim3(kWaves * 64), 0, st, (const T*)q, valid, kcmp, cvalid,
-                       D.H, D.N, D.l, D.ls, D.m, D.g, D.mask_own, D.k, sel);
+    hipLaunchKernelGGL((select_kernel<T, HD, K, 1>), grid, dim3(kWaves * 64), 0, st, (const float*)qpool, kcmp,
+                       cvalid, D.H, D.N, D.l, D.ls, D.m, D.g, D.mask_own, D.k, sel);
   else if (R == 2)
-    hipLaunchKernelGGL((select_kernel<T, HD, K, 2>), grid, dim3(kWaves * 64), 0, st, (const T*)q, valid, kcmp, cvalid,
-                       D.H, D.N, D.l, D.ls, D.m, D.g, D.mask_own, D.k, sel);
+    hipLaunchKernelGGL((select_kernel<T, HD, K, 2>), grid, dim3(kWaves * 64), 0, st, (const float*)qpool, kcmp,
+                       cvalid, D.H, D.N, D.l, D.ls, D.m, D.g, D.mask_own, D.k, sel);
   else
-    hipLaunchKernelGGL((select_kernel<T, HD, K, 4>), grid, dim3(kWaves * 64), 0, st, (const T*)q, valid, kcmp, cvalid,
-                       D.H, D.N, D.l, D.ls, D.m, D.g, D.mask_own, D.k, sel);
+    hipLaunchKernelGGL((select_kernel<T, HD, K, 4>), grid, dim3(kWaves * 64), 0, st, (const float*)qpool, kcmp,
+                       cvalid, D.H, D.N, D.l, D.ls, D.m, D.g, D.mask_own, D.k, sel);
   return hipGetLastError();
 }
 
 template <typename T, int HD>
 hipError_t select_hd(const Dims& D, const void* q, const uint8_t* valid, const float* kcmp, const uint8_t* cvalid,
-                     int* sel, hipStream_t st) {
-  if (D.k <= 4) return select_k<T, HD, 4>(D, q, valid, kcmp, cvalid, sel, st);
-  if (D.k <= 8) return select_k<T, HD, 8>(D, q, valid, kcmp, cvalid, sel, st);
-  return select_k<T, HD, 16>(D, q, valid, kcmp, cvalid, sel, st);
+                     int* sel, float* qpool, hipStream_t st) {
+  if (D.k <= 4) return select_k<T, HD, 4>(D, q, valid, kcmp, cvalid, sel, qpool, st);
+  if (D.k <= 8) return select_k<T, HD, 8>(D, q, valid, kcmp, cvalid, sel, qpool, st);
+  return select_k<T, HD, 16>(D, q, valid, kcmp, cvalid, sel, qpool, st);
 }
 
 }  // namespace
 
 hipError_t launch_select_topk(const Dims& D, const void* q, const uint8_t* valid, const float* kcmp,
-                              const uint8_t* cvalid, int* sel, hipStream_t st) {
+                              const uint8_t* cvalid, int* sel, float* qpool, hipStream_t st) {
   if (D.bf16)
-    return D.d == 64 ? select_hd<bf16_t, 64>(D, q, valid, kcmp, cvalid, sel, st)
-                     : select_hd<bf16_t, 32>(D, q, valid, kcmp, cvalid, sel, st);
-  return D.d == 64 ? select_hd<float, 64>(D, q, valid, kcmp, cvalid, sel, st)
-                   : select_hd<float, 32>(D, q, valid, kcmp, cvalid, sel, st);
+    return D.d == 64 ? select_hd<bf16_t, 64>(D, q, valid, kcmp, cvalid, sel, qpool, st)
+                     : select_hd<bf16_t, 32>(D, q, valid, kcmp, cvalid, sel, qpool, st);
+  return D.d == 64 ? select_hd<float, 64>(D, q, valid, kcmp, cvalid, sel, qpool, st)
+                   : select_hd<float, 32>(D, q, valid, kcmp, cvalid, sel, qpool, st);
 }
 
 }  // namespace bsa
