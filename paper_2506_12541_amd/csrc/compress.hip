@@ -80,22 +80,34 @@ __global__ void __launch_bounds__(kWaves * 64) mlp_fwd_kernel(const T* x, const 
       if (valid) vrow[rb] = valid + (size_t)b * N + (size_t)blk * l;
     }
   }
-  // Layer 1: pre^T[o][row] = sum_i W1^T[o][i] x[row][i]; A = W1^T, B = x^T.
-  for (int c = 0; c < ld / 32; ++c) {
+  // Layer 1: pre^T[o][row] = sum_i W1^T[o][i] x[row][i]; A = W1^T, B = x^T. The operands of
+  // chunk c + 1 are loaded while chunk c is multiplied.
+  typedef typename Chunk<T>::type CT;
+  CT bx[2][kRB], aw[2][OB];
+  auto fetch = [&](int c, CT (&bxs)[kRB], CT (&aws)[OB]) {
     const int i0 = 32 * c + 8 * j;
     const int tok = i0 / HD;
-    typename Chunk<T>::type bx[kRB];
 #pragma unroll
     for (int rb = 0; rb < kRB; ++rb) {
-      bx[rb] = zero_chunk(bx[rb]);
-      if (xrow[rb] && (vrow[rb] == nullptr || vrow[rb][tok])) bx[rb] = load_chunk(xrow[rb] + i0);
+      bxs[rb] = zero_chunk(bxs[rb]);
+      if (xrow[rb] && (vrow[rb] == nullptr || vrow[rb][tok])) bxs[rb] = load_chunk(xrow[rb] + i0);
     }
 #pragma unroll
-    for (int ob = 0; ob < OB; ++ob) {
-      auto aw = load_chunk(w1t + (size_t)(16 * ob + r) * ld + i0);
+    for (int ob = 0; ob < OB; ++ob) aws[ob] = load_chunk(w1t + (size_t)(16 * ob + r) * ld + i0);
+  };
+  auto mult = [&](const CT (&bxs)[kRB], const CT (&aws)[OB]) {
 #pragma unroll
-      for (int rb = 0; rb < kRB; ++rb) acc[rb][ob] = mma(aw, bx[rb], acc[rb][ob]);
-    }
+    for (int ob = 0; ob < OB; ++ob)
+#pragma unroll
+      for (int rb = 0; rb < kRB; ++rb) acc[rb][ob] = mma(aws[ob], bxs[rb], acc[rb][ob]);
+  };
+  const int nc = ld / 32;   // even: l*d is a multiple of 64
+  fetch(0, bx[0], aw[0]);
+  for (int c = 0; c < nc; c += 2) {
+    fetch(c + 1, bx[1], aw[1]);
+    mult(bx[0], aw[0]);
+    if (c + 2 < nc) fetch(c + 2, bx[0], aw[0]);
+    mult(bx[1], aw[1]);
   }
 
 #pragma unroll
