@@ -11,6 +11,12 @@
  *  - Every pointer argument is a device pointer on the current HIP device unless stated
  *    otherwise. Every call is asynchronous on `stream` (a hipStream_t passed as void*;
  *    NULL = the default stream) and returns once its kernels are queued.
+ *  - bsa_forward and bsa_backward run independent branches concurrently: on first use on
+ *    a device the library creates one auxiliary stream (default priority) and two events
+ *    for that device and keeps them until the process ends. Work on the auxiliary stream
+ *    starts after an event recorded on `stream` and is joined back into `stream` before
+ *    the call returns, so `stream` alone orders the call against the caller's other work.
+ *    Calls from several threads are serialised while they enqueue.
  *  - The library never allocates device memory and keeps no pointer after a call
  *    returns. The caller owns every buffer; sizes come from bsa_sizes() and
  *    bsa_ball_tree_workspace_bytes().
@@ -158,7 +164,7 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
 
 /* on = 1: start recording, clearing earlier records; on = 0: stop and clear. While on,
  * every timed phase of the library records a start and a stop HIP event on the stream
- * its kernels are launched on. Phases: "tree", "permute", "fwd.compress", "fwd.select",
+ * its kernels are launched on (phases on the two streams of a call may overlap in time). Phases: "tree", "permute", "fwd.compress", "fwd.select",
  * "fwd.ball", "fwd.cmp", "fwd.slc", "fwd.gate", "bwd.gate", "bwd.dq_ball", "bwd.dq_cmp",
  * "bwd.dq_slc", "bwd.kv_ball", "bwd.kv_cmp", "bwd.mlp", "bwd.slc_csr", "bwd.slc_kv".
  * Host-side bookkeeping only; no device memory is allocated. */

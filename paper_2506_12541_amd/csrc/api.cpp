@@ -6,6 +6,8 @@
 
 #include <cmath>
 #include <cstdio>
+#include <map>
+#include <mutex>
 #include <string>
 
 #include "kernels.hpp"
@@ -288,6 +290,39 @@ bsa_status_t bsa_saved_view(const bsa_params_t* p, void* base, bsa_saved_t* out)
   return BSA_OK;
 }
 
+// One auxiliary stream (default priority) and a fork/join event pair per device, created on
+// first use: independent branches run on it concurrently with the caller's stream. The
+// mutex is held while a call enqueues its work, so the shared events are never recorded
+// by two calls at once.
+struct Aux {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+std::mutex g_aux_mu;
+std::map<int, Aux> g_aux;
+
+static bsa_status_t get_aux(Aux* out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(BSA_ERR_HIP, "hipGetDevice failed");
+  auto it = g_aux.find(dev);
+  if (it == g_aux.end()) {
+    Aux a;
+    if (hipStreamCreateWithFlags(&a.s, hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&a.fork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&a.join, hipEventDisableTiming) != hipSuccess)
+      return fail(BSA_ERR_HIP, "creating the auxiliary stream and events failed");
+    it = g_aux.emplace(dev, a).first;
+  }
+  *out = it->second;
+  return BSA_OK;
+}
+
+static bsa_status_t join_aux(const Aux& a, hipStream_t st) {
+  if (hipEventRecord(a.join, a.s) != hipSuccess || hipStreamWaitEvent(st, a.join, 0) != hipSuccess)
+    return fail(BSA_ERR_HIP, "joining the auxiliary stream failed");
+  return BSA_OK;
+}
+
 static bool saved_ok(const bsa_saved_t* sv) {
   return sv && sv->sel_idx && sv->lse && sv->o_branch && sv->kcmp && sv->vcmp && sv->hid_k && sv->hid_v && sv->cvalid;
 }
@@ -310,6 +345,10 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   if (!ws || ws_bytes < W.total)
     return fail(BSA_ERR_WORKSPACE_TOO_SMALL, "forward workspace needs " + std::to_string(W.total) + " bytes");
   hipStream_t st = (hipStream_t)stream;
+  std::lock_guard<std::mutex> lock(g_aux_mu);
+  Aux aux;
+  s = get_aux(&aux);
+  if (s != BSA_OK) return s;
   char* w = (char*)ws;
   const size_t rows = (size_t)D.rows();
   char* ob = (char*)saved->o_branch;
@@ -333,17 +372,27 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
                                       : bsa::launch_compress_fwd(D, v, valid, mv, saved->vcmp, saved->hid_v, vc_lp,
                                                                  w + W.w1t_v, st)),
            "compression");
+  // ball and compressed attention on the auxiliary stream, selection on the caller's
+  if (hipEventRecord(aux.fork, st) != hipSuccess || hipStreamWaitEvent(aux.s, aux.fork, 0) != hipSuccess)
+    return fail(BSA_ERR_HIP, "forking the auxiliary stream failed");
+  {
+    hipStream_t st_main = st;
+    hipStream_t st = aux.s;
+    BSA_STEP("fwd.ball", bsa::launch_ball_fwd(D, q, k, v, valid, ob, saved->lse, st), "ball attention");
+    BSA_STEP("fwd.cmp",
+             bsa::launch_cmp_fwd(D, q, kc_lp, vc_lp, valid, valid ? saved->cvalid : nullptr, ob + ob_stride,
+                                 saved->lse + rows, st),
+             "compressed attention");
+    (void)st_main;
+  }
   BSA_STEP("fwd.select", bsa::launch_select_topk(D, q, valid, saved->kcmp, saved->cvalid, saved->sel_idx,
                                                   (float*)(w + W.qpool), st),
            "select");
-  BSA_STEP("fwd.ball", bsa::launch_ball_fwd(D, q, k, v, valid, ob, saved->lse, st), "ball attention");
-  BSA_STEP("fwd.cmp",
-           bsa::launch_cmp_fwd(D, q, kc_lp, vc_lp, valid, valid ? saved->cvalid : nullptr, ob + ob_stride,
-                               saved->lse + rows, st),
-           "compressed attention");
   BSA_STEP("fwd.slc",
            bsa::launch_slc_fwd(D, q, k, v, valid, saved->sel_idx, ob + 2 * ob_stride, saved->lse + 2 * rows, st),
            "selection attention");
+  s = join_aux(aux, st);
+  if (s != BSA_OK) return s;
   BSA_STEP("fwd.gate", bsa::launch_gate_fwd(D, ob, gate, valid, o, st), "gate");
 #undef BSA_STEP
   return BSA_OK;
@@ -371,6 +420,10 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   if (!ws || ws_bytes < W.total)
     return fail(BSA_ERR_WORKSPACE_TOO_SMALL, "backward workspace needs " + std::to_string(W.total) + " bytes");
   hipStream_t st = (hipStream_t)stream;
+  std::lock_guard<std::mutex> lock(g_aux_mu);
+  Aux aux;
+  s = get_aux(&aux);
+  if (s != BSA_OK) return s;
   char* w = (char*)ws;
   bsa::BwdArgs A{};
   A.q = q; A.k = k; A.v = v; A.dout = d_o; A.valid = valid; A.gate = gate;
@@ -386,7 +439,9 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   A.pair_keys_tmp = (uint32_t*)(w + W.pkt); A.pair_vals_tmp = (uint32_t*)(w + W.pvt);
   A.sort_hist = (uint32_t*)(w + W.hist);
   A.seg_start = (int*)(w + W.seg_s); A.seg_end = (int*)(w + W.seg_e);
-  BSA_TRY(bsa::launch_attn_bwd(D, A, st), "attention backward");
+  // after the dense dK/dV passes, the dQ passes run on the auxiliary stream while the
+  // compression and selection dK/dV passes run on the caller's
+  BSA_TRY(bsa::launch_attn_bwd(D, A, st, aux.s, aux.fork), "attention backward");
   bsa::MlpBwdWs mw{(float*)(w + W.dpre), (float*)(w + W.pw1), (float*)(w + W.psm), (void*)(w + W.w1lp),
                    W.mlp_chunks, W.mlp_chunks_small, (void*)(w + W.dplp)};
   bsa::Mlp mk{}, mv{};
@@ -403,7 +458,7 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   BSA_PHASE("bwd.mlp", st, e = bsa::launch_compress_bwd(D, v, valid, mv, saved->hid_v, A.dvc, dv, gv, mw, st));
   BSA_TRY(e, "compression backward V");
   BSA_TRY(bsa::launch_slc_csr(D, A, st), "selection backward");
-  return BSA_OK;
+  return join_aux(aux, st);
 }
 
 }  // extern "C"

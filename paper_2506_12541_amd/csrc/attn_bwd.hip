@@ -1175,7 +1175,7 @@ void launch_bwd_kv(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v
 }
 
 template <typename T, int HD>
-hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
+hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t st_q, hipEvent_t fork) {
   const long long rows = D.rows();
   const float sl2 = D.scale * kLog2e;
   const int nct = D.N / D.l;
@@ -1205,28 +1205,6 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
     kc = (const T*)A.kcmp;
     vc = (const T*)A.vcmp;
   }
-  // ---- dQ: ball (write), compressed (add), selection (add) ----
-  BSA_PHASE("bwd.dq_ball", st, {
-  if (D.m >= 128)
-    (launch_bwd_q<T, HD, 2, true, false>)(dim3(D.N / 128, D.H, D.B), st, q, k, v, dout, A.valid, qball, D.H, D.N,
-                                          D.N, D.m, sl2, D.scale, A.dq);
-  else
-    (launch_bwd_q<T, HD, 1, true, false>)(dim3(D.N / 64, D.H, D.B), st, q, k, v, dout, A.valid, qball, D.H, D.N,
-                                          D.N, D.m, sl2, D.scale, A.dq);
-  });
-  BSA_PHASE("bwd.dq_cmp", st,
-  (launch_bwd_q<T, HD, 2, false, true>)(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, dout,
-                                        A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq));
-  BSA_PHASE("bwd.dq_slc", st, {
-  if constexpr (sizeof(T) == 2) {
-    constexpr int NW = 2;
-    hipLaunchKernelGGL((slc_bwd_q_dma_kernel<HD, NW>), dim3(D.N / (16 * NW), D.H, D.B), dim3(64 * NW), 0, st, q, k, v,
-                       dout, A.valid, A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq);
-  } else {
-    hipLaunchKernelGGL((slc_bwd_q_kernel<T, HD>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, q, k, v, dout, A.valid,
-                       A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq);
-  }
-  });
   // ---- dK, dV of the ball branch (written) ----
   BSA_PHASE("bwd.kv_ball", st, {
   if (D.m >= 128)
@@ -1248,6 +1226,38 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
                        A.dkc);
     hipLaunchKernelGGL(sum_chunks_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.dvc_part, nch, n,
                        A.dvc);
+  }
+  // ---- dQ: ball (write), compressed (add), selection (add), on st_q ----
+  if (st_q != st) {
+    hipError_t e = hipEventRecord(fork, st);
+    if (e == hipSuccess) e = hipStreamWaitEvent(st_q, fork, 0);
+    if (e != hipSuccess) return e;
+  }
+  {
+  hipStream_t st_main = st;
+  hipStream_t st = st_q;   // the dQ chain below
+  BSA_PHASE("bwd.dq_ball", st, {
+  if (D.m >= 128)
+    (launch_bwd_q<T, HD, 2, true, false>)(dim3(D.N / 128, D.H, D.B), st, q, k, v, dout, A.valid, qball, D.H, D.N,
+                                          D.N, D.m, sl2, D.scale, A.dq);
+  else
+    (launch_bwd_q<T, HD, 1, true, false>)(dim3(D.N / 64, D.H, D.B), st, q, k, v, dout, A.valid, qball, D.H, D.N,
+                                          D.N, D.m, sl2, D.scale, A.dq);
+  });
+  BSA_PHASE("bwd.dq_cmp", st,
+  (launch_bwd_q<T, HD, 2, false, true>)(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, dout,
+                                        A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq));
+  BSA_PHASE("bwd.dq_slc", st, {
+  if constexpr (sizeof(T) == 2) {
+    constexpr int NW = 2;
+    hipLaunchKernelGGL((slc_bwd_q_dma_kernel<HD, NW>), dim3(D.N / (16 * NW), D.H, D.B), dim3(64 * NW), 0, st, q, k, v,
+                       dout, A.valid, A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq);
+  } else {
+    hipLaunchKernelGGL((slc_bwd_q_kernel<T, HD>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, q, k, v, dout, A.valid,
+                       A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq);
+  }
+  });
+  (void)st_main;
   }
   return hipGetLastError();
 }
@@ -1476,8 +1486,8 @@ hipError_t slc_kv_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
 
 }  // namespace
 
-hipError_t launch_attn_bwd(const Dims& D, const BwdArgs& A, hipStream_t st) {
-  return BSA_DISPATCH(bwd_impl, D, A, st);
+hipError_t launch_attn_bwd(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t st_q, hipEvent_t fork) {
+  return BSA_DISPATCH(bwd_impl, D, A, st, st_q, fork);
 }
 
 hipError_t launch_slc_csr(const Dims& D, const BwdArgs& A, hipStream_t st) {

@@ -75,7 +75,10 @@ struct BwdArgs {
 };
 
 // attn_bwd.hip
-hipError_t launch_attn_bwd(const Dims& D, const BwdArgs& A, hipStream_t st);
+// The dQ passes run on st_q (may equal st): after the ball and compressed dK/dV passes are
+// enqueued on st, `fork` is recorded there and st_q waits for it; the caller joins st_q
+// back into st.
+hipError_t launch_attn_bwd(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t st_q, hipEvent_t fork);
 hipError_t launch_slc_csr(const Dims& D, const BwdArgs& A, hipStream_t st);
 
 // compress.hip: backward of phi (dK^ -> token gradients added into dx, weight gradients)
