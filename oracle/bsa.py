@@ -22,7 +22,13 @@ Readings of points the paper leaves open (each is stated where it is used):
   * top-k orders by (higher score, lower index); indices are stored ascending, padded
     with -1 when fewer than k* blocks are eligible;
   * the selection set is per head; the gate is per token and shared across heads;
-  * a softmax row with no eligible key outputs zeros and has log-sum-exp -inf.
+  * a softmax row with no eligible key outputs zeros and has log-sum-exp -inf;
+  * query coarsening (Eq. 13) pools blocks of l queries, so the selection groups of Eq.
+    13-14 are those blocks (g = l); its MLP phi_q has the shape of phi_k, and its mean
+    form is the pooled query of Eq. 11;
+  * group compression (Eq. 15) attends from the coarse queries of Eq. 13 (a coarse query
+    is valid iff its block holds a real token) and copies each result to the real
+    queries of its block; dummy rows stay zero.
 """
 from __future__ import annotations
 
@@ -45,6 +51,12 @@ class Params:
     mask_own_ball: bool = True
     kv_pool: str = "mlp"      # "mlp" or "mean" (Eq. 5)
     scale: float | None = None
+    q_coarsen: str = "mean"   # "mean" (Eq. 11) or "mlp" (phi_q of Eq. 13; needs g = l)
+    group_compression: bool = False   # Eq. 15 (needs g = l)
+
+    def __post_init__(self):
+        if (self.q_coarsen == "mlp" or self.group_compression) and self.group != self.cmp_block:
+            raise ValueError("query coarsening over blocks (Eq. 13, 15) needs group == cmp_block")
 
     def sm_scale(self, d: int) -> float:
         return 1.0 / math.sqrt(d) if self.scale is None else float(self.scale)
@@ -138,11 +150,10 @@ def block_rows(x, valid, l):
     return xz.reshape(n // l, l * d)
 
 
-def compress(x, valid, phi, P: Params):
-    """Compressed tokens [N/l, d] and the cache needed for the backward pass."""
-    l = P.cmp_block
+def pool_blocks(x, valid, l, pool, phi):
+    """phi (an MLP, or the mean) of each length-l block of x: [N/l, d] and a cache."""
     flat = block_rows(x, valid, l)
-    if P.kv_pool == "mean":
+    if pool == "mean":
         d = x.shape[1]
         return flat.reshape(-1, l, d).sum(axis=1) / l, {"flat": flat}
     pre = flat @ phi["w1"] + phi["b1"]
@@ -151,11 +162,10 @@ def compress(x, valid, phi, P: Params):
     return out, {"flat": flat, "pre": pre, "hid": hid}
 
 
-def compress_backward(dout, cache, valid, phi, P: Params):
-    """Given d(compressed tokens), return (d tokens [N, d], dict of weight grads)."""
-    l = P.cmp_block
+def pool_blocks_backward(dout, cache, valid, l, pool, phi):
+    """Given d(pooled tokens), return (d tokens [N, d], dict of weight grads)."""
     d = dout.shape[1]
-    if P.kv_pool == "mean":
+    if pool == "mean":
         dflat = np.repeat(dout / l, l, axis=0)
         return np.where(valid[:, None], dflat, 0.0), {}
     grads = {
@@ -170,6 +180,27 @@ def compress_backward(dout, cache, valid, phi, P: Params):
                     "w1": np.abs(cache["flat"]).T @ np.abs(dpre), "b1": np.abs(dpre).sum(axis=0)}
     dx = (dpre @ phi["w1"].T).reshape(-1, d)
     return np.where(valid[:, None], dx, 0.0), grads
+
+
+def compress(x, valid, phi, P: Params):
+    """Compressed tokens [N/l, d] of Eq. 5 and the cache needed for the backward pass."""
+    return pool_blocks(x, valid, P.cmp_block, P.kv_pool, phi)
+
+
+def compress_backward(dout, cache, valid, phi, P: Params):
+    """Given d(compressed tokens), return (d tokens [N, d], dict of weight grads)."""
+    return pool_blocks_backward(dout, cache, valid, P.cmp_block, P.kv_pool, phi)
+
+
+def coarse_queries(q, valid, phi_q, P: Params):
+    """Coarse queries [N/g, d]: the pooled query of Eq. 11 (q_coarsen "mean": the group's
+    real queries summed and divided by g) or phi_q of each block of l = g queries, dummy
+    rows zero (Eq. 13)."""
+    return pool_blocks(q, valid, P.group, P.q_coarsen, phi_q)
+
+
+def coarse_queries_backward(dqc, cache, valid, phi_q, P: Params):
+    return pool_blocks_backward(dqc, cache, valid, P.group, P.q_coarsen, phi_q)
 
 
 def block_valid(valid, l):
@@ -201,23 +232,57 @@ def compression_branch_backward(q, kc, vc, cvalid, valid, P: Params, o, lse, do)
     return dq, dkc, dvc
 
 
+def group_compression_branch(qc, kc, vc, cvalid, valid, P: Params):
+    """Eq. 15: attention of the valid coarse queries to the compressed tokens, each result
+    copied to the real queries of its block. Returns (o [N, d], lse [N], oc, lsec)."""
+    l = P.cmp_block
+    n = valid.shape[0]
+    d = qc.shape[1]
+    oc = np.zeros((n // l, d))
+    lsec = np.full(n // l, NEG_INF)
+    rows = np.nonzero(cvalid)[0]
+    oc[rows], lsec[rows] = attend(qc[rows], kc, vc, cvalid, P.sm_scale(d))
+    blk = np.arange(n) // l
+    o = np.where(valid[:, None], oc[blk], 0.0)
+    lse = np.where(valid, lsec[blk], NEG_INF)
+    return o, lse, oc, lsec
+
+
+def group_compression_branch_backward(qc, kc, vc, cvalid, valid, P: Params, oc, lsec, do):
+    """Gradients of Eq. 15 given the branch's upstream gradient do [N, d]: the copy's
+    adjoint sums do over the real queries of each block. Returns (dqc, dkc, dvc)."""
+    l = P.cmp_block
+    n, d = do.shape
+    doc = np.where(valid[:, None], do, 0.0).reshape(n // l, l, d).sum(axis=1)
+    dqc = np.zeros_like(qc)
+    rows = np.nonzero(cvalid)[0]
+    gq, dkc, dvc = attend_backward(qc[rows], kc, vc, cvalid, P.sm_scale(d), oc[rows], lsec[rows],
+                                   doc[rows])
+    dqc[rows] = gq
+    return dqc, dkc, dvc
+
+
 # ----------------------------------------------------------------------------------
 # Branch 3: group-shared block selection (Eq. 6, 7, 10-12) and selection attention (Eq. 8).
 # ----------------------------------------------------------------------------------
-def group_block_scores(q, kc, valid, P: Params, groups=None):
+def group_block_scores(q, kc, valid, P: Params, groups=None, qc=None):
     """Scores [N/g, N/l'] of every selection block for every query group (or only for the
     listed groups, in that order).
 
-    Pooled query q_p = (1/g) * sum of the group's real queries (Eq. 11); compressed-block
-    score S_pc = <q_p, kc_c> (Eq. 6, 12); a selection block of r = l'/l compressed blocks
-    scores the mean of their scores. Own-ball and all-dummy blocks score -inf.
+    Pooled query q_p = (1/g) * sum of the group's real queries (Eq. 11), or the given
+    coarse queries qc [N/g, d] (Eq. 13); compressed-block score S_pc = <q_p, kc_c> (Eq. 6,
+    12, 14); a selection block of r = l'/l compressed blocks scores the mean of their
+    scores. Own-ball and all-dummy blocks score -inf.
     """
     n, d = q.shape
     g, l, ls, m = P.group, P.cmp_block, P.slc_block, P.ball
     r = ls // l
     groups = np.arange(n // g) if groups is None else np.asarray(groups)
-    qz = np.where(valid[:, None], q, 0.0).reshape(n // g, g, d)[groups]
-    qp = qz.sum(axis=1) / g
+    if qc is None:
+        qz = np.where(valid[:, None], q, 0.0).reshape(n // g, g, d)[groups]
+        qp = qz.sum(axis=1) / g
+    else:
+        qp = qc[groups]
     s_cmp = qp @ kc.T                                  # [groups, N/l]
     s_blk = s_cmp.reshape(len(groups), n // ls, r).mean(axis=2)
     blk_ok = block_valid(valid, ls)
@@ -298,14 +363,15 @@ def _phi64(phi):
     return {k: _f64(v) for k, v in phi.items()} if phi is not None else None
 
 
-def forward(q, k, v, valid, gate, phi_k, phi_v, P: Params):
-    """Full forward pass. Arrays as described in the module docstring.
+def forward(q, k, v, valid, gate, phi_k, phi_v, P: Params, phi_q=None):
+    """Full forward pass. Arrays as described in the module docstring; phi_q is the query
+    MLP of Eq. 13 (q_coarsen "mlp").
 
     Returns a dict with o [B,H,N,d], o_branch [3,B,H,N,d], lse [3,B,H,N], sel [B,H,N/g,k*],
-    kc/vc [B,H,N/l,d], and the compression caches for the backward pass.
+    kc/vc [B,H,N/l,d], qc [B,H,N/g,d] (coarse queries), and the caches for the backward.
     """
     q, k, v, gate = _f64(q), _f64(k), _f64(v), _f64(gate)
-    phi_k, phi_v = _phi64(phi_k), _phi64(phi_v)
+    phi_k, phi_v, phi_q = _phi64(phi_k), _phi64(phi_v), _phi64(phi_q)
     valid = np.asarray(valid, dtype=bool)
     B, H, n, d = q.shape
     l, g = P.cmp_block, P.group
@@ -314,6 +380,8 @@ def forward(q, k, v, valid, gate, phi_k, phi_v, P: Params):
     sel = np.full((B, H, n // g, P.topk), -1, dtype=np.int64)
     kc = np.zeros((B, H, n // l, d))
     vc = np.zeros((B, H, n // l, d))
+    qc = np.zeros((B, H, n // g, d))
+    ocs, lsecs = {}, {}
     caches = {}
     for b in range(B):
         vb = valid[b]
@@ -323,26 +391,32 @@ def forward(q, k, v, valid, gate, phi_k, phi_v, P: Params):
             ob[0, b, h], lse[0, b, h] = ball_branch(qq, kk, vv, vb, P)
             kc[b, h], ck = compress(kk, vb, phi_k, P)
             vc[b, h], cv = compress(vv, vb, phi_v, P)
-            caches[(b, h)] = (ck, cv)
-            ob[1, b, h], lse[1, b, h] = compression_branch(qq, kc[b, h], vc[b, h], cvalid, vb, P)
-            sel[b, h] = topk_blocks(group_block_scores(qq, kc[b, h], vb, P), P.topk)
+            qc[b, h], cq = coarse_queries(qq, vb, phi_q, P)
+            caches[(b, h)] = (ck, cv, cq)
+            if P.group_compression:
+                ob[1, b, h], lse[1, b, h], ocs[(b, h)], lsecs[(b, h)] = group_compression_branch(
+                    qc[b, h], kc[b, h], vc[b, h], cvalid, vb, P)
+            else:
+                ob[1, b, h], lse[1, b, h] = compression_branch(qq, kc[b, h], vc[b, h], cvalid, vb, P)
+            sel[b, h] = topk_blocks(group_block_scores(qq, kc[b, h], vb, P, qc=qc[b, h]), P.topk)
             ob[2, b, h], lse[2, b, h] = selection_branch(qq, kk, vv, vb, sel[b, h], P)
     sg = sigmoid(gate)                                # [B, N, 3]
     o = np.zeros((B, H, n, d))
     for br in range(3):
         o += sg[:, None, :, br, None] * ob[br]
-    return {"o": o, "o_branch": ob, "lse": lse, "sel": sel, "kc": kc, "vc": vc,
-            "caches": caches}
+    return {"o": o, "o_branch": ob, "lse": lse, "sel": sel, "kc": kc, "vc": vc, "qc": qc,
+            "oc": ocs, "lsec": lsecs, "caches": caches}
 
 
-def backward(q, k, v, valid, gate, phi_k, phi_v, P: Params, fwd, do):
-    """Gradients of sum(o * do) with respect to q, k, v, the gate logits and both MLPs.
+def backward(q, k, v, valid, gate, phi_k, phi_v, P: Params, fwd, do, phi_q=None):
+    """Gradients of sum(o * do) with respect to q, k, v, the gate logits and the MLPs.
 
-    The top-k selection is piecewise constant, so no gradient flows through the scores.
+    The top-k selection is piecewise constant, so no gradient flows through the scores;
+    phi_q therefore receives a gradient only through group compression (Eq. 15).
     Weight gradients are summed over batch, heads and blocks.
     """
     q, k, v, gate, do = _f64(q), _f64(k), _f64(v), _f64(gate), _f64(do)
-    phi_k, phi_v = _phi64(phi_k), _phi64(phi_v)
+    phi_k, phi_v, phi_q = _phi64(phi_k), _phi64(phi_v), _phi64(phi_q)
     valid = np.asarray(valid, dtype=bool)
     B, H, n, d = q.shape
     l = P.cmp_block
@@ -360,6 +434,9 @@ def backward(q, k, v, valid, gate, phi_k, phi_v, P: Params, fwd, do):
     dphi_v = {w: np.zeros_like(phi_v[w]) for w in wkeys} if P.kv_pool == "mlp" else {}
     abs_k = {w: np.zeros_like(phi_k[w]) for w in wkeys} if P.kv_pool == "mlp" else {}
     abs_v = {w: np.zeros_like(phi_v[w]) for w in wkeys} if P.kv_pool == "mlp" else {}
+    q_mlp = P.group_compression and P.q_coarsen == "mlp"
+    dphi_q = {w: np.zeros_like(phi_q[w]) for w in wkeys} if q_mlp else {}
+    abs_q = {w: np.zeros_like(phi_q[w]) for w in wkeys} if q_mlp else {}
     for b in range(B):
         vb = valid[b]
         cvalid = block_valid(vb, l)
@@ -367,9 +444,18 @@ def backward(q, k, v, valid, gate, phi_k, phi_v, P: Params, fwd, do):
             qq, kk, vv = q[b, h], k[b, h], v[b, h]
             dob = [sg[b, :, br, None] * do[b, h] for br in range(3)]
             g0 = ball_branch_backward(qq, kk, vv, vb, P, ob[0, b, h], lse[0, b, h], dob[0])
-            gq, gkc, gvc = compression_branch_backward(qq, fwd["kc"][b, h], fwd["vc"][b, h], cvalid,
-                                                       vb, P, ob[1, b, h], lse[1, b, h], dob[1])
-            ck, cv = fwd["caches"][(b, h)]
+            ck, cv, cq = fwd["caches"][(b, h)]
+            if P.group_compression:
+                gqc, gkc, gvc = group_compression_branch_backward(
+                    fwd["qc"][b, h], fwd["kc"][b, h], fwd["vc"][b, h], cvalid, vb, P, fwd["oc"][(b, h)],
+                    fwd["lsec"][(b, h)], dob[1])
+                gq, wq = coarse_queries_backward(gqc, cq, vb, phi_q, P)
+                for w in wkeys if wq else ():
+                    dphi_q[w] += wq[w]
+                    abs_q[w] += wq["abs"][w]
+            else:
+                gq, gkc, gvc = compression_branch_backward(qq, fwd["kc"][b, h], fwd["vc"][b, h], cvalid,
+                                                           vb, P, ob[1, b, h], lse[1, b, h], dob[1])
             dk_c, wk = compress_backward(gkc, ck, vb, phi_k, P)
             dv_c, wv = compress_backward(gvc, cv, vb, phi_v, P)
             g2 = selection_branch_backward(qq, kk, vv, vb, sel[b, h], P, ob[2, b, h], lse[2, b, h],
@@ -383,4 +469,4 @@ def backward(q, k, v, valid, gate, phi_k, phi_v, P: Params, fwd, do):
                 abs_k[w] += wk["abs"][w]
                 abs_v[w] += wv["abs"][w]
     return {"dq": dq, "dk": dk, "dv": dv, "dgate": dgate, "dphi_k": dphi_k, "dphi_v": dphi_v,
-            "abs": {"dgate": dgate_abs, "dphi_k": abs_k, "dphi_v": abs_v}}
+            "dphi_q": dphi_q, "abs": {"dgate": dgate_abs, "dphi_k": abs_k, "dphi_v": abs_v, "dphi_q": abs_q}}

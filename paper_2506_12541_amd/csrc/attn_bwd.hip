@@ -98,12 +98,11 @@ __global__ void sum_chunks_kernel(const float* part, int nchunks, long long n, f
 }
 
 // Per-query terms of one branch: log2 LSE, delta D = s * R, gate scale s.
+// Per query row of one branch: packed (log2 LSE, s, s * R, 0), where s scales the row's
+// dO (the branch gate sigmoid(gamma_b), or 1 for rows whose dO is already scaled) and
+// s * R is the softmax-backward delta rowsum(s dO * o_b). [B, H, N] float4.
 struct QTerms {
-  const float* lse;   // [B,H,N] of this branch
-  const float* R;     // [B,H,N] rowsum(dO * o_b) of this branch
-  const float* gate;  // [B,N,3]
-  int br;
-  const float4* t4;   // [B,H,N] packed (log2 LSE, s, s * R, 0) of this branch
+  const float4* t4;
 };
 
 // ==== query-major pass, dense key sets (ball: own ball; compression: all tokens) ====
@@ -143,9 +142,10 @@ __global__ void __launch_bounds__(256) dense_bwd_q_kernel(const T* q, const T* k
       qf[qb][c] = load_chunk(q + row * HD + 32 * c + 8 * j);
       df[qb][c] = load_chunk(dout + row * HD + 32 * c + 8 * j);
     }
-    l2[qb] = lse_log2(qt.lse[row]);
-    gs[qb] = sigmoidf(qt.gate[((size_t)b * N + wq0 + 16 * qb + r) * 3 + qt.br]);
-    dd[qb] = gs[qb] * qt.R[row];
+    const float4 t = qt.t4[row];
+    l2[qb] = t.x;
+    gs[qb] = t.y;
+    dd[qb] = t.z;
 #pragma unroll
     for (int db = 0; db < DB; ++db) acc[qb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
@@ -439,7 +439,7 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
   typedef TileIO<T, HD, kQT, NW * 64> IO;
   uint4 qreg[IO::RV], dreg[IO::RV];
   typename IO::V4 qtreg[IO::TV][4], dtreg[IO::TV][4];
-  float tl = 0.f, tg = 0.f, tr = 0.f;
+  float4 tv = make_float4(0.f, 0.f, 0.f, 0.f);
   auto fetch = [&](int t0) {
     IO::load_rows(qreg, qh, t0, N);
     IO::load_rows(dreg, dh, t0, N);
@@ -447,9 +447,7 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
     IO::load_tr(dtreg, dh, t0, N);
     if (threadIdx.x < kQT) {
       const long long row = rowbase + t0 + threadIdx.x;
-      tl = qt.lse[row];
-      tg = qt.gate[((size_t)b * N + t0 + threadIdx.x) * 3 + qt.br];
-      tr = qt.R[row];
+      tv = qt.t4[row];
     }
   };
   fetch(qbeg);
@@ -461,10 +459,9 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
     IO::store_tr(qtreg, qtr, TSTR);
     IO::store_tr(dtreg, dtr, TSTR);
     if (threadIdx.x < kQT) {
-      const float g = sigmoidf(tg);
-      l2s[threadIdx.x] = lse_log2(tl);
-      gss[threadIdx.x] = g;
-      dds[threadIdx.x] = g * tr;
+      l2s[threadIdx.x] = tv.x;
+      gss[threadIdx.x] = tv.y;
+      dds[threadIdx.x] = tv.z;
     }
     __syncthreads();
     if (t0 + kQT < qend) fetch(t0 + kQT);
@@ -717,9 +714,8 @@ __global__ void __launch_bounds__(256) slc_bwd_q_kernel(const T* q, const T* k, 
     qf[c] = load_chunk(q + row * HD + 32 * c + 8 * j);
     df[c] = load_chunk(dout + row * HD + 32 * c + 8 * j);
   }
-  const float l2 = lse_log2(qt.lse[row]);
-  const float gs = sigmoidf(qt.gate[((size_t)b * N + wq0 + r) * 3 + qt.br]);
-  const float dd = gs * qt.R[row];
+  const float4 tq = qt.t4[row];
+  const float l2 = tq.x, gs = tq.y, dd = tq.z;
   f32x4 acc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -1049,9 +1045,10 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_kernel(const T* q, const T* k,
       gv[i] = 0.f;
       if (rr < qrows) {
         const long long row = bh * N + qr0 + rr;
-        lv[i] = lse_log2(qt.lse[row]);
-        gv[i] = sigmoidf(qt.gate[((size_t)b * N + qr0 + rr) * 3 + qt.br]);
-        dvv[i] = gv[i] * qt.R[row];
+        const float4 t = qt.t4[row];
+        lv[i] = t.x;
+        gv[i] = t.y;
+        dvv[i] = t.z;
       }
     }
   };
@@ -1187,9 +1184,9 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t
                      D.N, A.dgate);
   });
   const float4* t4 = (const float4*)A.terms;
-  QTerms qball{A.lse, A.R, A.gate, 0, t4};
-  QTerms qcmp{A.lse + rows, A.R + rows, A.gate, 1, t4 + rows};
-  QTerms qslc{A.lse + 2 * rows, A.R + 2 * rows, A.gate, 2, t4 + 2 * rows};
+  QTerms qball{t4};
+  QTerms qcmp{t4 + rows};
+  QTerms qslc{t4 + 2 * rows};
   const T* q = (const T*)A.q;
   const T* k = (const T*)A.k;
   const T* v = (const T*)A.v;
@@ -1464,7 +1461,7 @@ template <typename T, int HD>
 hipError_t slc_kv_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
   const long long rows = D.rows();
   const float sl2 = D.scale * kLog2e;
-  QTerms qslc{A.lse + 2 * rows, A.R + 2 * rows, A.gate, 2, (const float4*)A.terms + 2 * rows};
+  QTerms qslc{(const float4*)A.terms + 2 * rows};
   const long long nseg = (long long)D.B * D.H * (D.N / D.ls);
   const int kbw = D.ls / 16;
   const dim3 grid((unsigned)nseg);

@@ -26,7 +26,7 @@ def _inputs(seed, B=2, H=2, n=64, d=8, n_real=53, P=None):
     phi = lambda: {"w1": x(P.cmp_block * d, d) * 0.2, "b1": x(d) * 0.2, "w2": x(d, d) * 0.2,
                    "b2": x(d) * 0.2}
     return dict(P=P, q=x(B, H, n, d), k=x(B, H, n, d), v=x(B, H, n, d), valid=valid,
-                gate=x(B, n, 3), phi_k=phi(), phi_v=phi(), do=x(B, H, n, d))
+                gate=x(B, n, 3), phi_k=phi(), phi_v=phi(), phi_q=phi(), do=x(B, H, n, d))
 
 
 def _dense_torch(inp, sel):
@@ -36,6 +36,7 @@ def _dense_torch(inp, sel):
     q, k, v, gate = t(inp["q"]), t(inp["k"]), t(inp["v"]), t(inp["gate"])
     pk = {w: t(a) for w, a in inp["phi_k"].items()}
     pv = {w: t(a) for w, a in inp["phi_v"].items()}
+    pq = {w: t(a) for w, a in inp["phi_q"].items()}
     B, H, n, d = q.shape
     valid = torch.from_numpy(inp["valid"])
     l, ls, g, m = P.cmp_block, P.slc_block, P.group, P.ball
@@ -64,6 +65,20 @@ def _dense_torch(inp, sel):
             kc, vc = mlp(kz, pk), mlp(vz, pv)
             cval = vb.reshape(n // l, l).any(dim=1)
             cmp_mask = cval[None, :] & qmask
+            if P.group_compression:
+                # Eq. 13 then Eq. 15 as matrices: coarse queries from the zero-padded blocks,
+                # one masked softmax over [N/l, N/l], then a copy matrix onto the real rows
+                qz = torch.where(vb[:, None], qq, 0.0)
+                if P.q_coarsen == "mlp":
+                    qc = mlp(qz.reshape(n // l, l * d), pq)
+                else:
+                    avg = (idx[None, :] // l == torch.arange(n // l)[:, None]).double() / l
+                    qc = avg @ qz
+                oc = masked_attn(qc, kc, vc, cval[None, :] & cval[:, None])
+                copy = ((idx[:, None] // l == torch.arange(n // l)[None, :]) & qmask).double()
+                o_cmp = copy @ oc
+            else:
+                o_cmp = masked_attn(qq, kc, vc, cmp_mask)
             chosen = torch.zeros(n // g, n // ls, dtype=torch.bool)
             for p in range(n // g):
                 for j in sel[b, h, p]:
@@ -72,7 +87,7 @@ def _dense_torch(inp, sel):
             slc_mask = chosen[idx // g][:, idx // ls] & vb[None, :] & qmask
             sg = torch.sigmoid(gate[b])
             out[b, h] = (sg[:, 0:1] * masked_attn(qq, kk, vv, ball_mask)
-                         + sg[:, 1:2] * masked_attn(qq, kc, vc, cmp_mask)
+                         + sg[:, 1:2] * o_cmp
                          + sg[:, 2:3] * masked_attn(qq, kk, vv, slc_mask))
     loss = (out * torch.from_numpy(inp["do"])).sum()
     loss.backward()
@@ -80,14 +95,15 @@ def _dense_torch(inp, sel):
     return out.detach().numpy(), {
         "dq": g(q), "dk": g(k), "dv": g(v), "dgate": g(gate),
         "dphi_k": {w: g(a) for w, a in pk.items()}, "dphi_v": {w: g(a) for w, a in pv.items()},
+        "dphi_q": {w: (g(a) if a.grad is not None else np.zeros(a.shape)) for w, a in pq.items()},
     }
 
 
 def _run_oracle(inp):
     fwd = bsa.forward(inp["q"], inp["k"], inp["v"], inp["valid"], inp["gate"], inp["phi_k"],
-                      inp["phi_v"], inp["P"])
+                      inp["phi_v"], inp["P"], phi_q=inp["phi_q"])
     grads = bsa.backward(inp["q"], inp["k"], inp["v"], inp["valid"], inp["gate"], inp["phi_k"],
-                         inp["phi_v"], inp["P"], fwd, inp["do"])
+                         inp["phi_v"], inp["P"], fwd, inp["do"], phi_q=inp["phi_q"])
     return fwd, grads
 
 
@@ -105,9 +121,30 @@ def test_against_torch_dense_autograd(seed, mask_own):
             assert np.allclose(grads[which][w], g_ref[which][w], atol=1e-11), (which, w)
 
 
-def test_finite_differences():
-    inp = _inputs(5, B=1, H=1, n=32, n_real=29,
-                  P=Params(ball=16, cmp_block=4, slc_block=8, topk=1, group=4))
+@pytest.mark.parametrize("seed,coarsen", [(2, "mlp"), (3, "mean")])
+def test_group_compression_against_torch_dense_autograd(seed, coarsen):
+    P = Params(ball=16, cmp_block=4, slc_block=8, topk=2, group=4, q_coarsen=coarsen,
+               group_compression=True)
+    inp = _inputs(seed, P=P)
+    fwd, grads = _run_oracle(inp)
+    o_ref, g_ref = _dense_torch(inp, fwd["sel"])
+    assert np.allclose(fwd["o"], o_ref, atol=1e-12)
+    for name in ("dq", "dk", "dv", "dgate"):
+        assert np.allclose(grads[name], g_ref[name], atol=1e-11), name
+    for which in ("dphi_k", "dphi_v", "dphi_q"):
+        for w in ("w1", "b1", "w2", "b2"):
+            ours = grads[which].get(w, np.zeros_like(g_ref[which][w]))
+            assert np.allclose(ours, g_ref[which][w], atol=1e-11), (which, w)
+    if coarsen == "mlp":
+        assert np.abs(g_ref["dphi_q"]["w1"]).max() > 1e-3     # the pin is not vacuous
+
+
+@pytest.mark.parametrize("P", [
+    Params(ball=16, cmp_block=4, slc_block=8, topk=1, group=4),
+    Params(ball=16, cmp_block=4, slc_block=8, topk=1, group=4, q_coarsen="mlp", group_compression=True),
+], ids=["regular", "group_compression_mlp"])
+def test_finite_differences(P):
+    inp = _inputs(5, B=1, H=1, n=32, n_real=29, P=P)
     fwd, grads = _run_oracle(inp)
     sel = fwd["sel"]
     h = 1e-6
@@ -115,7 +152,7 @@ def test_finite_differences():
 
     def loss(mod):
         f = bsa.forward(mod["q"], mod["k"], mod["v"], inp["valid"], mod["gate"], mod["phi_k"],
-                        mod["phi_v"], inp["P"])
+                        mod["phi_v"], inp["P"], phi_q=mod["phi_q"])
         assert np.array_equal(f["sel"], sel)      # the perturbation must not flip top-k
         return float(np.sum(f["o"] * inp["do"]))
 
@@ -138,3 +175,6 @@ def test_finite_differences():
     check(lambda m: m["gate"], grads["dgate"], inp["gate"])
     check(lambda m: m["phi_k"]["w1"], grads["dphi_k"]["w1"], inp["phi_k"]["w1"])
     check(lambda m: m["phi_v"]["b2"], grads["dphi_v"]["b2"], inp["phi_v"]["b2"])
+    if P.group_compression:
+        check(lambda m: m["phi_q"]["w1"], grads["dphi_q"]["w1"], inp["phi_q"]["w1"])
+        check(lambda m: m["phi_q"]["b2"], grads["dphi_q"]["b2"], inp["phi_q"]["b2"])

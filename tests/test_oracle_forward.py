@@ -224,3 +224,91 @@ def test_gate_saturation_isolates_branches(rng):
     # dummy query rows are zero in every branch
     for b in range(q.shape[0]):
         assert not out["o"][b][:, ~valid[b]].any()
+
+
+# ---- query coarsening (Eq. 13-14) and group compression (Eq. 15) ----
+
+def _isolate_cmp(gate):
+    g = np.full_like(gate, -40.0)
+    g[..., 1] = 40.0
+    return g
+
+
+def test_group_compression_l1_is_full_attention(rng):
+    # l = g = 1 with mean pooling: every query is its own coarse query and every key its
+    # own compressed token, so Eq. 15 is plain attention
+    B, H, n, d = 1, 2, 32, 8
+    P = Params(ball=16, cmp_block=1, slc_block=4, topk=2, group=1, kv_pool="mean",
+               group_compression=True)
+    q, k, v = rnd(rng, B, H, n, d), rnd(rng, B, H, n, d), rnd(rng, B, H, n, d)
+    out = bsa.forward(q, k, v, np.ones((B, n), bool), _isolate_cmp(rnd(rng, B, n, 3)), None, None, P)
+    for h in range(H):
+        assert np.allclose(out["o"][0, h], sdpa(q[0, h], k[0, h], v[0, h]), atol=1e-12)
+
+
+def test_group_compression_block_constant_queries_equal_regular(rng):
+    # queries equal within each block of l: the block mean is each of them, so Eq. 15
+    # gives what the per-token compression branch gives
+    B, H, n, d, l = 1, 2, 64, 8, 4
+    base = dict(ball=16, cmp_block=l, slc_block=8, topk=2, group=l)
+    q = np.repeat(rnd(rng, B, H, n // l, d), l, axis=2)
+    k, v = rnd(rng, B, H, n, d), rnd(rng, B, H, n, d)
+    phi = lambda: {"w1": rnd(rng, l * d, d) * 0.2, "b1": rnd(rng, d) * 0.2, "w2": rnd(rng, d, d) * 0.2,
+                   "b2": rnd(rng, d) * 0.2}
+    pk, pv = phi(), phi()
+    valid = np.ones((B, n), bool)
+    gate = rnd(rng, B, n, 3)
+    reg = bsa.forward(q, k, v, valid, gate, pk, pv, Params(**base))
+    grp = bsa.forward(q, k, v, valid, gate, pk, pv, Params(**base, group_compression=True))
+    assert np.allclose(grp["o_branch"][1], reg["o_branch"][1], atol=1e-12)
+    assert np.allclose(grp["lse"][1], reg["lse"][1], atol=1e-12)
+    assert np.array_equal(grp["sel"], reg["sel"])
+
+
+def test_group_compression_copies_to_real_rows(rng):
+    B, H, n, d, l = 1, 1, 64, 8, 4
+    P = Params(ball=16, cmp_block=l, slc_block=8, topk=2, group=l, group_compression=True)
+    q, k, v = rnd(rng, B, H, n, d), rnd(rng, B, H, n, d), rnd(rng, B, H, n, d)
+    valid = rng.random((B, n)) > 0.3
+    valid[0, 8:12] = False                                   # one block with no real token
+    phi = lambda: {"w1": rnd(rng, l * d, d) * 0.2, "b1": rnd(rng, d) * 0.2, "w2": rnd(rng, d, d) * 0.2,
+                   "b2": rnd(rng, d) * 0.2}
+    out = bsa.forward(q, k, v, valid, rnd(rng, B, n, 3), phi(), phi(), P)
+    o1, lse1 = out["o_branch"][1, 0, 0], out["lse"][1, 0, 0]
+    for c in range(n // l):
+        rows = [t for t in range(c * l, (c + 1) * l) if valid[0, t]]
+        for t in rows:
+            assert np.array_equal(o1[t], o1[rows[0]]) and lse1[t] == lse1[rows[0]]
+    assert not o1[~valid[0]].any() and np.all(np.isneginf(lse1[~valid[0]]))
+    # V = 1: every real row of a block with a real key outputs exactly 1 (rows sum to one)
+    vc_one = bsa.group_compression_branch(out["qc"][0, 0], out["kc"][0, 0], np.ones((n // l, d)),
+                                          bsa.block_valid(valid[0], l), valid[0], P)[0]
+    assert np.allclose(vc_one[valid[0]], 1.0, atol=1e-14)
+
+
+def test_mlp_coarsening_with_a_mean_mlp_equals_mean_coarsening(rng):
+    # phi_q whose first layer averages the block and shifts it by +1000 (where exact-erf
+    # GELU is the identity in float64), second layer identity with bias -1000: the MLP
+    # form of Eq. 13 then computes the mean form, so outputs and selections agree
+    B, H, n, d, l = 1, 2, 64, 8, 4
+    base = dict(ball=16, cmp_block=l, slc_block=8, topk=2, group=l, group_compression=True)
+    q, k, v = rnd(rng, B, H, n, d), rnd(rng, B, H, n, d), rnd(rng, B, H, n, d)
+    valid = rng.random((B, n)) > 0.2
+    phi = lambda: {"w1": rnd(rng, l * d, d) * 0.2, "b1": rnd(rng, d) * 0.2, "w2": rnd(rng, d, d) * 0.2,
+                   "b2": rnd(rng, d) * 0.2}
+    pk, pv = phi(), phi()
+    pq = {"w1": np.tile(np.eye(d), (l, 1)) / l, "b1": np.full(d, 1000.0), "w2": np.eye(d),
+          "b2": np.full(d, -1000.0)}
+    gate = rnd(rng, B, n, 3)
+    mean = bsa.forward(q, k, v, valid, gate, pk, pv, Params(**base))
+    mlp = bsa.forward(q, k, v, valid, gate, pk, pv, Params(**base, q_coarsen="mlp"), phi_q=pq)
+    assert np.allclose(mlp["qc"], mean["qc"], atol=1e-12)
+    assert np.array_equal(mlp["sel"], mean["sel"])
+    assert np.allclose(mlp["o"], mean["o"], atol=1e-11)
+
+
+def test_block_coarsening_needs_group_equal_block():
+    with pytest.raises(ValueError):
+        Params(ball=16, cmp_block=4, slc_block=8, topk=2, group=8, group_compression=True)
+    with pytest.raises(ValueError):
+        Params(ball=16, cmp_block=4, slc_block=8, topk=2, group=8, q_coarsen="mlp")
