@@ -49,6 +49,9 @@ typedef enum {
 
 typedef enum { BSA_F32 = 0, BSA_BF16 = 1 } bsa_dtype_t;
 typedef enum { BSA_POOL_MLP = 0, BSA_POOL_MEAN = 1 } bsa_pool_t;
+/* Coarse queries of the selection scores: the group mean of Eq. 11, or an MLP phi_q of
+ * each block of l queries (Eq. 13). */
+typedef enum { BSA_QC_MEAN = 0, BSA_QC_MLP = 1 } bsa_qcoarsen_t;
 
 /* Layer hyper-parameters (notation of Section 2). */
 typedef struct {
@@ -69,10 +72,16 @@ typedef struct {
   int32_t kv_pool;        /* bsa_pool_t: MLP (default) or mean pooling of Eq. 5        */
   int32_t dtype;          /* bsa_dtype_t of Q, K, V, O, dO and the saved branch outputs */
   float softmax_scale;    /* 0 -> 1/sqrt(d)                                            */
+  int32_t q_coarsen;      /* bsa_qcoarsen_t: BSA_QC_MEAN (default) or BSA_QC_MLP (Eq. 13-14;
+                             needs group_size == cmp_block)                            */
+  int32_t group_compression; /* 1: the compression branch attends from the coarse queries
+                             and copies each result to the real queries of its block
+                             (Eq. 15; needs group_size == cmp_block and n/cmp_block >= 64) */
 } bsa_params_t;
 
-/* One compression MLP phi (Eq. 5): y = GELU_erf(x W1 + b1) W2 + b2 for the token-major
- * flatten x of an l x d block (dummy rows zero). Float32, shared across heads:
+/* One compression MLP phi (Eq. 5; also phi_q of Eq. 13): y = GELU_erf(x W1 + b1) W2 + b2
+ * for the token-major flatten x of an l x d block (dummy rows zero). Float32, shared
+ * across heads:
  * w1 [l*d, d], b1 [d], w2 [d, d], b2 [d], row-major. For bf16 layers w1 should hold
  * bf16-representable values: the first layer runs on bf16 matrix cores. */
 typedef struct { const float *w1, *b1, *w2, *b2; } bsa_mlp_t;
@@ -89,6 +98,9 @@ typedef struct {
   float* hid_k;      /* [B, H, N/l, d] hidden pre-activation of phi_k                   */
   float* hid_v;      /* [B, H, N/l, d] hidden pre-activation of phi_v                   */
   uint8_t* cvalid;   /* [B, N/l] 1 if the compression block holds a real token          */
+  float* qcmp;       /* [B, H, N/g, d] coarse queries of the selection (Eq. 11 or 13)   */
+  float* hid_q;      /* [B, H, N/l, d] hidden pre-activation of phi_q (BSA_QC_MLP)      */
+  float* ocmp;       /* [B, H, N/l, d] coarse attention outputs of group compression    */
 } bsa_saved_t;
 
 /* ---- Ball tree (Section 2.1 "Ball Tree Attention"; the ordering every branch uses) ---- */
@@ -139,26 +151,29 @@ bsa_status_t bsa_saved_view(const bsa_params_t* p, void* base, bsa_saved_t* out)
  *   q, k, v: [B, H, N, d] dtype in ball order. valid: [B, N] uint8 (1 = real token) or
  *   NULL (all real). gate: [B, N, 3] float32 logits gamma_b in branch order (ball,
  *   compression, selection), shared across heads (Eq. 9). phi_k / phi_v: compression
- *   MLPs for keys / values (ignored for BSA_POOL_MEAN).
+ *   MLPs for keys / values (ignored for BSA_POOL_MEAN). phi_q: the query-coarsening MLP
+ *   (read only for BSA_QC_MLP; may be NULL otherwise).
  *   o: [B, H, N, d] dtype output = sum_b sigmoid(gamma_b) * o_b; rows of padding slots 0.
  *   saved: filled for bsa_backward (and readable as per-branch outputs, LSE and the
  *   selected block ids). ws: at least ws_fwd_bytes. */
 bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, const void* v,
                          const uint8_t* valid, const float* gate, const bsa_mlp_t* phi_k,
-                         const bsa_mlp_t* phi_v, void* o, const bsa_saved_t* saved,
-                         void* ws, size_t ws_bytes, void* stream);
+                         const bsa_mlp_t* phi_v, const bsa_mlp_t* phi_q, void* o,
+                         const bsa_saved_t* saved, void* ws, size_t ws_bytes, void* stream);
 
 /* Backward pass of bsa_forward given dO = d(loss)/d(o) ([B, H, N, d] dtype).
  * Outputs (overwritten, float32): dq, dk, dv [B, H, N, d]; dgate [B, N, 3];
  * dphi_k / dphi_v weight gradients summed over batch, heads and blocks (may be NULL for
- * BSA_POOL_MEAN). No gradient flows through the top-k selection. Rows of padding slots
+ * BSA_POOL_MEAN). dphi_q: gradient of phi_q, which receives one only through group
+ * compression (required for BSA_QC_MLP with group_compression = 1, else may be NULL and
+ * is not written). No gradient flows through the top-k selection. Rows of padding slots
  * get zero gradients. ws: at least ws_bwd_bytes. */
 bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, const void* v,
                           const uint8_t* valid, const float* gate, const bsa_mlp_t* phi_k,
-                          const bsa_mlp_t* phi_v, const bsa_saved_t* saved, const void* d_o,
-                          float* dq, float* dk, float* dv, float* dgate,
+                          const bsa_mlp_t* phi_v, const bsa_mlp_t* phi_q, const bsa_saved_t* saved,
+                          const void* d_o, float* dq, float* dk, float* dv, float* dgate,
                           const bsa_mlp_grad_t* dphi_k, const bsa_mlp_grad_t* dphi_v,
-                          void* ws, size_t ws_bytes, void* stream);
+                          const bsa_mlp_grad_t* dphi_q, void* ws, size_t ws_bytes, void* stream);
 
 /* ---- Measurement support (not part of the layer's computation) ---- */
 

@@ -13,6 +13,7 @@ LIB_PATH = os.path.join(HERE, "libbsa.so")
 BSA_OK, BSA_ERR_INVALID_ARGUMENT, BSA_ERR_UNSUPPORTED, BSA_ERR_WORKSPACE_TOO_SMALL, BSA_ERR_HIP = range(5)
 BSA_F32, BSA_BF16 = 0, 1
 BSA_POOL_MLP, BSA_POOL_MEAN = 0, 1
+BSA_QC_MEAN, BSA_QC_MLP = 0, 1
 
 
 class bsa_params_t(C.Structure):
@@ -22,6 +23,7 @@ class bsa_params_t(C.Structure):
         ("slc_block", C.c_int32), ("topk", C.c_int32), ("group_size", C.c_int32),
         ("mask_own_ball", C.c_int32), ("store_lse", C.c_int32), ("deterministic", C.c_int32),
         ("kv_pool", C.c_int32), ("dtype", C.c_int32), ("softmax_scale", C.c_float),
+        ("q_coarsen", C.c_int32), ("group_compression", C.c_int32),
     ]
 
 
@@ -36,7 +38,7 @@ class bsa_saved_t(C.Structure):
     _fields_ = [
         ("sel_idx", C.c_void_p), ("lse", C.c_void_p), ("o_branch", C.c_void_p),
         ("kcmp", C.c_void_p), ("vcmp", C.c_void_p), ("hid_k", C.c_void_p), ("hid_v", C.c_void_p),
-        ("cvalid", C.c_void_p),
+        ("cvalid", C.c_void_p), ("qcmp", C.c_void_p), ("hid_q", C.c_void_p), ("ocmp", C.c_void_p),
     ]
 
 
@@ -56,12 +58,13 @@ _SIGS = {
                             C.POINTER(C.c_size_t)]),
     "bsa_saved_view": (C.c_int, [C.POINTER(bsa_params_t), C.c_void_p, C.POINTER(bsa_saved_t)]),
     "bsa_forward": (C.c_int, [C.POINTER(bsa_params_t), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
-                              C.POINTER(bsa_mlp_t), C.POINTER(bsa_mlp_t), C.c_void_p, C.POINTER(bsa_saved_t),
-                              C.c_void_p, C.c_size_t, C.c_void_p]),
+                              C.POINTER(bsa_mlp_t), C.POINTER(bsa_mlp_t), C.POINTER(bsa_mlp_t), C.c_void_p,
+                              C.POINTER(bsa_saved_t), C.c_void_p, C.c_size_t, C.c_void_p]),
     "bsa_backward": (C.c_int, [C.POINTER(bsa_params_t), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
-                               C.POINTER(bsa_mlp_t), C.POINTER(bsa_mlp_t), C.POINTER(bsa_saved_t), C.c_void_p,
-                               C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(bsa_mlp_grad_t),
-                               C.POINTER(bsa_mlp_grad_t), C.c_void_p, C.c_size_t, C.c_void_p]),
+                               C.POINTER(bsa_mlp_t), C.POINTER(bsa_mlp_t), C.POINTER(bsa_mlp_t),
+                               C.POINTER(bsa_saved_t), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                               C.POINTER(bsa_mlp_grad_t), C.POINTER(bsa_mlp_grad_t), C.POINTER(bsa_mlp_grad_t),
+                               C.c_void_p, C.c_size_t, C.c_void_p]),
 }
 
 _lib = None

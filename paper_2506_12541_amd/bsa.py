@@ -12,10 +12,10 @@ import math
 import torch
 
 from . import _lib
-from ._lib import BSA_BF16, BSA_F32, BSA_POOL_MEAN, BSA_POOL_MLP, check
+from ._lib import BSA_BF16, BSA_F32, BSA_POOL_MEAN, BSA_POOL_MLP, BSA_QC_MEAN, BSA_QC_MLP, check
 
 __all__ = ["Params", "Saved", "build_ball_tree", "permute", "unpermute", "sizes", "forward", "backward",
-           "BSA_F32", "BSA_BF16", "BSA_POOL_MLP", "BSA_POOL_MEAN"]
+           "BSA_F32", "BSA_BF16", "BSA_POOL_MLP", "BSA_POOL_MEAN", "BSA_QC_MEAN", "BSA_QC_MLP"]
 
 
 @dataclasses.dataclass
@@ -36,13 +36,15 @@ class Params:
     kv_pool: int = BSA_POOL_MLP
     dtype: int = BSA_BF16
     softmax_scale: float = 0.0
+    q_coarsen: int = BSA_QC_MEAN
+    group_compression: int = 0
 
     def c(self) -> _lib.bsa_params_t:
         return _lib.bsa_params_t(
             self.batch, self.n, self.heads, self.head_dim, self.ball_size, self.cmp_block,
             self.cmp_block if self.cmp_stride is None else self.cmp_stride, self.slc_block, self.topk,
             self.group_size, self.mask_own_ball, self.store_lse, self.deterministic, self.kv_pool,
-            self.dtype, self.softmax_scale)
+            self.dtype, self.softmax_scale, self.q_coarsen, self.group_compression)
 
     @property
     def torch_dtype(self) -> torch.dtype:
@@ -163,6 +165,9 @@ class Saved:
         self.hid_k = view(self.c.hid_k, torch.float32, (B, H, N // p.cmp_block, d))
         self.hid_v = view(self.c.hid_v, torch.float32, (B, H, N // p.cmp_block, d))
         self.cvalid = view(self.c.cvalid, torch.uint8, (B, N // p.cmp_block))
+        self.qcmp = view(self.c.qcmp, torch.float32, (B, H, N // p.group_size, d))
+        self.hid_q = view(self.c.hid_q, torch.float32, (B, H, N // p.cmp_block, d)) if self.c.hid_q else None
+        self.ocmp = view(self.c.ocmp, torch.float32, (B, H, N // p.cmp_block, d)) if self.c.ocmp else None
 
 
 def _mlp(phi):
@@ -173,8 +178,8 @@ def _mlp(phi):
     return _lib.bsa_mlp_t(phi["w1"].data_ptr(), phi["b1"].data_ptr(), phi["w2"].data_ptr(), phi["b2"].data_ptr())
 
 
-def forward(p: Params, q, k, v, valid, gate, phi_k, phi_v, saved: Saved | None = None, stream=None):
-    """Layer forward. Returns (o, saved)."""
+def forward(p: Params, q, k, v, valid, gate, phi_k, phi_v, saved: Saved | None = None, stream=None, phi_q=None):
+    """Layer forward. Returns (o, saved). phi_q: the query-coarsening MLP (BSA_QC_MLP)."""
     lib = _lib.load()
     shape = (p.batch, p.heads, p.n, p.head_dim)
     for name, t in (("q", q), ("k", k), ("v", v)):
@@ -186,16 +191,17 @@ def forward(p: Params, q, k, v, valid, gate, phi_k, phi_v, saved: Saved | None =
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
     saved = saved or Saved(p, q.device)
     o = torch.empty(shape, dtype=p.torch_dtype, device=q.device)
-    mk, mv = _mlp(phi_k), _mlp(phi_v)
+    mk, mv, mq = _mlp(phi_k), _mlp(phi_v), _mlp(phi_q)
     cp = p.c()
     check(lib.bsa_forward(C.byref(cp), _ptr(q), _ptr(k), _ptr(v), _ptr(valid), _ptr(gate),
-                          C.byref(mk) if mk else None, C.byref(mv) if mv else None, _ptr(o), C.byref(saved.c),
-                          _ptr(ws), ws_bytes, _stream(stream)), "bsa_forward")
+                          C.byref(mk) if mk else None, C.byref(mv) if mv else None, C.byref(mq) if mq else None,
+                          _ptr(o), C.byref(saved.c), _ptr(ws), ws_bytes, _stream(stream)), "bsa_forward")
     return o, saved
 
 
-def backward(p: Params, q, k, v, valid, gate, phi_k, phi_v, saved: Saved, d_o, stream=None):
-    """Layer backward. Returns dict(dq, dk, dv, dgate, dphi_k, dphi_v) (float32)."""
+def backward(p: Params, q, k, v, valid, gate, phi_k, phi_v, saved: Saved, d_o, stream=None, phi_q=None):
+    """Layer backward. Returns dict(dq, dk, dv, dgate, dphi_k, dphi_v, dphi_q) (float32); dphi_q is
+    filled only with group compression and MLP query coarsening."""
     lib = _lib.load()
     shape = (p.batch, p.heads, p.n, p.head_dim)
     for name, t in (("q", q), ("k", k), ("v", v), ("d_o", d_o)):
@@ -210,20 +216,23 @@ def backward(p: Params, q, k, v, valid, gate, phi_k, phi_v, saved: Saved, d_o, s
     dgate = torch.empty((p.batch, p.n, 3), dtype=torch.float32, device=dev)
     grads = {}
     cgr = []
-    for name, phi in (("dphi_k", phi_k), ("dphi_v", phi_v)):
-        if p.kv_pool == BSA_POOL_MLP:
+    q_grad = p.group_compression and p.q_coarsen == BSA_QC_MLP
+    for name, phi, on in (("dphi_k", phi_k, p.kv_pool == BSA_POOL_MLP), ("dphi_v", phi_v, p.kv_pool == BSA_POOL_MLP),
+                          ("dphi_q", phi_q, q_grad)):
+        if on:
             g = {w: torch.empty_like(phi[w]) for w in ("w1", "b1", "w2", "b2")}
             grads[name] = g
             cgr.append(_lib.bsa_mlp_t(g["w1"].data_ptr(), g["b1"].data_ptr(), g["w2"].data_ptr(), g["b2"].data_ptr()))
         else:
             grads[name] = {}
             cgr.append(None)
-    mk, mv = _mlp(phi_k), _mlp(phi_v)
+    mk, mv, mq = _mlp(phi_k), _mlp(phi_v), _mlp(phi_q)
     cp = p.c()
     check(lib.bsa_backward(C.byref(cp), _ptr(q), _ptr(k), _ptr(v), _ptr(valid), _ptr(gate),
-                           C.byref(mk) if mk else None, C.byref(mv) if mv else None, C.byref(saved.c), _ptr(d_o),
-                           _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dgate),
+                           C.byref(mk) if mk else None, C.byref(mv) if mv else None, C.byref(mq) if mq else None,
+                           C.byref(saved.c), _ptr(d_o), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dgate),
                            C.byref(cgr[0]) if cgr[0] else None, C.byref(cgr[1]) if cgr[1] else None,
-                           _ptr(ws), ws_bytes, _stream(stream)), "bsa_backward")
+                           C.byref(cgr[2]) if cgr[2] else None, _ptr(ws), ws_bytes, _stream(stream)),
+          "bsa_backward")
     grads.update(dq=dq, dk=dk, dv=dv, dgate=dgate)
     return grads

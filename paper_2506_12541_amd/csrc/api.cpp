@@ -70,6 +70,16 @@ bsa_status_t check_params(const bsa_params_t* p, bsa::Dims* D) {
     return fail(BSA_ERR_UNSUPPORTED, "float32 layers support head_dim 32 (bf16 layers: 32 and 64)");
   if (!(p->softmax_scale >= 0.0f) || std::isinf(p->softmax_scale))
     return fail(BSA_ERR_INVALID_ARGUMENT, "softmax_scale must be finite and >= 0");
+  if (p->q_coarsen != BSA_QC_MEAN && p->q_coarsen != BSA_QC_MLP) return fail(BSA_ERR_INVALID_ARGUMENT, "bad q_coarsen");
+  if (p->group_compression != 0 && p->group_compression != 1)
+    return fail(BSA_ERR_INVALID_ARGUMENT, "group_compression must be 0/1");
+  if ((p->q_coarsen == BSA_QC_MLP || p->group_compression) && p->group_size != p->cmp_block)
+    return fail(BSA_ERR_INVALID_ARGUMENT,
+                "block query coarsening (Eq. 13) and group compression (Eq. 15) need group_size == cmp_block");
+  if (p->q_coarsen == BSA_QC_MLP && (p->cmp_block * p->head_dim) % 64 != 0)
+    return fail(BSA_ERR_UNSUPPORTED, "MLP query coarsening needs cmp_block * head_dim to be a multiple of 64");
+  if (p->group_compression && p->n / p->cmp_block < 64)
+    return fail(BSA_ERR_UNSUPPORTED, "group compression needs n / cmp_block >= 64");
   D->B = p->batch;
   D->H = p->heads;
   D->N = p->n;
@@ -82,6 +92,8 @@ bsa_status_t check_params(const bsa_params_t* p, bsa::Dims* D) {
   D->mask_own = p->mask_own_ball;
   D->pool = p->kv_pool;
   D->bf16 = p->dtype == BSA_BF16;
+  D->qc_mlp = p->q_coarsen == BSA_QC_MLP;
+  D->gcmp = p->group_compression;
   D->scale = p->softmax_scale > 0.f ? p->softmax_scale : 1.0f / std::sqrt((float)p->head_dim);
   return BSA_OK;
 }
@@ -89,7 +101,7 @@ bsa_status_t check_params(const bsa_params_t* p, bsa::Dims* D) {
 size_t elem_bytes(const bsa::Dims& D) { return D.bf16 ? 2 : 4; }
 
 struct SavedLayout {
-  size_t sel, lse, ob, kc, vc, hk, hv, cv, total;
+  size_t sel, lse, ob, kc, vc, hk, hv, cv, qc, hq, oc, total;
 };
 
 SavedLayout saved_layout(const bsa::Dims& D) {
@@ -106,12 +118,15 @@ SavedLayout saved_layout(const bsa::Dims& D) {
   L.hk = put(sizeof(float) * crows * D.d);
   L.hv = put(sizeof(float) * crows * D.d);
   L.cv = put((size_t)D.B * (D.N / D.l));
+  L.qc = put(sizeof(float) * (size_t)D.B * D.H * (D.N / D.g) * D.d);
+  L.hq = put(D.qc_mlp ? sizeof(float) * crows * D.d : 0);
+  L.oc = put(D.gcmp ? sizeof(float) * crows * D.d : 0);
   L.total = off;
   return L;
 }
 
 struct FwdWs {
-  size_t w1t_k, w1t_v, kc_lp, vc_lp, qpool, total;
+  size_t w1t_k, w1t_v, w1t_q, kc_lp, vc_lp, qc_lp, lsec, total;
 };
 
 FwdWs fwd_ws_layout(const bsa::Dims& D) {
@@ -123,12 +138,15 @@ FwdWs fwd_ws_layout(const bsa::Dims& D) {
   W.w1t_v = put(w1);
   W.kc_lp = put(elem_bytes(D) * (size_t)D.cmp_rows() * D.d);
   W.vc_lp = put(elem_bytes(D) * (size_t)D.cmp_rows() * D.d);
-  W.qpool = put(sizeof(float) * (size_t)D.B * D.H * (D.N / D.g) * D.d);
+  W.w1t_q = put(D.qc_mlp ? w1 : 0);
+  W.qc_lp = put(D.block_coarse() ? elem_bytes(D) * (size_t)D.cmp_rows() * D.d : 0);
+  W.lsec = put(D.gcmp ? sizeof(float) * (size_t)D.cmp_rows() : 0);
   W.total = off;
   return W;
 }
 
 struct BwdWs {
+  size_t qc_lp, doc, t4c, dqc;
   size_t R, terms, dplp, kc_lp, vc_lp, dkc_part, dvc_part, dkc, dvc, pk, pv, pkt, pvt, hist, seg_s, seg_e, dpre, pw1, psm, w1lp,
       total;
   int cmp_chunks, mlp_chunks, mlp_chunks_small;
@@ -166,6 +184,10 @@ BwdWs bwd_ws_layout(const bsa::Dims& D) {
   W.psm = put(sizeof(float) * (size_t)W.mlp_chunks_small * ((size_t)D.d * D.d + 2 * D.d));
   W.w1lp = put(elem_bytes(D) * (size_t)D.l * D.d * D.d);
   W.dplp = put(elem_bytes(D) * crows * D.d);
+  W.qc_lp = put(D.gcmp ? elem_bytes(D) * crows * D.d : 0);
+  W.doc = put(D.gcmp ? elem_bytes(D) * crows * D.d : 0);
+  W.t4c = put(D.gcmp ? 4 * sizeof(float) * crows : 0);
+  W.dqc = put(D.gcmp ? sizeof(float) * crows * D.d : 0);
   W.total = off;
   return W;
 }
@@ -287,6 +309,9 @@ bsa_status_t bsa_saved_view(const bsa_params_t* p, void* base, bsa_saved_t* out)
   out->hid_k = (float*)(c + L.hk);
   out->hid_v = (float*)(c + L.hv);
   out->cvalid = (uint8_t*)(c + L.cv);
+  out->qcmp = (float*)(c + L.qc);
+  out->hid_q = D.qc_mlp ? (float*)(c + L.hq) : nullptr;
+  out->ocmp = D.gcmp ? (float*)(c + L.oc) : nullptr;
   return BSA_OK;
 }
 
@@ -323,24 +348,26 @@ static bsa_status_t join_aux(const Aux& a, hipStream_t st) {
   return BSA_OK;
 }
 
-static bool saved_ok(const bsa_saved_t* sv) {
-  return sv && sv->sel_idx && sv->lse && sv->o_branch && sv->kcmp && sv->vcmp && sv->hid_k && sv->hid_v && sv->cvalid;
+static bool saved_ok(const bsa_saved_t* sv, const bsa::Dims& D) {
+  return sv && sv->sel_idx && sv->lse && sv->o_branch && sv->kcmp && sv->vcmp && sv->hid_k && sv->hid_v &&
+         sv->cvalid && sv->qcmp && (!D.qc_mlp || sv->hid_q) && (!D.gcmp || sv->ocmp);
 }
 
+static bool mlp_ok(const bsa_mlp_t* m) { return m && m->w1 && m->b1 && m->w2 && m->b2; }
+
 bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, const void* v, const uint8_t* valid,
-                         const float* gate, const bsa_mlp_t* phi_k, const bsa_mlp_t* phi_v, void* o,
-                         const bsa_saved_t* saved, void* ws, size_t ws_bytes, void* stream) {
+                         const float* gate, const bsa_mlp_t* phi_k, const bsa_mlp_t* phi_v, const bsa_mlp_t* phi_q,
+                         void* o, const bsa_saved_t* saved, void* ws, size_t ws_bytes, void* stream) {
   g_last_error.clear();
   bsa::Dims D;
   bsa_status_t s = check_params(p, &D);
   if (s != BSA_OK) return s;
   if (!q || !k || !v || !gate || !o) return fail(BSA_ERR_INVALID_ARGUMENT, "q, k, v, gate and o must be non-NULL");
-  if (!saved_ok(saved)) return fail(BSA_ERR_INVALID_ARGUMENT, "every saved buffer must be non-NULL");
-  if (D.pool == 0) {
-    if (!phi_k || !phi_v || !phi_k->w1 || !phi_k->b1 || !phi_k->w2 || !phi_k->b2 || !phi_v->w1 || !phi_v->b1 ||
-        !phi_v->w2 || !phi_v->b2)
-      return fail(BSA_ERR_INVALID_ARGUMENT, "MLP pooling needs phi_k and phi_v with all four tensors");
-  }
+  if (!saved_ok(saved, D)) return fail(BSA_ERR_INVALID_ARGUMENT, "every saved buffer must be non-NULL");
+  if (D.pool == 0 && (!mlp_ok(phi_k) || !mlp_ok(phi_v)))
+    return fail(BSA_ERR_INVALID_ARGUMENT, "MLP pooling needs phi_k and phi_v with all four tensors");
+  if (D.qc_mlp && !mlp_ok(phi_q))
+    return fail(BSA_ERR_INVALID_ARGUMENT, "MLP query coarsening needs phi_q with all four tensors");
   const FwdWs W = fwd_ws_layout(D);
   if (!ws || ws_bytes < W.total)
     return fail(BSA_ERR_WORKSPACE_TOO_SMALL, "forward workspace needs " + std::to_string(W.total) + " bytes");
@@ -353,13 +380,17 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   const size_t rows = (size_t)D.rows();
   char* ob = (char*)saved->o_branch;
   const size_t ob_stride = rows * D.d * elem_bytes(D);
-  bsa::Mlp mk{}, mv{};
+  bsa::Mlp mk{}, mv{}, mq{};
   if (D.pool == 0) {
     mk = {phi_k->w1, phi_k->b1, phi_k->w2, phi_k->b2};
     mv = {phi_v->w1, phi_v->b1, phi_v->w2, phi_v->b2};
   }
+  if (D.qc_mlp) mq = {phi_q->w1, phi_q->b1, phi_q->w2, phi_q->b2};
+  bsa::Dims Dq = D;   // coarse queries of Eq. 13: phi_q (MLP) or the block mean
+  Dq.pool = D.qc_mlp ? 0 : 1;
   void* kc_lp = w + W.kc_lp;
   void* vc_lp = w + W.vc_lp;
+  void* qc_lp = w + W.qc_lp;
   hipError_t e = hipSuccess;
 #define BSA_STEP(name, call, what)        \
   BSA_PHASE(name, st, e = (call));         \
@@ -372,6 +403,9 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
                                       : bsa::launch_compress_fwd(D, v, valid, mv, saved->vcmp, saved->hid_v, vc_lp,
                                                                  w + W.w1t_v, st)),
            "compression");
+  if (D.block_coarse())
+    BSA_STEP("fwd.compress", bsa::launch_compress_fwd(Dq, q, valid, mq, saved->qcmp, saved->hid_q, qc_lp, w + W.w1t_q, st),
+             "query coarsening");
   // ball and compressed attention on the auxiliary stream, selection on the caller's
   if (hipEventRecord(aux.fork, st) != hipSuccess || hipStreamWaitEvent(aux.s, aux.fork, 0) != hipSuccess)
     return fail(BSA_ERR_HIP, "forking the auxiliary stream failed");
@@ -379,14 +413,25 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
     hipStream_t st_main = st;
     hipStream_t st = aux.s;
     BSA_STEP("fwd.ball", bsa::launch_ball_fwd(D, q, k, v, valid, ob, saved->lse, st), "ball attention");
-    BSA_STEP("fwd.cmp",
-             bsa::launch_cmp_fwd(D, q, kc_lp, vc_lp, valid, valid ? saved->cvalid : nullptr, ob + ob_stride,
-                                 saved->lse + rows, st),
-             "compressed attention");
+    if (D.gcmp) {
+      float* oc = saved->ocmp;
+      float* lsec = (float*)(w + W.lsec);
+      BSA_STEP("fwd.cmp",
+               (bsa::launch_cmp_coarse_fwd(D, qc_lp, kc_lp, vc_lp, valid ? saved->cvalid : nullptr, oc, lsec, st) !=
+                        hipSuccess
+                    ? hipGetLastError()
+                    : bsa::launch_expand_coarse(D, oc, lsec, valid, ob + ob_stride, saved->lse + rows, st)),
+               "group compression");
+    } else {
+      BSA_STEP("fwd.cmp",
+               bsa::launch_cmp_fwd(D, q, kc_lp, vc_lp, valid, valid ? saved->cvalid : nullptr, ob + ob_stride,
+                                   saved->lse + rows, st),
+               "compressed attention");
+    }
     (void)st_main;
   }
   BSA_STEP("fwd.select", bsa::launch_select_topk(D, q, valid, saved->kcmp, saved->cvalid, saved->sel_idx,
-                                                  (float*)(w + W.qpool), st),
+                                                  saved->qcmp, D.block_coarse(), st),
            "select");
   BSA_STEP("fwd.slc",
            bsa::launch_slc_fwd(D, q, k, v, valid, saved->sel_idx, ob + 2 * ob_stride, saved->lse + 2 * rows, st),
@@ -399,23 +444,23 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
 }
 
 bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, const void* v, const uint8_t* valid,
-                          const float* gate, const bsa_mlp_t* phi_k, const bsa_mlp_t* phi_v, const bsa_saved_t* saved,
-                          const void* d_o, float* dq, float* dk, float* dv, float* dgate,
-                          const bsa_mlp_grad_t* dphi_k, const bsa_mlp_grad_t* dphi_v, void* ws, size_t ws_bytes,
-                          void* stream) {
+                          const float* gate, const bsa_mlp_t* phi_k, const bsa_mlp_t* phi_v, const bsa_mlp_t* phi_q,
+                          const bsa_saved_t* saved, const void* d_o, float* dq, float* dk, float* dv, float* dgate,
+                          const bsa_mlp_grad_t* dphi_k, const bsa_mlp_grad_t* dphi_v, const bsa_mlp_grad_t* dphi_q,
+                          void* ws, size_t ws_bytes, void* stream) {
   g_last_error.clear();
   bsa::Dims D;
   bsa_status_t s = check_params(p, &D);
   if (s != BSA_OK) return s;
   if (!q || !k || !v || !gate || !d_o || !dq || !dk || !dv || !dgate)
     return fail(BSA_ERR_INVALID_ARGUMENT, "q, k, v, gate, d_o, dq, dk, dv and dgate must be non-NULL");
-  if (!saved_ok(saved)) return fail(BSA_ERR_INVALID_ARGUMENT, "every saved buffer must be non-NULL");
-  if (D.pool == 0) {
-    auto full = [](const bsa_mlp_t* m) { return m && m->w1 && m->b1 && m->w2 && m->b2; };
-    auto fullg = [](const bsa_mlp_grad_t* m) { return m && m->w1 && m->b1 && m->w2 && m->b2; };
-    if (!full(phi_k) || !full(phi_v) || !fullg(dphi_k) || !fullg(dphi_v))
-      return fail(BSA_ERR_INVALID_ARGUMENT, "MLP pooling needs phi_k, phi_v, dphi_k and dphi_v with all four tensors");
-  }
+  if (!saved_ok(saved, D)) return fail(BSA_ERR_INVALID_ARGUMENT, "every saved buffer must be non-NULL");
+  auto fullg = [](const bsa_mlp_grad_t* m) { return m && m->w1 && m->b1 && m->w2 && m->b2; };
+  if (D.pool == 0 && (!mlp_ok(phi_k) || !mlp_ok(phi_v) || !fullg(dphi_k) || !fullg(dphi_v)))
+    return fail(BSA_ERR_INVALID_ARGUMENT, "MLP pooling needs phi_k, phi_v, dphi_k and dphi_v with all four tensors");
+  const bool q_grad = D.gcmp && D.qc_mlp;   // phi_q gets a gradient only through Eq. 15
+  if (q_grad && (!mlp_ok(phi_q) || !fullg(dphi_q)))
+    return fail(BSA_ERR_INVALID_ARGUMENT, "group compression with MLP coarsening needs phi_q and dphi_q");
   const BwdWs W = bwd_ws_layout(D);
   if (!ws || ws_bytes < W.total)
     return fail(BSA_ERR_WORKSPACE_TOO_SMALL, "backward workspace needs " + std::to_string(W.total) + " bytes");
@@ -439,6 +484,8 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   A.pair_keys_tmp = (uint32_t*)(w + W.pkt); A.pair_vals_tmp = (uint32_t*)(w + W.pvt);
   A.sort_hist = (uint32_t*)(w + W.hist);
   A.seg_start = (int*)(w + W.seg_s); A.seg_end = (int*)(w + W.seg_e);
+  A.qcmp = saved->qcmp; A.ocmp = saved->ocmp; A.qc_lp = w + W.qc_lp; A.doc = w + W.doc; A.t4c = (float*)(w + W.t4c);
+  A.dqc = (float*)(w + W.dqc);
   // after the dense dK/dV passes, the dQ passes run on the auxiliary stream while the
   // compression and selection dK/dV passes run on the caller's
   BSA_TRY(bsa::launch_attn_bwd(D, A, st, aux.s, aux.fork), "attention backward");
@@ -458,7 +505,22 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   BSA_PHASE("bwd.mlp", st, e = bsa::launch_compress_bwd(D, v, valid, mv, saved->hid_v, A.dvc, dv, gv, mw, st));
   BSA_TRY(e, "compression backward V");
   BSA_TRY(bsa::launch_slc_csr(D, A, st), "selection backward");
-  return join_aux(aux, st);
+  s = join_aux(aux, st);
+  if (s != BSA_OK) return s;
+  if (D.gcmp) {
+    // coarse-query gradient of Eq. 15 through phi_q (or the block mean) into dQ
+    bsa::Dims Dq = D;
+    Dq.pool = D.qc_mlp ? 0 : 1;
+    bsa::Mlp mq{};
+    bsa::MlpGrad gq{};
+    if (q_grad) {
+      mq = {phi_q->w1, phi_q->b1, phi_q->w2, phi_q->b2};
+      gq = {dphi_q->w1, dphi_q->b1, dphi_q->w2, dphi_q->b2};
+    }
+    BSA_PHASE("bwd.mlp", st, e = bsa::launch_compress_bwd(Dq, q, valid, mq, saved->hid_q, A.dqc, dq, gq, mw, st));
+    BSA_TRY(e, "query coarsening backward");
+  }
+  return BSA_OK;
 }
 
 }  // extern "C"

@@ -83,6 +83,41 @@ __global__ void gate_bwd_kernel(const float* R, const float* gate, const uint8_t
   }
 }
 
+// Group compression (Eq. 15), per coarse query: the copy's adjoint sums s_t dO_t over the
+// real rows t of its block (s_t = sigmoid(gamma_cmp) of row t), kept in the storage type
+// dO_c; its packed terms are (log2 LSE, 1, rowsum(dO_c * o_c), 0), the delta formed from
+// the rounded dO_c the attention passes use and the float32 coarse output o_c, so that it
+// equals their sum_j P_j dP_j to float32 rounding (near-uniform coarse softmaxes make dQ_c
+// small next to either term). The log2 LSE is the one every real row of the block
+// carries (+inf when the block has none). One thread per (coarse row, column); crows * hd
+// is a multiple of 64, so every wave is whole and a row's hd lanes sit in one wave.
+template <typename T>
+__global__ void coarse_rows_bwd_kernel(const T* dout, const float4* t4b, const float* oc, const uint8_t* valid, int H,
+                                       int N, int l, int hd, long long crows, T* doc, float4* t4c) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= crows * hd) return;
+  const long long cr = i / hd;
+  const int col = (int)(i % hd);
+  const int nct = N / l;
+  const long long bh = cr / nct;
+  const int c = (int)(cr % nct);
+  const int b = (int)(bh / H);
+  const long long r0 = bh * N + (long long)c * l;
+  const uint8_t* vb = valid ? valid + (size_t)b * N + (size_t)c * l : nullptr;
+  float acc = 0.f, l2 = __builtin_huge_valf();
+  for (int t = 0; t < l; ++t) {
+    if (vb != nullptr && vb[t] == 0) continue;
+    const float4 tt = t4b[r0 + t];
+    acc += tt.y * to_f32<T>(dout[(r0 + t) * hd + col]);
+    l2 = fminf(l2, tt.x);
+  }
+  const T dr = from_f32<T>(acc);
+  doc[cr * hd + col] = dr;
+  float dd = to_f32<T>(dr) * oc[cr * hd + col];
+  for (int off = hd / 2; off > 0; off >>= 1) dd += __shfl_xor(dd, off, 64);
+  if (col == 0) t4c[cr] = make_float4(l2, 1.f, dd, 0.f);
+}
+
 template <typename T>
 __global__ void cast_kernel(const float* x, long long n, T* y) {
   long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -1211,13 +1246,30 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t
     (launch_bwd_kv<T, HD, 2, true>)(dim3(D.N / 64, 1, D.B * D.H), st, q, k, v, dout, A.valid, qball, D.H, D.N, D.N,
                                   D.m, 1, sl2, D.scale, A.dk, A.dv);
   });
+  // group compression: coarse queries in the storage type, their dO and row terms
+  const T* qcl = nullptr;
+  const T* docl = nullptr;
+  QTerms qcoarse{(const float4*)A.t4c};
+  if (D.gcmp) {
+    const long long n = D.cmp_rows() * HD;
+    if (D.bf16) {
+      hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.qcmp, n, (T*)A.qc_lp);
+      qcl = (const T*)A.qc_lp;
+    } else {
+      qcl = (const T*)A.qcmp;
+    }
+    hipLaunchKernelGGL(coarse_rows_bwd_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, dout,
+                       t4 + rows, A.ocmp, A.valid, D.H, D.N, D.l, HD, D.cmp_rows(), (T*)A.doc, (float4*)A.t4c);
+    docl = (const T*)A.doc;
+  }
   // ---- dK^, dV^ of the compressed branch: chunked partials, then a fixed-order sum ----
   {
-    const int nch = D.N / kCmpChunks >= kQT ? kCmpChunks : 1;
+    const int nq = D.gcmp ? nct : D.N;   // query rows: tokens, or coarse queries (Eq. 15)
+    const int nch = nq / kCmpChunks >= kQT ? kCmpChunks : 1;
     BSA_PHASE("bwd.kv_cmp", st,
-    (launch_bwd_kv<T, HD, 4, false>)(dim3((nct + 127) / 128, nch, D.B * D.H), st, q, kc, vc, dout,
-                                   A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, nch, sl2, D.scale,
-                                   A.dkc_part, A.dvc_part));
+    (launch_bwd_kv<T, HD, 4, false>)(dim3((nct + 127) / 128, nch, D.B * D.H), st, D.gcmp ? qcl : q, kc, vc,
+                                   D.gcmp ? docl : dout, A.valid ? A.cvalid : nullptr, D.gcmp ? qcoarse : qcmp,
+                                   D.H, nq, nct, D.m, nch, sl2, D.scale, A.dkc_part, A.dvc_part));
     const long long n = D.cmp_rows() * HD;
     hipLaunchKernelGGL(sum_chunks_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.dkc_part, nch, n,
                        A.dkc);
@@ -1241,9 +1293,19 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t
     (launch_bwd_q<T, HD, 1, true, false>)(dim3(D.N / 64, D.H, D.B), st, q, k, v, dout, A.valid, qball, D.H, D.N,
                                           D.N, D.m, sl2, D.scale, A.dq);
   });
-  BSA_PHASE("bwd.dq_cmp", st,
-  (launch_bwd_q<T, HD, 2, false, true>)(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, dout,
-                                        A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq));
+  BSA_PHASE("bwd.dq_cmp", st, {
+  if (!D.gcmp)
+    (launch_bwd_q<T, HD, 2, false, true>)(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, dout,
+                                          A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq);
+  else if (nct % 128 == 0)   // gradient of the coarse queries (written); the caller maps it to dQ
+    (launch_bwd_q<T, HD, 2, false, false>)(dim3(nct / 128, D.H, D.B), st, qcl, kc, vc, docl,
+                                           A.valid ? A.cvalid : nullptr, qcoarse, D.H, nct, nct, D.m, sl2, D.scale,
+                                           A.dqc);
+  else
+    (launch_bwd_q<T, HD, 1, false, false>)(dim3(nct / 64, D.H, D.B), st, qcl, kc, vc, docl,
+                                           A.valid ? A.cvalid : nullptr, qcoarse, D.H, nct, nct, D.m, sl2, D.scale,
+                                           A.dqc);
+  });
   BSA_PHASE("bwd.dq_slc", st, {
   if constexpr (sizeof(T) == 2) {
     constexpr int NW = 2;

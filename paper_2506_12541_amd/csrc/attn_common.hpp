@@ -380,7 +380,9 @@ struct WaveAttn {
   }
 
   // Normalise and store O rows (query q0 + 16 qb + r) and natural-log LSE.
-  __device__ void finish(int lane, long long row0, T* out, float* lse, const uint8_t* qvalid, int qidx0) {
+  // out: rows in the storage type, or float32 where a caller needs the unrounded output
+  template <typename OT>
+  __device__ void finish(int lane, long long row0, OT* out, float* lse, const uint8_t* qvalid, int qidx0) {
     const int r = lane & 15, j = lane >> 4;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {

@@ -23,10 +23,10 @@ namespace {
 
 // Keys are staged 128 at a time (one pair of barriers) and consumed as two 64-key
 // halves; the next 128 keys are loaded into registers while the current ones are used.
-template <typename T, int HD, int QB, bool BALL>
+template <typename T, int HD, int QB, bool BALL, typename OT = T>
 __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, const T* v, const uint8_t* qvalid_all,
                                                         const uint8_t* kvalid_all, int H, int N, int nkeys_total,
-                                                        int m, float sl2, T* out, float* lse) {
+                                                        int m, float sl2, OT* out, float* lse) {
   constexpr int kFT = sizeof(T) == 2 ? 128 : 64;  // keys per staged tile (LDS stays < 64 KB)
   constexpr int KSTR = HD + 16 / (int)sizeof(T);  // LDS row stride of K (elements)
   constexpr int VSTR = kFT + 4;                   // LDS row stride of V^T
@@ -91,11 +91,11 @@ __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, 
 // transpose reads of the row-major V tile. The two buffers are distinct LDS objects and
 // the loop is unrolled by two, so the compiler can tell that loads in flight into one
 // buffer do not alias reads of the other and need not be waited for.
-template <int HD, int QB, int NW, bool BALL>
+template <int HD, int QB, int NW, bool BALL, typename OT = bf16_t>
 __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
                                                                 const uint8_t* qvalid_all, const uint8_t* kvalid_all,
                                                                 int H, int N, int nkeys_total, int m, float sl2,
-                                                                bf16_t* out, float* lse) {
+                                                                OT* out, float* lse) {
   constexpr int kFT = kKT;
   __shared__ __attribute__((aligned(16))) bf16_t ks0[kFT * HD], ks1[kFT * HD];
   __shared__ __attribute__((aligned(16))) bf16_t vs0[kFT * HD], vs1[kFT * HD];
@@ -363,15 +363,16 @@ __global__ void gate_fwd_vec_kernel(const T* ob, const float* gate, const uint8_
 
 // bf16 layers take the direct-load kernel (NW waves of QB 16-query blocks per workgroup);
 // f32 layers the register-staged one (4 waves).
-template <typename T, int HD, int QB, bool BALL, int NW = 4>
+// OT: type of the output rows (the storage type, or float32 for unrounded outputs)
+template <typename T, int HD, int QB, bool BALL, int NW = 4, typename OT = T>
 void launch_dense_fwd(dim3 grid, hipStream_t st, const void* q, const void* k, const void* v, const uint8_t* qvalid,
                       const uint8_t* kvalid, int H, int N, int nkeys_total, int m, float sl2, void* o, float* lse) {
   if constexpr (sizeof(T) == 2)
-    hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL>), grid, dim3(64 * NW), 0, st, (const bf16_t*)q,
-                       (const bf16_t*)k, (const bf16_t*)v, qvalid, kvalid, H, N, nkeys_total, m, sl2, (bf16_t*)o, lse);
+    hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT>), grid, dim3(64 * NW), 0, st, (const bf16_t*)q,
+                       (const bf16_t*)k, (const bf16_t*)v, qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
   else
-    hipLaunchKernelGGL((dense_fwd_kernel<T, HD, QB, BALL>), grid, dim3(256), 0, st, (const T*)q, (const T*)k,
-                       (const T*)v, qvalid, kvalid, H, N, nkeys_total, m, sl2, (T*)o, lse);
+    hipLaunchKernelGGL((dense_fwd_kernel<T, HD, QB, BALL, OT>), grid, dim3(256), 0, st, (const T*)q, (const T*)k,
+                       (const T*)v, qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
 }
 
 template <typename T, int HD>
@@ -394,6 +395,54 @@ hipError_t cmp_impl(const Dims& D, const void* q, const void* kc, const void* vc
   launch_dense_fwd<T, HD, 2, false>(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, valid, cvalid, D.H, D.N, D.N / D.l, D.m,
                                     sl2, o, lse);
   return hipGetLastError();
+}
+
+// Group compression (Eq. 15): the coarse queries attend to the compressed tokens; rows are
+// coarse queries [B, H, N/l, d], valid iff their block holds a real token. Outputs stay in
+// float32: the backward forms its softmax delta from them.
+template <typename T, int HD>
+hipError_t cmp_coarse_impl(const Dims& D, const void* qc, const void* kc, const void* vc, const uint8_t* cvalid,
+                           float* oc, float* lsec, hipStream_t st) {
+  const float sl2 = D.scale * kLog2e;
+  const int nct = D.N / D.l;
+  if (nct % 128 == 0)
+    launch_dense_fwd<T, HD, 2, false, 4, float>(dim3(nct / 128, D.H, D.B), st, qc, kc, vc, cvalid, cvalid, D.H, nct,
+                                                nct, D.m, sl2, oc, lsec);
+  else
+    launch_dense_fwd<T, HD, 1, false, 4, float>(dim3(nct / 64, D.H, D.B), st, qc, kc, vc, cvalid, cvalid, D.H, nct,
+                                                nct, D.m, sl2, oc, lsec);
+  return hipGetLastError();
+}
+
+// The copy of Eq. 15: row n of the compression branch takes float32 coarse row n / l (in
+// the storage type) when slot n holds a real token; padding rows get zeros and LSE -inf.
+// One thread per 16 output bytes.
+template <typename T>
+__global__ void expand_coarse_kernel(const float* oc, const float* lsec, const uint8_t* valid, int H, int N, int l,
+                                     int hd, long long rows, T* ob, float* lse) {
+  constexpr int EPV = 16 / (int)sizeof(T);
+  const int per_row = hd / EPV;
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows * per_row) return;
+  const long long row = i / per_row;   // (b * H + h) * N + n
+  const int c = (int)(i % per_row);
+  const long long bh = row / N;
+  const int n = (int)(row % N);
+  const int b = (int)(bh / H);
+  const bool ok = valid == nullptr || valid[(size_t)b * N + n] != 0;
+  const long long crow = bh * (N / l) + n / l;
+  T out[EPV];
+#pragma unroll
+  for (int e = 0; e < EPV; e += 4) {
+    float4 f = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (ok) f = *reinterpret_cast<const float4*>(oc + crow * hd + c * EPV + e);
+    out[e] = from_f32<T>(f.x);
+    out[e + 1] = from_f32<T>(f.y);
+    out[e + 2] = from_f32<T>(f.z);
+    out[e + 3] = from_f32<T>(f.w);
+  }
+  *reinterpret_cast<uint4*>(ob + row * hd + c * EPV) = *reinterpret_cast<const uint4*>(out);
+  if (c == 0) lse[row] = ok ? lsec[crow] : kNegInf;
 }
 
 template <typename T, int HD>
@@ -422,6 +471,25 @@ hipError_t launch_ball_fwd(const Dims& D, const void* q, const void* k, const vo
 hipError_t launch_cmp_fwd(const Dims& D, const void* q, const void* kc, const void* vc, const uint8_t* valid,
                           const uint8_t* cvalid, void* o, float* lse, hipStream_t st) {
   return BSA_DISPATCH(cmp_impl, D, q, kc, vc, valid, cvalid, o, lse, st);
+}
+
+hipError_t launch_cmp_coarse_fwd(const Dims& D, const void* qc, const void* kc, const void* vc, const uint8_t* cvalid,
+                                 float* oc, float* lsec, hipStream_t st) {
+  return BSA_DISPATCH(cmp_coarse_impl, D, qc, kc, vc, cvalid, oc, lsec, st);
+}
+
+hipError_t launch_expand_coarse(const Dims& D, const float* oc, const float* lsec, const uint8_t* valid, void* ob,
+                                float* lse, hipStream_t st) {
+  const long long rows = D.rows();
+  const long long per = rows * (D.d * (D.bf16 ? 2 : 4) / 16);
+  const unsigned grid = (unsigned)((per + 255) / 256);
+  if (D.bf16)
+    hipLaunchKernelGGL(expand_coarse_kernel<bf16_t>, dim3(grid), dim3(256), 0, st, oc, lsec, valid,
+                       D.H, D.N, D.l, D.d, rows, (bf16_t*)ob, lse);
+  else
+    hipLaunchKernelGGL(expand_coarse_kernel<float>, dim3(grid), dim3(256), 0, st, oc, lsec, valid,
+                       D.H, D.N, D.l, D.d, rows, (float*)ob, lse);
+  return hipGetLastError();
 }
 
 hipError_t launch_slc_fwd(const Dims& D, const void* q, const void* k, const void* v, const uint8_t* valid,

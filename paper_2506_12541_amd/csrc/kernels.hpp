@@ -17,8 +17,12 @@ struct Dims {
   int mask_own;        // exclude own-ball blocks from selection
   int pool;            // 0 = MLP, 1 = mean
   int bf16;            // 1 = bf16 storage of Q/K/V/O, 0 = f32
+  int qc_mlp;          // coarse queries by the MLP phi_q over blocks of l (Eq. 13)
+  int gcmp;            // group compression (Eq. 15)
   float scale;         // softmax scale
   long long rows() const { return (long long)B * H * N; }
+  // coarse queries come from blocks of l (Eq. 13), not the group mean computed by the top-k
+  bool block_coarse() const { return qc_mlp || gcmp; }
   long long cmp_rows() const { return (long long)B * H * (N / l); }
 };
 
@@ -38,10 +42,11 @@ hipError_t launch_block_valid(const Dims& D, const uint8_t* valid, uint8_t* cval
 hipError_t launch_compress_fwd(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi,
                                float* out, float* pre, void* out_lp, void* w1t_ws, hipStream_t st);
 
-// select.hip: pooled-query block scores and group top-k (Eq. 6, 7, 10-12)
-// qpool: workspace of B*H*(N/g)*d floats for the pooled queries
+// select.hip: pooled-query block scores and group top-k (Eq. 6, 7, 10-12, 14)
+// qpool: B*H*(N/g)*d floats of coarse queries; written here (group mean of Eq. 11) unless
+// `given`, when it already holds them (Eq. 13)
 hipError_t launch_select_topk(const Dims& D, const void* q, const uint8_t* valid, const float* kcmp,
-                              const uint8_t* cvalid, int* sel, float* qpool, hipStream_t st);
+                              const uint8_t* cvalid, int* sel, float* qpool, bool given, hipStream_t st);
 
 // attn_fwd.hip: the three attention branches (Eq. 3, 5, 8) and the gate (Eq. 9)
 hipError_t launch_ball_fwd(const Dims& D, const void* q, const void* k, const void* v, const uint8_t* valid,
@@ -50,6 +55,12 @@ hipError_t launch_cmp_fwd(const Dims& D, const void* q, const void* kc, const vo
                           const uint8_t* cvalid, void* o, float* lse, hipStream_t st);
 hipError_t launch_slc_fwd(const Dims& D, const void* q, const void* k, const void* v, const uint8_t* valid,
                           const int* sel, void* o, float* lse, hipStream_t st);
+// group compression (Eq. 15): coarse attention [B, H, N/l, d] (float32 outputs) and its
+// copy to the token rows in the storage type
+hipError_t launch_cmp_coarse_fwd(const Dims& D, const void* qc, const void* kc, const void* vc, const uint8_t* cvalid,
+                                 float* oc, float* lsec, hipStream_t st);
+hipError_t launch_expand_coarse(const Dims& D, const float* oc, const float* lsec, const uint8_t* valid, void* ob,
+                                float* lse, hipStream_t st);
 hipError_t launch_gate_fwd(const Dims& D, const void* ob, const float* gate, const uint8_t* valid, void* o,
                            hipStream_t st);
 
@@ -70,6 +81,13 @@ struct BwdArgs {
   float *dkc_part, *dvc_part;    // [chunks, B, H, N/l, d]
   float *dkc, *dvc;              // [B, H, N/l, d]
   uint32_t *pair_keys, *pair_vals, *pair_keys_tmp, *pair_vals_tmp, *sort_hist;
+  // group compression (Eq. 15)
+  const float* qcmp;             // [B, H, N/l, d] coarse queries
+  const float* ocmp;             // [B, H, N/l, d] their attention outputs (float32)
+  void* qc_lp;                   // coarse queries in the storage type
+  void* doc;                     // [B, H, N/l, d] dO of the coarse queries, storage type
+  float* t4c;                    // [B, H, N/l] packed row terms of the coarse queries
+  float* dqc;                    // [B, H, N/l, d] gradient of the coarse queries
   int *seg_start, *seg_end;
   const uint32_t* pair_groups;   // set internally: sorted group ids
 };

@@ -241,10 +241,11 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
 
 template <typename T, int HD, int K>
 hipError_t select_k(const Dims& D, const void* q, const uint8_t* valid, const float* kcmp, const uint8_t* cvalid,
-                    int* sel, float* qpool, hipStream_t st) {
+                    int* sel, float* qpool, bool given, hipStream_t st) {
   const long long total = (long long)D.B * D.H * (D.N / D.g) * HD;
-  hipLaunchKernelGGL((pool_q_kernel<T, HD>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, (const T*)q, valid,
-                     D.H, D.N, D.g, total, qpool);
+  if (!given)
+    hipLaunchKernelGGL((pool_q_kernel<T, HD>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, (const T*)q,
+                       valid, D.H, D.N, D.g, total, qpool);
   const int ngroups = D.N / D.g;
   dim3 grid((ngroups + 16 * kWaves - 1) / (16 * kWaves), D.B * D.H);
   const int R = D.ls / D.l;
@@ -262,21 +263,21 @@ hipError_t select_k(const Dims& D, const void* q, const uint8_t* valid, const fl
 
 template <typename T, int HD>
 hipError_t select_hd(const Dims& D, const void* q, const uint8_t* valid, const float* kcmp, const uint8_t* cvalid,
-                     int* sel, float* qpool, hipStream_t st) {
-  if (D.k <= 4) return select_k<T, HD, 4>(D, q, valid, kcmp, cvalid, sel, qpool, st);
-  if (D.k <= 8) return select_k<T, HD, 8>(D, q, valid, kcmp, cvalid, sel, qpool, st);
-  return select_k<T, HD, 16>(D, q, valid, kcmp, cvalid, sel, qpool, st);
+                     int* sel, float* qpool, bool given, hipStream_t st) {
+  if (D.k <= 4) return select_k<T, HD, 4>(D, q, valid, kcmp, cvalid, sel, qpool, given, st);
+  if (D.k <= 8) return select_k<T, HD, 8>(D, q, valid, kcmp, cvalid, sel, qpool, given, st);
+  return select_k<T, HD, 16>(D, q, valid, kcmp, cvalid, sel, qpool, given, st);
 }
 
 }  // namespace
 
 hipError_t launch_select_topk(const Dims& D, const void* q, const uint8_t* valid, const float* kcmp,
-                              const uint8_t* cvalid, int* sel, float* qpool, hipStream_t st) {
+                              const uint8_t* cvalid, int* sel, float* qpool, bool given, hipStream_t st) {
   if (D.bf16)
-    return D.d == 64 ? select_hd<bf16_t, 64>(D, q, valid, kcmp, cvalid, sel, qpool, st)
-                     : select_hd<bf16_t, 32>(D, q, valid, kcmp, cvalid, sel, qpool, st);
-  return D.d == 64 ? select_hd<float, 64>(D, q, valid, kcmp, cvalid, sel, qpool, st)
-                   : select_hd<float, 32>(D, q, valid, kcmp, cvalid, sel, qpool, st);
+    return D.d == 64 ? select_hd<bf16_t, 64>(D, q, valid, kcmp, cvalid, sel, qpool, given, st)
+                     : select_hd<bf16_t, 32>(D, q, valid, kcmp, cvalid, sel, qpool, given, st);
+  return D.d == 64 ? select_hd<float, 64>(D, q, valid, kcmp, cvalid, sel, qpool, given, st)
+                   : select_hd<float, 32>(D, q, valid, kcmp, cvalid, sel, qpool, given, st);
 }
 
 }  // namespace bsa

@@ -14,6 +14,20 @@ TOL = {"f32": 1e-4, "bf16": 2e-2}   # max-abs output tolerance per storage type
 TIE = 1e-6                          # score gap under which two blocks count as tied
 
 
+# C-side variant parameters -> oracle Params keywords
+def oracle_kw(pkw) -> dict:
+    okw = {}
+    if pkw.get("kv_pool") == 1:
+        okw["kv_pool"] = "mean"
+    if pkw.get("mask_own_ball") == 0:
+        okw["mask_own_ball"] = False
+    if pkw.get("q_coarsen") == 1:
+        okw["q_coarsen"] = "mlp"
+    if pkw.get("group_compression") == 1:
+        okw["group_compression"] = True
+    return okw
+
+
 def oracle_params(cfg, **kw) -> ob.Params:
     return ob.Params(ball=cfg.ball, cmp_block=cfg.cmp_block, slc_block=cfg.slc_block, topk=cfg.topk,
                      group=cfg.group, **kw)
@@ -39,12 +53,14 @@ def gpu_forward(cfg, inp, valid, **pkw):
     vd = None if valid is None else to_dev(valid.astype(np.uint8), torch.uint8)
     phi_k = {w: to_dev(a, torch.float32) for w, a in inp["phi_k"].items()}
     phi_v = {w: to_dev(a, torch.float32) for w, a in inp["phi_v"].items()}
-    o, saved = gb.forward(p, q, k, v, vd, gate, phi_k, phi_v)
+    phi_q = {w: to_dev(a, torch.float32) for w, a in inp["phi_q"].items()}
+    o, saved = gb.forward(p, q, k, v, vd, gate, phi_k, phi_v, phi_q=phi_q)
     torch.cuda.synchronize()
     f = lambda t: t.float().cpu().numpy()
     return {"o": f(o), "o_branch": f(saved.o_branch), "lse": saved.lse.cpu().numpy(),
             "sel": saved.sel_idx.cpu().numpy().astype(np.int64), "kc": saved.kcmp.cpu().numpy(),
-            "vc": saved.vcmp.cpu().numpy()}, (p, q, k, v, vd, gate, phi_k, phi_v, saved, o)
+            "vc": saved.vcmp.cpu().numpy(), "qc": saved.qcmp.cpu().numpy()}, \
+        (p, q, k, v, vd, gate, phi_k, phi_v, saved, o, phi_q)
 
 
 def check_indices(sel_gpu, sel_or, scores):

@@ -66,6 +66,11 @@ def test_valid_params(lib):
     (dict(store_lse=0), _lib.BSA_ERR_UNSUPPORTED),
     (dict(dtype=7), _lib.BSA_ERR_INVALID_ARGUMENT),
     (dict(softmax_scale=-1.0), _lib.BSA_ERR_INVALID_ARGUMENT),
+    (dict(q_coarsen=2), _lib.BSA_ERR_INVALID_ARGUMENT),
+    (dict(group_compression=2), _lib.BSA_ERR_INVALID_ARGUMENT),
+    (dict(group_size=16, q_coarsen=_lib.BSA_QC_MLP), _lib.BSA_ERR_INVALID_ARGUMENT),   # needs g == l
+    (dict(group_size=16, group_compression=1), _lib.BSA_ERR_INVALID_ARGUMENT),
+    (dict(n=256, group_compression=1), _lib.BSA_ERR_UNSUPPORTED),                       # n / l < 64
 ])
 def test_invalid_params(lib, kw, code):
     st, _, _ = _sizes(lib, base(**kw))
@@ -82,8 +87,33 @@ def test_forward_rejects_before_launch(lib):
     cp = p.c()
     saved = _lib.bsa_saved_t()
     # NULL q: rejected on the host, nothing launched
-    st = lib.bsa_forward(C.byref(cp), None, None, None, None, None, None, None, None, C.byref(saved), None, 0, None)
+    st = lib.bsa_forward(C.byref(cp), None, None, None, None, None, None, None, None, None, C.byref(saved), None, 0,
+                         None)
     assert st == _lib.BSA_ERR_INVALID_ARGUMENT
+
+
+def test_variant_params_and_sizes(lib):
+    # group compression and MLP query coarsening (Eq. 13-15) with g == l are accepted, and
+    # they need more workspace than the regular layer (coarse queries, coarse outputs)
+    st0, ws0, sv0 = _sizes(lib, base())
+    st1, ws1, sv1 = _sizes(lib, base(q_coarsen=_lib.BSA_QC_MLP, group_compression=1))
+    assert st0 == st1 == _lib.BSA_OK
+    assert ws1 > ws0 and sv1 > sv0
+
+
+def test_variant_forward_needs_phi_q(lib):
+    p = base(q_coarsen=_lib.BSA_QC_MLP)
+    cp = p.c()
+    saved = _lib.bsa_saved_t()
+    fake = C.c_void_p(256)
+    for f in ("sel_idx", "lse", "o_branch", "kcmp", "vcmp", "hid_k", "hid_v", "cvalid", "qcmp", "hid_q", "ocmp"):
+        setattr(saved, f, 256)
+    m = _lib.bsa_mlp_t(256, 256, 256, 256)
+    # phi_q missing: rejected on the host before any launch
+    st = lib.bsa_forward(C.byref(cp), fake, fake, fake, None, fake, C.byref(m), C.byref(m), None, fake,
+                         C.byref(saved), fake, 1 << 40, None)
+    assert st == _lib.BSA_ERR_INVALID_ARGUMENT
+    assert "phi_q" in lib.bsa_last_error().decode()
 
 
 def test_tree_argument_errors(lib):

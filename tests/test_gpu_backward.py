@@ -12,7 +12,7 @@ import pytest
 import torch
 
 from oracle import bsa as ob
-from parity import TOL, gpu_forward, max_abs, oracle_params, to_dev, valid_from_tree
+from parity import TOL, gpu_forward, max_abs, oracle_kw, oracle_params, to_dev, valid_from_tree
 from paper_2506_12541_amd import bsa as gb
 from workloads import CONFIGS, Config, make_inputs
 
@@ -23,7 +23,7 @@ def oracle_with_sel(inp, valid, P, sel):
     """Oracle forward caches, with the selection branch re-run on the given blocks."""
     f64 = lambda a: np.asarray(a, np.float64)
     q, k, v = f64(inp["q"]), f64(inp["k"]), f64(inp["v"])
-    fwd = ob.forward(q, k, v, valid, inp["gate"], inp["phi_k"], inp["phi_v"], P)
+    fwd = ob.forward(q, k, v, valid, inp["gate"], inp["phi_k"], inp["phi_v"], P, phi_q=inp.get("phi_q"))
     fwd["sel"] = sel
     B, H = q.shape[:2]
     for b in range(B):
@@ -37,18 +37,14 @@ def run_case(cfg, seed=None, gate_scale=1.0, **pkw):
     inp = make_inputs(cfg, seed, layout="ball", with_grad=True)
     inp["gate"] = (inp["gate"] * gate_scale).astype(np.float32)
     valid = valid_from_tree(cfg)
-    g, (p, q, k, v, vd, gate, phi_k, phi_v, saved, o) = gpu_forward(cfg, inp, valid, **pkw)
+    g, (p, q, k, v, vd, gate, phi_k, phi_v, saved, o, phi_q) = gpu_forward(cfg, inp, valid, **pkw)
     dout = to_dev(inp["do"], p.torch_dtype)
-    grads = gb.backward(p, q, k, v, vd, gate, phi_k, phi_v, saved, dout)
+    grads = gb.backward(p, q, k, v, vd, gate, phi_k, phi_v, saved, dout, phi_q=phi_q)
     torch.cuda.synchronize()
-    okw = {}
-    if pkw.get("kv_pool") == 1:
-        okw["kv_pool"] = "mean"
-    if pkw.get("mask_own_ball") == 0:
-        okw["mask_own_ball"] = False
-    P = oracle_params(cfg, **okw)
+    P = oracle_params(cfg, **oracle_kw(pkw))
     fwd = oracle_with_sel(inp, valid, P, g["sel"])
-    ref = ob.backward(inp["q"], inp["k"], inp["v"], valid, inp["gate"], inp["phi_k"], inp["phi_v"], P, fwd, inp["do"])
+    ref = ob.backward(inp["q"], inp["k"], inp["v"], valid, inp["gate"], inp["phi_k"], inp["phi_v"], P, fwd, inp["do"],
+                      phi_q=inp["phi_q"])
     tol = TOL[cfg.dtype]
     out = {n: grads[n].cpu().numpy() for n in ("dq", "dk", "dv", "dgate")}
     errs = {}
@@ -57,10 +53,12 @@ def run_case(cfg, seed=None, gate_scale=1.0, **pkw):
     # summed gradients: |gpu - oracle| relative to the magnitude of the summed terms
     rel = lambda g, r, a: float(np.max(np.abs(np.asarray(g, np.float64) - r) / np.maximum(a, 1e-30)))
     errs["dgate"] = rel(out["dgate"], ref["dgate"], ref["abs"]["dgate"])
-    if P.kv_pool == "mlp":
-        for which in ("dphi_k", "dphi_v"):
-            for w in ("w1", "b1", "w2", "b2"):
-                errs[f"{which}.{w}"] = rel(grads[which][w].cpu().numpy(), ref[which][w], ref["abs"][which][w])
+    mlps = ("dphi_k", "dphi_v") if P.kv_pool == "mlp" else ()
+    if P.group_compression and P.q_coarsen == "mlp":
+        mlps += ("dphi_q",)
+    for which in mlps:
+        for w in ("w1", "b1", "w2", "b2"):
+            errs[f"{which}.{w}"] = rel(grads[which][w].cpu().numpy(), ref[which][w], ref["abs"][which][w])
     print({k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
     bad = {k: v for k, v in errs.items() if not v < tol}
     assert not bad, bad
@@ -109,7 +107,7 @@ def test_backward_scaling_one_head():
     print("backward parity config 3 (head 5)", flush=True)
     inp = make_inputs(cfg, layout="ball", with_grad=True)
     valid = valid_from_tree(cfg)
-    g, (p, q, k, v, vd, gate, phi_k, phi_v, saved, o) = gpu_forward(cfg, inp, valid)
+    g, (p, q, k, v, vd, gate, phi_k, phi_v, saved, o, _) = gpu_forward(cfg, inp, valid)
     grads = gb.backward(p, q, k, v, vd, gate, phi_k, phi_v, saved, to_dev(inp["do"], p.torch_dtype))
     torch.cuda.synchronize()
     h = 5

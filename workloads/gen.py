@@ -208,7 +208,8 @@ def make_inputs(cfg: Config, seed: int | None = None, *, layout: str = "ball",
             gate[b, s:e] = (x @ wg).astype(np.float32)
     out["gate"] = gate
     ld = cfg.cmp_block * d
-    for name, rr in (("phi_k", r[5]), ("phi_v", r[6])):
+    # phi_q: the query-coarsening MLP of Eq. 13 (own stream; the other tensors are unchanged)
+    for name, rr in (("phi_k", r[5]), ("phi_v", r[6]), ("phi_q", r[8])):
         out[name] = {
             "w1": rnd((rr.standard_normal((ld, d)) * 0.02).astype(np.float32)),
             "b1": rnd((rr.standard_normal(d) * 0.02).astype(np.float32)),
