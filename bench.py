@@ -7,6 +7,8 @@ through the C ABI). Inputs are seeded synthetic data already resident in HBM: a
 256, compression blocks of 16, selection blocks of 32, top-16, groups of 16.
 
 Prints one JSON line (rank 0, N=1). Usage: python bench.py [--steps K] [--warmup W]
+[--variant bsa|group_cmp]. The default is the regular layer; group_cmp is the variant with
+MLP query coarsening (Eq. 13-14) and group compression (Eq. 15).
 """
 from __future__ import annotations
 
@@ -25,19 +27,27 @@ MFMA_BF16_PEAK = 2.5e15     # MI355X dense bf16 MFMA, FLOP/s
 HBM_PEAK = 8.0e12           # MI355X HBM3E, B/s
 
 
-def algorithmic_flops(cfg):
+VARIANTS = {
+    "bsa": {},
+    "group_cmp": {"q_coarsen": 1, "group_compression": 1},
+}
+
+
+def algorithmic_flops(cfg, variant="bsa"):
     """Work the method must do (not the dense work it avoids), per step.
 
-    Per head: ball 4 N m d; MLP 2 (N/l)(l d d + d d) per tensor (K and V); compressed
-    attention 4 N (N/l) d; scoring 2 (N/g)(N/l) d; selection 4 N k* l' d. Backward: 2.5x
-    each attention term (5 vs 2 matrix products), 2x the MLP, nothing for scoring.
+    Per head: ball 4 N m d; MLP 2 (N/l)(l d d + d d) per tensor (K and V, plus Q for the
+    group-compression variant); compressed attention 4 N (N/l) d (group compression:
+    4 (N/l)(N/l) d); scoring 2 (N/g)(N/l) d; selection 4 N k* l' d. Backward: 2.5x each
+    attention term (5 vs 2 matrix products), 2x the MLP, nothing for scoring.
     """
     B, H, N, d = cfg.batch, cfg.heads, cfg.n_pad, cfg.head_dim
     m, l, ls, k, g = cfg.ball, cfg.cmp_block, cfg.slc_block, cfg.topk, cfg.group
+    gc = variant == "group_cmp"
     per = {
         "ball": 4.0 * N * m * d,
-        "mlp": 2 * 2.0 * (N / l) * (l * d * d + d * d),
-        "cmp": 4.0 * N * (N / l) * d,
+        "mlp": (3 if gc else 2) * 2.0 * (N / l) * (l * d * d + d * d),
+        "cmp": 4.0 * (N / l if gc else N) * (N / l) * d,
         "score": 2.0 * (N / g) * (N / l) * d,
         "slc": 4.0 * N * k * ls * d,
     }
@@ -54,7 +64,7 @@ CONCURRENT_PHASES = ["fwd.ball", "fwd.cmp", "fwd.select", "fwd.slc", "bwd.dq_bal
                      "bwd.mlp", "bwd.slc_csr", "bwd.slc_kv"]
 
 
-def phase_flops(cfg):
+def phase_flops(cfg, variant="bsa"):
     """Algorithmic FLOPs of each timed phase (same totals as algorithmic_flops).
 
     Backward split: the key-major kernels compute the recomputed scores, dP, dK and dV
@@ -63,8 +73,9 @@ def phase_flops(cfg):
     """
     B, H, N, d = cfg.batch, cfg.heads, cfg.n_pad, cfg.head_dim
     m, l, ls, k, g = cfg.ball, cfg.cmp_block, cfg.slc_block, cfg.topk, cfg.group
-    pairs = {"ball": N * m, "cmp": N * (N // l), "slc": N * k * ls}
-    mlp = 2 * 2.0 * (N / l) * (l * d * d + d * d) * B * H
+    gc = variant == "group_cmp"
+    pairs = {"ball": N * m, "cmp": (N // l if gc else N) * (N // l), "slc": N * k * ls}
+    mlp = (3 if gc else 2) * 2.0 * (N / l) * (l * d * d + d * d) * B * H
     f = {"fwd.compress": mlp, "fwd.select": 2.0 * (N / g) * (N / l) * d * B * H, "bwd.mlp": 2 * mlp}
     for br, kv in (("ball", "kv_ball"), ("cmp", "kv_cmp"), ("slc", "slc_kv")):
         f[f"fwd.{br}"] = 4.0 * pairs[br] * d * B * H
@@ -176,6 +187,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--variant", choices=sorted(VARIANTS), default="bsa")
     ap.add_argument("--cpu-baseline", type=int, default=1, help="time the float64 oracle on a sample (0 = skip)")
     ap.add_argument("--copy-calibration", action="store_true", help="run only the 1 GiB plain copy")
     ap.add_argument("--summarize-traffic", nargs=4, metavar="CSV",
@@ -189,7 +201,7 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(cfg, pts_np, inp_np):
+def cpu_baseline(cfg, pts_np, inp_np, variant="bsa"):
     """The float64 oracle on a bounded sample of the same workload: the full ball tree
     plus one of the heads' forward and backward; the head time is scaled by the head
     count to give points/s for the whole step."""
@@ -199,7 +211,9 @@ def cpu_baseline(cfg, pts_np, inp_np):
     from oracle.tree import build_ball_tree
 
     cores = len(os.sched_getaffinity(0))
-    P = ob.Params(ball=cfg.ball, cmp_block=cfg.cmp_block, slc_block=cfg.slc_block, topk=cfg.topk, group=cfg.group)
+    okw = {"q_coarsen": "mlp", "group_compression": True} if variant == "group_cmp" else {}
+    P = ob.Params(ball=cfg.ball, cmp_block=cfg.cmp_block, slc_block=cfg.slc_block, topk=cfg.topk, group=cfg.group,
+                  **okw)
     t0 = time.perf_counter()
     perm = build_ball_tree(pts_np[0], cfg.n_pad)
     t_tree = time.perf_counter() - t0
@@ -208,8 +222,8 @@ def cpu_baseline(cfg, pts_np, inp_np):
     valid = (perm >= 0)[None]
     q, k, v, do = (sl(inp_np[n]) for n in ("q", "k", "v", "do"))
     t0 = time.perf_counter()
-    fwd = ob.forward(q, k, v, valid, inp_np["gate"], inp_np["phi_k"], inp_np["phi_v"], P)
-    ob.backward(q, k, v, valid, inp_np["gate"], inp_np["phi_k"], inp_np["phi_v"], P, fwd, do)
+    fwd = ob.forward(q, k, v, valid, inp_np["gate"], inp_np["phi_k"], inp_np["phi_v"], P, phi_q=inp_np["phi_q"])
+    ob.backward(q, k, v, valid, inp_np["gate"], inp_np["phi_k"], inp_np["phi_v"], P, fwd, do, phi_q=inp_np["phi_q"])
     t_head = time.perf_counter() - t0
     total = t_tree + cfg.heads * t_head
     return {"value": cfg.batch * cfg.n_real / total, "unit": "points/s", "cores": cores, "kind": "oracle",
@@ -243,7 +257,7 @@ def main():
     pts_np = make_points(cfg)
     inp_np = make_inputs(cfg, layout="points", with_grad=False)
     inp_np["do"] = make_inputs(cfg, layout="ball", with_grad=True)["do"]
-    p = gb.Params.from_config(cfg)
+    p = gb.Params.from_config(cfg, **VARIANTS[args.variant])
     dt = p.torch_dtype
     t = lambda a, d=None: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(d or torch.float32)
     pts = t(pts_np)
@@ -251,6 +265,7 @@ def main():
     gate_pts = t(inp_np["gate"])
     phi_k = {w: t(a) for w, a in inp_np["phi_k"].items()}
     phi_v = {w: t(a) for w, a in inp_np["phi_v"].items()}
+    phi_q = {w: t(a) for w, a in inp_np["phi_q"].items()}
     dout = t(inp_np["do"], dt)
     saved = gb.Saved(p, dev)
     H, d = cfg.heads, cfg.head_dim
@@ -263,8 +278,8 @@ def main():
         gate = gb.permute(gate_pts, perm, 1, 3).view(cfg.batch, cfg.n_pad, 3)
         # every slot holds a real point when n_real == n_pad: the layer may skip key masks
         vmask = None if cfg.n_real == cfg.n_pad else valid
-        o, sv = gb.forward(p, q, k, v, vmask, gate, phi_k, phi_v, saved=saved)
-        grads = gb.backward(p, q, k, v, vmask, gate, phi_k, phi_v, sv, dout)
+        o, sv = gb.forward(p, q, k, v, vmask, gate, phi_k, phi_v, saved=saved, phi_q=phi_q)
+        grads = gb.backward(p, q, k, v, vmask, gate, phi_k, phi_v, sv, dout, phi_q=phi_q)
         return o, grads
 
     for _ in range(args.warmup):
@@ -289,17 +304,18 @@ def main():
     lib.bsa_timing_enable(0)
 
     ms = elapsed / args.steps * 1e3
-    fwd_f, bwd_f = algorithmic_flops(cfg)
+    fwd_f, bwd_f = algorithmic_flops(cfg, args.variant)
     flops = sum(fwd_f.values()) + sum(bwd_f.values())
     # the layer runs independent branches concurrently on two streams, so its time is the
     # step's wall time less the serial tree and permutation phases, not the sum of phases
     layer_ms = ms - phases["tree"] - phases["permute"]
     tflops = flops / (layer_ms * 1e-3) / 1e12
-    pf = phase_flops(cfg)
+    pf = phase_flops(cfg, args.variant)
     # dominant kernel: the longest single-launch contraction phase that runs alone on the chip
     dom = max((n for n in MFMA_PHASES if n not in CONCURRENT_PHASES), key=lambda n: phases[n])
     achieved = pf[dom] / (phases[dom] * 1e-3) / 1e12
-    traffic = measured_traffic(dom, cfg.name)
+    wl = cfg.name if args.variant == "bsa" else f"{args.variant}_{cfg.name}"
+    traffic = measured_traffic(dom, wl)
     result = {
         "metric": "BSA layer fwd+bwd points/sec and TFLOP/s (fraction of MFMA peak) at N=65536, 1 GPU",
         "value": cfg.batch * cfg.n_real / (ms * 1e-3),
@@ -315,8 +331,11 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {cfg.batch}x{cfg.n_real} points (32-component Gaussian mixture), "
                                f"H={cfg.heads} d={cfg.head_dim}, ball {cfg.ball}, cmp block {cfg.cmp_block}, "
-                               f"slc block {cfg.slc_block}, top-{cfg.topk}, group {cfg.group}; tree + permute + "
-                               f"forward + backward",
+                               f"slc block {cfg.slc_block}, top-{cfg.topk}, group {cfg.group}"
+                               + ("" if args.variant == "bsa" else
+                                  "; MLP query coarsening (Eq. 13-14) + group compression (Eq. 15)")
+                               + "; tree + permute + forward + backward",
+                   "variant": args.variant,
                    "points": cfg.batch * cfg.n_real, "heads": cfg.heads, "head_dim": cfg.head_dim},
         "tflops": tflops,
         "mfma_frac": tflops * 1e12 / MFMA_BF16_PEAK,
@@ -332,7 +351,8 @@ def main():
     }
     if args.cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, pts_np, {**inp_np, **make_inputs(cfg, layout="ball",
-                                                                                     with_grad=True)})
+                                                                                     with_grad=True)},
+                                              args.variant)
     print(json.dumps(result))
 
 
