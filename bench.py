@@ -7,12 +7,14 @@ through the C ABI). Inputs are seeded synthetic data already resident in HBM: a
 256, compression blocks of 16, selection blocks of 32, top-16, groups of 16.
 
 Prints one JSON line (rank 0, N=1). Usage: python bench.py [--steps K] [--warmup W]
-[--variant bsa|group_cmp]. The default is the regular layer; group_cmp is the variant with
-MLP query coarsening (Eq. 13-14) and group compression (Eq. 15).
+[--variant bsa|group_cmp|g1]. The default is the regular layer; group_cmp is the variant
+with MLP query coarsening (Eq. 13-14) and group compression (Eq. 15); g1 selects blocks per
+token (Eq. 6-8 without the grouping of Eq. 10-12).
 """
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import math
 import os
@@ -30,6 +32,7 @@ HBM_PEAK = 8.0e12           # MI355X HBM3E, B/s
 VARIANTS = {
     "bsa": {},
     "group_cmp": {"q_coarsen": 1, "group_compression": 1},
+    "g1": {},          # per-token selection: the workload with group size 1
 }
 
 
@@ -253,6 +256,8 @@ def main():
     from workloads import CONFIGS, make_inputs, make_points
 
     cfg = CONFIGS[args.config]
+    if args.variant == "g1":
+        cfg = dataclasses.replace(cfg, group=1)
     dev = torch.device("cuda:0")
     pts_np = make_points(cfg)
     inp_np = make_inputs(cfg, layout="points", with_grad=False)
@@ -332,8 +337,9 @@ def main():
         "config": {"workload": f"{cfg.name}: {cfg.batch}x{cfg.n_real} points (32-component Gaussian mixture), "
                                f"H={cfg.heads} d={cfg.head_dim}, ball {cfg.ball}, cmp block {cfg.cmp_block}, "
                                f"slc block {cfg.slc_block}, top-{cfg.topk}, group {cfg.group}"
-                               + ("" if args.variant == "bsa" else
-                                  "; MLP query coarsening (Eq. 13-14) + group compression (Eq. 15)")
+                               + {"bsa": "", "group_cmp": "; MLP query coarsening (Eq. 13-14) + group compression "
+                                                          "(Eq. 15)",
+                                  "g1": "; per-token selection (Eq. 6-8, no grouping)"}[args.variant]
                                + "; tree + permute + forward + backward",
                    "variant": args.variant,
                    "points": cfg.batch * cfg.n_real, "heads": cfg.heads, "head_dim": cfg.head_dim},

@@ -53,12 +53,18 @@ bsa_status_t check_params(const bsa_params_t* p, bsa::Dims* D) {
     return fail(BSA_ERR_INVALID_ARGUMENT, "slc_block must be a multiple of 16 and of cmp_block and divide ball_size");
   const int r = p->slc_block / p->cmp_block;
   if (r != 1 && r != 2 && r != 4) return fail(BSA_ERR_UNSUPPORTED, "slc_block / cmp_block must be 1, 2 or 4");
-  if (!pow2(p->group_size) || p->group_size < 8 || p->ball_size % p->group_size != 0)
-    return fail(BSA_ERR_INVALID_ARGUMENT, "group_size must be a power of two >= 8 dividing ball_size");
+  if (!pow2(p->group_size) || p->ball_size % p->group_size != 0)
+    return fail(BSA_ERR_INVALID_ARGUMENT, "group_size must be a power of two dividing ball_size");
+  if (p->group_size != 1 && p->group_size < 8)
+    return fail(BSA_ERR_UNSUPPORTED, "group_size must be 1 (per-token selection) or >= 8");
+  if (p->group_size == 1 && p->dtype != BSA_BF16)
+    return fail(BSA_ERR_UNSUPPORTED, "per-token selection (group_size 1) needs bf16 storage");
   if (p->topk < 1 || p->topk > 16) return fail(BSA_ERR_UNSUPPORTED, "topk must be in [1, 16]");
   const int G = p->group_size >= 16 ? 1 : 16 / p->group_size;
-  if (G * p->topk * (p->slc_block / 16) > 256)
+  if (p->group_size >= 8 && G * p->topk * (p->slc_block / 16) > 256)
     return fail(BSA_ERR_UNSUPPORTED, "too many selected tokens per 16-query block (limit 4096)");
+  if ((int64_t)p->batch * p->heads * p->n * p->topk >= (int64_t)1 << 31)
+    return fail(BSA_ERR_UNSUPPORTED, "batch * heads * n * topk must stay below 2^31");
   if (p->mask_own_ball != 0 && p->mask_own_ball != 1) return fail(BSA_ERR_INVALID_ARGUMENT, "mask_own_ball must be 0/1");
   if (p->store_lse != 1) return fail(BSA_ERR_UNSUPPORTED, "store_lse must be 1");
   if (p->deterministic != 0 && p->deterministic != 1) return fail(BSA_ERR_INVALID_ARGUMENT, "deterministic must be 0/1");
@@ -126,8 +132,27 @@ SavedLayout saved_layout(const bsa::Dims& D) {
 }
 
 struct FwdWs {
-  size_t w1t_k, w1t_v, w1t_q, kc_lp, vc_lp, qc_lp, lsec, total;
+  size_t w1t_k, w1t_v, w1t_q, kc_lp, vc_lp, qc_lp, lsec;
+  size_t pk, pv, pkt, pvt, hist, seg_s, seg_e, part, ml;   // per-token selection (g = 1)
+  size_t total;
 };
+
+// Per-token selection buffers: sorted (query, slot) pairs, block ranges, partials.
+bsa::Slc1Ws slc1_ws(const bsa::Dims& D, char* w, size_t pk, size_t pv, size_t pkt, size_t pvt, size_t hist,
+                    size_t seg_s, size_t seg_e, size_t part, size_t ml) {
+  bsa::Slc1Ws W{};
+  W.keys = (uint32_t*)(w + pk);
+  W.vals = (uint32_t*)(w + pv);
+  W.keys_tmp = (uint32_t*)(w + pkt);
+  W.vals_tmp = (uint32_t*)(w + pvt);
+  W.hist = (uint32_t*)(w + hist);
+  W.seg_start = (int*)(w + seg_s);
+  W.seg_end = (int*)(w + seg_e);
+  W.part = (float*)(w + part);
+  W.ml = ml == (size_t)-1 ? nullptr : (float*)(w + ml);
+  (void)D;
+  return W;
+}
 
 FwdWs fwd_ws_layout(const bsa::Dims& D) {
   FwdWs W{};
@@ -141,12 +166,23 @@ FwdWs fwd_ws_layout(const bsa::Dims& D) {
   W.w1t_q = put(D.qc_mlp ? w1 : 0);
   W.qc_lp = put(D.block_coarse() ? elem_bytes(D) * (size_t)D.cmp_rows() * D.d : 0);
   W.lsec = put(D.gcmp ? sizeof(float) * (size_t)D.cmp_rows() : 0);
+  const size_t np = D.g == 1 ? bsa::slc1_pairs(D) : 0;
+  const size_t nseg = D.g == 1 ? (size_t)D.B * D.H * (D.N / D.ls) : 0;
+  W.pk = put(4 * np);
+  W.pv = put(4 * np);
+  W.pkt = put(4 * np);
+  W.pvt = put(4 * np);
+  W.hist = put(D.g == 1 ? 4 * bsa::radix_sort_hist_words((long long)np) : 0);
+  W.seg_s = put(4 * nseg);
+  W.seg_e = put(4 * nseg);
+  W.part = put(sizeof(float) * np * D.d);
+  W.ml = put(2 * sizeof(float) * np);
   W.total = off;
   return W;
 }
 
 struct BwdWs {
-  size_t qc_lp, doc, t4c, dqc;
+  size_t qc_lp, doc, t4c, dqc, dqpart;
   size_t R, terms, dplp, kc_lp, vc_lp, dkc_part, dvc_part, dkc, dvc, pk, pv, pkt, pvt, hist, seg_s, seg_e, dpre, pw1, psm, w1lp,
       total;
   int cmp_chunks, mlp_chunks, mlp_chunks_small;
@@ -188,6 +224,7 @@ BwdWs bwd_ws_layout(const bsa::Dims& D) {
   W.doc = put(D.gcmp ? elem_bytes(D) * crows * D.d : 0);
   W.t4c = put(D.gcmp ? 4 * sizeof(float) * crows : 0);
   W.dqc = put(D.gcmp ? sizeof(float) * crows * D.d : 0);
+  W.dqpart = put(D.g == 1 ? sizeof(float) * bsa::slc1_pairs(D) * D.d : 0);
   W.total = off;
   return W;
 }
@@ -433,9 +470,16 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   BSA_STEP("fwd.select", bsa::launch_select_topk(D, q, valid, saved->kcmp, saved->cvalid, saved->sel_idx,
                                                   saved->qcmp, D.block_coarse(), st),
            "select");
-  BSA_STEP("fwd.slc",
-           bsa::launch_slc_fwd(D, q, k, v, valid, saved->sel_idx, ob + 2 * ob_stride, saved->lse + 2 * rows, st),
-           "selection attention");
+  if (D.g == 1) {
+    const bsa::Slc1Ws S1 = slc1_ws(D, w, W.pk, W.pv, W.pkt, W.pvt, W.hist, W.seg_s, W.seg_e, W.part, W.ml);
+    BSA_STEP("fwd.slc",
+             bsa::launch_slc1_fwd(D, q, k, v, valid, saved->sel_idx, S1, ob + 2 * ob_stride, saved->lse + 2 * rows, st),
+             "per-token selection attention");
+  } else {
+    BSA_STEP("fwd.slc",
+             bsa::launch_slc_fwd(D, q, k, v, valid, saved->sel_idx, ob + 2 * ob_stride, saved->lse + 2 * rows, st),
+             "selection attention");
+  }
   s = join_aux(aux, st);
   if (s != BSA_OK) return s;
   BSA_STEP("fwd.gate", bsa::launch_gate_fwd(D, ob, gate, valid, o, st), "gate");
@@ -504,9 +548,19 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   BSA_TRY(e, "compression backward K");
   BSA_PHASE("bwd.mlp", st, e = bsa::launch_compress_bwd(D, v, valid, mv, saved->hid_v, A.dvc, dv, gv, mw, st));
   BSA_TRY(e, "compression backward V");
-  BSA_TRY(bsa::launch_slc_csr(D, A, st), "selection backward");
+  const bsa::Slc1Ws S1 = slc1_ws(D, w, W.pk, W.pv, W.pkt, W.pvt, W.hist, W.seg_s, W.seg_e, W.dqpart, (size_t)-1);
+  if (D.g == 1)
+    BSA_TRY(bsa::launch_slc1_bwd(D, q, k, v, d_o, valid, saved->sel_idx, (const float4*)A.terms + 2 * D.rows(), S1,
+                                 dk, dv, st),
+            "per-token selection backward");
+  else
+    BSA_TRY(bsa::launch_slc_csr(D, A, st), "selection backward");
   s = join_aux(aux, st);
   if (s != BSA_OK) return s;
+  if (D.g == 1) {   // the dQ parts of the per-token selection, after the dQ chain
+    BSA_PHASE("bwd.dq_slc", st, e = bsa::launch_slc1_merge_dq(D, saved->sel_idx, valid, S1, dq, st));
+    BSA_TRY(e, "per-token selection dQ");
+  }
   if (D.gcmp) {
     // coarse-query gradient of Eq. 15 through phi_q (or the block mean) into dQ
     bsa::Dims Dq = D;

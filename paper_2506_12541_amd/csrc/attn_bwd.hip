@@ -1306,6 +1306,7 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t
                                            A.valid ? A.cvalid : nullptr, qcoarse, D.H, nct, nct, D.m, sl2, D.scale,
                                            A.dqc);
   });
+  if (D.g != 1)   // per-token selection adds its dQ parts after the streams join
   BSA_PHASE("bwd.dq_slc", st, {
   if constexpr (sizeof(T) == 2) {
     constexpr int NW = 2;

@@ -114,6 +114,24 @@ hipError_t launch_compress_bwd(const Dims& D, const void* x, const uint8_t* vali
                                const float* dy, float* dx_accum, const MlpGrad& grad, const MlpBwdWs& ws,
                                hipStream_t st);
 
+// slc_token.hip: selection attention with per-token selection (g = 1), block-major.
+struct Slc1Ws {
+  uint32_t *keys, *vals, *keys_tmp, *vals_tmp, *hist;   // (query, slot) pairs and their sort
+  int *seg_start, *seg_end;                             // [B*H*N/l'] pair range of each block
+  float* part;   // [pairs, d] forward: unnormalised partial outputs; backward: dQ parts
+  float* ml;     // [pairs, 2] forward: scaled max and sum of each partial softmax
+};
+size_t slc1_pairs(const Dims& D);
+hipError_t launch_slc1_csr(const Dims& D, const int* sel, const uint8_t* valid, const Slc1Ws& W, uint32_t** vals_out,
+                           hipStream_t st);
+hipError_t launch_slc1_fwd(const Dims& D, const void* q, const void* k, const void* v, const uint8_t* valid,
+                           const int* sel, const Slc1Ws& W, void* o, float* lse, hipStream_t st);
+hipError_t launch_slc1_bwd(const Dims& D, const void* q, const void* k, const void* v, const void* dout,
+                           const uint8_t* valid, const int* sel, const float4* t4, const Slc1Ws& W, float* dk,
+                           float* dv, hipStream_t st);
+hipError_t launch_slc1_merge_dq(const Dims& D, const int* sel, const uint8_t* valid, const Slc1Ws& W, float* dq,
+                                hipStream_t st);
+
 // tree.hip: stable LSD radix sort of (key, value) pairs on the low `bits` key bits.
 size_t radix_sort_hist_words(long long n);
 hipError_t launch_radix_sort_pairs(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,

@@ -60,7 +60,8 @@ def test_valid_params(lib):
     (dict(slc_block=24), _lib.BSA_ERR_INVALID_ARGUMENT),
     (dict(slc_block=64, cmp_block=8), _lib.BSA_ERR_UNSUPPORTED),
     (dict(group_size=12), _lib.BSA_ERR_INVALID_ARGUMENT),
-    (dict(group_size=4), _lib.BSA_ERR_INVALID_ARGUMENT),
+    (dict(group_size=4), _lib.BSA_ERR_UNSUPPORTED),        # 1 (per token) or >= 8
+    (dict(group_size=1, dtype=_lib.BSA_F32), _lib.BSA_ERR_UNSUPPORTED),   # per token: bf16 only
     (dict(topk=0), _lib.BSA_ERR_UNSUPPORTED),
     (dict(topk=17), _lib.BSA_ERR_UNSUPPORTED),
     (dict(store_lse=0), _lib.BSA_ERR_UNSUPPORTED),
@@ -99,6 +100,13 @@ def test_variant_params_and_sizes(lib):
     st1, ws1, sv1 = _sizes(lib, base(q_coarsen=_lib.BSA_QC_MLP, group_compression=1))
     assert st0 == st1 == _lib.BSA_OK
     assert ws1 > ws0 and sv1 > sv0
+
+
+def test_per_token_selection_sizes(lib):
+    # g = 1 (Eq. 6-8 without grouping) is accepted for bf16 and needs the pair buffers
+    st0, ws0, _ = _sizes(lib, base(dtype=_lib.BSA_BF16))
+    st1, ws1, _ = _sizes(lib, base(dtype=_lib.BSA_BF16, group_size=1))
+    assert st0 == st1 == _lib.BSA_OK and ws1 > ws0
 
 
 def test_variant_forward_needs_phi_q(lib):

@@ -143,3 +143,43 @@ def test_mlp_coarsening_backward_leaves_phi_q():
     # gradients are those of the regular layer with the same selection
     print("variant backward parity config 1, mlp coarsening only", flush=True)
     run_case(CONFIGS[1], q_coarsen=1)
+
+
+# ---- per-token selection (g = 1: Eq. 6-8 without the grouping of Eq. 10-12) ----
+
+@pytest.mark.parametrize("cfg", [dataclasses.replace(CONFIGS[2], group=1, batch=4),
+                                 dataclasses.replace(SMALL, group=1)], ids=["airflow_l16", "small_l32"])
+def test_per_token_forward(cfg):
+    print(f"per-token selection forward parity {cfg.name} group 1", flush=True)
+    inp = make_inputs(cfg, seed=7, layout="ball", with_grad=False)
+    valid = valid_from_tree(cfg, seed=7)
+    g, _ = gpu_forward(cfg, inp, valid)
+    P = oracle_params(cfg)
+    ndiff = 0
+    for b in range(min(cfg.batch, 2)):
+        for h in range(cfg.heads):
+            ndiff += _check_head(inp, valid, g, b, h, P, TOL[cfg.dtype])
+    print(f"tie-justified index differences: {ndiff} rows")
+
+
+@pytest.mark.timeout(300)
+def test_per_token_scaling_sampled():
+    """The 65536-point workload with per-token selection; oracle on 256 sampled queries of
+    two heads."""
+    cfg = dataclasses.replace(CONFIGS[3], group=1)
+    print("per-token selection forward parity 65536 points (sampled)", flush=True)
+    inp = make_inputs(cfg, seed=3, layout="ball", with_grad=False)
+    valid = valid_from_tree(cfg, seed=3)
+    g, _ = gpu_forward(cfg, inp, valid)
+    P = oracle_params(cfg)
+    rng = np.random.default_rng(6)
+    for h in (0, cfg.heads - 1):
+        groups = np.unique(np.concatenate([[0, cfg.n_pad - 1], rng.choice(cfg.n_pad, 254, replace=False)]))
+        _check_head(inp, valid, g, 0, h, P, TOL[cfg.dtype], groups=groups)
+
+
+@pytest.mark.parametrize("cfg", [dataclasses.replace(CONFIGS[5], group=1, batch=2),
+                                 dataclasses.replace(SMALL, group=1)], ids=["airflow_l16", "small_l32"])
+def test_per_token_backward(cfg):
+    print(f"per-token selection backward parity {cfg.name} group 1", flush=True)
+    run_case(cfg, seed=9)

@@ -107,9 +107,10 @@ def _run_oracle(inp):
     return fwd, grads
 
 
-@pytest.mark.parametrize("seed,mask_own", [(0, True), (1, False)])
-def test_against_torch_dense_autograd(seed, mask_own):
-    P = Params(ball=16, cmp_block=4, slc_block=8, topk=2, group=4, mask_own_ball=mask_own)
+@pytest.mark.parametrize("seed,mask_own,group", [(0, True, 4), (1, False, 4), (4, True, 1)])
+def test_against_torch_dense_autograd(seed, mask_own, group):
+    # group 1: per-token selection (Eq. 6-8 without the grouping of Eq. 10-12)
+    P = Params(ball=16, cmp_block=4, slc_block=8, topk=2, group=group, mask_own_ball=mask_own)
     inp = _inputs(seed, P=P)
     fwd, grads = _run_oracle(inp)
     o_ref, g_ref = _dense_torch(inp, fwd["sel"])

@@ -182,6 +182,38 @@ def test_selection_all_blocks_is_full_attention(rng):
     assert np.allclose(o, sdpa(q, k, v), atol=1e-12)
 
 
+def test_per_token_selection_all_blocks_is_full_attention(rng):
+    # g = 1: every query selects on its own scores (Eq. 7); with all blocks selected each
+    # query attends to every key
+    n, d = 64, 8
+    P = Params(ball=16, cmp_block=4, slc_block=8, topk=8, group=1, mask_own_ball=False)
+    q, k, v = rnd(rng, n, d), rnd(rng, n, d), rnd(rng, n, d)
+    valid = np.ones(n, bool)
+    sel = bsa.topk_blocks(bsa.group_block_scores(q, rnd(rng, n // 4, d), valid, P), P.topk)
+    assert sel.shape == (n, 8) and np.all(sel >= 0)
+    o, _ = bsa.selection_branch(q, k, v, valid, sel, P)
+    assert np.allclose(o, sdpa(q, k, v), atol=1e-12)
+
+
+def test_per_token_selection_is_a_block_mask(rng):
+    # g = 1 with k* < blocks: query t attends exactly to the keys of its own selected blocks
+    n, d, ls = 64, 8, 8
+    P = Params(ball=16, cmp_block=4, slc_block=ls, topk=3, group=1)
+    q, k, v = rnd(rng, n, d), rnd(rng, n, d), rnd(rng, n, d)
+    valid = rng.random(n) > 0.2
+    sel = bsa.topk_blocks(bsa.group_block_scores(q, rnd(rng, n // 4, d), valid, P), P.topk)
+    mask = np.zeros((n, n), bool)
+    for t in range(n):
+        for j in sel[t]:
+            if j >= 0:
+                mask[t, j * ls:(j + 1) * ls] = True
+    mask &= valid[None, :]
+    o, _ = bsa.selection_branch(q, k, v, valid, sel, P)
+    rows = valid & mask.any(axis=1)
+    assert np.allclose(o[rows], sdpa(q, k, v, mask)[rows], atol=1e-12)
+    assert not o[~valid].any()
+
+
 def test_selection_all_candidates_masks_own_ball(rng):
     n, d = 64, 8
     P = Params(ball=16, cmp_block=4, slc_block=8, topk=6, group=4)
