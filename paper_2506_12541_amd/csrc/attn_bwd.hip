@@ -2,6 +2,9 @@
 // 8, 9). With dO_b = sigmoid(gamma_b) dO and per-row delta D_b = rowsum(dO_b * o_b), each
 // branch is softmax attention, so with P = exp(S - LSE):
 //     dP = dO_b V^T,  dS = P * (dP - D_b),  dQ = scale dS K,  dK = scale dS^T Q,  dV = P^T dO_b.
+// The kernels fold the gate scale s = sigmoid(gamma_b) into the exponent: with
+// E = s P = exp2(S log2e - (log2 LSE - log2 s)), dV = E^T dO and dS = E * (dO V^T - R_b),
+// R_b = rowsum(dO * o_b) the unscaled delta, so no element needs a separate multiply by s.
 // No gradient flows through the top-k selection (it is piecewise constant).
 //
 // Every gradient is produced without floating-point atomics, so results are
@@ -24,8 +27,8 @@ __device__ __forceinline__ float lse_log2(float lse) { return lse == -__builtin_
 
 // ---- gate backward: R_b = rowsum(dO * o_b) per (b,h,n); dgamma_b = s'(gamma_b) sum_h R_b ----
 // 8 lanes per row, each lane a 16-byte piece per tensor; partial sums reduced by shuffles.
-// The same pass packs each query row's terms for the attention passes: log2 LSE, the gate
-// scale s = sigmoid(gamma_b) and delta D_b = s R_b (16 bytes per row and branch).
+// The same pass packs each query row's terms for the attention passes (16 bytes per row
+// and branch; the layout QTerms describes).
 template <typename T>
 __global__ void gate_bwd_rows_kernel(const T* dout, const T* ob, long long rows, int hd, const float* lse,
                                      const float* gate, int H, int N, float* R, float4* terms) {
@@ -62,7 +65,8 @@ __global__ void gate_bwd_rows_kernel(const T* dout, const T* ob, long long rows,
     for (int br = 0; br < 3; ++br) {
       R[br * rows + row] = acc[br];
       const float sg = sigmoidf(gate[(b * N + n) * 3 + br]);
-      terms[br * rows + row] = make_float4(lse_log2(lse[br * rows + row]), sg, sg * acc[br], 0.f);
+      const float l2 = lse_log2(lse[br * rows + row]);
+      terms[br * rows + row] = make_float4(l2 - log2f(sg), sg, acc[br], l2);
     }
   }
 }
@@ -85,7 +89,7 @@ __global__ void gate_bwd_kernel(const float* R, const float* gate, const uint8_t
 
 // Group compression (Eq. 15), per coarse query: the copy's adjoint sums s_t dO_t over the
 // real rows t of its block (s_t = sigmoid(gamma_cmp) of row t), kept in the storage type
-// dO_c; its packed terms are (log2 LSE, 1, rowsum(dO_c * o_c), 0), the delta formed from
+// dO_c; its packed terms are (log2 LSE, 1, rowsum(dO_c * o_c), log2 LSE), the delta formed from
 // the rounded dO_c the attention passes use and the float32 coarse output o_c, so that it
 // equals their sum_j P_j dP_j to float32 rounding (near-uniform coarse softmaxes make dQ_c
 // small next to either term). The log2 LSE is the one every real row of the block
@@ -109,13 +113,13 @@ __global__ void coarse_rows_bwd_kernel(const T* dout, const float4* t4b, const f
     if (vb != nullptr && vb[t] == 0) continue;
     const float4 tt = t4b[r0 + t];
     acc += tt.y * to_f32<T>(dout[(r0 + t) * hd + col]);
-    l2 = fminf(l2, tt.x);
+    l2 = fminf(l2, tt.w);
   }
   const T dr = from_f32<T>(acc);
   doc[cr * hd + col] = dr;
   float dd = to_f32<T>(dr) * oc[cr * hd + col];
   for (int off = hd / 2; off > 0; off >>= 1) dd += __shfl_xor(dd, off, 64);
-  if (col == 0) t4c[cr] = make_float4(l2, 1.f, dd, 0.f);
+  if (col == 0) t4c[cr] = make_float4(l2, 1.f, dd, l2);
 }
 
 template <typename T>
@@ -132,10 +136,10 @@ __global__ void sum_chunks_kernel(const float* part, int nchunks, long long n, f
   out[i] = s;
 }
 
-// Per-query terms of one branch: log2 LSE, delta D = s * R, gate scale s.
-// Per query row of one branch: packed (log2 LSE, s, s * R, 0), where s scales the row's
-// dO (the branch gate sigmoid(gamma_b), or 1 for rows whose dO is already scaled) and
-// s * R is the softmax-backward delta rowsum(s dO * o_b). [B, H, N] float4.
+// Per query row of one branch, packed (log2 LSE - log2 s, s, R, log2 LSE): s scales the
+// row's dO (the branch gate sigmoid(gamma_b), or 1 for rows whose dO is already scaled),
+// R = rowsum(dO * o_b) for the unscaled dO, so exp2(S log2e - x) is s P and the softmax
+// gradient is s P (dO V^T - R). Rows without keys carry +inf in x and w. [B, H, N] float4.
 struct QTerms {
   const float4* t4;
 };
@@ -240,7 +244,7 @@ __global__ void __launch_bounds__(256) dense_bwd_q_kernel(const T* q, const T* k
           for (int i = 0; i < 4; ++i) {
             const float e = fast_exp2(__builtin_fmaf(sv[qb][kb][i], sl2, -l2[qb]));
             const float p = ((okw[kb] >> (8 * i)) & 1u) ? e : 0.f;
-            v8[kb][i] = p * __builtin_fmaf(dp[qb][kb][i], gs[qb], -dd[qb]);
+            v8[kb][i] = p * (dp[qb][kb][i] - dd[qb]);
           }
 #pragma unroll
         for (int kp = 0; kp < KB / 2; ++kp) {
@@ -279,7 +283,8 @@ __global__ void __launch_bounds__(256) dense_bwd_q_kernel(const T* q, const T* k
 // bf16 variant of the query-major pass: 64-key K and V tiles double-buffered in LDS (two
 // distinct objects, loop unrolled by two) and filled by direct global->LDS loads; the K^T
 // operand of the dQ product comes from transpose reads of the row-major K tile.
-template <int HD, int QB, bool BALL, bool ADD>
+// MASK = false: every key is real and the key count is a multiple of the tile.
+template <int HD, int QB, bool BALL, bool ADD, bool MASK = true>
 __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
                                                               const bf16_t* dout, const uint8_t* kvalid_all,
                                                               QTerms qt, int H, int N, int nkeys_total, int m,
@@ -328,7 +333,7 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
       qf[qb][c] = load_chunk(q + row * HD + 32 * c + 8 * j);
       df[qb][c] = load_chunk(dout + row * HD + 32 * c + 8 * j);
     }
-    const float4 t = qt.t4[row];   // log2 LSE, s, s R
+    const float4 t = qt.t4[row];   // log2 LSE - log2 s, s, R
     l2[qb] = t.x;
     gs[qb] = t.y;
     dd[qb] = t.z;
@@ -368,8 +373,8 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float e = fast_exp2(__builtin_fmaf(sv[qb][kb][i], sl2, -l2[qb]));
-          const float p = ((okw[kb] >> (8 * i)) & 1u) ? e : 0.f;
-          v8[kb][i] = p * __builtin_fmaf(dp[qb][kb][i], gs[qb], -dd[qb]);
+          const float p = !MASK || ((okw[kb] >> (8 * i)) & 1u) ? e : 0.f;
+          v8[kb][i] = p * (dp[qb][kb][i] - dd[qb]);
         }
 #pragma unroll
       for (int kp = 0; kp < KB / 2; ++kp) {
@@ -532,8 +537,8 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const float p = kok[kb] ? fast_exp2(__builtin_fmaf(sv[u][kb][i], sl2, -lv[i])) : 0.f;
-            a8[kb][4 * u + i] = p * gv[i];
-            b8[kb][4 * u + i] = p * __builtin_fmaf(dp[u][kb][i], gv[i], -dv4[i]);
+            a8[kb][4 * u + i] = p;
+            b8[kb][4 * u + i] = p * (dp[u][kb][i] - dv4[i]);
           }
       }
 #pragma unroll
@@ -572,7 +577,8 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
 // double-buffered in LDS (two distinct objects, loop unrolled by two) and filled by direct
 // global->LDS loads; the transposed operands of the dK^T and dV^T products come from
 // transpose reads of the same row-major tiles.
-template <int HD, int NW, bool BALL>
+// MASK = false: every key of the grid is real and in range (no per-key select).
+template <int HD, int NW, bool BALL, bool MASK = true>
 __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
                                                                    const bf16_t* dout, const uint8_t* kvalid_all,
                                                                    QTerms qt, int H, int N, int nkeys_total, int m,
@@ -662,12 +668,13 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
         const int qb = 2 * qp + u;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float4 t = tm[16 * qb + 4 * j + i];   // log2 LSE, s, s R
+          const float4 t = tm[16 * qb + 4 * j + i];   // log2 LSE - log2 s, s, R
 #pragma unroll
           for (int kb = 0; kb < KBW; ++kb) {
-            const float p = kok[kb] ? fast_exp2(__builtin_fmaf(sv[u][kb][i], sl2, -t.x)) : 0.f;
-            a8[kb][4 * u + i] = p * t.y;
-            b8[kb][4 * u + i] = p * __builtin_fmaf(dp[u][kb][i], t.y, -t.z);
+            const float e = fast_exp2(__builtin_fmaf(sv[u][kb][i], sl2, -t.x));
+            const float p = !MASK || kok[kb] ? e : 0.f;
+            a8[kb][4 * u + i] = p;
+            b8[kb][4 * u + i] = p * (dp[u][kb][i] - t.z);
           }
         }
       }
@@ -807,7 +814,7 @@ __global__ void __launch_bounds__(256) slc_bwd_q_kernel(const T* q, const T* k, 
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float p = ok[kb][i] ? fast_exp2(__builtin_fmaf(s[kb][i], sl2, -l2)) : 0.f;
-        w8[4 * kb + i] = p * __builtin_fmaf(dp[kb][i], gs, -dd);
+        w8[4 * kb + i] = p * (dp[kb][i] - dd);
       }
     const CT dsf = make_chunk<T>(w8);
 #pragma unroll
@@ -934,7 +941,7 @@ __global__ void __launch_bounds__(NW * 64) slc_bwd_q_dma_kernel(const bf16_t* q,
     qf[c] = load_chunk(q + row * HD + 32 * c + 8 * j);
     df[c] = load_chunk(dout + row * HD + 32 * c + 8 * j);
   }
-  const float4 tr = qt.t4[row];   // log2 LSE, s, s R of this lane's query
+  const float4 tr = qt.t4[row];   // log2 LSE - log2 s, s, R of this lane's query
   const float l2 = tr.x, gs = tr.y, dd = tr.z;
   f32x4 acc[DB];
 #pragma unroll
@@ -983,7 +990,7 @@ __global__ void __launch_bounds__(NW * 64) slc_bwd_q_dma_kernel(const bf16_t* q,
       for (int i = 0; i < 4; ++i) {
         const float e = fast_exp2(__builtin_fmaf(sv[kb][i], sl2, -l2));
         const float p = ((m[kb] >> (4 * j + i)) & 1u) ? e : 0.f;
-        w8[4 * kb + i] = p * __builtin_fmaf(dp[kb][i], gs, -dd);
+        w8[4 * kb + i] = p * (dp[kb][i] - dd);
       }
     const CT dsf = make_chunk<bf16_t>(w8);
 #pragma unroll
@@ -1120,8 +1127,8 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_kernel(const T* q, const T* k,
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float pr = kok[kb] ? fast_exp2(__builtin_fmaf(sv[i], sl2, -cl[i])) : 0.f;
-        pg[i] = pr * cg[i];
-        dsv[i] = pr * __builtin_fmaf(dp[i], cg[i], -cdv[i]);
+        pg[i] = pr;
+        dsv[i] = pr * (dp[i] - cdv[i]);
       }
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
@@ -1184,9 +1191,14 @@ template <typename T, int HD, int QB, bool BALL, bool ADD>
 void launch_bwd_q(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v, const T* dout,
                   const uint8_t* kvalid, QTerms qt, int H, int N, int nkeys_total, int m, float sl2, float scale,
                   float* dq) {
-  if constexpr (sizeof(T) == 2)
-    hipLaunchKernelGGL((dense_bwd_q_dma_kernel<HD, QB, BALL, ADD>), grid, dim3(256), 0, st, q, k, v, dout, kvalid,
-                       qt, H, N, nkeys_total, m, sl2, scale, dq);
+  if constexpr (sizeof(T) == 2) {
+    if (kvalid == nullptr && (BALL ? m : nkeys_total) % kKT == 0)
+      hipLaunchKernelGGL((dense_bwd_q_dma_kernel<HD, QB, BALL, ADD, false>), grid, dim3(256), 0, st, q, k, v, dout,
+                         kvalid, qt, H, N, nkeys_total, m, sl2, scale, dq);
+    else
+      hipLaunchKernelGGL((dense_bwd_q_dma_kernel<HD, QB, BALL, ADD, true>), grid, dim3(256), 0, st, q, k, v, dout,
+                         kvalid, qt, H, N, nkeys_total, m, sl2, scale, dq);
+  }
   else
     hipLaunchKernelGGL((dense_bwd_q_kernel<T, HD, QB, BALL, ADD>), grid, dim3(256), 0, st, q, k, v, dout, kvalid, qt,
                        H, N, nkeys_total, m, sl2, scale, dq);
@@ -1198,9 +1210,14 @@ template <typename T, int HD, int NW, bool BALL>
 void launch_bwd_kv(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v, const T* dout,
                    const uint8_t* kvalid, QTerms qt, int H, int N, int nkeys_total, int m, int nchunks, float sl2,
                    float scale, float* dk, float* dv) {
-  if constexpr (sizeof(T) == 2)
-    hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL>), grid, dim3(NW * 64), 0, st, q, k, v, dout, kvalid,
-                       qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
+  if constexpr (sizeof(T) == 2) {
+    if (kvalid == nullptr && nkeys_total % (NW * 32) == 0)
+      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, false>), grid, dim3(NW * 64), 0, st, q, k, v, dout,
+                         kvalid, qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
+    else
+      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, true>), grid, dim3(NW * 64), 0, st, q, k, v, dout,
+                         kvalid, qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
+  }
   else
     hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, NW, BALL>), grid, dim3(NW * 64), 0, st, q, k, v, dout, kvalid, qt,
                        H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
@@ -1411,7 +1428,7 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_dma_kernel(const bf16_t* q, co
     float cl[4], cg[4], cdv[4];
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
-      const float4 t = ts[4 * j + ii];                  // log2 LSE, s, s R
+      const float4 t = ts[4 * j + ii];                  // log2 LSE - log2 s, s, R
       cl[ii] = live && 4 * j + ii < qrows ? t.x : __builtin_huge_valf();
       cg[ii] = t.y;
       cdv[ii] = t.z;
@@ -1434,8 +1451,8 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_dma_kernel(const bf16_t* q, co
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
         const float pr = kok[kb] ? fast_exp2(__builtin_fmaf(sv[ii], sl2, -cl[ii])) : 0.f;
-        pg[ii] = pr * cg[ii];
-        dsv[ii] = pr * __builtin_fmaf(dp[ii], cg[ii], -cdv[ii]);
+        pg[ii] = pr;
+        dsv[ii] = pr * (dp[ii] - cdv[ii]);
       }
 #pragma unroll
       for (int db = 0; db < DB; ++db) {

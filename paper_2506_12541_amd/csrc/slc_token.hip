@@ -340,8 +340,8 @@ __global__ void __launch_bounds__(256) slc1_bwd_kernel(const bf16_t* q, const bf
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float pr = kok[kb] ? fast_exp2(__builtin_fmaf(sv[i], sl2, -cl[i])) : 0.f;
-        pg[i] = pr * cg[i];
-        dsv[i] = pr * __builtin_fmaf(dp[i], cg[i], -cdv[i]);
+        pg[i] = pr;
+        dsv[i] = pr * (dp[i] - cdv[i]);
         ps[(4 * j + i) * LS + 16 * kb + r] = f2bf(dsv[i]);
       }
 #pragma unroll
