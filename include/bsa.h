@@ -185,6 +185,11 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
  * Host-side bookkeeping only; no device memory is allocated. */
 bsa_status_t bsa_timing_enable(int32_t on);
 
+/* Restrict the recording to the comma-separated phase names in `phases` (NULL or "" =
+ * every phase), so that a measured region carries the events of the phases it reports
+ * and no others. Host-side bookkeeping only. */
+bsa_status_t bsa_timing_select(const char* phases);
+
 /* Sum of the recorded durations of `phase` (milliseconds) and the number of records;
  * waits for the recorded events to complete. */
 bsa_status_t bsa_timing_query(const char* phase, double* total_ms, int32_t* count);

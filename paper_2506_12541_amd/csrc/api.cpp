@@ -252,6 +252,12 @@ bsa_status_t bsa_timing_enable(int32_t on) {
   return BSA_OK;
 }
 
+bsa_status_t bsa_timing_select(const char* phases) {
+  g_last_error.clear();
+  bsa::timing_select(phases);
+  return BSA_OK;
+}
+
 bsa_status_t bsa_timing_query(const char* phase, double* total_ms, int32_t* count) {
   g_last_error.clear();
   if (!phase || !total_ms || !count) return fail(BSA_ERR_INVALID_ARGUMENT, "phase, total_ms and count must be non-NULL");

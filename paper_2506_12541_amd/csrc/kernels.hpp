@@ -141,6 +141,7 @@ hipError_t launch_radix_sort_pairs(uint32_t* keys, uint32_t* vals, uint32_t* key
 // timing.cpp: optional per-phase HIP-event timing (see bsa_timing_enable in bsa.h)
 bool timing_on();
 void timing_set(bool on);
+void timing_select(const char* phases);
 int timing_begin(const char* name, hipStream_t st);
 void timing_end(int id, hipStream_t st);
 hipError_t timing_query(const char* name, double* total_ms, int* count);

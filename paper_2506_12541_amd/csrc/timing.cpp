@@ -19,6 +19,7 @@ struct Record {
 
 std::mutex g_mu;
 bool g_on = false;
+std::vector<std::string> g_only;   // phases recorded while on; empty = every phase
 std::vector<Record> g_records;
 std::vector<hipEvent_t> g_free;
 
@@ -40,6 +41,22 @@ bool timing_on() {
   return g_on;
 }
 
+void timing_select(const char* phases) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_only.clear();
+  if (!phases) return;
+  std::string cur;
+  for (const char* c = phases;; ++c) {
+    if (*c == ',' || *c == '\0') {
+      if (!cur.empty()) g_only.push_back(cur);
+      cur.clear();
+      if (*c == '\0') break;
+    } else {
+      cur += *c;
+    }
+  }
+}
+
 void timing_set(bool on) {
   std::lock_guard<std::mutex> lk(g_mu);
   for (auto& r : g_records) {
@@ -54,6 +71,11 @@ void timing_set(bool on) {
 int timing_begin(const char* name, hipStream_t st) {
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_on) return -1;
+  if (!g_only.empty()) {
+    bool hit = false;
+    for (const auto& p : g_only) hit = hit || p == name;
+    if (!hit) return -1;
+  }
   Record r{name, take_event(), take_event()};
   if (!r.start || !r.stop) return -1;
   hipEventRecord(r.start, st);
