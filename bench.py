@@ -194,6 +194,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--variant", choices=sorted(VARIANTS), default="bsa")
+    ap.add_argument("--sweep", action="store_true",
+                    help="sequence-length sweep: BSA layer vs full attention (one JSON line per length)")
     ap.add_argument("--cpu-baseline", type=int, default=1, help="time the float64 oracle on a sample (0 = skip)")
     ap.add_argument("--copy-calibration", action="store_true", help="run only the 1 GiB plain copy")
     ap.add_argument("--summarize-traffic", nargs=4, metavar="CSV",
@@ -237,8 +239,85 @@ def cpu_baseline(cfg, pts_np, inp_np, variant="bsa"):
                       f"1 of {cfg.heads} heads ({t_head:.2f} s), scaled x{cfg.heads}; float64 numpy"}
 
 
+def sweep(args):
+    """Layer runtime against sequence length, BSA vs full attention (the shape of the
+    paper's Fig. 2, here for one layer rather than the 18-block model).
+
+    Each length N runs the 65536-point workload's layer settings on one N-point Gaussian
+    mixture cloud (H=8, d=64, bf16). BSA: forward + backward of the layer on rows already
+    in ball order, timed with host clocks over the steps (both streams). Full attention:
+    the same ball-attention kernels with one ball of N tokens (Eq. 3 with m = N is softmax
+    attention over every key), forward + backward, taken from their phase events with the
+    library on one stream so nothing overlaps them."""
+    import numpy as np
+    import torch
+
+    from paper_2506_12541_amd import _lib
+    from paper_2506_12541_amd import bsa as gb
+    from workloads import Config, make_inputs
+
+    lib = _lib.load()
+    dev = torch.device("cuda:0")
+    for n in (1024, 2048, 4096, 8192, 16384, 32768, 65536):
+        cfg = Config(f"sweep_{n}", 1, n, n, 8, 64, "bf16", 256, 16, 16, 32, 16, 16, "gmm", "fwdbwd")
+        inp = make_inputs(cfg, seed=3, layout="ball", with_grad=True)
+        t = lambda a, d=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(d)
+        q, k, v, do = (t(inp[x], torch.bfloat16) for x in ("q", "k", "v", "do"))
+        gate = t(inp["gate"])
+        phk = {w: t(a) for w, a in inp["phi_k"].items()}
+        phv = {w: t(a) for w, a in inp["phi_v"].items()}
+
+        def run(p, saved, steps):
+            for _ in range(steps):
+                o, sv = gb.forward(p, q, k, v, None, gate, phk, phv, saved=saved)
+                gb.backward(p, q, k, v, None, gate, phk, phv, sv, do)
+
+        p = gb.Params.from_config(cfg)
+        saved = gb.Saved(p, dev)
+        run(p, saved, 3)
+        torch.cuda.synchronize()
+        steps = max(5, min(50, (1 << 21) // n))
+        t0 = time.perf_counter()
+        run(p, saved, steps)
+        torch.cuda.synchronize()
+        bsa_ms = (time.perf_counter() - t0) / steps * 1e3
+
+        pf = gb.Params.from_config(dataclasses.replace(cfg, ball=n))
+        saved_f = gb.Saved(pf, dev)
+        _lib.check(lib.bsa_set_streams(1), "streams")
+        run(pf, saved_f, 2)
+        torch.cuda.synchronize()
+        fsteps = max(3, min(20, (1 << 19) // n))
+        phases = ("fwd.ball", "bwd.dq_ball", "bwd.kv_ball")
+        lib.bsa_timing_select(",".join(phases).encode())
+        lib.bsa_timing_enable(1)
+        run(pf, saved_f, fsteps)
+        torch.cuda.synchronize()
+        full_ms = 0.0
+        for name in phases:
+            tot, cnt = _lib.C.c_double(), _lib.C.c_int32()
+            _lib.check(lib.bsa_timing_query(name.encode(), _lib.C.byref(tot), _lib.C.byref(cnt)), "timing")
+            full_ms += tot.value / fsteps
+        lib.bsa_timing_enable(0)
+        lib.bsa_timing_select(None)
+        _lib.check(lib.bsa_set_streams(2), "streams")
+        fwd_f, bwd_f = algorithmic_flops(cfg)
+        full_flop = 3.5 * 4.0 * n * n * cfg.head_dim * cfg.heads   # forward 4 N^2 d + backward 2.5x
+        print(json.dumps({"n": n, "bsa_layer_ms": round(bsa_ms, 4), "full_attention_ms": round(full_ms, 4),
+                          "full_over_bsa": round(full_ms / bsa_ms, 3),
+                          "bsa_tflops": round((sum(fwd_f.values()) + sum(bwd_f.values())) / bsa_ms / 1e9, 1),
+                          "full_tflops": round(full_flop / full_ms / 1e9, 1),
+                          "workload": "1 cloud, H=8, d=64, bf16, ball 256, cmp 16, slc 32, top-16, group 16; "
+                                      "forward + backward of the layer"}), flush=True)
+        del saved, saved_f
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
+    if args.sweep:
+        sweep(args)
+        return
     if args.summarize_traffic:
         summarize_traffic(args)
         return

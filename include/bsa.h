@@ -16,7 +16,8 @@
  *    for that device and keeps them until the process ends. Work on the auxiliary stream
  *    starts after an event recorded on `stream` and is joined back into `stream` before
  *    the call returns, so `stream` alone orders the call against the caller's other work.
- *    Calls from several threads are serialised while they enqueue.
+ *    Calls from several threads are serialised while they enqueue. bsa_set_streams(1)
+ *    runs every branch on `stream` instead.
  *  - The library never allocates device memory and keeps no pointer after a call
  *    returns. The caller owns every buffer; sizes come from bsa_sizes() and
  *    bsa_ball_tree_workspace_bytes().
@@ -174,6 +175,11 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
                           const void* d_o, float* dq, float* dk, float* dv, float* dgate,
                           const bsa_mlp_grad_t* dphi_k, const bsa_mlp_grad_t* dphi_v,
                           const bsa_mlp_grad_t* dphi_q, void* ws, size_t ws_bytes, void* stream);
+
+/* Streams used by bsa_forward and bsa_backward: 2 (default) = the caller's stream plus
+ * the auxiliary stream, 1 = the caller's stream only (branches run one after another,
+ * e.g. to time each alone). Process-wide; BSA_ERR_INVALID_ARGUMENT for other values. */
+bsa_status_t bsa_set_streams(int32_t n);
 
 /* ---- Measurement support (not part of the layer's computation) ---- */
 

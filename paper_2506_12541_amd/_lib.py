@@ -47,6 +47,7 @@ _SIGS = {
     "bsa_last_error": (C.c_char_p, []),
     "bsa_timing_enable": (C.c_int, [C.c_int32]),
     "bsa_timing_select": (C.c_int, [C.c_char_p]),
+    "bsa_set_streams": (C.c_int, [C.c_int32]),
     "bsa_timing_query": (C.c_int, [C.c_char_p, C.POINTER(C.c_double), C.POINTER(C.c_int32)]),
     "bsa_ball_tree_workspace_bytes": (C.c_size_t, [C.c_int64, C.c_int64, C.c_int32, C.c_int32]),
     "bsa_build_ball_tree": (C.c_int, [C.c_void_p, C.c_int64, C.c_int32, C.c_int64, C.c_int32, C.c_void_p,

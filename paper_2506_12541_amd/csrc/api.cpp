@@ -368,6 +368,7 @@ struct Aux {
 };
 std::mutex g_aux_mu;
 std::map<int, Aux> g_aux;
+int g_streams = 2;   // 1: every branch on the caller's stream (bsa_set_streams)
 
 static bsa_status_t get_aux(Aux* out) {
   int dev = 0;
@@ -386,8 +387,17 @@ static bsa_status_t get_aux(Aux* out) {
 }
 
 static bsa_status_t join_aux(const Aux& a, hipStream_t st) {
+  if (a.s == st) return BSA_OK;
   if (hipEventRecord(a.join, a.s) != hipSuccess || hipStreamWaitEvent(st, a.join, 0) != hipSuccess)
     return fail(BSA_ERR_HIP, "joining the auxiliary stream failed");
+  return BSA_OK;
+}
+
+bsa_status_t bsa_set_streams(int32_t n) {
+  g_last_error.clear();
+  if (n != 1 && n != 2) return fail(BSA_ERR_INVALID_ARGUMENT, "streams must be 1 or 2");
+  std::lock_guard<std::mutex> lock(g_aux_mu);
+  g_streams = n;
   return BSA_OK;
 }
 
@@ -419,6 +429,7 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   Aux aux;
   s = get_aux(&aux);
   if (s != BSA_OK) return s;
+  if (g_streams == 1) aux.s = st;
   char* w = (char*)ws;
   const size_t rows = (size_t)D.rows();
   char* ob = (char*)saved->o_branch;
@@ -450,7 +461,8 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
     BSA_STEP("fwd.compress", bsa::launch_compress_fwd(Dq, q, valid, mq, saved->qcmp, saved->hid_q, qc_lp, w + W.w1t_q, st),
              "query coarsening");
   // ball and compressed attention on the auxiliary stream, selection on the caller's
-  if (hipEventRecord(aux.fork, st) != hipSuccess || hipStreamWaitEvent(aux.s, aux.fork, 0) != hipSuccess)
+  if (aux.s != st &&
+      (hipEventRecord(aux.fork, st) != hipSuccess || hipStreamWaitEvent(aux.s, aux.fork, 0) != hipSuccess))
     return fail(BSA_ERR_HIP, "forking the auxiliary stream failed");
   {
     hipStream_t st_main = st;
@@ -519,6 +531,7 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   Aux aux;
   s = get_aux(&aux);
   if (s != BSA_OK) return s;
+  if (g_streams == 1) aux.s = st;
   char* w = (char*)ws;
   bsa::BwdArgs A{};
   A.q = q; A.k = k; A.v = v; A.dout = d_o; A.valid = valid; A.gate = gate;
