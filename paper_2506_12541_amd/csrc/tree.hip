@@ -8,7 +8,7 @@
 // is free to use any partition that preserves them.
 //
 // GPU plan. The three per-axis orderings of every cloud are produced once by a stable
-// LSD radix sort (4-bit digits). Each node then keeps, for every axis, its points
+// LSD radix sort (8-bit digits). Each node then keeps, for every axis, its points
 // sorted on that axis, stored at the node's own slot range. A split reads the extremes
 // of each axis at the ends of the lists and the median at position ceil(n/2)-1 of the
 // split axis; every list is then stably partitioned by "key <= median key", which keeps
@@ -24,6 +24,8 @@ namespace {
 constexpr int kSortThreads = 256;
 constexpr int kSortItems = 8;
 constexpr int kSortTile = kSortThreads * kSortItems;  // 2048 keys per workgroup
+constexpr int kRadix = 256;                           // 8-bit digits (one per thread)
+constexpr int kScanChunk = 8192;                      // counts scanned per workgroup
 constexpr int kPartTile = 2048;                       // slots per partition workgroup
 constexpr int kBottom = 1024;                         // node size finished in LDS
 
@@ -79,16 +81,19 @@ __global__ void __launch_bounds__(kSortThreads) sort_init_kernel(const float* pt
   vals[(size_t)a * m + i] = (uint32_t)i;
 }
 
+// 8-bit digits: passes 0-3 sort on the key, later passes on the cloud index (val / n_real).
 __device__ __forceinline__ uint32_t sort_digit(uint32_t key, uint32_t val, int pass, int n_real) {
-  return pass < 8 ? (key >> (4 * pass)) & 15u : ((val / (uint32_t)n_real) >> (4 * (pass - 8))) & 15u;
+  return pass < 4 ? (key >> (8 * pass)) & 255u : ((val / (uint32_t)n_real) >> (8 * (pass - 4))) & 255u;
 }
 
+// Digit counts of one tile (kSortTile items, item i of the tile at it * 256 + thread),
+// stored digit-major: hist[(a * 256 + d) * ntiles + tile].
 __global__ void __launch_bounds__(kSortThreads) sort_hist_kernel(const uint32_t* keys, const uint32_t* vals,
                                                                  int m, int pass, int n_real, int ntiles,
                                                                  uint32_t* hist) {
-  __shared__ uint32_t cnt[16];
+  __shared__ uint32_t cnt[kRadix];
   const int a = blockIdx.y, tile = blockIdx.x;
-  if (threadIdx.x < 16) cnt[threadIdx.x] = 0;
+  cnt[threadIdx.x] = 0;
   __syncthreads();
   const uint32_t* K = keys + (size_t)a * m;
   const uint32_t* V = vals + (size_t)a * m;
@@ -97,82 +102,104 @@ __global__ void __launch_bounds__(kSortThreads) sort_hist_kernel(const uint32_t*
     if (i < m) atomicAdd(&cnt[sort_digit(K[i], V[i], pass, n_real)], 1u);
   }
   __syncthreads();
-  if (threadIdx.x < 16) hist[((size_t)a * 16 + threadIdx.x) * ntiles + tile] = cnt[threadIdx.x];
+  hist[((size_t)a * kRadix + threadIdx.x) * ntiles + tile] = cnt[threadIdx.x];
 }
 
-// Exclusive scan of hist[a] in digit-major order; one 1024-thread workgroup per axis.
-__global__ void __launch_bounds__(1024) sort_scan_kernel(uint32_t* hist, int ntiles) {
+// Exclusive scan of the digit-major counts of each axis in chunks of kScanChunk entries:
+// each workgroup scans one chunk in place and leaves the chunk total in sums.
+__global__ void __launch_bounds__(1024) sort_scan_kernel(uint32_t* hist, int total, uint32_t* sums) {
   __shared__ int tmp[17];
-  uint32_t* H = hist + (size_t)blockIdx.y * 16 * ntiles;
-  const int total = 16 * ntiles;
-  const int per = (total + 1023) / 1024;
+  const int chunk = blockIdx.x, nchunks = gridDim.x;
+  uint32_t* H = hist + (size_t)blockIdx.y * total + (size_t)chunk * kScanChunk;
+  const int n = min(kScanChunk, total - chunk * kScanChunk);
+  constexpr int per = kScanChunk / 1024;
   const int s = threadIdx.x * per;
   int sum = 0;
-  for (int i = s; i < s + per && i < total; ++i) sum += (int)H[i];
-  int run = block_exclusive_scan(sum, tmp, nullptr);
-  for (int i = s; i < s + per && i < total; ++i) {
+  for (int i = s; i < s + per && i < n; ++i) sum += (int)H[i];
+  int all = 0;
+  int run = block_exclusive_scan(sum, tmp, &all);
+  for (int i = s; i < s + per && i < n; ++i) {
     int t = (int)H[i];
     H[i] = (uint32_t)run;
     run += t;
   }
+  // a single chunk is already the whole scan: its offset is 0 (no chunk-total pass runs)
+  if (threadIdx.x == 0) sums[(size_t)blockIdx.y * nchunks + chunk] = nchunks == 1 ? 0u : (uint32_t)all;
 }
 
+// Exclusive scan of the chunk totals of each axis (one workgroup per axis).
+__global__ void __launch_bounds__(1024) sort_scan_sums_kernel(uint32_t* sums, int nchunks) {
+  __shared__ int tmp[17];
+  uint32_t* S = sums + (size_t)blockIdx.y * nchunks;
+  const int per = (nchunks + 1023) / 1024;
+  const int s = threadIdx.x * per;
+  int sum = 0;
+  for (int i = s; i < s + per && i < nchunks; ++i) sum += (int)S[i];
+  int run = block_exclusive_scan(sum, tmp, nullptr);
+  for (int i = s; i < s + per && i < nchunks; ++i) {
+    int t = (int)S[i];
+    S[i] = (uint32_t)run;
+    run += t;
+  }
+}
+
+// Stable scatter of one tile. Items are taken in index order, 256 per round: within a
+// round, an item's rank among equal digits comes from eight ballots (lanes of its wave
+// with the same digit and a lower lane id) plus the counts of the lower waves and of the
+// earlier rounds, all kept per digit in LDS.
 __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(const uint32_t* keys, const uint32_t* vals,
                                                                     uint32_t* keys_out, uint32_t* vals_out,
                                                                     int m, int pass, int n_real, int ntiles,
-                                                                    const uint32_t* hist) {
-  __shared__ int cnt[16 * kSortThreads];  // digit-major: cnt[d * 256 + thread]
-  __shared__ int tmp[8];
+                                                                    const uint32_t* hist, const uint32_t* sums,
+                                                                    int nchunks) {
+  __shared__ uint32_t run[kRadix];            // items of each digit in earlier rounds
+  __shared__ uint32_t base[kRadix];           // output start of each digit for this tile
+  __shared__ uint32_t wc[kSortThreads / 64][kRadix];   // this round's count per wave and digit
   const int a = blockIdx.y, tile = blockIdx.x, t = threadIdx.x;
+  const int lane = t & 63, wid = t >> 6;
   const uint32_t* K = keys + (size_t)a * m;
   const uint32_t* V = vals + (size_t)a * m;
-  uint32_t k[kSortItems], v[kSortItems];
-  int dg[kSortItems];
-  int mine[16];
-#pragma unroll
-  for (int d = 0; d < 16; ++d) mine[d] = 0;
-  const int base_i = tile * kSortTile + t * kSortItems;  // consecutive items per thread
-#pragma unroll
-  for (int it = 0; it < kSortItems; ++it) {
-    int i = base_i + it;
-    dg[it] = -1;
-    if (i < m) {
-      k[it] = K[i];
-      v[it] = V[i];
-      dg[it] = (int)sort_digit(k[it], v[it], pass, n_real);
-#pragma unroll
-      for (int d = 0; d < 16; ++d) mine[d] += (dg[it] == d);
-    }
+  {
+    const size_t e = (size_t)t * ntiles + tile;   // digit-major entry of (digit t, this tile)
+    base[t] = hist[(size_t)a * kRadix * ntiles + e] + sums[(size_t)a * nchunks + e / kScanChunk];
+    run[t] = 0;
   }
-#pragma unroll
-  for (int d = 0; d < 16; ++d) cnt[d * kSortThreads + t] = mine[d];
-  __syncthreads();
-  // scan 4096 digit-major entries: thread t owns entries [16t, 16t+16)
-  int loc[16];
-  int sum = 0;
-#pragma unroll
-  for (int e = 0; e < 16; ++e) { loc[e] = cnt[16 * t + e]; sum += loc[e]; }
-  int run = block_exclusive_scan(sum, tmp, nullptr);
-#pragma unroll
-  for (int e = 0; e < 16; ++e) { int x = loc[e]; cnt[16 * t + e] = run; run += x; }
-  __syncthreads();
-  // digit offsets within the tile: entry (d, thread 0) holds the start of digit d
-  int pos[16];
-  const uint32_t* H = hist + (size_t)a * 16 * ntiles;
-#pragma unroll
-  for (int d = 0; d < 16; ++d)
-    pos[d] = (int)H[(size_t)d * ntiles + tile] + cnt[d * kSortThreads + t] - cnt[d * kSortThreads];
+  const uint64_t below = (1ull << lane) - 1ull;
   uint32_t* KO = keys_out + (size_t)a * m;
   uint32_t* VO = vals_out + (size_t)a * m;
-#pragma unroll
   for (int it = 0; it < kSortItems; ++it) {
-    if (dg[it] < 0) continue;
-    int p = 0;
+    const int i = tile * kSortTile + it * kSortThreads + t;
+    const bool ok = i < m;
+    uint32_t k = 0, v = 0, d = 0;
+    if (ok) {
+      k = K[i];
+      v = V[i];
+      d = sort_digit(k, v, pass, n_real);
+    }
 #pragma unroll
-    for (int d = 0; d < 16; ++d)
-      if (dg[it] == d) p = pos[d]++;
-    KO[p] = k[it];
-    VO[p] = v[it];
+    for (int w = 0; w < kSortThreads / 64; ++w) wc[w][t] = 0;
+    uint64_t peers = __builtin_amdgcn_ballot_w64(ok);
+#pragma unroll
+    for (int bit = 0; bit < 8; ++bit) {
+      const bool on = (d >> bit) & 1u;
+      const uint64_t bb = __builtin_amdgcn_ballot_w64(on);
+      peers &= on ? bb : ~bb;
+    }
+    const uint32_t rank = (uint32_t)__builtin_popcountll(peers & below);
+    __syncthreads();   // wc cleared; run and base written
+    if (ok && rank == 0) wc[wid][d] = (uint32_t)__builtin_popcountll(peers);
+    __syncthreads();
+    if (ok) {
+      uint32_t off = base[d] + run[d] + rank;
+      for (int w = 0; w < wid; ++w) off += wc[w][d];
+      KO[off] = k;
+      VO[off] = v;
+    }
+    __syncthreads();   // every item of the round has read run
+    uint32_t add = 0;
+#pragma unroll
+    for (int w = 0; w < kSortThreads / 64; ++w) add += wc[w][t];
+    run[t] += add;
   }
 }
 
@@ -493,7 +520,8 @@ size_t tree_workspace_bytes(int64_t n_real, int64_t n_pad, int batch) {
   add(4 * 3 * m);          // keys b
   add(4 * 3 * m);          // vals a
   add(4 * 3 * m);          // vals b
-  add(4 * 3 * 16 * ntiles);  // histograms
+  add(4 * 3 * (size_t)kRadix * ntiles);   // digit counts
+  add(4 * 3 * ((kRadix * ntiles + kScanChunk - 1) / kScanChunk));   // chunk totals
   add(4 * 3 * slots);      // lists a
   add(4 * 3 * slots);      // lists b
   add(sizeof(NodeSplit) * (slots / 2 + 1));
@@ -512,7 +540,9 @@ hipError_t launch_build_tree(const float* pts, int64_t n_real, int dim, int64_t 
   uint32_t* kb = (uint32_t*)take(4 * 3 * m);
   uint32_t* va = (uint32_t*)take(4 * 3 * m);
   uint32_t* vb = (uint32_t*)take(4 * 3 * m);
-  uint32_t* hist = (uint32_t*)take(4 * 3 * 16 * (size_t)ntiles);
+  uint32_t* hist = (uint32_t*)take(4 * 3 * (size_t)kRadix * ntiles);
+  const int nchunks = (kRadix * ntiles + kScanChunk - 1) / kScanChunk;
+  uint32_t* sums = (uint32_t*)take(4 * 3 * (size_t)nchunks);
   int* la = (int*)take(4 * 3 * slots);
   int* lb = (int*)take(4 * 3 * slots);
   NodeSplit* splits = (NodeSplit*)take(sizeof(NodeSplit) * (slots / 2 + 1));
@@ -520,14 +550,15 @@ hipError_t launch_build_tree(const float* pts, int64_t n_real, int dim, int64_t 
 
   hipLaunchKernelGGL(sort_init_kernel, dim3((unsigned)((m + 255) / 256), 3), dim3(256), 0, st, pts, dim,
                      (int)m, ka, va);
-  int passes = 8;
-  for (int bits = 0; (1 << bits) < batch; bits += 4) ++passes;
+  int passes = 4;
+  for (int bits = 0; (1 << bits) < batch; bits += 8) ++passes;
   for (int pass = 0; pass < passes; ++pass) {
     hipLaunchKernelGGL(sort_hist_kernel, dim3(ntiles, 3), dim3(kSortThreads), 0, st, ka, va, (int)m, pass,
                        (int)n_real, ntiles, hist);
-    hipLaunchKernelGGL(sort_scan_kernel, dim3(1, 3), dim3(1024), 0, st, hist, ntiles);
+    hipLaunchKernelGGL(sort_scan_kernel, dim3(nchunks, 3), dim3(1024), 0, st, hist, kRadix * ntiles, sums);
+    if (nchunks > 1) hipLaunchKernelGGL(sort_scan_sums_kernel, dim3(1, 3), dim3(1024), 0, st, sums, nchunks);
     hipLaunchKernelGGL(sort_scatter_kernel, dim3(ntiles, 3), dim3(kSortThreads), 0, st, ka, va, kb, vb,
-                       (int)m, pass, (int)n_real, ntiles, hist);
+                       (int)m, pass, (int)n_real, ntiles, hist, sums, nchunks);
     std::swap(ka, kb);
     std::swap(va, vb);
   }
@@ -552,20 +583,26 @@ hipError_t launch_build_tree(const float* pts, int64_t n_real, int dim, int64_t 
   return hipGetLastError();
 }
 
-size_t radix_sort_hist_words(long long n) { return (size_t)16 * ((n + kSortTile - 1) / kSortTile); }
+size_t radix_sort_hist_words(long long n) {
+  const size_t ntiles = (size_t)((n + kSortTile - 1) / kSortTile);
+  return (size_t)kRadix * ntiles + (kRadix * ntiles + kScanChunk - 1) / kScanChunk;   // counts + chunk totals
+}
 
 hipError_t launch_radix_sort_pairs(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
                                    uint32_t* hist, long long n, int bits, uint32_t** keys_out, uint32_t** vals_out,
                                    hipStream_t st) {
   const int ntiles = (int)((n + kSortTile - 1) / kSortTile);
-  const int passes = (bits + 3) / 4;  // key digits only (pass < 8)
+  const int nchunks = (kRadix * ntiles + kScanChunk - 1) / kScanChunk;
+  uint32_t* sums = hist + (size_t)kRadix * ntiles;
+  const int passes = (bits + 7) / 8;  // key digits only (pass < 4)
   uint32_t *ka = keys, *va = vals, *kb = keys_tmp, *vb = vals_tmp;
   for (int pass = 0; pass < passes; ++pass) {
     hipLaunchKernelGGL(sort_hist_kernel, dim3(ntiles, 1), dim3(kSortThreads), 0, st, ka, va, (int)n, pass, 1, ntiles,
                        hist);
-    hipLaunchKernelGGL(sort_scan_kernel, dim3(1, 1), dim3(1024), 0, st, hist, ntiles);
+    hipLaunchKernelGGL(sort_scan_kernel, dim3(nchunks, 1), dim3(1024), 0, st, hist, kRadix * ntiles, sums);
+    if (nchunks > 1) hipLaunchKernelGGL(sort_scan_sums_kernel, dim3(1, 1), dim3(1024), 0, st, sums, nchunks);
     hipLaunchKernelGGL(sort_scatter_kernel, dim3(ntiles, 1), dim3(kSortThreads), 0, st, ka, va, kb, vb, (int)n, pass,
-                       1, ntiles, hist);
+                       1, ntiles, hist, sums, nchunks);
     std::swap(ka, kb);
     std::swap(va, vb);
   }

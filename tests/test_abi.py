@@ -132,3 +132,9 @@ def test_tree_argument_errors(lib):
     assert lib.bsa_build_ball_tree(fake, 10, 4, 16, 1, fake, fake, 1 << 20, None) == _lib.BSA_ERR_UNSUPPORTED
     assert lib.bsa_build_ball_tree(fake, 20, 3, 16, 1, fake, fake, 1 << 20, None) == _lib.BSA_ERR_INVALID_ARGUMENT
     assert lib.bsa_build_ball_tree(fake, 10, 3, 16, 1, fake, fake, 1, None) == _lib.BSA_ERR_WORKSPACE_TOO_SMALL
+
+
+def test_set_streams_validates(lib):
+    assert lib.bsa_set_streams(3) == _lib.BSA_ERR_INVALID_ARGUMENT
+    assert lib.bsa_set_streams(0) == _lib.BSA_ERR_INVALID_ARGUMENT
+    assert lib.bsa_set_streams(2) == _lib.BSA_OK

@@ -120,3 +120,26 @@ def test_backward_scaling_one_head():
     errs = {n: max_abs(grads[n][:, h:h + 1].cpu().numpy(), ref[n]) for n in ("dq", "dk", "dv")}
     print({k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
     assert all(e < TOL[cfg.dtype] for e in errs.values()), errs
+
+
+def test_one_stream_equals_two_streams():
+    """Every kernel is deterministic and the two-stream schedule only reorders independent
+    branches, so one-stream and two-stream runs give bit-identical results."""
+    cfg = Config("small_bf16", 2, 900, 1024, 2, 64, "bf16", 128, 16, 16, 32, 4, 16, "uniform", "fwdbwd")
+    from paper_2506_12541_amd import _lib
+    lib = _lib.load()
+    inp = make_inputs(cfg, 11, layout="ball", with_grad=True)
+    valid = valid_from_tree(cfg)
+    outs = []
+    try:
+        for n in (2, 1):
+            _lib.check(lib.bsa_set_streams(n), "streams")
+            g, (p, q, k, v, vd, gate, phi_k, phi_v, saved, o, phi_q) = gpu_forward(cfg, inp, valid)
+            grads = gb.backward(p, q, k, v, vd, gate, phi_k, phi_v, saved, to_dev(inp["do"], p.torch_dtype))
+            torch.cuda.synchronize()
+            outs.append((o.clone(), {n_: grads[n_].clone() for n_ in ("dq", "dk", "dv", "dgate")}))
+    finally:
+        lib.bsa_set_streams(2)
+    assert torch.equal(outs[0][0], outs[1][0])
+    for n_ in ("dq", "dk", "dv", "dgate"):
+        assert torch.equal(outs[0][1][n_], outs[1][1][n_]), n_
