@@ -1311,8 +1311,11 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t
                                           D.N, D.m, sl2, D.scale, A.dq);
   });
   BSA_PHASE("bwd.dq_cmp", st, {
-  if (!D.gcmp)
+  if (!D.gcmp && D.N % 128 == 0)
     (launch_bwd_q<T, HD, 2, false, true>)(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, dout,
+                                          A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq);
+  else if (!D.gcmp)   // 64 token slots
+    (launch_bwd_q<T, HD, 1, false, true>)(dim3(D.N / 64, D.H, D.B), st, q, kc, vc, dout,
                                           A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq);
   else if (nct % 128 == 0)   // gradient of the coarse queries (written); the caller maps it to dQ
     (launch_bwd_q<T, HD, 2, false, false>)(dim3(nct / 128, D.H, D.B), st, qcl, kc, vc, docl,

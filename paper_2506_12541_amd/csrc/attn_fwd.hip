@@ -392,8 +392,12 @@ template <typename T, int HD>
 hipError_t cmp_impl(const Dims& D, const void* q, const void* kc, const void* vc, const uint8_t* valid,
                     const uint8_t* cvalid, void* o, float* lse, hipStream_t st) {
   const float sl2 = D.scale * kLog2e;
-  launch_dense_fwd<T, HD, 2, false>(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, valid, cvalid, D.H, D.N, D.N / D.l, D.m,
-                                    sl2, o, lse);
+  if (D.N % 128 == 0)
+    launch_dense_fwd<T, HD, 2, false>(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, valid, cvalid, D.H, D.N, D.N / D.l,
+                                      D.m, sl2, o, lse);
+  else   // 64 token slots: one 64-query workgroup per head
+    launch_dense_fwd<T, HD, 1, false>(dim3(D.N / 64, D.H, D.B), st, q, kc, vc, valid, cvalid, D.H, D.N, D.N / D.l,
+                                      D.m, sl2, o, lse);
   return hipGetLastError();
 }
 
