@@ -113,11 +113,23 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
   uint64_t lst[K];
 #pragma unroll
   for (int t = 0; t < K; ++t) lst[t] = 0;
+  // The group's four lanes each keep a list; the group needs only its k* best (k* <= K).
+  // Each lane's K/4 best are all at least the smallest of the four lanes' (K/4)-th keys,
+  // so the group already holds K >= k* keys at or above that value and no candidate below
+  // it can enter the final k*: the lanes filter on it as well as on their own K-th key.
 
   auto step = [&](int t0, const bf16_t* kt, const uint8_t* ct, bf16_t* kn, uint8_t* cn) {
     vm_drain();
     __syncthreads();
     if (t0 + KT < ntok) issue(t0 + KT, kn, cn);
+    uint64_t gthr = lst[K / 4 - 1];
+    {
+      const uint64_t o1 = shfl_xor_u64(gthr, 16);
+      gthr = o1 < gthr ? o1 : gthr;
+      const uint64_t o2 = shfl_xor_u64(gthr, 32);
+      gthr = o2 < gthr ? o2 : gthr;
+    }
+    const uint64_t thr = gthr > lst[K - 1] ? gthr : lst[K - 1];
     // the tile's candidates of this lane (4 / R per 16-token sub-tile), 0 = none
     constexpr int NCAND = (KT / 16) * (4 / R);
     uint64_t cand[NCAND];
@@ -161,7 +173,7 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
         const int blk = (t0 + tl + u * R) / R;
         ok = ok && any && !(mask_own && (blk * ls) / m == my_ball);
         const uint64_t key = make_key(sc, blk);
-        cand[st * (4 / R) + u] = ok && key > lst[K - 1] ? key : 0;
+        cand[st * (4 / R) + u] = ok && key > thr ? key : 0;
       }
     }
     // insert the qualifying candidates best first; the wave repeats only as many times as
