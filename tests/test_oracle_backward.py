@@ -29,19 +29,13 @@ def _inputs(seed, B=2, H=2, n=64, d=8, n_real=53, P=None):
                 gate=x(B, n, 3), phi_k=phi(), phi_v=phi(), phi_q=phi(), do=x(B, H, n, d))
 
 
-def _dense_torch(inp, sel):
-    """The layer as three dense masked softmaxes, differentiable by torch autograd."""
-    P = inp["P"]
-    t = lambda a: torch.tensor(a, dtype=torch.float64, requires_grad=True)
-    q, k, v, gate = t(inp["q"]), t(inp["k"]), t(inp["v"]), t(inp["gate"])
-    pk = {w: t(a) for w, a in inp["phi_k"].items()}
-    pv = {w: t(a) for w, a in inp["phi_v"].items()}
-    pq = {w: t(a) for w, a in inp["phi_q"].items()}
+def dense_layer_torch(q, k, v, valid, gate, pk, pv, pq, P, sel):
+    """The layer as three dense masked softmaxes on torch float64 tensors (differentiable):
+    q, k, v [B, H, N, d], valid [B, N] bool tensor, gate [B, N, 3], MLP weight dicts."""
     B, H, n, d = q.shape
-    valid = torch.from_numpy(inp["valid"])
     l, ls, g, m = P.cmp_block, P.slc_block, P.group, P.ball
     idx = torch.arange(n)
-    out = torch.zeros(B, H, n, d, dtype=torch.float64)
+    outs = []
 
     def masked_attn(qq, kk, vv, mask):
         s = qq @ kk.T / d ** 0.5
@@ -57,6 +51,7 @@ def _dense_torch(inp, sel):
     for b in range(B):
         vb = valid[b]
         qmask = vb[:, None]
+        heads = []
         for h in range(H):
             qq, kk, vv = q[b, h], k[b, h], v[b, h]
             ball_mask = (idx[:, None] // m == idx[None, :] // m) & vb[None, :] & qmask
@@ -86,9 +81,22 @@ def _dense_torch(inp, sel):
                         chosen[p, j] = True
             slc_mask = chosen[idx // g][:, idx // ls] & vb[None, :] & qmask
             sg = torch.sigmoid(gate[b])
-            out[b, h] = (sg[:, 0:1] * masked_attn(qq, kk, vv, ball_mask)
+            heads.append(sg[:, 0:1] * masked_attn(qq, kk, vv, ball_mask)
                          + sg[:, 1:2] * o_cmp
                          + sg[:, 2:3] * masked_attn(qq, kk, vv, slc_mask))
+        outs.append(torch.stack(heads))
+    return torch.stack(outs)
+
+
+def _dense_torch(inp, sel):
+    """The layer as three dense masked softmaxes, differentiable by torch autograd."""
+    P = inp["P"]
+    t = lambda a: torch.tensor(a, dtype=torch.float64, requires_grad=True)
+    q, k, v, gate = t(inp["q"]), t(inp["k"]), t(inp["v"]), t(inp["gate"])
+    pk = {w: t(a) for w, a in inp["phi_k"].items()}
+    pv = {w: t(a) for w, a in inp["phi_v"].items()}
+    pq = {w: t(a) for w, a in inp["phi_q"].items()}
+    out = dense_layer_torch(q, k, v, torch.from_numpy(inp["valid"]), gate, pk, pv, pq, P, sel)
     loss = (out * torch.from_numpy(inp["do"])).sum()
     loss.backward()
     g = lambda x: x.grad.numpy()
