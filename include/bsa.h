@@ -181,13 +181,91 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
  * e.g. to time each alone). Process-wide; BSA_ERR_INVALID_ARGUMENT for other values. */
 bsa_status_t bsa_set_streams(int32_t n);
 
+/* ---- The transformer block around the layer (Section 3.1) ----
+ *
+ * The paper's model stacks 18 blocks of RMSNorm, a BSA layer and a SwiGLU. One block, with
+ * C = heads * head_dim channels and F SwiGLU hidden units, on tokens x [B, N, C] float32 in
+ * ball order (padding rows zero):
+ *   h = x + merge(BSA(Q, K, V; gate)) W_o^T,   [Q | K | V] = RMSNorm_1(x) W_qkv^T,
+ *   gate = RMSNorm_1(x) W_g^T,   y = h + (silu(z W_1^T) * (z W_3^T)) W_2^T, z = RMSNorm_2(h),
+ * RMSNorm(t) = t / sqrt(mean(t^2) + 1e-6) * gain; maps are bias-free and stored [out, in]
+ * (head h of Q takes output columns h d .. h d + d - 1 of W_qkv, then K, then V).
+ * Precision: bf16 layers only. The channel products take bf16 operands (round to nearest
+ * even) and accumulate in float32; Q, K, V, the layer output, u = z W_1^T, w = z W_3^T
+ * and silu(u) w are stored in bf16; the residual stream, the norms and the gate logits
+ * (from the unrounded norm output and float32 W_g) are float32. In the backward pass the
+ * gradients entering a product (dy, du, dw, dh, dO, dQ/dK/dV) are rounded to bf16.
+ * Requirements beyond bsa_sizes: dtype BSA_BF16, C in {128, 256, 512, 1024}, F a positive
+ * multiple of 128 (BSA_ERR_UNSUPPORTED otherwise). */
+typedef struct {
+  const float *g1;      /* [C]     gain of RMSNorm_1                                    */
+  const float *wqkv;    /* [3C, C]                                                      */
+  const float *wg;      /* [3, C]  gate logits (ball, compression, selection)           */
+  const float *wo;      /* [C, C]                                                       */
+  const float *g2;      /* [C]     gain of RMSNorm_2                                    */
+  const float *w1, *w3; /* [F, C]                                                       */
+  const float *w2;      /* [C, F]                                                       */
+  bsa_mlp_t phi_k, phi_v, phi_q;  /* the layer's MLPs (phi_q read only for BSA_QC_MLP)  */
+} bsa_block_weights_t;
+
+/* Gradients of the weights (float32, same shapes, overwritten). phi_q: written only for
+ * BSA_QC_MLP with group compression (as in bsa_backward). */
+typedef struct {
+  float *g1, *wqkv, *wg, *wo, *g2, *w1, *w3, *w2;
+  bsa_mlp_grad_t phi_k, phi_v, phi_q;
+} bsa_block_grads_t;
+
+/* Tensors the block's forward pass saves for its backward pass (device, caller-owned;
+ * bsa_block_saved_view() carves them out of one buffer). M = B * N token rows. */
+typedef struct {
+  bsa_saved_t layer;    /* the layer's own saved tensors                               */
+  float* rstd1;         /* [M]        1 / rms of each row of x                          */
+  float* rstd2;         /* [M]        1 / rms of each row of h                          */
+  void* xn1;            /* [M, C]     bf16 RMSNorm_1(x)                                 */
+  float* gate;          /* [B, N, 3]  gate logits                                       */
+  void* q;              /* [B, H, N, d] bf16 (k, v likewise)                            */
+  void* k;
+  void* v;
+  void* o;              /* [B, H, N, d] bf16 layer output                               */
+  float* h;             /* [M, C]     residual stream after the attention sublayer      */
+  void* xn2;            /* [M, C]     bf16 RMSNorm_2(h)                                 */
+  void* uw;             /* [M, 2F]    bf16 u (columns 0..F-1) and w (F..2F-1)           */
+  void* a;              /* [M, F]     bf16 silu(u) w                                    */
+} bsa_block_saved_t;
+
+/* Validate and report the forward workspace, backward workspace and saved-buffer sizes of
+ * one block with F = ffn_dim. Any size pointer may be NULL. */
+bsa_status_t bsa_block_sizes(const bsa_params_t* p, int32_t ffn_dim, size_t* ws_fwd_bytes,
+                             size_t* ws_bwd_bytes, size_t* saved_bytes);
+
+/* Point the fields of *out into `base` (saved_bytes of bsa_block_sizes). Host-only. */
+bsa_status_t bsa_block_saved_view(const bsa_params_t* p, int32_t ffn_dim, void* base,
+                                  bsa_block_saved_t* out);
+
+/* Block forward: x [B, N, C] float32 -> y [B, N, C] float32 (y may not alias x). valid as
+ * in bsa_forward. ws: at least ws_fwd_bytes. Asynchronous on `stream` (the layer inside
+ * may also use the library's auxiliary stream, joined before return). */
+bsa_status_t bsa_block_forward(const bsa_params_t* p, int32_t ffn_dim, const bsa_block_weights_t* w,
+                               const float* x, const uint8_t* valid, float* y,
+                               const bsa_block_saved_t* saved, void* ws, size_t ws_bytes, void* stream);
+
+/* Block backward given dy = d(loss)/d(y) [B, N, C] float32: dx [B, N, C] float32 and the
+ * weight gradients (summed over tokens in a fixed order; no float atomics). x and saved as
+ * given to / filled by bsa_block_forward. ws: at least ws_bwd_bytes. */
+bsa_status_t bsa_block_backward(const bsa_params_t* p, int32_t ffn_dim, const bsa_block_weights_t* w,
+                                const float* x, const uint8_t* valid, const bsa_block_saved_t* saved,
+                                const float* dy, float* dx, const bsa_block_grads_t* dw, void* ws,
+                                size_t ws_bytes, void* stream);
+
 /* ---- Measurement support (not part of the layer's computation) ---- */
 
 /* on = 1: start recording, clearing earlier records; on = 0: stop and clear. While on,
  * every timed phase of the library records a start and a stop HIP event on the stream
  * its kernels are launched on (phases on the two streams of a call may overlap in time). Phases: "tree", "permute", "fwd.compress", "fwd.select",
  * "fwd.ball", "fwd.cmp", "fwd.slc", "fwd.gate", "bwd.gate", "bwd.dq_ball", "bwd.dq_cmp",
- * "bwd.dq_slc", "bwd.kv_ball", "bwd.kv_cmp", "bwd.mlp", "bwd.slc_csr", "bwd.slc_kv".
+ * "bwd.dq_slc", "bwd.kv_ball", "bwd.kv_cmp", "bwd.mlp", "bwd.slc_csr", "bwd.slc_kv", and
+ * for the block "blk.norm", "blk.gemm" (activation products), "blk.wgrad" (weight
+ * gradients), "blk.elem" (SwiGLU, casts, layout changes).
  * Host-side bookkeeping only; no device memory is allocated. */
 bsa_status_t bsa_timing_enable(int32_t on);
 

@@ -42,6 +42,21 @@ class bsa_saved_t(C.Structure):
     ]
 
 
+_BLOCK_W = ("g1", "wqkv", "wg", "wo", "g2", "w1", "w3", "w2")
+
+
+class bsa_block_weights_t(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in _BLOCK_W] + [("phi_k", bsa_mlp_t), ("phi_v", bsa_mlp_t), ("phi_q", bsa_mlp_t)]
+
+
+bsa_block_grads_t = bsa_block_weights_t
+
+
+class bsa_block_saved_t(C.Structure):
+    _fields_ = [("layer", bsa_saved_t)] + [(n, C.c_void_p) for n in (
+        "rstd1", "rstd2", "xn1", "gate", "q", "k", "v", "o", "h", "xn2", "uw", "a")]
+
+
 _SIGS = {
     "bsa_status_string": (C.c_char_p, [C.c_int]),
     "bsa_last_error": (C.c_char_p, []),
@@ -67,6 +82,16 @@ _SIGS = {
                                C.POINTER(bsa_saved_t), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                                C.POINTER(bsa_mlp_grad_t), C.POINTER(bsa_mlp_grad_t), C.POINTER(bsa_mlp_grad_t),
                                C.c_void_p, C.c_size_t, C.c_void_p]),
+    "bsa_block_sizes": (C.c_int, [C.POINTER(bsa_params_t), C.c_int32, C.POINTER(C.c_size_t),
+                                  C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)]),
+    "bsa_block_saved_view": (C.c_int, [C.POINTER(bsa_params_t), C.c_int32, C.c_void_p,
+                                       C.POINTER(bsa_block_saved_t)]),
+    "bsa_block_forward": (C.c_int, [C.POINTER(bsa_params_t), C.c_int32, C.POINTER(bsa_block_weights_t), C.c_void_p,
+                                    C.c_void_p, C.c_void_p, C.POINTER(bsa_block_saved_t), C.c_void_p, C.c_size_t,
+                                    C.c_void_p]),
+    "bsa_block_backward": (C.c_int, [C.POINTER(bsa_params_t), C.c_int32, C.POINTER(bsa_block_weights_t),
+                                     C.c_void_p, C.c_void_p, C.POINTER(bsa_block_saved_t), C.c_void_p, C.c_void_p,
+                                     C.POINTER(bsa_block_grads_t), C.c_void_p, C.c_size_t, C.c_void_p]),
 }
 
 _lib = None

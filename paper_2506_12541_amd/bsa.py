@@ -15,6 +15,7 @@ from . import _lib
 from ._lib import BSA_BF16, BSA_F32, BSA_POOL_MEAN, BSA_POOL_MLP, BSA_QC_MEAN, BSA_QC_MLP, check
 
 __all__ = ["Params", "Saved", "build_ball_tree", "permute", "unpermute", "sizes", "forward", "backward",
+           "block_sizes", "BlockSaved", "block_forward", "block_backward", "BLOCK_WEIGHTS",
            "BSA_F32", "BSA_BF16", "BSA_POOL_MLP", "BSA_POOL_MEAN", "BSA_QC_MEAN", "BSA_QC_MLP"]
 
 
@@ -235,4 +236,114 @@ def backward(p: Params, q, k, v, valid, gate, phi_k, phi_v, saved: Saved, d_o, s
                            C.byref(cgr[2]) if cgr[2] else None, _ptr(ws), ws_bytes, _stream(stream)),
           "bsa_backward")
     grads.update(dq=dq, dk=dk, dv=dv, dgate=dgate)
+    return grads
+
+
+# ---- the transformer block around the layer (bsa_block_* in include/bsa.h) ----
+
+BLOCK_WEIGHTS = _lib._BLOCK_W
+
+
+def block_sizes(p: Params, ffn: int):
+    """(forward workspace, backward workspace, saved) byte counts of one block."""
+    lib = _lib.load()
+    a, b, c = C.c_size_t(), C.c_size_t(), C.c_size_t()
+    cp = p.c()
+    check(lib.bsa_block_sizes(C.byref(cp), ffn, C.byref(a), C.byref(b), C.byref(c)), "bsa_block_sizes")
+    return a.value, b.value, c.value
+
+
+class BlockSaved:
+    """Tensors saved by block_forward(): one device buffer plus typed views of its parts."""
+
+    def __init__(self, p: Params, ffn: int, device):
+        lib = _lib.load()
+        _, _, nbytes = block_sizes(p, ffn)
+        self.p, self.ffn = p, ffn
+        self.buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        self.c = _lib.bsa_block_saved_t()
+        cp = p.c()
+        check(lib.bsa_block_saved_view(C.byref(cp), ffn, _ptr(self.buf), C.byref(self.c)), "bsa_block_saved_view")
+        base = self.buf.data_ptr()
+        B, H, N, d = p.batch, p.heads, p.n, p.head_dim
+        Cc = H * d
+
+        def view(ptr, dtype, shape):
+            off = ptr - base
+            esz = torch.empty((), dtype=dtype).element_size()
+            return self.buf[off:off + math.prod(shape) * esz].view(dtype).view(shape)
+
+        bf, f32 = torch.bfloat16, torch.float32
+        self.rstd1 = view(self.c.rstd1, f32, (B, N))
+        self.rstd2 = view(self.c.rstd2, f32, (B, N))
+        self.xn1 = view(self.c.xn1, bf, (B, N, Cc))
+        self.gate = view(self.c.gate, f32, (B, N, 3))
+        self.q, self.k, self.v, self.o = (view(getattr(self.c, n), bf, (B, H, N, d)) for n in ("q", "k", "v", "o"))
+        self.h = view(self.c.h, f32, (B, N, Cc))
+        self.xn2 = view(self.c.xn2, bf, (B, N, Cc))
+        self.uw = view(self.c.uw, bf, (B, N, 2 * ffn))
+        self.a = view(self.c.a, bf, (B, N, ffn))
+        self.sel_idx = view(self.c.layer.sel_idx, torch.int32, (B, H, N // p.group_size, p.topk))
+
+
+def _mlp_struct(phi):
+    return _mlp(phi) if phi else _lib.bsa_mlp_t()
+
+
+def _block_weights(p: Params, ffn: int, W, phi_k, phi_v, phi_q):
+    Cc = p.heads * p.head_dim
+    shapes = {"g1": (Cc,), "wqkv": (3 * Cc, Cc), "wg": (3, Cc), "wo": (Cc, Cc), "g2": (Cc,), "w1": (ffn, Cc),
+              "w3": (ffn, Cc), "w2": (Cc, ffn)}
+    for n in BLOCK_WEIGHTS:
+        _require(W[n], n, torch.float32, shapes[n])
+    return _lib.bsa_block_weights_t(*[W[n].data_ptr() for n in BLOCK_WEIGHTS], _mlp_struct(phi_k), _mlp_struct(phi_v),
+                                    _mlp_struct(phi_q))
+
+
+def block_forward(p: Params, ffn: int, W, phi_k, phi_v, x, valid=None, saved: BlockSaved | None = None, phi_q=None,
+                  stream=None):
+    """One block forward: x [B, N, C] float32 -> (y, saved). W: dict of float32 weights
+    (BLOCK_WEIGHTS); phi_*: the layer's MLPs."""
+    lib = _lib.load()
+    Cc = p.heads * p.head_dim
+    _require(x, "x", torch.float32, (p.batch, p.n, Cc))
+    if valid is not None:
+        _require(valid, "valid", torch.uint8, (p.batch, p.n))
+    cw = _block_weights(p, ffn, W, phi_k, phi_v, phi_q)
+    ws_bytes, _, _ = block_sizes(p, ffn)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=x.device)
+    saved = saved or BlockSaved(p, ffn, x.device)
+    y = torch.empty_like(x)
+    cp = p.c()
+    check(lib.bsa_block_forward(C.byref(cp), ffn, C.byref(cw), _ptr(x), _ptr(valid), _ptr(y), C.byref(saved.c),
+                                _ptr(ws), ws_bytes, _stream(stream)), "bsa_block_forward")
+    return y, saved
+
+
+def block_backward(p: Params, ffn: int, W, phi_k, phi_v, x, saved: BlockSaved, dy, valid=None, phi_q=None,
+                   stream=None):
+    """One block backward: returns dict(dx, dW: {name: grad}, dphi_k, dphi_v, dphi_q) (float32)."""
+    lib = _lib.load()
+    Cc = p.heads * p.head_dim
+    _require(x, "x", torch.float32, (p.batch, p.n, Cc))
+    _require(dy, "dy", torch.float32, (p.batch, p.n, Cc))
+    cw = _block_weights(p, ffn, W, phi_k, phi_v, phi_q)
+    dev = x.device
+    _, ws_bytes, _ = block_sizes(p, ffn)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    dW = {n: torch.empty_like(W[n]) for n in BLOCK_WEIGHTS}
+    grads = {}
+    structs = []
+    q_grad = p.group_compression and p.q_coarsen == BSA_QC_MLP
+    for name, phi, on in (("dphi_k", phi_k, p.kv_pool == BSA_POOL_MLP), ("dphi_v", phi_v, p.kv_pool == BSA_POOL_MLP),
+                          ("dphi_q", phi_q, q_grad)):
+        g = {w: torch.empty_like(phi[w]) for w in ("w1", "b1", "w2", "b2")} if on else {}
+        grads[name] = g
+        structs.append(_mlp_struct(g))
+    cg = _lib.bsa_block_grads_t(*[dW[n].data_ptr() for n in BLOCK_WEIGHTS], *structs)
+    dx = torch.empty_like(x)
+    cp = p.c()
+    check(lib.bsa_block_backward(C.byref(cp), ffn, C.byref(cw), _ptr(x), _ptr(valid), C.byref(saved.c), _ptr(dy),
+                                 _ptr(dx), C.byref(cg), _ptr(ws), ws_bytes, _stream(stream)), "bsa_block_backward")
+    grads.update(dx=dx, dW=dW)
     return grads

@@ -597,3 +597,363 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
 }
 
 }  // extern "C"
+
+// ---- the transformer block around the layer (Section 3.1) ----
+
+namespace {
+
+struct BlockDims {
+  bsa::Dims D;
+  int C, F;
+  long long M;   // token rows B * N
+};
+
+bsa_status_t check_block(const bsa_params_t* p, int32_t ffn, BlockDims* X) {
+  bsa_status_t s = check_params(p, &X->D);
+  if (s != BSA_OK) return s;
+  const bsa::Dims& D = X->D;
+  if (!D.bf16) return fail(BSA_ERR_UNSUPPORTED, "the block runs bf16 layers only");
+  X->C = D.H * D.d;
+  if (X->C != 128 && X->C != 256 && X->C != 512 && X->C != 1024)
+    return fail(BSA_ERR_UNSUPPORTED, "the block needs heads * head_dim in {128, 256, 512, 1024}");
+  if (ffn <= 0 || ffn % 128 != 0) return fail(BSA_ERR_UNSUPPORTED, "ffn_dim must be a positive multiple of 128");
+  X->F = ffn;
+  X->M = (long long)D.B * D.N;
+  if (X->M > (1LL << 30) || X->M * 2 * ffn >= (1LL << 40))
+    return fail(BSA_ERR_UNSUPPORTED, "batch * n (or its SwiGLU activations) too large");
+  return BSA_OK;
+}
+
+struct BlockSavedLayout {
+  size_t layer, r1, r2, xn1, gate, q, k, v, o, h, xn2, uw, a, total;
+};
+
+BlockSavedLayout block_saved_layout(const BlockDims& X) {
+  BlockSavedLayout L{};
+  const size_t M = (size_t)X.M, C = (size_t)X.C, F = (size_t)X.F;
+  size_t off = 0;
+  auto put = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
+  L.layer = put(saved_layout(X.D).total);
+  L.r1 = put(4 * M);
+  L.r2 = put(4 * M);
+  L.xn1 = put(2 * M * C);
+  L.gate = put(4 * 3 * M);
+  L.q = put(2 * M * C);
+  L.k = put(2 * M * C);
+  L.v = put(2 * M * C);
+  L.o = put(2 * M * C);
+  L.h = put(4 * M * C);
+  L.xn2 = put(2 * M * C);
+  L.uw = put(2 * M * 2 * F);
+  L.a = put(2 * M * F);
+  L.total = off;
+  return L;
+}
+
+struct BlockFwdWs {
+  size_t wqkv, wo, w13, w2, layer, total;
+};
+
+BlockFwdWs block_fwd_ws(const BlockDims& X) {
+  BlockFwdWs L{};
+  const size_t C = (size_t)X.C, F = (size_t)X.F;
+  size_t off = 0;
+  auto put = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
+  L.wqkv = put(2 * 3 * C * C);
+  L.wo = put(2 * C * C);
+  L.w13 = put(2 * 2 * F * C);
+  L.w2 = put(2 * C * F);
+  L.layer = put(fwd_ws_layout(X.D).total);
+  L.total = off;
+  return L;
+}
+
+// weight-gradient products: dW [Mo, No] = sum over the M tokens; split-K partials
+struct WgradShape {
+  int Mo, No;
+};
+
+size_t wgrad_part_bytes(const BlockDims& X) {
+  const WgradShape sh[4] = {{X.C, X.F}, {2 * X.F, X.C}, {X.C, X.C}, {3 * X.C, X.C}};
+  size_t best = 0;
+  for (const WgradShape& w : sh) {
+    const size_t b = sizeof(float) * (size_t)bsa::gemm_splits(w.Mo, w.No, X.M) * w.Mo * w.No;
+    best = b > best ? b : best;
+  }
+  return best;
+}
+
+struct BlockBwdWs {
+  size_t wqkvt, wot, w13t, w2t, dy16, part, da, duw, dxn, dh, dh16, do16, dq, dk, dv, dgate, dqkv, npart, layer,
+      total;
+};
+
+BlockBwdWs block_bwd_ws(const BlockDims& X) {
+  BlockBwdWs L{};
+  const size_t M = (size_t)X.M, C = (size_t)X.C, F = (size_t)X.F;
+  size_t off = 0;
+  auto put = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
+  L.wqkvt = put(2 * 3 * C * C);
+  L.wot = put(2 * C * C);
+  L.w13t = put(2 * 2 * F * C);
+  L.w2t = put(2 * C * F);
+  L.dy16 = put(2 * M * C);
+  L.part = put(wgrad_part_bytes(X));
+  L.da = put(4 * M * F);
+  L.duw = put(2 * M * 2 * F);
+  L.dxn = put(4 * M * C);
+  L.dh = put(4 * M * C);
+  L.dh16 = put(2 * M * C);
+  L.do16 = put(2 * M * C);
+  L.dq = put(4 * M * C);
+  L.dk = put(4 * M * C);
+  L.dv = put(4 * M * C);
+  L.dgate = put(4 * 3 * M);
+  L.dqkv = put(2 * M * 3 * C);
+  L.npart = put(bsa::rmsnorm_bwd_part_bytes(X.M, X.C));
+  L.layer = put(bwd_ws_layout(X.D).total);
+  L.total = off;
+  return L;
+}
+
+int ilog2(long long x) {
+  int r = 0;
+  while ((1LL << r) < x) ++r;
+  return r;
+}
+
+bsa::GemmMat plain(const void* p, long long ld) { return bsa::GemmMat{(const uint16_t*)p, ld, 0, 0, 0}; }
+
+bsa::GemmMat heads_mat(const BlockDims& X, const void* p) {
+  return bsa::GemmMat{(const uint16_t*)p, 0, X.D.H, ilog2(X.D.N), ilog2(X.D.d)};
+}
+
+bsa::GemmOut out_f32(float* out, long long ldc, const float* res = nullptr, long long ldr = 0) {
+  bsa::GemmOut o{};
+  o.epi = bsa::kEpiF32;
+  o.out = out;
+  o.ldc = ldc;
+  o.res = res;
+  o.ldr = ldr;
+  return o;
+}
+
+bsa::GemmOut out_heads(const BlockDims& X, void* p0, void* p1, void* p2) {
+  bsa::GemmOut o{};
+  o.epi = bsa::kEpiHeads;
+  o.parts[0] = (uint16_t*)p0;
+  o.parts[1] = (uint16_t*)p1;
+  o.parts[2] = (uint16_t*)p2;
+  o.part_cols = X.C;
+  o.heads = X.D.H;
+  o.lgn = ilog2(X.D.N);
+  o.lgd = ilog2(X.D.d);
+  return o;
+}
+
+// dW [Mo, No] = A^T B over the M token rows (A [M, Mo], B [M, No]) into out (rows < split_row)
+// and out2 (the remaining rows, when out2 is given).
+hipError_t wgrad(const BlockDims& X, const bsa::GemmMat& a, const bsa::GemmMat& b, int Mo, int No, float* part,
+                 float* out, float* out2, int split_row, hipStream_t st) {
+  const int S = bsa::gemm_splits(Mo, No, X.M);
+  bsa::GemmOut o{};
+  o.epi = bsa::kEpiPart;
+  o.out = part;
+  o.ldc = No;
+  hipError_t e = bsa::launch_gemm(true, a, b, Mo, No, X.M, S, o, st);
+  if (e != hipSuccess) return e;
+  const long long stride = (long long)Mo * No;
+  if (!out2) return bsa::launch_splitk_sum(part, S, stride, stride, out, st);
+  e = bsa::launch_splitk_sum(part, S, stride, (long long)split_row * No, out, st);
+  if (e != hipSuccess) return e;
+  return bsa::launch_splitk_sum(part + (long long)split_row * No, S, stride, (long long)(Mo - split_row) * No, out2,
+                                st);
+}
+
+bool mlp_ok(const bsa_mlp_t& m) { return m.w1 && m.b1 && m.w2 && m.b2; }
+
+}  // namespace
+
+#define BSA_HIP(expr, where) BSA_TRY((expr), (where))
+
+extern "C" {
+
+bsa_status_t bsa_block_sizes(const bsa_params_t* p, int32_t ffn_dim, size_t* ws_fwd_bytes, size_t* ws_bwd_bytes,
+                             size_t* saved_bytes) {
+  g_last_error.clear();
+  BlockDims X;
+  bsa_status_t s = check_block(p, ffn_dim, &X);
+  if (s != BSA_OK) return s;
+  if (ws_fwd_bytes) *ws_fwd_bytes = block_fwd_ws(X).total;
+  if (ws_bwd_bytes) *ws_bwd_bytes = block_bwd_ws(X).total;
+  if (saved_bytes) *saved_bytes = block_saved_layout(X).total;
+  return BSA_OK;
+}
+
+bsa_status_t bsa_block_saved_view(const bsa_params_t* p, int32_t ffn_dim, void* base, bsa_block_saved_t* out) {
+  g_last_error.clear();
+  BlockDims X;
+  bsa_status_t s = check_block(p, ffn_dim, &X);
+  if (s != BSA_OK) return s;
+  if (!base || !out) return fail(BSA_ERR_INVALID_ARGUMENT, "base and out must be non-NULL");
+  const BlockSavedLayout L = block_saved_layout(X);
+  char* c = (char*)base;
+  s = bsa_saved_view(p, c + L.layer, &out->layer);
+  if (s != BSA_OK) return s;
+  out->rstd1 = (float*)(c + L.r1);
+  out->rstd2 = (float*)(c + L.r2);
+  out->xn1 = c + L.xn1;
+  out->gate = (float*)(c + L.gate);
+  out->q = c + L.q;
+  out->k = c + L.k;
+  out->v = c + L.v;
+  out->o = c + L.o;
+  out->h = (float*)(c + L.h);
+  out->xn2 = c + L.xn2;
+  out->uw = c + L.uw;
+  out->a = c + L.a;
+  return BSA_OK;
+}
+
+bsa_status_t bsa_block_forward(const bsa_params_t* p, int32_t ffn_dim, const bsa_block_weights_t* w, const float* x,
+                               const uint8_t* valid, float* y, const bsa_block_saved_t* saved, void* ws,
+                               size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  BlockDims X;
+  bsa_status_t s = check_block(p, ffn_dim, &X);
+  if (s != BSA_OK) return s;
+  if (!w || !x || !y || !saved || !ws) return fail(BSA_ERR_INVALID_ARGUMENT, "w, x, y, saved and ws must be non-NULL");
+  if (!w->g1 || !w->wqkv || !w->wg || !w->wo || !w->g2 || !w->w1 || !w->w3 || !w->w2)
+    return fail(BSA_ERR_INVALID_ARGUMENT, "every block weight must be non-NULL");
+  if (x == y) return fail(BSA_ERR_INVALID_ARGUMENT, "y may not alias x");
+  const BlockFwdWs L = block_fwd_ws(X);
+  if (ws_bytes < L.total) return fail(BSA_ERR_WORKSPACE_TOO_SMALL, "block forward workspace too small");
+  const bsa_block_saved_t& sv = *saved;
+  if (!sv.rstd1 || !sv.rstd2 || !sv.xn1 || !sv.gate || !sv.q || !sv.k || !sv.v || !sv.o || !sv.h || !sv.xn2 || !sv.uw ||
+      !sv.a)
+    return fail(BSA_ERR_INVALID_ARGUMENT, "saved tensors must be non-NULL");
+  hipStream_t st = (hipStream_t)stream;
+  const int C = X.C, F = X.F;
+  const long long M = X.M;
+  char* c = (char*)ws;
+  uint16_t *wqkv = (uint16_t*)(c + L.wqkv), *wo = (uint16_t*)(c + L.wo), *w13 = (uint16_t*)(c + L.w13),
+           *w2 = (uint16_t*)(c + L.w2);
+  BSA_PHASE("blk.elem", st, {
+    BSA_HIP(bsa::launch_cast_bf16(w->wqkv, 3LL * C * C, wqkv, st), "cast wqkv");
+    BSA_HIP(bsa::launch_cast_bf16(w->wo, (long long)C * C, wo, st), "cast wo");
+    BSA_HIP(bsa::launch_cast_bf16(w->w1, (long long)F * C, w13, st), "cast w1");
+    BSA_HIP(bsa::launch_cast_bf16(w->w3, (long long)F * C, w13 + (long long)F * C, st), "cast w3");
+    BSA_HIP(bsa::launch_cast_bf16(w->w2, (long long)C * F, w2, st), "cast w2");
+  });
+  BSA_PHASE("blk.norm", st,
+            BSA_HIP(bsa::launch_rmsnorm_fwd(x, w->g1, w->wg, M, C, (uint16_t*)sv.xn1, sv.rstd1, sv.gate, st),
+                    "rmsnorm 1"));
+  BSA_PHASE("blk.gemm", st,
+            BSA_HIP(bsa::launch_gemm(false, plain(sv.xn1, C), plain(wqkv, C), (int)M, 3 * C, C, 1,
+                                     out_heads(X, sv.q, sv.k, sv.v), st),
+                    "qkv product"));
+  s = bsa_forward(p, sv.q, sv.k, sv.v, valid, sv.gate, &w->phi_k, &w->phi_v, mlp_ok(w->phi_q) ? &w->phi_q : nullptr,
+                  sv.o, &sv.layer, c + L.layer, L.total - L.layer, stream);
+  if (s != BSA_OK) return s;
+  BSA_PHASE("blk.gemm", st,
+            BSA_HIP(bsa::launch_gemm(false, heads_mat(X, sv.o), plain(wo, C), (int)M, C, C, 1, out_f32(sv.h, C, x, C),
+                                     st),
+                    "output projection"));
+  BSA_PHASE("blk.norm", st,
+            BSA_HIP(bsa::launch_rmsnorm_fwd(sv.h, w->g2, nullptr, M, C, (uint16_t*)sv.xn2, sv.rstd2, nullptr, st),
+                    "rmsnorm 2"));
+  BSA_PHASE("blk.gemm", st, {
+    bsa::GemmOut o{};
+    o.epi = bsa::kEpiBf16;
+    o.out = sv.uw;
+    o.ldc = 2 * F;
+    BSA_HIP(bsa::launch_gemm(false, plain(sv.xn2, C), plain(w13, C), (int)M, 2 * F, C, 1, o, st), "swiglu in");
+  });
+  BSA_PHASE("blk.elem", st,
+            BSA_HIP(bsa::launch_swiglu_fwd((const uint16_t*)sv.uw, M, F, (uint16_t*)sv.a, st), "swiglu"));
+  BSA_PHASE("blk.gemm", st,
+            BSA_HIP(bsa::launch_gemm(false, plain(sv.a, F), plain(w2, F), (int)M, C, F, 1, out_f32(y, C, sv.h, C), st),
+                    "swiglu out"));
+  return BSA_OK;
+}
+
+bsa_status_t bsa_block_backward(const bsa_params_t* p, int32_t ffn_dim, const bsa_block_weights_t* w, const float* x,
+                                const uint8_t* valid, const bsa_block_saved_t* saved, const float* dy, float* dx,
+                                const bsa_block_grads_t* dw, void* ws, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  BlockDims X;
+  bsa_status_t s = check_block(p, ffn_dim, &X);
+  if (s != BSA_OK) return s;
+  if (!w || !x || !saved || !dy || !dx || !dw || !ws)
+    return fail(BSA_ERR_INVALID_ARGUMENT, "w, x, saved, dy, dx, dw and ws must be non-NULL");
+  if (!w->g1 || !w->wqkv || !w->wg || !w->wo || !w->g2 || !w->w1 || !w->w3 || !w->w2)
+    return fail(BSA_ERR_INVALID_ARGUMENT, "every block weight must be non-NULL");
+  if (!dw->g1 || !dw->wqkv || !dw->wg || !dw->wo || !dw->g2 || !dw->w1 || !dw->w3 || !dw->w2)
+    return fail(BSA_ERR_INVALID_ARGUMENT, "every block weight gradient must be non-NULL");
+  const BlockBwdWs L = block_bwd_ws(X);
+  if (ws_bytes < L.total) return fail(BSA_ERR_WORKSPACE_TOO_SMALL, "block backward workspace too small");
+  const bsa_block_saved_t& sv = *saved;
+  hipStream_t st = (hipStream_t)stream;
+  const int C = X.C, F = X.F;
+  const long long M = X.M;
+  char* c = (char*)ws;
+  auto u16 = [&](size_t off) { return (uint16_t*)(c + off); };
+  auto f32 = [&](size_t off) { return (float*)(c + off); };
+  uint16_t *wqkvt = u16(L.wqkvt), *wot = u16(L.wot), *w13t = u16(L.w13t), *w2t = u16(L.w2t);
+  uint16_t *dy16 = u16(L.dy16), *duw = u16(L.duw), *dh16 = u16(L.dh16), *do16 = u16(L.do16), *dqkv = u16(L.dqkv);
+  float *part = f32(L.part), *da = f32(L.da), *dxn = f32(L.dxn), *dh = f32(L.dh), *dq = f32(L.dq), *dk = f32(L.dk),
+        *dv = f32(L.dv), *dgate = f32(L.dgate), *npart = f32(L.npart);
+  BSA_PHASE("blk.elem", st, {
+    BSA_HIP(bsa::launch_cast_t(w->wqkv, 3 * C, C, wqkvt, 3 * C, st), "cast wqkv^T");
+    BSA_HIP(bsa::launch_cast_t(w->wo, C, C, wot, C, st), "cast wo^T");
+    BSA_HIP(bsa::launch_cast_t(w->w1, F, C, w13t, 2 * F, st), "cast w1^T");
+    BSA_HIP(bsa::launch_cast_t(w->w3, F, C, w13t + F, 2 * F, st), "cast w3^T");
+    BSA_HIP(bsa::launch_cast_t(w->w2, C, F, w2t, C, st), "cast w2^T");
+    BSA_HIP(bsa::launch_cast_bf16(dy, M * C, dy16, st), "cast dy");
+  });
+  // SwiGLU sublayer
+  BSA_PHASE("blk.wgrad", st,
+            BSA_HIP(wgrad(X, plain(dy16, C), plain(sv.a, F), C, F, part, dw->w2, nullptr, 0, st), "dW2"));
+  BSA_PHASE("blk.gemm", st,
+            BSA_HIP(bsa::launch_gemm(false, plain(dy16, C), plain(w2t, C), (int)M, F, C, 1, out_f32(da, F), st),
+                    "da"));
+  BSA_PHASE("blk.elem", st, BSA_HIP(bsa::launch_swiglu_bwd(da, (const uint16_t*)sv.uw, M, F, duw, st), "swiglu bwd"));
+  BSA_PHASE("blk.wgrad", st,
+            BSA_HIP(wgrad(X, plain(duw, 2 * F), plain(sv.xn2, C), 2 * F, C, part, dw->w1, dw->w3, F, st), "dW13"));
+  BSA_PHASE("blk.gemm", st,
+            BSA_HIP(bsa::launch_gemm(false, plain(duw, 2 * F), plain(w13t, 2 * F), (int)M, C, 2 * F, 1,
+                                     out_f32(dxn, C), st),
+                    "dxn2"));
+  BSA_PHASE("blk.norm", st,
+            BSA_HIP(bsa::launch_rmsnorm_bwd(dxn, sv.h, sv.rstd2, w->g2, dy, nullptr, nullptr, M, C, dh, dh16, npart,
+                                            dw->g2, nullptr, st),
+                    "rmsnorm 2 bwd"));
+  // attention sublayer
+  BSA_PHASE("blk.wgrad", st,
+            BSA_HIP(wgrad(X, plain(dh16, C), heads_mat(X, sv.o), C, C, part, dw->wo, nullptr, 0, st), "dWo"));
+  BSA_PHASE("blk.gemm", st,
+            BSA_HIP(bsa::launch_gemm(false, plain(dh16, C), plain(wot, C), (int)M, C, C, 1,
+                                     out_heads(X, do16, nullptr, nullptr), st),
+                    "dO"));
+  const bool dq_mlp = X.D.qc_mlp && X.D.gcmp;
+  s = bsa_backward(p, sv.q, sv.k, sv.v, valid, sv.gate, &w->phi_k, &w->phi_v, mlp_ok(w->phi_q) ? &w->phi_q : nullptr,
+                   &sv.layer, do16, dq, dk, dv, dgate, &dw->phi_k, &dw->phi_v, dq_mlp ? &dw->phi_q : nullptr,
+                   c + L.layer, L.total - L.layer, stream);
+  if (s != BSA_OK) return s;
+  BSA_PHASE("blk.elem", st,
+            BSA_HIP(bsa::launch_pack_qkv(dq, dk, dv, M, C, X.D.H, ilog2(X.D.N), ilog2(X.D.d), dqkv, st), "pack dqkv"));
+  BSA_PHASE("blk.wgrad", st,
+            BSA_HIP(wgrad(X, plain(dqkv, 3 * C), plain(sv.xn1, C), 3 * C, C, part, dw->wqkv, nullptr, 0, st),
+                    "dWqkv"));
+  BSA_PHASE("blk.gemm", st,
+            BSA_HIP(bsa::launch_gemm(false, plain(dqkv, 3 * C), plain(wqkvt, 3 * C), (int)M, C, 3 * C, 1,
+                                     out_f32(dxn, C), st),
+                    "dxn1"));
+  BSA_PHASE("blk.norm", st,
+            BSA_HIP(bsa::launch_rmsnorm_bwd(dxn, x, sv.rstd1, w->g1, dh, dgate, w->wg, M, C, dx, nullptr, npart,
+                                            dw->g1, dw->wg, st),
+                    "rmsnorm 1 bwd"));
+  return BSA_OK;
+}
+
+}  // extern "C"

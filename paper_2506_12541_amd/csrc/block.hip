@@ -1,0 +1,611 @@
+// The dense parts of the transformer block around the layer (Section 3.1: each block holds
+// an RMSNorm, the BSA layer and a SwiGLU): the channel matrix products on the bf16 matrix
+// cores with f32 accumulation, RMSNorm forward/backward, SwiGLU forward/backward, and the
+// casts, layout changes and deterministic reductions between them.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace bsa {
+namespace {
+
+constexpr float kNormEps = 1e-6f;
+
+// ---- matrix products C[M, N] = sum_k A(m, k) B(n, k) ----
+//
+// Workgroup tile 128 x 128, four waves of 64 x 64 (4 x 4 accumulator tiles of 16 x 16),
+// contraction tiles of 64, two LDS stages filled by direct global->LDS loads while the
+// other stage feeds the matrix cores.
+//   plain form (trans = false): A [M, K] and B [N, K], contraction index fastest; tiles are
+//     staged as 128 rows x 64 (row fragments read with ds_read_b128);
+//   transposed form (trans = true): A [K, M] and B [K, N], the contraction runs over their
+//     rows (the weight gradients dW = dY^T X over tokens); tiles are staged as 64 rows x 128
+//     and read with transposing LDS reads (ds_read_b64_tr_b16).
+// Accumulator lane L holds C[m0 + L % 16][n0 + 4 (L / 16) + e], e = 0..3 (the B fragment
+// is the first MFMA operand), so each lane stores 4 consecutive columns.
+
+// 16-byte chunk swizzle of a staged tile row: 8 chunks per row (row-fragment reads of 16
+// consecutive rows) or 16 chunks per row (transposing reads of 8 consecutive rows, chunk
+// pairs on distinct banks).
+template <int COLS>
+__device__ __forceinline__ int tile_swz(int x) {
+  return COLS == 64 ? (x & 7) : 2 * (x & 7);
+}
+
+// Staging of ROWS x COLS tiles of a logical row-major operand into LDS by the four waves
+// of the workgroup. Each wave instruction fills 1 KB of consecutive LDS; lane L's 16 bytes
+// land at bytes [16 L, 16 L + 16) and the lane fetches the chunk the swizzle puts there.
+// The element offset of that chunk splits into a per-lane part fixed for the kernel and a
+// wave-uniform part per contraction tile (tile kt starts at column 64 kt of the plain form
+// or at row 64 kt of the transposed form; shapes are whole tiles, as the launcher checks).
+template <int ROWS, int COLS>
+struct TileLoader {
+  static constexpr int CPR = COLS / 8;
+  static constexpr int NU = ROWS * CPR / 256;   // wave instructions per wave
+  const bf16_t* p;
+  long long lane_off[NU];
+
+  // (r0, c0): the tile origin of the operand block this workgroup owns, as (row, column)
+  // of the logical matrix at kt = 0.
+  __device__ __forceinline__ void init(const GemmMat& m, long long r0, int c0, int wid, int lane) {
+    p = reinterpret_cast<const bf16_t*>(m.p);
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const int idx = (wid * NU + u) * 64 + lane;
+      const int row = idx / CPR;
+      const int col = 8 * ((idx % CPR) ^ tile_swz<COLS>(row));
+      const long long r = r0 + row;
+      const int c = c0 + col;
+      if (m.heads == 0) {
+        lane_off[u] = r * m.ld + c;
+      } else {
+        const long long b = r >> m.lgn, t = r & ((1LL << m.lgn) - 1);
+        lane_off[u] = ((((b * m.heads + (c >> m.lgd)) << m.lgn) + t) << m.lgd) + (c & ((1 << m.lgd) - 1));
+      }
+    }
+  }
+  __device__ __forceinline__ void issue(bf16_t* lds, long long kt_off, int wid) const {
+#pragma unroll
+    for (int u = 0; u < NU; ++u)
+      __builtin_amdgcn_global_load_lds(p + kt_off + lane_off[u], lds + (wid * NU + u) * 512, 16, 0, 0);
+  }
+};
+
+// Wave-uniform element offset of contraction tile kt (64 wide) of an operand.
+// Plain form: columns 64 kt (heads layout: d <= 64 divides 64, so the tile covers 64 / d
+// whole heads, 64 N elements further per tile). Transposed form: rows 64 kt (heads layout:
+// 64 divides n, so a tile stays inside one cloud).
+template <bool TR>
+__device__ __forceinline__ long long kt_offset(const GemmMat& m, int kt) {
+  const long long k0 = (long long)kt * 64;
+  if (!TR) return m.heads == 0 ? k0 : k0 << m.lgn;
+  if (m.heads == 0) return k0 * m.ld;
+  const long long b = k0 >> m.lgn, t = k0 & ((1LL << m.lgn) - 1);
+  return ((b * m.heads << m.lgn) + t) << m.lgd;
+}
+
+__device__ __forceinline__ bf16x8 frag_row(const bf16_t* t, int row, int lc) {
+  return *reinterpret_cast<const bf16x8*>(t + row * 64 + 8 * (lc ^ tile_swz<64>(row)));
+}
+
+// LDS byte addresses of the two transposing reads that give lane (p = L % 16, j = L / 16)
+// the operand X[k0 + 4j + i][m0 + p] (i = 0..3) and X[k0 + 16 + 4j + i][m0 + p] of a
+// [64][128] tile X: within each 16-lane group, ds_read_b64_tr_b16 hands lane l element
+// l % 4 of the 4-element runs addressed by lanes l / 4, 4 + l / 4, 8 + l / 4, 12 + l / 4, so
+// lane p addresses row k0 + 4j + p / 4 (then + 16) at columns m0 + 4 (p % 4) + [0, 4).
+__device__ __forceinline__ void tr_addr(const bf16_t* t, int k0, int m0, int lane, uint32_t& o0, uint32_t& o1) {
+  const int p = lane & 15, j = lane >> 4;
+  const int col = m0 + 4 * (p & 3);
+  const int lc = col >> 3, sub = col & 7;
+  const int x0 = k0 + 4 * j + (p >> 2), x1 = x0 + 16;
+  const bf16_t* a0 = t + x0 * 128 + 8 * (lc ^ tile_swz<128>(x0)) + sub;
+  const bf16_t* a1 = t + x1 * 128 + 8 * (lc ^ tile_swz<128>(x1)) + sub;
+  o0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)a0;
+  o1 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)a1;
+}
+
+// The eight operand fragments of one 32-deep contraction step of the transposed form (A
+// tiles i = 0..3 at columns am0 + 16 i, B tiles at bm0 + 16 j), issued as one statement
+// that also waits for them: every use of the results follows the wait.
+__device__ __forceinline__ void tr_frags(const bf16_t* as, const bf16_t* bs, int k0, int am0, int bm0, int lane,
+                                         uint4 (&af)[4], uint4 (&bf)[4]) {
+  uint32_t a[8], b[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    tr_addr(as, k0, am0 + 16 * i, lane, a[2 * i], a[2 * i + 1]);
+    tr_addr(bs, k0, bm0 + 16 * i, lane, b[2 * i], b[2 * i + 1]);
+  }
+  uint2 r[16];
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %16\n\tds_read_b64_tr_b16 %1, %17\n\t"
+      "ds_read_b64_tr_b16 %2, %18\n\tds_read_b64_tr_b16 %3, %19\n\t"
+      "ds_read_b64_tr_b16 %4, %20\n\tds_read_b64_tr_b16 %5, %21\n\t"
+      "ds_read_b64_tr_b16 %6, %22\n\tds_read_b64_tr_b16 %7, %23\n\t"
+      "ds_read_b64_tr_b16 %8, %24\n\tds_read_b64_tr_b16 %9, %25\n\t"
+      "ds_read_b64_tr_b16 %10, %26\n\tds_read_b64_tr_b16 %11, %27\n\t"
+      "ds_read_b64_tr_b16 %12, %28\n\tds_read_b64_tr_b16 %13, %29\n\t"
+      "ds_read_b64_tr_b16 %14, %30\n\tds_read_b64_tr_b16 %15, %31\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]),
+        "=&v"(r[7]), "=&v"(r[8]), "=&v"(r[9]), "=&v"(r[10]), "=&v"(r[11]), "=&v"(r[12]), "=&v"(r[13]),
+        "=&v"(r[14]), "=&v"(r[15])
+      : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7]), "v"(b[0]),
+        "v"(b[1]), "v"(b[2]), "v"(b[3]), "v"(b[4]), "v"(b[5]), "v"(b[6]), "v"(b[7])
+      : "memory");
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    af[i] = make_uint4(r[2 * i].x, r[2 * i].y, r[2 * i + 1].x, r[2 * i + 1].y);
+    bf[i] = make_uint4(r[8 + 2 * i].x, r[8 + 2 * i].y, r[8 + 2 * i + 1].x, r[8 + 2 * i + 1].y);
+  }
+}
+
+struct GemmArgs {
+  GemmMat a, b;
+  int ntn;        // column tiles
+  int kt_per;     // contraction tiles per split
+  GemmOut o;
+  long long split_stride;   // elements between the partial products of two splits
+};
+
+template <bool TR>
+__global__ void __launch_bounds__(256, 2) gemm_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(1024))) bf16_t as0[8192], bs0[8192], as1[8192], bs1[8192];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int wm = wid >> 1, wn = wid & 1;
+  // workgroups are dealt to the 8 XCDs round-robin; give each XCD a contiguous run of
+  // tiles (row panels walked column tile by column tile) so it re-reads A from its own L2
+  const int nt = gridDim.x;
+  int id = blockIdx.x;
+  if ((nt & 7) == 0) id = (id & 7) * (nt >> 3) + (id >> 3);
+  const int tm = id / g.ntn, tn = id - tm * g.ntn;
+  const long long m0 = (long long)tm * 128, n0 = (long long)tn * 128;
+  const int kt0 = blockIdx.y * g.kt_per, kt1 = kt0 + g.kt_per;
+
+  constexpr int AR = TR ? 64 : 128, AC = TR ? 128 : 64;
+  TileLoader<AR, AC> la, lb;
+  if (!TR) {
+    la.init(g.a, m0, 0, wid, lane);
+    lb.init(g.b, n0, 0, wid, lane);
+  } else {
+    la.init(g.a, 0, (int)m0, wid, lane);
+    lb.init(g.b, 0, (int)n0, wid, lane);
+  }
+  auto issue = [&](int kt, bf16_t* as, bf16_t* bs) {
+    la.issue(as, kt_offset<TR>(g.a, kt), wid);
+    lb.issue(bs, kt_offset<TR>(g.b, kt), wid);
+  };
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto step = [&](const bf16_t* as, const bf16_t* bs) {
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8 af[4], bfr[4];
+      if (!TR) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          af[i] = frag_row(as, wm * 64 + 16 * i + (lane & 15), 4 * ks + (lane >> 4));
+          bfr[i] = frag_row(bs, wn * 64 + 16 * i + (lane & 15), 4 * ks + (lane >> 4));
+        }
+      } else {
+        uint4 au[4], bu[4];
+        tr_frags(as, bs, 32 * ks, wm * 64, wn * 64, lane, au, bu);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          af[i] = __builtin_bit_cast(bf16x8, au[i]);
+          bfr[i] = __builtin_bit_cast(bf16x8, bu[i]);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mma(bfr[j], af[i], acc[i][j]);
+    }
+  };
+
+  issue(kt0, as0, bs0);
+  for (int kt = kt0; kt < kt1; kt += 2) {
+    vm_drain();        // this wave's loads of tile kt have landed
+    __syncthreads();   // ... and every wave's; stage 1 is no longer read
+    if (kt + 1 < kt1) issue(kt + 1, as1, bs1);
+    step(as0, bs0);
+    if (kt + 1 < kt1) {
+      vm_drain();
+      __syncthreads();
+      if (kt + 2 < kt1) issue(kt + 2, as0, bs0);
+      step(as1, bs1);
+    }
+  }
+
+  const GemmOut& o = g.o;
+  const int r = lane & 15, jq = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const long long m = m0 + wm * 64 + 16 * i + r;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = (int)n0 + wn * 64 + 16 * j + 4 * jq;
+      f32x4 v = acc[i][j];
+      if (o.epi == kEpiF32 || o.epi == kEpiPart) {
+        float* dst = reinterpret_cast<float*>(o.out) + (o.epi == kEpiPart ? blockIdx.y * g.split_stride : 0) +
+                     m * o.ldc + n;
+        if (o.epi == kEpiF32 && o.res) {
+          const float4 rv = *reinterpret_cast<const float4*>(o.res + m * o.ldr + n);
+          v[0] += rv.x;
+          v[1] += rv.y;
+          v[2] += rv.z;
+          v[3] += rv.w;
+        }
+        *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+      } else {
+        bf16_t* dst;
+        if (o.epi == kEpiBf16) {
+          dst = reinterpret_cast<bf16_t*>(o.out) + m * o.ldc + n;
+        } else {   // kEpiHeads
+          const int p = n / o.part_cols, c = n - p * o.part_cols;
+          const long long b = m >> o.lgn, t = m & ((1LL << o.lgn) - 1);
+          const long long h = c >> o.lgd, dd = c & ((1 << o.lgd) - 1);
+          dst = reinterpret_cast<bf16_t*>(o.parts[p]) + ((((b * o.heads + h) << o.lgn) + t) << o.lgd) + dd;
+        }
+        const uint32_t lo = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+        const uint32_t hi = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+        *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
+      }
+    }
+  }
+}
+
+// ---- RMSNorm: one wave per row; lane L holds columns 2L + 128 t, t < C / 128 ----
+
+template <int CT>
+__global__ void __launch_bounds__(256) rmsnorm_fwd_kernel(const float* __restrict__ x, const float* __restrict__ gain,
+                                                          const float* __restrict__ wg, long long rows,
+                                                          bf16_t* __restrict__ xn, float* __restrict__ rstd,
+                                                          float* __restrict__ gate) {
+  constexpr int C = 128 * CT;
+  const int lane = threadIdx.x & 63;
+  const long long row = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const float* xr = x + row * C;
+  float2 v[CT];
+  float ss = 0.f;
+#pragma unroll
+  for (int t = 0; t < CT; ++t) {
+    v[t] = *reinterpret_cast<const float2*>(xr + 128 * t + 2 * lane);
+    ss += v[t].x * v[t].x + v[t].y * v[t].y;
+  }
+  ss = wave_sum(ss);
+  const float rs = 1.0f / sqrtf(ss / (float)C + kNormEps);
+  float gd[3] = {0.f, 0.f, 0.f};
+#pragma unroll
+  for (int t = 0; t < CT; ++t) {
+    const int c = 128 * t + 2 * lane;
+    const float2 gg = *reinterpret_cast<const float2*>(gain + c);
+    const float a0 = v[t].x * rs * gg.x, a1 = v[t].y * rs * gg.y;
+    *reinterpret_cast<uint32_t*>(xn + row * C + c) = (uint32_t)f2bf(a0) | ((uint32_t)f2bf(a1) << 16);
+    if (wg) {
+#pragma unroll
+      for (int jj = 0; jj < 3; ++jj) {
+        const float2 w = *reinterpret_cast<const float2*>(wg + jj * C + c);
+        gd[jj] += a0 * w.x + a1 * w.y;
+      }
+    }
+  }
+  if (wg) {
+#pragma unroll
+    for (int jj = 0; jj < 3; ++jj) gd[jj] = wave_sum(gd[jj]);
+    if (lane == 0) {
+#pragma unroll
+      for (int jj = 0; jj < 3; ++jj) gate[row * 3 + jj] = gd[jj];
+    }
+  }
+  if (lane == 0) rstd[row] = rs;
+}
+
+// dx = dres + r (dxh - xh mean(dxh xh)) with xh = x r, dxh = (dxn + dgate W_g) g, per row;
+// the wave's sums of dg = (dxn + dgate W_g) xh and dW_g = dgate (xh g) over its rows go to
+// part[wave][4C] (dg, then dW_g row by row; zero without dgate).
+template <int CT>
+__global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(const float* __restrict__ dxn, const float* __restrict__ x,
+                                                          const float* __restrict__ rstd, const float* __restrict__ gain,
+                                                          const float* __restrict__ dres, const float* __restrict__ dgate,
+                                                          const float* __restrict__ wg, long long rows, int rpw,
+                                                          float* __restrict__ dx, bf16_t* __restrict__ dx16,
+                                                          float* __restrict__ part) {
+  constexpr int C = 128 * CT;
+  const int lane = threadIdx.x & 63;
+  const long long gw = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const long long r0 = gw * rpw, r1 = r0 + rpw < rows ? r0 + rpw : rows;
+  float2 gg[CT], ag[CT], w[3][CT], aw[3][CT];
+#pragma unroll
+  for (int t = 0; t < CT; ++t) {
+    const int c = 128 * t + 2 * lane;
+    gg[t] = *reinterpret_cast<const float2*>(gain + c);
+    ag[t] = make_float2(0.f, 0.f);
+#pragma unroll
+    for (int jj = 0; jj < 3; ++jj) {
+      w[jj][t] = dgate ? *reinterpret_cast<const float2*>(wg + jj * C + c) : make_float2(0.f, 0.f);
+      aw[jj][t] = make_float2(0.f, 0.f);
+    }
+  }
+  for (long long row = r0; row < r1; ++row) {
+    const float rs = rstd[row];
+    float dga[3] = {0.f, 0.f, 0.f};
+    if (dgate) {
+#pragma unroll
+      for (int jj = 0; jj < 3; ++jj) dga[jj] = dgate[row * 3 + jj];
+    }
+    float2 dn[CT], xh[CT];
+    float s = 0.f;
+#pragma unroll
+    for (int t = 0; t < CT; ++t) {
+      const int c = 128 * t + 2 * lane;
+      dn[t] = *reinterpret_cast<const float2*>(dxn + row * C + c);
+      const float2 xv = *reinterpret_cast<const float2*>(x + row * C + c);
+#pragma unroll
+      for (int jj = 0; jj < 3; ++jj) {
+        dn[t].x += dga[jj] * w[jj][t].x;
+        dn[t].y += dga[jj] * w[jj][t].y;
+      }
+      xh[t] = make_float2(xv.x * rs, xv.y * rs);
+      s += dn[t].x * gg[t].x * xh[t].x + dn[t].y * gg[t].y * xh[t].y;
+      ag[t].x += dn[t].x * xh[t].x;
+      ag[t].y += dn[t].y * xh[t].y;
+#pragma unroll
+      for (int jj = 0; jj < 3; ++jj) {
+        aw[jj][t].x += dga[jj] * xh[t].x * gg[t].x;
+        aw[jj][t].y += dga[jj] * xh[t].y * gg[t].y;
+      }
+    }
+    s = wave_sum(s) / (float)C;
+#pragma unroll
+    for (int t = 0; t < CT; ++t) {
+      const int c = 128 * t + 2 * lane;
+      const float2 dr = *reinterpret_cast<const float2*>(dres + row * C + c);
+      const float d0 = rs * (dn[t].x * gg[t].x - xh[t].x * s) + dr.x;
+      const float d1 = rs * (dn[t].y * gg[t].y - xh[t].y * s) + dr.y;
+      *reinterpret_cast<float2*>(dx + row * C + c) = make_float2(d0, d1);
+      if (dx16) *reinterpret_cast<uint32_t*>(dx16 + row * C + c) = (uint32_t)f2bf(d0) | ((uint32_t)f2bf(d1) << 16);
+    }
+  }
+  float* pw = part + gw * 4 * C;
+#pragma unroll
+  for (int t = 0; t < CT; ++t) {
+    const int c = 128 * t + 2 * lane;
+    *reinterpret_cast<float2*>(pw + c) = ag[t];
+#pragma unroll
+    for (int jj = 0; jj < 3; ++jj) *reinterpret_cast<float2*>(pw + (1 + jj) * C + c) = aw[jj][t];
+  }
+}
+
+// out[c] = sum over p of part[p * ld + col0 + c], c < ncols, in a fixed order (four waves
+// each sum a quarter of the rows; the quarters are added in wave order).
+__global__ void __launch_bounds__(256) colsum_kernel(const float* __restrict__ part, int P, long long ld, int col0,
+                                                     int ncols, float* __restrict__ out) {
+  __shared__ float red[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + lane;
+  float s = 0.f;
+  if (c < ncols)
+    for (int p = w; p < P; p += 4) s += part[(long long)p * ld + col0 + c];
+  red[w][lane] = s;
+  __syncthreads();
+  if (w == 0 && c < ncols) out[c] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+}
+
+// out[i] = sum over s of part[s * stride + i], four elements per thread, splits in order.
+__global__ void __launch_bounds__(256) splitk_sum_kernel(const float* __restrict__ part, int S, long long stride,
+                                                         long long count4, float* __restrict__ out) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= count4) return;
+  float4 s = reinterpret_cast<const float4*>(part)[i];
+  for (int k = 1; k < S; ++k) {
+    const float4 v = reinterpret_cast<const float4*>(part + k * stride)[i];
+    s.x += v.x;
+    s.y += v.y;
+    s.z += v.z;
+    s.w += v.w;
+  }
+  reinterpret_cast<float4*>(out)[i] = s;
+}
+
+__device__ __forceinline__ float sigmoidf_(float u) { return 1.0f / (1.0f + __expf(-u)); }
+
+// a = silu(u) * w for uw = [u | w] rows of 2F (bf16), eight elements per thread.
+__global__ void __launch_bounds__(256) swiglu_fwd_kernel(const bf16_t* __restrict__ uw, long long rows, int F,
+                                                         bf16_t* __restrict__ a) {
+  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+  const int f8 = F / 8;
+  if (idx >= rows * f8) return;
+  const long long row = idx / f8;
+  const int c = (int)(idx - row * f8) * 8;
+  const bf16x8 u = load_chunk(uw + row * 2 * F + c), w = load_chunk(uw + row * 2 * F + F + c);
+  float o[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float uf = bf2f(chunk_elem(u, e)), wf = bf2f(chunk_elem(w, e));
+    o[e] = uf * sigmoidf_(uf) * wf;
+  }
+  *reinterpret_cast<bf16x8*>(a + row * F + c) = make_chunk<bf16_t>(o);
+}
+
+// du = da w silu'(u), dw = da silu(u), silu'(u) = s (1 + u (1 - s)), s = sigmoid(u).
+__global__ void __launch_bounds__(256) swiglu_bwd_kernel(const float* __restrict__ da, const bf16_t* __restrict__ uw,
+                                                         long long rows, int F, bf16_t* __restrict__ duw) {
+  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+  const int f8 = F / 8;
+  if (idx >= rows * f8) return;
+  const long long row = idx / f8;
+  const int c = (int)(idx - row * f8) * 8;
+  const bf16x8 u = load_chunk(uw + row * 2 * F + c), w = load_chunk(uw + row * 2 * F + F + c);
+  const f32x8 g = load_chunk(da + row * F + c);
+  float du[8], dw[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float uf = bf2f(chunk_elem(u, e)), wf = bf2f(chunk_elem(w, e));
+    const float s = sigmoidf_(uf);
+    du[e] = g[e] * wf * s * (1.0f + uf * (1.0f - s));
+    dw[e] = g[e] * uf * s;
+  }
+  *reinterpret_cast<bf16x8*>(duw + row * 2 * F + c) = make_chunk<bf16_t>(du);
+  *reinterpret_cast<bf16x8*>(duw + row * 2 * F + F + c) = make_chunk<bf16_t>(dw);
+}
+
+// [M, 3C] bf16 token-major rows from dq, dk, dv [B, H, N, d] f32, eight elements per thread.
+__global__ void __launch_bounds__(256) pack_qkv_kernel(const float* __restrict__ dq, const float* __restrict__ dk,
+                                                       const float* __restrict__ dv, long long rows, int C, int H,
+                                                       int lgn, int lgd, bf16_t* __restrict__ out) {
+  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+  const int c8 = 3 * C / 8;
+  if (idx >= rows * c8) return;
+  const long long m = idx / c8;
+  const int col = (int)(idx - m * c8) * 8;
+  const int p = col / C, c = col - p * C;
+  const float* src = p == 0 ? dq : (p == 1 ? dk : dv);
+  const long long b = m >> lgn, t = m & ((1LL << lgn) - 1);
+  const long long h = c >> lgd, dd = c & ((1 << lgd) - 1);
+  const f32x8 v = load_chunk(src + ((((b * H + h) << lgn) + t) << lgd) + dd);
+  float o[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = v[e];
+  *reinterpret_cast<bf16x8*>(out + m * 3 * C + col) = make_chunk<bf16_t>(o);
+}
+
+__global__ void __launch_bounds__(256) cast_bf16_kernel(const float* __restrict__ src, long long n8,
+                                                        bf16_t* __restrict__ dst) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n8) return;
+  const f32x8 v = load_chunk(src + 8 * i);
+  float o[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = v[e];
+  *reinterpret_cast<bf16x8*>(dst + 8 * i) = make_chunk<bf16_t>(o);
+}
+
+// dst[c * ldd + r] = bf16(src[r * cols + c]) for a [rows, cols] f32 matrix (32 x 32 tiles
+// through LDS; rows and cols multiples of 32).
+__global__ void __launch_bounds__(256) cast_t_kernel(const float* __restrict__ src, int rows, int cols,
+                                                     bf16_t* __restrict__ dst, long long ldd) {
+  __shared__ float tile[32][33];
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) tile[ty + 8 * k][tx] = src[(long long)(r0 + ty + 8 * k) * cols + c0 + tx];
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 4; ++k) dst[(long long)(c0 + ty + 8 * k) * ldd + r0 + tx] = f2bf(tile[tx][ty + 8 * k]);
+}
+
+unsigned blocks_for(long long n, int per) { return (unsigned)((n + per - 1) / per); }
+
+}  // namespace
+
+hipError_t launch_gemm(bool trans, const GemmMat& a, const GemmMat& b, int M, int N, long long K, int splits,
+                       const GemmOut& o, hipStream_t st) {
+  if (M <= 0 || N <= 0 || K <= 0 || M % 128 || N % 128 || K % 64 || splits < 1 || (K / 64) % splits)
+    return hipErrorInvalidValue;
+  if (o.epi != kEpiPart && splits != 1) return hipErrorInvalidValue;
+  GemmArgs g{a, b, N / 128, (int)((K / 64) / splits), o, (long long)M * o.ldc};
+  const dim3 grid((unsigned)((M / 128) * (N / 128)), (unsigned)splits);
+  if (trans)
+    gemm_kernel<true><<<grid, 256, 0, st>>>(g);
+  else
+    gemm_kernel<false><<<grid, 256, 0, st>>>(g);
+  return hipGetLastError();
+}
+
+int gemm_splits(int M, int N, long long K) {
+  const long long tiles = (long long)(M / 128) * (N / 128);
+  const long long nkt = K / 64;
+  int s = 1;
+  // enough workgroups to fill the chip, at least 16 contraction tiles per split
+  while (tiles * s < 1024 && nkt % (2 * s) == 0 && nkt / (2 * s) >= 16) s *= 2;
+  return s;
+}
+
+hipError_t launch_rmsnorm_fwd(const float* x, const float* gain, const float* wg, long long rows, int C, uint16_t* xn,
+                              float* rstd, float* gate, hipStream_t st) {
+  const unsigned nb = blocks_for(rows, 4);
+  bf16_t* o = reinterpret_cast<bf16_t*>(xn);
+  switch (C) {
+    case 128: rmsnorm_fwd_kernel<1><<<nb, 256, 0, st>>>(x, gain, wg, rows, o, rstd, gate); break;
+    case 256: rmsnorm_fwd_kernel<2><<<nb, 256, 0, st>>>(x, gain, wg, rows, o, rstd, gate); break;
+    case 512: rmsnorm_fwd_kernel<4><<<nb, 256, 0, st>>>(x, gain, wg, rows, o, rstd, gate); break;
+    case 1024: rmsnorm_fwd_kernel<8><<<nb, 256, 0, st>>>(x, gain, wg, rows, o, rstd, gate); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+int rmsnorm_bwd_waves(long long rows) { return (int)(rows < 2048 ? rows : 2048); }
+
+hipError_t launch_rmsnorm_bwd(const float* dxn, const float* x, const float* rstd, const float* gain, const float* dres,
+                              const float* dgate, const float* wg, long long rows, int C, float* dx, uint16_t* dx16,
+                              float* part, float* dgain, float* dwg, hipStream_t st) {
+  const int waves = rmsnorm_bwd_waves(rows);
+  const int rpw = (int)((rows + waves - 1) / waves);
+  const unsigned nb = blocks_for(waves, 4);
+  bf16_t* o16 = reinterpret_cast<bf16_t*>(dx16);
+  switch (C) {
+    case 128: rmsnorm_bwd_kernel<1><<<nb, 256, 0, st>>>(dxn, x, rstd, gain, dres, dgate, wg, rows, rpw, dx, o16, part); break;
+    case 256: rmsnorm_bwd_kernel<2><<<nb, 256, 0, st>>>(dxn, x, rstd, gain, dres, dgate, wg, rows, rpw, dx, o16, part); break;
+    case 512: rmsnorm_bwd_kernel<4><<<nb, 256, 0, st>>>(dxn, x, rstd, gain, dres, dgate, wg, rows, rpw, dx, o16, part); break;
+    case 1024: rmsnorm_bwd_kernel<8><<<nb, 256, 0, st>>>(dxn, x, rstd, gain, dres, dgate, wg, rows, rpw, dx, o16, part); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int P = (int)nb * 4;
+  colsum_kernel<<<blocks_for(C, 64), 256, 0, st>>>(part, P, 4LL * C, 0, C, dgain);
+  if (dgate) colsum_kernel<<<blocks_for(3LL * C, 64), 256, 0, st>>>(part, P, 4LL * C, C, 3 * C, dwg);
+  return hipGetLastError();
+}
+
+size_t rmsnorm_bwd_part_bytes(long long rows, int C) {
+  const long long waves = ((long long)rmsnorm_bwd_waves(rows) + 3) / 4 * 4;
+  return sizeof(float) * (size_t)waves * 4 * C;
+}
+
+hipError_t launch_splitk_sum(const float* part, int S, long long stride, long long count, float* out, hipStream_t st) {
+  if (count % 4 || stride % 4) return hipErrorInvalidValue;
+  splitk_sum_kernel<<<blocks_for(count / 4, 256), 256, 0, st>>>(part, S, stride, count / 4, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_fwd(const uint16_t* uw, long long rows, int F, uint16_t* a, hipStream_t st) {
+  if (F % 8) return hipErrorInvalidValue;
+  swiglu_fwd_kernel<<<blocks_for(rows * (F / 8), 256), 256, 0, st>>>(reinterpret_cast<const bf16_t*>(uw), rows, F,
+                                                                      reinterpret_cast<bf16_t*>(a));
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_bwd(const float* da, const uint16_t* uw, long long rows, int F, uint16_t* duw, hipStream_t st) {
+  if (F % 8) return hipErrorInvalidValue;
+  swiglu_bwd_kernel<<<blocks_for(rows * (F / 8), 256), 256, 0, st>>>(da, reinterpret_cast<const bf16_t*>(uw), rows, F,
+                                                                      reinterpret_cast<bf16_t*>(duw));
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_qkv(const float* dq, const float* dk, const float* dv, long long rows, int C, int H, int lgn,
+                           int lgd, uint16_t* out, hipStream_t st) {
+  if (C % 8) return hipErrorInvalidValue;
+  pack_qkv_kernel<<<blocks_for(rows * (3 * C / 8), 256), 256, 0, st>>>(dq, dk, dv, rows, C, H, lgn, lgd,
+                                                                        reinterpret_cast<bf16_t*>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_cast_bf16(const float* src, long long n, uint16_t* dst, hipStream_t st) {
+  if (n % 8) return hipErrorInvalidValue;
+  cast_bf16_kernel<<<blocks_for(n / 8, 256), 256, 0, st>>>(src, n / 8, reinterpret_cast<bf16_t*>(dst));
+  return hipGetLastError();
+}
+
+hipError_t launch_cast_t(const float* src, int rows, int cols, uint16_t* dst, long long ldd, hipStream_t st) {
+  if (rows % 32 || cols % 32) return hipErrorInvalidValue;
+  cast_t_kernel<<<dim3(cols / 32, rows / 32), 256, 0, st>>>(src, rows, cols, reinterpret_cast<bf16_t*>(dst), ldd);
+  return hipGetLastError();
+}
+
+}  // namespace bsa

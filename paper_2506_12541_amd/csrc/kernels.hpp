@@ -138,6 +138,44 @@ hipError_t launch_radix_sort_pairs(uint32_t* keys, uint32_t* vals, uint32_t* key
                                    uint32_t* hist, long long n, int bits, uint32_t** keys_out, uint32_t** vals_out,
                                    hipStream_t st);
 
+// block.hip: the dense parts of the transformer block (RMSNorm, channel products, SwiGLU)
+// A bf16 operand of the block's products: element (r, c) of a logical row-major matrix.
+// heads == 0: at p[r * ld + c]. heads > 0: the head-major layout [B, heads, n, d] of a
+// logical [B * n, heads * d] matrix (n = 2^lgn, d = 2^lgd).
+struct GemmMat {
+  const uint16_t* p;
+  long long ld;
+  int heads, lgn, lgd;
+};
+enum GemmEpi { kEpiF32 = 0, kEpiBf16 = 1, kEpiHeads = 2, kEpiPart = 3 };
+struct GemmOut {
+  int epi;
+  void* out;            // kEpiF32 / kEpiBf16: [M, ldc]; kEpiPart: f32 [splits][M][ldc]
+  long long ldc;
+  const float* res;     // kEpiF32: added to the product (may be NULL)
+  long long ldr;
+  uint16_t* parts[3];   // kEpiHeads: column block p (part_cols wide) -> head-major parts[p]
+  int part_cols, heads, lgn, lgd;
+};
+// C[M, N] = sum_k A(m, k) B(n, k); trans = false: A [M, K], B [N, K]; trans = true: A [K, M],
+// B [K, N]. M, N multiples of 128, K of 64; splits > 1 only with kEpiPart.
+hipError_t launch_gemm(bool trans, const GemmMat& a, const GemmMat& b, int M, int N, long long K, int splits,
+                       const GemmOut& o, hipStream_t st);
+int gemm_splits(int M, int N, long long K);
+hipError_t launch_rmsnorm_fwd(const float* x, const float* gain, const float* wg, long long rows, int C, uint16_t* xn,
+                              float* rstd, float* gate, hipStream_t st);
+hipError_t launch_rmsnorm_bwd(const float* dxn, const float* x, const float* rstd, const float* gain, const float* dres,
+                              const float* dgate, const float* wg, long long rows, int C, float* dx, uint16_t* dx16,
+                              float* part, float* dgain, float* dwg, hipStream_t st);
+size_t rmsnorm_bwd_part_bytes(long long rows, int C);
+hipError_t launch_splitk_sum(const float* part, int S, long long stride, long long count, float* out, hipStream_t st);
+hipError_t launch_swiglu_fwd(const uint16_t* uw, long long rows, int F, uint16_t* a, hipStream_t st);
+hipError_t launch_swiglu_bwd(const float* da, const uint16_t* uw, long long rows, int F, uint16_t* duw, hipStream_t st);
+hipError_t launch_pack_qkv(const float* dq, const float* dk, const float* dv, long long rows, int C, int H, int lgn,
+                           int lgd, uint16_t* out, hipStream_t st);
+hipError_t launch_cast_bf16(const float* src, long long n, uint16_t* dst, hipStream_t st);
+hipError_t launch_cast_t(const float* src, int rows, int cols, uint16_t* dst, long long ldd, hipStream_t st);
+
 // timing.cpp: optional per-phase HIP-event timing (see bsa_timing_enable in bsa.h)
 bool timing_on();
 void timing_set(bool on);

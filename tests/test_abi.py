@@ -138,3 +138,49 @@ def test_set_streams_validates(lib):
     assert lib.bsa_set_streams(3) == _lib.BSA_ERR_INVALID_ARGUMENT
     assert lib.bsa_set_streams(0) == _lib.BSA_ERR_INVALID_ARGUMENT
     assert lib.bsa_set_streams(2) == _lib.BSA_OK
+
+
+def _block_sizes(lib, p, ffn):
+    a, b, c = C.c_size_t(), C.c_size_t(), C.c_size_t()
+    cp = p.c()
+    return lib.bsa_block_sizes(C.byref(cp), ffn, C.byref(a), C.byref(b), C.byref(c)), a.value, b.value, c.value
+
+
+def test_block_sizes_and_validation(lib):
+    bf = dict(dtype=_lib.BSA_BF16)
+    st, wf, wb, sv = _block_sizes(lib, base(**bf), 512)        # C = 4 * 32 = 128
+    assert st == _lib.BSA_OK and wf > 0 and wb > wf and sv > 0
+    # the block's saved set holds the layer's
+    st_l, _, sv_l = _sizes(lib, base(**bf))
+    assert sv > sv_l
+    assert _block_sizes(lib, base(dtype=_lib.BSA_F32), 512)[0] == _lib.BSA_ERR_UNSUPPORTED  # float32 layer
+    assert _block_sizes(lib, base(heads=2, **bf), 512)[0] == _lib.BSA_ERR_UNSUPPORTED  # C = 64
+    assert _block_sizes(lib, base(**bf), 100)[0] == _lib.BSA_ERR_UNSUPPORTED           # F not a multiple of 128
+    assert _block_sizes(lib, base(**bf), 0)[0] == _lib.BSA_ERR_UNSUPPORTED
+
+
+def test_block_struct_layout_matches_header(tmp_path):
+    # the ctypes structs of the binding have the sizes the C compiler gives the header's
+    src = tmp_path / "sz.c"
+    src.write_text('#include "bsa.h"\n#include <stdio.h>\nint main(void) { printf("%zu %zu %zu %zu\\n", '
+                   'sizeof(bsa_params_t), sizeof(bsa_saved_t), sizeof(bsa_block_weights_t), '
+                   'sizeof(bsa_block_saved_t)); return 0; }\n')
+    exe = tmp_path / "sz"
+    import subprocess
+    subprocess.run(["gcc", f"-I{os.path.join(ROOT, 'include')}", str(src), "-o", str(exe)], check=True)
+    got = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split()]
+    assert got == [C.sizeof(_lib.bsa_params_t), C.sizeof(_lib.bsa_saved_t), C.sizeof(_lib.bsa_block_weights_t),
+                   C.sizeof(_lib.bsa_block_saved_t)]
+
+
+def test_block_forward_rejects_before_launch(lib):
+    p = base(dtype=_lib.BSA_BF16)
+    cp = p.c()
+    saved = _lib.bsa_block_saved_t()
+    w = _lib.bsa_block_weights_t()
+    fake = C.c_void_p(256)
+    st = lib.bsa_block_forward(C.byref(cp), 512, C.byref(w), fake, None, C.c_void_p(512), C.byref(saved), fake,
+                               1 << 40, None)
+    assert st == _lib.BSA_ERR_INVALID_ARGUMENT and "weight" in lib.bsa_last_error().decode()
+    st = lib.bsa_block_forward(C.byref(cp), 512, None, fake, None, fake, C.byref(saved), fake, 1 << 40, None)
+    assert st == _lib.BSA_ERR_INVALID_ARGUMENT

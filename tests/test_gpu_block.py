@@ -1,0 +1,157 @@
+"""GPU transformer block (RMSNorm + BSA layer + SwiGLU, the paper's model unit) vs the
+float64 block oracle with the same bf16 rounding points, forward and backward, on the same
+seeded inputs through the C ABI (bsa_block_forward / bsa_block_backward).
+
+The oracle runs with the GPU's selected blocks (the selection is piecewise constant; the
+GPU's Q and K can differ from the oracle's by a rounding flip, so near-tied blocks may be
+ordered differently) and the number of groups whose selection differs is reported.
+Bars:
+  * tensors stored in bf16 before the layer (norm1 output, Q, K, V): equal except where a
+    float32 vs float64 accumulation flips a rounding, in under 1% of the entries: by one
+    bf16 step; Q, K, V also by one step of an operand that flipped upstream (2^-8 of the
+    sum of the magnitudes of the product's terms); entries near zero by at most 2^-16 of
+    the tensor's RMS;
+  * the gate logits (float32 from float32 operands): max-abs 1e-4;
+  * the layer output: the layer's bf16 bar, max-abs 2e-2;
+  * everything downstream of the layer (h, norm2, u, w, a, y and dx): the bf16 bar 2e-2 on
+    the error of each entry relative to its own magnitude plus the tensor's RMS. The
+    layer's error enters each stage as an absolute error on the scale of the tensor; a
+    bf16 rounding flip of an input moves an entry in proportion to its own magnitude (a
+    product u w inherits the relative step of u or w);
+    a = silu(u) w combines the errors of u and w and its own rounding: 2 x 2e-2 + 2^-8;
+  * weight gradients (sums over all tokens): the error of each entry relative to the sum
+    of the magnitudes of its terms, 2e-2, as for the layer's weight gradients; the layer's
+    MLP gradients, whose dO here carries the error of the block's backward pass on top of
+    the layer's own, 2 x 2e-2."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import model as om
+from parity import TOL, oracle_kw, oracle_params, to_dev, valid_from_tree
+from paper_2506_12541_amd import bsa as gb
+from workloads import CONFIGS, Config, make_block_inputs
+
+pytestmark = pytest.mark.gpu
+
+# 2 clouds of 900 points in 1024 slots, H = 2, d = 64 (C = 128, F = 512)
+SMALL = Config("small_bf16", 2, 900, 1024, 2, 64, "bf16", 128, 16, 16, 32, 4, 16, "uniform", "fwdbwd")
+# the airflow layer settings (H = 8, d = 32: C = 256, F = 1024) on 2 clouds
+AIRFLOW2 = dataclasses.replace(CONFIGS[5], batch=2)
+
+
+def _bf16_steps(gpu, ref):
+    """Per-entry difference in units of the bf16 spacing at the reference value."""
+    ref = np.asarray(ref, np.float64)
+    spacing = np.ldexp(1.0, np.frexp(np.abs(ref))[1] - 8)
+    spacing[ref == 0] = 2.0 ** -133
+    return np.abs(np.asarray(gpu, np.float64) - ref) / spacing
+
+
+def _check_rounded(name, gpu, ref, errs, terms=None):
+    """A rounding flip moves an entry by one bf16 step. Entries of a product also move when
+    one of its bf16 operands flipped upstream, by at most one step of that operand's term,
+    bounded by 2^-8 of the sum of the magnitudes of the terms (``terms``), and entries
+    near zero by the float32 accumulation error, bounded by 2^-16 of the tensor's RMS."""
+    steps = _bf16_steps(gpu, ref)
+    diff = np.abs(np.asarray(gpu, np.float64) - ref)
+    rms = np.sqrt(np.mean(np.asarray(ref, np.float64) ** 2))
+    bound = 2.0 ** -16 * rms + (0.0 if terms is None else 2.0 ** -8 * terms)
+    frac = float(np.mean(steps > 0))
+    worst = float(np.max(np.where(steps <= 1.0 + 1e-9, 0.0, diff / bound)))
+    errs[name] = f"{frac:.1e} flips, max {steps.max():.2f} steps"
+    assert worst <= 1.0 and frac < 1e-2, (name, frac, steps.max(), worst)
+
+
+def _scaled(gpu, ref):
+    """max |gpu - ref| / (|ref| + RMS(ref)) over the entries."""
+    g, r = np.asarray(gpu, np.float64), np.asarray(ref, np.float64)
+    rms = np.sqrt(np.mean(r * r))
+    return float(np.max(np.abs(g - r) / (np.abs(r) + max(rms, 1e-30))))
+
+
+def run_block(cfg, seed=None, **pkw):
+    valid = valid_from_tree(cfg, seed)
+    inp = make_block_inputs(cfg, valid, seed=seed)
+    ffn = inp["ffn"]
+    p = gb.Params.from_config(cfg, **pkw)
+    dev32 = lambda a: to_dev(a, torch.float32)
+    W = {n: dev32(a) for n, a in inp["W"].items()}
+    phk, phv, phq = ({w: dev32(a) for w, a in inp[n].items()} for n in ("phi_k", "phi_v", "phi_q"))
+    x, dy = dev32(inp["x"]), dev32(inp["dy"])
+    vd = to_dev(valid.astype(np.uint8), torch.uint8)
+    y, saved = gb.block_forward(p, ffn, W, phk, phv, x, vd, phi_q=phq)
+    grads = gb.block_backward(p, ffn, W, phk, phv, x, saved, dy, vd, phi_q=phq)
+    torch.cuda.synchronize()
+    f = lambda t: t.float().cpu().numpy()
+    P = oracle_params(cfg, **oracle_kw(pkw))
+    H, d = cfg.heads, cfg.head_dim
+    sel = saved.sel_idx.cpu().numpy().astype(np.int64)
+    y_ref, cache = om.block_forward(inp["x"], valid, inp["W"], inp["phi_k"], inp["phi_v"], P, H, d, phi_q=inp["phi_q"],
+                                    bf16=True)
+    ndiff = int(np.sum(np.any(np.sort(cache["fwd"]["sel"], -1) != np.sort(sel, -1), axis=-1)))
+    if ndiff:   # evaluate the oracle on the GPU's selection
+        y_ref, cache = om.block_forward(inp["x"], valid, inp["W"], inp["phi_k"], inp["phi_v"], P, H, d, sel=sel,
+                                        phi_q=inp["phi_q"], bf16=True)
+    ref = om.block_backward(inp["dy"], cache, valid, inp["phi_k"], inp["phi_v"], P, H, d, phi_q=inp["phi_q"])
+    errs = {"groups with another selection": f"{ndiff} of {sel.shape[0] * sel.shape[1] * sel.shape[2]}"}
+    tol = TOL["bf16"]
+    # before the layer
+    _check_rounded("xn1", f(saved.xn1), cache["x1"], errs)
+    terms = np.abs(cache["x1"]) @ np.abs(cache["Wr"]["wqkv"]).T
+    Cc = H * d
+    for i, n in enumerate(("q", "k", "v")):
+        t = terms[..., i * Cc:(i + 1) * Cc].reshape(cfg.batch, cfg.n_pad, H, d).transpose(0, 2, 1, 3)
+        _check_rounded(n, f(getattr(saved, n)), cache[n], errs, t)
+    errs["gate"] = float(np.abs(f(saved.gate) - cache["gate"]).max())
+    assert errs["gate"] < 1e-4, errs
+    # the layer and downstream
+    vm = valid[:, None, :, None] & np.ones((1, H, 1, d), bool)
+    errs["o"] = float(np.abs(f(saved.o) - cache["fwd"]["o"])[vm].max())
+    assert errs["o"] < tol, errs
+    scaled = {
+        "h": _scaled(f(saved.h), cache["h"]),
+        "xn2": _scaled(f(saved.xn2), cache["x2"]),
+        "u": _scaled(f(saved.uw)[..., :ffn], cache["u"]),
+        "w": _scaled(f(saved.uw)[..., ffn:], cache["w"]),
+        "a": _scaled(f(saved.a), cache["a"]),
+        "y": _scaled(f(y), y_ref),
+        "dx": _scaled(f(grads["dx"]), ref["dx"]),
+    }
+    rel = lambda g, r, a: float(np.max(np.abs(np.asarray(g, np.float64) - r) / np.maximum(a, 1e-30)))
+    wgrad = {n: rel(f(grads["dW"][n]), ref["dW"][n], ref["abs"][n]) for n in om.WEIGHTS}
+    for which in ("dphi_k", "dphi_v"):
+        for w in ("w1", "b1", "w2", "b2"):
+            a = ref["layer"]["abs"][which][w]
+            if a.max() > 1e-12:
+                wgrad[f"{which}.{w}"] = rel(f(grads[which][w]), ref[which][w], a)
+    errs.update({k: f"{v:.2e}" for k, v in {**scaled, **wgrad}.items()})
+    print(errs, flush=True)
+    bars = {k: tol for k in {**scaled, **wgrad}}
+    bars["a"] = 2 * tol + 2.0 ** -8          # product of two tensors each within tol, then rounded
+    for k in wgrad:
+        if k.startswith("dphi"):
+            bars[k] = 2 * tol                 # the layer's bar, plus dO's own error from the block
+    bad = {k: v for k, v in {**scaled, **wgrad}.items() if not v < bars[k]}
+    assert not bad, bad
+    # padding rows stay zero in the forward pass
+    pad = ~valid
+    assert not np.any(f(y)[pad]) and not np.any(f(saved.h)[pad])
+
+
+def test_block_small():
+    print("block parity small bf16 (C = 128, F = 512)", flush=True)
+    run_block(SMALL, seed=11)
+
+
+def test_block_small_group_compression():
+    print("block parity small bf16, MLP coarsening + group compression", flush=True)
+    run_block(SMALL, seed=12, q_coarsen=1, group_compression=1)
+
+
+@pytest.mark.timeout(300)
+def test_block_airflow():
+    print("block parity airflow settings, 2 clouds (C = 256, F = 1024)", flush=True)
+    run_block(AIRFLOW2)

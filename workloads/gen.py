@@ -16,7 +16,7 @@ import math
 
 import numpy as np
 
-__all__ = ["Config", "CONFIGS", "make_points", "make_inputs", "round_bf16", "bf16_bits"]
+__all__ = ["Config", "CONFIGS", "make_points", "make_inputs", "make_block_inputs", "round_bf16", "bf16_bits"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -167,6 +167,16 @@ def _normal(rng, shape, scale=1.0, chunk=1 << 24) -> np.ndarray:
     return out
 
 
+def _mlp_weights(rr, ld: int, d: int, rnd) -> dict:
+    """One compression / coarsening MLP ld -> d -> d, entries N(0, 0.02^2)."""
+    return {
+        "w1": rnd((rr.standard_normal((ld, d)) * 0.02).astype(np.float32)),
+        "b1": rnd((rr.standard_normal(d) * 0.02).astype(np.float32)),
+        "w2": rnd((rr.standard_normal((d, d)) * 0.02).astype(np.float32)),
+        "b2": rnd((rr.standard_normal(d) * 0.02).astype(np.float32)),
+    }
+
+
 def make_inputs(cfg: Config, seed: int | None = None, *, layout: str = "ball",
                 with_grad: bool | None = None) -> dict:
     """Seeded layer inputs.
@@ -210,12 +220,37 @@ def make_inputs(cfg: Config, seed: int | None = None, *, layout: str = "ball",
     ld = cfg.cmp_block * d
     # phi_q: the query-coarsening MLP of Eq. 13 (own stream; the other tensors are unchanged)
     for name, rr in (("phi_k", r[5]), ("phi_v", r[6]), ("phi_q", r[8])):
-        out[name] = {
-            "w1": rnd((rr.standard_normal((ld, d)) * 0.02).astype(np.float32)),
-            "b1": rnd((rr.standard_normal(d) * 0.02).astype(np.float32)),
-            "w2": rnd((rr.standard_normal((d, d)) * 0.02).astype(np.float32)),
-            "b2": rnd((rr.standard_normal(d) * 0.02).astype(np.float32)),
-        }
+        out[name] = _mlp_weights(rr, ld, d, rnd)
     if with_grad:
         out["do"] = rnd(_normal(r[7], (B, H, cfg.n_pad, d)))
     return out
+
+
+def make_block_inputs(cfg: Config, valid: np.ndarray, ffn: int | None = None, seed: int | None = None) -> dict:
+    """Seeded inputs of one transformer block around the layer: tokens x [B, n_pad, C]
+    (N(0,1) on real slots, zero on padding slots), the block's float32 weights (norm gains
+    1 + N(0, 0.01), matrices N(0, 1/fan_in)), the layer's MLPs (as in make_inputs) and the
+    upstream gradient dy [B, n_pad, C] (N(0,1) on real slots, zero on padding slots).
+    C = heads * head_dim, F = ffn (default 4C)."""
+    seed = _default_seed(cfg, seed)
+    B, C = cfg.batch, cfg.heads * cfg.head_dim
+    F = ffn or 4 * C
+    r = _streams(seed * 1000 + 3, 12)
+    mask = np.asarray(valid, bool)[..., None]
+    x = _normal(r[0], (B, cfg.n_pad, C)) * mask
+    dy = _normal(r[1], (B, cfg.n_pad, C)) * mask
+    W = {
+        "g1": (1.0 + 0.1 * r[2].standard_normal(C)).astype(np.float32),
+        "wqkv": _normal(r[3], (3 * C, C), 1.0 / math.sqrt(C)),
+        "wg": _normal(r[4], (3, C), 1.0 / math.sqrt(C)),
+        "wo": _normal(r[5], (C, C), 1.0 / math.sqrt(C)),
+        "g2": (1.0 + 0.1 * r[6].standard_normal(C)).astype(np.float32),
+        "w1": _normal(r[7], (F, C), 1.0 / math.sqrt(C)),
+        "w3": _normal(r[8], (F, C), 1.0 / math.sqrt(C)),
+        "w2": _normal(r[9], (C, F), 1.0 / math.sqrt(F)),
+    }
+    ld = cfg.cmp_block * cfg.head_dim
+    rnd = round_bf16 if cfg.dtype == "bf16" else (lambda a: a)
+    return {"x": x.astype(np.float32), "dy": dy.astype(np.float32), "W": W, "ffn": F,
+            "phi_k": _mlp_weights(r[10], ld, cfg.head_dim, rnd), "phi_v": _mlp_weights(r[11], ld, cfg.head_dim, rnd),
+            "phi_q": _mlp_weights(_streams(seed * 1000 + 4, 1)[0], ld, cfg.head_dim, rnd)}
