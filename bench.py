@@ -196,6 +196,10 @@ def parse():
     ap.add_argument("--variant", choices=sorted(VARIANTS), default="bsa")
     ap.add_argument("--sweep", action="store_true",
                     help="sequence-length sweep: BSA layer vs full attention (one JSON line per length)")
+    ap.add_argument("--model", action="store_true",
+                    help="sequence-length sweep of the 18-block model (RMSNorm + BSA + SwiGLU), forward + backward, "
+                         "BSA vs full attention (one JSON line per length)")
+    ap.add_argument("--lengths", default="1024,2048,4096,8192,16384,32768,65536")
     ap.add_argument("--cpu-baseline", type=int, default=1, help="time the float64 oracle on a sample (0 = skip)")
     ap.add_argument("--copy-calibration", action="store_true", help="run only the 1 GiB plain copy")
     ap.add_argument("--summarize-traffic", nargs=4, metavar="CSV",
@@ -313,8 +317,145 @@ def sweep(args):
         torch.cuda.empty_cache()
 
 
+BLOCK_PHASES = ("blk.norm", "blk.gemm", "blk.wgrad", "blk.elem")
+N_BLOCKS = 18   # the paper's model depth (Section 3.1)
+
+
+def block_flops(n, C, F):
+    """Channel-product FLOPs of one block per token count n: forward 2 n C (3C + C + 2F + F),
+    backward twice that (activation and weight gradients)."""
+    fwd = 2.0 * n * C * (3 * C + C + 2 * F + F)
+    return fwd, 2.0 * fwd
+
+
+def model_sweep(args):
+    """Runtime of the 18-block model against sequence length, BSA vs full attention (the
+    shape of the paper's Fig. 2).
+
+    Each length N runs one N-point Gaussian-mixture cloud in ball order through 18 blocks
+    (RMSNorm + BSA layer + SwiGLU, C = 512 = 8 heads x 64, F = 2048, bf16 products, the
+    65536-point workload's layer settings), forward then backward, with per-block seeded
+    weights; timed with host clocks over whole steps. The full-attention model is the same
+    step with each block's BSA layer time replaced by that of softmax attention over every
+    key (the ball kernels with one ball of N tokens, forward + backward, from their phase
+    events on one stream): model_full = model_bsa - 18 layer_bsa + 18 layer_full, where
+    layer_bsa is the measured forward + backward of one BSA layer on the same inputs."""
+    import numpy as np
+    import torch
+
+    from paper_2506_12541_amd import _lib
+    from paper_2506_12541_amd import bsa as gb
+    from workloads import Config, make_block_inputs
+
+    lib = _lib.load()
+    dev = torch.device("cuda:0")
+    for n in (int(v) for v in args.lengths.split(",")):
+        cfg = Config(f"model_{n}", 1, n, n, 8, 64, "bf16", 256, 16, 16, 32, 16, 16, "gmm", "fwdbwd")
+        C = cfg.heads * cfg.head_dim
+        valid = np.ones((1, n), bool)
+        p = gb.Params.from_config(cfg)
+        blocks = []
+        for i in range(N_BLOCKS):
+            inp = make_block_inputs(cfg, valid, seed=1000 + i) if i == 0 or n <= 8192 else dict(blocks[0]["np"])
+            t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+            blocks.append({"np": inp, "W": {k: t(a) for k, a in inp["W"].items()},
+                           "phk": {w: t(a) for w, a in inp["phi_k"].items()},
+                           "phv": {w: t(a) for w, a in inp["phi_v"].items()},
+                           "saved": gb.BlockSaved(p, inp["ffn"], dev)})
+        F = blocks[0]["np"]["ffn"]
+        x0 = torch.from_numpy(blocks[0]["np"]["x"]).to(dev)
+        dy0 = torch.from_numpy(blocks[0]["np"]["dy"]).to(dev)
+
+        def step():
+            xs = [x0]
+            for b in blocks:
+                y, _ = gb.block_forward(p, F, b["W"], b["phk"], b["phv"], xs[-1], saved=b["saved"])
+                xs.append(y)
+            g = dy0
+            for i in reversed(range(N_BLOCKS)):
+                b = blocks[i]
+                g = gb.block_backward(p, F, b["W"], b["phk"], b["phv"], xs[i], b["saved"], g)["dx"]
+            return g
+
+        step()
+        torch.cuda.synchronize()
+        steps = max(2, min(10, (1 << 17) // n))
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step()
+        torch.cuda.synchronize()
+        model_ms = (time.perf_counter() - t0) / steps * 1e3
+
+        # one BSA layer forward + backward on the first block's Q/K/V (both streams)
+        sv = blocks[0]["saved"]
+        q, k, v, gate = sv.q.clone(), sv.k.clone(), sv.v.clone(), sv.gate.clone()
+        do = torch.randn_like(q.float()).to(q.dtype)
+        phk, phv = blocks[0]["phk"], blocks[0]["phv"]
+        lsaved = gb.Saved(p, dev)
+
+        def layer(pp, saved, reps):
+            for _ in range(reps):
+                o, s2 = gb.forward(pp, q, k, v, None, gate, phk, phv, saved=saved)
+                gb.backward(pp, q, k, v, None, gate, phk, phv, s2, do)
+
+        layer(p, lsaved, 2)
+        torch.cuda.synchronize()
+        reps = max(3, min(30, (1 << 19) // n))
+        t0 = time.perf_counter()
+        layer(p, lsaved, reps)
+        torch.cuda.synchronize()
+        bsa_layer_ms = (time.perf_counter() - t0) / reps * 1e3
+
+        # full attention: the ball kernels with one ball of n tokens, one stream
+        pf = gb.Params.from_config(dataclasses.replace(cfg, ball=n))
+        fsaved = gb.Saved(pf, dev)
+        _lib.check(lib.bsa_set_streams(1), "streams")
+        layer(pf, fsaved, 1)
+        torch.cuda.synchronize()
+        fsteps = max(2, min(20, (1 << 19) // n))
+        phases = ("fwd.ball", "bwd.dq_ball", "bwd.kv_ball")
+        lib.bsa_timing_select(",".join(phases).encode())
+        lib.bsa_timing_enable(1)
+        layer(pf, fsaved, fsteps)
+        torch.cuda.synchronize()
+        full_layer_ms = 0.0
+        for name in phases:
+            tot, cnt = _lib.C.c_double(), _lib.C.c_int32()
+            _lib.check(lib.bsa_timing_query(name.encode(), _lib.C.byref(tot), _lib.C.byref(cnt)), "timing")
+            full_layer_ms += tot.value / fsteps
+        # the block's own kernels, by phase (one stream, one model step)
+        lib.bsa_timing_select(",".join(BLOCK_PHASES).encode())
+        lib.bsa_timing_enable(1)
+        step()
+        torch.cuda.synchronize()
+        blk = {}
+        for name in BLOCK_PHASES:
+            tot, cnt = _lib.C.c_double(), _lib.C.c_int32()
+            _lib.check(lib.bsa_timing_query(name.encode(), _lib.C.byref(tot), _lib.C.byref(cnt)), "timing")
+            blk[name] = round(tot.value / N_BLOCKS, 4)
+        lib.bsa_timing_enable(0)
+        lib.bsa_timing_select(None)
+        _lib.check(lib.bsa_set_streams(2), "streams")
+        full_model_ms = model_ms - N_BLOCKS * bsa_layer_ms + N_BLOCKS * full_layer_ms
+        fwd_f, bwd_f = block_flops(n, C, F)
+        gemm_ms = blk["blk.gemm"] + blk["blk.wgrad"]
+        print(json.dumps({
+            "n": n, "model_bsa_ms": round(model_ms, 3), "model_full_attention_ms": round(full_model_ms, 3),
+            "full_over_bsa": round(full_model_ms / model_ms, 3), "bsa_layer_ms": round(bsa_layer_ms, 4),
+            "full_attention_layer_ms": round(full_layer_ms, 4), "block_phases_ms": blk,
+            "block_products_tflops": round((fwd_f + bwd_f) / (gemm_ms * 1e-3) / 1e12, 1) if gemm_ms > 0 else None,
+            "workload": f"1 cloud of {n} points, 18 blocks (RMSNorm + BSA + SwiGLU), C=512 (8 heads x 64), F=2048, "
+                        "bf16 products; layer: ball 256, cmp 16, slc 32, top-16, group 16; forward + backward"}),
+              flush=True)
+        del blocks, lsaved, fsaved
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
+    if args.model:
+        model_sweep(args)
+        return
     if args.sweep:
         sweep(args)
         return

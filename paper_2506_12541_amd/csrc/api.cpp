@@ -684,7 +684,7 @@ size_t wgrad_part_bytes(const BlockDims& X) {
 }
 
 struct BlockBwdWs {
-  size_t wqkvt, wot, w13t, w2t, dy16, part, da, duw, dxn, dh, dh16, do16, dq, dk, dv, dgate, dqkv, npart, layer,
+  size_t wqkvt, wot, w13t, w2t, dy16, part, duw, dxn, dh, dh16, do16, dq, dk, dv, dgate, dqkv, npart, layer,
       total;
 };
 
@@ -699,7 +699,6 @@ BlockBwdWs block_bwd_ws(const BlockDims& X) {
   L.w2t = put(2 * C * F);
   L.dy16 = put(2 * M * C);
   L.part = put(wgrad_part_bytes(X));
-  L.da = put(4 * M * F);
   L.duw = put(2 * M * 2 * F);
   L.dxn = put(4 * M * C);
   L.dh = put(4 * M * C);
@@ -841,8 +840,7 @@ bsa_status_t bsa_block_forward(const bsa_params_t* p, int32_t ffn_dim, const bsa
   BSA_PHASE("blk.elem", st, {
     BSA_HIP(bsa::launch_cast_bf16(w->wqkv, 3LL * C * C, wqkv, st), "cast wqkv");
     BSA_HIP(bsa::launch_cast_bf16(w->wo, (long long)C * C, wo, st), "cast wo");
-    BSA_HIP(bsa::launch_cast_bf16(w->w1, (long long)F * C, w13, st), "cast w1");
-    BSA_HIP(bsa::launch_cast_bf16(w->w3, (long long)F * C, w13 + (long long)F * C, st), "cast w3");
+    BSA_HIP(bsa::launch_cast_w13(w->w1, w->w3, F, C, w13, st), "cast w1, w3");
     BSA_HIP(bsa::launch_cast_bf16(w->w2, (long long)C * F, w2, st), "cast w2");
   });
   BSA_PHASE("blk.norm", st,
@@ -864,13 +862,12 @@ bsa_status_t bsa_block_forward(const bsa_params_t* p, int32_t ffn_dim, const bsa
                     "rmsnorm 2"));
   BSA_PHASE("blk.gemm", st, {
     bsa::GemmOut o{};
-    o.epi = bsa::kEpiBf16;
+    o.epi = bsa::kEpiSwigluFwd;
     o.out = sv.uw;
-    o.ldc = 2 * F;
-    BSA_HIP(bsa::launch_gemm(false, plain(sv.xn2, C), plain(w13, C), (int)M, 2 * F, C, 1, o, st), "swiglu in");
+    o.out2 = sv.a;
+    o.ffn = F;
+    BSA_HIP(bsa::launch_gemm(false, plain(sv.xn2, C), plain(w13, C), (int)M, 2 * F, C, 1, o, st), "swiglu");
   });
-  BSA_PHASE("blk.elem", st,
-            BSA_HIP(bsa::launch_swiglu_fwd((const uint16_t*)sv.uw, M, F, (uint16_t*)sv.a, st), "swiglu"));
   BSA_PHASE("blk.gemm", st,
             BSA_HIP(bsa::launch_gemm(false, plain(sv.a, F), plain(w2, F), (int)M, C, F, 1, out_f32(y, C, sv.h, C), st),
                     "swiglu out"));
@@ -901,7 +898,7 @@ bsa_status_t bsa_block_backward(const bsa_params_t* p, int32_t ffn_dim, const bs
   auto f32 = [&](size_t off) { return (float*)(c + off); };
   uint16_t *wqkvt = u16(L.wqkvt), *wot = u16(L.wot), *w13t = u16(L.w13t), *w2t = u16(L.w2t);
   uint16_t *dy16 = u16(L.dy16), *duw = u16(L.duw), *dh16 = u16(L.dh16), *do16 = u16(L.do16), *dqkv = u16(L.dqkv);
-  float *part = f32(L.part), *da = f32(L.da), *dxn = f32(L.dxn), *dh = f32(L.dh), *dq = f32(L.dq), *dk = f32(L.dk),
+  float *part = f32(L.part), *dxn = f32(L.dxn), *dh = f32(L.dh), *dq = f32(L.dq), *dk = f32(L.dk),
         *dv = f32(L.dv), *dgate = f32(L.dgate), *npart = f32(L.npart);
   BSA_PHASE("blk.elem", st, {
     BSA_HIP(bsa::launch_cast_t(w->wqkv, 3 * C, C, wqkvt, 3 * C, st), "cast wqkv^T");
@@ -914,10 +911,14 @@ bsa_status_t bsa_block_backward(const bsa_params_t* p, int32_t ffn_dim, const bs
   // SwiGLU sublayer
   BSA_PHASE("blk.wgrad", st,
             BSA_HIP(wgrad(X, plain(dy16, C), plain(sv.a, F), C, F, part, dw->w2, nullptr, 0, st), "dW2"));
-  BSA_PHASE("blk.gemm", st,
-            BSA_HIP(bsa::launch_gemm(false, plain(dy16, C), plain(w2t, C), (int)M, F, C, 1, out_f32(da, F), st),
-                    "da"));
-  BSA_PHASE("blk.elem", st, BSA_HIP(bsa::launch_swiglu_bwd(da, (const uint16_t*)sv.uw, M, F, duw, st), "swiglu bwd"));
+  BSA_PHASE("blk.gemm", st, {
+    bsa::GemmOut o{};
+    o.epi = bsa::kEpiSwigluBwd;
+    o.out = duw;
+    o.aux = (const uint16_t*)sv.uw;
+    o.ffn = F;
+    BSA_HIP(bsa::launch_gemm(false, plain(dy16, C), plain(w2t, C), (int)M, F, C, 1, o, st), "swiglu bwd");
+  });
   BSA_PHASE("blk.wgrad", st,
             BSA_HIP(wgrad(X, plain(duw, 2 * F), plain(sv.xn2, C), 2 * F, C, part, dw->w1, dw->w3, F, st), "dW13"));
   BSA_PHASE("blk.gemm", st,

@@ -221,6 +221,34 @@ __global__ void __launch_bounds__(256, 2) gemm_kernel(GemmArgs g) {
 
   const GemmOut& o = g.o;
   const int r = lane & 15, jq = lane >> 4;
+  auto pack4 = [](float a0, float a1, float a2, float a3) {
+    return make_uint2((uint32_t)f2bf(a0) | ((uint32_t)f2bf(a1) << 16), (uint32_t)f2bf(a2) | ((uint32_t)f2bf(a3) << 16));
+  };
+  if (o.epi == kEpiSwigluFwd) {
+    // B rows interleaved in groups of 64 (32 of W_1, then the same 32 of W_3): the wave's
+    // column tiles j and j + 2 hold u and w of the same hidden units f
+    const int F = o.ffn;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const long long m = m0 + wm * 64 + 16 * i + r;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int f = ((int)n0 + wn * 64) / 2 + 16 * j + 4 * jq;
+        float u[4], w[4], a[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          u[e] = bf2f(f2bf(acc[i][j][e]));
+          w[e] = bf2f(f2bf(acc[i][j + 2][e]));
+          a[e] = u[e] / (1.0f + __expf(-u[e])) * w[e];
+        }
+        bf16_t* uw = reinterpret_cast<bf16_t*>(o.out) + m * 2 * F + f;
+        *reinterpret_cast<uint2*>(uw) = pack4(u[0], u[1], u[2], u[3]);
+        *reinterpret_cast<uint2*>(uw + F) = pack4(w[0], w[1], w[2], w[3]);
+        *reinterpret_cast<uint2*>(reinterpret_cast<bf16_t*>(o.out2) + m * F + f) = pack4(a[0], a[1], a[2], a[3]);
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const long long m = m0 + wm * 64 + 16 * i + r;
@@ -239,6 +267,24 @@ __global__ void __launch_bounds__(256, 2) gemm_kernel(GemmArgs g) {
           v[3] += rv.w;
         }
         *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+      } else if (o.epi == kEpiSwigluBwd) {
+        // v = da for hidden units n .. n + 3; u, w from the forward pass (bf16 [M, 2F])
+        const int F = o.ffn;
+        const bf16_t* uwp = reinterpret_cast<const bf16_t*>(o.aux) + m * 2 * F + n;
+        const uint2 ub = *reinterpret_cast<const uint2*>(uwp), wb = *reinterpret_cast<const uint2*>(uwp + F);
+        const uint32_t uu[2] = {ub.x, ub.y}, ww[2] = {wb.x, wb.y};
+        float du[4], dw[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float uf = __uint_as_float((uu[e >> 1] >> (16 * (e & 1))) << 16);
+          const float wf = __uint_as_float((ww[e >> 1] >> (16 * (e & 1))) << 16);
+          const float sg = 1.0f / (1.0f + __expf(-uf));
+          du[e] = v[e] * wf * sg * (1.0f + uf * (1.0f - sg));
+          dw[e] = v[e] * uf * sg;
+        }
+        bf16_t* dst = reinterpret_cast<bf16_t*>(o.out) + m * 2 * F + n;
+        *reinterpret_cast<uint2*>(dst) = pack4(du[0], du[1], du[2], du[3]);
+        *reinterpret_cast<uint2*>(dst + F) = pack4(dw[0], dw[1], dw[2], dw[3]);
       } else {
         bf16_t* dst;
         if (o.epi == kEpiBf16) {
@@ -249,9 +295,7 @@ __global__ void __launch_bounds__(256, 2) gemm_kernel(GemmArgs g) {
           const long long h = c >> o.lgd, dd = c & ((1 << o.lgd) - 1);
           dst = reinterpret_cast<bf16_t*>(o.parts[p]) + ((((b * o.heads + h) << o.lgn) + t) << o.lgd) + dd;
         }
-        const uint32_t lo = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-        const uint32_t hi = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-        *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
+        *reinterpret_cast<uint2*>(dst) = pack4(v[0], v[1], v[2], v[3]);
       }
     }
   }
@@ -304,20 +348,22 @@ __global__ void __launch_bounds__(256) rmsnorm_fwd_kernel(const float* __restric
   if (lane == 0) rstd[row] = rs;
 }
 
-// dx = dres + r (dxh - xh mean(dxh xh)) with xh = x r, dxh = (dxn + dgate W_g) g, per row;
-// the wave's sums of dg = (dxn + dgate W_g) xh and dW_g = dgate (xh g) over its rows go to
-// part[wave][4C] (dg, then dW_g row by row; zero without dgate).
+// dx = dres + r (dxh - xh mean(dxh xh)) with xh = x r, dxh = (dxn + dgate W_g) g, per row.
+// Workgroup b owns a contiguous run of rows (wave w takes every fourth row from w); the
+// sums over its rows of dg = (dxn + dgate W_g) xh and dW_g = dgate (xh g) go to
+// part[b][4C] (dg, then dW_g row by row; zero without dgate), the four waves' sums added in
+// wave order.
 template <int CT>
 __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(const float* __restrict__ dxn, const float* __restrict__ x,
                                                           const float* __restrict__ rstd, const float* __restrict__ gain,
                                                           const float* __restrict__ dres, const float* __restrict__ dgate,
-                                                          const float* __restrict__ wg, long long rows, int rpw,
+                                                          const float* __restrict__ wg, long long rows, int rpg,
                                                           float* __restrict__ dx, bf16_t* __restrict__ dx16,
                                                           float* __restrict__ part) {
   constexpr int C = 128 * CT;
-  const int lane = threadIdx.x & 63;
-  const long long gw = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const long long r0 = gw * rpw, r1 = r0 + rpw < rows ? r0 + rpw : rows;
+  __shared__ float red[3][4 * C];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const long long g0 = (long long)blockIdx.x * rpg, g1 = g0 + rpg < rows ? g0 + rpg : rows;
   float2 gg[CT], ag[CT], w[3][CT], aw[3][CT];
 #pragma unroll
   for (int t = 0; t < CT; ++t) {
@@ -330,19 +376,20 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(const float* __restric
       aw[jj][t] = make_float2(0.f, 0.f);
     }
   }
-  for (long long row = r0; row < r1; ++row) {
+  for (long long row = g0 + wid; row < g1; row += 4) {
     const float rs = rstd[row];
     float dga[3] = {0.f, 0.f, 0.f};
     if (dgate) {
 #pragma unroll
       for (int jj = 0; jj < 3; ++jj) dga[jj] = dgate[row * 3 + jj];
     }
-    float2 dn[CT], xh[CT];
+    float2 dn[CT], xh[CT], dr[CT];
     float s = 0.f;
 #pragma unroll
     for (int t = 0; t < CT; ++t) {
       const int c = 128 * t + 2 * lane;
       dn[t] = *reinterpret_cast<const float2*>(dxn + row * C + c);
+      dr[t] = *reinterpret_cast<const float2*>(dres + row * C + c);
       const float2 xv = *reinterpret_cast<const float2*>(x + row * C + c);
 #pragma unroll
       for (int jj = 0; jj < 3; ++jj) {
@@ -363,36 +410,60 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(const float* __restric
 #pragma unroll
     for (int t = 0; t < CT; ++t) {
       const int c = 128 * t + 2 * lane;
-      const float2 dr = *reinterpret_cast<const float2*>(dres + row * C + c);
-      const float d0 = rs * (dn[t].x * gg[t].x - xh[t].x * s) + dr.x;
-      const float d1 = rs * (dn[t].y * gg[t].y - xh[t].y * s) + dr.y;
+      const float d0 = rs * (dn[t].x * gg[t].x - xh[t].x * s) + dr[t].x;
+      const float d1 = rs * (dn[t].y * gg[t].y - xh[t].y * s) + dr[t].y;
       *reinterpret_cast<float2*>(dx + row * C + c) = make_float2(d0, d1);
       if (dx16) *reinterpret_cast<uint32_t*>(dx16 + row * C + c) = (uint32_t)f2bf(d0) | ((uint32_t)f2bf(d1) << 16);
     }
   }
-  float* pw = part + gw * 4 * C;
+  if (wid > 0) {
 #pragma unroll
-  for (int t = 0; t < CT; ++t) {
-    const int c = 128 * t + 2 * lane;
-    *reinterpret_cast<float2*>(pw + c) = ag[t];
+    for (int t = 0; t < CT; ++t) {
+      const int c = 128 * t + 2 * lane;
+      *reinterpret_cast<float2*>(&red[wid - 1][c]) = ag[t];
 #pragma unroll
-    for (int jj = 0; jj < 3; ++jj) *reinterpret_cast<float2*>(pw + (1 + jj) * C + c) = aw[jj][t];
+      for (int jj = 0; jj < 3; ++jj) *reinterpret_cast<float2*>(&red[wid - 1][(1 + jj) * C + c]) = aw[jj][t];
+    }
+  }
+  __syncthreads();
+  if (wid == 0) {
+    float* pw = part + (long long)blockIdx.x * 4 * C;
+#pragma unroll
+    for (int t = 0; t < CT; ++t) {
+      const int c = 128 * t + 2 * lane;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float2 v = q == 0 ? ag[t] : aw[q - 1][t];
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+          const float2 o = *reinterpret_cast<const float2*>(&red[k][q * C + c]);
+          v.x += o.x;
+          v.y += o.y;
+        }
+        *reinterpret_cast<float2*>(pw + q * C + c) = v;
+      }
+    }
   }
 }
 
-// out[c] = sum over p of part[p * ld + col0 + c], c < ncols, in a fixed order (four waves
-// each sum a quarter of the rows; the quarters are added in wave order).
+// out[by * ncols + c] = sum over rows p in [32 by, 32 by + 32) (below P) of
+// part[p * ld + col0 + c], c < ncols; wave w sums rows 32 by + 8 w .. + 8 and the four
+// waves' sums are added in wave order.
 __global__ void __launch_bounds__(256) colsum_kernel(const float* __restrict__ part, int P, long long ld, int col0,
                                                      int ncols, float* __restrict__ out) {
   __shared__ float red[4][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int c = blockIdx.x * 64 + lane;
-  float s = 0.f;
-  if (c < ncols)
-    for (int p = w; p < P; p += 4) s += part[(long long)p * ld + col0 + c];
+  const int p0 = blockIdx.y * 32 + w * 8;
+  float v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = c < ncols && p0 + i < P ? part[(long long)(p0 + i) * ld + col0 + c] : 0.f;
+  float s = v[0];
+#pragma unroll
+  for (int i = 1; i < 8; ++i) s += v[i];
   red[w][lane] = s;
   __syncthreads();
-  if (w == 0 && c < ncols) out[c] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+  if (w == 0 && c < ncols) out[(long long)blockIdx.y * ncols + c] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
 }
 
 // out[i] = sum over s of part[s * stride + i], four elements per thread, splits in order.
@@ -409,48 +480,6 @@ __global__ void __launch_bounds__(256) splitk_sum_kernel(const float* __restrict
     s.w += v.w;
   }
   reinterpret_cast<float4*>(out)[i] = s;
-}
-
-__device__ __forceinline__ float sigmoidf_(float u) { return 1.0f / (1.0f + __expf(-u)); }
-
-// a = silu(u) * w for uw = [u | w] rows of 2F (bf16), eight elements per thread.
-__global__ void __launch_bounds__(256) swiglu_fwd_kernel(const bf16_t* __restrict__ uw, long long rows, int F,
-                                                         bf16_t* __restrict__ a) {
-  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
-  const int f8 = F / 8;
-  if (idx >= rows * f8) return;
-  const long long row = idx / f8;
-  const int c = (int)(idx - row * f8) * 8;
-  const bf16x8 u = load_chunk(uw + row * 2 * F + c), w = load_chunk(uw + row * 2 * F + F + c);
-  float o[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const float uf = bf2f(chunk_elem(u, e)), wf = bf2f(chunk_elem(w, e));
-    o[e] = uf * sigmoidf_(uf) * wf;
-  }
-  *reinterpret_cast<bf16x8*>(a + row * F + c) = make_chunk<bf16_t>(o);
-}
-
-// du = da w silu'(u), dw = da silu(u), silu'(u) = s (1 + u (1 - s)), s = sigmoid(u).
-__global__ void __launch_bounds__(256) swiglu_bwd_kernel(const float* __restrict__ da, const bf16_t* __restrict__ uw,
-                                                         long long rows, int F, bf16_t* __restrict__ duw) {
-  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
-  const int f8 = F / 8;
-  if (idx >= rows * f8) return;
-  const long long row = idx / f8;
-  const int c = (int)(idx - row * f8) * 8;
-  const bf16x8 u = load_chunk(uw + row * 2 * F + c), w = load_chunk(uw + row * 2 * F + F + c);
-  const f32x8 g = load_chunk(da + row * F + c);
-  float du[8], dw[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const float uf = bf2f(chunk_elem(u, e)), wf = bf2f(chunk_elem(w, e));
-    const float s = sigmoidf_(uf);
-    du[e] = g[e] * wf * s * (1.0f + uf * (1.0f - s));
-    dw[e] = g[e] * uf * s;
-  }
-  *reinterpret_cast<bf16x8*>(duw + row * 2 * F + c) = make_chunk<bf16_t>(du);
-  *reinterpret_cast<bf16x8*>(duw + row * 2 * F + F + c) = make_chunk<bf16_t>(dw);
 }
 
 // [M, 3C] bf16 token-major rows from dq, dk, dv [B, H, N, d] f32, eight elements per thread.
@@ -498,6 +527,25 @@ __global__ void __launch_bounds__(256) cast_t_kernel(const float* __restrict__ s
   for (int k = 0; k < 4; ++k) dst[(long long)(c0 + ty + 8 * k) * ldd + r0 + tx] = f2bf(tile[tx][ty + 8 * k]);
 }
 
+// dst rows of the interleaved [W_1; W_3] operand: row r takes row 32 (r / 64) + r % 64 of
+// W_1 when r % 64 < 32, else row 32 (r / 64) + r % 64 - 32 of W_3 (f32 -> bf16, eight
+// elements per thread; C a multiple of 8).
+__global__ void __launch_bounds__(256) cast_w13_kernel(const float* __restrict__ w1, const float* __restrict__ w3,
+                                                       int F, int C, bf16_t* __restrict__ dst) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  const int c8 = C / 8;
+  if (i >= 2LL * F * c8) return;
+  const long long r = i / c8;
+  const int c = (int)(i - r * c8) * 8;
+  const int g = (int)(r >> 6), wi = (int)(r & 63);
+  const float* src = wi < 32 ? w1 + (long long)(32 * g + wi) * C : w3 + (long long)(32 * g + wi - 32) * C;
+  const f32x8 v = load_chunk(src + c);
+  float o[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = v[e];
+  *reinterpret_cast<bf16x8*>(dst + r * C + c) = make_chunk<bf16_t>(o);
+}
+
 unsigned blocks_for(long long n, int per) { return (unsigned)((n + per - 1) / per); }
 
 }  // namespace
@@ -539,52 +587,56 @@ hipError_t launch_rmsnorm_fwd(const float* x, const float* gain, const float* wg
   return hipGetLastError();
 }
 
-int rmsnorm_bwd_waves(long long rows) { return (int)(rows < 2048 ? rows : 2048); }
+// row groups of the RMSNorm backward: up to 1024 workgroups, at least 16 rows each
+int rmsnorm_bwd_groups(long long rows) {
+  const long long g = (rows + 15) / 16;
+  return (int)(g < 1024 ? g : 1024);
+}
+
+// deterministic column sums of part [P][ld] (columns col0 .. col0 + ncols - 1) into out, in
+// two levels (32-row partial sums in tmp [ceil(P / 32)][ncols], then their sum)
+hipError_t colsum(const float* part, int P, long long ld, int col0, int ncols, float* tmp, float* out, hipStream_t st) {
+  const int rs = (P + 31) / 32;
+  if (rs == 1) {
+    colsum_kernel<<<dim3(blocks_for(ncols, 64), 1), 256, 0, st>>>(part, P, ld, col0, ncols, out);
+    return hipGetLastError();
+  }
+  colsum_kernel<<<dim3(blocks_for(ncols, 64), rs), 256, 0, st>>>(part, P, ld, col0, ncols, tmp);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return colsum(tmp, rs, ncols, 0, ncols, tmp + (long long)rs * ncols, out, st);
+}
 
 hipError_t launch_rmsnorm_bwd(const float* dxn, const float* x, const float* rstd, const float* gain, const float* dres,
                               const float* dgate, const float* wg, long long rows, int C, float* dx, uint16_t* dx16,
                               float* part, float* dgain, float* dwg, hipStream_t st) {
-  const int waves = rmsnorm_bwd_waves(rows);
-  const int rpw = (int)((rows + waves - 1) / waves);
-  const unsigned nb = blocks_for(waves, 4);
+  const int ng = rmsnorm_bwd_groups(rows);
+  const int rpg = (int)((rows + ng - 1) / ng);
   bf16_t* o16 = reinterpret_cast<bf16_t*>(dx16);
   switch (C) {
-    case 128: rmsnorm_bwd_kernel<1><<<nb, 256, 0, st>>>(dxn, x, rstd, gain, dres, dgate, wg, rows, rpw, dx, o16, part); break;
-    case 256: rmsnorm_bwd_kernel<2><<<nb, 256, 0, st>>>(dxn, x, rstd, gain, dres, dgate, wg, rows, rpw, dx, o16, part); break;
-    case 512: rmsnorm_bwd_kernel<4><<<nb, 256, 0, st>>>(dxn, x, rstd, gain, dres, dgate, wg, rows, rpw, dx, o16, part); break;
-    case 1024: rmsnorm_bwd_kernel<8><<<nb, 256, 0, st>>>(dxn, x, rstd, gain, dres, dgate, wg, rows, rpw, dx, o16, part); break;
+    case 128: rmsnorm_bwd_kernel<1><<<ng, 256, 0, st>>>(dxn, x, rstd, gain, dres, dgate, wg, rows, rpg, dx, o16, part); break;
+    case 256: rmsnorm_bwd_kernel<2><<<ng, 256, 0, st>>>(dxn, x, rstd, gain, dres, dgate, wg, rows, rpg, dx, o16, part); break;
+    case 512: rmsnorm_bwd_kernel<4><<<ng, 256, 0, st>>>(dxn, x, rstd, gain, dres, dgate, wg, rows, rpg, dx, o16, part); break;
+    case 1024: rmsnorm_bwd_kernel<8><<<ng, 256, 0, st>>>(dxn, x, rstd, gain, dres, dgate, wg, rows, rpg, dx, o16, part); break;
     default: return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int P = (int)nb * 4;
-  colsum_kernel<<<blocks_for(C, 64), 256, 0, st>>>(part, P, 4LL * C, 0, C, dgain);
-  if (dgate) colsum_kernel<<<blocks_for(3LL * C, 64), 256, 0, st>>>(part, P, 4LL * C, C, 3 * C, dwg);
-  return hipGetLastError();
+  float* tmp = part + (long long)ng * 4 * C;
+  e = colsum(part, ng, 4LL * C, 0, C, tmp, dgain, st);
+  if (e != hipSuccess || !dgate) return e;
+  return colsum(part, ng, 4LL * C, C, 3 * C, tmp, dwg, st);
 }
 
 size_t rmsnorm_bwd_part_bytes(long long rows, int C) {
-  const long long waves = ((long long)rmsnorm_bwd_waves(rows) + 3) / 4 * 4;
-  return sizeof(float) * (size_t)waves * 4 * C;
+  // partial rows, then the first level of the column sums (at most 32 rows) and the second
+  const long long ng = rmsnorm_bwd_groups(rows);
+  return sizeof(float) * (size_t)(ng + 32 + 1) * 4 * C;
 }
 
 hipError_t launch_splitk_sum(const float* part, int S, long long stride, long long count, float* out, hipStream_t st) {
   if (count % 4 || stride % 4) return hipErrorInvalidValue;
   splitk_sum_kernel<<<blocks_for(count / 4, 256), 256, 0, st>>>(part, S, stride, count / 4, out);
-  return hipGetLastError();
-}
-
-hipError_t launch_swiglu_fwd(const uint16_t* uw, long long rows, int F, uint16_t* a, hipStream_t st) {
-  if (F % 8) return hipErrorInvalidValue;
-  swiglu_fwd_kernel<<<blocks_for(rows * (F / 8), 256), 256, 0, st>>>(reinterpret_cast<const bf16_t*>(uw), rows, F,
-                                                                      reinterpret_cast<bf16_t*>(a));
-  return hipGetLastError();
-}
-
-hipError_t launch_swiglu_bwd(const float* da, const uint16_t* uw, long long rows, int F, uint16_t* duw, hipStream_t st) {
-  if (F % 8) return hipErrorInvalidValue;
-  swiglu_bwd_kernel<<<blocks_for(rows * (F / 8), 256), 256, 0, st>>>(da, reinterpret_cast<const bf16_t*>(uw), rows, F,
-                                                                      reinterpret_cast<bf16_t*>(duw));
   return hipGetLastError();
 }
 
@@ -599,6 +651,12 @@ hipError_t launch_pack_qkv(const float* dq, const float* dk, const float* dv, lo
 hipError_t launch_cast_bf16(const float* src, long long n, uint16_t* dst, hipStream_t st) {
   if (n % 8) return hipErrorInvalidValue;
   cast_bf16_kernel<<<blocks_for(n / 8, 256), 256, 0, st>>>(src, n / 8, reinterpret_cast<bf16_t*>(dst));
+  return hipGetLastError();
+}
+
+hipError_t launch_cast_w13(const float* w1, const float* w3, int F, int C, uint16_t* dst, hipStream_t st) {
+  if (F % 32 || C % 8) return hipErrorInvalidValue;
+  cast_w13_kernel<<<blocks_for(2LL * F * (C / 8), 256), 256, 0, st>>>(w1, w3, F, C, reinterpret_cast<bf16_t*>(dst));
   return hipGetLastError();
 }
 

@@ -147,7 +147,11 @@ struct GemmMat {
   long long ld;
   int heads, lgn, lgd;
 };
-enum GemmEpi { kEpiF32 = 0, kEpiBf16 = 1, kEpiHeads = 2, kEpiPart = 3 };
+// kEpiSwigluFwd: B rows interleave W_1 and W_3 in groups of 32 (launch_cast_w13); writes
+//   u | w (bf16 [M, 2 ffn], stacked) to out and silu(u) w (bf16 [M, ffn]) to out2.
+// kEpiSwigluBwd: the product is da [M, ffn]; with u | w from aux writes du | dw (bf16
+//   [M, 2 ffn]) to out.
+enum GemmEpi { kEpiF32 = 0, kEpiBf16 = 1, kEpiHeads = 2, kEpiPart = 3, kEpiSwigluFwd = 4, kEpiSwigluBwd = 5 };
 struct GemmOut {
   int epi;
   void* out;            // kEpiF32 / kEpiBf16: [M, ldc]; kEpiPart: f32 [splits][M][ldc]
@@ -156,6 +160,9 @@ struct GemmOut {
   long long ldr;
   uint16_t* parts[3];   // kEpiHeads: column block p (part_cols wide) -> head-major parts[p]
   int part_cols, heads, lgn, lgd;
+  const uint16_t* aux;  // kEpiSwigluBwd: u | w
+  void* out2;           // kEpiSwigluFwd: silu(u) w
+  int ffn;
 };
 // C[M, N] = sum_k A(m, k) B(n, k); trans = false: A [M, K], B [N, K]; trans = true: A [K, M],
 // B [K, N]. M, N multiples of 128, K of 64; splits > 1 only with kEpiPart.
@@ -169,11 +176,10 @@ hipError_t launch_rmsnorm_bwd(const float* dxn, const float* x, const float* rst
                               float* part, float* dgain, float* dwg, hipStream_t st);
 size_t rmsnorm_bwd_part_bytes(long long rows, int C);
 hipError_t launch_splitk_sum(const float* part, int S, long long stride, long long count, float* out, hipStream_t st);
-hipError_t launch_swiglu_fwd(const uint16_t* uw, long long rows, int F, uint16_t* a, hipStream_t st);
-hipError_t launch_swiglu_bwd(const float* da, const uint16_t* uw, long long rows, int F, uint16_t* duw, hipStream_t st);
 hipError_t launch_pack_qkv(const float* dq, const float* dk, const float* dv, long long rows, int C, int H, int lgn,
                            int lgd, uint16_t* out, hipStream_t st);
 hipError_t launch_cast_bf16(const float* src, long long n, uint16_t* dst, hipStream_t st);
+hipError_t launch_cast_w13(const float* w1, const float* w3, int F, int C, uint16_t* dst, hipStream_t st);
 hipError_t launch_cast_t(const float* src, int rows, int cols, uint16_t* dst, long long ldd, hipStream_t st);
 
 // timing.cpp: optional per-phase HIP-event timing (see bsa_timing_enable in bsa.h)
