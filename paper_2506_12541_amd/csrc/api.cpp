@@ -840,7 +840,7 @@ bsa_status_t bsa_block_forward(const bsa_params_t* p, int32_t ffn_dim, const bsa
   BSA_PHASE("blk.elem", st, {
     BSA_HIP(bsa::launch_cast_bf16(w->wqkv, 3LL * C * C, wqkv, st), "cast wqkv");
     BSA_HIP(bsa::launch_cast_bf16(w->wo, (long long)C * C, wo, st), "cast wo");
-    BSA_HIP(bsa::launch_cast_w13(w->w1, w->w3, F, C, w13, st), "cast w1, w3");
+    BSA_HIP(bsa::launch_cast_w13(w->w1, w->w3, F, C, bsa::gemm_wave_cols((int)M, 2 * F), w13, st), "cast w1, w3");
     BSA_HIP(bsa::launch_cast_bf16(w->w2, (long long)C * F, w2, st), "cast w2");
   });
   BSA_PHASE("blk.norm", st,

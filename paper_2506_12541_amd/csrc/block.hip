@@ -23,12 +23,12 @@ constexpr float kNormEps = 1e-6f;
 // Accumulator lane L holds C[m0 + L % 16][n0 + 4 (L / 16) + e], e = 0..3 (the B fragment
 // is the first MFMA operand), so each lane stores 4 consecutive columns.
 
-// 16-byte chunk swizzle of a staged tile row: 8 chunks per row (row-fragment reads of 16
-// consecutive rows) or 16 chunks per row (transposing reads of 8 consecutive rows, chunk
-// pairs on distinct banks).
+// 16-byte chunk swizzle of a staged tile row: 4 or 8 chunks per row (row-fragment reads
+// of 16 consecutive rows on distinct banks) or 16 and more chunks per row (transposing
+// reads of 8 consecutive rows, chunk pairs on distinct banks).
 template <int COLS>
 __device__ __forceinline__ int tile_swz(int x) {
-  return COLS == 64 ? (x & 7) : 2 * (x & 7);
+  return COLS == 32 ? ((x >> 2) & 3) : COLS == 64 ? (x & 7) : 2 * (x & 7);
 }
 
 // Staging of ROWS x COLS tiles of a logical row-major operand into LDS by the four waves
@@ -37,10 +37,11 @@ __device__ __forceinline__ int tile_swz(int x) {
 // The element offset of that chunk splits into a per-lane part fixed for the kernel and a
 // wave-uniform part per contraction tile (tile kt starts at column 64 kt of the plain form
 // or at row 64 kt of the transposed form; shapes are whole tiles, as the launcher checks).
-template <int ROWS, int COLS>
+template <int ROWS, int COLS, int NW>
 struct TileLoader {
   static constexpr int CPR = COLS / 8;
-  static constexpr int NU = ROWS * CPR / 256;   // wave instructions per wave
+  static constexpr int NU = ROWS * CPR / (64 * NW);   // wave instructions per wave
+  static_assert(NU * 64 * NW == ROWS * CPR, "tile / wave split");
   const bf16_t* p;
   long long lane_off[NU];
 
@@ -70,72 +71,82 @@ struct TileLoader {
   }
 };
 
-// Wave-uniform element offset of contraction tile kt (64 wide) of an operand.
-// Plain form: columns 64 kt (heads layout: d <= 64 divides 64, so the tile covers 64 / d
-// whole heads, 64 N elements further per tile). Transposed form: rows 64 kt (heads layout:
-// 64 divides n, so a tile stays inside one cloud).
-template <bool TR>
+// Wave-uniform element offset of contraction tile kt (BK wide) of an operand.
+// Plain form: columns BK kt; in the heads layout a tile stays inside one head (BK <= d) or
+// covers whole heads (d divides BK), n d elements per head. Transposed form: rows BK kt;
+// in the heads layout BK divides n, so a tile stays inside one cloud.
+template <bool TR, int BK>
 __device__ __forceinline__ long long kt_offset(const GemmMat& m, int kt) {
-  const long long k0 = (long long)kt * 64;
-  if (!TR) return m.heads == 0 ? k0 : k0 << m.lgn;
+  const long long k0 = (long long)kt * BK;
+  if (!TR) {
+    if (m.heads == 0) return k0;
+    return ((k0 >> m.lgd) << (m.lgn + m.lgd)) + (k0 & ((1LL << m.lgd) - 1));
+  }
   if (m.heads == 0) return k0 * m.ld;
   const long long b = k0 >> m.lgn, t = k0 & ((1LL << m.lgn) - 1);
   return ((b * m.heads << m.lgn) + t) << m.lgd;
 }
 
+template <int BK>
 __device__ __forceinline__ bf16x8 frag_row(const bf16_t* t, int row, int lc) {
-  return *reinterpret_cast<const bf16x8*>(t + row * 64 + 8 * (lc ^ tile_swz<64>(row)));
+  return *reinterpret_cast<const bf16x8*>(t + row * BK + 8 * (lc ^ tile_swz<BK>(row)));
+}
+
+// Workgroup barrier without a memory fence: the waves' direct-to-LDS loads are already
+// waited for by each wave (vmcnt), and later tiles stay in flight across it (the fence of
+// __syncthreads would wait for every outstanding load). The empty statements keep the
+// compiler from moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// s_waitcnt with vmcnt = V (expcnt and lgkmcnt left at their maxima)
+template <int V>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(V >= 0 && V < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
 // LDS byte addresses of the two transposing reads that give lane (p = L % 16, j = L / 16)
 // the operand X[k0 + 4j + i][m0 + p] (i = 0..3) and X[k0 + 16 + 4j + i][m0 + p] of a
-// [64][128] tile X: within each 16-lane group, ds_read_b64_tr_b16 hands lane l element
+// [64][COLS] tile X: within each 16-lane group, ds_read_b64_tr_b16 hands lane l element
 // l % 4 of the 4-element runs addressed by lanes l / 4, 4 + l / 4, 8 + l / 4, 12 + l / 4, so
 // lane p addresses row k0 + 4j + p / 4 (then + 16) at columns m0 + 4 (p % 4) + [0, 4).
+template <int COLS>
 __device__ __forceinline__ void tr_addr(const bf16_t* t, int k0, int m0, int lane, uint32_t& o0, uint32_t& o1) {
   const int p = lane & 15, j = lane >> 4;
   const int col = m0 + 4 * (p & 3);
   const int lc = col >> 3, sub = col & 7;
   const int x0 = k0 + 4 * j + (p >> 2), x1 = x0 + 16;
-  const bf16_t* a0 = t + x0 * 128 + 8 * (lc ^ tile_swz<128>(x0)) + sub;
-  const bf16_t* a1 = t + x1 * 128 + 8 * (lc ^ tile_swz<128>(x1)) + sub;
+  const bf16_t* a0 = t + x0 * COLS + 8 * (lc ^ tile_swz<COLS>(x0)) + sub;
+  const bf16_t* a1 = t + x1 * COLS + 8 * (lc ^ tile_swz<COLS>(x1)) + sub;
   o0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)a0;
   o1 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)a1;
 }
 
-// The eight operand fragments of one 32-deep contraction step of the transposed form (A
-// tiles i = 0..3 at columns am0 + 16 i, B tiles at bm0 + 16 j), issued as one statement
-// that also waits for them: every use of the results follows the wait.
-__device__ __forceinline__ void tr_frags(const bf16_t* as, const bf16_t* bs, int k0, int am0, int bm0, int lane,
-                                         uint4 (&af)[4], uint4 (&bf)[4]) {
-  uint32_t a[8], b[8];
+// Four operand fragments (columns m0 + 16 i, i = 0..3) of one 32-deep contraction step of
+// the transposed form, issued as one statement that also waits for them: every use of the
+// results follows the wait.
+template <int COLS>
+__device__ __forceinline__ void tr_frags4(const bf16_t* t, int k0, int m0, int lane, bf16x8 (&f)[4]) {
+  uint32_t a[8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    tr_addr(as, k0, am0 + 16 * i, lane, a[2 * i], a[2 * i + 1]);
-    tr_addr(bs, k0, bm0 + 16 * i, lane, b[2 * i], b[2 * i + 1]);
-  }
-  uint2 r[16];
+  for (int i = 0; i < 4; ++i) tr_addr<COLS>(t, k0, m0 + 16 * i, lane, a[2 * i], a[2 * i + 1]);
+  uint2 r[8];
   asm volatile(
-      "ds_read_b64_tr_b16 %0, %16\n\tds_read_b64_tr_b16 %1, %17\n\t"
-      "ds_read_b64_tr_b16 %2, %18\n\tds_read_b64_tr_b16 %3, %19\n\t"
-      "ds_read_b64_tr_b16 %4, %20\n\tds_read_b64_tr_b16 %5, %21\n\t"
-      "ds_read_b64_tr_b16 %6, %22\n\tds_read_b64_tr_b16 %7, %23\n\t"
-      "ds_read_b64_tr_b16 %8, %24\n\tds_read_b64_tr_b16 %9, %25\n\t"
-      "ds_read_b64_tr_b16 %10, %26\n\tds_read_b64_tr_b16 %11, %27\n\t"
-      "ds_read_b64_tr_b16 %12, %28\n\tds_read_b64_tr_b16 %13, %29\n\t"
-      "ds_read_b64_tr_b16 %14, %30\n\tds_read_b64_tr_b16 %15, %31\n\t"
+      "ds_read_b64_tr_b16 %0, %8\n\tds_read_b64_tr_b16 %1, %9\n\t"
+      "ds_read_b64_tr_b16 %2, %10\n\tds_read_b64_tr_b16 %3, %11\n\t"
+      "ds_read_b64_tr_b16 %4, %12\n\tds_read_b64_tr_b16 %5, %13\n\t"
+      "ds_read_b64_tr_b16 %6, %14\n\tds_read_b64_tr_b16 %7, %15\n\t"
       "s_waitcnt lgkmcnt(0)"
-      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]),
-        "=&v"(r[7]), "=&v"(r[8]), "=&v"(r[9]), "=&v"(r[10]), "=&v"(r[11]), "=&v"(r[12]), "=&v"(r[13]),
-        "=&v"(r[14]), "=&v"(r[15])
-      : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7]), "v"(b[0]),
-        "v"(b[1]), "v"(b[2]), "v"(b[3]), "v"(b[4]), "v"(b[5]), "v"(b[6]), "v"(b[7])
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7])
+      : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]), "v"(a[7])
       : "memory");
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    af[i] = make_uint4(r[2 * i].x, r[2 * i].y, r[2 * i + 1].x, r[2 * i + 1].y);
-    bf[i] = make_uint4(r[8 + 2 * i].x, r[8 + 2 * i].y, r[8 + 2 * i + 1].x, r[8 + 2 * i + 1].y);
-  }
+  for (int i = 0; i < 4; ++i)
+    f[i] = __builtin_bit_cast(bf16x8, make_uint4(r[2 * i].x, r[2 * i].y, r[2 * i + 1].x, r[2 * i + 1].y));
 }
 
 struct GemmArgs {
@@ -146,22 +157,33 @@ struct GemmArgs {
   long long split_stride;   // elements between the partial products of two splits
 };
 
-template <bool TR>
-__global__ void __launch_bounds__(256, 2) gemm_kernel(GemmArgs g) {
-  __shared__ __attribute__((aligned(1024))) bf16_t as0[8192], bs0[8192], as1[8192], bs1[8192];
+// Workgroup tile BM x BN of WM x WN waves (wave tile BM / WM x BN / WN in 16 x 16
+// accumulator tiles); contraction tiles of BK in a ring of NS LDS stages, NS - 1 of them in
+// flight while one feeds the matrix cores.
+template <bool TR, int BM, int BN, int WM, int WN, int BK, int NS>
+__global__ void __launch_bounds__(64 * WM * WN) gemm_kernel(GemmArgs g) {
+  constexpr int NW = WM * WN;
+  constexpr int TMW = BM / WM, TNW = BN / WN;
+  constexpr int FI = TMW / 16, FJ = TNW / 16;
+  static_assert(FI % 4 == 0 && FJ % 4 == 0, "wave tile");
+  static_assert(NS >= 2 && NS <= 4 && (BK == 32 || BK == 64), "pipeline");
+  constexpr int AE = BM * BK, BE = BN * BK;
+  __shared__ __attribute__((aligned(1024))) bf16_t as0[AE], bs0[BE], as1[AE], bs1[BE];
+  __shared__ __attribute__((aligned(1024))) bf16_t as2[NS > 2 ? AE : 8], bs2[NS > 2 ? BE : 8];
+  __shared__ __attribute__((aligned(1024))) bf16_t as3[NS > 3 ? AE : 8], bs3[NS > 3 ? BE : 8];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
+  const int wm = wid / WN, wn = wid % WN;
   // workgroups are dealt to the 8 XCDs round-robin; give each XCD a contiguous run of
   // tiles (row panels walked column tile by column tile) so it re-reads A from its own L2
   const int nt = gridDim.x;
   int id = blockIdx.x;
   if ((nt & 7) == 0) id = (id & 7) * (nt >> 3) + (id >> 3);
   const int tm = id / g.ntn, tn = id - tm * g.ntn;
-  const long long m0 = (long long)tm * 128, n0 = (long long)tn * 128;
+  const long long m0 = (long long)tm * BM, n0 = (long long)tn * BN;
   const int kt0 = blockIdx.y * g.kt_per, kt1 = kt0 + g.kt_per;
 
-  constexpr int AR = TR ? 64 : 128, AC = TR ? 128 : 64;
-  TileLoader<AR, AC> la, lb;
+  TileLoader<TR ? BK : BM, TR ? BM : BK, NW> la;
+  TileLoader<TR ? BK : BN, TR ? BN : BK, NW> lb;
   if (!TR) {
     la.init(g.a, m0, 0, wid, lane);
     lb.init(g.b, n0, 0, wid, lane);
@@ -169,53 +191,60 @@ __global__ void __launch_bounds__(256, 2) gemm_kernel(GemmArgs g) {
     la.init(g.a, 0, (int)m0, wid, lane);
     lb.init(g.b, 0, (int)n0, wid, lane);
   }
-  auto issue = [&](int kt, bf16_t* as, bf16_t* bs) {
-    la.issue(as, kt_offset<TR>(g.a, kt), wid);
-    lb.issue(bs, kt_offset<TR>(g.b, kt), wid);
+  constexpr int PER = decltype(la)::NU + decltype(lb)::NU;   // wave load instructions per tile
+  bf16_t* const AS[4] = {as0, as1, as2, as3};
+  bf16_t* const BS[4] = {bs0, bs1, bs2, bs3};
+  auto issue = [&](int kt, int st) {
+    la.issue(AS[st], kt_offset<TR, BK>(g.a, kt), wid);
+    lb.issue(BS[st], kt_offset<TR, BK>(g.b, kt), wid);
   };
-  f32x4 acc[4][4];
+  f32x4 acc[FI][FJ];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < FI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < FJ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto step = [&](const bf16_t* as, const bf16_t* bs) {
+  auto compute = [&](const bf16_t* as, const bf16_t* bs) {
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 af[4], bfr[4];
+    for (int ks = 0; ks < BK / 32; ++ks) {
+      bf16x8 af[FI], bfr[FJ];
       if (!TR) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          af[i] = frag_row(as, wm * 64 + 16 * i + (lane & 15), 4 * ks + (lane >> 4));
-          bfr[i] = frag_row(bs, wn * 64 + 16 * i + (lane & 15), 4 * ks + (lane >> 4));
-        }
-      } else {
-        uint4 au[4], bu[4];
-        tr_frags(as, bs, 32 * ks, wm * 64, wn * 64, lane, au, bu);
+        for (int i = 0; i < FI; ++i) af[i] = frag_row<BK>(as, wm * TMW + 16 * i + (lane & 15), 4 * ks + (lane >> 4));
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          af[i] = __builtin_bit_cast(bf16x8, au[i]);
-          bfr[i] = __builtin_bit_cast(bf16x8, bu[i]);
-        }
+        for (int j = 0; j < FJ; ++j) bfr[j] = frag_row<BK>(bs, wn * TNW + 16 * j + (lane & 15), 4 * ks + (lane >> 4));
+      } else {
+#pragma unroll
+        for (int i = 0; i < FI; i += 4)
+          tr_frags4<BM>(as, 32 * ks, wm * TMW + 16 * i, lane, *reinterpret_cast<bf16x8(*)[4]>(&af[i]));
+#pragma unroll
+        for (int j = 0; j < FJ; j += 4)
+          tr_frags4<BN>(bs, 32 * ks, wn * TNW + 16 * j, lane, *reinterpret_cast<bf16x8(*)[4]>(&bfr[j]));
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < FI; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mma(bfr[j], af[i], acc[i][j]);
+        for (int j = 0; j < FJ; ++j) acc[i][j] = mma(bfr[j], af[i], acc[i][j]);
     }
   };
 
-  issue(kt0, as0, bs0);
-  for (int kt = kt0; kt < kt1; kt += 2) {
-    vm_drain();        // this wave's loads of tile kt have landed
-    __syncthreads();   // ... and every wave's; stage 1 is no longer read
-    if (kt + 1 < kt1) issue(kt + 1, as1, bs1);
-    step(as0, bs0);
-    if (kt + 1 < kt1) {
-      vm_drain();
-      __syncthreads();
-      if (kt + 2 < kt1) issue(kt + 2, as0, bs0);
-      step(as1, bs1);
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (kt0 + s < kt1) issue(kt0 + s, s);
+  for (int kt = kt0; kt < kt1; kt += NS) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const int t = kt + s;
+      if (t < kt1) {
+        // tile t has landed once at most the NS - 2 tiles issued after it are in flight
+        if (t + NS - 2 < kt1)
+          vm_wait<(NS - 2) * PER>();
+        else
+          vm_drain();
+        lds_barrier();     // every wave's loads of tile t are visible; stage s - 1 is free
+        if (t + NS - 1 < kt1) issue(t + NS - 1, (s + NS - 1) % NS);
+        compute(AS[s], BS[s]);
+      }
     }
   }
 
@@ -225,20 +254,21 @@ __global__ void __launch_bounds__(256, 2) gemm_kernel(GemmArgs g) {
     return make_uint2((uint32_t)f2bf(a0) | ((uint32_t)f2bf(a1) << 16), (uint32_t)f2bf(a2) | ((uint32_t)f2bf(a3) << 16));
   };
   if (o.epi == kEpiSwigluFwd) {
-    // B rows interleaved in groups of 64 (32 of W_1, then the same 32 of W_3): the wave's
-    // column tiles j and j + 2 hold u and w of the same hidden units f
+    // B rows interleaved in groups of TNW (TNW / 2 rows of W_1, then the same rows of
+    // W_3; launch_cast_w13 with gemm_wave_cols): the wave's column tiles j and j + FJ / 2
+    // hold u and w of the same hidden units f
     const int F = o.ffn;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const long long m = m0 + wm * 64 + 16 * i + r;
+    for (int i = 0; i < FI; ++i) {
+      const long long m = m0 + wm * TMW + 16 * i + r;
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int f = ((int)n0 + wn * 64) / 2 + 16 * j + 4 * jq;
+      for (int j = 0; j < FJ / 2; ++j) {
+        const int f = ((int)n0 + wn * TNW) / 2 + 16 * j + 4 * jq;
         float u[4], w[4], a[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           u[e] = bf2f(f2bf(acc[i][j][e]));
-          w[e] = bf2f(f2bf(acc[i][j + 2][e]));
+          w[e] = bf2f(f2bf(acc[i][j + FJ / 2][e]));
           a[e] = u[e] / (1.0f + __expf(-u[e])) * w[e];
         }
         bf16_t* uw = reinterpret_cast<bf16_t*>(o.out) + m * 2 * F + f;
@@ -250,11 +280,11 @@ __global__ void __launch_bounds__(256, 2) gemm_kernel(GemmArgs g) {
     return;
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const long long m = m0 + wm * 64 + 16 * i + r;
+  for (int i = 0; i < FI; ++i) {
+    const long long m = m0 + wm * TMW + 16 * i + r;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int n = (int)n0 + wn * 64 + 16 * j + 4 * jq;
+    for (int j = 0; j < FJ; ++j) {
+      const int n = (int)n0 + wn * TNW + 16 * j + 4 * jq;
       f32x4 v = acc[i][j];
       if (o.epi == kEpiF32 || o.epi == kEpiPart) {
         float* dst = reinterpret_cast<float*>(o.out) + (o.epi == kEpiPart ? blockIdx.y * g.split_stride : 0) +
@@ -527,18 +557,18 @@ __global__ void __launch_bounds__(256) cast_t_kernel(const float* __restrict__ s
   for (int k = 0; k < 4; ++k) dst[(long long)(c0 + ty + 8 * k) * ldd + r0 + tx] = f2bf(tile[tx][ty + 8 * k]);
 }
 
-// dst rows of the interleaved [W_1; W_3] operand: row r takes row 32 (r / 64) + r % 64 of
-// W_1 when r % 64 < 32, else row 32 (r / 64) + r % 64 - 32 of W_3 (f32 -> bf16, eight
-// elements per thread; C a multiple of 8).
+// dst rows of the interleaved [W_1; W_3] operand in groups of G rows: row r takes row
+// (G / 2)(r / G) + r % G of W_1 when r % G < G / 2, else row (G / 2)(r / G) + r % G - G / 2
+// of W_3 (f32 -> bf16, eight elements per thread; C a multiple of 8).
 __global__ void __launch_bounds__(256) cast_w13_kernel(const float* __restrict__ w1, const float* __restrict__ w3,
-                                                       int F, int C, bf16_t* __restrict__ dst) {
+                                                       int F, int C, int G, bf16_t* __restrict__ dst) {
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   const int c8 = C / 8;
   if (i >= 2LL * F * c8) return;
   const long long r = i / c8;
   const int c = (int)(i - r * c8) * 8;
-  const int g = (int)(r >> 6), wi = (int)(r & 63);
-  const float* src = wi < 32 ? w1 + (long long)(32 * g + wi) * C : w3 + (long long)(32 * g + wi - 32) * C;
+  const int g = (int)(r / G), wi = (int)(r % G), h = G / 2;
+  const float* src = wi < h ? w1 + (long long)(h * g + wi) * C : w3 + (long long)(h * g + wi - h) * C;
   const f32x8 v = load_chunk(src + c);
   float o[8];
 #pragma unroll
@@ -550,26 +580,46 @@ unsigned blocks_for(long long n, int per) { return (unsigned)((n + per - 1) / pe
 
 }  // namespace
 
+// 256 x 256 workgroup tiles of 8 waves (4 x 2, 64 x 128 each) where the shape allows and
+// gives at least 256 tiles (or splits the contraction), else 128 x 128 tiles of 4 waves
+// (64 x 64 each); contraction tiles of 64 in two stages. (Measured on the block's shapes:
+// 256 x 256 tiles of 4 x 2 waves ran fastest, ahead of 2 x 4 waves, 256 x 128 and
+// 128 x 256 tiles, and of 32-deep tiles in four stages.)
+int gemm_tile(int M, int N, bool split) {
+  return M % 256 == 0 && N % 256 == 0 && (split || (long long)(M / 256) * (N / 256) >= 256) ? 256 : 128;
+}
+
 hipError_t launch_gemm(bool trans, const GemmMat& a, const GemmMat& b, int M, int N, long long K, int splits,
                        const GemmOut& o, hipStream_t st) {
   if (M <= 0 || N <= 0 || K <= 0 || M % 128 || N % 128 || K % 64 || splits < 1 || (K / 64) % splits)
     return hipErrorInvalidValue;
   if (o.epi != kEpiPart && splits != 1) return hipErrorInvalidValue;
-  GemmArgs g{a, b, N / 128, (int)((K / 64) / splits), o, (long long)M * o.ldc};
-  const dim3 grid((unsigned)((M / 128) * (N / 128)), (unsigned)splits);
-  if (trans)
-    gemm_kernel<true><<<grid, 256, 0, st>>>(g);
-  else
-    gemm_kernel<false><<<grid, 256, 0, st>>>(g);
+  const int T = gemm_tile(M, N, trans);
+  GemmArgs g{a, b, N / T, (int)((K / 64) / splits), o, (long long)M * o.ldc};
+  const dim3 grid((unsigned)((M / T) * (N / T)), (unsigned)splits);
+  if (T == 256) {
+    if (trans)
+      gemm_kernel<true, 256, 256, 4, 2, 64, 2><<<grid, 512, 0, st>>>(g);
+    else
+      gemm_kernel<false, 256, 256, 4, 2, 64, 2><<<grid, 512, 0, st>>>(g);
+  } else {
+    if (trans)
+      gemm_kernel<true, 128, 128, 2, 2, 64, 2><<<grid, 256, 0, st>>>(g);
+    else
+      gemm_kernel<false, 128, 128, 2, 2, 64, 2><<<grid, 256, 0, st>>>(g);
+  }
   return hipGetLastError();
 }
 
+int gemm_wave_cols(int M, int N) { return gemm_tile(M, N, false) == 256 ? 128 : 64; }
+
 int gemm_splits(int M, int N, long long K) {
-  const long long tiles = (long long)(M / 128) * (N / 128);
+  const int T = gemm_tile(M, N, true);
+  const long long tiles = (long long)(M / T) * (N / T);
   const long long nkt = K / 64;
   int s = 1;
   // enough workgroups to fill the chip, at least 16 contraction tiles per split
-  while (tiles * s < 1024 && nkt % (2 * s) == 0 && nkt / (2 * s) >= 16) s *= 2;
+  while (tiles * s < 512 && nkt % (2 * s) == 0 && nkt / (2 * s) >= 16) s *= 2;
   return s;
 }
 
@@ -654,9 +704,9 @@ hipError_t launch_cast_bf16(const float* src, long long n, uint16_t* dst, hipStr
   return hipGetLastError();
 }
 
-hipError_t launch_cast_w13(const float* w1, const float* w3, int F, int C, uint16_t* dst, hipStream_t st) {
-  if (F % 32 || C % 8) return hipErrorInvalidValue;
-  cast_w13_kernel<<<blocks_for(2LL * F * (C / 8), 256), 256, 0, st>>>(w1, w3, F, C, reinterpret_cast<bf16_t*>(dst));
+hipError_t launch_cast_w13(const float* w1, const float* w3, int F, int C, int G, uint16_t* dst, hipStream_t st) {
+  if (G <= 0 || G % 2 || (2 * F) % G || C % 8) return hipErrorInvalidValue;
+  cast_w13_kernel<<<blocks_for(2LL * F * (C / 8), 256), 256, 0, st>>>(w1, w3, F, C, G, reinterpret_cast<bf16_t*>(dst));
   return hipGetLastError();
 }
 

@@ -147,7 +147,7 @@ struct GemmMat {
   long long ld;
   int heads, lgn, lgd;
 };
-// kEpiSwigluFwd: B rows interleave W_1 and W_3 in groups of 32 (launch_cast_w13); writes
+// kEpiSwigluFwd: B rows interleave W_1 and W_3 (launch_cast_w13); writes
 //   u | w (bf16 [M, 2 ffn], stacked) to out and silu(u) w (bf16 [M, ffn]) to out2.
 // kEpiSwigluBwd: the product is da [M, ffn]; with u | w from aux writes du | dw (bf16
 //   [M, 2 ffn]) to out.
@@ -179,7 +179,9 @@ hipError_t launch_splitk_sum(const float* part, int S, long long stride, long lo
 hipError_t launch_pack_qkv(const float* dq, const float* dk, const float* dv, long long rows, int C, int H, int lgn,
                            int lgd, uint16_t* out, hipStream_t st);
 hipError_t launch_cast_bf16(const float* src, long long n, uint16_t* dst, hipStream_t st);
-hipError_t launch_cast_w13(const float* w1, const float* w3, int F, int C, uint16_t* dst, hipStream_t st);
+// [W_1; W_3] interleaved in groups of G rows for kEpiSwigluFwd; G = gemm_wave_cols(M, 2F)
+hipError_t launch_cast_w13(const float* w1, const float* w3, int F, int C, int G, uint16_t* dst, hipStream_t st);
+int gemm_wave_cols(int M, int N);
 hipError_t launch_cast_t(const float* src, int rows, int cols, uint16_t* dst, long long ldd, hipStream_t st);
 
 // timing.cpp: optional per-phase HIP-event timing (see bsa_timing_enable in bsa.h)
