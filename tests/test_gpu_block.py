@@ -155,3 +155,72 @@ def test_block_small_group_compression():
 def test_block_airflow():
     print("block parity airflow settings, 2 clouds (C = 256, F = 1024)", flush=True)
     run_block(AIRFLOW2)
+
+
+@pytest.mark.timeout(400)
+def test_block_scaling_sampled():
+    """The block at the model sweep's largest size (65536 tokens, C = 512, F = 2048: the
+    layer of the benchmarked workload), forward through the C ABI. The oracle follows 128
+    sampled rows (8 groups of 16) through the block: norm 1 and the Q/K/V products for every
+    row (the layer's keys), the layer's three branches for the sampled rows of all heads
+    (the GPU's selection), then the output projection, norm 2 and the SwiGLU per row."""
+    from oracle import bsa as ob
+    cfg = CONFIGS[3]
+    print("block parity 65536 tokens (sampled rows)", flush=True)
+    valid = np.ones((1, cfg.n_pad), bool)
+    inp = make_block_inputs(cfg, valid, seed=3)
+    ffn = inp["ffn"]
+    p = gb.Params.from_config(cfg)
+    dev32 = lambda a: to_dev(a, torch.float32)
+    W = {n: dev32(a) for n, a in inp["W"].items()}
+    phk, phv = ({w: dev32(a) for w, a in inp[n].items()} for n in ("phi_k", "phi_v"))
+    y, saved = gb.block_forward(p, ffn, W, phk, phv, dev32(inp["x"]))
+    torch.cuda.synchronize()
+    f = lambda t: t.float().cpu().numpy()
+    sel = saved.sel_idx.cpu().numpy().astype(np.int64)[0]
+    H, d, C = cfg.heads, cfg.head_dim, cfg.heads * cfg.head_dim
+    P = oracle_params(cfg)
+    rnd = om.round_bf16
+    Wd = {k: np.asarray(v, np.float64) for k, v in inp["W"].items()}
+    x = np.asarray(inp["x"][0], np.float64)
+    xn1, _ = om.rmsnorm(x, Wd["g1"])
+    qkv = rnd(rnd(xn1) @ rnd(Wd["wqkv"]).T)
+    gate = xn1 @ Wd["wg"].T
+    rng = np.random.default_rng(8)
+    ngroups = cfg.n_pad // cfg.group
+    groups = np.unique(np.concatenate([[0, ngroups - 1], rng.choice(ngroups, 6, replace=False)]))
+    rows = (groups[:, None] * cfg.group + np.arange(cfg.group)[None, :]).reshape(-1)
+    vb = valid[0]
+    o = np.zeros((rows.size, C))
+    phk64 = {w: np.asarray(a, np.float64) for w, a in inp["phi_k"].items()}
+    phv64 = {w: np.asarray(a, np.float64) for w, a in inp["phi_v"].items()}
+    cvalid = ob.block_valid(vb, P.cmp_block)
+    sg = 1.0 / (1.0 + np.exp(-gate[rows]))
+    for h in range(H):
+        q, k, v = (qkv[:, i * C + h * d:i * C + (h + 1) * d] for i in range(3))
+        kc, _ = ob.compress(k, vb, phk64, P)
+        vc, _ = ob.compress(v, vb, phv64, P)
+        ob_ = np.zeros((cfg.n_pad, d))
+        for s0 in np.unique((rows // P.ball) * P.ball):
+            sl = slice(s0, s0 + P.ball)
+            ob_[sl] = ob.ball_branch(q[sl], k[sl], v[sl], vb[sl], P)[0]
+        oc = ob.compression_branch(q, kc, vc, cvalid, vb, P, rows=rows)[0]
+        os_ = ob.selection_branch(q, k, v, vb, sel[h], P, groups=groups)[0]
+        o[:, h * d:(h + 1) * d] = sg[:, 0:1] * ob_[rows] + sg[:, 1:2] * oc[rows] + sg[:, 2:3] * os_[rows]
+    errs = {"o": float(np.abs(f(saved.o)[0][:, rows].transpose(1, 0, 2).reshape(rows.size, C) - o).max())}
+    h_ref = x[rows] + rnd(o) @ rnd(Wd["wo"]).T
+    xn2, _ = om.rmsnorm(h_ref, Wd["g2"])
+    x2 = rnd(xn2)
+    u, w = rnd(x2 @ rnd(Wd["w1"]).T), rnd(x2 @ rnd(Wd["w3"]).T)
+    a = rnd(om.silu(u) * w)
+    y_ref = h_ref + a @ rnd(Wd["w2"]).T
+    scaled = {"h": _scaled(f(saved.h)[0][rows], h_ref), "u": _scaled(f(saved.uw)[0][rows][:, :ffn], u),
+              "w": _scaled(f(saved.uw)[0][rows][:, ffn:], w), "a": _scaled(f(saved.a)[0][rows], a),
+              "y": _scaled(f(y)[0][rows], y_ref)}
+    errs.update({k: f"{v:.2e}" for k, v in scaled.items()})
+    print(errs, flush=True)
+    tol = TOL["bf16"]
+    assert errs["o"] < tol, errs
+    bars = {k: (2 * tol + 2.0 ** -8 if k == "a" else tol) for k in scaled}
+    bad = {k: v for k, v in scaled.items() if not v < bars[k]}
+    assert not bad, bad
