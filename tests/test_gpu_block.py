@@ -151,6 +151,11 @@ def test_block_small_group_compression():
     run_block(SMALL, seed=12, q_coarsen=1, group_compression=1)
 
 
+def test_block_small_per_token_selection():
+    print("block parity small bf16, per-token selection (g = 1)", flush=True)
+    run_block(dataclasses.replace(SMALL, group=1), seed=13)
+
+
 @pytest.mark.timeout(300)
 def test_block_airflow():
     print("block parity airflow settings, 2 clouds (C = 256, F = 1024)", flush=True)
