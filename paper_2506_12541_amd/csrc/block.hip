@@ -618,8 +618,9 @@ int gemm_splits(int M, int N, long long K) {
   const long long tiles = (long long)(M / T) * (N / T);
   const long long nkt = K / 64;
   int s = 1;
-  // enough workgroups to fill the chip, at least 16 contraction tiles per split
-  while (tiles * s < 512 && nkt % (2 * s) == 0 && nkt / (2 * s) >= 16) s *= 2;
+  // about one workgroup per CU (each split adds a partial product the sum reads back), at
+  // least 16 contraction tiles per split
+  while (tiles * s < 256 && nkt % (2 * s) == 0 && nkt / (2 * s) >= 16) s *= 2;
   return s;
 }
 
