@@ -50,12 +50,17 @@ def test_block_flops():
 
 def test_traffic_summary_tracks_its_sources(tmp_path, monkeypatch):
     import bench
-    # the committed summary is reported while its kernel sources are unchanged, and not
-    # once a source differs from the recorded hash
-    assert bench.measured_traffic("bwd.kv_cmp", "scaling_65536") > 0
-    text = open(bench.TRAFFIC_FILE.format(phase="bwd_kv_cmp", workload="scaling_65536")).read()
+    # a summary is reported while the sources it names hash as recorded, and not once one
+    # of them changes (a summary of the same form as the committed ones, on a scratch file)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "traffic_{phase}_{workload}.txt"))
-    (tmp_path / "traffic_bwd_kv_cmp_scaling_65536.txt").write_text(text.replace("sources_sha256: ", "sources_sha256: 0"))
+    src = tmp_path / "kernel.hip"
+    src.write_text("// kernel source\n")
+    (tmp_path / "traffic_bwd_kv_cmp_scaling_65536.txt").write_text(
+        "# HBM traffic\nphase: bwd.kv_cmp\nworkload: scaling_65536\ntraffic_bytes_per_launch: 1234\n"
+        f"sources: kernel.hip\nsources_sha256: {bench._sources_sha(['kernel.hip'])}\n")
+    assert bench.measured_traffic("bwd.kv_cmp", "scaling_65536") == 1234
+    src.write_text("// kernel source, changed\n")
     assert bench.measured_traffic("bwd.kv_cmp", "scaling_65536") is None
 
 
