@@ -12,9 +12,10 @@ constexpr float kNormEps = 1e-6f;
 
 // ---- matrix products C[M, N] = sum_k A(m, k) B(n, k) ----
 //
-// Workgroup tile 128 x 128, four waves of 64 x 64 (4 x 4 accumulator tiles of 16 x 16),
-// contraction tiles of 64, two LDS stages filled by direct global->LDS loads while the
-// other stage feeds the matrix cores.
+// Workgroup tiles of 256 x 256 (eight waves of 64 x 128) or 128 x 128 (four waves of
+// 64 x 64) in 16 x 16 accumulator tiles, contraction tiles of 64, two LDS stages filled by
+// direct global->LDS loads while the other stage feeds the matrix cores (launch_gemm picks
+// the tile from the shape).
 //   plain form (trans = false): A [M, K] and B [N, K], contraction index fastest; tiles are
 //     staged as 128 rows x 64 (row fragments read with ds_read_b128);
 //   transposed form (trans = true): A [K, M] and B [K, N], the contraction runs over their
@@ -31,12 +32,12 @@ __device__ __forceinline__ int tile_swz(int x) {
   return COLS == 32 ? ((x >> 2) & 3) : COLS == 64 ? (x & 7) : 2 * (x & 7);
 }
 
-// Staging of ROWS x COLS tiles of a logical row-major operand into LDS by the four waves
-// of the workgroup. Each wave instruction fills 1 KB of consecutive LDS; lane L's 16 bytes
+// Staging of ROWS x COLS tiles of a logical row-major operand into LDS by the NW waves of
+// the workgroup. Each wave instruction fills 1 KB of consecutive LDS; lane L's 16 bytes
 // land at bytes [16 L, 16 L + 16) and the lane fetches the chunk the swizzle puts there.
 // The element offset of that chunk splits into a per-lane part fixed for the kernel and a
-// wave-uniform part per contraction tile (tile kt starts at column 64 kt of the plain form
-// or at row 64 kt of the transposed form; shapes are whole tiles, as the launcher checks).
+// wave-uniform part per contraction tile (kt_offset; shapes are whole tiles, as the
+// launcher checks).
 template <int ROWS, int COLS, int NW>
 struct TileLoader {
   static constexpr int CPR = COLS / 8;
