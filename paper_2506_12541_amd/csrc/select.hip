@@ -13,6 +13,8 @@
 // 16 partial lists of each group are merged through LDS by wave-wide argmax rounds.
 // Scores stay in f32 end to end so that rankings match the float64 definition except
 // where two scores are closer than f32 rounding.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "attn_common.hpp"
@@ -32,15 +34,23 @@ __device__ __forceinline__ uint64_t make_key(float score, int blk) {
   return ((uint64_t)ordered_bits(score) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)blk);
 }
 
+// Inverse of ordered_bits (the score of a key's upper word).
+__device__ __forceinline__ float key_score(uint64_t key) {
+  const uint32_t b = (uint32_t)(key >> 32);
+  return __uint_as_float((b & 0x80000000u) ? (b & 0x7FFFFFFFu) : ~b);
+}
+
+// Insert x into the descending list (keys are unique, x > lst[K - 1]): every entry compares
+// with x independently, then each slot keeps its entry, takes x, or takes its upper
+// neighbour (slots are rewritten from the bottom, so the neighbour is still the old one).
 template <int K>
 __device__ __forceinline__ void topk_insert(uint64_t (&lst)[K], uint64_t x) {
-  if (x <= lst[K - 1]) return;
+  bool gt[K];
 #pragma unroll
-  for (int t = 0; t < K; ++t) {
-    uint64_t hi = lst[t] > x ? lst[t] : x;
-    x = lst[t] > x ? x : lst[t];
-    lst[t] = hi;
-  }
+  for (int t = 0; t < K; ++t) gt[t] = lst[t] > x;
+#pragma unroll
+  for (int t = K - 1; t >= 1; --t) lst[t] = gt[t] ? lst[t] : (gt[t - 1] ? x : lst[t - 1]);
+  lst[0] = gt[0] ? lst[0] : x;
 }
 
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int o) {
@@ -81,6 +91,7 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
   constexpr int GW = 16 * kWaves;   // groups per workgroup
   __shared__ __attribute__((aligned(16))) bf16_t ks0[KT * TW], ks1[KT * TW];
   __shared__ uint8_t cv0[KT], cv1[KT];
+  __shared__ uint32_t av0, av1;   // 1: every compressed token of the staged tile is real
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r = lane & 15, j = lane >> 4;
   const int ngroups = N / g;
@@ -92,14 +103,20 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
   const int ntok = N / l;
 
   // compressed-token tiles: f32 rows moved as 2*HD 16-bit units by direct global->LDS
-  // loads; token validity bytes are read before the tile loads
-  auto issue = [&](int t0, bf16_t* kd, uint8_t* cd) {
+  // loads; token validity bytes are read before the tile loads (by wave 0: KT == 64), and
+  // a flag marks tiles whose tokens are all real
+  static_assert(KT == 64, "wave 0 reads the validity of one tile");
+  auto issue = [&](int t0, bf16_t* kd, uint8_t* cd, uint32_t* ad) {
     uint8_t c = 0;
     if (threadIdx.x < KT) c = t0 + (int)threadIdx.x < ntok ? cv[t0 + threadIdx.x] : 0;
     dma_tile<TW, KT, kWaves>(kd, reinterpret_cast<const bf16_t*>(kh), t0, ntok, wid, lane);
     if (threadIdx.x < KT) cd[threadIdx.x] = c;
+    if (wid == 0) {
+      const uint64_t real = __builtin_amdgcn_ballot_w64(c != 0);
+      if (lane == 0) *ad = real == ~0ull ? 1u : 0u;
+    }
   };
-  issue(0, ks0, cv0);
+  issue(0, ks0, cv0, &av0);
 
   // pooled queries of this lane's group (B operand)
   const int pg = p0 + 16 * wid + r;
@@ -110,6 +127,9 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
 
   const int my_group = p0 + 16 * wid + r;
   const int my_ball = (my_group * g) / m;
+  // selection blocks of the group's own ball (excluded when mask_own)
+  const int own_lo = mask_own ? my_ball * (m / ls) : -1;
+  const int own_hi = mask_own ? own_lo + m / ls : -1;
   uint64_t lst[K];
 #pragma unroll
   for (int t = 0; t < K; ++t) lst[t] = 0;
@@ -118,10 +138,12 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
   // so the group already holds K >= k* keys at or above that value and no candidate below
   // it can enter the final k*: the lanes filter on it as well as on their own K-th key.
 
-  auto step = [&](int t0, const bf16_t* kt, const uint8_t* ct, bf16_t* kn, uint8_t* cn) {
+  auto step = [&](int t0, const bf16_t* kt, const uint8_t* ct, const uint32_t* at, bf16_t* kn, uint8_t* cn,
+                  uint32_t* an) {
     vm_drain();
     __syncthreads();
-    if (t0 + KT < ntok) issue(t0 + KT, kn, cn);
+    const bool all_real = *at != 0u;
+    if (t0 + KT < ntok) issue(t0 + KT, kn, cn, an);
     uint64_t gthr = lst[K / 4 - 1];
     {
       const uint64_t o1 = shfl_xor_u64(gthr, 16);
@@ -130,9 +152,15 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
       gthr = o2 < gthr ? o2 : gthr;
     }
     const uint64_t thr = gthr > lst[K - 1] ? gthr : lst[K - 1];
-    // the tile's candidates of this lane (4 / R per 16-token sub-tile), 0 = none
-    constexpr int NCAND = (KT / 16) * (4 / R);
-    uint64_t cand[NCAND];
+    // candidates pass on their score first (a key above thr has a score >= thr's); the
+    // exact key comparison is made for the candidate that is inserted
+    const float thr_f = thr == 0 ? kNegInf : key_score(thr);
+    // the tile's candidates of this lane (4 / R per 16-token sub-tile, ascending blocks),
+    // as scores; -inf = none
+    constexpr int NPS = 4 / R;
+    constexpr int NCAND = (KT / 16) * NPS;
+    const int blk0 = (t0 + 4 * j) / R;
+    float cand[NCAND];
     // scores of the tile's 4 sub-tiles: independent MFMA chains, interleaved
     f32x4 accs[KT / 16];
 #pragma unroll
@@ -154,49 +182,66 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
         for (int st = 0; st < KT / 16; ++st)
           accs[st] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[st][e], bq[c][e], accs[st], 0, 0, 0);
     }
+    // branch-free per candidate; the validity bytes are read only for tiles with padding
+    // (a wave-uniform choice)
+    auto build = [&](auto with_valid) {
 #pragma unroll
-    for (int st = 0; st < KT / 16; ++st) {
-      const f32x4 acc = accs[st];
-      // lane holds scores of compressed tokens t0 + 16 st + 4j + i for group my_group
-      const int tl = 16 * st + 4 * j;
+      for (int st = 0; st < KT / 16; ++st) {
+        const f32x4 acc = accs[st];
+        // lane holds scores of compressed tokens t0 + 16 st + 4j + i for group my_group
+        const int tl = 16 * st + 4 * j;
+        const bool in_range = t0 + 16 * st < ntok;
 #pragma unroll
-      for (int u = 0; u < 4 / R; ++u) {
-        float sc = 0.f;
-        bool ok = t0 + 16 * st < ntok;
-        bool any = false;
+        for (int u = 0; u < NPS; ++u) {
+          float sc = 0.f;
 #pragma unroll
-        for (int i = 0; i < R; ++i) {
-          sc += acc[u * R + i];
-          any |= ct[tl + u * R + i] != 0;
+          for (int i = 0; i < R; ++i) sc += acc[u * R + i];
+          sc *= 1.0f / (float)R;
+          bool ok = in_range;
+          if (decltype(with_valid)::value) {
+            uint32_t any = 0;
+#pragma unroll
+            for (int i = 0; i < R; ++i) any |= ct[tl + u * R + i];
+            ok = ok & (any != 0);
+          }
+          const int blk = blk0 + st * (16 / R) + u;
+          ok = ok & !((blk >= own_lo) & (blk < own_hi)) & (sc >= thr_f);
+          cand[st * NPS + u] = ok ? sc : kNegInf;
         }
-        sc *= 1.0f / (float)R;
-        const int blk = (t0 + tl + u * R) / R;
-        ok = ok && any && !(mask_own && (blk * ls) / m == my_ball);
-        const uint64_t key = make_key(sc, blk);
-        cand[st * (4 / R) + u] = ok && key > thr ? key : 0;
       }
-    }
+    };
+    if (all_real)
+      build(std::false_type{});
+    else
+      build(std::true_type{});
     // insert the qualifying candidates best first; the wave repeats only as many times as
     // its busiest lane needs (most candidates fall below the lane's current k-th key)
     for (;;) {
-      uint64_t best = 0;
+      float bs = kNegInf;
+      int bi = 0;
 #pragma unroll
-      for (int t = 0; t < NCAND; ++t) best = cand[t] > best ? cand[t] : best;
-      const bool take = best > lst[K - 1];
+      for (int t = 0; t < NCAND; ++t) {   // first maximum: the lowest block among equal scores
+        const bool better = cand[t] > bs;
+        bs = better ? cand[t] : bs;
+        bi = better ? t : bi;
+      }
+      const uint64_t key = bs > kNegInf ? make_key(bs, blk0 + (bi / NPS) * (16 / R) + bi % NPS) : 0;
+      const uint64_t lim = thr > lst[K - 1] ? thr : lst[K - 1];
+      const bool take = key > lim;
       if (!__builtin_amdgcn_ballot_w64(take)) break;
       if (take) {
-        topk_insert<K>(lst, best);
+        topk_insert<K>(lst, key);
 #pragma unroll
-        for (int t = 0; t < NCAND; ++t) cand[t] = cand[t] == best ? 0 : cand[t];
+        for (int t = 0; t < NCAND; ++t) cand[t] = t == bi ? kNegInf : cand[t];
       } else {
 #pragma unroll
-        for (int t = 0; t < NCAND; ++t) cand[t] = 0;
+        for (int t = 0; t < NCAND; ++t) cand[t] = kNegInf;
       }
     }
   };
   for (int t0 = 0; t0 < ntok; t0 += 2 * KT) {
-    step(t0, ks0, cv0, ks1, cv1);
-    if (t0 + KT < ntok) step(t0 + KT, ks1, cv1, ks0, cv0);
+    step(t0, ks0, cv0, &av0, ks1, cv1, &av1);
+    if (t0 + KT < ntok) step(t0 + KT, ks1, cv1, &av1, ks0, cv0, &av0);
   }
   // merge: the 4 partial lists of group r sit in lanes r, r+16, r+32, r+48; a wave's 16
   // groups go through LDS (the idle tile buffers) and are finalised one group at a time
