@@ -243,55 +243,53 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
     step(t0, ks0, cv0, &av0, ks1, cv1, &av1);
     if (t0 + KT < ntok) step(t0 + KT, ks1, cv1, &av1, ks0, cv0, &av0);
   }
-  // merge: the 4 partial lists of group r sit in lanes r, r+16, r+32, r+48; a wave's 16
-  // groups go through LDS (the idle tile buffers) and are finalised one group at a time
-  __syncthreads();
-  // 16 groups x 4 lists x K keys per wave: the two tile buffers hold them when large enough
-  constexpr bool kReuse = KT * TW * 2 >= 2 * 16 * 4 * K * 8;
-  __shared__ uint64_t part_own[kReuse ? 1 : kWaves * 16 * 4 * K];
-  uint64_t* part = kReuse ? reinterpret_cast<uint64_t*>(wid < 2 ? ks0 : ks1) + (wid & 1) * 16 * 4 * K
-                          : part_own + wid * 16 * 4 * K;
+  // merge: the 4 sorted lists of group r sit in lanes r, r + 16, r + 32, r + 48 (the wave's
+  // 16 groups side by side). k* rounds of a 4-way merge: the group's best head (two
+  // exchanges) is chosen and its owner drops it; lane j keeps the blocks of rounds
+  // j, j + 4, ... (-1 once the lists run dry).
+  int mine[4] = {-1, -1, -1, -1};
 #pragma unroll
-  for (int t = 0; t < K; ++t) part[r * 4 * K + j * K + t] = lst[t];
-  wave_sync();
-  constexpr int NC = 4 * K;   // candidates per group
-  for (int gl = 0; gl < 16; ++gl) {
-    uint64_t cand[(NC + 63) / 64];
-#pragma unroll
-    for (int u = 0; u < (NC + 63) / 64; ++u) {
-      int idx = u * 64 + lane;
-      cand[u] = idx < NC ? part[gl * NC + idx] : 0;
+  for (int t = 0; t < K; ++t) {
+    if (t >= kk) break;
+    const uint64_t head = lst[0];
+    uint64_t w = head;
+    {
+      const uint64_t o1 = shfl_xor_u64(w, 16);
+      w = o1 > w ? o1 : w;
+      const uint64_t o2 = shfl_xor_u64(w, 32);
+      w = o2 > w ? o2 : w;
     }
-    int mine = -1;
-    for (int t = 0; t < kk; ++t) {
-      uint64_t best = 0;
-      int bu = 0;
+    const bool pop = w != 0 && head == w;   // keys are unique: one lane of the group holds w
 #pragma unroll
-      for (int u = 0; u < (NC + 63) / 64; ++u)
-        if (cand[u] > best) { best = cand[u]; bu = u; }
-      uint64_t w = best;
+    for (int i = 0; i < K - 1; ++i) lst[i] = pop ? lst[i + 1] : lst[i];
+    lst[K - 1] = pop ? 0 : lst[K - 1];
+    const int blk = w == 0 ? -1 : (int)(0xFFFFFFFFu - (uint32_t)(w & 0xFFFFFFFFu));
+    mine[t >> 2] = (t & 3) == j ? blk : mine[t >> 2];
+  }
+  // stored ascending with -1 in unused slots: each chosen block goes to its rank among the
+  // group's (at most 16) chosen blocks, which every lane of the group gathers
+  int all[16];
 #pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        uint64_t y = shfl_xor_u64(w, o);
-        w = y > w ? y : w;
+  for (int q4 = 0; q4 < 4; ++q4)
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) all[4 * q4 + s4] = __shfl(mine[s4], r + 16 * q4, 64);
+  int nsel = 0;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) nsel += all[e] >= 0;
+  const int p = p0 + 16 * wid + r;
+  if (p < ngroups) {
+    int* out = sel + ((size_t)bh * ngroups + p) * kk;
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) {
+      const int v = mine[s4];
+      if (v >= 0) {
+        int rank = 0;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) rank += (all[e] >= 0) & (all[e] < v);
+        out[rank] = v;
       }
-      if (w == 0) break;
-      if (best == w) cand[bu] = 0;   // keys are unique: exactly one lane holds w
-      if (lane == t) mine = (int)(0xFFFFFFFFu - (uint32_t)(w & 0xFFFFFFFFu));
-    }
-    // ascending order of the chosen blocks: rank among lanes < K
-    const int p = p0 + 16 * wid + gl;
-    int rank = 0;
-    for (int t = 0; t < kk; ++t) {
-      int other = __shfl(mine, t, 64);
-      if (other >= 0 && mine >= 0 && (other < mine)) ++rank;
-    }
-    int nsel = 0;
-    for (int t = 0; t < kk; ++t) nsel += __shfl(mine, t, 64) >= 0;
-    if (p < ngroups && lane < kk) {
-      int* out = sel + ((size_t)bh * ngroups + p) * kk;
-      if (mine >= 0) out[rank] = mine;
-      if (lane >= nsel) out[lane] = -1;
+      const int slot = j + 4 * s4;
+      if (slot < kk && slot >= nsel) out[slot] = -1;
     }
   }
 }
