@@ -132,7 +132,7 @@ SavedLayout saved_layout(const bsa::Dims& D) {
 }
 
 struct FwdWs {
-  size_t w1t_k, w1t_v, w1t_q, kc_lp, vc_lp, qc_lp, lsec;
+  size_t w1t_k, w1t_v, w1t_q, kc_lp, vc_lp, qc_lp, lsec, kplanes;
   size_t pk, pv, pkt, pvt, hist, seg_s, seg_e, part, ml;   // per-token selection (g = 1)
   size_t total;
 };
@@ -166,6 +166,7 @@ FwdWs fwd_ws_layout(const bsa::Dims& D) {
   W.w1t_q = put(D.qc_mlp ? w1 : 0);
   W.qc_lp = put(D.block_coarse() ? elem_bytes(D) * (size_t)D.cmp_rows() * D.d : 0);
   W.lsec = put(D.gcmp ? sizeof(float) * (size_t)D.cmp_rows() : 0);
+  W.kplanes = put(3 * sizeof(uint16_t) * (size_t)D.cmp_rows() * D.d);
   const size_t np = D.g == 1 ? bsa::slc1_pairs(D) : 0;
   const size_t nseg = D.g == 1 ? (size_t)D.B * D.H * (D.N / D.ls) : 0;
   W.pk = put(4 * np);
@@ -486,7 +487,7 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
     (void)st_main;
   }
   BSA_STEP("fwd.select", bsa::launch_select_topk(D, q, valid, saved->kcmp, saved->cvalid, saved->sel_idx,
-                                                  saved->qcmp, D.block_coarse(), st),
+                                                  saved->qcmp, D.block_coarse(), (uint16_t*)(w + W.kplanes), st),
            "select");
   if (D.g == 1) {
     const bsa::Slc1Ws S1 = slc1_ws(D, w, W.pk, W.pv, W.pkt, W.pvt, W.hist, W.seg_s, W.seg_e, W.part, W.ml);

@@ -44,9 +44,11 @@ hipError_t launch_compress_fwd(const Dims& D, const void* x, const uint8_t* vali
 
 // select.hip: pooled-query block scores and group top-k (Eq. 6, 7, 10-12, 14)
 // qpool: B*H*(N/g)*d floats of coarse queries; written here (group mean of Eq. 11) unless
-// `given`, when it already holds them (Eq. 13)
+// `given`, when it already holds them (Eq. 13); kplanes: 3 * B*H*(N/l)*d bf16 of workspace
+// (the compressed keys in three bf16 parts)
 hipError_t launch_select_topk(const Dims& D, const void* q, const uint8_t* valid, const float* kcmp,
-                              const uint8_t* cvalid, int* sel, float* qpool, bool given, hipStream_t st);
+                              const uint8_t* cvalid, int* sel, float* qpool, bool given, uint16_t* kplanes,
+                              hipStream_t st);
 
 // attn_fwd.hip: the three attention branches (Eq. 3, 5, 8) and the gate (Eq. 9)
 hipError_t launch_ball_fwd(const Dims& D, const void* q, const void* k, const void* v, const uint8_t* valid,

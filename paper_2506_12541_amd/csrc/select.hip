@@ -10,9 +10,13 @@
 // one head: the pooled queries sit in registers as the B operand of f32 MFMA tiles, the
 // four waves stream disjoint 16-token slices of the compressed keys from L2, and every
 // lane keeps a running top-k of (ordered score, ~index) 64-bit keys for its group. The
-// 16 partial lists of each group are merged through LDS by wave-wide argmax rounds.
-// Scores stay in f32 end to end so that rankings match the float64 definition except
-// where two scores are closer than f32 rounding.
+// four lists of each group are merged in registers at the end.
+// Scores keep f32 accuracy so that rankings match the float64 definition except where two
+// scores are closer than f32 rounding: each f32 operand is split into three bf16 parts
+// (x = hi + mid + lo up to 2^-27 |x|) and a score is the f32 sum of the six products
+// whose weight reaches 2^-16 (hi hi, hi mid, mid hi, hi lo, lo hi, mid mid), each exact in
+// the bf16 matrix cores: about the error of an f32 product, at 6 bf16 MFMAs per 32-wide
+// slice instead of 8 f32 ones per 4-wide slice.
 #include <type_traits>
 
 #include "common.hpp"
@@ -81,15 +85,51 @@ __global__ void pool_q_kernel(const T* q, const uint8_t* valid, int H, int N, in
   qpool[i] = s / (float)g;
 }
 
+// hi = bf16(x), mid = bf16(x - hi), lo = bf16(x - hi - mid) (the differences are exact in
+// f32); eight elements per thread.
+__device__ __forceinline__ void split3(const float* x, bf16x8& hi, bf16x8& mid, bf16x8& lo) {
+  float h[8], md[8], lw[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float a = x[e];
+    const float ah = bf2f(f2bf(a));
+    const float r1 = a - ah;
+    const float am = bf2f(f2bf(r1));
+    h[e] = ah;
+    md[e] = am;
+    lw[e] = r1 - am;
+  }
+  hi = make_chunk<bf16_t>(h);
+  mid = make_chunk<bf16_t>(md);
+  lo = make_chunk<bf16_t>(lw);
+}
+
+__global__ void __launch_bounds__(256) split3_kernel(const float* __restrict__ x, long long n8,
+                                                     bf16_t* __restrict__ hi, bf16_t* __restrict__ mid,
+                                                     bf16_t* __restrict__ lo) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n8) return;
+  const f32x8 v = load_chunk(x + 8 * i);
+  float a[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) a[e] = v[e];
+  bf16x8 h, m, l;
+  split3(a, h, m, l);
+  *reinterpret_cast<bf16x8*>(hi + 8 * i) = h;
+  *reinterpret_cast<bf16x8*>(mid + 8 * i) = m;
+  *reinterpret_cast<bf16x8*>(lo + 8 * i) = l;
+}
+
 template <typename T, int HD, int K, int R>
-__global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool, const float* kcmp,
+__global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool, const bf16_t* kplanes,
                                                              const uint8_t* cvalid, int H, int N, int l, int ls,
                                                              int m, int g, int mask_own, int kk, int* sel) {
   constexpr int NCH = HD / 32;
   constexpr int KT = 64;        // compressed tokens per staged tile
-  constexpr int TW = 2 * HD;    // tile row width in 16-bit units (f32 rows)
   constexpr int GW = 16 * kWaves;   // groups per workgroup
-  __shared__ __attribute__((aligned(16))) bf16_t ks0[KT * TW], ks1[KT * TW];
+  // the three bf16 parts of a tile of compressed keys, double-buffered (distinct objects)
+  __shared__ __attribute__((aligned(16))) bf16_t kh0[KT * HD], km0[KT * HD], kl0[KT * HD];
+  __shared__ __attribute__((aligned(16))) bf16_t kh1[KT * HD], km1[KT * HD], kl1[KT * HD];
   __shared__ uint8_t cv0[KT], cv1[KT];
   __shared__ uint32_t av0, av1;   // 1: every compressed token of the staged tile is real
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -98,32 +138,41 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
   const int bh = blockIdx.y;
   const int b = bh / H;
   const int p0 = blockIdx.x * GW;
-  const float* kh = kcmp + (size_t)bh * (N / l) * HD;
-  const uint8_t* cv = cvalid + (size_t)b * (N / l);
   const int ntok = N / l;
+  const size_t plane = (size_t)gridDim.y * ntok * HD;   // elements of one part
+  const bf16_t* ph = kplanes + (size_t)bh * ntok * HD;
+  const uint8_t* cv = cvalid + (size_t)b * (N / l);
 
-  // compressed-token tiles: f32 rows moved as 2*HD 16-bit units by direct global->LDS
-  // loads; token validity bytes are read before the tile loads (by wave 0: KT == 64), and
-  // a flag marks tiles whose tokens are all real
+  // compressed-token tiles: the three parts moved by direct global->LDS loads; token
+  // validity bytes are read before the tile loads (by wave 0: KT == 64), and a flag marks
+  // tiles whose tokens are all real
   static_assert(KT == 64, "wave 0 reads the validity of one tile");
-  auto issue = [&](int t0, bf16_t* kd, uint8_t* cd, uint32_t* ad) {
+  auto issue = [&](int t0, bf16_t* dh, bf16_t* dm, bf16_t* dl, uint8_t* cd, uint32_t* ad) {
     uint8_t c = 0;
     if (threadIdx.x < KT) c = t0 + (int)threadIdx.x < ntok ? cv[t0 + threadIdx.x] : 0;
-    dma_tile<TW, KT, kWaves>(kd, reinterpret_cast<const bf16_t*>(kh), t0, ntok, wid, lane);
+    dma_tile<HD, KT, kWaves>(dh, ph, t0, ntok, wid, lane);
+    dma_tile<HD, KT, kWaves>(dm, ph + plane, t0, ntok, wid, lane);
+    dma_tile<HD, KT, kWaves>(dl, ph + 2 * plane, t0, ntok, wid, lane);
     if (threadIdx.x < KT) cd[threadIdx.x] = c;
     if (wid == 0) {
       const uint64_t real = __builtin_amdgcn_ballot_w64(c != 0);
       if (lane == 0) *ad = real == ~0ull ? 1u : 0u;
     }
   };
-  issue(0, ks0, cv0, &av0);
+  issue(0, kh0, km0, kl0, cv0, &av0);
 
-  // pooled queries of this lane's group (B operand)
+  // pooled queries of this lane's group (B operand), in three bf16 parts
   const int pg = p0 + 16 * wid + r;
   const float* qpr = qpool + ((size_t)bh * ngroups + (pg < ngroups ? pg : 0)) * HD;
-  f32x8 bq[NCH];
+  bf16x8 qh[NCH], qm[NCH], ql[NCH];
 #pragma unroll
-  for (int c = 0; c < NCH; ++c) bq[c] = load_chunk(qpr + 32 * c + 8 * j);
+  for (int c = 0; c < NCH; ++c) {
+    const f32x8 v = load_chunk(qpr + 32 * c + 8 * j);
+    float a[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) a[e] = v[e];
+    split3(a, qh[c], qm[c], ql[c]);
+  }
 
   const int my_group = p0 + 16 * wid + r;
   const int my_ball = (my_group * g) / m;
@@ -138,12 +187,12 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
   // so the group already holds K >= k* keys at or above that value and no candidate below
   // it can enter the final k*: the lanes filter on it as well as on their own K-th key.
 
-  auto step = [&](int t0, const bf16_t* kt, const uint8_t* ct, const uint32_t* at, bf16_t* kn, uint8_t* cn,
-                  uint32_t* an) {
+  auto step = [&](int t0, const bf16_t* th, const bf16_t* tm, const bf16_t* tl_, const uint8_t* ct,
+                  const uint32_t* at, bf16_t* nh, bf16_t* nm, bf16_t* nl, uint8_t* cn, uint32_t* an) {
     vm_drain();
     __syncthreads();
     const bool all_real = *at != 0u;
-    if (t0 + KT < ntok) issue(t0 + KT, kn, cn, an);
+    if (t0 + KT < ntok) issue(t0 + KT, nh, nm, nl, cn, an);
     uint64_t gthr = lst[K / 4 - 1];
     {
       const uint64_t o1 = shfl_xor_u64(gthr, 16);
@@ -167,20 +216,26 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
     for (int st = 0; st < KT / 16; ++st) accs[st] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-      f32x8 a[KT / 16];
+      bf16x8 ah[KT / 16], am[KT / 16], al[KT / 16];
 #pragma unroll
-      for (int st = 0; st < KT / 16; ++st) {
-        // 8 floats of row 16 st + r: 16-bit chunks 8c + 2j and 8c + 2j + 1
-        const uint4 lo = __builtin_bit_cast(uint4, lds_row_chunk<TW>(kt, 16 * st + r, 8 * c + 2 * j));
-        const uint4 hi = __builtin_bit_cast(uint4, lds_row_chunk<TW>(kt, 16 * st + r, 8 * c + 2 * j + 1));
-        a[st] = f32x8{__uint_as_float(lo.x), __uint_as_float(lo.y), __uint_as_float(lo.z), __uint_as_float(lo.w),
-                      __uint_as_float(hi.x), __uint_as_float(hi.y), __uint_as_float(hi.z), __uint_as_float(hi.w)};
+      for (int st = 0; st < KT / 16; ++st) {   // row 16 st + r, dims 32 c + 8 j ..
+        ah[st] = lds_row_chunk<HD>(th, 16 * st + r, 4 * c + j);
+        am[st] = lds_row_chunk<HD>(tm, 16 * st + r, 4 * c + j);
+        al[st] = lds_row_chunk<HD>(tl_, 16 * st + r, 4 * c + j);
       }
+      // smaller terms first
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
+      for (int st = 0; st < KT / 16; ++st) accs[st] = mma(al[st], qh[c], accs[st]);
 #pragma unroll
-        for (int st = 0; st < KT / 16; ++st)
-          accs[st] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[st][e], bq[c][e], accs[st], 0, 0, 0);
+      for (int st = 0; st < KT / 16; ++st) accs[st] = mma(ah[st], ql[c], accs[st]);
+#pragma unroll
+      for (int st = 0; st < KT / 16; ++st) accs[st] = mma(am[st], qm[c], accs[st]);
+#pragma unroll
+      for (int st = 0; st < KT / 16; ++st) accs[st] = mma(am[st], qh[c], accs[st]);
+#pragma unroll
+      for (int st = 0; st < KT / 16; ++st) accs[st] = mma(ah[st], qm[c], accs[st]);
+#pragma unroll
+      for (int st = 0; st < KT / 16; ++st) accs[st] = mma(ah[st], qh[c], accs[st]);
     }
     // branch-free per candidate; the validity bytes are read only for tiles with padding
     // (a wave-uniform choice)
@@ -240,8 +295,8 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
     }
   };
   for (int t0 = 0; t0 < ntok; t0 += 2 * KT) {
-    step(t0, ks0, cv0, &av0, ks1, cv1, &av1);
-    if (t0 + KT < ntok) step(t0 + KT, ks1, cv1, &av1, ks0, cv0, &av0);
+    step(t0, kh0, km0, kl0, cv0, &av0, kh1, km1, kl1, cv1, &av1);
+    if (t0 + KT < ntok) step(t0 + KT, kh1, km1, kl1, cv1, &av1, kh0, km0, kl0, cv0, &av0);
   }
   // merge: the 4 sorted lists of group r sit in lanes r, r + 16, r + 32, r + 48 (the wave's
   // 16 groups side by side). k* rounds of a 4-way merge: the group's best head (two
@@ -296,43 +351,48 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
 
 template <typename T, int HD, int K>
 hipError_t select_k(const Dims& D, const void* q, const uint8_t* valid, const float* kcmp, const uint8_t* cvalid,
-                    int* sel, float* qpool, bool given, hipStream_t st) {
+                    int* sel, float* qpool, bool given, uint16_t* kplanes, hipStream_t st) {
   const long long total = (long long)D.B * D.H * (D.N / D.g) * HD;
   if (!given)
     hipLaunchKernelGGL((pool_q_kernel<T, HD>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, (const T*)q,
                        valid, D.H, D.N, D.g, total, qpool);
+  const long long n8 = D.cmp_rows() * HD / 8;
+  bf16_t* kp = reinterpret_cast<bf16_t*>(kplanes);
+  hipLaunchKernelGGL(split3_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, st, kcmp, n8, kp,
+                     kp + D.cmp_rows() * HD, kp + 2 * D.cmp_rows() * HD);
   const int ngroups = D.N / D.g;
   dim3 grid((ngroups + 16 * kWaves - 1) / (16 * kWaves), D.B * D.H);
   const int R = D.ls / D.l;
   if (R == 1)
-    hipLaunchKernelGGL((select_kernel<T, HD, K, 1>), grid, dim3(kWaves * 64), 0, st, (const float*)qpool, kcmp,
+    hipLaunchKernelGGL((select_kernel<T, HD, K, 1>), grid, dim3(kWaves * 64), 0, st, (const float*)qpool, (const bf16_t*)kp,
                        cvalid, D.H, D.N, D.l, D.ls, D.m, D.g, D.mask_own, D.k, sel);
   else if (R == 2)
-    hipLaunchKernelGGL((select_kernel<T, HD, K, 2>), grid, dim3(kWaves * 64), 0, st, (const float*)qpool, kcmp,
+    hipLaunchKernelGGL((select_kernel<T, HD, K, 2>), grid, dim3(kWaves * 64), 0, st, (const float*)qpool, (const bf16_t*)kp,
                        cvalid, D.H, D.N, D.l, D.ls, D.m, D.g, D.mask_own, D.k, sel);
   else
-    hipLaunchKernelGGL((select_kernel<T, HD, K, 4>), grid, dim3(kWaves * 64), 0, st, (const float*)qpool, kcmp,
+    hipLaunchKernelGGL((select_kernel<T, HD, K, 4>), grid, dim3(kWaves * 64), 0, st, (const float*)qpool, (const bf16_t*)kp,
                        cvalid, D.H, D.N, D.l, D.ls, D.m, D.g, D.mask_own, D.k, sel);
   return hipGetLastError();
 }
 
 template <typename T, int HD>
 hipError_t select_hd(const Dims& D, const void* q, const uint8_t* valid, const float* kcmp, const uint8_t* cvalid,
-                     int* sel, float* qpool, bool given, hipStream_t st) {
-  if (D.k <= 4) return select_k<T, HD, 4>(D, q, valid, kcmp, cvalid, sel, qpool, given, st);
-  if (D.k <= 8) return select_k<T, HD, 8>(D, q, valid, kcmp, cvalid, sel, qpool, given, st);
-  return select_k<T, HD, 16>(D, q, valid, kcmp, cvalid, sel, qpool, given, st);
+                     int* sel, float* qpool, bool given, uint16_t* kplanes, hipStream_t st) {
+  if (D.k <= 4) return select_k<T, HD, 4>(D, q, valid, kcmp, cvalid, sel, qpool, given, kplanes, st);
+  if (D.k <= 8) return select_k<T, HD, 8>(D, q, valid, kcmp, cvalid, sel, qpool, given, kplanes, st);
+  return select_k<T, HD, 16>(D, q, valid, kcmp, cvalid, sel, qpool, given, kplanes, st);
 }
 
 }  // namespace
 
 hipError_t launch_select_topk(const Dims& D, const void* q, const uint8_t* valid, const float* kcmp,
-                              const uint8_t* cvalid, int* sel, float* qpool, bool given, hipStream_t st) {
+                              const uint8_t* cvalid, int* sel, float* qpool, bool given, uint16_t* kplanes,
+                              hipStream_t st) {
   if (D.bf16)
-    return D.d == 64 ? select_hd<bf16_t, 64>(D, q, valid, kcmp, cvalid, sel, qpool, given, st)
-                     : select_hd<bf16_t, 32>(D, q, valid, kcmp, cvalid, sel, qpool, given, st);
-  return D.d == 64 ? select_hd<float, 64>(D, q, valid, kcmp, cvalid, sel, qpool, given, st)
-                   : select_hd<float, 32>(D, q, valid, kcmp, cvalid, sel, qpool, given, st);
+    return D.d == 64 ? select_hd<bf16_t, 64>(D, q, valid, kcmp, cvalid, sel, qpool, given, kplanes, st)
+                     : select_hd<bf16_t, 32>(D, q, valid, kcmp, cvalid, sel, qpool, given, kplanes, st);
+  return D.d == 64 ? select_hd<float, 64>(D, q, valid, kcmp, cvalid, sel, qpool, given, kplanes, st)
+                   : select_hd<float, 32>(D, q, valid, kcmp, cvalid, sel, qpool, given, kplanes, st);
 }
 
 }  // namespace bsa
