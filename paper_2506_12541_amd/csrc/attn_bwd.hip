@@ -136,6 +136,18 @@ __global__ void sum_chunks_kernel(const float* part, int nchunks, long long n, f
   out[i] = s;
 }
 
+// Exact sign flip of 8 bf16 values (the sign bits). The backward passes multiply dO by -V
+// (or -dO by V) so that the row term R of dS = P (dP - R) enters as the MFMA's accumulator
+// input: the product then yields R - dP, and the sign moves into the final scale.
+__device__ __forceinline__ bf16x8 neg_chunk(bf16x8 x) {
+  uint4 u = __builtin_bit_cast(uint4, x);
+  u.x ^= 0x80008000u;
+  u.y ^= 0x80008000u;
+  u.z ^= 0x80008000u;
+  u.w ^= 0x80008000u;
+  return __builtin_bit_cast(bf16x8, u);
+}
+
 // Per query row of one branch, packed (log2 LSE - log2 s, s, R, log2 LSE): s scales the
 // row's dO (the branch gate sigmoid(gamma_b), or 1 for rows whose dO is already scaled),
 // R = rowsum(dO * o_b) for the unscaled dO, so exp2(S log2e - x) is s P and the softmax
@@ -322,21 +334,21 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
   };
   issue(0, ks0, vs0, ok0);
 
+  // df holds -dO and rr the lane's R, so the dP product yields R - dO V^T
   CT qf[QB][NCH], df[QB][NCH];
-  float l2[QB], dd[QB], gs[QB];
-  f32x4 acc[QB][DB];
+  float l2[QB];
+  f32x4 rr[QB], acc[QB][DB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const long long row = bh * N + wq0 + 16 * qb + r;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       qf[qb][c] = load_chunk(q + row * HD + 32 * c + 8 * j);
-      df[qb][c] = load_chunk(dout + row * HD + 32 * c + 8 * j);
+      df[qb][c] = neg_chunk(load_chunk(dout + row * HD + 32 * c + 8 * j));
     }
     const float4 t = qt.t4[row];   // log2 LSE - log2 s, s, R
     l2[qb] = t.x;
-    gs[qb] = t.y;
-    dd[qb] = t.z;
+    rr[qb] = f32x4{t.z, t.z, t.z, t.z};
 #pragma unroll
     for (int db = 0; db < DB; ++db) acc[qb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
@@ -361,9 +373,10 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
           sv[qb][kb] = mma(ak, qf[qb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sv[qb][kb]);
-          dp[qb][kb] = mma(av, df[qb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : dp[qb][kb]);
+          dp[qb][kb] = mma(av, df[qb][c], c == 0 ? rr[qb] : dp[qb][kb]);
         }
       }
+    // dsf = P (R - dP) = -dS
     CT dsf[QB][KB / 2];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -374,7 +387,7 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
         for (int i = 0; i < 4; ++i) {
           const float e = fast_exp2(__builtin_fmaf(sv[qb][kb][i], sl2, -l2[qb]));
           const float p = !MASK || ((okw[kb] >> (8 * i)) & 1u) ? e : 0.f;
-          v8[kb][i] = p * (dp[qb][kb][i] - dd[qb]);
+          v8[kb][i] = p * dp[qb][kb][i];
         }
 #pragma unroll
       for (int kp = 0; kp < KB / 2; ++kp) {
@@ -403,7 +416,7 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
       float* dst = dq + row * HD + 16 * db + 4 * j;
-      f32x4 val = acc[qb][db] * scale;
+      f32x4 val = acc[qb][db] * -scale;
       if (ADD) {
         float4 old = *reinterpret_cast<float4*>(dst);
         val[0] += old.x; val[1] += old.y; val[2] += old.z; val[3] += old.w;
@@ -589,7 +602,9 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
   typedef bf16x8 CT;
   __shared__ __attribute__((aligned(16))) bf16_t qs0[kQT * HD], qs1[kQT * HD];
   __shared__ __attribute__((aligned(16))) bf16_t ds0[kQT * HD], ds1[kQT * HD];
-  __shared__ __attribute__((aligned(16))) float4 tm0[kQT], tm1[kQT];
+  // row terms as two arrays (log2 LSE - log2 s, and R) so that a lane reads the values of
+  // its four accumulator rows with one 16-byte load
+  __shared__ __attribute__((aligned(16))) float tx0[kQT], tz0[kQT], tx1[kQT], tz1[kQT];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r = lane & 15, j = lane >> 4;
   const int bh = blockIdx.z;
@@ -610,12 +625,16 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
   const bf16_t* dh = dout + (size_t)bh * N * HD;
   const float4* th = qt.t4 + (size_t)bh * N;
 
-  auto issue = [&](int t0, bf16_t* qd, bf16_t* dd, float4* td) {
+  auto issue = [&](int t0, bf16_t* qd, bf16_t* dd, float* txd, float* tzd) {
     dma_tile<HD, kQT, NW>(qd, qh, t0, N, wid, lane);
     dma_tile<HD, kQT, NW>(dd, dh, t0, N, wid, lane);
-    if (wid == NW - 1) __builtin_amdgcn_global_load_lds(th + t0 + lane, td, 16, 0, 0);
+    if (wid == NW - 1) {
+      const float* t = reinterpret_cast<const float*>(th + t0 + lane);
+      __builtin_amdgcn_global_load_lds(t, txd, 4, 0, 0);
+      __builtin_amdgcn_global_load_lds(t + 2, tzd, 4, 0, 0);
+    }
   };
-  issue(qbeg, qs0, ds0, tm0);
+  issue(qbeg, qs0, ds0, tx0, tz0);
 
   CT kf[KBW][NCH], vf[KBW][NCH];
   bool kok[KBW];
@@ -629,7 +648,7 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
       vf[kb][c] = zero_chunk(vf[kb][c]);
       if (key < nkeys_total) {
         kf[kb][c] = load_chunk(k + ((size_t)bh * nkeys_total + key) * HD + 32 * c + 8 * j);
-        vf[kb][c] = load_chunk(v + ((size_t)bh * nkeys_total + key) * HD + 32 * c + 8 * j);
+        vf[kb][c] = neg_chunk(load_chunk(v + ((size_t)bh * nkeys_total + key) * HD + 32 * c + 8 * j));
       }
     }
   }
@@ -639,17 +658,20 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
 #pragma unroll
     for (int db = 0; db < DB; ++db) { dka[kb][db] = f32x4{0.f, 0.f, 0.f, 0.f}; dva[kb][db] = dka[kb][db]; }
 
-  auto step = [&](int t0, const bf16_t* qs, const bf16_t* ds, const float4* tm, bf16_t* qn, bf16_t* dn,
-                  float4* tn) {
+  auto step = [&](int t0, const bf16_t* qs, const bf16_t* ds, const float* tx, const float* tz, bf16_t* qn,
+                  bf16_t* dn, float* txn, float* tzn) {
     vm_drain();          // this wave's loads of the tile have landed
     __syncthreads();     // ... and every wave's; the previous tile is no longer read
-    if (t0 + kQT < qend) issue(t0 + kQT, qn, dn, tn);
+    if (t0 + kQT < qend) issue(t0 + kQT, qn, dn, txn, tzn);
 #pragma unroll
     for (int qp = 0; qp < kQT / 32; ++qp) {
-      f32x4 sv[2][KBW], dp[2][KBW];
+      // lane holds queries 16qb + 4j + i for its key; dp = R - dO V^T (vf holds -V)
+      f32x4 sv[2][KBW], dp[2][KBW], lx[2];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int qb = 2 * qp + u;
+        lx[u] = *reinterpret_cast<const f32x4*>(&tx[16 * qb + 4 * j]);   // log2 LSE - log2 s
+        const f32x4 rz = *reinterpret_cast<const f32x4*>(&tz[16 * qb + 4 * j]);
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
           CT aq = lds_row_chunk<HD>(qs, 16 * qb + r, 4 * c + j);
@@ -657,24 +679,22 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
 #pragma unroll
           for (int kb = 0; kb < KBW; ++kb) {
             sv[u][kb] = mma(aq, kf[kb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sv[u][kb]);
-            dp[u][kb] = mma(ad, vf[kb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : dp[u][kb]);
+            dp[u][kb] = mma(ad, vf[kb][c], c == 0 ? rz : dp[u][kb]);
           }
         }
       }
-      // lane holds queries 16qb + 4j + i for its key
+      // a8 = P, b8 = P (R - dP) = -dS
       float a8[KBW][8], b8[KBW][8];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        const int qb = 2 * qp + u;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float4 t = tm[16 * qb + 4 * j + i];   // log2 LSE - log2 s, s, R
 #pragma unroll
           for (int kb = 0; kb < KBW; ++kb) {
-            const float e = fast_exp2(__builtin_fmaf(sv[u][kb][i], sl2, -t.x));
+            const float e = fast_exp2(__builtin_fmaf(sv[u][kb][i], sl2, -lx[u][i]));
             const float p = !MASK || kok[kb] ? e : 0.f;
             a8[kb][4 * u + i] = p;
-            b8[kb][4 * u + i] = p * (dp[u][kb][i] - t.z);
+            b8[kb][4 * u + i] = p * dp[u][kb][i];
           }
         }
       }
@@ -697,10 +717,10 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
     }
   };
   for (int t0 = qbeg; t0 < qend; t0 += 2 * kQT) {
-    step(t0, qs0, ds0, tm0, qs1, ds1, tm1);
-    if (t0 + kQT < qend) step(t0 + kQT, qs1, ds1, tm1, qs0, ds0, tm0);
+    step(t0, qs0, ds0, tx0, tz0, qs1, ds1, tx1, tz1);
+    if (t0 + kQT < qend) step(t0 + kQT, qs1, ds1, tx1, tz1, qs0, ds0, tx0, tz0);
   }
-  // lane: key wk0 + 16kb + r, dims 16db + 4j + i
+  // lane: key wk0 + 16kb + r, dims 16db + 4j + i; dka holds -dK / scale
   const size_t out_base = (size_t)chunk * ((size_t)gridDim.z * nkeys_total * HD);
 #pragma unroll
   for (int kb = 0; kb < KBW; ++kb) {
@@ -709,7 +729,7 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
     const size_t off = out_base + ((size_t)bh * nkeys_total + key) * HD;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      store4(dk_out + off + 16 * db + 4 * j, dka[kb][db], scale);
+      store4(dk_out + off + 16 * db + 4 * j, dka[kb][db], -scale);
       store4(dv_out + off + 16 * db + 4 * j, dva[kb][db], 1.0f);
     }
   }
