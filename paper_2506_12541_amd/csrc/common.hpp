@@ -103,15 +103,33 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 // Reduce across the four lane groups {L, L^16, L^32, L^48} (one accumulator column).
+// The exchanges are gfx950's VALU lane swaps rather than LDS permutes: with both operands
+// holding x, v_permlane16_swap leaves each lane the values of its 16-lane group and of
+// the group next to it (L^16), v_permlane32_swap those of L and L^32. Keeping the
+// exchange off the LDS pipe also means it does not wait behind LDS reads in flight.
+__device__ __forceinline__ float xor16_pair(float x, float& other) {
+  const auto t = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  other = __uint_as_float(t[1]);
+  return __uint_as_float(t[0]);
+}
+__device__ __forceinline__ float xor32_pair(float x, float& other) {
+  const auto t = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  other = __uint_as_float(t[1]);
+  return __uint_as_float(t[0]);
+}
 __device__ __forceinline__ float col_max(float x) {
-  x = fmaxf(x, __shfl_xor(x, 16, 64));
-  x = fmaxf(x, __shfl_xor(x, 32, 64));
-  return x;
+  float y;
+  x = xor16_pair(x, y);
+  x = fmaxf(x, y);
+  x = xor32_pair(x, y);
+  return fmaxf(x, y);
 }
 __device__ __forceinline__ float col_sum(float x) {
-  x += __shfl_xor(x, 16, 64);
-  x += __shfl_xor(x, 32, 64);
-  return x;
+  float y;
+  x = xor16_pair(x, y);
+  x += y;
+  x = xor32_pair(x, y);
+  return x + y;
 }
 // Reduce across the 16 lanes of one lane group (one accumulator row set).
 __device__ __forceinline__ float row16_sum(float x) {
