@@ -57,11 +57,45 @@ __device__ __forceinline__ void topk_insert(uint64_t (&lst)[K], uint64_t x) {
   lst[0] = gt[0] ? lst[0] : x;
 }
 
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int o) {
-  uint32_t lo = (uint32_t)x, hi = (uint32_t)(x >> 32);
-  lo = __shfl_xor(lo, o, 64);
-  hi = __shfl_xor(hi, o, 64);
-  return ((uint64_t)hi << 32) | lo;
+// The group's four lanes L, L^16, L^32, L^48 exchange through gfx950's VALU lane swaps
+// (no LDS traffic). With both operands holding x, v_permlane16_swap returns the values of
+// the even and the odd 16-lane row of the lane's row pair, v_permlane32_swap those of the
+// lower and the upper half; min and max are symmetric, so either order serves.
+__device__ __forceinline__ void swap16_u64(uint64_t x, uint64_t& a, uint64_t& b) {
+  const auto lo = __builtin_amdgcn_permlane16_swap((uint32_t)x, (uint32_t)x, false, false);
+  const auto hi = __builtin_amdgcn_permlane16_swap((uint32_t)(x >> 32), (uint32_t)(x >> 32), false, false);
+  a = ((uint64_t)hi[0] << 32) | lo[0];
+  b = ((uint64_t)hi[1] << 32) | lo[1];
+}
+__device__ __forceinline__ void swap32_u64(uint64_t x, uint64_t& a, uint64_t& b) {
+  const auto lo = __builtin_amdgcn_permlane32_swap((uint32_t)x, (uint32_t)x, false, false);
+  const auto hi = __builtin_amdgcn_permlane32_swap((uint32_t)(x >> 32), (uint32_t)(x >> 32), false, false);
+  a = ((uint64_t)hi[0] << 32) | lo[0];
+  b = ((uint64_t)hi[1] << 32) | lo[1];
+}
+__device__ __forceinline__ uint64_t group_min_u64(uint64_t x) {
+  uint64_t a, b;
+  swap16_u64(x, a, b);
+  x = a < b ? a : b;
+  swap32_u64(x, a, b);
+  return a < b ? a : b;
+}
+__device__ __forceinline__ uint64_t group_max_u64(uint64_t x) {
+  uint64_t a, b;
+  swap16_u64(x, a, b);
+  x = a > b ? a : b;
+  swap32_u64(x, a, b);
+  return a > b ? a : b;
+}
+// x of the lanes r, r + 16, r + 32, r + 48 (r = L mod 16), in that order
+__device__ __forceinline__ void group_gather(int x, int (&out)[4]) {
+  const auto p = __builtin_amdgcn_permlane16_swap((uint32_t)x, (uint32_t)x, false, false);
+  const auto e = __builtin_amdgcn_permlane32_swap(p[0], p[0], false, false);   // rows 0, 2
+  const auto o = __builtin_amdgcn_permlane32_swap(p[1], p[1], false, false);   // rows 1, 3
+  out[0] = (int)e[0];
+  out[1] = (int)o[0];
+  out[2] = (int)e[1];
+  out[3] = (int)o[1];
 }
 
 // Pooled queries (Eq. 11): q_p = (1/g) * sum of the group's real queries, one thread per
@@ -193,13 +227,7 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
     __syncthreads();
     const bool all_real = *at != 0u;
     if (t0 + KT < ntok) issue(t0 + KT, nh, nm, nl, cn, an);
-    uint64_t gthr = lst[K / 4 - 1];
-    {
-      const uint64_t o1 = shfl_xor_u64(gthr, 16);
-      gthr = o1 < gthr ? o1 : gthr;
-      const uint64_t o2 = shfl_xor_u64(gthr, 32);
-      gthr = o2 < gthr ? o2 : gthr;
-    }
+    const uint64_t gthr = group_min_u64(lst[K / 4 - 1]);
     const uint64_t thr = gthr > lst[K - 1] ? gthr : lst[K - 1];
     // candidates pass on their score first (a key above thr has a score >= thr's); the
     // exact key comparison is made for the candidate that is inserted
@@ -307,13 +335,7 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
   for (int t = 0; t < K; ++t) {
     if (t >= kk) break;
     const uint64_t head = lst[0];
-    uint64_t w = head;
-    {
-      const uint64_t o1 = shfl_xor_u64(w, 16);
-      w = o1 > w ? o1 : w;
-      const uint64_t o2 = shfl_xor_u64(w, 32);
-      w = o2 > w ? o2 : w;
-    }
+    const uint64_t w = group_max_u64(head);
     const bool pop = w != 0 && head == w;   // keys are unique: one lane of the group holds w
 #pragma unroll
     for (int i = 0; i < K - 1; ++i) lst[i] = pop ? lst[i + 1] : lst[i];
@@ -325,9 +347,12 @@ __global__ void __launch_bounds__(kWaves * 64) select_kernel(const float* qpool,
   // group's (at most 16) chosen blocks, which every lane of the group gathers
   int all[16];
 #pragma unroll
-  for (int q4 = 0; q4 < 4; ++q4)
+  for (int s4 = 0; s4 < 4; ++s4) {
+    int g4[4];
+    group_gather(mine[s4], g4);
 #pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) all[4 * q4 + s4] = __shfl(mine[s4], r + 16 * q4, 64);
+    for (int q4 = 0; q4 < 4; ++q4) all[4 * q4 + s4] = g4[q4];
+  }
   int nsel = 0;
 #pragma unroll
   for (int e = 0; e < 16; ++e) nsel += all[e] >= 0;
