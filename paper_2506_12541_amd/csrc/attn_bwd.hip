@@ -1362,15 +1362,18 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t
   return hipGetLastError();
 }
 
-// bf16 variant of the selection key-major pass. Each wave keeps a ring of three item
-// slots in LDS (16 query rows of Q and dO and their packed row terms), filled by direct
+// bf16 variant of the selection key-major pass. NWV waves share a block's items (one
+// wave per workgroup by default: it walks all of the block's items, which spreads the
+// start-up latency of the K/V fragments, the row list and the first item over more
+// items, and a workgroup of one wave needs only 15 KB of LDS, so eight blocks run per
+// CU). Each wave keeps a ring of three item slots in LDS (16 query rows of Q and dO and their packed row terms), filled by direct
 // global->LDS loads two items ahead. The slots are three distinct LDS objects and the item
 // loop is unrolled by three with a straight-line body (steps past the end of the list
 // compute with zero weights), so reads of a slot wait only for that slot's loads. Item row
 // indices come from a per-wave list in LDS. The dK^T and dV^T products take their Q^T and
 // dO^T operands from transpose reads of the slot tiles.
-template <int HD, int KBW>
-__global__ void __launch_bounds__(256) slc_bwd_kv_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
+template <int HD, int KBW, int NWV>
+__global__ void __launch_bounds__(64 * NWV) slc_bwd_kv_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
                                                              const bf16_t* dout, const uint8_t* valid_all,
                                                              const uint32_t* groups, const int* seg_start,
                                                              const int* seg_end, QTerms qt, int H, int N, int ls,
@@ -1381,8 +1384,8 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_dma_kernel(const bf16_t* q, co
   constexpr int SLOT = 2 * SL + 64 * 8;   // one wave's slot: Q tile, dO tile, 64 lanes' row terms
   constexpr int kRound = 128;             // items per wave per round of the row list
   typedef bf16x8 CT;
-  __shared__ __attribute__((aligned(16))) bf16_t ring0[4 * SLOT], ring1[4 * SLOT], ring2[4 * SLOT];
-  __shared__ int rows_all[4][kRound];
+  __shared__ __attribute__((aligned(16))) bf16_t ring0[NWV * SLOT], ring1[NWV * SLOT], ring2[NWV * SLOT];
+  __shared__ int rows_all[NWV][kRound];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r = lane & 15, j = lane >> 4;
   const long long seg = blockIdx.x;
@@ -1401,7 +1404,7 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_dma_kernel(const bf16_t* q, co
   const int qblocks = g >= 16 ? g / 16 : 1;
   const int qrows = g >= 16 ? 16 : g;       // real rows of each 16-query block
   const int nwork = (s1 - s0) * qblocks;    // (group, 16-query block) items of this block
-  const int nmine = nwork > wid ? (nwork - wid + 3) / 4 : 0;   // items w, w+4, ... of this wave
+  const int nmine = nwork > wid ? (nwork - wid + NWV - 1) / NWV : 0;   // items w, w+NWV, ... of this wave
 
   CT kf[KBW][NCH], vf[KBW][NCH];
   bool kok[KBW];
@@ -1488,7 +1491,7 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_dma_kernel(const bf16_t* q, co
     cnt = __builtin_amdgcn_readfirstlane(min(kRound, nmine - base));
     wave_sync();   // the previous round's row list and slots are no longer read
     for (int e = lane; e < cnt; e += 64) {
-      const int item = wid + 4 * (base + e);
+      const int item = wid + NWV * (base + e);
       rows[e] = (int)groups[s0 + item / qblocks] * g + 16 * (item % qblocks);
     }
     vm_drain();    // key/value fragments and row indices are in before the ring starts
@@ -1502,14 +1505,14 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_dma_kernel(const bf16_t* q, co
     }
     vm_drain();    // the repeats still in flight land before the slots are reused
   }
-  // fixed-order sum of the four waves' partials: wave 0 accumulates waves 1, 2, 3, one
-  // 16-key block at a time, through the (now idle) first two ring slots
+  // fixed-order sum of the waves' partials (NWV > 1): wave 0 accumulates waves 1, 2, ...,
+  // one 16-key block at a time, through the (now idle) first two ring slots
   float* red0 = reinterpret_cast<float*>(ring0);
   float* red1 = reinterpret_cast<float*>(ring1);
-  static_assert(16 * HD * 4 <= 4 * SLOT * 2, "reduction buffer");
+  static_assert(NWV == 1 || 16 * HD * 4 <= NWV * SLOT * 2, "reduction buffer");
 #pragma unroll
   for (int kb = 0; kb < KBW; ++kb) {
-    for (int w = 1; w < 4; ++w) {
+    for (int w = 1; w < NWV; ++w) {
       __syncthreads();
       if (wid == w) {
 #pragma unroll
@@ -1553,7 +1556,7 @@ void launch_slc_kv(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v
                    const uint8_t* valid, const uint32_t* groups, const int* seg_start, const int* seg_end, QTerms qt,
                    int H, int N, int ls, int g, long long nseg, float sl2, float scale, float* dk, float* dv) {
   if constexpr (sizeof(T) == 2)
-    hipLaunchKernelGGL((slc_bwd_kv_dma_kernel<HD, KBW>), grid, dim3(256), 0, st, q, k, v, dout, valid, groups,
+    hipLaunchKernelGGL((slc_bwd_kv_dma_kernel<HD, KBW, 1>), grid, dim3(64), 0, st, q, k, v, dout, valid, groups,
                        seg_start, seg_end, qt, H, N, ls, g, nseg, sl2, scale, dk, dv);
   else
     hipLaunchKernelGGL((slc_bwd_kv_kernel<T, HD, KBW>), grid, dim3(256), 0, st, q, k, v, dout, valid, groups,
