@@ -13,6 +13,9 @@
 // one key, S = Q K^T). The compressed branch splits its queries into chunks whose
 // partial dK/dV are summed in a fixed order; the selection branch inverts the selected
 // block lists (block -> groups, ascending) by a stable radix sort first.
+#include <algorithm>
+#include <limits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "attn_common.hpp"
@@ -430,6 +433,8 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
 // Queries are staged 64 at a time in LDS (row-major for the S and dP products, transposed
 // for the dK^T and dV^T products); each wave owns 32 keys in registers.
 constexpr int kQT = 64;
+constexpr int kSlcLightItems = 256;   // selection dK/dV: blocks with more items get eight waves
+constexpr int kSlcHeavyGroups = 256;  // persistent eight-wave workgroups of that second launch
 
 template <typename T, int HD, int NW, bool BALL>
 __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const T* k, const T* v, const T* dout,
@@ -1362,11 +1367,14 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t
   return hipGetLastError();
 }
 
-// bf16 variant of the selection key-major pass. NWV waves share a block's items (one
-// wave per workgroup by default: it walks all of the block's items, which spreads the
-// start-up latency of the K/V fragments, the row list and the first item over more
-// items, and a workgroup of one wave needs only 15 KB of LDS, so eight blocks run per
-// CU). Each wave keeps a ring of three item slots in LDS (16 query rows of Q and dO and their packed row terms), filled by direct
+// bf16 variant of the selection key-major pass. NWV waves share a block's items. Blocks
+// with at most kSlcLightItems items take one wave per workgroup: it walks all of the
+// block's items, which spreads the start-up latency of the K/V fragments, the row list and
+// the first item over more items, and a workgroup of one wave needs only 15 KB of LDS, so
+// eight blocks run per CU. Blocks chosen by many groups (selection can concentrate on a
+// few blocks) take a second launch of eight-wave workgroups, so that no single wave walks
+// a long list; each launch skips the other's blocks. Each wave keeps a ring of three item
+// slots in LDS (16 query rows of Q and dO and their packed row terms), filled by direct
 // global->LDS loads two items ahead. The slots are three distinct LDS objects and the item
 // loop is unrolled by three with a straight-line body (steps past the end of the list
 // compute with zero weights), so reads of a slot wait only for that slot's loads. Item row
@@ -1378,7 +1386,7 @@ __global__ void __launch_bounds__(64 * NWV) slc_bwd_kv_dma_kernel(const bf16_t* 
                                                              const uint32_t* groups, const int* seg_start,
                                                              const int* seg_end, QTerms qt, int H, int N, int ls,
                                                              int g, long long nseg, float sl2, float scale, float* dk,
-                                                             float* dv) {
+                                                             float* dv, int min_items, int max_items) {
   constexpr int NCH = HD / 32, DB = HD / 16;
   constexpr int SL = 16 * HD;             // elements of one 16-row tile
   constexpr int SLOT = 2 * SL + 64 * 8;   // one wave's slot: Q tile, dO tile, 64 lanes' row terms
@@ -1388,165 +1396,193 @@ __global__ void __launch_bounds__(64 * NWV) slc_bwd_kv_dma_kernel(const bf16_t* 
   __shared__ int rows_all[NWV][kRound];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r = lane & 15, j = lane >> 4;
-  const long long seg = blockIdx.x;
-  const int nblk = N / ls;
-  const long long bh = seg / nblk;
-  const int blk = (int)(seg % nblk);
-  const int b = (int)(bh / H);
-  const int s0 = seg_start[seg], s1 = seg_end[seg];
-  if (s1 <= s0) return;                     // uniform over the workgroup
-  const bf16_t* qh = q + (size_t)bh * N * HD;
-  const bf16_t* dh = dout + (size_t)bh * N * HD;
-  const float4* th = qt.t4 + (size_t)bh * N;
-  const uint8_t* val = valid_all ? valid_all + (size_t)b * N : nullptr;
-  int* rows = rows_all[wid];
+  // one block of the selection: its partial dK/dV over its items, added into dk/dv
+  auto block = [&](long long seg) {
+    const int nblk = N / ls;
+    const long long bh = seg / nblk;
+    const int blk = (int)(seg % nblk);
+    const int b = (int)(bh / H);
+    const int s0 = seg_start[seg], s1 = seg_end[seg];
+    if (s1 <= s0) return;                     // uniform over the workgroup
+    const bf16_t* qh = q + (size_t)bh * N * HD;
+    const bf16_t* dh = dout + (size_t)bh * N * HD;
+    const float4* th = qt.t4 + (size_t)bh * N;
+    const uint8_t* val = valid_all ? valid_all + (size_t)b * N : nullptr;
+    int* rows = rows_all[wid];
 
-  const int qblocks = g >= 16 ? g / 16 : 1;
-  const int qrows = g >= 16 ? 16 : g;       // real rows of each 16-query block
-  const int nwork = (s1 - s0) * qblocks;    // (group, 16-query block) items of this block
-  const int nmine = nwork > wid ? (nwork - wid + NWV - 1) / NWV : 0;   // items w, w+NWV, ... of this wave
+    const int qblocks = g >= 16 ? g / 16 : 1;
+    const int qrows = g >= 16 ? 16 : g;       // real rows of each 16-query block
+    const int nwork = (s1 - s0) * qblocks;    // (group, 16-query block) items of this block
+    if (nwork < min_items || nwork > max_items) return;   // the other launch's block
+    const int nmine = nwork > wid ? (nwork - wid + NWV - 1) / NWV : 0;   // items w, w+NWV, ... of this wave
 
-  CT kf[KBW][NCH], vf[KBW][NCH];
-  bool kok[KBW];
-#pragma unroll
-  for (int kb = 0; kb < KBW; ++kb) {
-    const int key = blk * ls + 16 * kb + r;
-    kok[kb] = val == nullptr || val[key];
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      kf[kb][c] = load_chunk(k + ((size_t)bh * N + key) * HD + 32 * c + 8 * j);
-      vf[kb][c] = load_chunk(v + ((size_t)bh * N + key) * HD + 32 * c + 8 * j);
-    }
-  }
-  f32x4 dka[KBW][DB], dva[KBW][DB];
-#pragma unroll
-  for (int kb = 0; kb < KBW; ++kb)
-#pragma unroll
-    for (int db = 0; db < DB; ++db) { dka[kb][db] = f32x4{0.f, 0.f, 0.f, 0.f}; dva[kb][db] = dka[kb][db]; }
-
-  int cnt = 0;   // items of the current round
-  // item i's rows into a slot (past the round: a repeat of the last item, never used);
-  // every lane loads a row term (lanes 16-63 repeat rows 0-15), so no load sits under a
-  // lane mask
-  auto issue = [&](int i, bf16_t* slot) {
-    const int qr0 = rows[min(i, cnt - 1)];
-    bf16_t* base = slot + wid * SLOT;
-    dma_tile<HD, 16, 1>(base, qh, qr0, N, 0, lane);
-    dma_tile<HD, 16, 1>(base + SL, dh, qr0, N, 0, lane);
-    __builtin_amdgcn_global_load_lds(th + min(qr0 + (lane & 15), N - 1), base + 2 * SL, 16, 0, 0);
-  };
-  // global->LDS loads per item: waiting until at most this many are outstanding leaves
-  // only the next item's in flight
-  constexpr int kPerItem = 2 * (HD / 32) + 1;
-  auto step = [&](int i, const bf16_t* cur, bf16_t* next) {
-    __builtin_amdgcn_s_waitcnt(0x0F70 | kPerItem);   // vmcnt(kPerItem): this slot has landed
-    issue(i + 2, next);
-    const bf16_t* qs = cur + wid * SLOT;
-    const bf16_t* ds = qs + SL;
-    const float4* ts = reinterpret_cast<const float4*>(qs + 2 * SL);
-    const bool live = i < cnt;   // steps past the end of the round compute with zero weights
-    CT aq[NCH], ad[NCH];
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      aq[c] = lds_row_chunk<HD>(qs, r, 4 * c + j);
-      ad[c] = lds_row_chunk<HD>(ds, r, 4 * c + j);
-    }
-    float cl[4], cg[4], cdv[4];
-#pragma unroll
-    for (int ii = 0; ii < 4; ++ii) {
-      const float4 t = ts[4 * j + ii];                  // log2 LSE - log2 s, s, R
-      cl[ii] = live && 4 * j + ii < qrows ? t.x : __builtin_huge_valf();
-      cg[ii] = t.y;
-      cdv[ii] = t.z;
-    }
-    uint2 aqt[DB], adt[DB];
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      aqt[db] = lds_tr4<HD>(qs, 0, 16 * db, lane);
-      adt[db] = lds_tr4<HD>(ds, 0, 16 * db, lane);
-    }
-#pragma unroll
+    CT kf[KBW][NCH], vf[KBW][NCH];
+    bool kok[KBW];
+  #pragma unroll
     for (int kb = 0; kb < KBW; ++kb) {
-      f32x4 sv = f32x4{0.f, 0.f, 0.f, 0.f}, dp = sv;
-#pragma unroll
+      const int key = blk * ls + 16 * kb + r;
+      kok[kb] = val == nullptr || val[key];
+  #pragma unroll
       for (int c = 0; c < NCH; ++c) {
-        sv = mma(aq[c], kf[kb][c], sv);
-        dp = mma(ad[c], vf[kb][c], dp);
+        kf[kb][c] = load_chunk(k + ((size_t)bh * N + key) * HD + 32 * c + 8 * j);
+        vf[kb][c] = load_chunk(v + ((size_t)bh * N + key) * HD + 32 * c + 8 * j);
       }
-      float pg[4], dsv[4];
-#pragma unroll
+    }
+    f32x4 dka[KBW][DB], dva[KBW][DB];
+  #pragma unroll
+    for (int kb = 0; kb < KBW; ++kb)
+  #pragma unroll
+      for (int db = 0; db < DB; ++db) { dka[kb][db] = f32x4{0.f, 0.f, 0.f, 0.f}; dva[kb][db] = dka[kb][db]; }
+
+    int cnt = 0;   // items of the current round
+    // item i's rows into a slot (past the round: a repeat of the last item, never used);
+    // every lane loads a row term (lanes 16-63 repeat rows 0-15), so no load sits under a
+    // lane mask
+    auto issue = [&](int i, bf16_t* slot) {
+      const int qr0 = rows[min(i, cnt - 1)];
+      bf16_t* base = slot + wid * SLOT;
+      dma_tile<HD, 16, 1>(base, qh, qr0, N, 0, lane);
+      dma_tile<HD, 16, 1>(base + SL, dh, qr0, N, 0, lane);
+      __builtin_amdgcn_global_load_lds(th + min(qr0 + (lane & 15), N - 1), base + 2 * SL, 16, 0, 0);
+    };
+    // global->LDS loads per item: waiting until at most this many are outstanding leaves
+    // only the next item's in flight
+    constexpr int kPerItem = 2 * (HD / 32) + 1;
+    auto step = [&](int i, const bf16_t* cur, bf16_t* next) {
+      __builtin_amdgcn_s_waitcnt(0x0F70 | kPerItem);   // vmcnt(kPerItem): this slot has landed
+      issue(i + 2, next);
+      const bf16_t* qs = cur + wid * SLOT;
+      const bf16_t* ds = qs + SL;
+      const float4* ts = reinterpret_cast<const float4*>(qs + 2 * SL);
+      const bool live = i < cnt;   // steps past the end of the round compute with zero weights
+      CT aq[NCH], ad[NCH];
+  #pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        aq[c] = lds_row_chunk<HD>(qs, r, 4 * c + j);
+        ad[c] = lds_row_chunk<HD>(ds, r, 4 * c + j);
+      }
+      float cl[4], cg[4], cdv[4];
+  #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
-        const float pr = kok[kb] ? fast_exp2(__builtin_fmaf(sv[ii], sl2, -cl[ii])) : 0.f;
-        pg[ii] = pr;
-        dsv[ii] = pr * (dp[ii] - cdv[ii]);
+        const float4 t = ts[4 * j + ii];                  // log2 LSE - log2 s, s, R
+        cl[ii] = live && 4 * j + ii < qrows ? t.x : __builtin_huge_valf();
+        cg[ii] = t.y;
+        cdv[ii] = t.z;
       }
-#pragma unroll
+      uint2 aqt[DB], adt[DB];
+  #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        dva[kb][db] = mma16(adt[db], pg, dva[kb][db]);
-        dka[kb][db] = mma16(aqt[db], dsv, dka[kb][db]);
+        aqt[db] = lds_tr4<HD>(qs, 0, 16 * db, lane);
+        adt[db] = lds_tr4<HD>(ds, 0, 16 * db, lane);
+      }
+  #pragma unroll
+      for (int kb = 0; kb < KBW; ++kb) {
+        f32x4 sv = f32x4{0.f, 0.f, 0.f, 0.f}, dp = sv;
+  #pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+          sv = mma(aq[c], kf[kb][c], sv);
+          dp = mma(ad[c], vf[kb][c], dp);
+        }
+        float pg[4], dsv[4];
+  #pragma unroll
+        for (int ii = 0; ii < 4; ++ii) {
+          const float pr = kok[kb] ? fast_exp2(__builtin_fmaf(sv[ii], sl2, -cl[ii])) : 0.f;
+          pg[ii] = pr;
+          dsv[ii] = pr * (dp[ii] - cdv[ii]);
+        }
+  #pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          dva[kb][db] = mma16(adt[db], pg, dva[kb][db]);
+          dka[kb][db] = mma16(aqt[db], dsv, dka[kb][db]);
+        }
+      }
+    };
+    for (int base = 0; base < nmine; base += kRound) {
+      cnt = __builtin_amdgcn_readfirstlane(min(kRound, nmine - base));
+      wave_sync();   // the previous round's row list and slots are no longer read
+      for (int e = lane; e < cnt; e += 64) {
+        const int item = wid + NWV * (base + e);
+        rows[e] = (int)groups[s0 + item / qblocks] * g + 16 * (item % qblocks);
+      }
+      vm_drain();    // key/value fragments and row indices are in before the ring starts
+      wave_sync();
+      issue(0, ring0);
+      issue(1, ring1);
+      for (int i = 0; i < cnt; i += 3) {   // straight-line body
+        step(i, ring0, ring2);
+        step(i + 1, ring1, ring0);
+        step(i + 2, ring2, ring1);
+      }
+      vm_drain();    // the repeats still in flight land before the slots are reused
+    }
+    // fixed-order sum of the waves' partials (NWV > 1): wave 0 accumulates waves 1, 2, ...,
+    // one 16-key block at a time, through the (now idle) first two ring slots
+    float* red0 = reinterpret_cast<float*>(ring0);
+    float* red1 = reinterpret_cast<float*>(ring1);
+    static_assert(NWV == 1 || 16 * HD * 4 <= NWV * SLOT * 2, "reduction buffer");
+  #pragma unroll
+    for (int kb = 0; kb < KBW; ++kb) {
+      for (int w = 1; w < NWV; ++w) {
+        __syncthreads();
+        if (wid == w) {
+  #pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            const int o = r * HD + 16 * db + 4 * j;
+            *reinterpret_cast<f32x4*>(&red0[o]) = dka[kb][db];
+            *reinterpret_cast<f32x4*>(&red1[o]) = dva[kb][db];
+          }
+        }
+        __syncthreads();
+        if (wid == 0) {
+  #pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            const int o = r * HD + 16 * db + 4 * j;
+            dka[kb][db] += *reinterpret_cast<const f32x4*>(&red0[o]);
+            dva[kb][db] += *reinterpret_cast<const f32x4*>(&red1[o]);
+          }
+        }
+      }
+    }
+    if (wid != 0) return;
+  #pragma unroll
+    for (int kb = 0; kb < KBW; ++kb) {
+      const size_t off = ((size_t)bh * N + blk * ls + 16 * kb + r) * HD;
+  #pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        float* pk = dk + off + 16 * db + 4 * j;
+        float* pv = dv + off + 16 * db + 4 * j;
+        float4 ok4 = *reinterpret_cast<float4*>(pk), ov4 = *reinterpret_cast<float4*>(pv);
+        f32x4 a = dka[kb][db] * scale, c = dva[kb][db];
+        a[0] += ok4.x; a[1] += ok4.y; a[2] += ok4.z; a[3] += ok4.w;
+        c[0] += ov4.x; c[1] += ov4.y; c[2] += ov4.z; c[3] += ov4.w;
+        store4(pk, a, 1.0f);
+        store4(pv, c, 1.0f);
       }
     }
   };
-  for (int base = 0; base < nmine; base += kRound) {
-    cnt = __builtin_amdgcn_readfirstlane(min(kRound, nmine - base));
-    wave_sync();   // the previous round's row list and slots are no longer read
-    for (int e = lane; e < cnt; e += 64) {
-      const int item = wid + NWV * (base + e);
-      rows[e] = (int)groups[s0 + item / qblocks] * g + 16 * (item % qblocks);
-    }
-    vm_drain();    // key/value fragments and row indices are in before the ring starts
-    wave_sync();
-    issue(0, ring0);
-    issue(1, ring1);
-    for (int i = 0; i < cnt; i += 3) {   // straight-line body
-      step(i, ring0, ring2);
-      step(i + 1, ring1, ring0);
-      step(i + 2, ring2, ring1);
-    }
-    vm_drain();    // the repeats still in flight land before the slots are reused
-  }
-  // fixed-order sum of the waves' partials (NWV > 1): wave 0 accumulates waves 1, 2, ...,
-  // one 16-key block at a time, through the (now idle) first two ring slots
-  float* red0 = reinterpret_cast<float*>(ring0);
-  float* red1 = reinterpret_cast<float*>(ring1);
-  static_assert(NWV == 1 || 16 * HD * 4 <= NWV * SLOT * 2, "reduction buffer");
-#pragma unroll
-  for (int kb = 0; kb < KBW; ++kb) {
-    for (int w = 1; w < NWV; ++w) {
+  if constexpr (NWV == 1) {
+    block(blockIdx.x);
+  } else {
+    // persistent workgroups: each takes the blocks blockIdx.x + gridDim.x * t, reads their
+    // item counts together, and walks the ones of this launch's size class in turn
+    __shared__ int todo[64 * NWV];
+    __shared__ int ntodo;
+    const int qb = g >= 16 ? g / 16 : 1;
+    for (long long base = blockIdx.x; base < nseg; base += (long long)gridDim.x * (64 * NWV)) {
+      __syncthreads();   // the previous round's list is no longer read
+      if (threadIdx.x == 0) ntodo = 0;
       __syncthreads();
-      if (wid == w) {
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const int o = r * HD + 16 * db + 4 * j;
-          *reinterpret_cast<f32x4*>(&red0[o]) = dka[kb][db];
-          *reinterpret_cast<f32x4*>(&red1[o]) = dva[kb][db];
-        }
+      const long long sg = base + (long long)gridDim.x * threadIdx.x;
+      if (sg < nseg) {
+        const int nw = (seg_end[sg] - seg_start[sg]) * qb;
+        if (nw >= min_items && nw <= max_items) todo[atomicAdd(&ntodo, 1)] = (int)(sg - base);
       }
       __syncthreads();
-      if (wid == 0) {
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const int o = r * HD + 16 * db + 4 * j;
-          dka[kb][db] += *reinterpret_cast<const f32x4*>(&red0[o]);
-          dva[kb][db] += *reinterpret_cast<const f32x4*>(&red1[o]);
-        }
+      const int cnt = ntodo;
+      for (int e = 0; e < cnt; ++e) {
+        block(base + (long long)todo[e]);
+        __syncthreads();   // LDS slots and the reduction buffer are reused by the next block
       }
-    }
-  }
-  if (wid != 0) return;
-#pragma unroll
-  for (int kb = 0; kb < KBW; ++kb) {
-    const size_t off = ((size_t)bh * N + blk * ls + 16 * kb + r) * HD;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      float* pk = dk + off + 16 * db + 4 * j;
-      float* pv = dv + off + 16 * db + 4 * j;
-      float4 ok4 = *reinterpret_cast<float4*>(pk), ov4 = *reinterpret_cast<float4*>(pv);
-      f32x4 a = dka[kb][db] * scale, c = dva[kb][db];
-      a[0] += ok4.x; a[1] += ok4.y; a[2] += ok4.z; a[3] += ok4.w;
-      c[0] += ov4.x; c[1] += ov4.y; c[2] += ov4.z; c[3] += ov4.w;
-      store4(pk, a, 1.0f);
-      store4(pv, c, 1.0f);
     }
   }
 }
@@ -1555,12 +1591,17 @@ template <typename T, int HD, int KBW>
 void launch_slc_kv(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v, const T* dout,
                    const uint8_t* valid, const uint32_t* groups, const int* seg_start, const int* seg_end, QTerms qt,
                    int H, int N, int ls, int g, long long nseg, float sl2, float scale, float* dk, float* dv) {
-  if constexpr (sizeof(T) == 2)
+  if constexpr (sizeof(T) == 2) {
     hipLaunchKernelGGL((slc_bwd_kv_dma_kernel<HD, KBW, 1>), grid, dim3(64), 0, st, q, k, v, dout, valid, groups,
-                       seg_start, seg_end, qt, H, N, ls, g, nseg, sl2, scale, dk, dv);
-  else
+                       seg_start, seg_end, qt, H, N, ls, g, nseg, sl2, scale, dk, dv, 1, kSlcLightItems);
+    const dim3 pgrid((unsigned)std::min<long long>(nseg, kSlcHeavyGroups));   // persistent: one per CU
+    hipLaunchKernelGGL((slc_bwd_kv_dma_kernel<HD, KBW, 8>), pgrid, dim3(512), 0, st, q, k, v, dout, valid, groups,
+                       seg_start, seg_end, qt, H, N, ls, g, nseg, sl2, scale, dk, dv, kSlcLightItems + 1,
+                       std::numeric_limits<int>::max());
+  } else {
     hipLaunchKernelGGL((slc_bwd_kv_kernel<T, HD, KBW>), grid, dim3(256), 0, st, q, k, v, dout, valid, groups,
                        seg_start, seg_end, qt, H, N, ls, g, nseg, sl2, scale, dk, dv);
+  }
 }
 
 template <typename T, int HD>
