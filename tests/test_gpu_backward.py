@@ -131,6 +131,35 @@ def test_backward_scaling_one_head():
     assert all(e < TOL[cfg.dtype] for e in errs.values()), errs
 
 
+def test_backward_scaling_group_compression_one_head():
+    """The 65536-point workload with MLP query coarsening and group compression (Eq. 13-15),
+    one head against the oracle. Its selection concentrates on a few blocks (one block is
+    chosen by about a thousand groups), so the selection dK/dV pass takes its path for
+    blocks with many items (more than 256 (group, query-block) items: eight waves per
+    block); the test checks that such a block is present."""
+    cfg = CONFIGS[3]
+    pkw = dict(q_coarsen=1, group_compression=1)
+    print("backward parity config 3, group compression (head 2)", flush=True)
+    inp = make_inputs(cfg, layout="ball", with_grad=True)
+    valid = valid_from_tree(cfg)
+    g, (p, q, k, v, vd, gate, phi_k, phi_v, saved, o, phi_q) = gpu_forward(cfg, inp, valid, **pkw)
+    grads = gb.backward(p, q, k, v, vd, gate, phi_k, phi_v, saved, to_dev(inp["do"], p.torch_dtype), phi_q=phi_q)
+    torch.cuda.synchronize()
+    h = 2
+    sel = g["sel"][:, h:h + 1]
+    counts = np.bincount(sel[sel >= 0].ravel(), minlength=cfg.n_pad // cfg.slc_block)
+    assert counts.max() > 256, counts.max()
+    one = {n: np.ascontiguousarray(inp[n][:, h:h + 1]) for n in ("q", "k", "v", "do")}
+    one.update(gate=inp["gate"], phi_k=inp["phi_k"], phi_v=inp["phi_v"], phi_q=inp["phi_q"])
+    P = oracle_params(cfg, **oracle_kw(pkw))
+    fwd = oracle_with_sel(one, valid, P, sel)
+    ref = ob.backward(one["q"], one["k"], one["v"], valid, one["gate"], one["phi_k"], one["phi_v"], P, fwd,
+                      one["do"], phi_q=one["phi_q"])
+    errs = {n: max_abs(grads[n][:, h:h + 1].cpu().numpy(), ref[n]) for n in ("dq", "dk", "dv")}
+    print({k: f"{v:.2e}" for k, v in errs.items()}, "most items in one block:", int(counts.max()), flush=True)
+    assert all(e < TOL[cfg.dtype] for e in errs.values()), errs
+
+
 def test_one_stream_equals_two_streams():
     """Every kernel is deterministic and the two-stream schedule only reorders independent
     branches, so one-stream and two-stream runs give bit-identical results."""
