@@ -1594,8 +1594,11 @@ void launch_slc_kv(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v
   if constexpr (sizeof(T) == 2) {
     hipLaunchKernelGGL((slc_bwd_kv_dma_kernel<HD, KBW, 1>), grid, dim3(64), 0, st, q, k, v, dout, valid, groups,
                        seg_start, seg_end, qt, H, N, ls, g, nseg, sl2, scale, dk, dv, 1, kSlcLightItems);
-    const dim3 pgrid((unsigned)std::min<long long>(nseg, kSlcHeavyGroups));   // persistent: one per CU
-    hipLaunchKernelGGL((slc_bwd_kv_dma_kernel<HD, KBW, 8>), pgrid, dim3(512), 0, st, q, k, v, dout, valid, groups,
+    // persistent: one workgroup per CU; eight waves, or four where a wave holds four key
+    // blocks (eight would not fit their registers)
+    constexpr int NH = KBW >= 4 ? 4 : 8;
+    const dim3 pgrid((unsigned)std::min<long long>(nseg, kSlcHeavyGroups));
+    hipLaunchKernelGGL((slc_bwd_kv_dma_kernel<HD, KBW, NH>), pgrid, dim3(64 * NH), 0, st, q, k, v, dout, valid, groups,
                        seg_start, seg_end, qt, H, N, ls, g, nseg, sl2, scale, dk, dv, kSlcLightItems + 1,
                        std::numeric_limits<int>::max());
   } else {

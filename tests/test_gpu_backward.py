@@ -14,7 +14,7 @@ import torch
 from oracle import bsa as ob
 from parity import TOL, gpu_forward, max_abs, oracle_kw, oracle_params, to_dev, valid_from_tree
 from paper_2506_12541_amd import bsa as gb
-from workloads import CONFIGS, Config, make_inputs
+from workloads import CONFIGS, Config, make_inputs, round_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -33,8 +33,8 @@ def oracle_with_sel(inp, valid, P, sel):
     return fwd
 
 
-def run_case(cfg, seed=None, gate_scale=1.0, **pkw):
-    inp = make_inputs(cfg, seed, layout="ball", with_grad=True)
+def run_case(cfg, seed=None, gate_scale=1.0, inp=None, **pkw):
+    inp = make_inputs(cfg, seed, layout="ball", with_grad=True) if inp is None else inp
     inp["gate"] = (inp["gate"] * gate_scale).astype(np.float32)
     valid = valid_from_tree(cfg)
     g, (p, q, k, v, vd, gate, phi_k, phi_v, saved, o, phi_q) = gpu_forward(cfg, inp, valid, **pkw)
@@ -75,6 +75,7 @@ def run_case(cfg, seed=None, gate_scale=1.0, **pkw):
     for n in ("dq", "dk", "dv"):
         for b in range(cfg.batch):
             assert not np.any(out[n][b][:, ~valid[b]])
+    return g
 
 
 def test_backward_tiny_fp32():
@@ -106,6 +107,30 @@ def test_backward_small_bf16_with_padding():
     cfg = Config("small_bf16", 2, 900, 1024, 2, 64, "bf16", 128, 16, 16, 32, 4, 16, "uniform", "fwdbwd")
     print("backward parity small bf16 d=64", flush=True)
     run_case(cfg, seed=11)
+
+
+def test_backward_heavily_selected_block():
+    """One selection block chosen by every query group outside its ball (its keys and every
+    query share a strong common direction; mean-pooled compressed keys keep that direction),
+    so its item list exceeds the one-wave limit of the selection dK/dV pass and takes the
+    pass's heavy-block path; l' = 32 (eight waves per heavy block) and l' = 64 (four)."""
+    for ls in (32, 64):
+        cfg = Config(f"heavy_block_ls{ls}", 1, 8192, 8192, 2, 64, "bf16", 256, 16, 16, ls, 4, 16, "uniform", "fwdbwd")
+        inp = make_inputs(cfg, 7, layout="ball", with_grad=True)
+        u = np.zeros(cfg.head_dim)
+        u[::2] = 1.0 / np.sqrt(cfg.head_dim / 2)
+        hot = 77                                          # the selection block everyone chooses
+        # (kept representable in bfloat16, as the generator's inputs are)
+        inp["q"] = round_bf16(inp["q"] + 2.0 * u).astype(inp["q"].dtype)
+        k = inp["k"].astype(np.float64)
+        k[:, :, hot * ls:(hot + 1) * ls] += 4.0 * u
+        inp["k"] = round_bf16(k).astype(inp["k"].dtype)
+        print(f"backward parity, heavily selected block, l' = {ls}", flush=True)
+        g = run_case(cfg, inp=inp, kv_pool=1)
+        sel = g["sel"]
+        most = max(int(np.bincount(sel[0, h][sel[0, h] >= 0].ravel()).max()) for h in range(cfg.heads))
+        print("most items in one block:", most, flush=True)
+        assert most > 256, most
 
 
 def test_backward_scaling_one_head():
