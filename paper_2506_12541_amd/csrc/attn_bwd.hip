@@ -1372,8 +1372,9 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t
 // block's items, which spreads the start-up latency of the K/V fragments, the row list and
 // the first item over more items, and a workgroup of one wave needs only 15 KB of LDS, so
 // eight blocks run per CU. Blocks chosen by many groups (selection can concentrate on a
-// few blocks) take a second launch of eight-wave workgroups, so that no single wave walks
-// a long list; each launch skips the other's blocks. Each wave keeps a ring of three item
+// few blocks) take a second launch of persistent workgroups of eight waves (four where a
+// wave holds four key blocks), so that no single wave walks a long list; each launch
+// skips the other's blocks. Each wave keeps a ring of three item
 // slots in LDS (16 query rows of Q and dO and their packed row terms), filled by direct
 // global->LDS loads two items ahead. The slots are three distinct LDS objects and the item
 // loop is unrolled by three with a straight-line body (steps past the end of the list
@@ -1575,6 +1576,7 @@ __global__ void __launch_bounds__(64 * NWV) slc_bwd_kv_dma_kernel(const bf16_t* 
       const long long sg = base + (long long)gridDim.x * threadIdx.x;
       if (sg < nseg) {
         const int nw = (seg_end[sg] - seg_start[sg]) * qb;
+        // (the list's order varies from run to run; each block's result does not depend on it)
         if (nw >= min_items && nw <= max_items) todo[atomicAdd(&ntodo, 1)] = (int)(sg - base);
       }
       __syncthreads();
