@@ -320,14 +320,17 @@ __global__ void __launch_bounds__(256) part_scatter_kernel(const float* pts, int
 }
 
 // ---- the last levels of one node of capacity T <= 1024, in LDS ----
-__global__ void __launch_bounds__(256) bottom_kernel(const float* pts, int dim, int n_real, int n_pad,
+// kBottomThreads threads per node, each owning a contiguous run of kBottomItems list slots
+constexpr int kBottomThreads = 1024;
+constexpr int kBottomItems = 3 * kBottom / kBottomThreads;
+__global__ void __launch_bounds__(kBottomThreads) bottom_kernel(const float* pts, int dim, int n_real, int n_pad,
                                                      int log2_npad, int log2t, int nodes, const int* lists,
                                                      int* perm) {
   __shared__ float4 el[3 * kBottom];   // (x, y, z, point as int bits) per list slot
   __shared__ int sub_axis[kBottom / 2];
   __shared__ int sub_idx[kBottom / 2];
   __shared__ float sub_med[kBottom / 2];
-  __shared__ int tmp[8];
+  __shared__ int tmp[kBottomThreads / 64 + 1];
   const int T = 1 << log2t;
   const int nd = blockIdx.x;
   const size_t slots = (size_t)nodes << log2t;
@@ -336,7 +339,7 @@ __global__ void __launch_bounds__(256) bottom_kernel(const float* pts, int dim, 
   const int node_in_cloud = nd % per_cloud;
   const int cloud = nd / per_cloud;
   const int cnt0 = node_count(n_real, log2_npad, log2t, node_in_cloud);
-  for (int i = threadIdx.x; i < 3 * T; i += 256) {
+  for (int i = threadIdx.x; i < 3 * T; i += kBottomThreads) {
     int a = i / T, r = i % T;
     float4 e = make_float4(0.f, 0.f, 0.f, __int_as_float(-1));
     if (r < cnt0) {
@@ -346,12 +349,12 @@ __global__ void __launch_bounds__(256) bottom_kernel(const float* pts, int dim, 
     el[i] = e;
   }
   __syncthreads();
-  const int items = (3 * T + 255) / 256;  // <= 12
+  const int items = (3 * T + kBottomThreads - 1) / kBottomThreads;  // <= kBottomItems
   for (int log2c = log2t; log2c >= 1; --log2c) {
     const int C = 1 << log2c;
     const int nsub = T >> log2c;
     // split of every sub-node
-    for (int s = threadIdx.x; s < nsub; s += 256) {
+    for (int s = threadIdx.x; s < nsub; s += kBottomThreads) {
       int cnt = node_count(n_real, log2_npad, log2c, node_in_cloud * nsub + s);
       int axis = 0, midx = -1;
       float med = 0.f;
@@ -373,11 +376,11 @@ __global__ void __launch_bounds__(256) bottom_kernel(const float* pts, int dim, 
       sub_med[s] = med;
     }
     __syncthreads();
-    float4 e[12];
-    int f[12];
+    float4 e[kBottomItems];
+    int f[kBottomItems];
     int mine = 0;
 #pragma unroll
-    for (int it = 0; it < 12; ++it) {
+    for (int it = 0; it < kBottomItems; ++it) {
       f[it] = -1;
       int i = threadIdx.x * items + it;
       if (it < items && i < 3 * T) {
@@ -400,7 +403,7 @@ __global__ void __launch_bounds__(256) bottom_kernel(const float* pts, int dim, 
     {
       int run = pre;
 #pragma unroll
-      for (int it = 0; it < 12; ++it) {
+      for (int it = 0; it < kBottomItems; ++it) {
         int i = threadIdx.x * items + it;
         if (it < items && i < 3 * T) {
           if ((i & (C - 1)) == 0) start_pref[i >> log2c] = run;
@@ -410,12 +413,12 @@ __global__ void __launch_bounds__(256) bottom_kernel(const float* pts, int dim, 
     }
     __syncthreads();
     // all old values are in registers: rewrite the lists in place
-    for (int i = threadIdx.x; i < 3 * T; i += 256) el[i] = make_float4(0.f, 0.f, 0.f, __int_as_float(-1));
+    for (int i = threadIdx.x; i < 3 * T; i += kBottomThreads) el[i] = make_float4(0.f, 0.f, 0.f, __int_as_float(-1));
     __syncthreads();
     {
       int run = pre;
 #pragma unroll
-      for (int it = 0; it < 12; ++it) {
+      for (int it = 0; it < kBottomItems; ++it) {
         int i = threadIdx.x * items + it;
         if (it < items && i < 3 * T && f[it] >= 0) {
           int sub_start = i & ~(C - 1);
@@ -429,7 +432,7 @@ __global__ void __launch_bounds__(256) bottom_kernel(const float* pts, int dim, 
     }
     __syncthreads();
   }
-  for (int r = threadIdx.x; r < T; r += 256) {
+  for (int r = threadIdx.x; r < T; r += kBottomThreads) {
     int g = __float_as_int(el[r].w);
     perm[start + r] = g >= 0 ? g - cloud * n_real : -1;
   }
@@ -578,7 +581,7 @@ hipError_t launch_build_tree(const float* pts, int64_t n_real, int dim, int64_t 
     std::swap(la, lb);
   }
   const int nodes = (int)(slots >> log2t);
-  hipLaunchKernelGGL(bottom_kernel, dim3(nodes), dim3(256), 0, st, pts, dim, (int)n_real, (int)n_pad,
+  hipLaunchKernelGGL(bottom_kernel, dim3(nodes), dim3(kBottomThreads), 0, st, pts, dim, (int)n_real, (int)n_pad,
                      log2_npad, log2t, nodes, la, perm);
   return hipGetLastError();
 }
