@@ -65,11 +65,19 @@ typedef struct {
   int32_t cmp_stride;     /* compression stride; must equal cmp_block (Eq. 5)          */
   int32_t slc_block;      /* l': selection block length of Eq. 8 (l'=r*l, r in 1,2,4;
                              multiple of 16; divides m)                                */
-  int32_t topk;           /* k*: selected blocks per group (Eq. 7), 1..32              */
-  int32_t group_size;     /* g: query group size of Eq. 10 (8, 16, 32 or 64; divides m) */
+  int32_t topk;           /* k*: selected blocks per group (Eq. 7), 1..16; also
+                             (16/g or 1) * k* * l' <= 4096                             */
+  int32_t group_size;     /* g: query group size of Eq. 10: 1 (per-token selection, bf16
+                             only) or a power of two >= 8 dividing m                   */
   int32_t mask_own_ball;  /* 1: a group may not select blocks of its own ball          */
-  int32_t store_lse;      /* must be 1: log-sum-exp rows are saved by the forward pass */
-  int32_t deterministic;  /* accepted for 0 and 1: every kernel is atomic-free on floats */
+  int32_t store_lse;      /* 1: the forward keeps each branch's log-sum-exp rows for the
+                             backward; 0: they are not kept (saved.lse is NULL) and the
+                             backward recomputes them by the branches' forward kernels
+                             without the value products (same tiles and order: equal
+                             to the stored rows bit for bit)                          */
+  int32_t deterministic;  /* 0 or 1, no effect: every kernel is deterministic (no float
+                             atomics; fixed-order sums), so both values give
+                             bit-identical results                                     */
   int32_t kv_pool;        /* bsa_pool_t: MLP (default) or mean pooling of Eq. 5        */
   int32_t dtype;          /* bsa_dtype_t of Q, K, V, O, dO and the saved branch outputs */
   float softmax_scale;    /* 0 -> 1/sqrt(d)                                            */
@@ -92,8 +100,10 @@ typedef struct { float *w1, *b1, *w2, *b2; } bsa_mlp_grad_t;
  * bsa_saved_view() carves them out of one buffer of bsa_sizes()'s saved_bytes. */
 typedef struct {
   int32_t* sel_idx;  /* [B, H, N/g, k*] selected block ids, ascending, -1 = empty slot  */
-  float* lse;        /* [3, B, H, N] natural-log log-sum-exp per branch, -inf = no key  */
-  void* o_branch;    /* [3, B, H, N, d] dtype: ball, compression, selection outputs     */
+  float* lse;        /* [3, B, H, N] natural-log log-sum-exp per branch, -inf = no key;
+                        NULL with store_lse = 0 (if set anyway, the forward fills it and
+                        the backward still recomputes the rows)                         */
+  void* o_branch;    /* [2, B, H, N, d] dtype: ball (0) and selection (1) outputs       */
   float* kcmp;       /* [B, H, N/l, d] compressed keys                                  */
   float* vcmp;       /* [B, H, N/l, d] compressed values                                */
   float* hid_k;      /* [B, H, N/l, d] hidden pre-activation of phi_k                   */
@@ -102,6 +112,11 @@ typedef struct {
   float* qcmp;       /* [B, H, N/g, d] coarse queries of the selection (Eq. 11 or 13)   */
   float* hid_q;      /* [B, H, N/l, d] hidden pre-activation of phi_q (BSA_QC_MLP)      */
   float* ocmp;       /* [B, H, N/l, d] coarse attention outputs of group compression    */
+  float* o_cmp;      /* [B, H, N, d] float32 output of the compression branch. Kept
+                        unrounded: the backward's softmax delta rowsum(dO o) comes from
+                        it, and an error in that delta is common to every compressed key
+                        of the query, so it would add up over the blocks in the
+                        compression MLP's weight gradients                              */
 } bsa_saved_t;
 
 /* ---- Ball tree (Section 2.1 "Ball Tree Attention"; the ordering every branch uses) ---- */
@@ -262,7 +277,7 @@ bsa_status_t bsa_block_backward(const bsa_params_t* p, int32_t ffn_dim, const bs
 /* on = 1: start recording, clearing earlier records; on = 0: stop and clear. While on,
  * every timed phase of the library records a start and a stop HIP event on the stream
  * its kernels are launched on (phases on the two streams of a call may overlap in time). Phases: "tree", "permute", "fwd.compress", "fwd.select",
- * "fwd.ball", "fwd.cmp", "fwd.slc", "fwd.gate", "bwd.gate", "bwd.dq_ball", "bwd.dq_cmp",
+ * "fwd.ball", "fwd.cmp", "fwd.slc", "fwd.gate", "bwd.lse" (store_lse = 0), "bwd.gate", "bwd.dq_ball", "bwd.dq_cmp",
  * "bwd.dq_slc", "bwd.kv_ball", "bwd.kv_cmp", "bwd.mlp", "bwd.slc_csr", "bwd.slc_kv", and
  * for the block "blk.norm", "blk.gemm" (activation products), "blk.wgrad" (weight
  * gradients), "blk.elem" (SwiGLU, casts, layout changes).

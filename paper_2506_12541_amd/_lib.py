@@ -39,6 +39,7 @@ class bsa_saved_t(C.Structure):
         ("sel_idx", C.c_void_p), ("lse", C.c_void_p), ("o_branch", C.c_void_p),
         ("kcmp", C.c_void_p), ("vcmp", C.c_void_p), ("hid_k", C.c_void_p), ("hid_v", C.c_void_p),
         ("cvalid", C.c_void_p), ("qcmp", C.c_void_p), ("hid_q", C.c_void_p), ("ocmp", C.c_void_p),
+        ("o_cmp", C.c_void_p),
     ]
 
 

@@ -159,8 +159,10 @@ class Saved:
             return self.buf[off:off + count * esz].view(dtype).view(shape)
 
         self.sel_idx = view(self.c.sel_idx, torch.int32, (B, H, N // p.group_size, p.topk))
-        self.lse = view(self.c.lse, torch.float32, (3, B, H, N))
-        self.o_branch = view(self.c.o_branch, p.torch_dtype, (3, B, H, N, d))
+        # store_lse = 0: the statistics are not kept (the backward recomputes them)
+        self.lse = view(self.c.lse, torch.float32, (3, B, H, N)) if self.c.lse else None
+        self.o_branch = view(self.c.o_branch, p.torch_dtype, (2, B, H, N, d))   # ball, selection
+        self.o_cmp = view(self.c.o_cmp, torch.float32, (B, H, N, d))
         self.kcmp = view(self.c.kcmp, torch.float32, (B, H, N // p.cmp_block, d))
         self.vcmp = view(self.c.vcmp, torch.float32, (B, H, N // p.cmp_block, d))
         self.hid_k = view(self.c.hid_k, torch.float32, (B, H, N // p.cmp_block, d))
@@ -169,6 +171,12 @@ class Saved:
         self.qcmp = view(self.c.qcmp, torch.float32, (B, H, N // p.group_size, d))
         self.hid_q = view(self.c.hid_q, torch.float32, (B, H, N // p.cmp_block, d)) if self.c.hid_q else None
         self.ocmp = view(self.c.ocmp, torch.float32, (B, H, N // p.cmp_block, d)) if self.c.ocmp else None
+
+
+    def branch_outputs(self) -> torch.Tensor:
+        """The three branch outputs as one float32 [3, B, H, N, d] tensor (ball, compression,
+        selection); a copy, for inspection."""
+        return torch.stack([self.o_branch[0].float(), self.o_cmp, self.o_branch[1].float()])
 
 
 def _mlp(phi):

@@ -66,7 +66,7 @@ bsa_status_t check_params(const bsa_params_t* p, bsa::Dims* D) {
   if ((int64_t)p->batch * p->heads * p->n * p->topk >= (int64_t)1 << 31)
     return fail(BSA_ERR_UNSUPPORTED, "batch * heads * n * topk must stay below 2^31");
   if (p->mask_own_ball != 0 && p->mask_own_ball != 1) return fail(BSA_ERR_INVALID_ARGUMENT, "mask_own_ball must be 0/1");
-  if (p->store_lse != 1) return fail(BSA_ERR_UNSUPPORTED, "store_lse must be 1");
+  if (p->store_lse != 0 && p->store_lse != 1) return fail(BSA_ERR_INVALID_ARGUMENT, "store_lse must be 0/1");
   if (p->deterministic != 0 && p->deterministic != 1) return fail(BSA_ERR_INVALID_ARGUMENT, "deterministic must be 0/1");
   if (p->kv_pool != BSA_POOL_MLP && p->kv_pool != BSA_POOL_MEAN) return fail(BSA_ERR_INVALID_ARGUMENT, "bad kv_pool");
   if (p->kv_pool == BSA_POOL_MLP && (p->cmp_block * p->head_dim) % 64 != 0)
@@ -100,6 +100,7 @@ bsa_status_t check_params(const bsa_params_t* p, bsa::Dims* D) {
   D->bf16 = p->dtype == BSA_BF16;
   D->qc_mlp = p->q_coarsen == BSA_QC_MLP;
   D->gcmp = p->group_compression;
+  D->store_lse = p->store_lse;
   D->scale = p->softmax_scale > 0.f ? p->softmax_scale : 1.0f / std::sqrt((float)p->head_dim);
   return BSA_OK;
 }
@@ -107,7 +108,7 @@ bsa_status_t check_params(const bsa_params_t* p, bsa::Dims* D) {
 size_t elem_bytes(const bsa::Dims& D) { return D.bf16 ? 2 : 4; }
 
 struct SavedLayout {
-  size_t sel, lse, ob, kc, vc, hk, hv, cv, qc, hq, oc, total;
+  size_t sel, lse, ob, ocf, kc, vc, hk, hv, cv, qc, hq, oc, total;
 };
 
 SavedLayout saved_layout(const bsa::Dims& D) {
@@ -117,8 +118,9 @@ SavedLayout saved_layout(const bsa::Dims& D) {
   size_t off = 0;
   auto put = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
   L.sel = put(sizeof(int32_t) * (size_t)D.B * D.H * (D.N / D.g) * D.k);
-  L.lse = put(sizeof(float) * 3 * rows);
-  L.ob = put(elem_bytes(D) * 3 * rows * D.d);
+  L.lse = put(D.store_lse ? sizeof(float) * 3 * rows : 0);
+  L.ob = put(elem_bytes(D) * 2 * rows * D.d);
+  L.ocf = put(sizeof(float) * rows * D.d);
   L.kc = put(sizeof(float) * crows * D.d);
   L.vc = put(sizeof(float) * crows * D.d);
   L.hk = put(sizeof(float) * crows * D.d);
@@ -132,7 +134,7 @@ SavedLayout saved_layout(const bsa::Dims& D) {
 }
 
 struct FwdWs {
-  size_t w1t_k, w1t_v, w1t_q, kc_lp, vc_lp, qc_lp, lsec, kplanes;
+  size_t w1t_k, w1t_v, w1t_q, kc_lp, vc_lp, qc_lp, lsec, kplanes, lse;
   size_t pk, pv, pkt, pvt, hist, seg_s, seg_e, part, ml;   // per-token selection (g = 1)
   size_t total;
 };
@@ -167,6 +169,7 @@ FwdWs fwd_ws_layout(const bsa::Dims& D) {
   W.qc_lp = put(D.block_coarse() ? elem_bytes(D) * (size_t)D.cmp_rows() * D.d : 0);
   W.lsec = put(D.gcmp ? sizeof(float) * (size_t)D.cmp_rows() : 0);
   W.kplanes = put(3 * sizeof(uint16_t) * (size_t)D.cmp_rows() * D.d);
+  W.lse = put(D.store_lse ? 0 : sizeof(float) * 3 * (size_t)D.rows());   // not kept: forward scratch
   const size_t np = D.g == 1 ? bsa::slc1_pairs(D) : 0;
   const size_t nseg = D.g == 1 ? (size_t)D.B * D.H * (D.N / D.ls) : 0;
   W.pk = put(4 * np);
@@ -183,7 +186,7 @@ FwdWs fwd_ws_layout(const bsa::Dims& D) {
 }
 
 struct BwdWs {
-  size_t qc_lp, doc, t4c, dqc, dqpart;
+  size_t qc_lp, doc, t4c, dqc, dqpart, lse, lsec, ml;
   size_t R, terms, dplp, kc_lp, vc_lp, dkc_part, dvc_part, dkc, dvc, pk, pv, pkt, pvt, hist, seg_s, seg_e, dpre, pw1, psm, w1lp,
       total;
   int cmp_chunks, mlp_chunks, mlp_chunks_small;
@@ -226,6 +229,10 @@ BwdWs bwd_ws_layout(const bsa::Dims& D) {
   W.t4c = put(D.gcmp ? 4 * sizeof(float) * crows : 0);
   W.dqc = put(D.gcmp ? sizeof(float) * crows * D.d : 0);
   W.dqpart = put(D.g == 1 ? sizeof(float) * bsa::slc1_pairs(D) * D.d : 0);
+  // store_lse = 0: recomputed log-sum-exp rows (and what their recomputation needs)
+  W.lse = put(D.store_lse ? 0 : sizeof(float) * 3 * rows);
+  W.lsec = put(!D.store_lse && D.gcmp ? sizeof(float) * crows : 0);
+  W.ml = put(!D.store_lse && D.g == 1 ? 2 * sizeof(float) * bsa::slc1_pairs(D) : 0);
   W.total = off;
   return W;
 }
@@ -346,8 +353,9 @@ bsa_status_t bsa_saved_view(const bsa_params_t* p, void* base, bsa_saved_t* out)
   SavedLayout L = saved_layout(D);
   char* c = (char*)base;
   out->sel_idx = (int32_t*)(c + L.sel);
-  out->lse = (float*)(c + L.lse);
+  out->lse = D.store_lse ? (float*)(c + L.lse) : nullptr;
   out->o_branch = (void*)(c + L.ob);
+  out->o_cmp = (float*)(c + L.ocf);
   out->kcmp = (float*)(c + L.kc);
   out->vcmp = (float*)(c + L.vc);
   out->hid_k = (float*)(c + L.hk);
@@ -394,6 +402,26 @@ static bsa_status_t join_aux(const Aux& a, hipStream_t st) {
   return BSA_OK;
 }
 
+// Joins the auxiliary stream back into the caller's on every exit after a fork, so that a
+// call that fails part-way still leaves no kernel of its own running past the caller's
+// stream (it may still read the caller's buffers). join() does it early on the normal path.
+struct AuxJoin {
+  const Aux& a;
+  hipStream_t st;
+  bool armed = true;
+  AuxJoin(const Aux& a_, hipStream_t st_) : a(a_), st(st_) {}
+  bsa_status_t join() {
+    armed = false;
+    return join_aux(a, st);
+  }
+  ~AuxJoin() {
+    if (armed && a.s != st) {
+      (void)hipEventRecord(a.join, a.s);
+      (void)hipStreamWaitEvent(st, a.join, 0);
+    }
+  }
+};
+
 bsa_status_t bsa_set_streams(int32_t n) {
   g_last_error.clear();
   if (n != 1 && n != 2) return fail(BSA_ERR_INVALID_ARGUMENT, "streams must be 1 or 2");
@@ -403,7 +431,7 @@ bsa_status_t bsa_set_streams(int32_t n) {
 }
 
 static bool saved_ok(const bsa_saved_t* sv, const bsa::Dims& D) {
-  return sv && sv->sel_idx && sv->lse && sv->o_branch && sv->kcmp && sv->vcmp && sv->hid_k && sv->hid_v &&
+  return sv && sv->sel_idx && (sv->lse || !D.store_lse) && sv->o_branch && sv->o_cmp && sv->kcmp && sv->vcmp && sv->hid_k && sv->hid_v &&
          sv->cvalid && sv->qcmp && (!D.qc_mlp || sv->hid_q) && (!D.gcmp || sv->ocmp);
 }
 
@@ -434,6 +462,8 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   char* w = (char*)ws;
   const size_t rows = (size_t)D.rows();
   char* ob = (char*)saved->o_branch;
+  // store_lse = 0 with no saved buffer: the log-sum-exp rows go to forward scratch
+  float* lse = saved->lse ? saved->lse : (float*)(w + W.lse);
   const size_t ob_stride = rows * D.d * elem_bytes(D);
   bsa::Mlp mk{}, mv{}, mq{};
   if (D.pool == 0) {
@@ -465,10 +495,11 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   if (aux.s != st &&
       (hipEventRecord(aux.fork, st) != hipSuccess || hipStreamWaitEvent(aux.s, aux.fork, 0) != hipSuccess))
     return fail(BSA_ERR_HIP, "forking the auxiliary stream failed");
+  AuxJoin joiner(aux, st);
   {
     hipStream_t st_main = st;
     hipStream_t st = aux.s;
-    BSA_STEP("fwd.ball", bsa::launch_ball_fwd(D, q, k, v, valid, ob, saved->lse, st), "ball attention");
+    BSA_STEP("fwd.ball", bsa::launch_ball_fwd(D, q, k, v, valid, ob, lse, st), "ball attention");
     if (D.gcmp) {
       float* oc = saved->ocmp;
       float* lsec = (float*)(w + W.lsec);
@@ -476,12 +507,12 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
                (bsa::launch_cmp_coarse_fwd(D, qc_lp, kc_lp, vc_lp, valid ? saved->cvalid : nullptr, oc, lsec, st) !=
                         hipSuccess
                     ? hipGetLastError()
-                    : bsa::launch_expand_coarse(D, oc, lsec, valid, ob + ob_stride, saved->lse + rows, st)),
+                    : bsa::launch_expand_coarse(D, oc, lsec, valid, saved->o_cmp, lse + rows, st)),
                "group compression");
     } else {
       BSA_STEP("fwd.cmp",
-               bsa::launch_cmp_fwd(D, q, kc_lp, vc_lp, valid, valid ? saved->cvalid : nullptr, ob + ob_stride,
-                                   saved->lse + rows, st),
+               bsa::launch_cmp_fwd(D, q, kc_lp, vc_lp, valid, valid ? saved->cvalid : nullptr, saved->o_cmp,
+                                   lse + rows, st),
                "compressed attention");
     }
     (void)st_main;
@@ -492,16 +523,16 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   if (D.g == 1) {
     const bsa::Slc1Ws S1 = slc1_ws(D, w, W.pk, W.pv, W.pkt, W.pvt, W.hist, W.seg_s, W.seg_e, W.part, W.ml);
     BSA_STEP("fwd.slc",
-             bsa::launch_slc1_fwd(D, q, k, v, valid, saved->sel_idx, S1, ob + 2 * ob_stride, saved->lse + 2 * rows, st),
+             bsa::launch_slc1_fwd(D, q, k, v, valid, saved->sel_idx, S1, ob + ob_stride, lse + 2 * rows, st),
              "per-token selection attention");
   } else {
     BSA_STEP("fwd.slc",
-             bsa::launch_slc_fwd(D, q, k, v, valid, saved->sel_idx, ob + 2 * ob_stride, saved->lse + 2 * rows, st),
+             bsa::launch_slc_fwd(D, q, k, v, valid, saved->sel_idx, ob + ob_stride, lse + 2 * rows, st),
              "selection attention");
   }
-  s = join_aux(aux, st);
+  s = joiner.join();
   if (s != BSA_OK) return s;
-  BSA_STEP("fwd.gate", bsa::launch_gate_fwd(D, ob, gate, valid, o, st), "gate");
+  BSA_STEP("fwd.gate", bsa::launch_gate_fwd(D, ob, saved->o_cmp, gate, valid, o, st), "gate");
 #undef BSA_STEP
   return BSA_OK;
 }
@@ -536,7 +567,7 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   char* w = (char*)ws;
   bsa::BwdArgs A{};
   A.q = q; A.k = k; A.v = v; A.dout = d_o; A.valid = valid; A.gate = gate;
-  A.o_branch = saved->o_branch; A.lse = saved->lse; A.kcmp = saved->kcmp; A.vcmp = saved->vcmp;
+  A.o_branch = saved->o_branch; A.o_cmp = saved->o_cmp; A.lse = saved->lse; A.kcmp = saved->kcmp; A.vcmp = saved->vcmp;
   A.hid_k = saved->hid_k; A.hid_v = saved->hid_v; A.sel = saved->sel_idx; A.cvalid = saved->cvalid;
   A.dq = dq; A.dk = dk; A.dv = dv; A.dgate = dgate;
   A.R = (float*)(w + W.R);
@@ -550,8 +581,13 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   A.seg_start = (int*)(w + W.seg_s); A.seg_end = (int*)(w + W.seg_e);
   A.qcmp = saved->qcmp; A.ocmp = saved->ocmp; A.qc_lp = w + W.qc_lp; A.doc = w + W.doc; A.t4c = (float*)(w + W.t4c);
   A.dqc = (float*)(w + W.dqc);
+  A.lse_ws = (float*)(w + W.lse);
+  A.lsec_ws = (float*)(w + W.lsec);
+  if (D.g == 1)
+    A.s1 = slc1_ws(D, w, W.pk, W.pv, W.pkt, W.pvt, W.hist, W.seg_s, W.seg_e, W.dqpart, D.store_lse ? (size_t)-1 : W.ml);
   // after the dense dK/dV passes, the dQ passes run on the auxiliary stream while the
   // compression and selection dK/dV passes run on the caller's
+  AuxJoin joiner(aux, st);
   BSA_TRY(bsa::launch_attn_bwd(D, A, st, aux.s, aux.fork), "attention backward");
   bsa::MlpBwdWs mw{(float*)(w + W.dpre), (float*)(w + W.pw1), (float*)(w + W.psm), (void*)(w + W.w1lp),
                    W.mlp_chunks, W.mlp_chunks_small, (void*)(w + W.dplp)};
@@ -575,7 +611,7 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
             "per-token selection backward");
   else
     BSA_TRY(bsa::launch_slc_csr(D, A, st), "selection backward");
-  s = join_aux(aux, st);
+  s = joiner.join();
   if (s != BSA_OK) return s;
   if (D.g == 1) {   // the dQ parts of the per-token selection, after the dQ chain
     BSA_PHASE("bwd.dq_slc", st, e = bsa::launch_slc1_merge_dq(D, saved->sel_idx, valid, S1, dq, st));

@@ -33,8 +33,8 @@ __device__ __forceinline__ float lse_log2(float lse) { return lse == -__builtin_
 // The same pass packs each query row's terms for the attention passes (16 bytes per row
 // and branch; the layout QTerms describes).
 template <typename T>
-__global__ void gate_bwd_rows_kernel(const T* dout, const T* ob, long long rows, int hd, const float* lse,
-                                     const float* gate, int H, int N, float* R, float4* terms) {
+__global__ void gate_bwd_rows_kernel(const T* dout, const T* ob, const float* oc, long long rows, int hd,
+                                     const float* lse, const float* gate, int H, int N, float* R, float4* terms) {
   constexpr int EPV = 16 / (int)sizeof(T);
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long row = gid >> 3;
@@ -46,11 +46,17 @@ __global__ void gate_bwd_rows_kernel(const T* dout, const T* ob, long long rows,
       const uint4 dv = *reinterpret_cast<const uint4*>(dout + row * hd + c);
       const T* dp = reinterpret_cast<const T*>(&dv);
 #pragma unroll
-      for (int br = 0; br < 3; ++br) {
-        const uint4 ov = *reinterpret_cast<const uint4*>(ob + br * per + row * hd + c);
+      for (int br = 0; br < 3; br += 2) {   // ball and selection rows (storage type)
+        const uint4 ov = *reinterpret_cast<const uint4*>(ob + (br / 2) * per + row * hd + c);
         const T* op = reinterpret_cast<const T*>(&ov);
 #pragma unroll
         for (int e = 0; e < EPV; ++e) acc[br] += to_f32<T>(dp[e]) * to_f32<T>(op[e]);
+      }
+#pragma unroll
+      for (int e = 0; e < EPV; e += 4) {    // compressed-branch rows (float32)
+        const float4 f = *reinterpret_cast<const float4*>(oc + row * hd + c + e);
+        acc[1] += to_f32<T>(dp[e]) * f.x + to_f32<T>(dp[e + 1]) * f.y + to_f32<T>(dp[e + 2]) * f.z +
+                  to_f32<T>(dp[e + 3]) * f.w;
       }
     }
   }
@@ -1253,10 +1259,48 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t
   const long long rows = D.rows();
   const float sl2 = D.scale * kLog2e;
   const int nct = D.N / D.l;
+  // compressed tokens (and the coarse queries of Eq. 15) in the storage type, as the
+  // forward pass consumed them
+  const T* kc = (const T*)A.kc_lp;
+  const T* vc = (const T*)A.vc_lp;
+  const T* qcl = nullptr;
+  if (D.bf16) {
+    const long long n = D.cmp_rows() * HD;
+    hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.kcmp, n, (T*)A.kc_lp);
+    hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.vcmp, n, (T*)A.vc_lp);
+    if (D.gcmp) {
+      hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.qcmp, n, (T*)A.qc_lp);
+      qcl = (const T*)A.qc_lp;
+    }
+  } else {
+    kc = (const T*)A.kcmp;
+    vc = (const T*)A.vcmp;
+    qcl = (const T*)A.qcmp;
+  }
+  // store_lse = 0: each branch's log-sum-exp rows are recomputed by its forward kernel
+  // without the value products (the same tiles and order, so they equal the stored ones)
+  const float* lse = A.lse;
+  if (!D.store_lse) {
+    hipError_t e = hipSuccess;
+    BSA_PHASE("bwd.lse", st, {
+      e = launch_ball_fwd(D, A.q, A.k, A.v, A.valid, nullptr, A.lse_ws, st);
+      if (e == hipSuccess && D.gcmp) {
+        e = launch_cmp_coarse_fwd(D, qcl, kc, vc, A.valid ? A.cvalid : nullptr, nullptr, A.lsec_ws, st);
+        if (e == hipSuccess) e = launch_expand_coarse(D, nullptr, A.lsec_ws, A.valid, nullptr, A.lse_ws + rows, st);
+      } else if (e == hipSuccess) {
+        e = launch_cmp_fwd(D, A.q, kc, vc, A.valid, A.valid ? A.cvalid : nullptr, nullptr, A.lse_ws + rows, st);
+      }
+      if (e == hipSuccess)
+        e = D.g == 1 ? launch_slc1_fwd(D, A.q, A.k, A.v, A.valid, A.sel, A.s1, nullptr, A.lse_ws + 2 * rows, st)
+                     : launch_slc_fwd(D, A.q, A.k, A.v, A.valid, A.sel, nullptr, A.lse_ws + 2 * rows, st);
+    });
+    if (e != hipSuccess) return e;
+    lse = A.lse_ws;
+  }
   // per-branch row sums and the gate gradient
   BSA_PHASE("bwd.gate", st, {
   hipLaunchKernelGGL(gate_bwd_rows_kernel<T>, dim3((unsigned)((rows * 8 + 255) / 256)), dim3(256), 0, st, (const T*)A.dout,
-                     (const T*)A.o_branch, rows, HD, A.lse, A.gate, D.H, D.N, A.R, (float4*)A.terms);
+                     (const T*)A.o_branch, A.o_cmp, rows, HD, lse, A.gate, D.H, D.N, A.R, (float4*)A.terms);
   hipLaunchKernelGGL(gate_bwd_kernel, dim3((D.B * D.N + 255) / 256), dim3(256), 0, st, A.R, A.gate, A.valid, D.B, D.H,
                      D.N, A.dgate);
   });
@@ -1268,17 +1312,6 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t
   const T* k = (const T*)A.k;
   const T* v = (const T*)A.v;
   const T* dout = (const T*)A.dout;
-  // compressed tokens in the storage type, as the forward pass consumed them
-  const T* kc = (const T*)A.kc_lp;
-  const T* vc = (const T*)A.vc_lp;
-  if (D.bf16) {
-    const long long n = D.cmp_rows() * HD;
-    hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.kcmp, n, (T*)A.kc_lp);
-    hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.vcmp, n, (T*)A.vc_lp);
-  } else {
-    kc = (const T*)A.kcmp;
-    vc = (const T*)A.vcmp;
-  }
   // ---- dK, dV of the ball branch (written) ----
   BSA_PHASE("bwd.kv_ball", st, {
   if (D.m >= 128)
@@ -1288,18 +1321,11 @@ hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t
     (launch_bwd_kv<T, HD, 2, true>)(dim3(D.N / 64, 1, D.B * D.H), st, q, k, v, dout, A.valid, qball, D.H, D.N, D.N,
                                   D.m, 1, sl2, D.scale, A.dk, A.dv);
   });
-  // group compression: coarse queries in the storage type, their dO and row terms
-  const T* qcl = nullptr;
+  // group compression: the coarse queries' dO and row terms
   const T* docl = nullptr;
   QTerms qcoarse{(const float4*)A.t4c};
   if (D.gcmp) {
     const long long n = D.cmp_rows() * HD;
-    if (D.bf16) {
-      hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.qcmp, n, (T*)A.qc_lp);
-      qcl = (const T*)A.qc_lp;
-    } else {
-      qcl = (const T*)A.qcmp;
-    }
     hipLaunchKernelGGL(coarse_rows_bwd_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, dout,
                        t4 + rows, A.ocmp, A.valid, D.H, D.N, D.l, HD, D.cmp_rows(), (T*)A.doc, (float4*)A.t4c);
     docl = (const T*)A.doc;

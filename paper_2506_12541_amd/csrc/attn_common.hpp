@@ -292,7 +292,10 @@ template <> __device__ __forceinline__ f32x8 ones_chunk<float>() {
   return f32x8{1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f};
 }
 
-template <typename T, int HD, int QB>
+// LSE_ONLY: only the softmax statistics (reference maximum and row sums) are formed, in
+// exactly the order of the full step, so the log-sum-exp equals the full step's bit for
+// bit; the V^T reads and the P V products are skipped and finish() writes no output rows.
+template <typename T, int HD, int QB, bool LSE_ONLY = false>
 struct WaveAttn {
   static constexpr int NCH = HD / 32;  // chunks of the head dim
   static constexpr int DB = HD / 16;   // 16-wide dim blocks of O^T
@@ -328,10 +331,12 @@ struct WaveAttn {
       }
     // V^T fragments are read now so that their LDS latency hides behind the softmax
     CT vr[DB][KB / 2];
+    if constexpr (!LSE_ONLY) {
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+      for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int kp = 0; kp < KB / 2; ++kp) vr[db][kp] = vfrag(db, kp);
+        for (int kp = 0; kp < KB / 2; ++kp) vr[db][kp] = vfrag(db, kp);
+    }
     CT pf[QB][KB / 2];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -351,8 +356,10 @@ struct WaveAttn {
         const float alpha = raise ? fast_exp2(mx[qb] - mnew) : 1.0f;
         mx[qb] = mnew;
         lsum[qb] *= alpha;
+        if constexpr (!LSE_ONLY) {
 #pragma unroll
-        for (int db = 0; db < DB; ++db) o[qb][db] *= alpha;
+          for (int db = 0; db < DB; ++db) o[qb][db] *= alpha;
+        }
       }
       const float mref = mx[qb] == kNegInf ? 0.f : mx[qb];
 #pragma unroll
@@ -371,12 +378,14 @@ struct WaveAttn {
     for (int kp = 0; kp < KB / 2; ++kp)
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) lsum[qb] = mma(ones, pf[qb][kp], lsum[qb]);
+    if constexpr (!LSE_ONLY) {
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+      for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int kp = 0; kp < KB / 2; ++kp)
+        for (int kp = 0; kp < KB / 2; ++kp)
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) o[qb][db] = mma(vr[db][kp], pf[qb][kp], o[qb][db]);
+          for (int qb = 0; qb < QB; ++qb) o[qb][db] = mma(vr[db][kp], pf[qb][kp], o[qb][db]);
+    }
   }
 
   // Normalise and store O rows (query q0 + 16 qb + r) and natural-log LSE.
@@ -391,20 +400,22 @@ struct WaveAttn {
       const bool any = qok && l > 0.f;
       const float inv = any ? 1.0f / l : 0.f;
       const long long row = row0 + 16 * qb + r;
+      if constexpr (!LSE_ONLY) {
 #pragma unroll
-      for (int db = 0; db < DB; ++db) store4(out + row * HD + 16 * db + 4 * j, o[qb][db], inv);
+        for (int db = 0; db < DB; ++db) store4(out + row * HD + 16 * db + 4 * j, o[qb][db], inv);
+      }
       if (j == 0) lse[row] = any ? (mx[qb] + log2f(l)) * kLn2 : kNegInf;
     }
   }
 };
 
-template <typename T, int HD, int QB>
-__device__ __forceinline__ void load_q(WaveAttn<T, HD, QB>& w, const T* qrow0, int lane) {
+template <typename T, int HD, int QB, bool LO>
+__device__ __forceinline__ void load_q(WaveAttn<T, HD, QB, LO>& w, const T* qrow0, int lane) {
   const int r = lane & 15, j = lane >> 4;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-    for (int c = 0; c < WaveAttn<T, HD, QB>::NCH; ++c)
+    for (int c = 0; c < WaveAttn<T, HD, QB, LO>::NCH; ++c)
       w.qf[qb][c] = load_chunk(qrow0 + (size_t)(16 * qb + r) * HD + 32 * c + 8 * j);
 }
 

@@ -23,7 +23,7 @@ namespace {
 
 // Keys are staged 128 at a time (one pair of barriers) and consumed as two 64-key
 // halves; the next 128 keys are loaded into registers while the current ones are used.
-template <typename T, int HD, int QB, bool BALL, typename OT = T>
+template <typename T, int HD, int QB, bool BALL, typename OT = T, bool LO = false>
 __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, const T* v, const uint8_t* qvalid_all,
                                                         const uint8_t* kvalid_all, int H, int N, int nkeys_total,
                                                         int m, float sl2, OT* out, float* lse) {
@@ -45,7 +45,7 @@ __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, 
   const uint8_t* kval = kvalid_all ? kvalid_all + (size_t)b * nkeys_total + key0 : nullptr;
   const uint8_t* qval = qvalid_all ? qvalid_all + (size_t)b * N : nullptr;
 
-  WaveAttn<T, HD, QB> w;
+  WaveAttn<T, HD, QB, LO> w;
   w.init();
   const int wq0 = q0 + wid * 16 * QB;
   load_q(w, q + (bh * N + wq0) * HD, lane);
@@ -91,7 +91,8 @@ __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, 
 // transpose reads of the row-major V tile. The two buffers are distinct LDS objects and
 // the loop is unrolled by two, so the compiler can tell that loads in flight into one
 // buffer do not alias reads of the other and need not be waited for.
-template <int HD, int QB, int NW, bool BALL, typename OT = bf16_t>
+// LO: log-sum-exp rows only (the V tiles are not loaded; no output rows).
+template <int HD, int QB, int NW, bool BALL, typename OT = bf16_t, bool LO = false>
 __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
                                                                 const uint8_t* qvalid_all, const uint8_t* kvalid_all,
                                                                 int H, int N, int nkeys_total, int m, float sl2,
@@ -121,10 +122,10 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q,
       okv = key < nkeys && (kval == nullptr || kval[key]);
     }
     dma_tile<HD, kFT, NW>(kd, kh, t0, nkeys, wid, lane);
-    dma_tile<HD, kFT, NW>(vd, vh, t0, nkeys, wid, lane);
+    if constexpr (!LO) dma_tile<HD, kFT, NW>(vd, vh, t0, nkeys, wid, lane);
     if (threadIdx.x < kFT) okd[threadIdx.x] = okv;
   };
-  WaveAttn<bf16_t, HD, QB> w;
+  WaveAttn<bf16_t, HD, QB, LO> w;
   w.init();
   const int wq0 = q0 + wid * 16 * QB;
   auto step = [&](int t0, const bf16_t* kt, const bf16_t* vt, const uint8_t* ok, bf16_t* kn, bf16_t* vn,
@@ -156,7 +157,7 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q,
 // group's blocks. Keys are walked in tiles of 32 (two 16-key sub-blocks, each inside one
 // selected block since l' is a multiple of 16).
 
-template <typename T, int HD>
+template <typename T, int HD, bool LO = false>
 __global__ void __launch_bounds__(256) slc_fwd_kernel(const T* q, const T* k, const T* v, const uint8_t* valid_all,
                                                       const int* sel, int H, int N, int ls, int kk, int g,
                                                       float sl2, T* out, float* lse) {
@@ -189,7 +190,7 @@ __global__ void __launch_bounds__(256) slc_fwd_kernel(const T* q, const T* k, co
   }
   wave_sync();   // LDS regions are per wave
 
-  WaveAttn<T, HD, 1> w;
+  WaveAttn<T, HD, 1, LO> w;
   w.init();
   load_q(w, q + (bh * N + wq0) * HD, lane);
   vm_drain();
@@ -241,7 +242,8 @@ __global__ void __launch_bounds__(256) slc_fwd_kernel(const T* q, const T* k, co
 // a straight-line body (tiles past the end are loaded from row 0 and masked). Key validity
 // is gathered into 16-bit masks while the sub-block list is built, so no load other than
 // the tile loads runs in the loop.
-template <int HD, int NW>
+// LO: log-sum-exp rows only (the V tiles are not loaded; no output rows).
+template <int HD, int NW, bool LO = false>
 __global__ void __launch_bounds__(NW * 64) slc_fwd_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
                                                               const uint8_t* valid_all, const int* sel, int H, int N,
                                                               int ls, int kk, int g, float sl2, bf16_t* out,
@@ -283,7 +285,7 @@ __global__ void __launch_bounds__(NW * 64) slc_fwd_dma_kernel(const bf16_t* q, c
     }
     okm[e] = m;
   }
-  WaveAttn<bf16_t, HD, 1> w;
+  WaveAttn<bf16_t, HD, 1, LO> w;
   w.init();
   load_q(w, q + (bh * N + wq0) * HD, lane);
   vm_drain();
@@ -297,7 +299,7 @@ __global__ void __launch_bounds__(NW * 64) slc_fwd_dma_kernel(const bf16_t* q, c
       const int row = e >= 0 ? (e & 0xFFFFFF) : 0;
       bf16_t* base = slot + wid * SLOT + kb * 16 * HD;
       dma_tile<HD, 16, 1>(base, kh, row, N, 0, lane);
-      dma_tile<HD, 16, 1>(base + TILE, vh, row, N, 0, lane);
+      if constexpr (!LO) dma_tile<HD, 16, 1>(base + TILE, vh, row, N, 0, lane);
     }
   };
   auto step = [&](int t, const bf16_t* cur, bf16_t* next) {
@@ -329,10 +331,11 @@ __global__ void __launch_bounds__(NW * 64) slc_fwd_dma_kernel(const bf16_t* q, c
 }
 
 // 16 bytes per thread (8 bf16 or 4 f32 channels of one row): one sigmoid per branch and row
-// chunk, vector loads and stores.
+// chunk, vector loads and stores. ob holds the ball and selection rows (storage type), oc
+// the compressed branch's (float32).
 template <typename T>
-__global__ void gate_fwd_vec_kernel(const T* ob, const float* gate, const uint8_t* valid, int H, int N, int hd,
-                                    long long per_branch, T* out) {
+__global__ void gate_fwd_vec_kernel(const T* ob, const float* oc, const float* gate, const uint8_t* valid, int H,
+                                    int N, int hd, long long per_branch, T* out) {
   constexpr int EPV = 16 / (int)sizeof(T);
   const long long v = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long i = v * EPV;
@@ -348,7 +351,18 @@ __global__ void gate_fwd_vec_kernel(const T* ob, const float* gate, const uint8_
 #pragma unroll
     for (int br = 0; br < 3; ++br) {
       const float sg = 1.0f / (1.0f + __expf(-gm[br]));
-      const uint4 u = *reinterpret_cast<const uint4*>(ob + br * per_branch + i);
+      if (br == 1) {
+#pragma unroll
+        for (int e = 0; e < EPV; e += 4) {
+          const float4 f = *reinterpret_cast<const float4*>(oc + i + e);
+          acc[e] += sg * f.x;
+          acc[e + 1] += sg * f.y;
+          acc[e + 2] += sg * f.z;
+          acc[e + 3] += sg * f.w;
+        }
+        continue;
+      }
+      const uint4 u = *reinterpret_cast<const uint4*>(ob + (br / 2) * per_branch + i);
       const T* x = reinterpret_cast<const T*>(&u);
 #pragma unroll
       for (int e = 0; e < EPV; ++e) acc[e] += sg * to_f32<T>(x[e]);
@@ -363,16 +377,28 @@ __global__ void gate_fwd_vec_kernel(const T* ob, const float* gate, const uint8_
 
 // bf16 layers take the direct-load kernel (NW waves of QB 16-query blocks per workgroup);
 // f32 layers the register-staged one (4 waves).
-// OT: type of the output rows (the storage type, or float32 for unrounded outputs)
+// OT: type of the output rows (the storage type, or float32 for unrounded outputs).
+// o == nullptr: log-sum-exp rows only (the same kernel without the value products, so the
+// statistics equal those of the full launch bit for bit).
 template <typename T, int HD, int QB, bool BALL, int NW = 4, typename OT = T>
 void launch_dense_fwd(dim3 grid, hipStream_t st, const void* q, const void* k, const void* v, const uint8_t* qvalid,
                       const uint8_t* kvalid, int H, int N, int nkeys_total, int m, float sl2, void* o, float* lse) {
-  if constexpr (sizeof(T) == 2)
-    hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT>), grid, dim3(64 * NW), 0, st, (const bf16_t*)q,
-                       (const bf16_t*)k, (const bf16_t*)v, qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
-  else
-    hipLaunchKernelGGL((dense_fwd_kernel<T, HD, QB, BALL, OT>), grid, dim3(256), 0, st, (const T*)q, (const T*)k,
-                       (const T*)v, qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
+  if constexpr (sizeof(T) == 2) {
+    if (o)
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT>), grid, dim3(64 * NW), 0, st, (const bf16_t*)q,
+                         (const bf16_t*)k, (const bf16_t*)v, qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
+    else
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, true>), grid, dim3(64 * NW), 0, st,
+                         (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, qvalid, kvalid, H, N, nkeys_total, m,
+                         sl2, (OT*)o, lse);
+  } else {
+    if (o)
+      hipLaunchKernelGGL((dense_fwd_kernel<T, HD, QB, BALL, OT>), grid, dim3(256), 0, st, (const T*)q, (const T*)k,
+                         (const T*)v, qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
+    else
+      hipLaunchKernelGGL((dense_fwd_kernel<T, HD, QB, BALL, OT, true>), grid, dim3(256), 0, st, (const T*)q,
+                         (const T*)k, (const T*)v, qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
+  }
 }
 
 template <typename T, int HD>
@@ -388,16 +414,19 @@ hipError_t ball_impl(const Dims& D, const void* q, const void* k, const void* v,
   return hipGetLastError();
 }
 
+// The compressed branch keeps float32 output rows: the backward's softmax delta
+// rowsum(dO o) is formed from them, and a delta error is shared by every compressed key of
+// the query, so it would add up over the blocks in the MLP weight gradients.
 template <typename T, int HD>
 hipError_t cmp_impl(const Dims& D, const void* q, const void* kc, const void* vc, const uint8_t* valid,
-                    const uint8_t* cvalid, void* o, float* lse, hipStream_t st) {
+                    const uint8_t* cvalid, float* o, float* lse, hipStream_t st) {
   const float sl2 = D.scale * kLog2e;
   if (D.N % 128 == 0)
-    launch_dense_fwd<T, HD, 2, false>(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, valid, cvalid, D.H, D.N, D.N / D.l,
-                                      D.m, sl2, o, lse);
+    launch_dense_fwd<T, HD, 2, false, 4, float>(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, valid, cvalid, D.H, D.N,
+                                                D.N / D.l, D.m, sl2, o, lse);
   else   // 64 token slots: one 64-query workgroup per head
-    launch_dense_fwd<T, HD, 1, false>(dim3(D.N / 64, D.H, D.B), st, q, kc, vc, valid, cvalid, D.H, D.N, D.N / D.l,
-                                      D.m, sl2, o, lse);
+    launch_dense_fwd<T, HD, 1, false, 4, float>(dim3(D.N / 64, D.H, D.B), st, q, kc, vc, valid, cvalid, D.H, D.N,
+                                                D.N / D.l, D.m, sl2, o, lse);
   return hipGetLastError();
 }
 
@@ -418,13 +447,12 @@ hipError_t cmp_coarse_impl(const Dims& D, const void* qc, const void* kc, const 
   return hipGetLastError();
 }
 
-// The copy of Eq. 15: row n of the compression branch takes float32 coarse row n / l (in
-// the storage type) when slot n holds a real token; padding rows get zeros and LSE -inf.
-// One thread per 16 output bytes.
-template <typename T>
+// The copy of Eq. 15: row n of the compression branch takes float32 coarse row n / l when
+// slot n holds a real token; padding rows get zeros and LSE -inf. One thread per 16
+// output bytes; ob == nullptr copies the log-sum-exp rows only.
 __global__ void expand_coarse_kernel(const float* oc, const float* lsec, const uint8_t* valid, int H, int N, int l,
-                                     int hd, long long rows, T* ob, float* lse) {
-  constexpr int EPV = 16 / (int)sizeof(T);
+                                     int hd, long long rows, float* ob, float* lse) {
+  constexpr int EPV = 4;
   const int per_row = hd / EPV;
   const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= rows * per_row) return;
@@ -435,17 +463,13 @@ __global__ void expand_coarse_kernel(const float* oc, const float* lsec, const u
   const int b = (int)(bh / H);
   const bool ok = valid == nullptr || valid[(size_t)b * N + n] != 0;
   const long long crow = bh * (N / l) + n / l;
-  T out[EPV];
-#pragma unroll
-  for (int e = 0; e < EPV; e += 4) {
-    float4 f = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (ok) f = *reinterpret_cast<const float4*>(oc + crow * hd + c * EPV + e);
-    out[e] = from_f32<T>(f.x);
-    out[e + 1] = from_f32<T>(f.y);
-    out[e + 2] = from_f32<T>(f.z);
-    out[e + 3] = from_f32<T>(f.w);
+  if (ob == nullptr) {   // log-sum-exp rows only
+    if (c == 0) lse[row] = ok ? lsec[crow] : kNegInf;
+    return;
   }
-  *reinterpret_cast<uint4*>(ob + row * hd + c * EPV) = *reinterpret_cast<const uint4*>(out);
+  float4 f = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (ok) f = *reinterpret_cast<const float4*>(oc + crow * hd + c * EPV);
+  *reinterpret_cast<float4*>(ob + row * hd + c * EPV) = f;
   if (c == 0) lse[row] = ok ? lsec[crow] : kNegInf;
 }
 
@@ -455,12 +479,21 @@ hipError_t slc_impl(const Dims& D, const void* q, const void* k, const void* v, 
   const float sl2 = D.scale * kLog2e;
   if constexpr (sizeof(T) == 2) {
     constexpr int NW = 2;
-    hipLaunchKernelGGL((slc_fwd_dma_kernel<HD, NW>), dim3(D.N / (16 * NW), D.H, D.B), dim3(64 * NW), 0, st,
-                       (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, valid, sel, D.H, D.N, D.ls, D.k, D.g,
-                       sl2, (bf16_t*)o, lse);
+    if (o)
+      hipLaunchKernelGGL((slc_fwd_dma_kernel<HD, NW>), dim3(D.N / (16 * NW), D.H, D.B), dim3(64 * NW), 0, st,
+                         (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, valid, sel, D.H, D.N, D.ls, D.k, D.g,
+                         sl2, (bf16_t*)o, lse);
+    else
+      hipLaunchKernelGGL((slc_fwd_dma_kernel<HD, NW, true>), dim3(D.N / (16 * NW), D.H, D.B), dim3(64 * NW), 0, st,
+                         (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, valid, sel, D.H, D.N, D.ls, D.k, D.g,
+                         sl2, (bf16_t*)o, lse);
   } else {
-    hipLaunchKernelGGL((slc_fwd_kernel<T, HD>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, (const T*)q,
-                       (const T*)k, (const T*)v, valid, sel, D.H, D.N, D.ls, D.k, D.g, sl2, (T*)o, lse);
+    if (o)
+      hipLaunchKernelGGL((slc_fwd_kernel<T, HD>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, (const T*)q,
+                         (const T*)k, (const T*)v, valid, sel, D.H, D.N, D.ls, D.k, D.g, sl2, (T*)o, lse);
+    else
+      hipLaunchKernelGGL((slc_fwd_kernel<T, HD, true>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, (const T*)q,
+                         (const T*)k, (const T*)v, valid, sel, D.H, D.N, D.ls, D.k, D.g, sl2, (T*)o, lse);
   }
   return hipGetLastError();
 }
@@ -473,7 +506,7 @@ hipError_t launch_ball_fwd(const Dims& D, const void* q, const void* k, const vo
 }
 
 hipError_t launch_cmp_fwd(const Dims& D, const void* q, const void* kc, const void* vc, const uint8_t* valid,
-                          const uint8_t* cvalid, void* o, float* lse, hipStream_t st) {
+                          const uint8_t* cvalid, float* o, float* lse, hipStream_t st) {
   return BSA_DISPATCH(cmp_impl, D, q, kc, vc, valid, cvalid, o, lse, st);
 }
 
@@ -482,17 +515,13 @@ hipError_t launch_cmp_coarse_fwd(const Dims& D, const void* qc, const void* kc, 
   return BSA_DISPATCH(cmp_coarse_impl, D, qc, kc, vc, cvalid, oc, lsec, st);
 }
 
-hipError_t launch_expand_coarse(const Dims& D, const float* oc, const float* lsec, const uint8_t* valid, void* ob,
+hipError_t launch_expand_coarse(const Dims& D, const float* oc, const float* lsec, const uint8_t* valid, float* ob,
                                 float* lse, hipStream_t st) {
   const long long rows = D.rows();
-  const long long per = rows * (D.d * (D.bf16 ? 2 : 4) / 16);
+  const long long per = rows * (D.d / 4);
   const unsigned grid = (unsigned)((per + 255) / 256);
-  if (D.bf16)
-    hipLaunchKernelGGL(expand_coarse_kernel<bf16_t>, dim3(grid), dim3(256), 0, st, oc, lsec, valid,
-                       D.H, D.N, D.l, D.d, rows, (bf16_t*)ob, lse);
-  else
-    hipLaunchKernelGGL(expand_coarse_kernel<float>, dim3(grid), dim3(256), 0, st, oc, lsec, valid,
-                       D.H, D.N, D.l, D.d, rows, (float*)ob, lse);
+  hipLaunchKernelGGL(expand_coarse_kernel, dim3(grid), dim3(256), 0, st, oc, lsec, valid, D.H, D.N, D.l, D.d, rows, ob,
+                     lse);
   return hipGetLastError();
 }
 
@@ -501,15 +530,15 @@ hipError_t launch_slc_fwd(const Dims& D, const void* q, const void* k, const voi
   return BSA_DISPATCH(slc_impl, D, q, k, v, valid, sel, o, lse, st);
 }
 
-hipError_t launch_gate_fwd(const Dims& D, const void* ob, const float* gate, const uint8_t* valid, void* o,
-                           hipStream_t st) {
+hipError_t launch_gate_fwd(const Dims& D, const void* ob, const float* ocmp, const float* gate, const uint8_t* valid,
+                           void* o, hipStream_t st) {
   const long long per = D.rows() * D.d;
   if (D.bf16)
     hipLaunchKernelGGL(gate_fwd_vec_kernel<bf16_t>, dim3((unsigned)((per / 8 + 255) / 256)), dim3(256), 0, st,
-                       (const bf16_t*)ob, gate, valid, D.H, D.N, D.d, per, (bf16_t*)o);
+                       (const bf16_t*)ob, ocmp, gate, valid, D.H, D.N, D.d, per, (bf16_t*)o);
   else
     hipLaunchKernelGGL(gate_fwd_vec_kernel<float>, dim3((unsigned)((per / 4 + 255) / 256)), dim3(256), 0, st,
-                       (const float*)ob, gate, valid, D.H, D.N, D.d, per, (float*)o);
+                       (const float*)ob, ocmp, gate, valid, D.H, D.N, D.d, per, (float*)o);
   return hipGetLastError();
 }
 

@@ -19,6 +19,7 @@ struct Dims {
   int bf16;            // 1 = bf16 storage of Q/K/V/O, 0 = f32
   int qc_mlp;          // coarse queries by the MLP phi_q over blocks of l (Eq. 13)
   int gcmp;            // group compression (Eq. 15)
+  int store_lse;       // 1: the forward keeps the log-sum-exp rows; 0: the backward recomputes them
   float scale;         // softmax scale
   long long rows() const { return (long long)B * H * N; }
   // coarse queries come from blocks of l (Eq. 13), not the group mean computed by the top-k
@@ -53,25 +54,37 @@ hipError_t launch_select_topk(const Dims& D, const void* q, const uint8_t* valid
 // attn_fwd.hip: the three attention branches (Eq. 3, 5, 8) and the gate (Eq. 9)
 hipError_t launch_ball_fwd(const Dims& D, const void* q, const void* k, const void* v, const uint8_t* valid,
                            void* o, float* lse, hipStream_t st);
+// the compressed branch writes float32 rows (its backward forms the softmax delta from them)
 hipError_t launch_cmp_fwd(const Dims& D, const void* q, const void* kc, const void* vc, const uint8_t* valid,
-                          const uint8_t* cvalid, void* o, float* lse, hipStream_t st);
+                          const uint8_t* cvalid, float* o, float* lse, hipStream_t st);
 hipError_t launch_slc_fwd(const Dims& D, const void* q, const void* k, const void* v, const uint8_t* valid,
                           const int* sel, void* o, float* lse, hipStream_t st);
 // group compression (Eq. 15): coarse attention [B, H, N/l, d] (float32 outputs) and its
-// copy to the token rows in the storage type
+// copy to the token rows (float32)
 hipError_t launch_cmp_coarse_fwd(const Dims& D, const void* qc, const void* kc, const void* vc, const uint8_t* cvalid,
                                  float* oc, float* lsec, hipStream_t st);
-hipError_t launch_expand_coarse(const Dims& D, const float* oc, const float* lsec, const uint8_t* valid, void* ob,
+hipError_t launch_expand_coarse(const Dims& D, const float* oc, const float* lsec, const uint8_t* valid, float* ocmp,
                                 float* lse, hipStream_t st);
-hipError_t launch_gate_fwd(const Dims& D, const void* ob, const float* gate, const uint8_t* valid, void* o,
-                           hipStream_t st);
+// ob: ball and selection outputs [2, B, H, N, d] (storage type); ocmp: the compressed
+// branch's [B, H, N, d] float32
+hipError_t launch_gate_fwd(const Dims& D, const void* ob, const float* ocmp, const float* gate, const uint8_t* valid,
+                           void* o, hipStream_t st);
+
+// Buffers of the per-token selection (g = 1, slc_token.hip), block-major.
+struct Slc1Ws {
+  uint32_t *keys, *vals, *keys_tmp, *vals_tmp, *hist;   // (query, slot) pairs and their sort
+  int *seg_start, *seg_end;                             // [B*H*N/l'] pair range of each block
+  float* part;   // [pairs, d] forward: unnormalised partial outputs; backward: dQ parts
+  float* ml;     // [pairs, 2] forward: scaled max and sum of each partial softmax
+};
 
 // Backward pass buffers (inputs, saved tensors, outputs and workspace parts).
 struct BwdArgs {
   const void *q, *k, *v, *dout;
   const uint8_t* valid;
   const float* gate;
-  const void* o_branch;
+  const void* o_branch;          // [2, B, H, N, d] ball and selection outputs (storage type)
+  const float* o_cmp;            // [B, H, N, d] compressed-branch output (float32)
   const float *lse, *kcmp, *vcmp, *hid_k, *hid_v;
   const int* sel;
   const uint8_t* cvalid;
@@ -92,6 +105,10 @@ struct BwdArgs {
   float* dqc;                    // [B, H, N/l, d] gradient of the coarse queries
   int *seg_start, *seg_end;
   const uint32_t* pair_groups;   // set internally: sorted group ids
+  // store_lse = 0: the log-sum-exp rows are recomputed into lse_ws before the first pass
+  float* lse_ws;                 // [3, B, H, N]
+  float* lsec_ws;                // [B, H, N/l] coarse rows (group compression)
+  Slc1Ws s1;                     // per-token selection buffers (g = 1; ml holds 2 floats per pair)
 };
 
 // attn_bwd.hip
@@ -116,13 +133,6 @@ hipError_t launch_compress_bwd(const Dims& D, const void* x, const uint8_t* vali
                                const float* dy, float* dx_accum, const MlpGrad& grad, const MlpBwdWs& ws,
                                hipStream_t st);
 
-// slc_token.hip: selection attention with per-token selection (g = 1), block-major.
-struct Slc1Ws {
-  uint32_t *keys, *vals, *keys_tmp, *vals_tmp, *hist;   // (query, slot) pairs and their sort
-  int *seg_start, *seg_end;                             // [B*H*N/l'] pair range of each block
-  float* part;   // [pairs, d] forward: unnormalised partial outputs; backward: dQ parts
-  float* ml;     // [pairs, 2] forward: scaled max and sum of each partial softmax
-};
 size_t slc1_pairs(const Dims& D);
 hipError_t launch_slc1_csr(const Dims& D, const int* sel, const uint8_t* valid, const Slc1Ws& W, uint32_t** vals_out,
                            hipStream_t st);

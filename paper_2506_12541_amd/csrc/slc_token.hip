@@ -78,8 +78,9 @@ __global__ void seg_bounds1_kernel(const uint32_t* keys, long long total, uint32
 // ---- forward: partial softmax states of every (query, block) pair ----
 // S^T = K Q^T puts one query per accumulator column (lane % 16) and the block's keys on
 // the rows, so the softmax reductions run over a lane's rows and its column's four lane
-// groups, and P^T is already the B operand of O^T = V^T P^T.
-template <int HD, int KBW>
+// groups, and P^T is already the B operand of O^T = V^T P^T. LO: the softmax states only
+// (no V operand, no partial outputs), formed exactly as in the full launch.
+template <int HD, int KBW, bool LO = false>
 __global__ void __launch_bounds__(256) slc1_fwd_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
                                                        const uint8_t* valid_all, const uint32_t* vals,
                                                        const int* seg_start, const int* seg_end, int H, int N,
@@ -108,8 +109,10 @@ __global__ void __launch_bounds__(256) slc1_fwd_kernel(const bf16_t* q, const bf
   for (int kb = 0; kb < KBW; ++kb) {
 #pragma unroll
     for (int c = 0; c < NCH; ++c) kf[kb][c] = load_chunk(kh + (size_t)(16 * kb + r) * HD + 32 * c + 8 * j);
+    if constexpr (!LO) {
 #pragma unroll
-    for (int db = 0; db < DB; ++db) vt[kb][db] = gather_col4<HD>(vh, 16 * kb + 4 * j, 16 * db + r);
+      for (int db = 0; db < DB; ++db) vt[kb][db] = gather_col4<HD>(vh, 16 * kb + 4 * j, 16 * db + r);
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) kok[kb][i] = val == nullptr || val[16 * kb + 4 * j + i] != 0;
   }
@@ -160,23 +163,28 @@ __global__ void __launch_bounds__(256) slc1_fwd_kernel(const bf16_t* q, const bf
         pr[i] = fast_exp2(st[kb][i] - mref);   // masked keys: exp2(-inf) = 0
         l += pr[i];
       }
+      if constexpr (!LO) {
 #pragma unroll
-      for (int db = 0; db < DB; ++db) o[db] = mma16bf(vt[kb][db], pr, o[db]);
+        for (int db = 0; db < DB; ++db) o[db] = mma16bf(vt[kb][db], pr, o[db]);
+      }
     }
     l = col_sum(l);
     if (pv != 0xFFFFFFFFu) {
       const size_t pair = ((size_t)bh * N) * kk + pv;   // ((b*H + h) * N + p) * k* + slot
-      float* op = opart + pair * HD;
+      if constexpr (!LO) {
+        float* op = opart + pair * HD;
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
-        *reinterpret_cast<float4*>(op + 16 * db + 4 * j) = make_float4(o[db][0], o[db][1], o[db][2], o[db][3]);
+        for (int db = 0; db < DB; ++db)
+          *reinterpret_cast<float4*>(op + 16 * db + 4 * j) = make_float4(o[db][0], o[db][1], o[db][2], o[db][3]);
+      }
       if (j == 0) mlpart[pair] = make_float2(mx, l);
     }
   }
 }
 
 // Output row and LSE of each query from its k* partial states (slot order); padding rows
-// and rows without any eligible key get zeros and LSE -inf. One thread per 4 columns.
+// and rows without any eligible key get zeros and LSE -inf. One thread per 4 columns;
+// out == nullptr: the LSE only (one thread per row does the work).
 template <typename T, int HD>
 __global__ void slc1_merge_kernel(const float* opart, const float2* mlpart, const int* sel, const uint8_t* valid,
                                   int H, int N, int kk, long long rows, T* out, float* lse) {
@@ -190,6 +198,7 @@ __global__ void slc1_merge_kernel(const float* opart, const float2* mlpart, cons
   const int b = (int)(bh / H);
   const bool ok = valid == nullptr || valid[(size_t)b * N + n] != 0;
   const int* srow = sel + row * kk;
+  if (out == nullptr && c != 0) return;
   float M = kNegInf;
   if (ok)
     for (int s = 0; s < kk; ++s)
@@ -206,6 +215,7 @@ __global__ void slc1_merge_kernel(const float* opart, const float2* mlpart, cons
         if (ml.y > 0.f) {
           const float w = exp2f(ml.x - M);
           L += w * ml.y;
+          if (out == nullptr) continue;
           const float4 op = *reinterpret_cast<const float4*>(opart + (row * kk + s) * HD + 4 * c);
           acc.x += w * op.x;
           acc.y += w * op.y;
@@ -213,13 +223,14 @@ __global__ void slc1_merge_kernel(const float* opart, const float2* mlpart, cons
           acc.w += w * op.w;
         }
       }
+  if (c == 0) lse[row] = L > 0.f ? (M + log2f(L)) * kLn2 : kNegInf;
+  if (out == nullptr) return;
   const float inv = L > 0.f ? 1.0f / L : 0.f;
   T* po = out + row * HD + 4 * c;
   po[0] = from_f32<T>(acc.x * inv);
   po[1] = from_f32<T>(acc.y * inv);
   po[2] = from_f32<T>(acc.z * inv);
   po[3] = from_f32<T>(acc.w * inv);
-  if (c == 0) lse[row] = L > 0.f ? (M + log2f(L)) * kLn2 : kNegInf;
 }
 
 // ---- backward: dK, dV of the block and each pair's dQ part ----
@@ -441,9 +452,13 @@ __global__ void slc1_merge_dq_kernel(const float* dqpart, const int* sel, const 
 
 template <int HD, int KBW>
 void fwd_launch(const Dims& D, const bf16_t* q, const bf16_t* k, const bf16_t* v, const uint8_t* valid,
-                const uint32_t* vals, const Slc1Ws& W, long long nseg, float sl2, hipStream_t st) {
-  hipLaunchKernelGGL((slc1_fwd_kernel<HD, KBW>), dim3((unsigned)nseg), dim3(256), 0, st, q, k, v, valid, vals,
-                     W.seg_start, W.seg_end, D.H, D.N, D.ls, D.k, sl2, W.part, (float2*)W.ml);
+                const uint32_t* vals, const Slc1Ws& W, long long nseg, float sl2, bool lse_only, hipStream_t st) {
+  if (lse_only)
+    hipLaunchKernelGGL((slc1_fwd_kernel<HD, KBW, true>), dim3((unsigned)nseg), dim3(256), 0, st, q, k, v, valid,
+                       vals, W.seg_start, W.seg_end, D.H, D.N, D.ls, D.k, sl2, W.part, (float2*)W.ml);
+  else
+    hipLaunchKernelGGL((slc1_fwd_kernel<HD, KBW>), dim3((unsigned)nseg), dim3(256), 0, st, q, k, v, valid, vals,
+                       W.seg_start, W.seg_end, D.H, D.N, D.ls, D.k, sl2, W.part, (float2*)W.ml);
 }
 
 template <int HD, int KBW>
@@ -490,13 +505,13 @@ hipError_t launch_slc1_fwd(const Dims& D, const void* q, const void* k, const vo
   const bf16_t *qq = (const bf16_t*)q, *kk = (const bf16_t*)k, *vv = (const bf16_t*)v;
   const int kbw = D.ls / 16;
   if (D.d == 64) {
-    if (kbw == 1) fwd_launch<64, 1>(D, qq, kk, vv, valid, vals, W, nseg, sl2, st);
-    else if (kbw == 2) fwd_launch<64, 2>(D, qq, kk, vv, valid, vals, W, nseg, sl2, st);
-    else fwd_launch<64, 4>(D, qq, kk, vv, valid, vals, W, nseg, sl2, st);
+    if (kbw == 1) fwd_launch<64, 1>(D, qq, kk, vv, valid, vals, W, nseg, sl2, o == nullptr, st);
+    else if (kbw == 2) fwd_launch<64, 2>(D, qq, kk, vv, valid, vals, W, nseg, sl2, o == nullptr, st);
+    else fwd_launch<64, 4>(D, qq, kk, vv, valid, vals, W, nseg, sl2, o == nullptr, st);
   } else {
-    if (kbw == 1) fwd_launch<32, 1>(D, qq, kk, vv, valid, vals, W, nseg, sl2, st);
-    else if (kbw == 2) fwd_launch<32, 2>(D, qq, kk, vv, valid, vals, W, nseg, sl2, st);
-    else fwd_launch<32, 4>(D, qq, kk, vv, valid, vals, W, nseg, sl2, st);
+    if (kbw == 1) fwd_launch<32, 1>(D, qq, kk, vv, valid, vals, W, nseg, sl2, o == nullptr, st);
+    else if (kbw == 2) fwd_launch<32, 2>(D, qq, kk, vv, valid, vals, W, nseg, sl2, o == nullptr, st);
+    else fwd_launch<32, 4>(D, qq, kk, vv, valid, vals, W, nseg, sl2, o == nullptr, st);
   }
   const long long rows = D.rows();
   const long long nt = rows * (D.d / 4);

@@ -57,7 +57,8 @@ def gpu_forward(cfg, inp, valid, **pkw):
     o, saved = gb.forward(p, q, k, v, vd, gate, phi_k, phi_v, phi_q=phi_q)
     torch.cuda.synchronize()
     f = lambda t: t.float().cpu().numpy()
-    return {"o": f(o), "o_branch": f(saved.o_branch), "lse": saved.lse.cpu().numpy(),
+    lse = saved.lse.cpu().numpy() if saved.lse is not None else None
+    return {"o": f(o), "o_branch": f(saved.branch_outputs()), "lse": lse,
             "sel": saved.sel_idx.cpu().numpy().astype(np.int64), "kc": saved.kcmp.cpu().numpy(),
             "vc": saved.vcmp.cpu().numpy(), "qc": saved.qcmp.cpu().numpy()}, \
         (p, q, k, v, vd, gate, phi_k, phi_v, saved, o, phi_q)

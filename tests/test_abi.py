@@ -64,7 +64,7 @@ def test_valid_params(lib):
     (dict(group_size=1, dtype=_lib.BSA_F32), _lib.BSA_ERR_UNSUPPORTED),   # per token: bf16 only
     (dict(topk=0), _lib.BSA_ERR_UNSUPPORTED),
     (dict(topk=17), _lib.BSA_ERR_UNSUPPORTED),
-    (dict(store_lse=0), _lib.BSA_ERR_UNSUPPORTED),
+    (dict(store_lse=2), _lib.BSA_ERR_INVALID_ARGUMENT),
     (dict(dtype=7), _lib.BSA_ERR_INVALID_ARGUMENT),
     (dict(softmax_scale=-1.0), _lib.BSA_ERR_INVALID_ARGUMENT),
     (dict(q_coarsen=2), _lib.BSA_ERR_INVALID_ARGUMENT),
@@ -114,7 +114,8 @@ def test_variant_forward_needs_phi_q(lib):
     cp = p.c()
     saved = _lib.bsa_saved_t()
     fake = C.c_void_p(256)
-    for f in ("sel_idx", "lse", "o_branch", "kcmp", "vcmp", "hid_k", "hid_v", "cvalid", "qcmp", "hid_q", "ocmp"):
+    for f in ("sel_idx", "lse", "o_branch", "kcmp", "vcmp", "hid_k", "hid_v", "cvalid", "qcmp", "hid_q", "ocmp",
+              "o_cmp"):
         setattr(saved, f, 256)
     m = _lib.bsa_mlp_t(256, 256, 256, 256)
     # phi_q missing: rejected on the host before any launch

@@ -187,3 +187,75 @@ def test_finite_differences(P):
     if P.group_compression:
         check(lambda m: m["phi_q"]["w1"], grads["dphi_q"]["w1"], inp["phi_q"]["w1"])
         check(lambda m: m["phi_q"]["b2"], grads["dphi_q"]["b2"], inp["phi_q"]["b2"])
+
+
+def test_summed_gradient_bars_reject_planted_mistakes():
+    """The summed-gradient bar of the GPU tests (tests/bars.py) on the airflow backward
+    workload's generator and shapes (2 of its 16 clouds): the oracle's own gradients and
+    bf16-sized noise pass; a zeroed or sign-flipped key-MLP gradient (b1, w2), a 6% error
+    on the largest entry of w1 and a zeroed gate gradient each fail; the identically zero
+    output bias of the key MLP is recognised as such."""
+    import dataclasses
+
+    from bars import check_summed, oracle_summed, summed_error, summed_ok
+    from oracle.tree import build_ball_tree
+    from workloads import CONFIGS, make_inputs, make_points
+
+    cfg = dataclasses.replace(CONFIGS[5], batch=2)
+    inp = make_inputs(cfg, 5, layout="ball", with_grad=True)
+    pts = make_points(cfg, 5)
+    valid = np.stack([build_ball_tree(pts[b], cfg.n_pad) >= 0 for b in range(cfg.batch)])
+    P = Params(ball=cfg.ball, cmp_block=cfg.cmp_block, slc_block=cfg.slc_block, topk=cfg.topk, group=cfg.group)
+    fwd = bsa.forward(inp["q"], inp["k"], inp["v"], valid, inp["gate"], inp["phi_k"], inp["phi_v"], P)
+    ref = bsa.backward(inp["q"], inp["k"], inp["v"], valid, inp["gate"], inp["phi_k"], inp["phi_v"], P, fwd,
+                       inp["do"])
+    flat = oracle_summed(ref)
+    tol = 2e-2
+    names = [n for n in flat if n != "abs"]
+    res = check_summed({n: flat[n] for n in names}, flat, tol)
+    assert res["dphi_k.b2"][0] == "cancel" and all(res[n][0] == "rel" for n in names if n != "dphi_k.b2")
+    rng = np.random.default_rng(0)
+    noisy = {n: flat[n] + 2e-3 * np.abs(flat[n]).max() * rng.standard_normal(flat[n].shape) for n in names}
+    check_summed(noisy, flat, tol)
+
+    def fails(name, value):
+        kind, err = summed_error(name, value, flat[name], flat["abs"][name])
+        return not summed_ok(kind, err, tol)
+
+    for name in ("dphi_k.b1", "dphi_k.w2", "dgate"):
+        assert fails(name, np.zeros_like(flat[name])), name
+        assert fails(name, -flat[name]), name
+    w1 = flat["dphi_k.w1"].copy()
+    i = np.unravel_index(np.argmax(np.abs(w1)), w1.shape)
+    w1[i] *= 1.06
+    assert fails("dphi_k.w1", w1)
+
+
+def test_rounded_compressed_output_biases_mlp_gradients():
+    """Why the compressed branch's output is kept in float32: at the airflow backward
+    workload's shapes (2 clouds), rounding that output to bf16 before the backward (so its
+    softmax delta rowsum(dO o) carries the rounding) moves the key MLP's b1 gradient by
+    several percent of its largest entry, beyond the 2e-2 bar; rounding the ball or the
+    selection output leaves the MLP gradients unchanged."""
+    import dataclasses
+
+    from oracle.tree import build_ball_tree
+    from workloads import CONFIGS, make_inputs, make_points, round_bf16
+
+    cfg = dataclasses.replace(CONFIGS[5], batch=2)
+    inp = make_inputs(cfg, 5, layout="ball", with_grad=True)
+    pts = make_points(cfg, 5)
+    valid = np.stack([build_ball_tree(pts[b], cfg.n_pad) >= 0 for b in range(cfg.batch)])
+    P = Params(ball=cfg.ball, cmp_block=cfg.cmp_block, slc_block=cfg.slc_block, topk=cfg.topk, group=cfg.group)
+    args = (inp["q"], inp["k"], inp["v"], valid, inp["gate"], inp["phi_k"], inp["phi_v"], P)
+    fwd = bsa.forward(*args)
+    ref = bsa.backward(*args, fwd, inp["do"])
+    err = {}
+    for br in range(3):
+        f2 = dict(fwd)
+        f2["o_branch"] = fwd["o_branch"].copy()
+        f2["o_branch"][br] = round_bf16(fwd["o_branch"][br].astype(np.float32))
+        r2 = bsa.backward(*args, f2, inp["do"])
+        err[br] = float(np.abs(r2["dphi_k"]["b1"] - ref["dphi_k"]["b1"]).max() / np.abs(ref["dphi_k"]["b1"]).max())
+    assert err[1] > 2e-2, err
+    assert err[0] == 0.0 and err[2] == 0.0, err
