@@ -137,6 +137,20 @@ bsa_status_t bsa_build_ball_tree(const float* points, int64_t n_real, int32_t di
                                  int64_t n_pad, int32_t batch, int32_t* perm,
                                  void* ws, size_t ws_bytes, void* stream);
 
+/* bsa_build_ball_tree without a workspace argument and without any device allocation, for
+ * callers that cannot allocate (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Same arguments, ordering and errors as
+ * bsa_build_ball_tree, minus ws / ws_bytes. The workspace is a static device array of the
+ * library (10.7 MB on each device the library runs on, held until the process
+ * ends) that covers batch * n_pad <= 131072 slots; larger sizes return
+ * BSA_ERR_UNSUPPORTED and launch nothing. Every call on one device shares that array and
+ * overwrites it: calls that overlap in time on one device (e.g. on two streams without
+ * ordering between them) race and give wrong orderings; calls ordered on one stream are
+ * safe. Nothing in the array needs clearing between calls (every word is written before
+ * it is read). */
+bsa_status_t bsa_build_ball_tree_noalloc(const float* points, int64_t n_real, int32_t dim, int64_t n_pad,
+                                         int32_t batch, int32_t* perm, void* stream);
+
 /* Gather per-point rows into ball order (the ordering step before Eq. 3):
  *   src  [batch, n_real, heads*head_dim] (dtype) -> dst [batch, heads, n_pad, head_dim],
  *   dst row = 0 where perm is -1. valid_out [batch, n_pad] (may be NULL) receives

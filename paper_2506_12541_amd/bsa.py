@@ -14,7 +14,7 @@ import torch
 from . import _lib
 from ._lib import BSA_BF16, BSA_F32, BSA_POOL_MEAN, BSA_POOL_MLP, BSA_QC_MEAN, BSA_QC_MLP, check
 
-__all__ = ["Params", "Saved", "build_ball_tree", "permute", "unpermute", "sizes", "forward", "backward",
+__all__ = ["Params", "Saved", "build_ball_tree", "build_ball_tree_noalloc", "permute", "unpermute", "sizes", "forward", "backward",
            "block_sizes", "BlockSaved", "block_forward", "block_backward", "BLOCK_WEIGHTS",
            "BSA_F32", "BSA_BF16", "BSA_POOL_MLP", "BSA_POOL_MEAN", "BSA_QC_MEAN", "BSA_QC_MLP"]
 
@@ -90,6 +90,20 @@ def build_ball_tree(points: torch.Tensor, n_pad: int, stream=None) -> torch.Tens
     perm = torch.empty((B, n_pad), dtype=torch.int32, device=points.device)
     check(lib.bsa_build_ball_tree(_ptr(points), n_real, dim, n_pad, B, _ptr(perm), _ptr(ws), ws_bytes,
                                   _stream(stream)), "bsa_build_ball_tree")
+    return perm
+
+
+def build_ball_tree_noalloc(points: torch.Tensor, perm: torch.Tensor, stream=None) -> torch.Tensor:
+    """bsa_build_ball_tree_noalloc: fills the caller's perm [B, n_pad] int32 from clouds
+    [B, n_real, dim] f32 using the library's static scratch (no workspace, no allocation)."""
+    lib = _lib.load()
+    _require(points, "points", torch.float32)
+    _require(perm, "perm", torch.int32)
+    B, n_real, dim = points.shape
+    if perm.dim() != 2 or perm.shape[0] != B:
+        raise ValueError("perm must be [B, n_pad]")
+    check(lib.bsa_build_ball_tree_noalloc(_ptr(points), n_real, dim, perm.shape[1], B, _ptr(perm), _stream(stream)),
+          "bsa_build_ball_tree_noalloc")
     return perm
 
 

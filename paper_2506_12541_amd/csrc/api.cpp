@@ -300,6 +300,30 @@ bsa_status_t bsa_build_ball_tree(const float* points, int64_t n_real, int32_t di
   return BSA_OK;
 }
 
+bsa_status_t bsa_build_ball_tree_noalloc(const float* points, int64_t n_real, int32_t dim, int64_t n_pad,
+                                         int32_t batch, int32_t* perm, void* stream) {
+  g_last_error.clear();
+  if (!points || !perm) return fail(BSA_ERR_INVALID_ARGUMENT, "points and perm must be non-NULL");
+  if (dim < 1 || dim > 3) return fail(BSA_ERR_UNSUPPORTED, "dim must be 1, 2 or 3");
+  if (batch < 1) return fail(BSA_ERR_INVALID_ARGUMENT, "batch must be >= 1");
+  if (!pow2(n_pad) || n_pad > (1 << 24)) return fail(BSA_ERR_INVALID_ARGUMENT, "n_pad must be a power of two <= 2^24");
+  if (n_real < 1 || n_real > n_pad) return fail(BSA_ERR_INVALID_ARGUMENT, "need 1 <= n_real <= n_pad");
+  if ((int64_t)batch * n_pad > bsa::tree_scratch_slots())
+    return fail(BSA_ERR_UNSUPPORTED, "batch * n_pad = " + std::to_string((int64_t)batch * n_pad) +
+                                         " exceeds the allocation-free tree build's limit of " +
+                                         std::to_string(bsa::tree_scratch_slots()) +
+                                         " slots; use bsa_build_ball_tree with a workspace");
+  if (bsa_ball_tree_workspace_bytes(n_real, n_pad, dim, batch) > bsa::tree_scratch_bytes())
+    return fail(BSA_ERR_UNSUPPORTED, "tree workspace exceeds the static scratch");
+  void* scratch = nullptr;
+  BSA_TRY(bsa::tree_scratch(&scratch), "bsa_build_ball_tree_noalloc (scratch address)");
+  hipError_t e;
+  BSA_PHASE("tree", (hipStream_t)stream,
+            e = bsa::launch_build_tree(points, n_real, dim, n_pad, batch, perm, scratch, (hipStream_t)stream));
+  BSA_TRY(e, "bsa_build_ball_tree_noalloc");
+  return BSA_OK;
+}
+
 static bsa_status_t permute_common(const void* src, const int32_t* perm, int64_t n_real, int64_t n_pad, int32_t batch,
                                    int32_t heads, int32_t head_dim, int32_t dtype, void* dst) {
   if (!src || !perm || !dst) return fail(BSA_ERR_INVALID_ARGUMENT, "src, perm and dst must be non-NULL");

@@ -32,6 +32,11 @@ struct MlpGrad { float *w1, *b1, *w2, *b2; };
 
 // tree.hip
 size_t tree_workspace_bytes(int64_t n_real, int64_t n_pad, int batch);
+// The allocation-free tree build's static scratch: its slot limit (batch * n_pad), its size,
+// and its address on the current device (looked up once per device).
+int64_t tree_scratch_slots();
+size_t tree_scratch_bytes();
+hipError_t tree_scratch(void** ptr);
 hipError_t launch_build_tree(const float* pts, int64_t n_real, int dim, int64_t n_pad, int batch,
                              int* perm, void* ws, hipStream_t st);
 hipError_t launch_permute(const void* src, const int* perm, int64_t n_real, int64_t n_pad, int batch,

@@ -15,6 +15,9 @@
 // all three lists sorted in both children. Levels with nodes larger than 1024 slots run
 // as three small kernels per level over all nodes; the last ten levels run inside one
 // workgroup per 1024-slot node, entirely in LDS.
+#include <map>
+#include <mutex>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -513,23 +516,57 @@ inline int ilog2(int64_t x) {
 
 }  // namespace
 
-size_t tree_workspace_bytes(int64_t n_real, int64_t n_pad, int batch) {
-  const size_t m = (size_t)batch * n_real;
-  const size_t slots = (size_t)batch * n_pad;
+namespace {
+
+constexpr size_t align256c(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Workspace bytes of the tree build over m real points in `slots` slots (all clouds); the
+// carve-up in launch_build_tree follows the same order.
+constexpr size_t tree_ws_bytes(size_t m, size_t slots) {
   const size_t ntiles = (m + kSortTile - 1) / kSortTile;
-  size_t b = 0;
-  auto add = [&](size_t x) { b += (x + 255) & ~size_t(255); };
-  add(4 * 3 * m);          // keys a
-  add(4 * 3 * m);          // keys b
-  add(4 * 3 * m);          // vals a
-  add(4 * 3 * m);          // vals b
-  add(4 * 3 * (size_t)kRadix * ntiles);   // digit counts
-  add(4 * 3 * ((kRadix * ntiles + kScanChunk - 1) / kScanChunk));   // chunk totals
-  add(4 * 3 * slots);      // lists a
-  add(4 * 3 * slots);      // lists b
-  add(sizeof(NodeSplit) * (slots / 2 + 1));
-  add(4 * 3 * (slots / kPartTile + 1));
-  return b;
+  return 4 * align256c(4 * 3 * m)                                            // keys and values, twice
+         + align256c(4 * 3 * (size_t)kRadix * ntiles)                        // digit counts
+         + align256c(4 * 3 * ((kRadix * ntiles + kScanChunk - 1) / kScanChunk))   // chunk totals
+         + 2 * align256c(4 * 3 * slots)                                      // node lists, twice
+         + align256c(sizeof(NodeSplit) * (slots / 2 + 1))
+         + align256c(4 * 3 * (slots / kPartTile + 1));
+}
+
+// Scratch of the allocation-free tree build (bsa_build_ball_tree_noalloc): the workspace
+// of up to kTreeScratchSlots slots, as one file-scope device array. Every term of
+// tree_ws_bytes grows with m <= slots, so m = slots = the limit bounds every call. Each
+// device holds its own copy; host code reaches it only through the address that
+// hipGetSymbolAddress returns for the current device.
+constexpr int64_t kTreeScratchSlots = int64_t(1) << 17;
+constexpr size_t kTreeScratchBytes = tree_ws_bytes(kTreeScratchSlots, kTreeScratchSlots);
+static __device__ __align__(256) unsigned char scratch[kTreeScratchBytes];
+
+std::mutex g_scratch_mu;
+std::map<int, void*> g_scratch_ptr;   // device -> address of its scratch array
+
+}  // namespace
+
+size_t tree_workspace_bytes(int64_t n_real, int64_t n_pad, int batch) {
+  return tree_ws_bytes((size_t)batch * n_real, (size_t)batch * n_pad);
+}
+
+int64_t tree_scratch_slots() { return kTreeScratchSlots; }
+size_t tree_scratch_bytes() { return kTreeScratchBytes; }
+
+hipError_t tree_scratch(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  auto it = g_scratch_ptr.find(dev);
+  if (it == g_scratch_ptr.end()) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));   // the current device's copy
+    if (e != hipSuccess) return e;
+    it = g_scratch_ptr.emplace(dev, p).first;
+  }
+  *ptr = it->second;
+  return hipSuccess;
 }
 
 hipError_t launch_build_tree(const float* pts, int64_t n_real, int dim, int64_t n_pad, int batch,
