@@ -87,10 +87,101 @@ def phase_flops(cfg, variant="bsa"):
     return f
 
 
+def phase_bytes(cfg, variant="bsa"):
+    """Compulsory HBM bytes of each timed phase: every tensor the phase must read or write
+    once (bf16 storage, float32 gradients and compressed-branch output, 16 bytes of packed
+    row terms per query row and branch in the backward). Intermediate partial sums and the
+    re-reads that tiling causes are not counted: they are what the counters measure on top.
+    The selection phases count K and V once (every block is selected by some group)."""
+    B, H, N, d = cfg.batch, cfg.heads, cfg.n_pad, cfg.head_dim
+    l, ls, k, g = cfg.cmp_block, cfg.slc_block, cfg.topk, cfg.group
+    e = 2 if cfg.dtype == "bf16" else 4
+    R = B * H * N                 # token rows
+    Rc = B * H * (N // l)         # compressed rows
+    Rg = B * H * (N // g)         # query groups
+    gc = variant == "group_cmp"
+    Rq = Rc if gc else R          # query rows of the compressed branch
+    x = R * d * e                 # one token tensor in the storage type
+    xc = Rc * d * e
+    sel = Rg * k * 4
+    return {
+        "tree": B * N * (3 * 4 + 4),
+        "permute": 3 * 2 * x + 2 * B * N * 3 * 4,
+        "fwd.compress": (3 if gc else 2) * (x + Rc * d * (4 + 4 + e)),
+        "fwd.select": x + 3 * 2 * Rc * d + sel,
+        "fwd.ball": 4 * x + 4 * R,
+        "fwd.cmp": Rq * d * e + 2 * xc + R * d * 4 + 4 * R,
+        "fwd.slc": 4 * x + sel + 4 * R,
+        "fwd.gate": 2 * x + R * d * 4 + x + B * N * 12,
+        "bwd.gate": x + 2 * x + R * d * 4 + 4 * 3 * R + 3 * 16 * R,
+        "bwd.kv_ball": 4 * x + 16 * R + 2 * R * d * 4,
+        "bwd.dq_ball": 4 * x + 16 * R + R * d * 4,
+        "bwd.kv_cmp": 2 * Rq * d * e + 2 * xc + 16 * Rq + 2 * Rc * d * 4,
+        "bwd.dq_cmp": 2 * Rq * d * e + 2 * xc + 16 * Rq + 2 * Rq * d * 4,
+        "bwd.dq_slc": 4 * x + sel + 16 * R + 2 * R * d * 4,
+        "bwd.slc_kv": 4 * x + sel + 16 * R + 4 * R * d * 4,
+        "bwd.slc_csr": 4 * sel,
+        "bwd.mlp": (3 if gc else 2) * (2 * x + 2 * R * d * 4 + 3 * Rc * d * 4),
+    }
+
+
+# the phases of each attention branch, forward and backward
+BRANCH_PHASES = {"ball": ("fwd.ball", "bwd.kv_ball", "bwd.dq_ball"),
+                 "cmp": ("fwd.cmp", "bwd.kv_cmp", "bwd.dq_cmp"),
+                 "slc": ("fwd.slc", "bwd.slc_csr", "bwd.slc_kv", "bwd.dq_slc")}
+
+
+def gathered_bytes(cfg):
+    """Selection K/V bytes gathered per pass if no gather hits a cache: every group reads
+    its k* blocks of l' keys and values."""
+    B, H, N, d = cfg.batch, cfg.heads, cfg.n_pad, cfg.head_dim
+    e = 2 if cfg.dtype == "bf16" else 4
+    return B * H * (N // cfg.group) * cfg.topk * cfg.slc_block * d * e * 2
+
+
+def rooflines(cfg, variant, ms):
+    """Per phase and per branch: algorithmic TFLOP/s, fraction of the bf16 MFMA peak, and
+    fraction of the attainable roofline min(peak, I * HBM) at the phase's compulsory
+    intensity I (FLOP per byte)."""
+    pf, pb = phase_flops(cfg, variant), phase_bytes(cfg, variant)
+    out = {}
+    for n, t in ms.items():
+        if n not in pf or t <= 0:
+            continue
+        inten = pf[n] / pb[n]
+        att = min(MFMA_BF16_PEAK, inten * HBM_PEAK)
+        ach = pf[n] / (t * 1e-3)
+        out[n] = {"tflops": round(ach / 1e12, 1), "frac_peak": round(ach / MFMA_BF16_PEAK, 4),
+                  "flop_per_byte": round(inten, 1), "attainable_tflops": round(att / 1e12, 1),
+                  "frac_attainable": round(ach / att, 4), "bound": "mfma" if att >= MFMA_BF16_PEAK else "hbm",
+                  "hbm_gbps_compulsory": round(pb[n] / (t * 1e-3) / 1e9, 1)}
+    branches = {}
+    for br, names in BRANCH_PHASES.items():
+        if not all(n in ms for n in names):
+            continue
+        t = sum(ms[n] for n in names)
+        f = sum(pf.get(n, 0.0) for n in names)
+        byt = sum(pb[n] for n in names)
+        att = min(MFMA_BF16_PEAK, f / byt * HBM_PEAK)
+        ach = f / (t * 1e-3)
+        branches[br] = {"ms": round(t, 4), "tflops": round(ach / 1e12, 1), "frac_peak": round(ach / MFMA_BF16_PEAK, 4),
+                        "flop_per_byte": round(f / byt, 1), "attainable_tflops": round(att / 1e12, 1),
+                        "frac_attainable": round(ach / att, 4)}
+    if "slc" in branches:
+        # the selection's gathers: g FLOP per gathered byte if every gather came from HBM
+        gb = gathered_bytes(cfg)
+        fs = pf["fwd.slc"]
+        branches["slc"]["fwd_gathered_gb"] = round(gb / 1e9, 2)
+        branches["slc"]["fwd_gather_tbps"] = round(gb / (ms["fwd.slc"] * 1e-3) / 1e12, 2)
+        branches["slc"]["fwd_attainable_tflops_hbm_gathers"] = round(fs / gb * HBM_PEAK / 1e12, 1)
+    return out, branches
+
+
 # single-launch phases whose work is a dense bf16 contraction (roofline candidates)
 PHASES = ("tree", "permute", "fwd.compress", "fwd.select", "fwd.ball", "fwd.cmp", "fwd.slc", "fwd.gate", "bwd.gate",
           "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc", "bwd.kv_ball", "bwd.kv_cmp", "bwd.mlp", "bwd.slc_csr", "bwd.slc_kv")
-PHASE_STEPS = 5   # steps of the phase-breakdown pass (run before the timed region)
+PHASE_STEPS = 5   # steps of each phase-breakdown pass (run before the timed region)
+FLUSH_BYTES = 512 << 20   # written before each cold step: twice the MALL
 MFMA_PHASES = ("fwd.ball", "fwd.cmp", "fwd.slc", "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc", "bwd.kv_ball",
                "bwd.kv_cmp")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_{phase}_{workload}.txt")
@@ -187,6 +278,118 @@ def summarize_traffic(args):
     print(open(out).read())
 
 
+SQ_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CU_CYCLES", "SQ_INSTS_VALU",
+               "SQ_INSTS_MFMA", "SQ_INSTS_LDS", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_VALU", "GRBM_GUI_ACTIVE")
+N_CU = 256
+N_XCD = 8
+
+
+def _short_kernel(name):
+    """Kernel name without namespaces, return type and argument list (template arguments kept)."""
+    n = name.replace("(anonymous namespace)::", "").replace("bsa::", "")
+    if n.startswith("void "):
+        n = n[5:]
+    depth = 0
+    for i, ch in enumerate(n):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            return n[:i]
+    return n
+
+
+def _per_kernel(csv_path, counters):
+    """{kernel: {counter: mean value per dispatch, "_n": dispatches}} from a rocprofv3 counter CSV."""
+    import csv
+    acc = {}
+    for r in csv.DictReader(open(csv_path)):
+        if r["Counter_Name"] not in counters:
+            continue
+        k = _short_kernel(r["Kernel_Name"])
+        d = acc.setdefault(k, {})
+        d.setdefault(r["Counter_Name"], {})[r["Dispatch_Id"]] = d.get(r["Counter_Name"], {}).get(
+            r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    out = {}
+    for k, d in acc.items():
+        out[k] = {c: sum(v.values()) / len(v) for c, v in d.items()}
+        out[k]["_n"] = max(len(v) for v in d.values())
+    return out
+
+
+def summarize_counters(args):
+    """Per-kernel table from one rocprofv3 kernel trace (durations) and counter runs:
+    FETCH_SIZE, WRITE_SIZE (HBM bytes, scaled by a plain 1 GiB copy) and the SQ/GRBM
+    instruction and MFMA counters."""
+    import csv
+    trace, fetch, write, sq, cfetch, cwrite = args.summarize_counters
+    dur = {}
+    for r in csv.DictReader(open(trace)):
+        k = _short_kernel(r["Kernel_Name"])
+        dur.setdefault(k, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
+    f = _per_kernel(fetch, ("FETCH_SIZE",))
+    w = _per_kernel(write, ("WRITE_SIZE",))
+    q = _per_kernel(sq, SQ_COUNTERS)
+    is_copy = lambda n: "copy" in n.lower()
+    cf = [v["FETCH_SIZE"] for k, v in _per_kernel(cfetch, ("FETCH_SIZE",)).items() if is_copy(k)]
+    cw = [v["WRITE_SIZE"] for k, v in _per_kernel(cwrite, ("WRITE_SIZE",)).items() if is_copy(k)]
+    ff, fw = COPY_BYTES / (cf[0] * 1024), COPY_BYTES / (cw[0] * 1024)
+    total = sum(sum(v) for v in dur.values())
+    rows = []
+    for k, ds in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
+        t = sum(ds) / len(ds)
+        if sum(ds) < 0.002 * total:
+            continue
+        fb = f.get(k, {}).get("FETCH_SIZE", float("nan")) * 1024 * ff
+        wb = w.get(k, {}).get("WRITE_SIZE", float("nan")) * 1024 * fw
+        c = q.get(k, {})
+        mops = c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)
+        gui = c.get("GRBM_GUI_ACTIVE", float("nan"))
+        rows.append({
+            "kernel": k, "calls": len(ds), "avg_us": t * 1e6, "gpu_time_pct": 100 * sum(ds) / total,
+            "fetch_mb": fb / 1e6, "write_mb": wb / 1e6, "hbm_gbps": (fb + wb) / t / 1e9,
+            "mfma_tflops_executed": 512 * mops / t / 1e12,
+            # GRBM_GUI_ACTIVE counts GPU-busy cycles summed over the 8 XCDs
+            "mfma_busy_pct": 100 * c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (gui / N_XCD * N_CU * 4) if gui == gui
+            else float("nan"),
+            "clock_ghz": gui / N_XCD / t / 1e9 if gui == gui else float("nan"),
+            "valu_insts": c.get("SQ_INSTS_VALU", float("nan")), "mfma_insts": c.get("SQ_INSTS_MFMA", float("nan")),
+            "lds_insts": c.get("SQ_INSTS_LDS", float("nan")),
+        })
+    out = args.counters_out
+    with open(out, "w") as fh:
+        fh.write(f"# Per-kernel counters: {args.counters_title}\n\n")
+        fh.write("Commands (repository root on the MI355X box, after `cd /tmp && export TMPDIR=/tmp`):\n\n")
+        for cmd in args.commands:
+            fh.write(f"    {cmd}\n")
+        fh.write("\nDurations from the kernel trace (every kernel alone: the library on one stream). HBM bytes =\n"
+                 "FETCH_SIZE and WRITE_SIZE (KiB per dispatch) scaled by what they read for a plain 1 GiB device\n"
+                 f"copy (fetch x{ff:.3f}, write x{fw:.3f}). MFMA TFLOP/s executed = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16 /\n"
+                 "duration (every MFMA FLOP issued, recomputation included). MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES /\n"
+                 "(GRBM_GUI_ACTIVE / 8 XCDs x 256 CUs x 4 SIMDs); clock = GRBM_GUI_ACTIVE / 8 / duration. Instruction\n"
+                 "counts are per dispatch (all waves). Kernels under 0.2% of GPU time are left out.\n\n")
+        cols = ("kernel", "calls", "avg_us", "gpu_time_pct", "fetch_mb", "write_mb", "hbm_gbps",
+                "mfma_tflops_executed", "mfma_busy_pct", "clock_ghz", "valu_insts", "mfma_insts", "lds_insts")
+        fh.write("| " + " | ".join(cols) + " |\n|" + "---|" * len(cols) + "\n")
+        for r in rows:
+            cells = []
+            for c in cols:
+                v = r[c]
+                if isinstance(v, str):
+                    cells.append(f"`{v}`")
+                elif c in ("calls",):
+                    cells.append(str(v))
+                elif c.endswith("insts"):
+                    cells.append(f"{v:.3g}")
+                elif c == "clock_ghz":
+                    cells.append(f"{v:.2f}")
+                else:
+                    cells.append(f"{v:.1f}")
+            fh.write("| " + " | ".join(cells) + " |\n")
+    print(open(out).read())
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -201,6 +404,8 @@ def parse():
                          "BSA vs full attention (one JSON line per length)")
     ap.add_argument("--lengths", default="1024,2048,4096,8192,16384,32768,65536")
     ap.add_argument("--cpu-baseline", type=int, default=1, help="time the float64 oracle on a sample (0 = skip)")
+    ap.add_argument("--rep-steps", type=int, default=100,
+                    help="steps of the warm and of the cold median after the timed region (0 = skip)")
     ap.add_argument("--copy-calibration", action="store_true", help="run only the 1 GiB plain copy")
     ap.add_argument("--summarize-traffic", nargs=4, metavar="CSV",
                     help="counter CSVs: FETCH_SIZE bench, WRITE_SIZE bench, FETCH_SIZE copy, WRITE_SIZE copy")
@@ -210,6 +415,12 @@ def parse():
                                          "paper_2506_12541_amd/csrc/common.hpp paper_2506_12541_amd/csrc/kernels.hpp "
                                          "paper_2506_12541_amd/build.py")
     ap.add_argument("--commands", nargs="*", default=[])
+    ap.add_argument("--summarize-counters", nargs=6, metavar="CSV",
+                    help="kernel trace, FETCH_SIZE, WRITE_SIZE and SQ counter CSVs of the bench, FETCH_SIZE and "
+                         "WRITE_SIZE CSVs of --copy-calibration")
+    ap.add_argument("--counters-out", default=os.path.join(ROOT, "profiles", "counters.md"))
+    ap.add_argument("--counters-title", default="")
+    ap.add_argument("--streams", type=int, default=2, help="library streams (1 = every kernel alone)")
     return ap.parse_args()
 
 
@@ -462,6 +673,9 @@ def main():
     if args.summarize_traffic:
         summarize_traffic(args)
         return
+    if args.summarize_counters:
+        summarize_counters(args)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the multi-GPU sharding is a design "
               "in DESIGN.md, not a measured path", file=sys.stderr)
@@ -510,10 +724,11 @@ def main():
         grads = gb.backward(p, q, k, v, vmask, gate, phi_k, phi_v, sv, dout, phi_q=phi_q)
         return o, grads
 
+    lib = _lib.load()
+    _lib.check(lib.bsa_set_streams(args.streams), "streams")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    lib = _lib.load()
 
     def phase_ms(names, steps):
         out = {}
@@ -524,8 +739,10 @@ def main():
             out[name] = tot.value / max(1, steps)
         return out
 
-    # phase pass (not the timed region): every phase records a pair of events, which
-    # itself adds a little time, so the breakdown is taken on its own steps
+    # phase passes (not the timed region): every phase records a pair of events, which
+    # itself adds a little time, so the breakdowns are taken on steps of their own: first
+    # as the step runs (two streams; phases that overlap share the chip), then with every
+    # kernel alone (one stream), which gives each phase's own roofline
     lib.bsa_timing_select(None)
     lib.bsa_timing_enable(1)
     for _ in range(PHASE_STEPS):
@@ -533,21 +750,60 @@ def main():
     torch.cuda.synchronize()
     phases = phase_ms(PHASES, PHASE_STEPS)
     lib.bsa_timing_enable(0)
-    # dominant kernel: the longest single-launch contraction phase that runs alone on the chip
-    dom = max((n for n in MFMA_PHASES if n not in CONCURRENT_PHASES), key=lambda n: phases[n])
+    _lib.check(lib.bsa_set_streams(1), "streams")
+    lib.bsa_timing_enable(1)
+    for _ in range(PHASE_STEPS):
+        step()
+    torch.cuda.synchronize()
+    alone = phase_ms(PHASES, PHASE_STEPS)
+    lib.bsa_timing_enable(0)
+    _lib.check(lib.bsa_set_streams(args.streams), "streams")
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    # dominant kernel: the bf16 contraction phase with the longest time of its own
+    dom = max(MFMA_PHASES, key=lambda n: alone[n])
 
-    # timed region: only the dominant kernel's phase records events (its live duration)
+    # timed region: exactly `steps` steps; only the dominant kernel's phase records events
+    # (its live duration), plus one event per step on the caller's stream (the step's own
+    # work ends there: the library joins its second stream back into it)
     lib.bsa_timing_select(dom.encode())
     lib.bsa_timing_enable(1)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    ev[0].record()
+    for i in range(args.steps):
         step()
+        ev[i + 1].record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     dom_ms = phase_ms([dom], args.steps)[dom]
     lib.bsa_timing_enable(0)
     lib.bsa_timing_select(None)
+    step_ms = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
+    median_ms = step_ms[len(step_ms) // 2] if len(step_ms) % 2 else 0.5 * (step_ms[len(step_ms) // 2 - 1] +
+                                                                            step_ms[len(step_ms) // 2])
+
+    # warm and cold medians (after the timed region; not part of `value`): warm = steps back
+    # to back; cold = a 512 MiB write before each step evicts the 256 MB MALL and the L2s
+    def median_of(flush, n):
+        flush_buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev) if flush else None
+        times = []
+        a_ev = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        b_ev = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        for i in range(n):
+            if flush:
+                flush_buf.fill_(float(i))
+            a_ev[i].record()
+            step()
+            b_ev[i].record()
+        torch.cuda.synchronize()
+        times = sorted(a_ev[i].elapsed_time(b_ev[i]) for i in range(n))
+        return times[n // 2]
+
+    warm_ms = median_of(False, args.rep_steps) if args.rep_steps else None
+    cold_ms = median_of(True, args.rep_steps) if args.rep_steps else None
 
     ms = elapsed / args.steps * 1e3
     fwd_f, bwd_f = algorithmic_flops(cfg, args.variant)
@@ -560,6 +816,7 @@ def main():
     achieved = pf[dom] / (dom_ms * 1e-3) / 1e12
     wl = cfg.name if args.variant == "bsa" else f"{args.variant}_{cfg.name}"
     traffic = measured_traffic(dom, wl)
+    phase_roof, branch_roof = rooflines(cfg, args.variant, alone)
     result = {
         "metric": "BSA layer fwd+bwd points/sec and TFLOP/s (fraction of MFMA peak) at N=65536, 1 GPU",
         "value": cfg.batch * cfg.n_real / (ms * 1e-3),
@@ -582,6 +839,12 @@ def main():
                                + "; tree + permute + forward + backward",
                    "variant": args.variant,
                    "points": cfg.batch * cfg.n_real, "heads": cfg.heads, "head_dim": cfg.head_dim},
+        "ms_per_step_median": round(median_ms, 4),
+        "timing": {"warm_median_ms": None if warm_ms is None else round(warm_ms, 4),
+                   "cold_median_ms": None if cold_ms is None else round(cold_ms, 4),
+                   "steps_each": args.rep_steps, "cold_flush_bytes": FLUSH_BYTES,
+                   "note": "medians of per-step HIP events after the timed region; cold = a 512 MiB device "
+                           "write before each step"},
         "tflops": tflops,
         "mfma_frac": tflops * 1e12 / MFMA_BF16_PEAK,
         "algorithmic_gflop_per_step": flops / 1e9,
@@ -590,10 +853,12 @@ def main():
         # these phases run on the library's second stream beside others, so their
         # durations include time shared with the concurrent branch
         "concurrent_phases": CONCURRENT_PHASES,
-        "phase_tflops": {n: round(pf[n] / (phases[n] * 1e-3) / 1e12, 1) for n in pf if phases[n] > 0},
+        "phase_ms_alone": {n: round(v, 4) for n, v in alone.items()},
+        "phase_roofline": phase_roof,
+        "branch_roofline": branch_roof,
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": MFMA_BF16_PEAK / 1e12,
                      "unit": "TFLOP/s", "frac": achieved * 1e12 / MFMA_BF16_PEAK, "traffic": traffic,
-                     "launch_ms": dom_ms,
+                     "launch_ms": dom_ms, "launch_ms_alone": round(alone[dom], 4),
                      "algorithmic_gflop_per_launch": pf[dom] / 1e9},
     }
     if args.cpu_baseline:
