@@ -198,10 +198,12 @@ template <int HD, int ROWS, int NW>
 __device__ __forceinline__ void dma_tile(bf16_t* lds, const bf16_t* g, int r0, int nrows, int wid, int lane) {
   constexpr int CPR = HD / 8;           // 16-byte chunks per row
   constexpr int NI = ROWS * CPR / 64;   // 1 KB wave instructions per tile
-  static_assert(NI % NW == 0, "tile / wave split");
+  static_assert(NI % NW == 0 || NW % NI == 0, "tile / wave split");
+  constexpr int PER = NI >= NW ? NI / NW : 1;   // fewer instructions than waves: one each
+  if (NI < NW && wid >= NI) return;
 #pragma unroll
-  for (int u = 0; u < NI / NW; ++u) {
-    const int blk = wid * (NI / NW) + u;
+  for (int u = 0; u < PER; ++u) {
+    const int blk = wid * PER + u;
     const int idx = blk * 64 + lane;
     const int row = idx / CPR;
     const int lc = (idx % CPR) ^ swz<HD>(row);
@@ -385,6 +387,95 @@ struct WaveAttn {
         for (int kp = 0; kp < KB / 2; ++kp)
 #pragma unroll
           for (int qb = 0; qb < QB; ++qb) o[qb][db] = mma(vr[db][kp], pf[qb][kp], o[qb][db]);
+    }
+  }
+
+  // ---- the step split into its stages, for kernels that software-pipeline key tiles ----
+  // Scores S^T of a tile of KB 16-key blocks: s[qb][kb] (this lane: keys 4j + i of block kb
+  // for query r of block qb).
+  template <int KB, typename KF>
+  __device__ __forceinline__ void scores(f32x4 (&s)[QB][KB], KF kfrag) const {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        CT a = kfrag(kb, c);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) s[qb][kb] = mma(a, qf[qb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : s[qb][kb]);
+      }
+  }
+  // Masks a score tile (MASK: keyok(kb, i) false -> -inf) and moves the reference maximum:
+  // like tile(), it is raised only when the tile's maximum exceeds it by more than
+  // kRescale. Returns whether any query of the wave raised it (wave-uniform); alpha[qb] is
+  // then the factor for the accumulated O and row sums (1 where not raised).
+  template <int KB, bool MASK, typename OK>
+  __device__ __forceinline__ bool tile_max(f32x4 (&s)[QB][KB], float sl2, OK keyok, float (&alpha)[QB]) {
+    bool any = false;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float tmax = kNegInf;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if constexpr (MASK) s[qb][kb][i] = keyok(kb, i) ? s[qb][kb][i] : kNegInf;
+          tmax = fmaxf(tmax, s[qb][kb][i]);
+        }
+      tmax = col_max(tmax) * sl2;
+      const bool raise = tmax > mx[qb] + kRescale;
+      const float mnew = raise ? tmax : mx[qb];
+      alpha[qb] = raise ? fast_exp2(mx[qb] - mnew) : 1.0f;
+      mx[qb] = mnew;
+      any = any || __builtin_amdgcn_ballot_w64(raise) != 0;
+    }
+    return any;
+  }
+  __device__ __forceinline__ void rescale(const float (&alpha)[QB]) {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      lsum[qb] *= alpha[qb];
+      if constexpr (!LSE_ONLY) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[qb][db] *= alpha[qb];
+      }
+    }
+  }
+  // Probabilities of a masked score tile against the current reference maxima, packed as
+  // the B operands of the P V product.
+  template <int KB>
+  __device__ __forceinline__ void probs(const f32x4 (&s)[QB][KB], float sl2, CT (&pf)[QB][KB / 2]) const {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const float mref = mx[qb] == kNegInf ? 0.f : mx[qb];
+#pragma unroll
+      for (int kp = 0; kp < KB / 2; ++kp) {
+        float v8[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          v8[i] = fast_exp2(__builtin_fmaf(s[qb][2 * kp][i], sl2, -mref));
+          v8[4 + i] = fast_exp2(__builtin_fmaf(s[qb][2 * kp + 1][i], sl2, -mref));
+        }
+        pf[qb][kp] = make_chunk<T>(v8);
+      }
+    }
+  }
+  // Row sums and O += V^T P^T for one tile (vfrag as in tile()).
+  template <int KB, typename VF>
+  __device__ __forceinline__ void pv(const CT (&pf)[QB][KB / 2], VF vfrag) {
+    const CT ones = ones_chunk<T>();
+#pragma unroll
+    for (int kp = 0; kp < KB / 2; ++kp)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) lsum[qb] = mma(ones, pf[qb][kp], lsum[qb]);
+    if constexpr (!LSE_ONLY) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int kp = 0; kp < KB / 2; ++kp) {
+          const CT vr = vfrag(db, kp);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) o[qb][db] = mma(vr, pf[qb][kp], o[qb][db]);
+        }
     }
   }
 

@@ -12,6 +12,8 @@
 // lane owns one query column, so the probabilities produced by the first product are
 // already laid out as the B operand of the second and never leave registers. V enters
 // as V^T, which the kernels stage through LDS (transposing while storing).
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "attn_common.hpp"
@@ -86,18 +88,53 @@ __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, 
   w.finish(lane, bh * N + wq0, out, lse, qval, wq0);
 }
 
-// bf16 variant: 64-key K and V tiles double-buffered in LDS and filled by direct
-// global->LDS loads (no staging registers, one barrier per tile); V^T fragments come from
-// transpose reads of the row-major V tile. The two buffers are distinct LDS objects and
-// the loop is unrolled by two, so the compiler can tell that loads in flight into one
-// buffer do not alias reads of the other and need not be waited for.
+// Instruction interleaving of the pipelined forward's two regions (scheduling-group
+// barriers of the AMDGPU backend: 0x8 MFMA, 0x2 VALU, 0x100 LDS read). Region 1: NM score
+// MFMAs, each followed by five VALU instructions of the exponentials (about 80 per tile),
+// the K fragments read two ahead. Region 2: NM P V MFMAs, each followed by two VALU
+// instructions of the next tile's row maxima, its V^T fragment reads (ND) spread among them.
+template <int NM>
+__device__ __forceinline__ void interleave_scores_exps() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+    if (i % 2 == 0) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+}
+template <int NM, int ND>
+__device__ __forceinline__ void interleave_pv_max() {
+  __builtin_amdgcn_sched_group_barrier(0x100, ND > 4 ? 4 : ND, 0);
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+    if (i + 4 < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+}
+
+// bf16 variant: 64-key tiles filled by direct global->LDS loads (no staging registers),
+// V^T fragments from transpose reads of the row-major V tile, software-pipelined so that
+// the matrix cores and the vector ALUs work at the same time. The scores of tile t + 1 are
+// formed while the probabilities of tile t are exponentiated, and the P V product of tile t
+// runs while the row maxima of tile t + 1 are taken; without that, each wave ran its MFMA
+// and VALU work back to back (about 320 + 345 ns per 64-key tile of 32 queries). K therefore
+// runs one tile ahead of V in LDS: iteration t reads K(t + 1) and V(t) while K(t + 2) and
+// V(t + 1) load into the buffers that K(t) and V(t - 1) left. Each buffer is its own LDS
+// object and the loop is unrolled by two, so the compiler can tell that loads in flight
+// into one buffer do not alias reads of another. MASK = false: every key of the launch is
+// real and the key count a multiple of 64 (no per-key select).
 // LO: log-sum-exp rows only (the V tiles are not loaded; no output rows).
-template <int HD, int QB, int NW, bool BALL, typename OT = bf16_t, bool LO = false>
+template <int HD, int QB, int NW, bool BALL, typename OT = bf16_t, bool LO = false, bool MASK = true>
 __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
                                                                 const uint8_t* qvalid_all, const uint8_t* kvalid_all,
                                                                 int H, int N, int nkeys_total, int m, float sl2,
                                                                 OT* out, float* lse) {
   constexpr int kFT = kKT;
+  constexpr int KB = kFT / 16;
+  typedef WaveAttn<bf16_t, HD, QB, LO> WA;
+  typedef typename WA::CT CT;
   __shared__ __attribute__((aligned(16))) bf16_t ks0[kFT * HD], ks1[kFT * HD];
   __shared__ __attribute__((aligned(16))) bf16_t vs0[kFT * HD], vs1[kFT * HD];
   __shared__ uint8_t ok0[kFT], ok1[kFT];
@@ -112,41 +149,96 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q,
   const bf16_t* vh = v + (bh * nkeys_total + key0) * HD;
   const uint8_t* kval = kvalid_all ? kvalid_all + (size_t)b * nkeys_total + key0 : nullptr;
   const uint8_t* qval = qvalid_all ? qvalid_all + (size_t)b * N : nullptr;
+  const int nt = (nkeys + kFT - 1) / kFT;   // key tiles
 
-  // key-validity bytes are read before the tile loads, so waiting for them does not
-  // wait for the tile
-  auto issue = [&](int t0, bf16_t* kd, bf16_t* vd, uint8_t* okd) {
-    uint8_t okv = 0;
-    if (threadIdx.x < kFT) {
-      const int key = t0 + threadIdx.x;
-      okv = key < nkeys && (kval == nullptr || kval[key]);
+  // K tile (and its key-validity bytes, read before the tile loads so that waiting for them
+  // does not wait for the tile) / V tile of tile t. Tiles past the end are loaded too (their
+  // rows clamp to the last key; the buffer is free and nothing reads them): no branch
+  // splits the regions of the pipelined step.
+  auto issue_k = [&](int t, bf16_t* kd, uint8_t* okd) {
+    if constexpr (MASK) {
+      uint8_t okv = 0;
+      if (threadIdx.x < kFT) {
+        const int key = t * kFT + threadIdx.x;
+        okv = key < nkeys && (kval == nullptr || kval[key]);
+      }
+      dma_tile<HD, kFT, NW>(kd, kh, t * kFT, nkeys, wid, lane);
+      if (threadIdx.x < kFT) okd[threadIdx.x] = okv;
+    } else {
+      dma_tile<HD, kFT, NW>(kd, kh, t * kFT, nkeys, wid, lane);
     }
-    dma_tile<HD, kFT, NW>(kd, kh, t0, nkeys, wid, lane);
-    if constexpr (!LO) dma_tile<HD, kFT, NW>(vd, vh, t0, nkeys, wid, lane);
-    if (threadIdx.x < kFT) okd[threadIdx.x] = okv;
   };
-  WaveAttn<bf16_t, HD, QB, LO> w;
+  auto issue_v = [&](int t, bf16_t* vd) {
+    if constexpr (!LO) dma_tile<HD, kFT, NW>(vd, vh, t * kFT, nkeys, wid, lane);
+  };
+  WA w;
   w.init();
   const int wq0 = q0 + wid * 16 * QB;
-  auto step = [&](int t0, const bf16_t* kt, const bf16_t* vt, const uint8_t* ok, bf16_t* kn, bf16_t* vn,
-                  uint8_t* okn) {
-    vm_drain();          // this wave's loads of the tile have landed
-    __syncthreads();     // ... and every wave's; the previous tile is no longer read
-    if (t0 + kFT < nkeys) issue(t0 + kFT, kn, vn, okn);
-    auto kfrag = [&](int kb, int c) { return lds_row_chunk<HD>(kt, kb * 16 + r, 4 * c + j); };
-    auto vfrag = [&](int db, int kp) { return lds_tr_chunk<HD>(vt, 32 * kp, 16 * db, lane); };
-    if (kval == nullptr && t0 + kFT <= nkeys) {
-      w.template tile<kFT / 16>(sl2, kfrag, vfrag, [](int, int, int) { return true; });
-    } else {
-      auto keyok = [&](int kb, int i, int) { return ok[kb * 16 + 4 * j + i] != 0; };
-      w.template tile<kFT / 16>(sl2, kfrag, vfrag, keyok);
+  f32x4 s_cur[QB][KB], s_nxt[QB][KB];
+  float alpha[QB];
+  bool raise = false;
+
+  auto kfrag_of = [&](const bf16_t* kt) {
+    return [=](int kb, int c) { return lds_row_chunk<HD>(kt, kb * 16 + r, 4 * c + j); };
+  };
+  auto keyok_of = [&](const uint8_t* ok) {
+    return [=](int kb, int i) { return ok[kb * 16 + 4 * j + i] != 0; };
+  };
+  // iteration t: LDS holds K(t + 1) in kn/okn and V(t) in vc; kc/okc (K(t)) and vn
+  // (V(t - 1)) are free once every wave has passed the barrier. MORE: tile t + 1 exists
+  // (the last iteration has no next tile; keeping the test out of the other iterations
+  // keeps each of their two regions one straight-line block the scheduler can interleave).
+  auto step = [&](auto more_t, int t, bf16_t* kc, uint8_t* okc, const bf16_t* kn, const uint8_t* okn,
+                  const bf16_t* vc, bf16_t* vn) {
+    constexpr bool MORE = decltype(more_t)::value;
+    vm_drain();          // this wave's loads of K(t + 1) and V(t) have landed
+    __syncthreads();     // ... and every wave's; K(t) and V(t - 1) are no longer read
+    issue_k(t + 2, kc, okc);
+    issue_v(t + 1, vn);
+    // region 1: scores of tile t + 1 beside the exponentials of tile t
+    CT pf[QB][KB / 2];
+    if constexpr (MORE) w.template scores<KB>(s_nxt, kfrag_of(kn));
+    w.template probs<KB>(s_cur, sl2, pf);
+    if constexpr (MORE) interleave_scores_exps<KB * WA::NCH * QB>();
+    // the probabilities are complete here: the compiler may not sink their computation
+    // below the rescale branch, out of the block holding the score MFMAs
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+      for (int kp = 0; kp < KB / 2; ++kp) asm volatile("" : "+v"(pf[qb][kp]));
+    if (raise) w.rescale(alpha);   // rare: a query's maximum rose (wave-uniform)
+    // region 2: P V of tile t beside the row maxima of tile t + 1
+    w.template pv<KB>(pf, [&](int db, int kp) { return lds_tr_chunk<HD>(vc, 32 * kp, 16 * db, lane); });
+    if constexpr (MORE) {
+      raise = w.template tile_max<KB, MASK>(s_nxt, sl2, keyok_of(okn), alpha);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) s_cur[qb][kb] = s_nxt[qb][kb];
+      interleave_pv_max<(KB / 2) * QB * (LO ? 1 : 1 + WA::DB), LO ? 0 : WA::DB * (KB / 2) * 2>();
     }
   };
-  issue(0, ks0, vs0, ok0);
+  using more = std::true_type;
+  using last = std::false_type;
+  // prologue: K(0) in, scores and maxima of tile 0, then K(1) and V(0) in flight
+  issue_k(0, ks0, ok0);
   load_q(w, q + (bh * N + wq0) * HD, lane);
-  for (int t0 = 0; t0 < nkeys; t0 += 2 * kFT) {
-    step(t0, ks0, vs0, ok0, ks1, vs1, ok1);
-    if (t0 + kFT < nkeys) step(t0 + kFT, ks1, vs1, ok1, ks0, vs0, ok0);
+  vm_drain();
+  __syncthreads();
+  w.template scores<KB>(s_cur, kfrag_of(ks0));
+  raise = w.template tile_max<KB, MASK>(s_cur, sl2, keyok_of(ok0), alpha);
+  issue_k(1, ks1, ok1);
+  issue_v(0, vs0);
+  int t = 0;
+  for (; t + 2 < nt; t += 2) {
+    step(more{}, t, ks0, ok0, ks1, ok1, vs0, vs1);
+    step(more{}, t + 1, ks1, ok1, ks0, ok0, vs1, vs0);
+  }
+  if (t + 1 < nt) {   // two tiles left
+    step(more{}, t, ks0, ok0, ks1, ok1, vs0, vs1);
+    step(last{}, t + 1, ks1, ok1, ks0, ok0, vs1, vs0);
+  } else {            // one tile left
+    step(last{}, t, ks0, ok0, ks1, ok1, vs0, vs1);
   }
   w.finish(lane, bh * N + wq0, out, lse, qval, wq0);
 }
@@ -384,13 +476,22 @@ template <typename T, int HD, int QB, bool BALL, int NW = 4, typename OT = T>
 void launch_dense_fwd(dim3 grid, hipStream_t st, const void* q, const void* k, const void* v, const uint8_t* qvalid,
                       const uint8_t* kvalid, int H, int N, int nkeys_total, int m, float sl2, void* o, float* lse) {
   if constexpr (sizeof(T) == 2) {
-    if (o)
-      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT>), grid, dim3(64 * NW), 0, st, (const bf16_t*)q,
-                         (const bf16_t*)k, (const bf16_t*)v, qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
+    // every key real and whole 64-key tiles: no per-key select
+    const bool mask = kvalid != nullptr || (BALL ? m : nkeys_total) % kKT != 0;
+    const bf16_t *qq = (const bf16_t*)q, *kk = (const bf16_t*)k, *vv = (const bf16_t*)v;
+    const dim3 blk(64 * NW);
+    if (o && mask)
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, false, true>), grid, blk, 0, st, qq, kk, vv,
+                         qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
+    else if (o)
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, false, false>), grid, blk, 0, st, qq, kk, vv,
+                         qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
+    else if (mask)
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, true, true>), grid, blk, 0, st, qq, kk, vv,
+                         qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
     else
-      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, true>), grid, dim3(64 * NW), 0, st,
-                         (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, qvalid, kvalid, H, N, nkeys_total, m,
-                         sl2, (OT*)o, lse);
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, true, false>), grid, blk, 0, st, qq, kk, vv,
+                         qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
   } else {
     if (o)
       hipLaunchKernelGGL((dense_fwd_kernel<T, HD, QB, BALL, OT>), grid, dim3(256), 0, st, (const T*)q, (const T*)k,
