@@ -157,7 +157,8 @@ def rooflines(cfg, variant, ms):
                   "hbm_gbps_compulsory": round(pb[n] / (t * 1e-3) / 1e9, 1)}
     branches = {}
     for br, names in BRANCH_PHASES.items():
-        if not all(n in ms for n in names):
+        names = [n for n in names if ms.get(n, 0.0) > 0.0]   # phases that ran
+        if not names:
             continue
         t = sum(ms[n] for n in names)
         f = sum(pf.get(n, 0.0) for n in names)
@@ -167,7 +168,7 @@ def rooflines(cfg, variant, ms):
         branches[br] = {"ms": round(t, 4), "tflops": round(ach / 1e12, 1), "frac_peak": round(ach / MFMA_BF16_PEAK, 4),
                         "flop_per_byte": round(f / byt, 1), "attainable_tflops": round(att / 1e12, 1),
                         "frac_attainable": round(ach / att, 4)}
-    if "slc" in branches:
+    if "slc" in branches and ms.get("fwd.slc", 0.0) > 0.0:
         # the selection's gathers: g FLOP per gathered byte if every gather came from HBM
         gb = gathered_bytes(cfg)
         fs = pf["fwd.slc"]
@@ -421,6 +422,8 @@ def parse():
     ap.add_argument("--counters-out", default=os.path.join(ROOT, "profiles", "counters.md"))
     ap.add_argument("--counters-title", default="")
     ap.add_argument("--streams", type=int, default=2, help="library streams (1 = every kernel alone)")
+    ap.add_argument("--forward-only", action="store_true",
+                    help="time tree + permute + forward (e.g. --config 4, the 2^20-point workload)")
     return ap.parse_args()
 
 
@@ -452,6 +455,50 @@ def cpu_baseline(cfg, pts_np, inp_np, variant="bsa"):
     return {"value": cfg.batch * cfg.n_real / total, "unit": "points/s", "cores": cores, "kind": "oracle",
             "sample": f"ball tree of the full {cfg.n_real}-point cloud ({t_tree:.2f} s) + forward and backward of "
                       f"1 of {cfg.heads} heads ({t_head:.2f} s), scaled x{cfg.heads}; float64 numpy"}
+
+
+def cpu_baseline_large(cfg, pts_np, hi, groups=32):
+    """The float64 oracle's forward on a bounded sample of the 2^20-point workload: the full
+    ball tree, then for one head the compression of every block (the part that does not
+    shrink with the sample) and the three branches and the gate for `groups` sampled query
+    groups; extrapolated linearly to every group and head (labelled as such)."""
+    import numpy as np
+
+    from oracle import bsa as ob
+    from oracle.tree import build_ball_tree
+
+    cores = len(os.sched_getaffinity(0))
+    P = ob.Params(ball=cfg.ball, cmp_block=cfg.cmp_block, slc_block=cfg.slc_block, topk=cfg.topk, group=cfg.group)
+    t0 = time.perf_counter()
+    perm = build_ball_tree(pts_np[0], cfg.n_pad)
+    t_tree = time.perf_counter() - t0
+    valid = perm >= 0
+    x = {n: a.astype(np.float64) for n, a in hi.head(0).items()}
+    phk = {w: a.astype(np.float64) for w, a in hi.phi_k.items()}
+    phv = {w: a.astype(np.float64) for w, a in hi.phi_v.items()}
+    t0 = time.perf_counter()
+    kc, _ = ob.compress(x["k"], valid, phk, P)
+    vc, _ = ob.compress(x["v"], valid, phv, P)
+    t_fixed = time.perf_counter() - t0
+    ngroups = cfg.n_pad // cfg.group
+    gs = np.random.default_rng(0).choice(ngroups, groups, replace=False)
+    t0 = time.perf_counter()
+    sel = ob.topk_blocks(ob.group_block_scores(x["q"], kc, valid, P, groups=gs), P.topk)
+    full_sel = np.full((ngroups, P.topk), -1, np.int64)
+    full_sel[gs] = sel
+    rows = (gs[:, None] * cfg.group + np.arange(cfg.group)[None, :]).reshape(-1)
+    for s0 in np.unique((rows // cfg.ball) * cfg.ball):
+        sl = slice(s0, s0 + cfg.ball)
+        ob.ball_branch(x["q"][sl], x["k"][sl], x["v"][sl], valid[sl], P)
+    ob.compression_branch(x["q"], kc, vc, ob.block_valid(valid, cfg.cmp_block), valid, P, rows=rows)
+    ob.selection_branch(x["q"], x["k"], x["v"], valid, full_sel, P, groups=gs)
+    t_groups = time.perf_counter() - t0
+    total = t_tree + cfg.heads * (t_fixed + t_groups * ngroups / groups)
+    return {"value": cfg.batch * cfg.n_real / total, "unit": "points/s", "cores": cores, "kind": "oracle",
+            "sample": f"ball tree of the full {cfg.n_real}-point cloud ({t_tree:.1f} s) + one head's compression of "
+                      f"every block ({t_fixed:.1f} s) and forward of {groups} of {ngroups} query groups "
+                      f"({t_groups:.1f} s); extrapolated x{ngroups // groups} groups, x{cfg.heads} heads; "
+                      "forward only, float64 numpy"}
 
 
 def sweep(args):
@@ -697,20 +744,40 @@ def main():
         cfg = dataclasses.replace(cfg, group=1)
     dev = torch.device("cuda:0")
     pts_np = make_points(cfg)
-    inp_np = make_inputs(cfg, layout="points", with_grad=False)
-    inp_np["do"] = make_inputs(cfg, layout="ball", with_grad=True)["do"]
     p = gb.Params.from_config(cfg, **VARIANTS[args.variant])
     dt = p.torch_dtype
     t = lambda a, d=None: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(d or torch.float32)
+    H, d = cfg.heads, cfg.head_dim
     pts = t(pts_np)
-    xq, xk, xv = (t(inp_np[n], dt) for n in ("q", "k", "v"))
-    gate_pts = t(inp_np["gate"])
+    large = cfg.batch == 1 and cfg.n_real == cfg.n_pad and cfg.n_pad >= (1 << 20)
+    if large:
+        # 2^20 points x 16 heads: inputs drawn head by head into the per-point layout (every
+        # slot is a real point, so a head's [n, d] draw serves as its per-point columns)
+        from workloads import HeadInputs
+        hi = HeadInputs(cfg)
+        xq, xk, xv = (torch.empty((1, cfg.n_real, H * d), dtype=dt, device=dev) for _ in range(3))
+        dout = None if args.forward_only else torch.empty((1, H, cfg.n_pad, d), dtype=dt, device=dev)
+        names = ("q", "k", "v") if args.forward_only else ("q", "k", "v", "do")
+
+        def put(h, x):
+            for name, dst in (("q", xq), ("k", xk), ("v", xv)):
+                dst[0, :, h * d:(h + 1) * d].copy_(t(x[name], dt))
+            if dout is not None:
+                dout[0, h].copy_(t(x["do"], dt))
+
+        hi.heads(put, names)
+        gate_pts = t(hi.gate)
+        inp_np = {"phi_k": hi.phi_k, "phi_v": hi.phi_v, "phi_q": hi.phi_q}
+    else:
+        inp_np = make_inputs(cfg, layout="points", with_grad=False)
+        inp_np["do"] = make_inputs(cfg, layout="ball", with_grad=True)["do"]
+        xq, xk, xv = (t(inp_np[n], dt) for n in ("q", "k", "v"))
+        gate_pts = t(inp_np["gate"])
+        dout = t(inp_np["do"], dt)
     phi_k = {w: t(a) for w, a in inp_np["phi_k"].items()}
     phi_v = {w: t(a) for w, a in inp_np["phi_v"].items()}
     phi_q = {w: t(a) for w, a in inp_np["phi_q"].items()}
-    dout = t(inp_np["do"], dt)
     saved = gb.Saved(p, dev)
-    H, d = cfg.heads, cfg.head_dim
 
     def step():
         perm = gb.build_ball_tree(pts, cfg.n_pad)
@@ -721,6 +788,8 @@ def main():
         # every slot holds a real point when n_real == n_pad: the layer may skip key masks
         vmask = None if cfg.n_real == cfg.n_pad else valid
         o, sv = gb.forward(p, q, k, v, vmask, gate, phi_k, phi_v, saved=saved, phi_q=phi_q)
+        if args.forward_only:
+            return o, None
         grads = gb.backward(p, q, k, v, vmask, gate, phi_k, phi_v, sv, dout, phi_q=phi_q)
         return o, grads
 
@@ -807,7 +876,7 @@ def main():
 
     ms = elapsed / args.steps * 1e3
     fwd_f, bwd_f = algorithmic_flops(cfg, args.variant)
-    flops = sum(fwd_f.values()) + sum(bwd_f.values())
+    flops = sum(fwd_f.values()) + (0.0 if args.forward_only else sum(bwd_f.values()))
     # the layer runs independent branches concurrently on two streams, so its time is the
     # step's wall time less the serial tree and permutation phases, not the sum of phases
     layer_ms = ms - phases["tree"] - phases["permute"]
@@ -818,7 +887,9 @@ def main():
     traffic = measured_traffic(dom, wl)
     phase_roof, branch_roof = rooflines(cfg, args.variant, alone)
     result = {
-        "metric": "BSA layer fwd+bwd points/sec and TFLOP/s (fraction of MFMA peak) at N=65536, 1 GPU",
+        "metric": ("BSA layer forward points/sec and TFLOP/s (fraction of MFMA peak) at "
+                   f"N={cfg.n_pad}, 1 GPU" if args.forward_only else
+                   "BSA layer fwd+bwd points/sec and TFLOP/s (fraction of MFMA peak) at N=65536, 1 GPU"),
         "value": cfg.batch * cfg.n_real / (ms * 1e-3),
         "unit": "points/s",
         "n_gpus": 1,
@@ -836,7 +907,8 @@ def main():
                                + {"bsa": "", "group_cmp": "; MLP query coarsening (Eq. 13-14) + group compression "
                                                           "(Eq. 15)",
                                   "g1": "; per-token selection (Eq. 6-8, no grouping)"}[args.variant]
-                               + "; tree + permute + forward + backward",
+                               + ("; tree + permute + forward" if args.forward_only else
+                                  "; tree + permute + forward + backward"),
                    "variant": args.variant,
                    "points": cfg.batch * cfg.n_real, "heads": cfg.heads, "head_dim": cfg.head_dim},
         "ms_per_step_median": round(median_ms, 4),
@@ -861,7 +933,9 @@ def main():
                      "launch_ms": dom_ms, "launch_ms_alone": round(alone[dom], 4),
                      "algorithmic_gflop_per_launch": pf[dom] / 1e9},
     }
-    if args.cpu_baseline:
+    if args.cpu_baseline and large:
+        result["cpu_baseline"] = cpu_baseline_large(cfg, pts_np, hi)
+    elif args.cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, pts_np, {**inp_np, **make_inputs(cfg, layout="ball",
                                                                                      with_grad=True)},
                                               args.variant)

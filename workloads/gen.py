@@ -16,7 +16,8 @@ import math
 
 import numpy as np
 
-__all__ = ["Config", "CONFIGS", "make_points", "make_inputs", "make_block_inputs", "round_bf16", "bf16_bits"]
+__all__ = ["Config", "CONFIGS", "make_points", "make_inputs", "make_block_inputs", "round_bf16", "bf16_bits",
+           "HeadInputs"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -224,6 +225,69 @@ def make_inputs(cfg: Config, seed: int | None = None, *, layout: str = "ball",
     if with_grad:
         out["do"] = rnd(_normal(r[7], (B, H, cfg.n_pad, d)))
     return out
+
+
+def _gate_logits_chunked(seq, rows: int, C: int, threads: int = 8) -> np.ndarray:
+    """Gate logits [1, rows, 3] = X W_g with W_g ~ N(0, 1/C) [C, 3] (drawn in float64, stored
+    as float32) and X ~ N(0,1) [rows, C] drawn in float32 in chunks of 2^16 rows, one stream
+    per chunk; the product is formed in float32. Chunks run in a thread pool."""
+    from concurrent.futures import ThreadPoolExecutor
+    nch = (rows + (1 << 16) - 1) >> 16
+    seqs = seq.spawn(nch + 1)
+    wg = (np.random.default_rng(seqs[0]).standard_normal((C, 3)) / math.sqrt(C)).astype(np.float32)
+    gate = np.empty((1, rows, 3), np.float32)
+
+    def chunk(i):
+        s0, e = i << 16, min(rows, (i + 1) << 16)
+        x = np.empty((e - s0, C), np.float32)
+        np.random.default_rng(seqs[i + 1]).standard_normal(out=x, dtype=np.float32)
+        gate[0, s0:e] = x @ wg
+
+    with ThreadPoolExecutor(threads) as ex:
+        list(ex.map(chunk, range(nch)))
+    return gate
+
+
+class HeadInputs:
+    """Seeded layer inputs drawn one head at a time, for workloads whose Q/K/V do not fit
+    comfortably in host memory at once (2^20 points x 16 heads): each (tensor, head) pair has
+    its own stream spawned from SeedSequence(seed * 1000 + 5), so any head can be drawn alone.
+    Same distributions as make_inputs (N(0,1) Q/K/V/dO rounded to bf16 for bf16 workloads,
+    gate logits X W_g, MLP weights N(0, 0.02^2)); cfg.batch must be 1."""
+
+    def __init__(self, cfg: Config, seed: int | None = None):
+        if cfg.batch != 1:
+            raise ValueError("HeadInputs draws one cloud")
+        self.cfg = cfg
+        self.seed = _default_seed(cfg, seed)
+        self._rnd = round_bf16 if cfg.dtype == "bf16" else (lambda a: a)
+        self._seqs = np.random.SeedSequence(self.seed * 1000 + 5).spawn(4 * cfg.heads + 4)
+        r = [np.random.default_rng(s) for s in self._seqs[4 * cfg.heads + 1:]]
+        ld = cfg.cmp_block * cfg.head_dim
+        self.gate = _gate_logits_chunked(self._seqs[4 * cfg.heads], cfg.n_pad, cfg.heads * cfg.head_dim)
+        self.phi_k = _mlp_weights(r[0], ld, cfg.head_dim, self._rnd)
+        self.phi_v = _mlp_weights(r[1], ld, cfg.head_dim, self._rnd)
+        self.phi_q = _mlp_weights(r[2], ld, cfg.head_dim, self._rnd)
+
+    def head(self, h: int, names=("q", "k", "v")) -> dict:
+        """{name: float32 [n_pad, d]} of head h (names among q, k, v, do)."""
+        out = {}
+        for i, n in enumerate(("q", "k", "v", "do")):
+            if n in names:
+                x = np.empty((self.cfg.n_pad, self.cfg.head_dim), np.float32)
+                np.random.default_rng(self._seqs[4 * h + i]).standard_normal(out=x, dtype=np.float32)
+                out[n] = self._rnd(x)
+        return out
+
+    def heads(self, fn, names=("q", "k", "v"), threads: int = 8):
+        """Calls fn(h, head(h, names)) for every head, drawing up to `threads` heads at once
+        (fn runs on the calling thread, in head order)."""
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(threads) as ex:
+            futs = [ex.submit(self.head, h, names) for h in range(self.cfg.heads)]
+            for h, f in enumerate(futs):
+                fn(h, f.result())
+                futs[h] = None
 
 
 def make_block_inputs(cfg: Config, valid: np.ndarray, ffn: int | None = None, seed: int | None = None) -> dict:
