@@ -422,6 +422,8 @@ def parse():
     ap.add_argument("--counters-out", default=os.path.join(ROOT, "profiles", "counters.md"))
     ap.add_argument("--counters-title", default="")
     ap.add_argument("--streams", type=int, default=2, help="library streams (1 = every kernel alone)")
+    ap.add_argument("--oracle-baselines", action="store_true",
+                    help="time the float64 oracle in full on configs 1, 2, 3 and 5 (CPU only)")
     ap.add_argument("--forward-only", action="store_true",
                     help="time tree + permute + forward (e.g. --config 4, the 2^20-point workload)")
     return ap.parse_args()
@@ -499,6 +501,41 @@ def cpu_baseline_large(cfg, pts_np, hi, groups=32):
                       f"every block ({t_fixed:.1f} s) and forward of {groups} of {ngroups} query groups "
                       f"({t_groups:.1f} s); extrapolated x{ngroups // groups} groups, x{cfg.heads} heads; "
                       "forward only, float64 numpy"}
+
+
+def oracle_baselines(args):
+    """The float64 oracle timed in full on configs 1, 2, 3 and 5 (forward for 1 and 2,
+    forward + backward for 3 and 5), tree included, on this host's cores; one JSON line each."""
+    import numpy as np
+
+    from oracle import bsa as ob
+    from oracle.tree import build_ball_tree
+    from workloads import CONFIGS, make_inputs, make_points
+
+    cores = len(os.sched_getaffinity(0))
+    for cid in (1, 2, 5, 3):
+        cfg = CONFIGS[cid]
+        pts = make_points(cfg)
+        inp = make_inputs(cfg, layout="ball", with_grad=cfg.passes == "fwdbwd")
+        P = ob.Params(ball=cfg.ball, cmp_block=cfg.cmp_block, slc_block=cfg.slc_block, topk=cfg.topk,
+                      group=cfg.group)
+        t0 = time.perf_counter()
+        valid = np.stack([build_ball_tree(pts[b], cfg.n_pad) >= 0 for b in range(cfg.batch)])
+        t_tree = time.perf_counter() - t0
+        args_ = (inp["q"], inp["k"], inp["v"], valid, inp["gate"], inp["phi_k"], inp["phi_v"], P)
+        t0 = time.perf_counter()
+        fwd = ob.forward(*args_)
+        t_fwd = time.perf_counter() - t0
+        t_bwd = 0.0
+        if cfg.passes == "fwdbwd":
+            t0 = time.perf_counter()
+            ob.backward(*args_, fwd, inp["do"])
+            t_bwd = time.perf_counter() - t0
+        total = t_tree + t_fwd + t_bwd
+        print(json.dumps({"config": cid, "workload": cfg.name, "passes": cfg.passes, "cores": cores,
+                          "tree_s": round(t_tree, 2), "forward_s": round(t_fwd, 2), "backward_s": round(t_bwd, 2),
+                          "points_per_s": round(cfg.batch * cfg.n_real / total, 1), "kind": "oracle, float64 numpy"}),
+              flush=True)
 
 
 def sweep(args):
@@ -722,6 +759,9 @@ def main():
         return
     if args.summarize_counters:
         summarize_counters(args)
+        return
+    if args.oracle_baselines:
+        oracle_baselines(args)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the multi-GPU sharding is a design "

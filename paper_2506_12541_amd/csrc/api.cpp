@@ -609,10 +609,21 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   A.lsec_ws = (float*)(w + W.lsec);
   if (D.g == 1)
     A.s1 = slc1_ws(D, w, W.pk, W.pv, W.pkt, W.pvt, W.hist, W.seg_s, W.seg_e, W.dqpart, D.store_lse ? (size_t)-1 : W.ml);
-  // after the dense dK/dV passes, the dQ passes run on the auxiliary stream while the
-  // compression and selection dK/dV passes run on the caller's
+  // Schedule over the two streams (with one stream the same order runs on `st`): the row
+  // terms and the ball and compressed dK/dV passes first, alone; then the dQ chain (ball
+  // writes, compressed and selection add) on the auxiliary stream beside the MLP backward
+  // and the selection dK/dV pass on the caller's. (Running the selection and MLP passes
+  // beside the compressed dK/dV pass instead gave the same step time: the kernels do not
+  // share CUs well, and the compressed pass's own time then includes the sharing.)
   AuxJoin joiner(aux, st);
-  BSA_TRY(bsa::launch_attn_bwd(D, A, st, aux.s, aux.fork), "attention backward");
+  BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::prep, st), "backward row terms");
+  BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::kv_ball, st), "ball dK/dV");
+  BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::kv_cmp, st), "compressed dK/dV");
+  if (aux.s != st && (hipEventRecord(aux.fork, st) != hipSuccess || hipStreamWaitEvent(aux.s, aux.fork, 0) != hipSuccess))
+    return fail(BSA_ERR_HIP, "forking the auxiliary stream failed");
+  BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::dq_ball, aux.s), "ball dQ");
+  BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::dq_cmp, aux.s), "compressed dQ");
+  if (D.g != 1) BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::dq_slc, aux.s), "selection dQ");
   bsa::MlpBwdWs mw{(float*)(w + W.dpre), (float*)(w + W.pw1), (float*)(w + W.psm), (void*)(w + W.w1lp),
                    W.mlp_chunks, W.mlp_chunks_small, (void*)(w + W.dplp)};
   bsa::Mlp mk{}, mv{};
@@ -629,12 +640,15 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   BSA_PHASE("bwd.mlp", st, e = bsa::launch_compress_bwd(D, v, valid, mv, saved->hid_v, A.dvc, dv, gv, mw, st));
   BSA_TRY(e, "compression backward V");
   const bsa::Slc1Ws S1 = slc1_ws(D, w, W.pk, W.pv, W.pkt, W.pvt, W.hist, W.seg_s, W.seg_e, W.dqpart, (size_t)-1);
-  if (D.g == 1)
+  if (D.g == 1) {
     BSA_TRY(bsa::launch_slc1_bwd(D, q, k, v, d_o, valid, saved->sel_idx, (const float4*)A.terms + 2 * D.rows(), S1,
                                  dk, dv, st),
             "per-token selection backward");
-  else
-    BSA_TRY(bsa::launch_slc_csr(D, A, st), "selection backward");
+  } else {
+    const uint32_t* slc_groups = nullptr;
+    BSA_TRY(bsa::launch_slc_csr(D, A, st, &slc_groups), "selection lists");
+    BSA_TRY(bsa::launch_slc_kv(D, A, slc_groups, st), "selection dK/dV");
+  }
   s = joiner.join();
   if (s != BSA_OK) return s;
   if (D.g == 1) {   // the dQ parts of the per-token selection, after the dQ chain

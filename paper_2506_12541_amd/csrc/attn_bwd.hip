@@ -1254,141 +1254,143 @@ void launch_bwd_kv(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v
                        H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
 }
 
+// The backward pass in stages; bsa_backward orders them across its two streams (the
+// stages' buffer dependencies are listed with BwdStage in kernels.hpp).
 template <typename T, int HD>
-hipError_t bwd_impl(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t st_q, hipEvent_t fork) {
+hipError_t bwd_stage_impl(const Dims& D, const BwdArgs& A, BwdStage stage, hipStream_t st) {
   const long long rows = D.rows();
   const float sl2 = D.scale * kLog2e;
   const int nct = D.N / D.l;
   // compressed tokens (and the coarse queries of Eq. 15) in the storage type, as the
-  // forward pass consumed them
-  const T* kc = (const T*)A.kc_lp;
-  const T* vc = (const T*)A.vc_lp;
-  const T* qcl = nullptr;
-  if (D.bf16) {
-    const long long n = D.cmp_rows() * HD;
-    hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.kcmp, n, (T*)A.kc_lp);
-    hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.vcmp, n, (T*)A.vc_lp);
-    if (D.gcmp) {
-      hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.qcmp, n, (T*)A.qc_lp);
-      qcl = (const T*)A.qc_lp;
-    }
-  } else {
-    kc = (const T*)A.kcmp;
-    vc = (const T*)A.vcmp;
-    qcl = (const T*)A.qcmp;
-  }
-  // store_lse = 0: each branch's log-sum-exp rows are recomputed by its forward kernel
-  // without the value products (the same tiles and order, so they equal the stored ones)
-  const float* lse = A.lse;
-  if (!D.store_lse) {
-    hipError_t e = hipSuccess;
-    BSA_PHASE("bwd.lse", st, {
-      e = launch_ball_fwd(D, A.q, A.k, A.v, A.valid, nullptr, A.lse_ws, st);
-      if (e == hipSuccess && D.gcmp) {
-        e = launch_cmp_coarse_fwd(D, qcl, kc, vc, A.valid ? A.cvalid : nullptr, nullptr, A.lsec_ws, st);
-        if (e == hipSuccess) e = launch_expand_coarse(D, nullptr, A.lsec_ws, A.valid, nullptr, A.lse_ws + rows, st);
-      } else if (e == hipSuccess) {
-        e = launch_cmp_fwd(D, A.q, kc, vc, A.valid, A.valid ? A.cvalid : nullptr, nullptr, A.lse_ws + rows, st);
-      }
-      if (e == hipSuccess)
-        e = D.g == 1 ? launch_slc1_fwd(D, A.q, A.k, A.v, A.valid, A.sel, A.s1, nullptr, A.lse_ws + 2 * rows, st)
-                     : launch_slc_fwd(D, A.q, A.k, A.v, A.valid, A.sel, nullptr, A.lse_ws + 2 * rows, st);
-    });
-    if (e != hipSuccess) return e;
-    lse = A.lse_ws;
-  }
-  // per-branch row sums and the gate gradient
-  BSA_PHASE("bwd.gate", st, {
-  hipLaunchKernelGGL(gate_bwd_rows_kernel<T>, dim3((unsigned)((rows * 8 + 255) / 256)), dim3(256), 0, st, (const T*)A.dout,
-                     (const T*)A.o_branch, A.o_cmp, rows, HD, lse, A.gate, D.H, D.N, A.R, (float4*)A.terms);
-  hipLaunchKernelGGL(gate_bwd_kernel, dim3((D.B * D.N + 255) / 256), dim3(256), 0, st, A.R, A.gate, A.valid, D.B, D.H,
-                     D.N, A.dgate);
-  });
+  // forward pass consumed them (cast in the prep stage)
+  const T* kc = D.bf16 ? (const T*)A.kc_lp : (const T*)A.kcmp;
+  const T* vc = D.bf16 ? (const T*)A.vc_lp : (const T*)A.vcmp;
+  const T* qcl = D.bf16 ? (const T*)A.qc_lp : (const T*)A.qcmp;
   const float4* t4 = (const float4*)A.terms;
   QTerms qball{t4};
   QTerms qcmp{t4 + rows};
   QTerms qslc{t4 + 2 * rows};
+  QTerms qcoarse{(const float4*)A.t4c};
   const T* q = (const T*)A.q;
   const T* k = (const T*)A.k;
   const T* v = (const T*)A.v;
   const T* dout = (const T*)A.dout;
-  // ---- dK, dV of the ball branch (written) ----
-  BSA_PHASE("bwd.kv_ball", st, {
-  if (D.m >= 128)
-    (launch_bwd_kv<T, HD, 4, true>)(dim3(D.N / 128, 1, D.B * D.H), st, q, k, v, dout, A.valid, qball, D.H, D.N, D.N,
-                                  D.m, 1, sl2, D.scale, A.dk, A.dv);
-  else
-    (launch_bwd_kv<T, HD, 2, true>)(dim3(D.N / 64, 1, D.B * D.H), st, q, k, v, dout, A.valid, qball, D.H, D.N, D.N,
-                                  D.m, 1, sl2, D.scale, A.dk, A.dv);
-  });
-  // group compression: the coarse queries' dO and row terms
-  const T* docl = nullptr;
-  QTerms qcoarse{(const float4*)A.t4c};
-  if (D.gcmp) {
-    const long long n = D.cmp_rows() * HD;
-    hipLaunchKernelGGL(coarse_rows_bwd_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, dout,
-                       t4 + rows, A.ocmp, A.valid, D.H, D.N, D.l, HD, D.cmp_rows(), (T*)A.doc, (float4*)A.t4c);
-    docl = (const T*)A.doc;
-  }
-  // ---- dK^, dV^ of the compressed branch: chunked partials, then a fixed-order sum ----
-  {
-    const int nq = D.gcmp ? nct : D.N;   // query rows: tokens, or coarse queries (Eq. 15)
-    const int nch = nq / kCmpChunks >= kQT ? kCmpChunks : 1;
-    BSA_PHASE("bwd.kv_cmp", st,
-    (launch_bwd_kv<T, HD, 4, false>)(dim3((nct + 127) / 128, nch, D.B * D.H), st, D.gcmp ? qcl : q, kc, vc,
-                                   D.gcmp ? docl : dout, A.valid ? A.cvalid : nullptr, D.gcmp ? qcoarse : qcmp,
-                                   D.H, nq, nct, D.m, nch, sl2, D.scale, A.dkc_part, A.dvc_part));
-    const long long n = D.cmp_rows() * HD;
-    hipLaunchKernelGGL(sum_chunks_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.dkc_part, nch, n,
-                       A.dkc);
-    hipLaunchKernelGGL(sum_chunks_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.dvc_part, nch, n,
-                       A.dvc);
-  }
-  // ---- dQ: ball (write), compressed (add), selection (add), on st_q ----
-  if (st_q != st) {
-    hipError_t e = hipEventRecord(fork, st);
-    if (e == hipSuccess) e = hipStreamWaitEvent(st_q, fork, 0);
-    if (e != hipSuccess) return e;
-  }
-  {
-  hipStream_t st_main = st;
-  hipStream_t st = st_q;   // the dQ chain below
-  BSA_PHASE("bwd.dq_ball", st, {
-  if (D.m >= 128)
-    (launch_bwd_q<T, HD, 2, true, false>)(dim3(D.N / 128, D.H, D.B), st, q, k, v, dout, A.valid, qball, D.H, D.N,
-                                          D.N, D.m, sl2, D.scale, A.dq);
-  else
-    (launch_bwd_q<T, HD, 1, true, false>)(dim3(D.N / 64, D.H, D.B), st, q, k, v, dout, A.valid, qball, D.H, D.N,
-                                          D.N, D.m, sl2, D.scale, A.dq);
-  });
-  BSA_PHASE("bwd.dq_cmp", st, {
-  if (!D.gcmp && D.N % 128 == 0)
-    (launch_bwd_q<T, HD, 2, false, true>)(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, dout,
-                                          A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq);
-  else if (!D.gcmp)   // 64 token slots
-    (launch_bwd_q<T, HD, 1, false, true>)(dim3(D.N / 64, D.H, D.B), st, q, kc, vc, dout,
-                                          A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale, A.dq);
-  else if (nct % 128 == 0)   // gradient of the coarse queries (written); the caller maps it to dQ
-    (launch_bwd_q<T, HD, 2, false, false>)(dim3(nct / 128, D.H, D.B), st, qcl, kc, vc, docl,
-                                           A.valid ? A.cvalid : nullptr, qcoarse, D.H, nct, nct, D.m, sl2, D.scale,
-                                           A.dqc);
-  else
-    (launch_bwd_q<T, HD, 1, false, false>)(dim3(nct / 64, D.H, D.B), st, qcl, kc, vc, docl,
-                                           A.valid ? A.cvalid : nullptr, qcoarse, D.H, nct, nct, D.m, sl2, D.scale,
-                                           A.dqc);
-  });
-  if (D.g != 1)   // per-token selection adds its dQ parts after the streams join
-  BSA_PHASE("bwd.dq_slc", st, {
-  if constexpr (sizeof(T) == 2) {
-    constexpr int NW = 2;
-    hipLaunchKernelGGL((slc_bwd_q_dma_kernel<HD, NW>), dim3(D.N / (16 * NW), D.H, D.B), dim3(64 * NW), 0, st, q, k, v,
-                       dout, A.valid, A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq);
-  } else {
-    hipLaunchKernelGGL((slc_bwd_q_kernel<T, HD>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, q, k, v, dout, A.valid,
-                       A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq);
-  }
-  });
-  (void)st_main;
+  const T* docl = (const T*)A.doc;
+  switch (stage) {
+    case BwdStage::prep: {
+      if (D.bf16) {
+        const long long n = D.cmp_rows() * HD;
+        hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.kcmp, n,
+                           (T*)A.kc_lp);
+        hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.vcmp, n,
+                           (T*)A.vc_lp);
+        if (D.gcmp)
+          hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.qcmp, n,
+                             (T*)A.qc_lp);
+      }
+      // store_lse = 0: each branch's log-sum-exp rows are recomputed by its forward kernel
+      // without the value products (the same tiles and order, so they equal the stored ones)
+      const float* lse = A.lse;
+      if (!D.store_lse) {
+        hipError_t e = hipSuccess;
+        BSA_PHASE("bwd.lse", st, {
+          e = launch_ball_fwd(D, A.q, A.k, A.v, A.valid, nullptr, A.lse_ws, st);
+          if (e == hipSuccess && D.gcmp) {
+            e = launch_cmp_coarse_fwd(D, qcl, kc, vc, A.valid ? A.cvalid : nullptr, nullptr, A.lsec_ws, st);
+            if (e == hipSuccess)
+              e = launch_expand_coarse(D, nullptr, A.lsec_ws, A.valid, nullptr, A.lse_ws + rows, st);
+          } else if (e == hipSuccess) {
+            e = launch_cmp_fwd(D, A.q, kc, vc, A.valid, A.valid ? A.cvalid : nullptr, nullptr, A.lse_ws + rows, st);
+          }
+          if (e == hipSuccess)
+            e = D.g == 1 ? launch_slc1_fwd(D, A.q, A.k, A.v, A.valid, A.sel, A.s1, nullptr, A.lse_ws + 2 * rows, st)
+                         : launch_slc_fwd(D, A.q, A.k, A.v, A.valid, A.sel, nullptr, A.lse_ws + 2 * rows, st);
+        });
+        if (e != hipSuccess) return e;
+        lse = A.lse_ws;
+      }
+      // per-branch row sums, the packed row terms and the gate gradient
+      BSA_PHASE("bwd.gate", st, {
+        hipLaunchKernelGGL(gate_bwd_rows_kernel<T>, dim3((unsigned)((rows * 8 + 255) / 256)), dim3(256), 0, st,
+                           dout, (const T*)A.o_branch, A.o_cmp, rows, HD, lse, A.gate, D.H, D.N, A.R,
+                           (float4*)A.terms);
+        hipLaunchKernelGGL(gate_bwd_kernel, dim3((D.B * D.N + 255) / 256), dim3(256), 0, st, A.R, A.gate, A.valid,
+                           D.B, D.H, D.N, A.dgate);
+      });
+      // group compression: the coarse queries' dO and row terms
+      if (D.gcmp) {
+        const long long n = D.cmp_rows() * HD;
+        hipLaunchKernelGGL(coarse_rows_bwd_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, dout,
+                           t4 + rows, A.ocmp, A.valid, D.H, D.N, D.l, HD, D.cmp_rows(), (T*)A.doc, (float4*)A.t4c);
+      }
+      break;
+    }
+    case BwdStage::kv_ball:   // dK, dV of the ball branch (written)
+      BSA_PHASE("bwd.kv_ball", st, {
+        if (D.m >= 128)
+          (launch_bwd_kv<T, HD, 4, true>)(dim3(D.N / 128, 1, D.B * D.H), st, q, k, v, dout, A.valid, qball, D.H,
+                                        D.N, D.N, D.m, 1, sl2, D.scale, A.dk, A.dv);
+        else
+          (launch_bwd_kv<T, HD, 2, true>)(dim3(D.N / 64, 1, D.B * D.H), st, q, k, v, dout, A.valid, qball, D.H,
+                                        D.N, D.N, D.m, 1, sl2, D.scale, A.dk, A.dv);
+      });
+      break;
+    case BwdStage::kv_cmp: {   // dK^, dV^ of the compressed branch: chunked partials, fixed-order sum
+      const int nq = D.gcmp ? nct : D.N;   // query rows: tokens, or coarse queries (Eq. 15)
+      const int nch = nq / kCmpChunks >= kQT ? kCmpChunks : 1;
+      BSA_PHASE("bwd.kv_cmp", st,
+      (launch_bwd_kv<T, HD, 4, false>)(dim3((nct + 127) / 128, nch, D.B * D.H), st, D.gcmp ? qcl : q, kc, vc,
+                                     D.gcmp ? docl : dout, A.valid ? A.cvalid : nullptr, D.gcmp ? qcoarse : qcmp,
+                                     D.H, nq, nct, D.m, nch, sl2, D.scale, A.dkc_part, A.dvc_part));
+      const long long n = D.cmp_rows() * HD;
+      hipLaunchKernelGGL(sum_chunks_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.dkc_part, nch, n,
+                         A.dkc);
+      hipLaunchKernelGGL(sum_chunks_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.dvc_part, nch, n,
+                         A.dvc);
+      break;
+    }
+    case BwdStage::dq_ball:   // dQ of the ball branch (written)
+      BSA_PHASE("bwd.dq_ball", st, {
+        if (D.m >= 128)
+          (launch_bwd_q<T, HD, 2, true, false>)(dim3(D.N / 128, D.H, D.B), st, q, k, v, dout, A.valid, qball, D.H,
+                                                D.N, D.N, D.m, sl2, D.scale, A.dq);
+        else
+          (launch_bwd_q<T, HD, 1, true, false>)(dim3(D.N / 64, D.H, D.B), st, q, k, v, dout, A.valid, qball, D.H,
+                                                D.N, D.N, D.m, sl2, D.scale, A.dq);
+      });
+      break;
+    case BwdStage::dq_cmp:   // dQ of the compressed branch (added), or the coarse queries' (written)
+      BSA_PHASE("bwd.dq_cmp", st, {
+        if (!D.gcmp && D.N % 128 == 0)
+          (launch_bwd_q<T, HD, 2, false, true>)(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, dout,
+                                                A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale,
+                                                A.dq);
+        else if (!D.gcmp)   // 64 token slots
+          (launch_bwd_q<T, HD, 1, false, true>)(dim3(D.N / 64, D.H, D.B), st, q, kc, vc, dout,
+                                                A.valid ? A.cvalid : nullptr, qcmp, D.H, D.N, nct, D.m, sl2, D.scale,
+                                                A.dq);
+        else if (nct % 128 == 0)
+          (launch_bwd_q<T, HD, 2, false, false>)(dim3(nct / 128, D.H, D.B), st, qcl, kc, vc, docl,
+                                                 A.valid ? A.cvalid : nullptr, qcoarse, D.H, nct, nct, D.m, sl2,
+                                                 D.scale, A.dqc);
+        else
+          (launch_bwd_q<T, HD, 1, false, false>)(dim3(nct / 64, D.H, D.B), st, qcl, kc, vc, docl,
+                                                 A.valid ? A.cvalid : nullptr, qcoarse, D.H, nct, nct, D.m, sl2,
+                                                 D.scale, A.dqc);
+      });
+      break;
+    case BwdStage::dq_slc:   // dQ of the selection branch (added); groups of g >= 8 only
+      BSA_PHASE("bwd.dq_slc", st, {
+        if constexpr (sizeof(T) == 2) {
+          constexpr int NW = 2;
+          hipLaunchKernelGGL((slc_bwd_q_dma_kernel<HD, NW>), dim3(D.N / (16 * NW), D.H, D.B), dim3(64 * NW), 0, st,
+                             q, k, v, dout, A.valid, A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq);
+        } else {
+          hipLaunchKernelGGL((slc_bwd_q_kernel<T, HD>), dim3(D.N / 64, D.H, D.B), dim3(256), 0, st, q, k, v, dout,
+                             A.valid, A.sel, qslc, D.H, D.N, D.ls, D.k, D.g, sl2, D.scale, A.dq);
+        }
+      });
+      break;
   }
   return hipGetLastError();
 }
@@ -1661,11 +1663,11 @@ hipError_t slc_kv_impl(const Dims& D, const BwdArgs& A, hipStream_t st) {
 
 }  // namespace
 
-hipError_t launch_attn_bwd(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t st_q, hipEvent_t fork) {
-  return BSA_DISPATCH(bwd_impl, D, A, st, st_q, fork);
+hipError_t launch_bwd_stage(const Dims& D, const BwdArgs& A, BwdStage stage, hipStream_t st) {
+  return BSA_DISPATCH(bwd_stage_impl, D, A, stage, st);
 }
 
-hipError_t launch_slc_csr(const Dims& D, const BwdArgs& A, hipStream_t st) {
+hipError_t launch_slc_csr(const Dims& D, const BwdArgs& A, hipStream_t st, const uint32_t** groups_out) {
   const long long total = (long long)D.B * D.H * (D.N / D.g) * D.k;
   const int nblk = D.N / D.ls;
   const long long nseg = (long long)D.B * D.H * nblk;
@@ -1685,8 +1687,13 @@ hipError_t launch_slc_csr(const Dims& D, const BwdArgs& A, hipStream_t st) {
   hipLaunchKernelGGL(seg_bounds_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, kout, total, sentinel,
                      A.seg_start, A.seg_end);
   timing_end(tid, st);
+  *groups_out = vout;
+  return hipGetLastError();
+}
+
+hipError_t launch_slc_kv(const Dims& D, const BwdArgs& A, const uint32_t* groups, hipStream_t st) {
   BwdArgs A2 = A;
-  A2.pair_groups = vout;
+  A2.pair_groups = groups;
   hipError_t r;
   BSA_PHASE("bwd.slc_kv", st, r = BSA_DISPATCH(slc_kv_impl, D, A2, st));
   return r;

@@ -116,12 +116,23 @@ struct BwdArgs {
   Slc1Ws s1;                     // per-token selection buffers (g = 1; ml holds 2 floats per pair)
 };
 
-// attn_bwd.hip
-// The dQ passes run on st_q (may equal st): after the ball and compressed dK/dV passes are
-// enqueued on st, `fork` is recorded there and st_q waits for it; the caller joins st_q
-// back into st.
-hipError_t launch_attn_bwd(const Dims& D, const BwdArgs& A, hipStream_t st, hipStream_t st_q, hipEvent_t fork);
-hipError_t launch_slc_csr(const Dims& D, const BwdArgs& A, hipStream_t st);
+// attn_bwd.hip: the backward pass in stages. What each stage reads and writes:
+//   prep     casts K^/V^ (and the coarse queries) to the storage type; recomputes the LSE
+//            rows if not stored; writes R, the packed row terms and dgate (and the coarse
+//            queries' dO and terms under group compression). Every later stage needs it.
+//   kv_ball  writes dK, dV (the first writer of both).
+//   kv_cmp   writes dK^, dV^ (dkc, dvc).
+//   dq_ball  writes dQ (the first writer).
+//   dq_cmp   adds into dQ (group compression: writes the coarse-query gradient instead).
+//   dq_slc   adds into dQ (g >= 8).
+// launch_slc_csr inverts the selection lists (no dependency but prep); launch_slc_kv adds
+// into dK, dV; launch_compress_bwd (compress.hip) adds dK^/dV^'s token gradients into dK,
+// dV. Stages that add into the same tensor must be ordered after its first writer and
+// after each other.
+enum class BwdStage { prep, kv_ball, kv_cmp, dq_ball, dq_cmp, dq_slc };
+hipError_t launch_bwd_stage(const Dims& D, const BwdArgs& A, BwdStage stage, hipStream_t st);
+hipError_t launch_slc_csr(const Dims& D, const BwdArgs& A, hipStream_t st, const uint32_t** groups_out);
+hipError_t launch_slc_kv(const Dims& D, const BwdArgs& A, const uint32_t* groups, hipStream_t st);
 
 // compress.hip: backward of phi (dK^ -> token gradients added into dx, weight gradients)
 struct MlpBwdWs {
