@@ -637,8 +637,8 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
   const float4* th = qt.t4 + (size_t)bh * N;
 
   auto issue = [&](int t0, bf16_t* qd, bf16_t* dd, float* txd, float* tzd) {
-    dma_tile<HD, kQT, NW>(qd, qh, t0, N, wid, lane);
-    dma_tile<HD, kQT, NW>(dd, dh, t0, N, wid, lane);
+    dma_tile_full<HD, kQT, NW>(qd, qh + (size_t)t0 * HD, wid, lane);   // query tiles are whole (N % 64 == 0)
+    dma_tile_full<HD, kQT, NW>(dd, dh + (size_t)t0 * HD, wid, lane);
     if (wid == NW - 1) {
       const float* t = reinterpret_cast<const float*>(th + t0 + lane);
       __builtin_amdgcn_global_load_lds(t, txd, 4, 0, 0);
@@ -987,8 +987,8 @@ __global__ void __launch_bounds__(NW * 64) slc_bwd_q_dma_kernel(const bf16_t* q,
       const int e = 2 * t + kb < nsub ? sub[2 * t + kb] : -1;
       const int r0 = e >= 0 ? (e & 0xFFFFFF) : 0;
       bf16_t* base = slot + wid * SLOT + kb * 16 * HD;
-      dma_tile<HD, 16, 1>(base, kh, r0, N, 0, lane);
-      dma_tile<HD, 16, 1>(base + TILE, vh, r0, N, 0, lane);
+      dma_tile_full<HD, 16, 1>(base, kh + (size_t)r0 * HD, 0, lane);
+      dma_tile_full<HD, 16, 1>(base + TILE, vh + (size_t)r0 * HD, 0, lane);
     }
   };
   auto step = [&](int t, const bf16_t* cur, bf16_t* next) {
@@ -1470,6 +1470,8 @@ __global__ void __launch_bounds__(64 * NWV) slc_bwd_kv_dma_kernel(const bf16_t* 
     auto issue = [&](int i, bf16_t* slot) {
       const int qr0 = rows[min(i, cnt - 1)];
       bf16_t* base = slot + wid * SLOT;
+      // an item's 16 rows start at group * g: for g < 16 the last group's tile reaches g rows
+      // past the end (rows clamp; those rows have zero weight)
       dma_tile<HD, 16, 1>(base, qh, qr0, N, 0, lane);
       dma_tile<HD, 16, 1>(base + SL, dh, qr0, N, 0, lane);
       __builtin_amdgcn_global_load_lds(th + min(qr0 + (lane & 15), N - 1), base + 2 * SL, 16, 0, 0);

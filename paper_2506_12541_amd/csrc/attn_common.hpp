@@ -212,6 +212,26 @@ __device__ __forceinline__ void dma_tile(bf16_t* lds, const bf16_t* g, int r0, i
   }
 }
 
+// dma_tile for a tile known to lie inside the matrix: `g` points at the tile's first row.
+// A lane's offset inside the tile depends only on its wave and lane, so the compiler keeps
+// it in a register across tiles; per tile only the scalar base moves (no per-row clamp).
+template <int HD, int ROWS, int NW>
+__device__ __forceinline__ void dma_tile_full(bf16_t* lds, const bf16_t* g, int wid, int lane) {
+  constexpr int CPR = HD / 8;
+  constexpr int NI = ROWS * CPR / 64;
+  static_assert(NI % NW == 0 || NW % NI == 0, "tile / wave split");
+  constexpr int PER = NI >= NW ? NI / NW : 1;
+  if (NI < NW && wid >= NI) return;
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int blk = wid * PER + u;
+    const int idx = blk * 64 + lane;
+    const int row = idx / CPR;
+    const int lc = (idx % CPR) ^ swz<HD>(row);
+    __builtin_amdgcn_global_load_lds(g + (row * HD + 8 * lc), lds + blk * 512, 16, 0, 0);
+  }
+}
+
 // 8 consecutive elements of row x starting at logical chunk lc (an MFMA row fragment).
 template <int HD>
 __device__ __forceinline__ bf16x8 lds_row_chunk(const bf16_t* t, int x, int lc) {
@@ -426,7 +446,7 @@ struct WaveAttn {
       const float mnew = raise ? tmax : mx[qb];
       alpha[qb] = raise ? fast_exp2(mx[qb] - mnew) : 1.0f;
       mx[qb] = mnew;
-      any = any || __builtin_amdgcn_ballot_w64(raise) != 0;
+      any |= __builtin_amdgcn_ballot_w64(raise) != 0;   // no short-circuit: no branch
     }
     return any;
   }

@@ -164,12 +164,17 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q,
       }
       dma_tile<HD, kFT, NW>(kd, kh, t * kFT, nkeys, wid, lane);
       if (threadIdx.x < kFT) okd[threadIdx.x] = okv;
-    } else {
-      dma_tile<HD, kFT, NW>(kd, kh, t * kFT, nkeys, wid, lane);
+    } else {   // whole tiles; a tile past the end reloads the last one
+      dma_tile_full<HD, kFT, NW>(kd, kh + (size_t)(t < nt ? t : nt - 1) * kFT * HD, wid, lane);
     }
   };
   auto issue_v = [&](int t, bf16_t* vd) {
-    if constexpr (!LO) dma_tile<HD, kFT, NW>(vd, vh, t * kFT, nkeys, wid, lane);
+    if constexpr (!LO) {
+      if constexpr (MASK)
+        dma_tile<HD, kFT, NW>(vd, vh, t * kFT, nkeys, wid, lane);
+      else
+        dma_tile_full<HD, kFT, NW>(vd, vh + (size_t)(t < nt ? t : nt - 1) * kFT * HD, wid, lane);
+    }
   };
   WA w;
   w.init();
@@ -390,8 +395,8 @@ __global__ void __launch_bounds__(NW * 64) slc_fwd_dma_kernel(const bf16_t* q, c
       const int e = 2 * t + kb < nsub ? sub[2 * t + kb] : -1;
       const int row = e >= 0 ? (e & 0xFFFFFF) : 0;
       bf16_t* base = slot + wid * SLOT + kb * 16 * HD;
-      dma_tile<HD, 16, 1>(base, kh, row, N, 0, lane);
-      if constexpr (!LO) dma_tile<HD, 16, 1>(base + TILE, vh, row, N, 0, lane);
+      dma_tile_full<HD, 16, 1>(base, kh + (size_t)row * HD, 0, lane);
+      if constexpr (!LO) dma_tile_full<HD, 16, 1>(base + TILE, vh + (size_t)row * HD, 0, lane);
     }
   };
   auto step = [&](int t, const bf16_t* cur, bf16_t* next) {
