@@ -369,7 +369,9 @@ def summarize_counters(args):
                  f"copy (fetch x{ff:.3f}, write x{fw:.3f}). MFMA TFLOP/s executed = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16 /\n"
                  "duration (every MFMA FLOP issued, recomputation included). MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES /\n"
                  "(GRBM_GUI_ACTIVE / 8 XCDs x 256 CUs x 4 SIMDs); clock = GRBM_GUI_ACTIVE / 8 / duration. Instruction\n"
-                 "counts are per dispatch (all waves). Kernels under 0.2% of GPU time are left out.\n\n")
+                 "counts are per dispatch (all waves). Kernels under 0.2% of GPU time are left out. GRBM_GUI_ACTIVE\n"
+                 "spans the dispatch's whole busy window, which for a short kernel includes launch and drain time\n"
+                 "outside its traced duration: clock and MFMA busy are meaningful for kernels of 100 us and more.\n\n")
         cols = ("kernel", "calls", "avg_us", "gpu_time_pct", "fetch_mb", "write_mb", "hbm_gbps",
                 "mfma_tflops_executed", "mfma_busy_pct", "clock_ghz", "valu_insts", "mfma_insts", "lds_insts")
         fh.write("| " + " | ".join(cols) + " |\n|" + "---|" * len(cols) + "\n")
