@@ -319,9 +319,10 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
   __shared__ __attribute__((aligned(16))) uint8_t ok0[KT], ok1[KT];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r = lane & 15, j = lane >> 4;
-  const int b = blockIdx.z, h = blockIdx.y;
+  const dim3 blk = xcd_grouped_block(BALL ? m / (64 * QB) : (int)gridDim.x);
+  const int b = blk.z, h = blk.y;
   const long long bh = (long long)b * H + h;
-  const int q0 = blockIdx.x * (64 * QB);
+  const int q0 = blk.x * (64 * QB);
   const int nkeys = BALL ? m : nkeys_total;
   const int key0 = BALL ? (q0 / m) * m : 0;
   const bf16_t* kh = k + (bh * nkeys_total + key0) * HD;
@@ -618,10 +619,11 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
   __shared__ __attribute__((aligned(16))) float tx0[kQT], tz0[kQT], tx1[kQT], tz1[kQT];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r = lane & 15, j = lane >> 4;
-  const int bh = blockIdx.z;
+  const dim3 blk = xcd_grouped_block(BALL ? m / (NW * 32) : (int)gridDim.x);
+  const int bh = blk.z;
   const int b = bh / H;
-  const int chunk = blockIdx.y;
-  const int key0 = blockIdx.x * (NW * 32);
+  const int chunk = blk.y;
+  const int key0 = blk.x * (NW * 32);
   const int wk0 = key0 + wid * 32;
   int qbeg, qend;
   if (BALL) {

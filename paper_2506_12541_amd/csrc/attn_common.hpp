@@ -183,6 +183,24 @@ struct TileIO {
 // 128-wide rows (f32 rows of 64) are read as row fragments: 16 consecutive rows on
 // distinct banks with c ^ (x mod 16). Wider rows are only read by transpose reads; for
 // them chunk pairs of 8 consecutive rows land on distinct banks with c ^ 2 (x mod 8).
+// Workgroups are dealt to the 8 XCDs round-robin by linear id, and each XCD has its own
+// L2. When runs of `per` consecutive x-tiles (within one y, z) read the same rows (the
+// query tiles of one ball; every key tile of one query chunk; every query tile of one
+// head's compressed keys), the grid is renumbered so that each XCD takes whole runs, in
+// order: the shared rows then enter that XCD's L2 once instead of once per XCD. The
+// renumbering is a bijection of the grid; it needs gridDim.x % per == 0 and the run count
+// to be a multiple of 8, else the grid is kept.
+__device__ __forceinline__ dim3 xcd_grouped_block(int per) {
+  constexpr unsigned kXcds = 8;
+  const unsigned nx = gridDim.x, ny = gridDim.y;
+  const unsigned runs = nx * ny * gridDim.z / (unsigned)max(per, 1);
+  if (per <= 1 || nx % (unsigned)per != 0 || runs % kXcds != 0) return dim3(blockIdx.x, blockIdx.y, blockIdx.z);
+  const unsigned lin = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
+  const unsigned slot = lin / kXcds;
+  const unsigned l = ((lin % kXcds) * (runs / kXcds) + slot / per) * per + slot % per;
+  return dim3(l % nx, (l / nx) % ny, l / (nx * ny));
+}
+
 template <int HD>
 __device__ __forceinline__ int swz(int x) {
   static_assert(HD == 32 || HD == 64 || HD == 128 || HD >= 256, "tile width");

@@ -140,9 +140,10 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q,
   __shared__ uint8_t ok0[kFT], ok1[kFT];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r = lane & 15, j = lane >> 4;
-  const int b = blockIdx.z, h = blockIdx.y;
+  const dim3 blk = xcd_grouped_block(BALL ? m / (16 * QB * NW) : (int)gridDim.x);
+  const int b = blk.z, h = blk.y;
   const long long bh = (long long)b * H + h;
-  const int q0 = blockIdx.x * (16 * QB * NW);
+  const int q0 = blk.x * (16 * QB * NW);
   const int nkeys = BALL ? m : nkeys_total;
   const int key0 = BALL ? (q0 / m) * m : 0;
   const bf16_t* kh = k + (bh * nkeys_total + key0) * HD;
