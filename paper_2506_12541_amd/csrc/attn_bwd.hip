@@ -937,9 +937,10 @@ __global__ void __launch_bounds__(NW * 64) slc_bwd_q_dma_kernel(const bf16_t* q,
   __shared__ uint32_t okm_all[NW][kMaxSub];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r = lane & 15, j = lane >> 4;
-  const int b = blockIdx.z, h = blockIdx.y;
+  const dim3 blk = xcd_grouped_block((int)gridDim.x);   // one head's groups per XCD run
+  const int b = blk.z, h = blk.y;
   const long long bh = (long long)b * H + h;
-  const int wq0 = (blockIdx.x * NW + wid) * 16;
+  const int wq0 = (blk.x * NW + wid) * 16;
   const int G = g >= 16 ? 1 : 16 / g;
   const int p0 = wq0 / g;
   const int my_gi = g >= 16 ? 0 : r / g;
@@ -1594,7 +1595,7 @@ __global__ void __launch_bounds__(64 * NWV) slc_bwd_kv_dma_kernel(const bf16_t* 
     }
   };
   if constexpr (NWV == 1) {
-    block(blockIdx.x);
+    block(xcd_grouped_block(N / ls).x);   // one head's blocks per XCD run
   } else {
     // persistent workgroups: each takes the blocks blockIdx.x + gridDim.x * t, reads their
     // item counts together, and walks the ones of this launch's size class in turn

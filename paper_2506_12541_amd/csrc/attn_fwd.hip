@@ -353,9 +353,10 @@ __global__ void __launch_bounds__(NW * 64) slc_fwd_dma_kernel(const bf16_t* q, c
   __shared__ uint32_t okm_all[NW][kMaxSub];     // bit t: key t of the sub-block is a real token
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int r = lane & 15, j = lane >> 4;
-  const int b = blockIdx.z, h = blockIdx.y;
+  const dim3 blk = xcd_grouped_block((int)gridDim.x);   // one head's groups per XCD run
+  const int b = blk.z, h = blk.y;
   const long long bh = (long long)b * H + h;
-  const int wq0 = (blockIdx.x * NW + wid) * 16;
+  const int wq0 = (blk.x * NW + wid) * 16;
   const int G = g >= 16 ? 1 : 16 / g;
   const int p0 = wq0 / g;
   const int my_gi = g >= 16 ? 0 : r / g;
