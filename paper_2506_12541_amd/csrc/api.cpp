@@ -507,7 +507,7 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   BSA_STEP("fwd.compress", (bsa::launch_block_valid(D, valid, saved->cvalid, st) != hipSuccess
                                 ? hipGetLastError()
                                 : bsa::launch_compress_fwd(D, k, valid, mk, saved->kcmp, saved->hid_k, kc_lp,
-                                                           w + W.w1t_k, st) != hipSuccess
+                                                           w + W.w1t_k, st, bsa::cmp_key_scale(D)) != hipSuccess
                                       ? hipGetLastError()
                                       : bsa::launch_compress_fwd(D, v, valid, mv, saved->vcmp, saved->hid_v, vc_lp,
                                                                  w + W.w1t_v, st)),

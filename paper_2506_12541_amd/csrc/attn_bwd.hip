@@ -31,7 +31,8 @@ __device__ __forceinline__ float lse_log2(float lse) { return lse == -__builtin_
 // ---- gate backward: R_b = rowsum(dO * o_b) per (b,h,n); dgamma_b = s'(gamma_b) sum_h R_b ----
 // 8 lanes per row, each lane a 16-byte piece per tensor; partial sums reduced by shuffles.
 // The same pass packs each query row's terms for the attention passes (16 bytes per row
-// and branch; the layout QTerms describes).
+// and branch; the layout QTerms describes). In bf16 layers the compressed branch's first
+// term is stored negated: its passes start each score MFMA from it (prescaled keys).
 template <typename T>
 __global__ void gate_bwd_rows_kernel(const T* dout, const T* ob, const float* oc, long long rows, int hd,
                                      const float* lse, const float* gate, int H, int N, float* R, float4* terms) {
@@ -75,7 +76,8 @@ __global__ void gate_bwd_rows_kernel(const T* dout, const T* ob, const float* oc
       R[br * rows + row] = acc[br];
       const float sg = sigmoidf(gate[(b * N + n) * 3 + br]);
       const float l2 = lse_log2(lse[br * rows + row]);
-      terms[br * rows + row] = make_float4(l2 - log2f(sg), sg, acc[br], l2);
+      const float x = l2 - log2f(sg);
+      terms[br * rows + row] = make_float4(sizeof(T) == 2 && br == 1 ? -x : x, sg, acc[br], l2);
     }
   }
 }
@@ -128,13 +130,13 @@ __global__ void coarse_rows_bwd_kernel(const T* dout, const float4* t4b, const f
   doc[cr * hd + col] = dr;
   float dd = to_f32<T>(dr) * oc[cr * hd + col];
   for (int off = hd / 2; off > 0; off >>= 1) dd += __shfl_xor(dd, off, 64);
-  if (col == 0) t4c[cr] = make_float4(l2, 1.f, dd, l2);
+  if (col == 0) t4c[cr] = make_float4(sizeof(T) == 2 ? -l2 : l2, 1.f, dd, l2);   // negated in bf16, as above
 }
 
 template <typename T>
-__global__ void cast_kernel(const float* x, long long n, T* y) {
+__global__ void cast_kernel(const float* x, long long n, float sc, T* y) {
   long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) y[i] = from_f32<T>(x[i]);
+  if (i < n) y[i] = from_f32<T>(x[i] * sc);
 }
 
 __global__ void sum_chunks_kernel(const float* part, int nchunks, long long n, float* out) {
@@ -161,6 +163,8 @@ __device__ __forceinline__ bf16x8 neg_chunk(bf16x8 x) {
 // row's dO (the branch gate sigmoid(gamma_b), or 1 for rows whose dO is already scaled),
 // R = rowsum(dO * o_b) for the unscaled dO, so exp2(S log2e - x) is s P and the softmax
 // gradient is s P (dO V^T - R). Rows without keys carry +inf in x and w. [B, H, N] float4.
+// The compressed branch of bf16 layers stores -x instead (its keys come prescaled, so the
+// score MFMA starting from -x yields the exponent S log2e - x directly).
 struct QTerms {
   const float4* t4;
 };
@@ -305,7 +309,9 @@ __global__ void __launch_bounds__(256) dense_bwd_q_kernel(const T* q, const T* k
 // distinct objects, loop unrolled by two) and filled by direct global->LDS loads; the K^T
 // operand of the dQ product comes from transpose reads of the row-major K tile.
 // MASK = false: every key is real and the key count is a multiple of the tile.
-template <int HD, int QB, bool BALL, bool ADD, bool MASK = true>
+// PS: prescaled keys (the compressed tokens of bf16 layers): scores start from the stored
+// -x and come out as exponents; dQ = dS K takes 1/log2(e) for the keys' extra factor.
+template <int HD, int QB, bool BALL, bool ADD, bool MASK = true, bool PS = false>
 __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
                                                               const bf16_t* dout, const uint8_t* kvalid_all,
                                                               QTerms qt, int H, int N, int nkeys_total, int m,
@@ -347,7 +353,7 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
   // df holds -dO and rr the lane's R, so the dP product yields R - dO V^T
   CT qf[QB][NCH], df[QB][NCH];
   float l2[QB];
-  f32x4 rr[QB], acc[QB][DB];
+  f32x4 rr[QB], acc[QB][DB], s0[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const long long row = bh * N + wq0 + 16 * qb + r;
@@ -356,9 +362,10 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
       qf[qb][c] = load_chunk(q + row * HD + 32 * c + 8 * j);
       df[qb][c] = neg_chunk(load_chunk(dout + row * HD + 32 * c + 8 * j));
     }
-    const float4 t = qt.t4[row];   // log2 LSE - log2 s, s, R
+    const float4 t = qt.t4[row];   // log2 LSE - log2 s (negated with PS), s, R
     l2[qb] = t.x;
     rr[qb] = f32x4{t.z, t.z, t.z, t.z};
+    s0[qb] = PS ? f32x4{t.x, t.x, t.x, t.x} : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int db = 0; db < DB; ++db) acc[qb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
@@ -372,7 +379,8 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
     // key validity of the rows 4j+i of each key block, one 32-bit word per block
     uint32_t okw[KB];
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) okw[kb] = all_ok ? 0x01010101u : *reinterpret_cast<const uint32_t*>(&ok[kb * 16 + 4 * j]);
+    for (int kb = 0; kb < KB; ++kb)
+      okw[kb] = all_ok ? 0x01010101u : *reinterpret_cast<const uint32_t*>(&ok[kb * 16 + 4 * j]);
     f32x4 sv[QB][KB], dp[QB][KB];
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
@@ -382,7 +390,7 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
         CT av = lds_row_chunk<HD>(vt, kb * 16 + r, 4 * c + j);
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
-          sv[qb][kb] = mma(ak, qf[qb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sv[qb][kb]);
+          sv[qb][kb] = mma(ak, qf[qb][c], c == 0 ? s0[qb] : sv[qb][kb]);
           dp[qb][kb] = mma(av, df[qb][c], c == 0 ? rr[qb] : dp[qb][kb]);
         }
       }
@@ -395,7 +403,7 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float e = fast_exp2(__builtin_fmaf(sv[qb][kb][i], sl2, -l2[qb]));
+          const float e = PS ? fast_exp2(sv[qb][kb][i]) : fast_exp2(__builtin_fmaf(sv[qb][kb][i], sl2, -l2[qb]));
           const float p = !MASK || ((okw[kb] >> (8 * i)) & 1u) ? e : 0.f;
           v8[kb][i] = p * dp[qb][kb][i];
         }
@@ -426,7 +434,7 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
       float* dst = dq + row * HD + 16 * db + 4 * j;
-      f32x4 val = acc[qb][db] * -scale;
+      f32x4 val = acc[qb][db] * (PS ? -scale / sl2 : -scale);
       if (ADD) {
         float4 old = *reinterpret_cast<float4*>(dst);
         val[0] += old.x; val[1] += old.y; val[2] += old.z; val[3] += old.w;
@@ -603,7 +611,9 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
 // global->LDS loads; the transposed operands of the dK^T and dV^T products come from
 // transpose reads of the same row-major tiles.
 // MASK = false: every key of the grid is real and in range (no per-key select).
-template <int HD, int NW, bool BALL, bool MASK = true>
+// PS: prescaled keys (the compressed tokens of bf16 layers): scores start from the stored
+// -x and come out as exponents (dK and dV do not involve the keys).
+template <int HD, int NW, bool BALL, bool MASK = true, bool PS = false>
 __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
                                                                    const bf16_t* dout, const uint8_t* kvalid_all,
                                                                    QTerms qt, int H, int N, int nkeys_total, int m,
@@ -683,7 +693,7 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int qb = 2 * qp + u;
-        lx[u] = *reinterpret_cast<const f32x4*>(&tx[16 * qb + 4 * j]);   // log2 LSE - log2 s
+        lx[u] = *reinterpret_cast<const f32x4*>(&tx[16 * qb + 4 * j]);   // log2 LSE - log2 s (negated with PS)
         const f32x4 rz = *reinterpret_cast<const f32x4*>(&tz[16 * qb + 4 * j]);
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
@@ -691,7 +701,7 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
           CT ad = lds_row_chunk<HD>(ds, 16 * qb + r, 4 * c + j);
 #pragma unroll
           for (int kb = 0; kb < KBW; ++kb) {
-            sv[u][kb] = mma(aq, kf[kb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : sv[u][kb]);
+            sv[u][kb] = mma(aq, kf[kb][c], c == 0 ? (PS ? lx[u] : f32x4{0.f, 0.f, 0.f, 0.f}) : sv[u][kb]);
             dp[u][kb] = mma(ad, vf[kb][c], c == 0 ? rz : dp[u][kb]);
           }
         }
@@ -704,7 +714,7 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
         for (int i = 0; i < 4; ++i) {
 #pragma unroll
           for (int kb = 0; kb < KBW; ++kb) {
-            const float e = fast_exp2(__builtin_fmaf(sv[u][kb][i], sl2, -lx[u][i]));
+            const float e = PS ? fast_exp2(sv[u][kb][i]) : fast_exp2(__builtin_fmaf(sv[u][kb][i], sl2, -lx[u][i]));
             const float p = !MASK || kok[kb] ? e : 0.f;
             a8[kb][4 * u + i] = p;
             b8[kb][4 * u + i] = p * dp[u][kb][i];
@@ -1220,18 +1230,18 @@ __global__ void __launch_bounds__(256) slc_bwd_kv_kernel(const T* q, const T* k,
 constexpr int kCmpChunks = 8;   // query chunks of the compressed branch's key-major pass
 
 // Query-major pass launcher: bf16 layers take the direct-load kernel, f32 layers the
-// register-staged one.
+// register-staged one. Non-ball (compressed) launches of bf16 layers read prescaled keys.
 template <typename T, int HD, int QB, bool BALL, bool ADD>
 void launch_bwd_q(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v, const T* dout,
                   const uint8_t* kvalid, QTerms qt, int H, int N, int nkeys_total, int m, float sl2, float scale,
                   float* dq) {
   if constexpr (sizeof(T) == 2) {
     if (kvalid == nullptr && (BALL ? m : nkeys_total) % kKT == 0)
-      hipLaunchKernelGGL((dense_bwd_q_dma_kernel<HD, QB, BALL, ADD, false>), grid, dim3(256), 0, st, q, k, v, dout,
-                         kvalid, qt, H, N, nkeys_total, m, sl2, scale, dq);
+      hipLaunchKernelGGL((dense_bwd_q_dma_kernel<HD, QB, BALL, ADD, false, !BALL>), grid, dim3(256), 0, st, q, k, v,
+                         dout, kvalid, qt, H, N, nkeys_total, m, sl2, scale, dq);
     else
-      hipLaunchKernelGGL((dense_bwd_q_dma_kernel<HD, QB, BALL, ADD, true>), grid, dim3(256), 0, st, q, k, v, dout,
-                         kvalid, qt, H, N, nkeys_total, m, sl2, scale, dq);
+      hipLaunchKernelGGL((dense_bwd_q_dma_kernel<HD, QB, BALL, ADD, true, !BALL>), grid, dim3(256), 0, st, q, k, v,
+                         dout, kvalid, qt, H, N, nkeys_total, m, sl2, scale, dq);
   }
   else
     hipLaunchKernelGGL((dense_bwd_q_kernel<T, HD, QB, BALL, ADD>), grid, dim3(256), 0, st, q, k, v, dout, kvalid, qt,
@@ -1239,18 +1249,18 @@ void launch_bwd_q(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v,
 }
 
 // Key-major pass launcher: bf16 layers take the direct-load kernel, f32 layers the
-// register-staged one.
+// register-staged one. Non-ball (compressed) launches of bf16 layers read prescaled keys.
 template <typename T, int HD, int NW, bool BALL>
 void launch_bwd_kv(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v, const T* dout,
                    const uint8_t* kvalid, QTerms qt, int H, int N, int nkeys_total, int m, int nchunks, float sl2,
                    float scale, float* dk, float* dv) {
   if constexpr (sizeof(T) == 2) {
     if (kvalid == nullptr && nkeys_total % (NW * 32) == 0)
-      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, false>), grid, dim3(NW * 64), 0, st, q, k, v, dout,
-                         kvalid, qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
+      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, false, !BALL>), grid, dim3(NW * 64), 0, st, q, k,
+                         v, dout, kvalid, qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
     else
-      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, true>), grid, dim3(NW * 64), 0, st, q, k, v, dout,
-                         kvalid, qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
+      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, true, !BALL>), grid, dim3(NW * 64), 0, st, q, k,
+                         v, dout, kvalid, qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
   }
   else
     hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, NW, BALL>), grid, dim3(NW * 64), 0, st, q, k, v, dout, kvalid, qt,
@@ -1283,12 +1293,13 @@ hipError_t bwd_stage_impl(const Dims& D, const BwdArgs& A, BwdStage stage, hipSt
     case BwdStage::prep: {
       if (D.bf16) {
         const long long n = D.cmp_rows() * HD;
+        // the compressed keys carry the softmax scale times log2(e), as in the forward
         hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.kcmp, n,
-                           (T*)A.kc_lp);
-        hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.vcmp, n,
+                           cmp_key_scale(D), (T*)A.kc_lp);
+        hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.vcmp, n, 1.0f,
                            (T*)A.vc_lp);
         if (D.gcmp)
-          hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.qcmp, n,
+          hipLaunchKernelGGL(cast_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.qcmp, n, 1.0f,
                              (T*)A.qc_lp);
       }
       // store_lse = 0: each branch's log-sum-exp rows are recomputed by its forward kernel

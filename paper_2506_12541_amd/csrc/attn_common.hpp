@@ -335,7 +335,11 @@ template <> __device__ __forceinline__ f32x8 ones_chunk<float>() {
 // LSE_ONLY: only the softmax statistics (reference maximum and row sums) are formed, in
 // exactly the order of the full step, so the log-sum-exp equals the full step's bit for
 // bit; the V^T reads and the P V products are skipped and finish() writes no output rows.
-template <typename T, int HD, int QB, bool LSE_ONLY = false>
+// PS (staged steps only): the keys arrive multiplied by the softmax scale times log2(e), so
+// a score is already in the exponent's units, and each score MFMA starts from minus the
+// reference maximum: its result is the exponent itself, with no multiply-add per score.
+// A tile whose maximum raises the reference is shifted once by the rise (shift()).
+template <typename T, int HD, int QB, bool LSE_ONLY = false, bool PS = false>
 struct WaveAttn {
   static constexpr int NCH = HD / 32;  // chunks of the head dim
   static constexpr int DB = HD / 16;   // 16-wide dim blocks of O^T
@@ -344,11 +348,13 @@ struct WaveAttn {
   float mx[QB];      // reference maximum (log2 domain, scaled)
   f32x4 o[QB][DB];
   f32x4 lsum[QB];    // row sums (every element holds the same sum)
+  f32x4 cneg[QB];    // PS: minus the reference maximum (0 while it is -inf), the scores' start
 
   __device__ void init() {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       mx[qb] = kNegInf;
+      cneg[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
       lsum[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int db = 0; db < DB; ++db) o[qb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -439,15 +445,19 @@ struct WaveAttn {
       for (int c = 0; c < NCH; ++c) {
         CT a = kfrag(kb, c);
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) s[qb][kb] = mma(a, qf[qb][c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : s[qb][kb]);
+        for (int qb = 0; qb < QB; ++qb)
+          s[qb][kb] = mma(a, qf[qb][c], c == 0 ? (PS ? cneg[qb] : f32x4{0.f, 0.f, 0.f, 0.f}) : s[qb][kb]);
       }
   }
   // Masks a score tile (MASK: keyok(kb, i) false -> -inf) and moves the reference maximum:
   // like tile(), it is raised only when the tile's maximum exceeds it by more than
   // kRescale. Returns whether any query of the wave raised it (wave-uniform); alpha[qb] is
   // then the factor for the accumulated O and row sums (1 where not raised).
+  // PS: delta[qb] is the rise of the reference against the one the tile's scores start
+  // from (0 where not raised), for shift().
   template <int KB, bool MASK, typename OK>
-  __device__ __forceinline__ bool tile_max(f32x4 (&s)[QB][KB], float sl2, OK keyok, float (&alpha)[QB]) {
+  __device__ __forceinline__ bool tile_max(f32x4 (&s)[QB][KB], float sl2, OK keyok, float (&alpha)[QB],
+                                           float (&delta)[QB]) {
     bool any = false;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -459,14 +469,30 @@ struct WaveAttn {
           if constexpr (MASK) s[qb][kb][i] = keyok(kb, i) ? s[qb][kb][i] : kNegInf;
           tmax = fmaxf(tmax, s[qb][kb][i]);
         }
-      tmax = col_max(tmax) * sl2;
+      const float cref = -cneg[qb][0];
+      tmax = PS ? col_max(tmax) + cref : col_max(tmax) * sl2;
       const bool raise = tmax > mx[qb] + kRescale;
       const float mnew = raise ? tmax : mx[qb];
       alpha[qb] = raise ? fast_exp2(mx[qb] - mnew) : 1.0f;
       mx[qb] = mnew;
+      if constexpr (PS) delta[qb] = raise ? mnew - cref : 0.f;
       any |= __builtin_amdgcn_ballot_w64(raise) != 0;   // no short-circuit: no branch
     }
     return any;
+  }
+  // PS, after a raise: moves a score tile that started from the previous reference onto
+  // the new one, and makes the new one the start of the next tiles' scores
+  template <int KB>
+  __device__ __forceinline__ void shift(f32x4 (&s)[QB][KB], const float (&delta)[QB]) {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s[qb][kb][i] -= delta[qb];
+      const float c = mx[qb] == kNegInf ? 0.f : -mx[qb];
+      cneg[qb] = f32x4{c, c, c, c};
+    }
   }
   __device__ __forceinline__ void rescale(const float (&alpha)[QB]) {
 #pragma unroll
@@ -490,8 +516,13 @@ struct WaveAttn {
         float v8[8];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          v8[i] = fast_exp2(__builtin_fmaf(s[qb][2 * kp][i], sl2, -mref));
-          v8[4 + i] = fast_exp2(__builtin_fmaf(s[qb][2 * kp + 1][i], sl2, -mref));
+          if constexpr (PS) {
+            v8[i] = fast_exp2(s[qb][2 * kp][i]);
+            v8[4 + i] = fast_exp2(s[qb][2 * kp + 1][i]);
+          } else {
+            v8[i] = fast_exp2(__builtin_fmaf(s[qb][2 * kp][i], sl2, -mref));
+            v8[4 + i] = fast_exp2(__builtin_fmaf(s[qb][2 * kp + 1][i], sl2, -mref));
+          }
         }
         pf[qb][kp] = make_chunk<T>(v8);
       }
@@ -538,13 +569,13 @@ struct WaveAttn {
   }
 };
 
-template <typename T, int HD, int QB, bool LO>
-__device__ __forceinline__ void load_q(WaveAttn<T, HD, QB, LO>& w, const T* qrow0, int lane) {
+template <typename T, int HD, int QB, bool LO, bool PS>
+__device__ __forceinline__ void load_q(WaveAttn<T, HD, QB, LO, PS>& w, const T* qrow0, int lane) {
   const int r = lane & 15, j = lane >> 4;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-    for (int c = 0; c < WaveAttn<T, HD, QB, LO>::NCH; ++c)
+    for (int c = 0; c < WaveAttn<T, HD, QB, LO, PS>::NCH; ++c)
       w.qf[qb][c] = load_chunk(qrow0 + (size_t)(16 * qb + r) * HD + 32 * c + 8 * j);
 }
 

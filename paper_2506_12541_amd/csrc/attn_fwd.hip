@@ -126,14 +126,16 @@ __device__ __forceinline__ void interleave_pv_max() {
 // into one buffer do not alias reads of another. MASK = false: every key of the launch is
 // real and the key count a multiple of 64 (no per-key select).
 // LO: log-sum-exp rows only (the V tiles are not loaded; no output rows).
-template <int HD, int QB, int NW, bool BALL, typename OT = bf16_t, bool LO = false, bool MASK = true>
+// PS: the keys are stored multiplied by sl2 (scores come out in the exponent's units, see
+// WaveAttn); sl2 is then not applied again.
+template <int HD, int QB, int NW, bool BALL, typename OT = bf16_t, bool LO = false, bool MASK = true, bool PS = false>
 __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
                                                                 const uint8_t* qvalid_all, const uint8_t* kvalid_all,
                                                                 int H, int N, int nkeys_total, int m, float sl2,
                                                                 OT* out, float* lse) {
   constexpr int kFT = kKT;
   constexpr int KB = kFT / 16;
-  typedef WaveAttn<bf16_t, HD, QB, LO> WA;
+  typedef WaveAttn<bf16_t, HD, QB, LO, PS> WA;
   typedef typename WA::CT CT;
   __shared__ __attribute__((aligned(16))) bf16_t ks0[kFT * HD], ks1[kFT * HD];
   __shared__ __attribute__((aligned(16))) bf16_t vs0[kFT * HD], vs1[kFT * HD];
@@ -181,7 +183,7 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q,
   w.init();
   const int wq0 = q0 + wid * 16 * QB;
   f32x4 s_cur[QB][KB], s_nxt[QB][KB];
-  float alpha[QB];
+  float alpha[QB], delta[QB];
   bool raise = false;
 
   auto kfrag_of = [&](const bf16_t* kt) {
@@ -201,6 +203,14 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q,
     __syncthreads();     // ... and every wave's; K(t) and V(t - 1) are no longer read
     issue_k(t + 2, kc, okc);
     issue_v(t + 1, vn);
+    if constexpr (PS) {
+      // rare: a query's maximum rose (wave-uniform); tile t's scores started from the
+      // previous reference, tile t + 1's will start from the new one
+      if (raise) {
+        w.rescale(alpha);
+        w.template shift<KB>(s_cur, delta);
+      }
+    }
     // region 1: scores of tile t + 1 beside the exponentials of tile t
     CT pf[QB][KB / 2];
     if constexpr (MORE) w.template scores<KB>(s_nxt, kfrag_of(kn));
@@ -212,11 +222,13 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q,
     for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
       for (int kp = 0; kp < KB / 2; ++kp) asm volatile("" : "+v"(pf[qb][kp]));
-    if (raise) w.rescale(alpha);   // rare: a query's maximum rose (wave-uniform)
+    if constexpr (!PS) {
+      if (raise) w.rescale(alpha);   // rare: a query's maximum rose (wave-uniform)
+    }
     // region 2: P V of tile t beside the row maxima of tile t + 1
     w.template pv<KB>(pf, [&](int db, int kp) { return lds_tr_chunk<HD>(vc, 32 * kp, 16 * db, lane); });
     if constexpr (MORE) {
-      raise = w.template tile_max<KB, MASK>(s_nxt, sl2, keyok_of(okn), alpha);
+      raise = w.template tile_max<KB, MASK>(s_nxt, sl2, keyok_of(okn), alpha, delta);
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
@@ -232,7 +244,7 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q,
   vm_drain();
   __syncthreads();
   w.template scores<KB>(s_cur, kfrag_of(ks0));
-  raise = w.template tile_max<KB, MASK>(s_cur, sl2, keyok_of(ok0), alpha);
+  raise = w.template tile_max<KB, MASK>(s_cur, sl2, keyok_of(ok0), alpha, delta);
   issue_k(1, ks1, ok1);
   issue_v(0, vs0);
   int t = 0;
@@ -479,7 +491,8 @@ __global__ void gate_fwd_vec_kernel(const T* ob, const float* oc, const float* g
 // OT: type of the output rows (the storage type, or float32 for unrounded outputs).
 // o == nullptr: log-sum-exp rows only (the same kernel without the value products, so the
 // statistics equal those of the full launch bit for bit).
-template <typename T, int HD, int QB, bool BALL, int NW = 4, typename OT = T>
+// PS: bf16 keys stored multiplied by sl2 (the compressed tokens; f32 layers keep them plain).
+template <typename T, int HD, int QB, bool BALL, int NW = 4, typename OT = T, bool PS = false>
 void launch_dense_fwd(dim3 grid, hipStream_t st, const void* q, const void* k, const void* v, const uint8_t* qvalid,
                       const uint8_t* kvalid, int H, int N, int nkeys_total, int m, float sl2, void* o, float* lse) {
   if constexpr (sizeof(T) == 2) {
@@ -488,16 +501,16 @@ void launch_dense_fwd(dim3 grid, hipStream_t st, const void* q, const void* k, c
     const bf16_t *qq = (const bf16_t*)q, *kk = (const bf16_t*)k, *vv = (const bf16_t*)v;
     const dim3 blk(64 * NW);
     if (o && mask)
-      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, false, true>), grid, blk, 0, st, qq, kk, vv,
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, false, true, PS>), grid, blk, 0, st, qq, kk, vv,
                          qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
     else if (o)
-      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, false, false>), grid, blk, 0, st, qq, kk, vv,
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, false, false, PS>), grid, blk, 0, st, qq, kk, vv,
                          qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
     else if (mask)
-      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, true, true>), grid, blk, 0, st, qq, kk, vv,
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, true, true, PS>), grid, blk, 0, st, qq, kk, vv,
                          qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
     else
-      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, true, false>), grid, blk, 0, st, qq, kk, vv,
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, true, false, PS>), grid, blk, 0, st, qq, kk, vv,
                          qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
   } else {
     if (o)
@@ -530,11 +543,11 @@ hipError_t cmp_impl(const Dims& D, const void* q, const void* kc, const void* vc
                     const uint8_t* cvalid, float* o, float* lse, hipStream_t st) {
   const float sl2 = D.scale * kLog2e;
   if (D.N % 128 == 0)
-    launch_dense_fwd<T, HD, 2, false, 4, float>(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, valid, cvalid, D.H, D.N,
-                                                D.N / D.l, D.m, sl2, o, lse);
+    launch_dense_fwd<T, HD, 2, false, 4, float, true>(dim3(D.N / 128, D.H, D.B), st, q, kc, vc, valid, cvalid,
+                                                      D.H, D.N, D.N / D.l, D.m, sl2, o, lse);
   else   // 64 token slots: one 64-query workgroup per head
-    launch_dense_fwd<T, HD, 1, false, 4, float>(dim3(D.N / 64, D.H, D.B), st, q, kc, vc, valid, cvalid, D.H, D.N,
-                                                D.N / D.l, D.m, sl2, o, lse);
+    launch_dense_fwd<T, HD, 1, false, 4, float, true>(dim3(D.N / 64, D.H, D.B), st, q, kc, vc, valid, cvalid,
+                                                      D.H, D.N, D.N / D.l, D.m, sl2, o, lse);
   return hipGetLastError();
 }
 
@@ -547,11 +560,11 @@ hipError_t cmp_coarse_impl(const Dims& D, const void* qc, const void* kc, const 
   const float sl2 = D.scale * kLog2e;
   const int nct = D.N / D.l;
   if (nct % 128 == 0)
-    launch_dense_fwd<T, HD, 2, false, 4, float>(dim3(nct / 128, D.H, D.B), st, qc, kc, vc, cvalid, cvalid, D.H, nct,
-                                                nct, D.m, sl2, oc, lsec);
+    launch_dense_fwd<T, HD, 2, false, 4, float, true>(dim3(nct / 128, D.H, D.B), st, qc, kc, vc, cvalid, cvalid,
+                                                      D.H, nct, nct, D.m, sl2, oc, lsec);
   else
-    launch_dense_fwd<T, HD, 1, false, 4, float>(dim3(nct / 64, D.H, D.B), st, qc, kc, vc, cvalid, cvalid, D.H, nct,
-                                                nct, D.m, sl2, oc, lsec);
+    launch_dense_fwd<T, HD, 1, false, 4, float, true>(dim3(nct / 64, D.H, D.B), st, qc, kc, vc, cvalid, cvalid,
+                                                      D.H, nct, nct, D.m, sl2, oc, lsec);
   return hipGetLastError();
 }
 

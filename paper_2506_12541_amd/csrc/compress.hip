@@ -44,7 +44,7 @@ template <typename T, int HD>
 __global__ void __launch_bounds__(kWaves * 64) mlp_fwd_kernel(const T* x, const uint8_t* valid, int H, int N, int l,
                                                               long long rows, const T* w1t, const float* b1,
                                                               const float* w2, const float* b2, float* out,
-                                                              float* pre_out, T* out_lp) {
+                                                              float* pre_out, T* out_lp, float lp_scale) {
   constexpr int OB = HD / 16;  // 16-wide output blocks
   __shared__ float w2s[HD * HD];
   __shared__ float b1s[HD], b2s[HD];
@@ -147,10 +147,10 @@ __global__ void __launch_bounds__(kWaves * 64) mlp_fwd_kernel(const T* x, const 
         *reinterpret_cast<float4*>(pre_out + row * HD + o) = pv;
         float4 yv = make_float4(y[ob][0] + b2s[o], y[ob][1] + b2s[o + 1], y[ob][2] + b2s[o + 2], y[ob][3] + b2s[o + 3]);
         *reinterpret_cast<float4*>(out + row * HD + o) = yv;
-        out_lp[row * HD + o + 0] = from_f32<T>(yv.x);
-        out_lp[row * HD + o + 1] = from_f32<T>(yv.y);
-        out_lp[row * HD + o + 2] = from_f32<T>(yv.z);
-        out_lp[row * HD + o + 3] = from_f32<T>(yv.w);
+        out_lp[row * HD + o + 0] = from_f32<T>(yv.x * lp_scale);
+        out_lp[row * HD + o + 1] = from_f32<T>(yv.y * lp_scale);
+        out_lp[row * HD + o + 2] = from_f32<T>(yv.z * lp_scale);
+        out_lp[row * HD + o + 3] = from_f32<T>(yv.w * lp_scale);
       }
     }
   }
@@ -159,7 +159,7 @@ __global__ void __launch_bounds__(kWaves * 64) mlp_fwd_kernel(const T* x, const 
 // Mean pooling: y = (1/l) * sum of the block's real rows.
 template <typename T>
 __global__ void mean_pool_kernel(const T* x, const uint8_t* valid, int H, int N, int l, int hd, long long rows,
-                                 float* out, T* out_lp) {
+                                 float* out, T* out_lp, float lp_scale) {
   long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= rows * hd) return;
   long long row = i / hd;
@@ -175,7 +175,7 @@ __global__ void mean_pool_kernel(const T* x, const uint8_t* valid, int H, int N,
   }
   s /= (float)l;
   out[i] = s;
-  out_lp[i] = from_f32<T>(s);
+  out_lp[i] = from_f32<T>(s * lp_scale);
 }
 
 // ---------------------------------------------------------------------------------
@@ -782,12 +782,12 @@ hipError_t compress_bwd_impl(const Dims& D, const void* x, const uint8_t* valid,
 
 template <typename T, int HD>
 hipError_t compress_impl(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi, float* out,
-                         float* pre, void* out_lp, void* w1t_ws, hipStream_t st) {
+                         float* pre, void* out_lp, void* w1t_ws, hipStream_t st, float lp_scale) {
   const long long rows = D.cmp_rows();
   if (D.pool == 1) {
     const long long tot = rows * HD;
     hipLaunchKernelGGL(mean_pool_kernel<T>, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, st, (const T*)x, valid,
-                       D.H, D.N, D.l, HD, rows, out, (T*)out_lp);
+                       D.H, D.N, D.l, HD, rows, out, (T*)out_lp, lp_scale);
     return hipGetLastError();
   }
   const int ld = D.l * HD;
@@ -796,7 +796,7 @@ hipError_t compress_impl(const Dims& D, const void* x, const uint8_t* valid, con
   const long long per_wg = (long long)kWaves * 16 * kRB;
   const unsigned grid = (unsigned)((rows + per_wg - 1) / per_wg);
   hipLaunchKernelGGL((mlp_fwd_kernel<T, HD>), dim3(grid), dim3(kWaves * 64), 0, st, (const T*)x, valid, D.H, D.N,
-                     D.l, rows, (const T*)w1t, phi.b1, phi.w2, phi.b2, out, pre, (T*)out_lp);
+                     D.l, rows, (const T*)w1t, phi.b1, phi.w2, phi.b2, out, pre, (T*)out_lp, lp_scale);
   return hipGetLastError();
 }
 
@@ -831,13 +831,13 @@ hipError_t launch_compress_bwd(const Dims& D, const void* x, const uint8_t* vali
 }
 
 hipError_t launch_compress_fwd(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi, float* out,
-                               float* pre, void* out_lp, void* w1t_ws, hipStream_t st) {
+                               float* pre, void* out_lp, void* w1t_ws, hipStream_t st, float lp_scale) {
   if (D.bf16) {
-    return D.d == 64 ? compress_impl<bf16_t, 64>(D, x, valid, phi, out, pre, out_lp, w1t_ws, st)
-                     : compress_impl<bf16_t, 32>(D, x, valid, phi, out, pre, out_lp, w1t_ws, st);
+    return D.d == 64 ? compress_impl<bf16_t, 64>(D, x, valid, phi, out, pre, out_lp, w1t_ws, st, lp_scale)
+                     : compress_impl<bf16_t, 32>(D, x, valid, phi, out, pre, out_lp, w1t_ws, st, lp_scale);
   }
-  return D.d == 64 ? compress_impl<float, 64>(D, x, valid, phi, out, pre, out_lp, w1t_ws, st)
-                   : compress_impl<float, 32>(D, x, valid, phi, out, pre, out_lp, w1t_ws, st);
+  return D.d == 64 ? compress_impl<float, 64>(D, x, valid, phi, out, pre, out_lp, w1t_ws, st, lp_scale)
+                   : compress_impl<float, 32>(D, x, valid, phi, out, pre, out_lp, w1t_ws, st, lp_scale);
 }
 
 }  // namespace bsa

@@ -45,8 +45,13 @@ hipError_t launch_permute(const void* src, const int* perm, int64_t n_real, int6
 
 // compress.hip: compression phi of Eq. 5 and its backward
 hipError_t launch_block_valid(const Dims& D, const uint8_t* valid, uint8_t* cvalid, hipStream_t st);
+// out_lp: the rows in the storage type, multiplied by lp_scale (the compressed keys of bf16
+// layers carry the softmax scale times log2(e) there; see launch_cmp_fwd)
 hipError_t launch_compress_fwd(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi,
-                               float* out, float* pre, void* out_lp, void* w1t_ws, hipStream_t st);
+                               float* out, float* pre, void* out_lp, void* w1t_ws, hipStream_t st,
+                               float lp_scale = 1.0f);
+// the bf16 layers' scale of the compressed keys' storage-type copy
+inline float cmp_key_scale(const Dims& D) { return D.bf16 ? D.scale * 1.4426950408889634f : 1.0f; }
 
 // select.hip: pooled-query block scores and group top-k (Eq. 6, 7, 10-12, 14)
 // qpool: B*H*(N/g)*d floats of coarse queries; written here (group mean of Eq. 11) unless
