@@ -339,14 +339,19 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
   // key-validity bytes are read before the tile loads, so waiting for them does not
   // wait for the tile
   auto issue = [&](int t0, bf16_t* kd, bf16_t* vd, uint8_t* okd) {
-    uint8_t okv = 0;
-    if (threadIdx.x < KT) {
-      const int key = t0 + threadIdx.x;
-      okv = key < nkeys && (kval == nullptr || kval[key]);
+    if constexpr (MASK) {
+      uint8_t okv = 0;
+      if (threadIdx.x < KT) {
+        const int key = t0 + threadIdx.x;
+        okv = key < nkeys && (kval == nullptr || kval[key]);
+      }
+      dma_tile<HD, KT, 4>(kd, kh, t0, nkeys, wid, lane);
+      dma_tile<HD, KT, 4>(vd, vh, t0, nkeys, wid, lane);
+      if (threadIdx.x < KT) okd[threadIdx.x] = okv;
+    } else {   // whole tiles, every key real
+      dma_tile_full<HD, KT, 4>(kd, kh + (size_t)t0 * HD, wid, lane);
+      dma_tile_full<HD, KT, 4>(vd, vh + (size_t)t0 * HD, wid, lane);
     }
-    dma_tile<HD, KT, 4>(kd, kh, t0, nkeys, wid, lane);
-    dma_tile<HD, KT, 4>(vd, vh, t0, nkeys, wid, lane);
-    if (threadIdx.x < KT) okd[threadIdx.x] = okv;
   };
   issue(0, ks0, vs0, ok0);
 
