@@ -281,6 +281,9 @@ def summarize_traffic(args):
 
 SQ_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CU_CYCLES", "SQ_INSTS_VALU",
                "SQ_INSTS_MFMA", "SQ_INSTS_LDS", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_VALU", "GRBM_GUI_ACTIVE")
+# second pass: instruction mix for the issue bound, and cycles where MFMA and VALU overlap
+SQ_ISSUE_COUNTERS = ("SQ_INSTS_VALU_TRANS_F32", "SQ_VALU_MFMA_COEXEC_CYCLES", "SQ_VALU_MFMA_BUSY_CYCLES",
+                     "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "GRBM_GUI_ACTIVE")
 N_CU = 256
 N_XCD = 8
 
@@ -324,7 +327,7 @@ def summarize_counters(args):
     FETCH_SIZE, WRITE_SIZE (HBM bytes, scaled by a plain 1 GiB copy) and the SQ/GRBM
     instruction and MFMA counters."""
     import csv
-    trace, fetch, write, sq, cfetch, cwrite = args.summarize_counters
+    trace, fetch, write, sq, sq2, cfetch, cwrite = args.summarize_counters
     dur = {}
     for r in csv.DictReader(open(trace)):
         k = _short_kernel(r["Kernel_Name"])
@@ -332,6 +335,7 @@ def summarize_counters(args):
     f = _per_kernel(fetch, ("FETCH_SIZE",))
     w = _per_kernel(write, ("WRITE_SIZE",))
     q = _per_kernel(sq, SQ_COUNTERS)
+    q2 = _per_kernel(sq2, SQ_ISSUE_COUNTERS)
     is_copy = lambda n: "copy" in n.lower()
     cf = [v["FETCH_SIZE"] for k, v in _per_kernel(cfetch, ("FETCH_SIZE",)).items() if is_copy(k)]
     cw = [v["WRITE_SIZE"] for k, v in _per_kernel(cwrite, ("WRITE_SIZE",)).items() if is_copy(k)]
@@ -345,8 +349,16 @@ def summarize_counters(args):
         fb = f.get(k, {}).get("FETCH_SIZE", float("nan")) * 1024 * ff
         wb = w.get(k, {}).get("WRITE_SIZE", float("nan")) * 1024 * fw
         c = q.get(k, {})
+        c2 = q2.get(k, {})
         mops = c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)
         gui = c.get("GRBM_GUI_ACTIVE", float("nan"))
+        clk = gui / N_XCD / t if gui == gui else float("nan")   # Hz
+        # issue-serialized time: every MFMA (16x16x32, 16 cycles), transcendental (quarter
+        # rate, 16 cycles) and other VALU instruction (wave64 over 16 lanes, 4 cycles) of
+        # the launch issued one after another on the 1024 SIMDs, at the measured clock
+        nm, ntr, nv = (c2.get(x, float("nan")) for x in ("SQ_INSTS_MFMA", "SQ_INSTS_VALU_TRANS_F32", "SQ_INSTS_VALU"))
+        issue_s = (16 * nm + 16 * ntr + 4 * (nv - nm - ntr)) / (N_CU * 4) / clk
+        busy2 = c2.get("SQ_VALU_MFMA_BUSY_CYCLES", float("nan"))
         rows.append({
             "kernel": k, "calls": len(ds), "avg_us": t * 1e6, "gpu_time_pct": 100 * sum(ds) / total,
             "fetch_mb": fb / 1e6, "write_mb": wb / 1e6, "hbm_gbps": (fb + wb) / t / 1e9,
@@ -356,7 +368,9 @@ def summarize_counters(args):
             else float("nan"),
             "clock_ghz": gui / N_XCD / t / 1e9 if gui == gui else float("nan"),
             "valu_insts": c.get("SQ_INSTS_VALU", float("nan")), "mfma_insts": c.get("SQ_INSTS_MFMA", float("nan")),
-            "lds_insts": c.get("SQ_INSTS_LDS", float("nan")),
+            "trans_insts": ntr, "lds_insts": c.get("SQ_INSTS_LDS", float("nan")),
+            "issue_bound_pct": 100 * issue_s / t,
+            "coexec_pct": 100 * c2.get("SQ_VALU_MFMA_COEXEC_CYCLES", float("nan")) / busy2 if busy2 else float("nan"),
         })
     out = args.counters_out
     with open(out, "w") as fh:
@@ -371,9 +385,16 @@ def summarize_counters(args):
                  "(GRBM_GUI_ACTIVE / 8 XCDs x 256 CUs x 4 SIMDs); clock = GRBM_GUI_ACTIVE / 8 / duration. Instruction\n"
                  "counts are per dispatch (all waves). Kernels under 0.2% of GPU time are left out. GRBM_GUI_ACTIVE\n"
                  "spans the dispatch's whole busy window, which for a short kernel includes launch and drain time\n"
-                 "outside its traced duration: clock and MFMA busy are meaningful for kernels of 100 us and more.\n\n")
+                 "outside its traced duration: clock and MFMA busy are meaningful for kernels of 100 us and more.\n"
+                 "Issue bound = the time the launch's MFMA (16 cycles each), transcendental (16) and other VALU\n"
+                 "instructions (4; SQ_INSTS_VALU counts MFMA and transcendental instructions too) take issued one\n"
+                 "after another on the 1024 SIMDs at the measured clock, over the duration: near 100 the kernel is\n"
+                 "bound by issue with MFMA and VALU work serialised. Co-exec = SQ_VALU_MFMA_COEXEC_CYCLES /\n"
+                 "SQ_VALU_MFMA_BUSY_CYCLES, the share of MFMA-busy cycles in which VALU work also ran (second\n"
+                 "counter pass, with the transcendental count).\n\n")
         cols = ("kernel", "calls", "avg_us", "gpu_time_pct", "fetch_mb", "write_mb", "hbm_gbps",
-                "mfma_tflops_executed", "mfma_busy_pct", "clock_ghz", "valu_insts", "mfma_insts", "lds_insts")
+                "mfma_tflops_executed", "mfma_busy_pct", "clock_ghz", "valu_insts", "mfma_insts", "trans_insts",
+                "lds_insts", "issue_bound_pct", "coexec_pct")
         fh.write("| " + " | ".join(cols) + " |\n|" + "---|" * len(cols) + "\n")
         for r in rows:
             cells = []
@@ -418,9 +439,9 @@ def parse():
                                          "paper_2506_12541_amd/csrc/common.hpp paper_2506_12541_amd/csrc/kernels.hpp "
                                          "paper_2506_12541_amd/build.py")
     ap.add_argument("--commands", nargs="*", default=[])
-    ap.add_argument("--summarize-counters", nargs=6, metavar="CSV",
-                    help="kernel trace, FETCH_SIZE, WRITE_SIZE and SQ counter CSVs of the bench, FETCH_SIZE and "
-                         "WRITE_SIZE CSVs of --copy-calibration")
+    ap.add_argument("--summarize-counters", nargs=7, metavar="CSV",
+                    help="kernel trace, FETCH_SIZE, WRITE_SIZE, SQ and SQ issue counter CSVs of the bench, "
+                         "FETCH_SIZE and WRITE_SIZE CSVs of --copy-calibration")
     ap.add_argument("--counters-out", default=os.path.join(ROOT, "profiles", "counters.md"))
     ap.add_argument("--counters-title", default="")
     ap.add_argument("--streams", type=int, default=2, help="library streams (1 = every kernel alone)")
