@@ -414,6 +414,35 @@ def summarize_counters(args):
     print(open(out).read())
 
 
+LDS_COUNTERS = ("SQ_INSTS_LDS", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_ADDR_CONFLICT",
+                "SQ_LDS_UNALIGNED_STALL", "SQ_WAIT_INST_LDS", "GRBM_GUI_ACTIVE")
+
+
+def summarize_lds(args):
+    """Per-kernel LDS bank-conflict table from one rocprofv3 --pmc run of LDS_COUNTERS."""
+    (csv_path,) = args.summarize_lds
+    q = _per_kernel(csv_path, LDS_COUNTERS)
+    rows = sorted(((k, c) for k, c in q.items() if c.get("SQ_INSTS_LDS", 0) > 0),
+                  key=lambda kc: -kc[1].get("SQ_LDS_IDX_ACTIVE", 0))
+    with open(args.counters_out, "w") as fh:
+        fh.write(f"# LDS bank conflicts per kernel: {args.counters_title}\n\n")
+        fh.write("Commands (repository root on the MI355X box, after `cd /tmp && export TMPDIR=/tmp`):\n\n")
+        for cmd in args.commands:
+            fh.write(f"    {cmd}\n")
+        fh.write("\nPer dispatch, summed over the chip: LDS instructions, LDS busy cycles (SQ_LDS_IDX_ACTIVE) and\n"
+                 "the cycles of those lost to bank and address conflicts and unaligned accesses; conflict % =\n"
+                 "SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE. Kernels without LDS instructions are left out.\n\n")
+        fh.write("| kernel | dispatches | lds_insts | lds_active_cycles | bank_conflict_cycles | conflict_pct | "
+                 "addr_conflict_cycles | unaligned_stall_cycles |\n|---|---|---|---|---|---|---|---|\n")
+        for k, c in rows:
+            act = c.get("SQ_LDS_IDX_ACTIVE", 0.0)
+            bank = c.get("SQ_LDS_BANK_CONFLICT", 0.0)
+            fh.write(f"| `{k}` | {c['_n']} | {c.get('SQ_INSTS_LDS', 0):.3g} | {act:.3g} | {bank:.3g} | "
+                     f"{100 * bank / act if act else 0.0:.2f} | {c.get('SQ_LDS_ADDR_CONFLICT', 0):.3g} | "
+                     f"{c.get('SQ_LDS_UNALIGNED_STALL', 0):.3g} |\n")
+    print(open(args.counters_out).read())
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -442,6 +471,7 @@ def parse():
     ap.add_argument("--summarize-counters", nargs=7, metavar="CSV",
                     help="kernel trace, FETCH_SIZE, WRITE_SIZE, SQ and SQ issue counter CSVs of the bench, "
                          "FETCH_SIZE and WRITE_SIZE CSVs of --copy-calibration")
+    ap.add_argument("--summarize-lds", nargs=1, metavar="CSV", help="LDS counter CSV of the bench (LDS_COUNTERS)")
     ap.add_argument("--counters-out", default=os.path.join(ROOT, "profiles", "counters.md"))
     ap.add_argument("--counters-title", default="")
     ap.add_argument("--streams", type=int, default=2, help="library streams (1 = every kernel alone)")
@@ -782,6 +812,9 @@ def main():
         return
     if args.summarize_counters:
         summarize_counters(args)
+        return
+    if args.summarize_lds:
+        summarize_lds(args)
         return
     if args.oracle_baselines:
         oracle_baselines(args)
