@@ -129,6 +129,30 @@ def test_recomputed_lse_gives_identical_gradients(case):
     run_case(cfg, seed=seed, store_lse=0, **pkw)
 
 
+@pytest.mark.timeout(600)
+def test_recomputed_lse_identical_at_scaling_shape():
+    """The benchmarked shape (65536 points, H=8, d=64, bf16): store_lse = 0 gives the
+    gradients of store_lse = 1 bit for bit (both against the oracle at this size are covered
+    by test_backward_scaling_all_heads)."""
+    cfg = CONFIGS[3]
+    inp = make_inputs(cfg, layout="ball", with_grad=True)
+    valid = valid_from_tree(cfg)
+    outs = []
+    for store in (1, 0):
+        print(f"recompute-LSE at 65536 points, store_lse={store}", flush=True)
+        g, (p, q, k, v, vd, gate, phi_k, phi_v, saved, o, phi_q) = gpu_forward(cfg, inp, valid, store_lse=store)
+        grads = gb.backward(p, q, k, v, vd, gate, phi_k, phi_v, saved, to_dev(inp["do"], p.torch_dtype))
+        torch.cuda.synchronize()
+        flat = {n: grads[n].clone() for n in ("dq", "dk", "dv", "dgate")}
+        for m in ("dphi_k", "dphi_v"):
+            flat.update({f"{m}.{w}": t.clone() for w, t in grads[m].items()})
+        outs.append((o.clone(), flat))
+        del g, saved, grads
+    assert torch.equal(outs[0][0], outs[1][0])
+    for n in outs[0][1]:
+        assert torch.equal(outs[0][1][n], outs[1][1][n]), n
+
+
 def test_backward_variants():
     cfg = CONFIGS[1]
     for kw in (dict(mask_own_ball=0), dict(kv_pool=1)):
