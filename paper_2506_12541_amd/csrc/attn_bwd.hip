@@ -323,7 +323,7 @@ __global__ void __launch_bounds__(256) dense_bwd_q_dma_kernel(const bf16_t* q, c
   __shared__ __attribute__((aligned(16))) bf16_t ks0[KT * HD], ks1[KT * HD];
   __shared__ __attribute__((aligned(16))) bf16_t vs0[KT * HD], vs1[KT * HD];
   __shared__ __attribute__((aligned(16))) uint8_t ok0[KT], ok1[KT];
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, j = lane >> 4;
   const dim3 blk = xcd_grouped_block(BALL ? m / (64 * QB) : (int)gridDim.x);
   const int b = blk.z, h = blk.y;
@@ -632,7 +632,7 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
   // row terms as two arrays (log2 LSE - log2 s, and R) so that a lane reads the values of
   // its four accumulator rows with one 16-byte load
   __shared__ __attribute__((aligned(16))) float tx0[kQT], tz0[kQT], tx1[kQT], tz1[kQT];
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, j = lane >> 4;
   const dim3 blk = xcd_grouped_block(BALL ? m / (NW * 32) : (int)gridDim.x);
   const int bh = blk.z;

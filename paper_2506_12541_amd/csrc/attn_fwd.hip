@@ -140,7 +140,7 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q,
   __shared__ __attribute__((aligned(16))) bf16_t ks0[kFT * HD], ks1[kFT * HD];
   __shared__ __attribute__((aligned(16))) bf16_t vs0[kFT * HD], vs1[kFT * HD];
   __shared__ uint8_t ok0[kFT], ok1[kFT];
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, j = lane >> 4;
   const dim3 blk = xcd_grouped_block(BALL ? m / (16 * QB * NW) : (int)gridDim.x);
   const int b = blk.z, h = blk.y;
