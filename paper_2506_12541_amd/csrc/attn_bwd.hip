@@ -1021,11 +1021,12 @@ __global__ void __launch_bounds__(NW * 64) slc_bwd_q_dma_kernel(const bf16_t* q,
       const int e = t < nt && se < nsub ? sub[se] : -1;
       m[kb] = e >= 0 && (e >> 24) == my_gi ? okm[se] : 0u;
     }
+    // dp starts from -dd, so the product yields dP - dd directly
     f32x4 sv[2], dp[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       sv[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      dp[kb] = sv[kb];
+      dp[kb] = f32x4{-dd, -dd, -dd, -dd};
 #pragma unroll
       for (int c = 0; c < NCH; ++c) {
         sv[kb] = mma(lds_row_chunk<HD>(kt, 16 * kb + r, 4 * c + j), qf[c], sv[kb]);
@@ -1036,11 +1037,16 @@ __global__ void __launch_bounds__(NW * 64) slc_bwd_q_dma_kernel(const bf16_t* q,
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float e = fast_exp2(__builtin_fmaf(sv[kb][i], sl2, -l2));
-        const float p = ((m[kb] >> (4 * j + i)) & 1u) ? e : 0.f;
-        w8[4 * kb + i] = p * (dp[kb][i] - dd);
-      }
+      for (int i = 0; i < 4; ++i) w8[4 * kb + i] = fast_exp2(__builtin_fmaf(sv[kb][i], sl2, -l2)) * dp[kb][i];
+    // keys that are padding, of another lane's group or of a missing block contribute 0 (the
+    // loaded rows are finite); skipped when every key of the tile is seen by every lane
+    if (__builtin_amdgcn_ballot_w64((m[0] & m[1]) != 0xFFFFu) != 0) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (!((m[kb] >> (4 * j + i)) & 1u)) w8[4 * kb + i] = 0.f;
+    }
     const CT dsf = make_chunk<bf16_t>(w8);
 #pragma unroll
     for (int db = 0; db < DB; ++db) acc[db] = mma(lds_tr_chunk_nowait<HD>(kt, 0, 16 * db, lane), dsf, acc[db]);

@@ -364,7 +364,8 @@ struct WaveAttn {
   // Process one tile of KB 16-key blocks (KB even). kfrag(kb, c) gives the A chunk of
   // key block kb, vfrag(db, kp) the A chunk of V^T for dim block db and key pair kp,
   // keyok(kb, i, qb) whether key 4j+i of block kb may be seen by this lane's query.
-  template <int KB, typename KF, typename VF, typename OK>
+  // MASKED = false: every key of the tile may be seen by every query (keyok is not called).
+  template <int KB, typename KF, typename VF, typename OK, bool MASKED = true>
   __device__ __forceinline__ void tile(float sl2, KF kfrag, VF vfrag, OK keyok) {
     f32x4 s[QB][KB];
 #pragma unroll
@@ -391,7 +392,7 @@ struct WaveAttn {
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float x = keyok(kb, i, qb) ? s[qb][kb][i] : kNegInf;
+          float x = !MASKED || keyok(kb, i, qb) ? s[qb][kb][i] : kNegInf;
           s[qb][kb][i] = x;
           tmax = fmaxf(tmax, x);
         }

@@ -418,19 +418,21 @@ __global__ void __launch_bounds__(NW * 64) slc_fwd_dma_kernel(const bf16_t* q, c
     issue(t + 1, next);
     const bf16_t* kt = cur + wid * SLOT;
     const bf16_t* vt = kt + TILE;
-    bool ok[2][4];
+    uint32_t m[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       const int se = 2 * t + kb;
       const int e = t < nt && se < nsub ? sub[se] : -1;
-      const uint32_t m = e >= 0 && (e >> 24) == my_gi ? okm[se] : 0u;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) ok[kb][i] = (m >> (4 * j + i)) & 1u;
+      m[kb] = e >= 0 && (e >> 24) == my_gi ? okm[se] : 0u;
     }
     auto kfrag = [&](int kb, int c) { return lds_row_chunk<HD>(kt, 16 * kb + r, 4 * c + j); };
     auto vfrag = [&](int db, int kp) { return lds_tr_chunk_nowait<HD>(vt, 32 * kp, 16 * db, lane); };
-    auto keyok = [&](int kb, int i, int) { return ok[kb][i]; };
-    w.template tile<2>(sl2, kfrag, vfrag, keyok);
+    auto keyok = [&](int kb, int i, int) { return ((m[kb] >> (4 * j + i)) & 1u) != 0; };
+    // every key of both sub-blocks real and of every lane's group: no per-key select
+    if (__builtin_amdgcn_ballot_w64((m[0] & m[1]) != 0xFFFFu) == 0)
+      w.template tile<2, decltype(kfrag), decltype(vfrag), decltype(keyok), false>(sl2, kfrag, vfrag, keyok);
+    else
+      w.template tile<2>(sl2, kfrag, vfrag, keyok);
   };
   issue(0, buf0);
   for (int t = 0; t < nt; t += 2) {   // straight-line body
