@@ -504,17 +504,18 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
 #define BSA_STEP(name, call, what)        \
   BSA_PHASE(name, st, e = (call));         \
   BSA_TRY(e, what)
+  // keys and values in one launch
+  const bsa::CompressJob kv_jobs[2] = {
+      {k, mk, saved->kcmp, saved->hid_k, kc_lp, w + W.w1t_k, bsa::cmp_key_scale(D)},
+      {v, mv, saved->vcmp, saved->hid_v, vc_lp, w + W.w1t_v, 1.0f}};
   BSA_STEP("fwd.compress", (bsa::launch_block_valid(D, valid, saved->cvalid, st) != hipSuccess
                                 ? hipGetLastError()
-                                : bsa::launch_compress_fwd(D, k, valid, mk, saved->kcmp, saved->hid_k, kc_lp,
-                                                           w + W.w1t_k, st, bsa::cmp_key_scale(D)) != hipSuccess
-                                      ? hipGetLastError()
-                                      : bsa::launch_compress_fwd(D, v, valid, mv, saved->vcmp, saved->hid_v, vc_lp,
-                                                                 w + W.w1t_v, st)),
+                                : bsa::launch_compress_fwd(D, kv_jobs, 2, valid, st)),
            "compression");
-  if (D.block_coarse())
-    BSA_STEP("fwd.compress", bsa::launch_compress_fwd(Dq, q, valid, mq, saved->qcmp, saved->hid_q, qc_lp, w + W.w1t_q, st),
-             "query coarsening");
+  if (D.block_coarse()) {
+    const bsa::CompressJob q_job = {q, mq, saved->qcmp, saved->hid_q, qc_lp, w + W.w1t_q, 1.0f};
+    BSA_STEP("fwd.compress", bsa::launch_compress_fwd(Dq, &q_job, 1, valid, st), "query coarsening");
+  }
   // ball and compressed attention on the auxiliary stream, selection on the caller's
   if (aux.s != st &&
       (hipEventRecord(aux.fork, st) != hipSuccess || hipStreamWaitEvent(aux.s, aux.fork, 0) != hipSuccess))

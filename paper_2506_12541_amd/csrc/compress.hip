@@ -39,12 +39,29 @@ __global__ void transpose_w1_kernel(const float* w1, int ld, int d, T* w1t) {
 
 __device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
 
+// One compression of a forward launch: its input rows, weights (W1 transposed, in the storage
+// type) and outputs.
+struct MlpFwdJob {
+  const void* x;
+  const void* w1t;
+  const float *b1, *w2, *b2;
+  float *out, *pre;
+  void* out_lp;
+  float lp_scale;
+};
+
 // One wave: kRB blocks of 16 rows (coarse tokens); the workgroup stages W2 and b1/b2.
+// grid.y picks the job (the key and value compressions share one launch).
 template <typename T, int HD>
-__global__ void __launch_bounds__(kWaves * 64) mlp_fwd_kernel(const T* x, const uint8_t* valid, int H, int N, int l,
-                                                              long long rows, const T* w1t, const float* b1,
-                                                              const float* w2, const float* b2, float* out,
-                                                              float* pre_out, T* out_lp, float lp_scale) {
+__global__ void __launch_bounds__(kWaves * 64) mlp_fwd_kernel(const uint8_t* valid, int H, int N, int l,
+                                                              long long rows, MlpFwdJob j0, MlpFwdJob j1) {
+  const MlpFwdJob& job = blockIdx.y ? j1 : j0;
+  const T* x = (const T*)job.x;
+  const T* w1t = (const T*)job.w1t;
+  const float *b1 = job.b1, *w2 = job.w2, *b2 = job.b2;
+  float *out = job.out, *pre_out = job.pre;
+  T* out_lp = (T*)job.out_lp;
+  const float lp_scale = job.lp_scale;
   constexpr int OB = HD / 16;  // 16-wide output blocks
   __shared__ float w2s[HD * HD];
   __shared__ float b1s[HD], b2s[HD];
@@ -780,23 +797,31 @@ hipError_t compress_bwd_impl(const Dims& D, const void* x, const uint8_t* valid,
   return hipGetLastError();
 }
 
+// n (1 or 2) compressions of the same shape; with the MLP they share one launch (grid.y).
 template <typename T, int HD>
-hipError_t compress_impl(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi, float* out,
-                         float* pre, void* out_lp, void* w1t_ws, hipStream_t st, float lp_scale) {
+hipError_t compress_impl(const Dims& D, const CompressJob* jobs, int n, const uint8_t* valid, hipStream_t st) {
   const long long rows = D.cmp_rows();
   if (D.pool == 1) {
     const long long tot = rows * HD;
-    hipLaunchKernelGGL(mean_pool_kernel<T>, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, st, (const T*)x, valid,
-                       D.H, D.N, D.l, HD, rows, out, (T*)out_lp, lp_scale);
+    for (int i = 0; i < n; ++i)
+      hipLaunchKernelGGL(mean_pool_kernel<T>, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, st,
+                         (const T*)jobs[i].x, valid, D.H, D.N, D.l, HD, rows, jobs[i].out, (T*)jobs[i].out_lp,
+                         jobs[i].lp_scale);
     return hipGetLastError();
   }
   const int ld = D.l * HD;
-  T* w1t = (T*)w1t_ws;
-  hipLaunchKernelGGL(transpose_w1_kernel<T>, dim3((ld * HD + 255) / 256), dim3(256), 0, st, phi.w1, ld, HD, w1t);
+  MlpFwdJob mj[2];
+  for (int i = 0; i < n; ++i) {
+    const CompressJob& c = jobs[i];
+    hipLaunchKernelGGL(transpose_w1_kernel<T>, dim3((ld * HD + 255) / 256), dim3(256), 0, st, c.phi.w1, ld, HD,
+                       (T*)c.w1t_ws);
+    mj[i] = MlpFwdJob{c.x, c.w1t_ws, c.phi.b1, c.phi.w2, c.phi.b2, c.out, c.pre, c.out_lp, c.lp_scale};
+  }
+  if (n == 1) mj[1] = mj[0];
   const long long per_wg = (long long)kWaves * 16 * kRB;
   const unsigned grid = (unsigned)((rows + per_wg - 1) / per_wg);
-  hipLaunchKernelGGL((mlp_fwd_kernel<T, HD>), dim3(grid), dim3(kWaves * 64), 0, st, (const T*)x, valid, D.H, D.N,
-                     D.l, rows, (const T*)w1t, phi.b1, phi.w2, phi.b2, out, pre, (T*)out_lp, lp_scale);
+  hipLaunchKernelGGL((mlp_fwd_kernel<T, HD>), dim3(grid, (unsigned)n), dim3(kWaves * 64), 0, st, valid, D.H, D.N, D.l,
+                     rows, mj[0], mj[1]);
   return hipGetLastError();
 }
 
@@ -830,14 +855,11 @@ hipError_t launch_compress_bwd(const Dims& D, const void* x, const uint8_t* vali
   return BSA_DISPATCH(compress_bwd_impl, D, x, valid, phi, pre, dy, dx_accum, grad, ws, st);
 }
 
-hipError_t launch_compress_fwd(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi, float* out,
-                               float* pre, void* out_lp, void* w1t_ws, hipStream_t st, float lp_scale) {
-  if (D.bf16) {
-    return D.d == 64 ? compress_impl<bf16_t, 64>(D, x, valid, phi, out, pre, out_lp, w1t_ws, st, lp_scale)
-                     : compress_impl<bf16_t, 32>(D, x, valid, phi, out, pre, out_lp, w1t_ws, st, lp_scale);
-  }
-  return D.d == 64 ? compress_impl<float, 64>(D, x, valid, phi, out, pre, out_lp, w1t_ws, st, lp_scale)
-                   : compress_impl<float, 32>(D, x, valid, phi, out, pre, out_lp, w1t_ws, st, lp_scale);
+hipError_t launch_compress_fwd(const Dims& D, const CompressJob* jobs, int n, const uint8_t* valid, hipStream_t st) {
+  if (n < 1 || n > 2) return hipErrorInvalidValue;
+  if (D.bf16)
+    return D.d == 64 ? compress_impl<bf16_t, 64>(D, jobs, n, valid, st) : compress_impl<bf16_t, 32>(D, jobs, n, valid, st);
+  return D.d == 64 ? compress_impl<float, 64>(D, jobs, n, valid, st) : compress_impl<float, 32>(D, jobs, n, valid, st);
 }
 
 }  // namespace bsa

@@ -45,11 +45,21 @@ hipError_t launch_permute(const void* src, const int* perm, int64_t n_real, int6
 
 // compress.hip: compression phi of Eq. 5 and its backward
 hipError_t launch_block_valid(const Dims& D, const uint8_t* valid, uint8_t* cvalid, hipStream_t st);
-// out_lp: the rows in the storage type, multiplied by lp_scale (the compressed keys of bf16
-// layers carry the softmax scale times log2(e) there; see launch_cmp_fwd)
-hipError_t launch_compress_fwd(const Dims& D, const void* x, const uint8_t* valid, const Mlp& phi,
-                               float* out, float* pre, void* out_lp, void* w1t_ws, hipStream_t st,
-                               float lp_scale = 1.0f);
+// One compression: x [B, H, N, d] in the storage type; out (float32) and out_lp (the rows in
+// the storage type, multiplied by lp_scale: the compressed keys of bf16 layers carry the
+// softmax scale times log2(e) there; see launch_cmp_fwd) are [B, H, N/l, d]; pre: the MLP's
+// pre-activations (unused for mean pooling); w1t_ws: l*d*d elements of workspace.
+struct CompressJob {
+  const void* x;
+  Mlp phi;
+  float* out;
+  float* pre;
+  void* out_lp;
+  void* w1t_ws;
+  float lp_scale;
+};
+// n = 1 or 2 compressions of the same shape (the keys and values share one launch)
+hipError_t launch_compress_fwd(const Dims& D, const CompressJob* jobs, int n, const uint8_t* valid, hipStream_t st);
 // the bf16 layers' scale of the compressed keys' storage-type copy
 inline float cmp_key_scale(const Dims& D) { return D.bf16 ? D.scale * 1.4426950408889634f : 1.0f; }
 
