@@ -29,6 +29,7 @@ constexpr int kSortItems = 8;
 constexpr int kSortTile = kSortThreads * kSortItems;  // 2048 keys per workgroup
 constexpr int kRadix = 256;                           // 8-bit digits (one per thread)
 constexpr int kScanChunk = 8192;                      // counts scanned per workgroup
+constexpr int kLocalScanTiles = 64;   // up to this many tiles, each scatter workgroup scans itself
 constexpr int kPartTile = 2048;                       // slots per partition workgroup
 constexpr int kBottom = 1024;                         // node size finished in LDS
 
@@ -149,7 +150,9 @@ __global__ void __launch_bounds__(1024) sort_scan_sums_kernel(uint32_t* sums, in
 // Stable scatter of one tile. Items are taken in index order, 256 per round: within a
 // round, an item's rank among equal digits comes from eight ballots (lanes of its wave
 // with the same digit and a lower lane id) plus the counts of the lower waves and of the
-// earlier rounds, all kept per digit in LDS.
+// earlier rounds, all kept per digit in LDS. sums == nullptr (few tiles): the tile's output
+// starts come from the unscanned counts, each thread summing its digit's row of tiles and
+// the workgroup scanning those totals over the digits (no scan launches).
 __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(const uint32_t* keys, const uint32_t* vals,
                                                                     uint32_t* keys_out, uint32_t* vals_out,
                                                                     int m, int pass, int n_real, int ntiles,
@@ -162,7 +165,18 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(const uint32
   const int lane = t & 63, wid = t >> 6;
   const uint32_t* K = keys + (size_t)a * m;
   const uint32_t* V = vals + (size_t)a * m;
-  {
+  if (sums == nullptr) {
+    __shared__ int tmp[kSortThreads / 64 + 1];
+    const uint32_t* hd = hist + ((size_t)a * kRadix + t) * ntiles;   // digit t's counts over tiles
+    uint32_t tot = 0, part = 0;
+    for (int tl = 0; tl < ntiles; ++tl) {
+      const uint32_t c = hd[tl];
+      tot += c;
+      part += tl < tile ? c : 0u;
+    }
+    base[t] = (uint32_t)block_exclusive_scan((int)tot, tmp, nullptr) + part;
+    run[t] = 0;
+  } else {
     const size_t e = (size_t)t * ntiles + tile;   // digit-major entry of (digit t, this tile)
     base[t] = hist[(size_t)a * kRadix * ntiles + e] + sums[(size_t)a * nchunks + e / kScanChunk];
     run[t] = 0;
@@ -225,11 +239,10 @@ struct NodeSplit {
   int cnt;
 };
 
-__global__ void node_split_kernel(const float* pts, int dim, int n_real, int n_pad, int log2_npad,
-                                  int log2c, int nodes, const int* lists, NodeSplit* out) {
-  int nd = blockIdx.x * blockDim.x + threadIdx.x;
-  if (nd >= nodes) return;
-  const size_t slots = (size_t)(nodes) << log2c;
+// The split of node nd (of `slots` list slots in all): the axis of largest spread of its
+// real points, and the median (the left child takes the ceiling half).
+__device__ NodeSplit node_split_of(const float* pts, int dim, int n_real, int n_pad, int log2_npad, int log2c,
+                                   size_t slots, const int* lists, int nd) {
   const int per_cloud = n_pad >> log2c;
   int cnt = node_count(n_real, log2_npad, log2c, nd % per_cloud);
   size_t start = (size_t)nd << log2c;
@@ -245,7 +258,7 @@ __global__ void node_split_kernel(const float* pts, int dim, int n_real, int n_p
     s.med_idx = lists[s.axis * slots + start + (cnt + 1) / 2 - 1];
     s.med = coord(pts, dim, s.med_idx, s.axis);
   }
-  out[nd] = s;
+  return s;
 }
 
 __device__ __forceinline__ bool goes_left(const float* pts, int dim, int g, const NodeSplit& s) {
@@ -253,16 +266,25 @@ __device__ __forceinline__ bool goes_left(const float* pts, int dim, int g, cons
   return c < s.med || (c == s.med && g <= s.med_idx);
 }
 
-__global__ void __launch_bounds__(256) part_count_kernel(const float* pts, int dim, int log2c, const int* lists,
-                                                         const NodeSplit* splits, int tiles_per_list,
-                                                         int* tilecnt) {
+// Left-going points of one tile of one axis list. Each workgroup forms its node's split
+// itself (a tile lies inside one node); the node's first tile of axis 0 stores it for the
+// scatter.
+__global__ void __launch_bounds__(256) part_count_kernel(const float* pts, int dim, int n_real, int n_pad,
+                                                         int log2_npad, int log2c, const int* lists,
+                                                         NodeSplit* splits, int tiles_per_list, int* tilecnt) {
   __shared__ int tmp[8];
+  __shared__ NodeSplit sps;
   const int a = blockIdx.y, tile = blockIdx.x;
   const size_t slots = (size_t)tiles_per_list * kPartTile;
   const size_t s0 = (size_t)tile * kPartTile;
   const int nd = (int)(s0 >> log2c);
-  NodeSplit sp = splits[nd];
   const int off = (int)(s0 - ((size_t)nd << log2c));
+  if (threadIdx.x == 0) {
+    sps = node_split_of(pts, dim, n_real, n_pad, log2_npad, log2c, slots, lists, nd);
+    if (a == 0 && off == 0) splits[nd] = sps;
+  }
+  __syncthreads();
+  const NodeSplit sp = sps;
   int c = 0;
   for (int i = threadIdx.x; i < kPartTile; i += 256) {
     if (off + i < sp.cnt) c += goes_left(pts, dim, lists[a * slots + s0 + i], sp);
@@ -592,13 +614,16 @@ hipError_t launch_build_tree(const float* pts, int64_t n_real, int dim, int64_t 
                      (int)m, ka, va);
   int passes = 4;
   for (int bits = 0; (1 << bits) < batch; bits += 8) ++passes;
+  const bool local_scan = ntiles <= kLocalScanTiles;
   for (int pass = 0; pass < passes; ++pass) {
     hipLaunchKernelGGL(sort_hist_kernel, dim3(ntiles, 3), dim3(kSortThreads), 0, st, ka, va, (int)m, pass,
                        (int)n_real, ntiles, hist);
-    hipLaunchKernelGGL(sort_scan_kernel, dim3(nchunks, 3), dim3(1024), 0, st, hist, kRadix * ntiles, sums);
-    if (nchunks > 1) hipLaunchKernelGGL(sort_scan_sums_kernel, dim3(1, 3), dim3(1024), 0, st, sums, nchunks);
+    if (!local_scan) {
+      hipLaunchKernelGGL(sort_scan_kernel, dim3(nchunks, 3), dim3(1024), 0, st, hist, kRadix * ntiles, sums);
+      if (nchunks > 1) hipLaunchKernelGGL(sort_scan_sums_kernel, dim3(1, 3), dim3(1024), 0, st, sums, nchunks);
+    }
     hipLaunchKernelGGL(sort_scatter_kernel, dim3(ntiles, 3), dim3(kSortThreads), 0, st, ka, va, kb, vb,
-                       (int)m, pass, (int)n_real, ntiles, hist, sums, nchunks);
+                       (int)m, pass, (int)n_real, ntiles, hist, local_scan ? nullptr : sums, nchunks);
     std::swap(ka, kb);
     std::swap(va, vb);
   }
@@ -607,12 +632,9 @@ hipError_t launch_build_tree(const float* pts, int64_t n_real, int dim, int64_t 
   const int log2_npad = ilog2(n_pad);
   const int log2t = log2_npad < 10 ? log2_npad : 10;
   for (int log2c = log2_npad; log2c > log2t; --log2c) {
-    const int nodes = (int)(slots >> log2c);
     const int tiles = (int)(slots / kPartTile);
-    hipLaunchKernelGGL(node_split_kernel, dim3((nodes + 63) / 64), dim3(64), 0, st, pts, dim, (int)n_real,
-                       (int)n_pad, log2_npad, log2c, nodes, la, splits);
-    hipLaunchKernelGGL(part_count_kernel, dim3(tiles, 3), dim3(256), 0, st, pts, dim, log2c, la, splits,
-                       tiles, tilecnt);
+    hipLaunchKernelGGL(part_count_kernel, dim3(tiles, 3), dim3(256), 0, st, pts, dim, (int)n_real, (int)n_pad,
+                       log2_npad, log2c, la, splits, tiles, tilecnt);
     hipLaunchKernelGGL(part_scatter_kernel, dim3(tiles, 3), dim3(256), 0, st, pts, dim, log2c, la, lb,
                        splits, tiles, tilecnt);
     std::swap(la, lb);
@@ -636,13 +658,16 @@ hipError_t launch_radix_sort_pairs(uint32_t* keys, uint32_t* vals, uint32_t* key
   uint32_t* sums = hist + (size_t)kRadix * ntiles;
   const int passes = (bits + 7) / 8;  // key digits only (pass < 4)
   uint32_t *ka = keys, *va = vals, *kb = keys_tmp, *vb = vals_tmp;
+  const bool local_scan = ntiles <= kLocalScanTiles;
   for (int pass = 0; pass < passes; ++pass) {
     hipLaunchKernelGGL(sort_hist_kernel, dim3(ntiles, 1), dim3(kSortThreads), 0, st, ka, va, (int)n, pass, 1, ntiles,
                        hist);
-    hipLaunchKernelGGL(sort_scan_kernel, dim3(nchunks, 1), dim3(1024), 0, st, hist, kRadix * ntiles, sums);
-    if (nchunks > 1) hipLaunchKernelGGL(sort_scan_sums_kernel, dim3(1, 1), dim3(1024), 0, st, sums, nchunks);
+    if (!local_scan) {
+      hipLaunchKernelGGL(sort_scan_kernel, dim3(nchunks, 1), dim3(1024), 0, st, hist, kRadix * ntiles, sums);
+      if (nchunks > 1) hipLaunchKernelGGL(sort_scan_sums_kernel, dim3(1, 1), dim3(1024), 0, st, sums, nchunks);
+    }
     hipLaunchKernelGGL(sort_scatter_kernel, dim3(ntiles, 1), dim3(kSortThreads), 0, st, ka, va, kb, vb, (int)n, pass,
-                       1, ntiles, hist, sums, nchunks);
+                       1, ntiles, hist, local_scan ? nullptr : sums, nchunks);
     std::swap(ka, kb);
     std::swap(va, vb);
   }
