@@ -618,14 +618,14 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
 // MASK = false: every key of the grid is real and in range (no per-key select).
 // PS: prescaled keys (the compressed tokens of bf16 layers): scores start from the stored
 // -x and come out as exponents (dK and dV do not involve the keys).
-template <int HD, int NW, bool BALL, bool MASK = true, bool PS = false>
+// KBW: 16-key blocks per wave (1 halves the registers: more waves for the HBM-bound ball pass).
+template <int HD, int NW, bool BALL, bool MASK = true, bool PS = false, int KBW = 2>
 __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
                                                                    const bf16_t* dout, const uint8_t* kvalid_all,
                                                                    QTerms qt, int H, int N, int nkeys_total, int m,
                                                                    int nchunks, float sl2, float scale, float* dk_out,
                                                                    float* dv_out) {
   constexpr int NCH = HD / 32, DB = HD / 16;
-  constexpr int KBW = 2;  // 16-key blocks per wave
   typedef bf16x8 CT;
   __shared__ __attribute__((aligned(16))) bf16_t qs0[kQT * HD], qs1[kQT * HD];
   __shared__ __attribute__((aligned(16))) bf16_t ds0[kQT * HD], ds1[kQT * HD];
@@ -634,12 +634,12 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t*
   __shared__ __attribute__((aligned(16))) float tx0[kQT], tz0[kQT], tx1[kQT], tz1[kQT];
   const int lane = threadIdx.x & 63, wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, j = lane >> 4;
-  const dim3 blk = xcd_grouped_block(BALL ? m / (NW * 32) : (int)gridDim.x);
+  const dim3 blk = xcd_grouped_block(BALL ? m / (NW * 16 * KBW) : (int)gridDim.x);
   const int bh = blk.z;
   const int b = bh / H;
   const int chunk = blk.y;
-  const int key0 = blk.x * (NW * 32);
-  const int wk0 = key0 + wid * 32;
+  const int key0 = blk.x * (NW * 16 * KBW);
+  const int wk0 = key0 + wid * 16 * KBW;
   int qbeg, qend;
   if (BALL) {
     qbeg = (key0 / m) * m;
@@ -1261,17 +1261,17 @@ void launch_bwd_q(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v,
 
 // Key-major pass launcher: bf16 layers take the direct-load kernel, f32 layers the
 // register-staged one. Non-ball (compressed) launches of bf16 layers read prescaled keys.
-template <typename T, int HD, int NW, bool BALL>
+template <typename T, int HD, int NW, bool BALL, int KBW = 2>
 void launch_bwd_kv(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v, const T* dout,
                    const uint8_t* kvalid, QTerms qt, int H, int N, int nkeys_total, int m, int nchunks, float sl2,
                    float scale, float* dk, float* dv) {
   if constexpr (sizeof(T) == 2) {
-    if (kvalid == nullptr && nkeys_total % (NW * 32) == 0)
-      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, false, !BALL>), grid, dim3(NW * 64), 0, st, q, k,
-                         v, dout, kvalid, qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
+    if (kvalid == nullptr && nkeys_total % (NW * 16 * KBW) == 0)
+      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, false, !BALL, KBW>), grid, dim3(NW * 64), 0, st, q,
+                         k, v, dout, kvalid, qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
     else
-      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, true, !BALL>), grid, dim3(NW * 64), 0, st, q, k,
-                         v, dout, kvalid, qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
+      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, true, !BALL, KBW>), grid, dim3(NW * 64), 0, st, q,
+                         k, v, dout, kvalid, qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
   }
   else
     hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, NW, BALL>), grid, dim3(NW * 64), 0, st, q, k, v, dout, kvalid, qt,
@@ -1352,12 +1352,18 @@ hipError_t bwd_stage_impl(const Dims& D, const BwdArgs& A, BwdStage stage, hipSt
     }
     case BwdStage::kv_ball:   // dK, dV of the ball branch (written)
       BSA_PHASE("bwd.kv_ball", st, {
-        if (D.m >= 128)
+        // bf16: one 16-key block per wave (64 keys per workgroup; ball_size >= 64): half the
+        // registers, twice the waves for this HBM-bound pass
+        if constexpr (sizeof(T) == 2) {
+          (launch_bwd_kv<T, HD, 4, true, 1>)(dim3(D.N / 64, 1, D.B * D.H), st, q, k, v, dout, A.valid, qball, D.H,
+                                           D.N, D.N, D.m, 1, sl2, D.scale, A.dk, A.dv);
+        } else if (D.m >= 128) {
           (launch_bwd_kv<T, HD, 4, true>)(dim3(D.N / 128, 1, D.B * D.H), st, q, k, v, dout, A.valid, qball, D.H,
                                         D.N, D.N, D.m, 1, sl2, D.scale, A.dk, A.dv);
-        else
+        } else {
           (launch_bwd_kv<T, HD, 2, true>)(dim3(D.N / 64, 1, D.B * D.H), st, q, k, v, dout, A.valid, qball, D.H,
                                         D.N, D.N, D.m, 1, sl2, D.scale, A.dk, A.dv);
+        }
       });
       break;
     case BwdStage::kv_cmp: {   // dK^, dV^ of the compressed branch: chunked partials, fixed-order sum
