@@ -89,17 +89,20 @@ __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, 
 }
 
 // Instruction interleaving of the pipelined forward's two regions (scheduling-group
-// barriers of the AMDGPU backend: 0x8 MFMA, 0x2 VALU, 0x100 LDS read). Region 1: NM score
-// MFMAs, each followed by five VALU instructions of the exponentials (about 80 per tile),
-// the K fragments read two ahead. Region 2: NM P V MFMAs, each followed by two VALU
-// instructions of the next tile's row maxima, its V^T fragment reads (ND) spread among them.
+// barriers of the AMDGPU backend: 0x8 MFMA, 0x400 transcendental, 0x2 other VALU, 0x100
+// LDS read; the VALU group does not take the exponentials, which otherwise cluster). Region
+// 1: NM score MFMAs, each followed by two exponentials and two other VALU instructions of
+// the probabilities, the K fragments read two ahead. Region 2: NM P V MFMAs, each followed
+// by two VALU instructions of the next tile's row maxima, its V^T fragment reads (ND)
+// spread among them.
 template <int NM>
 __device__ __forceinline__ void interleave_scores_exps() {
   __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
   for (int i = 0; i < NM; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+    __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
     if (i % 2 == 0) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
   }
 }
