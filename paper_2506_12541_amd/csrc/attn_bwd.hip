@@ -619,12 +619,14 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
 // PS: prescaled keys (the compressed tokens of bf16 layers): scores start from the stored
 // -x and come out as exponents (dK and dV do not involve the keys).
 // KBW: 16-key blocks per wave (1 halves the registers: more waves for the HBM-bound ball pass).
+// The unmasked compressed pass is held to 168 registers, three waves per SIMD instead of
+// two: its MFMA pipe idles while a wave waits on its LDS reads and on its own results,
+// and a third wave fills more of that (a few registers spill, outside the loop).
 template <int HD, int NW, bool BALL, bool MASK = true, bool PS = false, int KBW = 2>
-__global__ void __launch_bounds__(NW * 64) dense_bwd_kv_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
-                                                                   const bf16_t* dout, const uint8_t* kvalid_all,
-                                                                   QTerms qt, int H, int N, int nkeys_total, int m,
-                                                                   int nchunks, float sl2, float scale, float* dk_out,
-                                                                   float* dv_out) {
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(PS && !MASK ? 3 : 1)))
+dense_bwd_kv_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v, const bf16_t* dout,
+                        const uint8_t* kvalid_all, QTerms qt, int H, int N, int nkeys_total, int m, int nchunks,
+                        float sl2, float scale, float* dk_out, float* dv_out) {
   constexpr int NCH = HD / 32, DB = HD / 16;
   typedef bf16x8 CT;
   __shared__ __attribute__((aligned(16))) bf16_t qs0[kQT * HD], qs1[kQT * HD];
