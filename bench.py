@@ -84,6 +84,7 @@ def phase_flops(cfg, variant="bsa"):
         f[f"fwd.{br}"] = 4.0 * pairs[br] * d * B * H
         f[f"bwd.dq_{br}"] = 2.0 * pairs[br] * d * B * H
         f[f"bwd.{kv}"] = 8.0 * pairs[br] * d * B * H
+    f["bwd.kv"] = f["bwd.kv_ball"] + f["bwd.kv_cmp"]   # both key-major passes in one launch
     return f
 
 
@@ -104,7 +105,7 @@ def phase_bytes(cfg, variant="bsa"):
     x = R * d * e                 # one token tensor in the storage type
     xc = Rc * d * e
     sel = Rg * k * 4
-    return {
+    out = {
         "tree": B * N * (3 * 4 + 4),
         "permute": 3 * 2 * x + 2 * B * N * 3 * 4,
         "fwd.compress": (3 if gc else 2) * (x + Rc * d * (4 + 4 + e)),
@@ -123,11 +124,18 @@ def phase_bytes(cfg, variant="bsa"):
         "bwd.slc_csr": 4 * sel,
         "bwd.mlp": (3 if gc else 2) * (2 * x + 2 * R * d * 4 + 3 * Rc * d * 4),
     }
+    # the key-major passes in one launch: Q and dO once (unless the compressed pass reads
+    # the coarse queries)
+    out["bwd.kv"] = out["bwd.kv_ball"] + out["bwd.kv_cmp"] - (0 if gc else 2 * x)
+    return out
 
 
-# the phases of each attention branch, forward and backward
+# the phases of each attention branch, forward and backward; where the ball and
+# compressed key-major passes share one launch (phase bwd.kv) that launch is its own entry
+# and the two branches' entries hold their forward and dQ phases
 BRANCH_PHASES = {"ball": ("fwd.ball", "bwd.kv_ball", "bwd.dq_ball"),
                  "cmp": ("fwd.cmp", "bwd.kv_cmp", "bwd.dq_cmp"),
+                 "ball_cmp_kv": ("bwd.kv",),
                  "slc": ("fwd.slc", "bwd.slc_csr", "bwd.slc_kv", "bwd.dq_slc")}
 
 
@@ -180,11 +188,12 @@ def rooflines(cfg, variant, ms):
 
 # single-launch phases whose work is a dense bf16 contraction (roofline candidates)
 PHASES = ("tree", "permute", "fwd.compress", "fwd.select", "fwd.ball", "fwd.cmp", "fwd.slc", "fwd.gate", "bwd.gate",
-          "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc", "bwd.kv_ball", "bwd.kv_cmp", "bwd.mlp", "bwd.slc_csr", "bwd.slc_kv")
+          "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc", "bwd.kv_ball", "bwd.kv_cmp", "bwd.kv", "bwd.mlp", "bwd.slc_csr",
+          "bwd.slc_kv")
 PHASE_STEPS = 5   # steps of each phase-breakdown pass (run before the timed region)
 FLUSH_BYTES = 512 << 20   # written before each cold step: twice the MALL
 MFMA_PHASES = ("fwd.ball", "fwd.cmp", "fwd.slc", "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc", "bwd.kv_ball",
-               "bwd.kv_cmp")
+               "bwd.kv_cmp", "bwd.kv")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_{phase}_{workload}.txt")
 
 
@@ -462,8 +471,8 @@ def parse():
     ap.add_argument("--copy-calibration", action="store_true", help="run only the 1 GiB plain copy")
     ap.add_argument("--summarize-traffic", nargs=4, metavar="CSV",
                     help="counter CSVs: FETCH_SIZE bench, WRITE_SIZE bench, FETCH_SIZE copy, WRITE_SIZE copy")
-    ap.add_argument("--phase", default="bwd.kv_cmp")
-    ap.add_argument("--kernel", default="dense_bwd_kv_kernel")
+    ap.add_argument("--phase", default="bwd.kv")
+    ap.add_argument("--kernel", default="dense_bwd_kv_pair_kernel<64, false>")
     ap.add_argument("--sources", default="paper_2506_12541_amd/csrc/attn_bwd.hip paper_2506_12541_amd/csrc/attn_common.hpp "
                                          "paper_2506_12541_amd/csrc/common.hpp paper_2506_12541_amd/csrc/kernels.hpp "
                                          "paper_2506_12541_amd/build.py")

@@ -618,8 +618,7 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   // share CUs well, and the compressed pass's own time then includes the sharing.)
   AuxJoin joiner(aux, st);
   BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::prep, st), "backward row terms");
-  BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::kv_ball, st), "ball dK/dV");
-  BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::kv_cmp, st), "compressed dK/dV");
+  BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::kv_pair, st), "ball and compressed dK/dV");
   if (aux.s != st && (hipEventRecord(aux.fork, st) != hipSuccess || hipStreamWaitEvent(aux.s, aux.fork, 0) != hipSuccess))
     return fail(BSA_ERR_HIP, "forking the auxiliary stream failed");
   BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::dq_ball, aux.s), "ball dQ");

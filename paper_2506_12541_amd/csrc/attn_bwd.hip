@@ -622,21 +622,46 @@ __global__ void __launch_bounds__(NW * 64) dense_bwd_kv_kernel(const T* q, const
 // The unmasked compressed pass is held to 168 registers, three waves per SIMD instead of
 // two: its MFMA pipe idles while a wave waits on its LDS reads and on its own results,
 // and a third wave fills more of that (a few registers spill, outside the loop).
-template <int HD, int NW, bool BALL, bool MASK = true, bool PS = false, int KBW = 2>
-__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(PS && !MASK ? 3 : 1)))
-dense_bwd_kv_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v, const bf16_t* dout,
-                        const uint8_t* kvalid_all, QTerms qt, int H, int N, int nkeys_total, int m, int nchunks,
-                        float sl2, float scale, float* dk_out, float* dv_out) {
+// LDS of the key-major pass: query and dO tiles and the row terms, double buffered
+// (distinct objects, so that the compiler can tell in-flight loads into one buffer from
+// reads of the other). The row terms are two arrays (log2 LSE - log2 s, and R) so that a
+// lane reads the values of its four accumulator rows with one 16-byte load.
+struct KvLds {
+  bf16_t *qs0, *qs1, *ds0, *ds1;
+  float *tx0, *tz0, *tx1, *tz1;
+};
+#define BSA_KV_LDS(L)                                                                      \
+  __shared__ __attribute__((aligned(16))) bf16_t L##_qs0[kQT * HD], L##_qs1[kQT * HD];     \
+  __shared__ __attribute__((aligned(16))) bf16_t L##_ds0[kQT * HD], L##_ds1[kQT * HD];     \
+  __shared__ __attribute__((aligned(16))) float L##_tx0[kQT], L##_tz0[kQT], L##_tx1[kQT], \
+      L##_tz1[kQT];                                                                        \
+  const KvLds L{L##_qs0, L##_qs1, L##_ds0, L##_ds1, L##_tx0, L##_tz0, L##_tx1, L##_tz1}
+
+struct KvArgs {
+  const bf16_t *q, *k, *v, *dout;
+  const uint8_t* kvalid_all;
+  QTerms qt;
+  int H, N, nkeys_total, m, nchunks;
+  float sl2, scale;
+  float *dk_out, *dv_out;
+};
+
+// One workgroup of the pass: `lin` is its linear id in a grid of shape `grid`.
+template <int HD, int NW, bool BALL, bool MASK, bool PS, int KBW>
+__device__ __forceinline__ void kv_dma_body(const KvLds& L, dim3 grid, unsigned lin, const KvArgs& a) {
   constexpr int NCH = HD / 32, DB = HD / 16;
   typedef bf16x8 CT;
-  __shared__ __attribute__((aligned(16))) bf16_t qs0[kQT * HD], qs1[kQT * HD];
-  __shared__ __attribute__((aligned(16))) bf16_t ds0[kQT * HD], ds1[kQT * HD];
-  // row terms as two arrays (log2 LSE - log2 s, and R) so that a lane reads the values of
-  // its four accumulator rows with one 16-byte load
-  __shared__ __attribute__((aligned(16))) float tx0[kQT], tz0[kQT], tx1[kQT], tz1[kQT];
+  bf16_t *const qs0 = L.qs0, *const qs1 = L.qs1, *const ds0 = L.ds0, *const ds1 = L.ds1;
+  float *const tx0 = L.tx0, *const tz0 = L.tz0, *const tx1 = L.tx1, *const tz1 = L.tz1;
+  const bf16_t *const q = a.q, *const k = a.k, *const v = a.v, *const dout = a.dout;
+  const uint8_t* const kvalid_all = a.kvalid_all;
+  const QTerms qt = a.qt;
+  const int H = a.H, N = a.N, nkeys_total = a.nkeys_total, m = a.m, nchunks = a.nchunks;
+  const float sl2 = a.sl2, scale = a.scale;
+  float *const dk_out = a.dk_out, *const dv_out = a.dv_out;
   const int lane = threadIdx.x & 63, wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, j = lane >> 4;
-  const dim3 blk = xcd_grouped_block(BALL ? m / (NW * 16 * KBW) : (int)gridDim.x);
+  const dim3 blk = xcd_grouped_block_at(lin, grid, BALL ? m / (NW * 16 * KBW) : (int)grid.x);
   const int bh = blk.z;
   const int b = bh / H;
   const int chunk = blk.y;
@@ -751,7 +776,7 @@ dense_bwd_kv_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v, const
     if (t0 + kQT < qend) step(t0 + kQT, qs1, ds1, tx1, tz1, qs0, ds0, tx0, tz0);
   }
   // lane: key wk0 + 16kb + r, dims 16db + 4j + i; dka holds -dK / scale
-  const size_t out_base = (size_t)chunk * ((size_t)gridDim.z * nkeys_total * HD);
+  const size_t out_base = (size_t)chunk * ((size_t)grid.z * nkeys_total * HD);
 #pragma unroll
   for (int kb = 0; kb < KBW; ++kb) {
     const int key = wk0 + 16 * kb + r;
@@ -763,6 +788,31 @@ dense_bwd_kv_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v, const
       store4(dv_out + off + 16 * db + 4 * j, dva[kb][db], 1.0f);
     }
   }
+}
+
+
+// The pass as its own launch.
+template <int HD, int NW, bool BALL, bool MASK = true, bool PS = false, int KBW = 2>
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(PS && !MASK ? 3 : 1)))
+dense_bwd_kv_dma_kernel(KvArgs a) {
+  BSA_KV_LDS(L);
+  kv_dma_body<HD, NW, BALL, MASK, PS, KBW>(L, gridDim, blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z),
+                                          a);
+}
+
+// The compressed pass (prescaled keys, unmasked) and the ball pass (one 16-key block per
+// wave) in one launch: the compressed workgroups first, then the ball workgroups, which
+// fill the CUs that the compressed pass's last round leaves idle (its workgroups are long
+// and few, about 2.7 per CU slot) and overlap their HBM traffic with its MFMA work.
+template <int HD, bool BMASK>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
+dense_bwd_kv_pair_kernel(KvArgs cmp, dim3 cgrid, KvArgs ball, dim3 bgrid) {
+  BSA_KV_LDS(L);
+  const unsigned ncmp = cgrid.x * cgrid.y * cgrid.z;
+  if (blockIdx.x < ncmp)
+    kv_dma_body<HD, 4, false, false, true, 2>(L, cgrid, blockIdx.x, cmp);
+  else
+    kv_dma_body<HD, 4, true, BMASK, false, 1>(L, bgrid, blockIdx.x - ncmp, ball);
 }
 
 // ==== selection branch, query-major: dQ over the tokens of the selected blocks ====
@@ -1268,12 +1318,11 @@ void launch_bwd_kv(dim3 grid, hipStream_t st, const T* q, const T* k, const T* v
                    const uint8_t* kvalid, QTerms qt, int H, int N, int nkeys_total, int m, int nchunks, float sl2,
                    float scale, float* dk, float* dv) {
   if constexpr (sizeof(T) == 2) {
+    const KvArgs a{q, k, v, dout, kvalid, qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv};
     if (kvalid == nullptr && nkeys_total % (NW * 16 * KBW) == 0)
-      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, false, !BALL, KBW>), grid, dim3(NW * 64), 0, st, q,
-                         k, v, dout, kvalid, qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
+      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, false, !BALL, KBW>), grid, dim3(NW * 64), 0, st, a);
     else
-      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, true, !BALL, KBW>), grid, dim3(NW * 64), 0, st, q,
-                         k, v, dout, kvalid, qt, H, N, nkeys_total, m, nchunks, sl2, scale, dk, dv);
+      hipLaunchKernelGGL((dense_bwd_kv_dma_kernel<HD, NW, BALL, true, !BALL, KBW>), grid, dim3(NW * 64), 0, st, a);
   }
   else
     hipLaunchKernelGGL((dense_bwd_kv_kernel<T, HD, NW, BALL>), grid, dim3(NW * 64), 0, st, q, k, v, dout, kvalid, qt,
@@ -1368,6 +1417,31 @@ hipError_t bwd_stage_impl(const Dims& D, const BwdArgs& A, BwdStage stage, hipSt
         }
       });
       break;
+    case BwdStage::kv_pair: {   // kv_ball and kv_cmp, in one launch where both are unmasked bf16 passes
+      if constexpr (sizeof(T) == 2) {
+        const int nq = D.gcmp ? nct : D.N;
+        const int nch = nq / kCmpChunks >= kQT ? kCmpChunks : 1;
+        const dim3 cg((nct + 127) / 128, nch, D.B * D.H), bg(D.N / 64, 1, D.B * D.H);
+        if (A.valid == nullptr && nct % 128 == 0 && D.N % 64 == 0 && D.m % 64 == 0 && (cg.x * cg.y * cg.z) % 8 == 0) {
+          const KvArgs cmp{D.gcmp ? qcl : q, kc, vc, D.gcmp ? docl : dout, nullptr, D.gcmp ? qcoarse : qcmp, D.H, nq,
+                           nct, D.m, nch, sl2, D.scale, A.dkc_part, A.dvc_part};
+          const KvArgs ball{q, k, v, dout, nullptr, qball, D.H, D.N, D.N, D.m, 1, sl2, D.scale, A.dk, A.dv};
+          BSA_PHASE("bwd.kv", st,
+                    hipLaunchKernelGGL((dense_bwd_kv_pair_kernel<HD, false>),
+                                       dim3(cg.x * cg.y * cg.z + bg.x * bg.y * bg.z), dim3(256), 0, st, cmp, cg, ball,
+                                       bg));
+          const long long n = D.cmp_rows() * HD;
+          hipLaunchKernelGGL(sum_chunks_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.dkc_part, nch,
+                             n, A.dkc);
+          hipLaunchKernelGGL(sum_chunks_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, A.dvc_part, nch,
+                             n, A.dvc);
+          break;
+        }
+      }
+      hipError_t e = bwd_stage_impl<T, HD>(D, A, BwdStage::kv_ball, st);
+      if (e != hipSuccess) return e;
+      return bwd_stage_impl<T, HD>(D, A, BwdStage::kv_cmp, st);
+    }
     case BwdStage::kv_cmp: {   // dK^, dV^ of the compressed branch: chunked partials, fixed-order sum
       const int nq = D.gcmp ? nct : D.N;   // query rows: tokens, or coarse queries (Eq. 15)
       const int nch = nq / kCmpChunks >= kQT ? kCmpChunks : 1;

@@ -190,15 +190,19 @@ struct TileIO {
 // order: the shared rows then enter that XCD's L2 once instead of once per XCD. The
 // renumbering is a bijection of the grid; it needs gridDim.x % per == 0 and the run count
 // to be a multiple of 8, else the grid is kept.
-__device__ __forceinline__ dim3 xcd_grouped_block(int per) {
+// The same renumbering for a workgroup given by its linear id in a grid of the given
+// shape (a grid that is one part of a launch; its first workgroup's id is a multiple of 8).
+__device__ __forceinline__ dim3 xcd_grouped_block_at(unsigned lin, dim3 g, int per) {
   constexpr unsigned kXcds = 8;
-  const unsigned nx = gridDim.x, ny = gridDim.y;
-  const unsigned runs = nx * ny * gridDim.z / (unsigned)max(per, 1);
-  if (per <= 1 || nx % (unsigned)per != 0 || runs % kXcds != 0) return dim3(blockIdx.x, blockIdx.y, blockIdx.z);
-  const unsigned lin = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
+  const unsigned nx = g.x, ny = g.y;
+  const unsigned runs = nx * ny * g.z / (unsigned)max(per, 1);
+  if (per <= 1 || nx % (unsigned)per != 0 || runs % kXcds != 0) return dim3(lin % nx, (lin / nx) % ny, lin / (nx * ny));
   const unsigned slot = lin / kXcds;
   const unsigned l = ((lin % kXcds) * (runs / kXcds) + slot / per) * per + slot % per;
   return dim3(l % nx, (l / nx) % ny, l / (nx * ny));
+}
+__device__ __forceinline__ dim3 xcd_grouped_block(int per) {
+  return xcd_grouped_block_at(blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z), gridDim, per);
 }
 
 template <int HD>

@@ -137,6 +137,7 @@ struct BwdArgs {
 //            queries' dO and terms under group compression). Every later stage needs it.
 //   kv_ball  writes dK, dV (the first writer of both).
 //   kv_cmp   writes dK^, dV^ (dkc, dvc).
+//   kv_pair  kv_ball and kv_cmp (one launch for unmasked bf16 layers, else the two).
 //   dq_ball  writes dQ (the first writer).
 //   dq_cmp   adds into dQ (group compression: writes the coarse-query gradient instead).
 //   dq_slc   adds into dQ (g >= 8).
@@ -144,7 +145,7 @@ struct BwdArgs {
 // into dK, dV; launch_compress_bwd (compress.hip) adds dK^/dV^'s token gradients into dK,
 // dV. Stages that add into the same tensor must be ordered after its first writer and
 // after each other.
-enum class BwdStage { prep, kv_ball, kv_cmp, dq_ball, dq_cmp, dq_slc };
+enum class BwdStage { prep, kv_ball, kv_cmp, kv_pair, dq_ball, dq_cmp, dq_slc };
 hipError_t launch_bwd_stage(const Dims& D, const BwdArgs& A, BwdStage stage, hipStream_t st);
 hipError_t launch_slc_csr(const Dims& D, const BwdArgs& A, hipStream_t st, const uint32_t** groups_out);
 hipError_t launch_slc_kv(const Dims& D, const BwdArgs& A, const uint32_t* groups, hipStream_t st);
