@@ -63,7 +63,7 @@ def algorithmic_flops(cfg, variant="bsa"):
 # phases that share the chip with a concurrent branch: forward ball + compressed attention
 # beside top-k selection + selection attention; the backward dQ chain beside the
 # compression and selection dK/dV passes
-CONCURRENT_PHASES = ["fwd.ball", "fwd.cmp", "fwd.select", "fwd.slc", "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc",
+CONCURRENT_PHASES = ["fwd.ball", "fwd.cmp", "fwd.ball_cmp", "fwd.select", "fwd.slc", "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc",
                      "bwd.mlp", "bwd.slc_csr", "bwd.slc_kv"]
 
 
@@ -85,6 +85,7 @@ def phase_flops(cfg, variant="bsa"):
         f[f"bwd.dq_{br}"] = 2.0 * pairs[br] * d * B * H
         f[f"bwd.{kv}"] = 8.0 * pairs[br] * d * B * H
     f["bwd.kv"] = f["bwd.kv_ball"] + f["bwd.kv_cmp"]   # both key-major passes in one launch
+    f["fwd.ball_cmp"] = f["fwd.ball"] + f["fwd.cmp"]   # both forward passes in one launch
     return f
 
 
@@ -127,6 +128,7 @@ def phase_bytes(cfg, variant="bsa"):
     # the key-major passes in one launch: Q and dO once (unless the compressed pass reads
     # the coarse queries)
     out["bwd.kv"] = out["bwd.kv_ball"] + out["bwd.kv_cmp"] - (0 if gc else 2 * x)
+    out["fwd.ball_cmp"] = out["fwd.ball"] + out["fwd.cmp"] - (0 if gc else x)
     return out
 
 
@@ -135,6 +137,7 @@ def phase_bytes(cfg, variant="bsa"):
 # and the two branches' entries hold their forward and dQ phases
 BRANCH_PHASES = {"ball": ("fwd.ball", "bwd.kv_ball", "bwd.dq_ball"),
                  "cmp": ("fwd.cmp", "bwd.kv_cmp", "bwd.dq_cmp"),
+                 "ball_cmp_fwd": ("fwd.ball_cmp",),
                  "ball_cmp_kv": ("bwd.kv",),
                  "slc": ("fwd.slc", "bwd.slc_csr", "bwd.slc_kv", "bwd.dq_slc")}
 
@@ -187,12 +190,12 @@ def rooflines(cfg, variant, ms):
 
 
 # single-launch phases whose work is a dense bf16 contraction (roofline candidates)
-PHASES = ("tree", "permute", "fwd.compress", "fwd.select", "fwd.ball", "fwd.cmp", "fwd.slc", "fwd.gate", "bwd.gate",
-          "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc", "bwd.kv_ball", "bwd.kv_cmp", "bwd.kv", "bwd.mlp", "bwd.slc_csr",
-          "bwd.slc_kv")
+PHASES = ("tree", "permute", "fwd.compress", "fwd.select", "fwd.ball", "fwd.cmp", "fwd.ball_cmp", "fwd.slc", "fwd.gate",
+          "bwd.gate", "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc", "bwd.kv_ball", "bwd.kv_cmp", "bwd.kv", "bwd.mlp",
+          "bwd.slc_csr", "bwd.slc_kv")
 PHASE_STEPS = 5   # steps of each phase-breakdown pass (run before the timed region)
 FLUSH_BYTES = 512 << 20   # written before each cold step: twice the MALL
-MFMA_PHASES = ("fwd.ball", "fwd.cmp", "fwd.slc", "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc", "bwd.kv_ball",
+MFMA_PHASES = ("fwd.ball", "fwd.cmp", "fwd.ball_cmp", "fwd.slc", "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc", "bwd.kv_ball",
                "bwd.kv_cmp", "bwd.kv")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_{phase}_{workload}.txt")
 

@@ -524,21 +524,27 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   {
     hipStream_t st_main = st;
     hipStream_t st = aux.s;
-    BSA_STEP("fwd.ball", bsa::launch_ball_fwd(D, q, k, v, valid, ob, lse, st), "ball attention");
-    if (D.gcmp) {
-      float* oc = saved->ocmp;
-      float* lsec = (float*)(w + W.lsec);
-      BSA_STEP("fwd.cmp",
-               (bsa::launch_cmp_coarse_fwd(D, qc_lp, kc_lp, vc_lp, valid ? saved->cvalid : nullptr, oc, lsec, st) !=
-                        hipSuccess
-                    ? hipGetLastError()
-                    : bsa::launch_expand_coarse(D, oc, lsec, valid, saved->o_cmp, lse + rows, st)),
-               "group compression");
+    if (valid == nullptr && bsa::ball_cmp_fwd_fits(D)) {
+      BSA_STEP("fwd.ball_cmp",
+               bsa::launch_ball_cmp_fwd(D, q, k, v, kc_lp, vc_lp, ob, lse, saved->o_cmp, lse + rows, st),
+               "ball and compressed attention");
     } else {
-      BSA_STEP("fwd.cmp",
-               bsa::launch_cmp_fwd(D, q, kc_lp, vc_lp, valid, valid ? saved->cvalid : nullptr, saved->o_cmp,
-                                   lse + rows, st),
-               "compressed attention");
+      BSA_STEP("fwd.ball", bsa::launch_ball_fwd(D, q, k, v, valid, ob, lse, st), "ball attention");
+      if (D.gcmp) {
+        float* oc = saved->ocmp;
+        float* lsec = (float*)(w + W.lsec);
+        const uint8_t* cv = valid ? saved->cvalid : nullptr;
+        BSA_STEP("fwd.cmp",
+                 (bsa::launch_cmp_coarse_fwd(D, qc_lp, kc_lp, vc_lp, cv, oc, lsec, st) != hipSuccess
+                      ? hipGetLastError()
+                      : bsa::launch_expand_coarse(D, oc, lsec, valid, saved->o_cmp, lse + rows, st)),
+                 "group compression");
+      } else {
+        BSA_STEP("fwd.cmp",
+                 bsa::launch_cmp_fwd(D, q, kc_lp, vc_lp, valid, valid ? saved->cvalid : nullptr, saved->o_cmp,
+                                     lse + rows, st),
+                 "compressed attention");
+      }
     }
     (void)st_main;
   }

@@ -131,21 +131,46 @@ __device__ __forceinline__ void interleave_pv_max() {
 // LO: log-sum-exp rows only (the V tiles are not loaded; no output rows).
 // PS: the keys are stored multiplied by sl2 (scores come out in the exponent's units, see
 // WaveAttn); sl2 is then not applied again.
-template <int HD, int QB, int NW, bool BALL, typename OT = bf16_t, bool LO = false, bool MASK = true, bool PS = false>
-__global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q, const bf16_t* k, const bf16_t* v,
-                                                                const uint8_t* qvalid_all, const uint8_t* kvalid_all,
-                                                                int H, int N, int nkeys_total, int m, float sl2,
-                                                                OT* out, float* lse) {
+// LDS of the pipelined forward: K and V tiles and key-validity bytes, double buffered
+// (each buffer its own object)
+struct FwdLds {
+  bf16_t *ks0, *ks1, *vs0, *vs1;
+  uint8_t *ok0, *ok1;
+};
+#define BSA_FWD_LDS(L)                                                                   \
+  __shared__ __attribute__((aligned(16))) bf16_t L##_ks0[kKT * HD], L##_ks1[kKT * HD]; \
+  __shared__ __attribute__((aligned(16))) bf16_t L##_vs0[kKT * HD], L##_vs1[kKT * HD]; \
+  __shared__ uint8_t L##_ok0[kKT], L##_ok1[kKT];                                        \
+  const FwdLds L{L##_ks0, L##_ks1, L##_vs0, L##_vs1, L##_ok0, L##_ok1}
+
+template <typename OT>
+struct FwdArgs {
+  const bf16_t *q, *k, *v;
+  const uint8_t *qvalid_all, *kvalid_all;
+  int H, N, nkeys_total, m;
+  float sl2;
+  OT* out;
+  float* lse;
+};
+
+// One workgroup: `lin` is its linear id in a grid of shape `grid`.
+template <int HD, int QB, int NW, bool BALL, typename OT, bool LO, bool MASK, bool PS>
+__device__ __forceinline__ void fwd_dma_body(const FwdLds& L, dim3 grid, unsigned lin, const FwdArgs<OT>& a) {
   constexpr int kFT = kKT;
   constexpr int KB = kFT / 16;
   typedef WaveAttn<bf16_t, HD, QB, LO, PS> WA;
   typedef typename WA::CT CT;
-  __shared__ __attribute__((aligned(16))) bf16_t ks0[kFT * HD], ks1[kFT * HD];
-  __shared__ __attribute__((aligned(16))) bf16_t vs0[kFT * HD], vs1[kFT * HD];
-  __shared__ uint8_t ok0[kFT], ok1[kFT];
+  bf16_t *const ks0 = L.ks0, *const ks1 = L.ks1, *const vs0 = L.vs0, *const vs1 = L.vs1;
+  uint8_t *const ok0 = L.ok0, *const ok1 = L.ok1;
+  const bf16_t *const q = a.q, *const k = a.k, *const v = a.v;
+  const uint8_t *const qvalid_all = a.qvalid_all, *const kvalid_all = a.kvalid_all;
+  const int H = a.H, N = a.N, nkeys_total = a.nkeys_total, m = a.m;
+  const float sl2 = a.sl2;
+  OT* const out = a.out;
+  float* const lse = a.lse;
   const int lane = threadIdx.x & 63, wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, j = lane >> 4;
-  const dim3 blk = xcd_grouped_block(BALL ? m / (16 * QB * NW) : (int)gridDim.x);
+  const dim3 blk = xcd_grouped_block_at(lin, grid, BALL ? m / (16 * QB * NW) : (int)grid.x);
   const int b = blk.z, h = blk.y;
   const long long bh = (long long)b * H + h;
   const int q0 = blk.x * (16 * QB * NW);
@@ -262,6 +287,28 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(const bf16_t* q,
     step(last{}, t, ks0, ok0, ks1, ok1, vs0, vs1);
   }
   w.finish(lane, bh * N + wq0, out, lse, qval, wq0);
+}
+
+template <int HD, int QB, int NW, bool BALL, typename OT = bf16_t, bool LO = false, bool MASK = true, bool PS = false>
+__global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(FwdArgs<OT> a) {
+  BSA_FWD_LDS(L);
+  fwd_dma_body<HD, QB, NW, BALL, OT, LO, MASK, PS>(L, gridDim,
+                                                   blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z), a);
+}
+
+// The compressed attention (prescaled keys, float32 rows) and the ball attention (bf16
+// rows) of unmasked bf16 layers in one launch: the compressed workgroups first, then the
+// ball workgroups, which fill the CUs that the compressed launch's last round leaves idle
+// and overlap their HBM traffic with its MFMA work.
+template <int HD>
+__global__ void __launch_bounds__(256) dense_fwd_pair_kernel(FwdArgs<float> cmp, dim3 cgrid, FwdArgs<bf16_t> ball,
+                                                             dim3 bgrid) {
+  BSA_FWD_LDS(L);
+  const unsigned ncmp = cgrid.x * cgrid.y * cgrid.z;
+  if (blockIdx.x < ncmp)
+    fwd_dma_body<HD, 2, 4, false, float, false, false, true>(L, cgrid, blockIdx.x, cmp);
+  else
+    fwd_dma_body<HD, 2, 4, true, bf16_t, false, false, false>(L, bgrid, blockIdx.x - ncmp, ball);
 }
 
 // ---- selection kernel: one wave = 16 queries; keys = the selected blocks of its group(s) ----
@@ -503,20 +550,17 @@ void launch_dense_fwd(dim3 grid, hipStream_t st, const void* q, const void* k, c
   if constexpr (sizeof(T) == 2) {
     // every key real and whole 64-key tiles: no per-key select
     const bool mask = kvalid != nullptr || (BALL ? m : nkeys_total) % kKT != 0;
-    const bf16_t *qq = (const bf16_t*)q, *kk = (const bf16_t*)k, *vv = (const bf16_t*)v;
+    const FwdArgs<OT> a{(const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, qvalid, kvalid, H, N, nkeys_total, m,
+                        sl2, (OT*)o, lse};
     const dim3 blk(64 * NW);
     if (o && mask)
-      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, false, true, PS>), grid, blk, 0, st, qq, kk, vv,
-                         qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, false, true, PS>), grid, blk, 0, st, a);
     else if (o)
-      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, false, false, PS>), grid, blk, 0, st, qq, kk, vv,
-                         qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, false, false, PS>), grid, blk, 0, st, a);
     else if (mask)
-      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, true, true, PS>), grid, blk, 0, st, qq, kk, vv,
-                         qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, true, true, PS>), grid, blk, 0, st, a);
     else
-      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, true, false, PS>), grid, blk, 0, st, qq, kk, vv,
-                         qvalid, kvalid, H, N, nkeys_total, m, sl2, (OT*)o, lse);
+      hipLaunchKernelGGL((dense_fwd_dma_kernel<HD, QB, NW, BALL, OT, true, false, PS>), grid, blk, 0, st, a);
   } else {
     if (o)
       hipLaunchKernelGGL((dense_fwd_kernel<T, HD, QB, BALL, OT>), grid, dim3(256), 0, st, (const T*)q, (const T*)k,
@@ -554,6 +598,23 @@ hipError_t cmp_impl(const Dims& D, const void* q, const void* kc, const void* vc
     launch_dense_fwd<T, HD, 1, false, 4, float, true>(dim3(D.N / 64, D.H, D.B), st, q, kc, vc, valid, cvalid,
                                                       D.H, D.N, D.N / D.l, D.m, sl2, o, lse);
   return hipGetLastError();
+}
+
+// Ball and compressed attention of an unmasked bf16 layer in one launch (dense_fwd_pair_kernel).
+template <typename T, int HD>
+hipError_t ball_cmp_impl(const Dims& D, const void* q, const void* k, const void* v, const void* kc, const void* vc,
+                         void* ob, float* lse_ball, float* ocmp, float* lse_cmp, hipStream_t st) {
+  if constexpr (sizeof(T) == 2) {
+    const float sl2 = D.scale * kLog2e;
+    const FwdArgs<float> cmp{(const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, nullptr, nullptr, D.H, D.N,
+                             D.N / D.l, D.m, sl2, ocmp, lse_cmp};
+    const FwdArgs<bf16_t> ball{(const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, nullptr, nullptr, D.H, D.N, D.N,
+                               D.m, sl2, (bf16_t*)ob, lse_ball};
+    const dim3 g(D.N / 128, D.H, D.B);
+    hipLaunchKernelGGL((dense_fwd_pair_kernel<HD>), dim3(2 * g.x * g.y * g.z), dim3(256), 0, st, cmp, g, ball, g);
+    return hipGetLastError();
+  }
+  return hipErrorNotSupported;
 }
 
 // Group compression (Eq. 15): the coarse queries attend to the compressed tokens; rows are
@@ -634,6 +695,18 @@ hipError_t launch_ball_fwd(const Dims& D, const void* q, const void* k, const vo
 hipError_t launch_cmp_fwd(const Dims& D, const void* q, const void* kc, const void* vc, const uint8_t* valid,
                           const uint8_t* cvalid, float* o, float* lse, hipStream_t st) {
   return BSA_DISPATCH(cmp_impl, D, q, kc, vc, valid, cvalid, o, lse, st);
+}
+
+bool ball_cmp_fwd_fits(const Dims& D) {
+  const int nct = D.N / D.l;
+  return D.bf16 && !D.gcmp && D.m >= 128 && D.m % kKT == 0 && D.N % 128 == 0 && nct % kKT == 0 &&
+         (D.N / 128) * D.H * D.B % 8 == 0;
+}
+
+hipError_t launch_ball_cmp_fwd(const Dims& D, const void* q, const void* k, const void* v, const void* kc, const void* vc,
+                               void* ob, float* lse_ball, float* ocmp, float* lse_cmp, hipStream_t st) {
+  if (!ball_cmp_fwd_fits(D)) return hipErrorNotSupported;
+  return BSA_DISPATCH(ball_cmp_impl, D, q, k, v, kc, vc, ob, lse_ball, ocmp, lse_cmp, st);
 }
 
 hipError_t launch_cmp_coarse_fwd(const Dims& D, const void* qc, const void* kc, const void* vc, const uint8_t* cvalid,

@@ -79,6 +79,12 @@ hipError_t launch_cmp_fwd(const Dims& D, const void* q, const void* kc, const vo
                           const uint8_t* cvalid, float* o, float* lse, hipStream_t st);
 hipError_t launch_slc_fwd(const Dims& D, const void* q, const void* k, const void* v, const uint8_t* valid,
                           const int* sel, void* o, float* lse, hipStream_t st);
+// both in one launch for unmasked bf16 layers (call only where ball_cmp_fwd_fits and
+// there is no validity mask; else hipErrorNotSupported): ob and lse_ball as for
+// launch_ball_fwd, ocmp and lse_cmp as for launch_cmp_fwd
+bool ball_cmp_fwd_fits(const Dims& D);
+hipError_t launch_ball_cmp_fwd(const Dims& D, const void* q, const void* k, const void* v, const void* kc, const void* vc,
+                               void* ob, float* lse_ball, float* ocmp, float* lse_cmp, hipStream_t st);
 // group compression (Eq. 15): coarse attention [B, H, N/l, d] (float32 outputs) and its
 // copy to the token rows (float32)
 hipError_t launch_cmp_coarse_fwd(const Dims& D, const void* qc, const void* kc, const void* vc, const uint8_t* cvalid,
