@@ -101,9 +101,18 @@ __global__ void __launch_bounds__(kSortThreads) sort_hist_kernel(const uint32_t*
   __syncthreads();
   const uint32_t* K = keys + (size_t)a * m;
   const uint32_t* V = vals + (size_t)a * m;
+  // every item's loads first (one round trip), then the counts
+  uint32_t kk[kSortItems], vv[kSortItems];
+#pragma unroll
   for (int it = 0; it < kSortItems; ++it) {
-    int i = tile * kSortTile + it * kSortThreads + threadIdx.x;
-    if (i < m) atomicAdd(&cnt[sort_digit(K[i], V[i], pass, n_real)], 1u);
+    const int i = tile * kSortTile + it * kSortThreads + threadIdx.x;
+    kk[it] = i < m ? K[i] : 0u;
+    vv[it] = i < m && pass >= 4 ? V[i] : 0u;
+  }
+#pragma unroll
+  for (int it = 0; it < kSortItems; ++it) {
+    const int i = tile * kSortTile + it * kSortThreads + threadIdx.x;
+    if (i < m) atomicAdd(&cnt[sort_digit(kk[it], vv[it], pass, n_real)], 1u);
   }
   __syncthreads();
   hist[((size_t)a * kRadix + threadIdx.x) * ntiles + tile] = cnt[threadIdx.x];
@@ -184,15 +193,20 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(const uint32
   const uint64_t below = (1ull << lane) - 1ull;
   uint32_t* KO = keys_out + (size_t)a * m;
   uint32_t* VO = vals_out + (size_t)a * m;
+  // the tile's items are loaded before the rounds (one round trip instead of one per round)
+  uint32_t kk[kSortItems], vv[kSortItems];
+#pragma unroll
+  for (int it = 0; it < kSortItems; ++it) {
+    const int i = tile * kSortTile + it * kSortThreads + t;
+    kk[it] = i < m ? K[i] : 0u;
+    vv[it] = i < m ? V[i] : 0u;
+  }
+#pragma unroll
   for (int it = 0; it < kSortItems; ++it) {
     const int i = tile * kSortTile + it * kSortThreads + t;
     const bool ok = i < m;
-    uint32_t k = 0, v = 0, d = 0;
-    if (ok) {
-      k = K[i];
-      v = V[i];
-      d = sort_digit(k, v, pass, n_real);
-    }
+    const uint32_t k = kk[it], v = vv[it];
+    const uint32_t d = ok ? sort_digit(k, v, pass, n_real) : 0u;
 #pragma unroll
     for (int w = 0; w < kSortThreads / 64; ++w) wc[w][t] = 0;
     uint64_t peers = __builtin_amdgcn_ballot_w64(ok);
@@ -240,25 +254,47 @@ struct NodeSplit {
 };
 
 // The split of node nd (of `slots` list slots in all): the axis of largest spread of its
-// real points, and the median (the left child takes the ceiling half).
-__device__ NodeSplit node_split_of(const float* pts, int dim, int n_real, int n_pad, int log2_npad, int log2c,
-                                   size_t slots, const int* lists, int nd) {
+// real points, and the median (the left child takes the ceiling half). Formed by the
+// first nine threads of the workgroup together: each axis's two ends and its median
+// candidate are loaded at once (two dependent round trips instead of eight), then thread
+// 0 picks the axis. Every thread calls it; the split is returned to all of them.
+__device__ NodeSplit node_split_block(const float* pts, int dim, int n_real, int n_pad, int log2_npad, int log2c,
+                                     size_t slots, const int* lists, int nd) {
+  __shared__ float ends[3][2];
+  __shared__ int med_idx[3];
+  __shared__ float med[3];
+  __shared__ NodeSplit out;
   const int per_cloud = n_pad >> log2c;
-  int cnt = node_count(n_real, log2_npad, log2c, nd % per_cloud);
-  size_t start = (size_t)nd << log2c;
-  NodeSplit s{0, -1, 0.0f, cnt};
-  if (cnt > 0) {
-    double best = -1.0;
-    for (int a = 0; a < 3; ++a) {
-      float lo = coord(pts, dim, lists[a * slots + start], a);
-      float hi = coord(pts, dim, lists[a * slots + start + cnt - 1], a);
-      double sp = (double)hi - (double)lo;
-      if (sp > best) { best = sp; s.axis = a; }
+  const int cnt = node_count(n_real, log2_npad, log2c, nd % per_cloud);
+  const size_t start = (size_t)nd << log2c;
+  const int t = threadIdx.x;
+  if (cnt > 0 && t < 9) {
+    if (t < 6) {   // axis t / 2: its lowest (t even) or highest (t odd) coordinate
+      const int ax = t >> 1;
+      ends[ax][t & 1] = coord(pts, dim, lists[ax * slots + start + ((t & 1) ? cnt - 1 : 0)], ax);
+    } else {       // axis t - 6: its median
+      const int ax = t - 6;
+      const int g = lists[ax * slots + start + (cnt + 1) / 2 - 1];
+      med_idx[ax] = g;
+      med[ax] = coord(pts, dim, g, ax);
     }
-    s.med_idx = lists[s.axis * slots + start + (cnt + 1) / 2 - 1];
-    s.med = coord(pts, dim, s.med_idx, s.axis);
   }
-  return s;
+  __syncthreads();
+  if (t == 0) {
+    NodeSplit s{0, -1, 0.0f, cnt};
+    if (cnt > 0) {
+      double best = -1.0;
+      for (int a = 0; a < 3; ++a) {
+        const double sp = (double)ends[a][1] - (double)ends[a][0];
+        if (sp > best) { best = sp; s.axis = a; }
+      }
+      s.med_idx = med_idx[s.axis];
+      s.med = med[s.axis];
+    }
+    out = s;
+  }
+  __syncthreads();
+  return out;
 }
 
 __device__ __forceinline__ bool goes_left(const float* pts, int dim, int g, const NodeSplit& s) {
@@ -273,22 +309,23 @@ __global__ void __launch_bounds__(256) part_count_kernel(const float* pts, int d
                                                          int log2_npad, int log2c, const int* lists,
                                                          NodeSplit* splits, int tiles_per_list, int* tilecnt) {
   __shared__ int tmp[8];
-  __shared__ NodeSplit sps;
   const int a = blockIdx.y, tile = blockIdx.x;
   const size_t slots = (size_t)tiles_per_list * kPartTile;
   const size_t s0 = (size_t)tile * kPartTile;
   const int nd = (int)(s0 >> log2c);
   const int off = (int)(s0 - ((size_t)nd << log2c));
-  if (threadIdx.x == 0) {
-    sps = node_split_of(pts, dim, n_real, n_pad, log2_npad, log2c, slots, lists, nd);
-    if (a == 0 && off == 0) splits[nd] = sps;
+  const NodeSplit sp = node_split_block(pts, dim, n_real, n_pad, log2_npad, log2c, slots, lists, nd);
+  if (threadIdx.x == 0 && a == 0 && off == 0) splits[nd] = sp;
+  // the tile's list entries first, then their coordinates (two round trips)
+  int g[kPartTile / 256];
+#pragma unroll
+  for (int it = 0; it < kPartTile / 256; ++it) {
+    const int i = threadIdx.x + 256 * it;
+    g[it] = off + i < sp.cnt ? lists[a * slots + s0 + i] : -1;
   }
-  __syncthreads();
-  const NodeSplit sp = sps;
   int c = 0;
-  for (int i = threadIdx.x; i < kPartTile; i += 256) {
-    if (off + i < sp.cnt) c += goes_left(pts, dim, lists[a * slots + s0 + i], sp);
-  }
+#pragma unroll
+  for (int it = 0; it < kPartTile / 256; ++it) c += g[it] >= 0 && goes_left(pts, dim, g[it], sp);
   int total;
   block_exclusive_scan(c, tmp, &total);
   if (threadIdx.x == 0) tilecnt[a * tiles_per_list + tile] = total;
