@@ -365,11 +365,13 @@ def summarize_counters(args):
         mops = c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)
         gui = c.get("GRBM_GUI_ACTIVE", float("nan"))
         clk = gui / N_XCD / t if gui == gui else float("nan")   # Hz
-        # issue-serialized time: every MFMA (16x16x32, 16 cycles), transcendental (quarter
-        # rate, 16 cycles) and other VALU instruction (wave64 over 16 lanes, 4 cycles) of
-        # the launch issued one after another on the 1024 SIMDs, at the measured clock
+        # issue-serialized time: every MFMA (16x16x32 bf16: 16 cycles at the published 2.5
+        # PFLOP/s), transcendental (a quarter of the fp32 rate: 8 cycles) and other VALU
+        # instruction (wave64 at the fp32 rate of the published 157.3 TFLOP/s, 32 lanes per
+        # SIMD: 2 cycles; a lower bound, some forms take longer) of the launch issued one
+        # after another on the 1024 SIMDs, at the measured clock
         nm, ntr, nv = (c2.get(x, float("nan")) for x in ("SQ_INSTS_MFMA", "SQ_INSTS_VALU_TRANS_F32", "SQ_INSTS_VALU"))
-        issue_s = (16 * nm + 16 * ntr + 4 * (nv - nm - ntr)) / (N_CU * 4) / clk
+        issue_s = (16 * nm + 8 * ntr + 2 * (nv - nm - ntr)) / (N_CU * 4) / clk
         busy2 = c2.get("SQ_VALU_MFMA_BUSY_CYCLES", float("nan"))
         rows.append({
             "kernel": k, "calls": len(ds), "avg_us": t * 1e6, "gpu_time_pct": 100 * sum(ds) / total,
@@ -398,10 +400,12 @@ def summarize_counters(args):
                  "counts are per dispatch (all waves). Kernels under 0.2% of GPU time are left out. GRBM_GUI_ACTIVE\n"
                  "spans the dispatch's whole busy window, which for a short kernel includes launch and drain time\n"
                  "outside its traced duration: clock and MFMA busy are meaningful for kernels of 100 us and more.\n"
-                 "Issue bound = the time the launch's MFMA (16 cycles each), transcendental (16) and other VALU\n"
-                 "instructions (4; SQ_INSTS_VALU counts MFMA and transcendental instructions too) take issued one\n"
-                 "after another on the 1024 SIMDs at the measured clock, over the duration: near 100 the kernel is\n"
-                 "bound by issue with MFMA and VALU work serialised. Co-exec = SQ_VALU_MFMA_COEXEC_CYCLES /\n"
+                 "Issue bound = the time the launch's MFMA (16 cycles each, from the bf16 peak), transcendental\n"
+                 "(8, a quarter of the fp32 rate) and other VALU instructions (2, the fp32 rate of the published\n"
+                 "157.3 TFLOP/s; a lower bound; SQ_INSTS_VALU counts MFMA and transcendental instructions too)\n"
+                 "take issued one after another on the 1024 SIMDs at the measured clock, over the duration: near\n"
+                 "100 the kernel is bound by issue with MFMA and VALU work serialised, well below 100 it waits on\n"
+                 "latency (LDS, memory, dependencies). Co-exec = SQ_VALU_MFMA_COEXEC_CYCLES /\n"
                  "SQ_VALU_MFMA_BUSY_CYCLES, the share of MFMA-busy cycles in which VALU work also ran (second\n"
                  "counter pass, with the transcendental count).\n\n")
         cols = ("kernel", "calls", "avg_us", "gpu_time_pct", "fetch_mb", "write_mb", "hbm_gbps",
@@ -486,7 +490,8 @@ def parse():
     ap.add_argument("--summarize-lds", nargs=1, metavar="CSV", help="LDS counter CSV of the bench (LDS_COUNTERS)")
     ap.add_argument("--counters-out", default=os.path.join(ROOT, "profiles", "counters.md"))
     ap.add_argument("--counters-title", default="")
-    ap.add_argument("--streams", type=int, default=2, help="library streams (1 = every kernel alone)")
+    ap.add_argument("--streams", type=int, default=2,
+                    help="library streams (1 = every kernel alone; 0 = also no shared launches)")
     ap.add_argument("--oracle-baselines", action="store_true",
                     help="time the float64 oracle in full on configs 1, 2, 3 and 5 (CPU only)")
     ap.add_argument("--forward-only", action="store_true",
@@ -648,7 +653,7 @@ def sweep(args):
 
         pf = gb.Params.from_config(dataclasses.replace(cfg, ball=n))
         saved_f = gb.Saved(pf, dev)
-        _lib.check(lib.bsa_set_streams(1), "streams")
+        _lib.check(lib.bsa_set_streams(0), "streams")   # one stream, the ball kernels in launches of their own
         run(pf, saved_f, 2)
         torch.cuda.synchronize()
         fsteps = max(3, min(20, (1 << 19) // n))
@@ -766,10 +771,11 @@ def model_sweep(args):
         torch.cuda.synchronize()
         bsa_layer_ms = (time.perf_counter() - t0) / reps * 1e3
 
-        # full attention: the ball kernels with one ball of n tokens, one stream
+        # full attention: the ball kernels with one ball of n tokens, one stream, in
+        # launches of their own
         pf = gb.Params.from_config(dataclasses.replace(cfg, ball=n))
         fsaved = gb.Saved(pf, dev)
-        _lib.check(lib.bsa_set_streams(1), "streams")
+        _lib.check(lib.bsa_set_streams(0), "streams")
         layer(pf, fsaved, 1)
         torch.cuda.synchronize()
         fsteps = max(2, min(20, (1 << 19) // n))
@@ -934,6 +940,15 @@ def main():
     torch.cuda.synchronize()
     alone = phase_ms(PHASES, PHASE_STEPS)
     lib.bsa_timing_enable(0)
+    # and every branch in launches of its own (streams mode 0: the shared launches split),
+    # for the per-branch rooflines
+    _lib.check(lib.bsa_set_streams(0), "streams")
+    lib.bsa_timing_enable(1)
+    for _ in range(PHASE_STEPS):
+        step()
+    torch.cuda.synchronize()
+    separate = phase_ms(PHASES, PHASE_STEPS)
+    lib.bsa_timing_enable(0)
     _lib.check(lib.bsa_set_streams(args.streams), "streams")
     for _ in range(2):
         step()
@@ -993,7 +1008,7 @@ def main():
     achieved = pf[dom] / (dom_ms * 1e-3) / 1e12
     wl = cfg.name if args.variant == "bsa" else f"{args.variant}_{cfg.name}"
     traffic = measured_traffic(dom, wl)
-    phase_roof, branch_roof = rooflines(cfg, args.variant, alone)
+    phase_roof, branch_roof = rooflines(cfg, args.variant, separate)
     result = {
         "metric": ("BSA layer forward points/sec and TFLOP/s (fraction of MFMA peak) at "
                    f"N={cfg.n_pad}, 1 GPU" if args.forward_only else
@@ -1034,6 +1049,8 @@ def main():
         # durations include time shared with the concurrent branch
         "concurrent_phases": CONCURRENT_PHASES,
         "phase_ms_alone": {n: round(v, 4) for n, v in alone.items()},
+        # one stream and no shared launches: each branch's own phases (the rooflines below)
+        "phase_ms_separate": {n: round(v, 4) for n, v in separate.items()},
         "phase_roofline": phase_roof,
         "branch_roofline": branch_roof,
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": MFMA_BF16_PEAK / 1e12,

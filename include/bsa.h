@@ -17,7 +17,7 @@
  *    starts after an event recorded on `stream` and is joined back into `stream` before
  *    the call returns, so `stream` alone orders the call against the caller's other work.
  *    Calls from several threads are serialised while they enqueue. bsa_set_streams(1)
- *    runs every branch on `stream` instead.
+ *    runs every branch on `stream` instead (0: also without shared launches).
  *  - The library never allocates device memory and keeps no pointer after a call
  *    returns. The caller owns every buffer; sizes come from bsa_sizes() and
  *    bsa_ball_tree_workspace_bytes().
@@ -207,7 +207,11 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
 
 /* Streams used by bsa_forward and bsa_backward: 2 (default) = the caller's stream plus
  * the auxiliary stream, 1 = the caller's stream only (branches run one after another,
- * e.g. to time each alone). Process-wide; BSA_ERR_INVALID_ARGUMENT for other values. */
+ * e.g. to time each alone), 0 = as 1, and the branches that otherwise share a launch
+ * (ball and compressed attention forward, and their key-major backward passes, for bf16
+ * layers without padding) get launches of their own, so that each branch can be timed.
+ * Results are the same bit for bit in every mode. Process-wide; BSA_ERR_INVALID_ARGUMENT
+ * for other values. */
 bsa_status_t bsa_set_streams(int32_t n);
 
 /* ---- The transformer block around the layer (Section 3.1) ----

@@ -401,7 +401,7 @@ struct Aux {
 };
 std::mutex g_aux_mu;
 std::map<int, Aux> g_aux;
-int g_streams = 2;   // 1: every branch on the caller's stream (bsa_set_streams)
+int g_streams = 2;   // 1: every branch on the caller's stream; 0: also no shared launches (bsa_set_streams)
 
 static bsa_status_t get_aux(Aux* out) {
   int dev = 0;
@@ -448,7 +448,7 @@ struct AuxJoin {
 
 bsa_status_t bsa_set_streams(int32_t n) {
   g_last_error.clear();
-  if (n != 1 && n != 2) return fail(BSA_ERR_INVALID_ARGUMENT, "streams must be 1 or 2");
+  if (n < 0 || n > 2) return fail(BSA_ERR_INVALID_ARGUMENT, "streams must be 0, 1 or 2");
   std::lock_guard<std::mutex> lock(g_aux_mu);
   g_streams = n;
   return BSA_OK;
@@ -482,7 +482,7 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   Aux aux;
   s = get_aux(&aux);
   if (s != BSA_OK) return s;
-  if (g_streams == 1) aux.s = st;
+  if (g_streams < 2) aux.s = st;
   char* w = (char*)ws;
   const size_t rows = (size_t)D.rows();
   char* ob = (char*)saved->o_branch;
@@ -524,7 +524,7 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   {
     hipStream_t st_main = st;
     hipStream_t st = aux.s;
-    if (valid == nullptr && bsa::ball_cmp_fwd_fits(D)) {
+    if (valid == nullptr && g_streams != 0 && bsa::ball_cmp_fwd_fits(D)) {
       BSA_STEP("fwd.ball_cmp",
                bsa::launch_ball_cmp_fwd(D, q, k, v, kc_lp, vc_lp, ob, lse, saved->o_cmp, lse + rows, st),
                "ball and compressed attention");
@@ -594,7 +594,7 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   Aux aux;
   s = get_aux(&aux);
   if (s != BSA_OK) return s;
-  if (g_streams == 1) aux.s = st;
+  if (g_streams < 2) aux.s = st;
   char* w = (char*)ws;
   bsa::BwdArgs A{};
   A.q = q; A.k = k; A.v = v; A.dout = d_o; A.valid = valid; A.gate = gate;
@@ -624,7 +624,12 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
   // share CUs well, and the compressed pass's own time then includes the sharing.)
   AuxJoin joiner(aux, st);
   BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::prep, st), "backward row terms");
-  BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::kv_pair, st), "ball and compressed dK/dV");
+  if (g_streams != 0) {
+    BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::kv_pair, st), "ball and compressed dK/dV");
+  } else {
+    BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::kv_ball, st), "ball dK/dV");
+    BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::kv_cmp, st), "compressed dK/dV");
+  }
   if (aux.s != st && (hipEventRecord(aux.fork, st) != hipSuccess || hipStreamWaitEvent(aux.s, aux.fork, 0) != hipSuccess))
     return fail(BSA_ERR_HIP, "forking the auxiliary stream failed");
   BSA_TRY(bsa::launch_bwd_stage(D, A, bsa::BwdStage::dq_ball, aux.s), "ball dQ");

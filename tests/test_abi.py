@@ -137,7 +137,8 @@ def test_tree_argument_errors(lib):
 
 def test_set_streams_validates(lib):
     assert lib.bsa_set_streams(3) == _lib.BSA_ERR_INVALID_ARGUMENT
-    assert lib.bsa_set_streams(0) == _lib.BSA_ERR_INVALID_ARGUMENT
+    assert lib.bsa_set_streams(-1) == _lib.BSA_ERR_INVALID_ARGUMENT
+    assert lib.bsa_set_streams(0) == _lib.BSA_OK
     assert lib.bsa_set_streams(2) == _lib.BSA_OK
 
 

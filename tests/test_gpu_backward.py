@@ -160,6 +160,12 @@ def test_backward_variants():
         run_case(cfg, **kw)
 
 
+def test_backward_full_clouds_unmasked():
+    """Clouds with no padding launch without a mask, as the benchmark does: the unmasked
+    kernels and the shared launches (ball and compressed forward; their key-major passes)."""
+    run_case(Config("full_bf16", 2, 2048, 2048, 2, 64, "bf16", 128, 16, 16, 32, 4, 16, "uniform", "fwdbwd"), seed=21)
+
+
 def test_backward_small_bf16_with_padding():
     cfg = Config("small_bf16", 2, 900, 1024, 2, 64, "bf16", 128, 16, 16, 32, 4, 16, "uniform", "fwdbwd")
     print("backward parity small bf16 d=64", flush=True)
@@ -244,17 +250,23 @@ def test_backward_scaling_group_compression_one_head():
     assert all(e < TOL[cfg.dtype] for e in errs.values()), errs
 
 
-def test_one_stream_equals_two_streams():
+@pytest.mark.parametrize("full", [False, True])
+def test_one_stream_equals_two_streams(full):
     """Every kernel is deterministic and the two-stream schedule only reorders independent
-    branches, so one-stream and two-stream runs give bit-identical results."""
+    branches, so one-stream and two-stream runs give bit-identical results; so do runs
+    without the shared launches (streams mode 0: the ball and compressed forward, and their
+    key-major backward passes, each in launches of their own). full: 2048-point clouds with
+    no padding (no mask: the shared launches run in modes 1 and 2)."""
     cfg = Config("small_bf16", 2, 900, 1024, 2, 64, "bf16", 128, 16, 16, 32, 4, 16, "uniform", "fwdbwd")
+    if full:
+        cfg = Config("full_bf16", 2, 2048, 2048, 2, 64, "bf16", 128, 16, 16, 32, 4, 16, "uniform", "fwdbwd")
     from paper_2506_12541_amd import _lib
     lib = _lib.load()
     inp = make_inputs(cfg, 11, layout="ball", with_grad=True)
     valid = valid_from_tree(cfg)
     outs = []
     try:
-        for n in (2, 1):
+        for n in (2, 1, 0):
             _lib.check(lib.bsa_set_streams(n), "streams")
             g, (p, q, k, v, vd, gate, phi_k, phi_v, saved, o, phi_q) = gpu_forward(cfg, inp, valid)
             grads = gb.backward(p, q, k, v, vd, gate, phi_k, phi_v, saved, to_dev(inp["do"], p.torch_dtype))
@@ -262,6 +274,7 @@ def test_one_stream_equals_two_streams():
             outs.append((o.clone(), {n_: grads[n_].clone() for n_ in ("dq", "dk", "dv", "dgate")}))
     finally:
         lib.bsa_set_streams(2)
-    assert torch.equal(outs[0][0], outs[1][0])
-    for n_ in ("dq", "dk", "dv", "dgate"):
-        assert torch.equal(outs[0][1][n_], outs[1][1][n_]), n_
+    for other in outs[1:]:
+        assert torch.equal(outs[0][0], other[0])
+        for n_ in ("dq", "dk", "dv", "dgate"):
+            assert torch.equal(outs[0][1][n_], other[1][n_]), n_

@@ -82,7 +82,7 @@ def run_block(cfg, seed=None, **pkw):
     W = {n: dev32(a) for n, a in inp["W"].items()}
     phk, phv, phq = ({w: dev32(a) for w, a in inp[n].items()} for n in ("phi_k", "phi_v", "phi_q"))
     x, dy = dev32(inp["x"]), dev32(inp["dy"])
-    vd = to_dev(valid.astype(np.uint8), torch.uint8)
+    vd = None if valid.all() else to_dev(valid.astype(np.uint8), torch.uint8)   # full clouds: no mask
     y, saved = gb.block_forward(p, ffn, W, phk, phv, x, vd, phi_q=phq)
     grads = gb.block_backward(p, ffn, W, phk, phv, x, saved, dy, vd, phi_q=phq)
     torch.cuda.synchronize()
