@@ -1008,7 +1008,12 @@ def main():
     achieved = pf[dom] / (dom_ms * 1e-3) / 1e12
     wl = cfg.name if args.variant == "bsa" else f"{args.variant}_{cfg.name}"
     traffic = measured_traffic(dom, wl)
-    phase_roof, branch_roof = rooflines(cfg, args.variant, separate)
+    # per phase and branch from the separate launches; the shared launches from the pass
+    # that runs them (their own entries)
+    roof_ms = dict(separate)
+    for n in ("fwd.ball_cmp", "bwd.kv"):
+        roof_ms[n] = alone.get(n, 0.0)
+    phase_roof, branch_roof = rooflines(cfg, args.variant, roof_ms)
     result = {
         "metric": ("BSA layer forward points/sec and TFLOP/s (fraction of MFMA peak) at "
                    f"N={cfg.n_pad}, 1 GPU" if args.forward_only else
