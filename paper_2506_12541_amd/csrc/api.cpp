@@ -482,7 +482,10 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   Aux aux;
   s = get_aux(&aux);
   if (s != BSA_OK) return s;
-  if (g_streams < 2) aux.s = st;
+  // the shared ball + compressed launch fills every CU (registers and LDS) until its tail,
+  // so selection on a second stream would only wait beside it: one stream then
+  const bool shared = valid == nullptr && g_streams != 0 && bsa::ball_cmp_fwd_fits(D);
+  if (g_streams < 2 || shared) aux.s = st;
   char* w = (char*)ws;
   const size_t rows = (size_t)D.rows();
   char* ob = (char*)saved->o_branch;
@@ -516,7 +519,8 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
     const bsa::CompressJob q_job = {q, mq, saved->qcmp, saved->hid_q, qc_lp, w + W.w1t_q, 1.0f};
     BSA_STEP("fwd.compress", bsa::launch_compress_fwd(Dq, &q_job, 1, valid, st), "query coarsening");
   }
-  // ball and compressed attention on the auxiliary stream, selection on the caller's
+  // ball and compressed attention on the auxiliary stream (the caller's one with the shared
+  // launch), selection on the caller's
   if (aux.s != st &&
       (hipEventRecord(aux.fork, st) != hipSuccess || hipStreamWaitEvent(aux.s, aux.fork, 0) != hipSuccess))
     return fail(BSA_ERR_HIP, "forking the auxiliary stream failed");
@@ -524,7 +528,7 @@ bsa_status_t bsa_forward(const bsa_params_t* p, const void* q, const void* k, co
   {
     hipStream_t st_main = st;
     hipStream_t st = aux.s;
-    if (valid == nullptr && g_streams != 0 && bsa::ball_cmp_fwd_fits(D)) {
+    if (shared) {
       BSA_STEP("fwd.ball_cmp",
                bsa::launch_ball_cmp_fwd(D, q, k, v, kc_lp, vc_lp, ob, lse, saved->o_cmp, lse + rows, st),
                "ball and compressed attention");

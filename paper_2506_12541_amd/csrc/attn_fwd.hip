@@ -88,51 +88,22 @@ __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, 
   w.finish(lane, bh * N + wq0, out, lse, qval, wq0);
 }
 
-// Instruction interleaving of the pipelined forward's two regions (scheduling-group
-// barriers of the AMDGPU backend: 0x8 MFMA, 0x400 transcendental, 0x2 other VALU, 0x100
-// LDS read; the VALU group does not take the exponentials, which otherwise cluster). Region
-// 1: NM score MFMAs, each followed by two exponentials and two other VALU instructions of
-// the probabilities, the K fragments read two ahead. Region 2: NM P V MFMAs, each followed
-// by two VALU instructions of the next tile's row maxima, its V^T fragment reads (ND)
-// spread among them.
-template <int NM>
-__device__ __forceinline__ void interleave_scores_exps() {
-  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-#pragma unroll
-  for (int i = 0; i < NM; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
-    if (i % 2 == 0) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-  }
-}
-template <int NM, int ND>
-__device__ __forceinline__ void interleave_pv_max() {
-  __builtin_amdgcn_sched_group_barrier(0x100, ND > 4 ? 4 : ND, 0);
-#pragma unroll
-  for (int i = 0; i < NM; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
-    if (i + 4 < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-  }
-}
-
 // bf16 variant: 64-key tiles filled by direct global->LDS loads (no staging registers),
-// V^T fragments from transpose reads of the row-major V tile, software-pipelined so that
-// the matrix cores and the vector ALUs work at the same time. The scores of tile t + 1 are
-// formed while the probabilities of tile t are exponentiated, and the P V product of tile t
-// runs while the row maxima of tile t + 1 are taken; without that, each wave ran its MFMA
-// and VALU work back to back (about 320 + 345 ns per 64-key tile of 32 queries). K therefore
-// runs one tile ahead of V in LDS: iteration t reads K(t + 1) and V(t) while K(t + 2) and
-// V(t + 1) load into the buffers that K(t) and V(t - 1) left. Each buffer is its own LDS
-// object and the loop is unrolled by two, so the compiler can tell that loads in flight
-// into one buffer do not alias reads of another. MASK = false: every key of the launch is
-// real and the key count a multiple of 64 (no per-key select).
+// V^T fragments from transpose reads of the row-major V tile. Each iteration takes one tile
+// through its scores, row maxima, exponentials and P V product in turn while the next
+// tile's K and V load into the other buffers; each buffer is its own LDS object and the
+// loop is unrolled by two, so the compiler can tell that loads in flight into one buffer
+// do not alias reads of another. A wave's MFMA and VALU phases alternate, and with up to
+// four waves per SIMD (126 registers at d = 64, QB = 2) the MFMA bursts of the other waves
+// fill each wave's exponentials. (A software-pipelined form that formed the scores of tile
+// t + 1 beside the exponentials of tile t held two tiles of scores, took up to 208
+// registers, ran at two waves per SIMD and was 8% slower.) MASK = false: every key of the
+// launch is real and the key count a multiple of 64 (no per-key select).
 // LO: log-sum-exp rows only (the V tiles are not loaded; no output rows).
 // PS: the keys are stored multiplied by sl2 (scores come out in the exponent's units, see
 // WaveAttn); sl2 is then not applied again.
-// LDS of the pipelined forward: K and V tiles and key-validity bytes, double buffered
-// (each buffer its own object)
+// LDS of the forward: K and V tiles and key-validity bytes, double buffered (each buffer
+// its own object)
 struct FwdLds {
   bf16_t *ks0, *ks1, *vs0, *vs1;
   uint8_t *ok0, *ok1;
@@ -183,9 +154,9 @@ __device__ __forceinline__ void fwd_dma_body(const FwdLds& L, dim3 grid, unsigne
   const int nt = (nkeys + kFT - 1) / kFT;   // key tiles
 
   // K tile (and its key-validity bytes, read before the tile loads so that waiting for them
-  // does not wait for the tile) / V tile of tile t. Tiles past the end are loaded too (their
-  // rows clamp to the last key; the buffer is free and nothing reads them): no branch
-  // splits the regions of the pipelined step.
+  // does not wait for the tile) / V tile of tile t. The tile past the end is loaded too (its
+  // rows clamp to the last key; the buffer is free and nothing reads it): with the issue
+  // under a branch the loop took 15 more registers, a wave per SIMD fewer.
   auto issue_k = [&](int t, bf16_t* kd, uint8_t* okd) {
     if constexpr (MASK) {
       uint8_t okv = 0;
@@ -210,9 +181,7 @@ __device__ __forceinline__ void fwd_dma_body(const FwdLds& L, dim3 grid, unsigne
   WA w;
   w.init();
   const int wq0 = q0 + wid * 16 * QB;
-  f32x4 s_cur[QB][KB], s_nxt[QB][KB];
   float alpha[QB], delta[QB];
-  bool raise = false;
 
   auto kfrag_of = [&](const bf16_t* kt) {
     return [=](int kb, int c) { return lds_row_chunk<HD>(kt, kb * 16 + r, 4 * c + j); };
@@ -220,77 +189,39 @@ __device__ __forceinline__ void fwd_dma_body(const FwdLds& L, dim3 grid, unsigne
   auto keyok_of = [&](const uint8_t* ok) {
     return [=](int kb, int i) { return ok[kb * 16 + 4 * j + i] != 0; };
   };
-  // iteration t: LDS holds K(t + 1) in kn/okn and V(t) in vc; kc/okc (K(t)) and vn
-  // (V(t - 1)) are free once every wave has passed the barrier. MORE: tile t + 1 exists
-  // (the last iteration has no next tile; keeping the test out of the other iterations
-  // keeps each of their two regions one straight-line block the scheduler can interleave).
-  auto step = [&](auto more_t, int t, bf16_t* kc, uint8_t* okc, const bf16_t* kn, const uint8_t* okn,
-                  const bf16_t* vc, bf16_t* vn) {
-    constexpr bool MORE = decltype(more_t)::value;
-    vm_drain();          // this wave's loads of K(t + 1) and V(t) have landed
-    __syncthreads();     // ... and every wave's; K(t) and V(t - 1) are no longer read
-    issue_k(t + 2, kc, okc);
+  // iteration t: LDS holds K(t) and V(t); the other buffers are free once every wave has
+  // passed the barrier and take tile t + 1 while this one is computed
+  auto step = [&](int t, const bf16_t* kc, const uint8_t* okc, const bf16_t* vc, bf16_t* kn, uint8_t* okn,
+                  bf16_t* vn) {
+    vm_drain();
+    __syncthreads();
+    issue_k(t + 1, kn, okn);
     issue_v(t + 1, vn);
-    if constexpr (PS) {
-      // rare: a query's maximum rose (wave-uniform); tile t's scores started from the
-      // previous reference, tile t + 1's will start from the new one
-      if (raise) {
-        w.rescale(alpha);
-        w.template shift<KB>(s_cur, delta);
-      }
+    f32x4 s[QB][KB];
+    w.template scores<KB>(s, kfrag_of(kc));
+    if (w.template tile_max<KB, MASK>(s, sl2, keyok_of(okc), alpha, delta)) {
+      w.rescale(alpha);   // rare: a query's maximum rose (wave-uniform)
+      if constexpr (PS) w.template shift<KB>(s, delta);
     }
-    // region 1: scores of tile t + 1 beside the exponentials of tile t
     CT pf[QB][KB / 2];
-    if constexpr (MORE) w.template scores<KB>(s_nxt, kfrag_of(kn));
-    w.template probs<KB>(s_cur, sl2, pf);
-    if constexpr (MORE) interleave_scores_exps<KB * WA::NCH * QB>();
-    // the probabilities are complete here: the compiler may not sink their computation
-    // below the rescale branch, out of the block holding the score MFMAs
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-      for (int kp = 0; kp < KB / 2; ++kp) asm volatile("" : "+v"(pf[qb][kp]));
-    if constexpr (!PS) {
-      if (raise) w.rescale(alpha);   // rare: a query's maximum rose (wave-uniform)
-    }
-    // region 2: P V of tile t beside the row maxima of tile t + 1
+    w.template probs<KB>(s, sl2, pf);
     w.template pv<KB>(pf, [&](int db, int kp) { return lds_tr_chunk<HD>(vc, 32 * kp, 16 * db, lane); });
-    if constexpr (MORE) {
-      raise = w.template tile_max<KB, MASK>(s_nxt, sl2, keyok_of(okn), alpha, delta);
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) s_cur[qb][kb] = s_nxt[qb][kb];
-      interleave_pv_max<(KB / 2) * QB * (LO ? 1 : 1 + WA::DB), LO ? 0 : WA::DB * (KB / 2) * 2>();
-    }
   };
-  using more = std::true_type;
-  using last = std::false_type;
-  // prologue: K(0) in, scores and maxima of tile 0, then K(1) and V(0) in flight
   issue_k(0, ks0, ok0);
-  load_q(w, q + (bh * N + wq0) * HD, lane);
-  vm_drain();
-  __syncthreads();
-  w.template scores<KB>(s_cur, kfrag_of(ks0));
-  raise = w.template tile_max<KB, MASK>(s_cur, sl2, keyok_of(ok0), alpha, delta);
-  issue_k(1, ks1, ok1);
   issue_v(0, vs0);
-  int t = 0;
-  for (; t + 2 < nt; t += 2) {
-    step(more{}, t, ks0, ok0, ks1, ok1, vs0, vs1);
-    step(more{}, t + 1, ks1, ok1, ks0, ok0, vs1, vs0);
+  load_q(w, q + (bh * N + wq0) * HD, lane);
+  for (int t = 0; t < nt; t += 2) {
+    step(t, ks0, ok0, vs0, ks1, ok1, vs1);
+    if (t + 1 < nt) step(t + 1, ks1, ok1, vs1, ks0, ok0, vs0);
   }
-  if (t + 1 < nt) {   // two tiles left
-    step(more{}, t, ks0, ok0, ks1, ok1, vs0, vs1);
-    step(last{}, t + 1, ks1, ok1, ks0, ok0, vs1, vs0);
-  } else {            // one tile left
-    step(last{}, t, ks0, ok0, ks1, ok1, vs0, vs1);
-  }
+  vm_drain();   // the last step's loads (a repeat of the last tile, never read)
   w.finish(lane, bh * N + wq0, out, lse, qval, wq0);
 }
 
+// Unmasked launches are held to 128 registers (four waves per SIMD; no spills at d = 64).
 template <int HD, int QB, int NW, bool BALL, typename OT = bf16_t, bool LO = false, bool MASK = true, bool PS = false>
-__global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(FwdArgs<OT> a) {
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MASK ? 1 : 4)))
+dense_fwd_dma_kernel(FwdArgs<OT> a) {
   BSA_FWD_LDS(L);
   fwd_dma_body<HD, QB, NW, BALL, OT, LO, MASK, PS>(L, gridDim,
                                                    blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z), a);
@@ -299,10 +230,10 @@ __global__ void __launch_bounds__(NW * 64) dense_fwd_dma_kernel(FwdArgs<OT> a) {
 // The compressed attention (prescaled keys, float32 rows) and the ball attention (bf16
 // rows) of unmasked bf16 layers in one launch: the compressed workgroups first, then the
 // ball workgroups, which fill the CUs that the compressed launch's last round leaves idle
-// and overlap their HBM traffic with its MFMA work.
+// and overlap their HBM traffic with its MFMA work. Four waves per SIMD, as above.
 template <int HD>
-__global__ void __launch_bounds__(256) dense_fwd_pair_kernel(FwdArgs<float> cmp, dim3 cgrid, FwdArgs<bf16_t> ball,
-                                                             dim3 bgrid) {
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
+dense_fwd_pair_kernel(FwdArgs<float> cmp, dim3 cgrid, FwdArgs<bf16_t> ball, dim3 bgrid) {
   BSA_FWD_LDS(L);
   const unsigned ncmp = cgrid.x * cgrid.y * cgrid.z;
   if (blockIdx.x < ncmp)
