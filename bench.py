@@ -61,10 +61,17 @@ def algorithmic_flops(cfg, variant="bsa"):
 
 
 # phases that share the chip with a concurrent branch: forward ball + compressed attention
-# beside top-k selection + selection attention; the backward dQ chain beside the
-# compression and selection dK/dV passes
-CONCURRENT_PHASES = ["fwd.ball", "fwd.cmp", "fwd.ball_cmp", "fwd.select", "fwd.slc", "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc",
+# beside top-k selection + selection attention where the two run as separate launches (the
+# forward of the shared ball + compressed launch runs on one stream); the backward dQ chain
+# beside the compression and selection dK/dV passes
+CONCURRENT_PHASES = ["fwd.ball", "fwd.cmp", "fwd.select", "fwd.slc", "bwd.dq_ball", "bwd.dq_cmp", "bwd.dq_slc",
                      "bwd.mlp", "bwd.slc_csr", "bwd.slc_kv"]
+
+
+def concurrent_phases(phase_ms):
+    """The phases of CONCURRENT_PHASES that shared the chip in this run."""
+    shared_fwd = phase_ms.get("fwd.ball_cmp", 0.0) > 0
+    return [p for p in CONCURRENT_PHASES if not (shared_fwd and p.startswith("fwd."))]
 
 
 def phase_flops(cfg, variant="bsa"):
@@ -1052,7 +1059,7 @@ def main():
         "phase_ms_steps": PHASE_STEPS,
         # these phases run on the library's second stream beside others, so their
         # durations include time shared with the concurrent branch
-        "concurrent_phases": CONCURRENT_PHASES,
+        "concurrent_phases": concurrent_phases(phases),
         "phase_ms_alone": {n: round(v, 4) for n, v in alone.items()},
         # one stream and no shared launches: each branch's own phases (the rooflines below)
         "phase_ms_separate": {n: round(v, 4) for n, v in separate.items()},

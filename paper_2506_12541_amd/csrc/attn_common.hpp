@@ -457,13 +457,14 @@ struct WaveAttn {
   // Masks a score tile (MASK: keyok(kb, i) false -> -inf) and moves the reference maximum:
   // like tile(), it is raised only when the tile's maximum exceeds it by more than
   // kRescale. Returns whether any query of the wave raised it (wave-uniform); alpha[qb] is
-  // then the factor for the accumulated O and row sums (1 where not raised).
-  // PS: delta[qb] is the rise of the reference against the one the tile's scores start
-  // from (0 where not raised), for shift().
+  // then the factor for the accumulated O and row sums (1 where not raised), and, PS,
+  // delta[qb] the rise of the reference against the one the tile's scores start from (0
+  // where not raised), for shift(). Neither is written when it returns false.
   template <int KB, bool MASK, typename OK>
   __device__ __forceinline__ bool tile_max(f32x4 (&s)[QB][KB], float sl2, OK keyok, float (&alpha)[QB],
                                            float (&delta)[QB]) {
-    bool any = false;
+    float tloc[QB];
+    bool up = false;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       float tmax = kNegInf;
@@ -474,8 +475,19 @@ struct WaveAttn {
           if constexpr (MASK) s[qb][kb][i] = keyok(kb, i) ? s[qb][kb][i] : kNegInf;
           tmax = fmaxf(tmax, s[qb][kb][i]);
         }
+      tloc[qb] = tmax;
+      // the test below on this lane's maximum alone: the query's maximum over its four
+      // lanes passes it exactly when one of them does (rounding keeps the order)
+      up |= (PS ? tmax + -cneg[qb][0] : tmax * sl2) > mx[qb] + kRescale;
+    }
+    // the usual case once the first tiles are in: no query's reference moves, and the
+    // cross-lane maxima, new references and factors are skipped (wave-uniform branch)
+    if (__builtin_amdgcn_ballot_w64(up) == 0) return false;
+    bool any = false;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
       const float cref = -cneg[qb][0];
-      tmax = PS ? col_max(tmax) + cref : col_max(tmax) * sl2;
+      const float tmax = PS ? col_max(tloc[qb]) + cref : col_max(tloc[qb]) * sl2;
       const bool raise = tmax > mx[qb] + kRescale;
       const float mnew = raise ? tmax : mx[qb];
       alpha[qb] = raise ? fast_exp2(mx[qb] - mnew) : 1.0f;
