@@ -13,7 +13,9 @@
  *    NULL = the default stream) and returns once its kernels are queued.
  *  - bsa_forward and bsa_backward run independent branches concurrently: on first use on
  *    a device the library creates one auxiliary stream (default priority) and two events
- *    for that device and keeps them until the process ends. Work on the auxiliary stream
+ *    for that device and keeps them until the process ends. (The forward of a bf16 layer
+ *    without padding, whose ball and compressed attention share one launch, runs on
+ *    `stream` alone.) Work on the auxiliary stream
  *    starts after an event recorded on `stream` and is joined back into `stream` before
  *    the call returns, so `stream` alone orders the call against the caller's other work.
  *    Calls from several threads are serialised while they enqueue. bsa_set_streams(1)
@@ -206,7 +208,8 @@ bsa_status_t bsa_backward(const bsa_params_t* p, const void* q, const void* k, c
                           const bsa_mlp_grad_t* dphi_q, void* ws, size_t ws_bytes, void* stream);
 
 /* Streams used by bsa_forward and bsa_backward: 2 (default) = the caller's stream plus
- * the auxiliary stream, 1 = the caller's stream only (branches run one after another,
+ * the auxiliary stream (in the forward only where ball and compressed attention run as
+ * separate launches), 1 = the caller's stream only (branches run one after another,
  * e.g. to time each alone), 0 = as 1, and the branches that otherwise share a launch
  * (ball and compressed attention forward, and their key-major backward passes, for bf16
  * layers without padding) get launches of their own, so that each branch can be timed.
