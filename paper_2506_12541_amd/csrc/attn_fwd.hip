@@ -94,7 +94,7 @@ __global__ void __launch_bounds__(256) dense_fwd_kernel(const T* q, const T* k, 
 // tile's K and V load into the other buffers; each buffer is its own LDS object and the
 // loop is unrolled by two, so the compiler can tell that loads in flight into one buffer
 // do not alias reads of another. A wave's MFMA and VALU phases alternate, and with up to
-// four waves per SIMD (126 registers at d = 64, QB = 2) the MFMA bursts of the other waves
+// four waves per SIMD (128 registers at d = 64, QB = 2) the MFMA bursts of the other waves
 // fill each wave's exponentials. (A software-pipelined form that formed the scores of tile
 // t + 1 beside the exponentials of tile t held two tiles of scores, took up to 208
 // registers, ran at two waves per SIMD and was 8% slower.) MASK = false: every key of the
