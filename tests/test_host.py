@@ -86,3 +86,32 @@ def test_generators_are_seeded_and_padding_is_zero():
     assert not np.any(blk["x"][0, 100:124]) and not np.any(blk["dy"][0, 100:124])
     assert np.all(np.any(blk["x"][0, :100] != 0, axis=-1))
     assert blk["W"]["w1"].shape == (blk["ffn"], cfg.heads * cfg.head_dim)
+
+
+def test_rising_inputs_move_the_reference_in_every_tile():
+    """Premise of the rising-maxima forward parity test: on its inputs every query's
+    maximum over a 64-key tile exceeds its running maximum over the earlier tiles by more
+    than the lazy-rescale margin (8 log2 units) in every tile after the first, in the ball
+    branch (a middle ball of each head) and in the compressed branch (mean-pooled blocks of
+    16 keys, every query). float64 on the inputs of both storage types."""
+    from rising import rising_config, rising_inputs
+    for dtype in ("bf16", "f32"):
+        _check_rising(rising_config(dtype), rising_inputs(rising_config(dtype)))
+
+
+def _check_rising(cfg, inp):
+    d, m, n, l = cfg.head_dim, cfg.ball, cfg.n_pad, cfg.cmp_block
+    sl2 = 1.0 / np.sqrt(d) / np.log(2.0)    # softmax scale in log2 units
+
+    def tile_rises(s):
+        tmax = s.reshape(s.shape[0], -1, 64).max(-1)
+        return tmax[:, 1:] - np.maximum.accumulate(tmax, axis=1)[:, :-1]
+
+    for h in range(cfg.heads):
+        q = inp["q"][0, h].astype(np.float64)
+        k = inp["k"][0, h].astype(np.float64)
+        b0 = (n // m // 2) * m
+        ball = q[b0:b0 + m] @ k[b0:b0 + m].T * sl2
+        assert tile_rises(ball).min() > 8.0
+        kc = k.reshape(n // l, l, d).mean(1)
+        assert tile_rises(q @ kc.T * sl2).min() > 8.0
