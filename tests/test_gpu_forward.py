@@ -110,21 +110,24 @@ def test_forward_no_own_ball_mask_and_mean_pool():
             _check_head(cfg, inp, valid, g, 0, h, P, TOL[cfg.dtype])
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_forward_rising_maxima(dtype):
+@pytest.mark.parametrize("dtype,padded", [("bf16", False), ("f32", False), ("bf16", True)])
+def test_forward_rising_maxima(dtype, padded):
     """Scores that rise along the key order by more than the lazy-rescale margin (8 in
     log2 units) in every 64-key tile, so the running maximum of the ball and compressed
     forward moves in each tile (O and row sums rescaled, prescaled scores shifted) instead
     of settling after the first tiles as on random data (the premise is checked on the
-    CPU: test_host). Unmasked layer of 8192 points and two heads (bf16: the shared forward
-    launch, whole tiles; f32: the register-staged kernels); mean pooling, so that the
+    CPU: test_host). A layer of 8192 points and two heads (bf16 unpadded: the shared
+    forward launch, whole tiles; f32: the register-staged kernels; bf16 padded, every 97th
+    slot a dummy: the masked kernels on two streams); mean pooling, so that the
     compressed keys are block means and rise with the keys. Scores stay within 52 log2
     units, where the compressed keys' bf16 storage moves a log-sum-exp by at most 0.008
     (float64 on the same inputs), inside the bf16 bar."""
     cfg = rising_config(dtype)
-    print(f"forward parity, rising maxima (8192 points, 2 heads, {dtype})", flush=True)
+    print(f"forward parity, rising maxima (8192 points, 2 heads, {dtype}, padded={padded})", flush=True)
     inp = rising_inputs(cfg)
     valid = np.ones((1, cfg.n_pad), bool)
+    if padded:
+        valid[0, np.arange(cfg.n_pad) % 97 == 5] = False
     g, _ = gpu_forward(cfg, inp, valid, kv_pool=1)
     P = oracle_params(cfg, kv_pool="mean")
     for h in range(cfg.heads):
